@@ -1,0 +1,188 @@
+"""Brute-force reference for tiny problems (D <= 4, N <= 8) -- TEST INFRASTRUCTURE ONLY.
+
+A second, literal implementation of one OpenAI-ES generation of the evosax
+report (arXiv 2212.04180, Sec. 2.1 ask / evaluate / tell; FD gradient
+estimator; centered ranks of Sec. 3.2; Adam), written in pure Python with
+integers and exact rationals.  It shares nothing with ``esoracle.c`` (its own
+Philox, its own Box-Muller, its own ranking by counting, the population matrix
+E built explicitly) and is used only to pin that oracle.
+
+fp32 rounding is done exactly: every fp32 result is the round-to-nearest-even
+of the exact rational value (``f32``), so a fused multiply-add is one rounding
+by construction.  Transcendentals use Python's fp64 ``math`` functions and
+then one fp32 rounding.
+"""
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+
+import numpy as np
+
+M0, M1 = 0xD2511F53, 0xCD9E8D57   # Philox-4x32 multipliers (Salmon et al., SC'11)
+W0, W1 = 0x9E3779B9, 0xBB67AE85   # Weyl key increments
+MASK = 0xFFFFFFFF
+
+
+def philox(key, ctr, rounds=10):
+    """Philox-4x32-R block: R rounds of two 32x32->64 products and xors with the key."""
+    k0, k1 = key
+    c0, c1, c2, c3 = ctr
+    for i in range(rounds):
+        if i:
+            k0, k1 = (k0 + W0) & MASK, (k1 + W1) & MASK
+        p0, p1 = M0 * c0, M1 * c2
+        c0, c1, c2, c3 = ((p1 >> 32) ^ c1 ^ k0, p1 & MASK, (p0 >> 32) ^ c3 ^ k1, p0 & MASK)
+    return [c0, c1, c2, c3]
+
+
+def _q(v) -> Fraction:
+    """Exact rational value of an int, float, numpy scalar or Fraction."""
+    if isinstance(v, (Fraction, int)):
+        return Fraction(v)
+    return Fraction(float(v))
+
+
+def f32(q) -> float:
+    """Round an exact rational (or int / float) to the nearest fp32, ties to even."""
+    q = _q(q)
+    if q == 0:
+        return 0.0
+    sgn = -1 if q < 0 else 1
+    a = abs(q)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1
+    # 2^e <= a < 2^(e+1); fp32 keeps 24 significant bits down to 2^-149
+    lsb_exp = max(e - 23, -149)
+    scaled = a / Fraction(2) ** lsb_exp
+    n = scaled.numerator // scaled.denominator
+    rem = scaled - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    val = Fraction(n) * Fraction(2) ** lsb_exp
+    if val >= Fraction(2) ** 128 - Fraction(2) ** 103:
+        return sgn * math.inf
+    return float(np.float32(sgn * float(val)))
+
+
+def fma32(a, b, c):
+    return f32(_q(a) * _q(b) + _q(c))
+
+
+def normals_block(seed, domain, row, t, b):
+    """Four N(0,1) values of Philox block b: Box-Muller on (w0,w1), (w2,w3)."""
+    w = philox((seed & MASK, (seed >> 32) & MASK), (b & MASK, row, t, domain))
+    out = []
+    for h in range(2):
+        u = ((w[2 * h] >> 8) + 1) * 2.0 ** -24
+        th = (w[2 * h + 1] >> 8) * 2.0 ** -24
+        r = math.sqrt(-2.0 * math.log(u))
+        a = 2.0 * math.pi * th
+        out += [f32(r * math.cos(a)), f32(r * math.sin(a))]
+    return out
+
+
+def eps_vector(seed, domain, row, t, D):
+    v = []
+    for b in range((D + 3) // 4):
+        v += normals_block(seed, domain, row, t, b)
+    return v[:D]
+
+
+def init_uniform(seed, D, lo, hi):
+    rng = f32(_q(f32(hi)) - _q(f32(lo)))
+    m = []
+    for d in range(D):
+        w = philox((seed & MASK, (seed >> 32) & MASK), (d // 4, 0, 0, 1))[d % 4]
+        m.append(fma32(rng, Fraction(w >> 8, 2 ** 24), f32(lo)))
+    return m
+
+
+def fitness(problem, x, s=None, a=10.0):
+    """Benchmark problems on fp32 x: exact rational sums (sphere, shifted sphere,
+    Rosenbrock) or an exact sum of fp64 terms (Rastrigin), one fp32 rounding."""
+    D = len(x)
+    X = [_q(v) for v in x]
+    if problem == "sphere":
+        return f32(sum(v * v for v in X))
+    if problem == "shifted_sphere":
+        return f32(sum((X[i] - _q(s[i])) ** 2 for i in range(D)))
+    if problem == "rosenbrock":
+        return f32(sum(100 * (X[i + 1] - X[i] ** 2) ** 2 + (1 - X[i]) ** 2 for i in range(D - 1)))
+    if problem == "rastrigin":
+        xs = [float(v) for v in x]
+        terms = [a * D] + [xs[i] * xs[i] - a * math.cos(2.0 * math.pi * xs[i]) for i in range(D)]
+        return f32(math.fsum(terms))
+    raise ValueError(problem)
+
+
+def ranks(f, maximize=False):
+    """rank_j = #{k: key_k < key_j} + #{k < j: key_k == key_j}; NaN is worst."""
+    def key(v):
+        k = -v if maximize else v
+        return math.inf if math.isnan(k) else k
+    keys = [key(v) for v in f]
+    N = len(f)
+    return [sum(1 for k in range(N) if keys[k] < keys[j] or (keys[k] == keys[j] and k < j))
+            for j in range(N)]
+
+
+def centered(f, maximize=False):
+    N = len(f)
+    return [f32(Fraction(2 * r - (N - 1), 2 * (N - 1))) for r in ranks(f, maximize)]
+
+
+class BruteES:
+    """R=1 OpenAI-ES with antithetic pairs (+eps first half, -eps second half)."""
+
+    def __init__(self, problem, D, N, sigma, lr, seed, lo, hi, s=None, maximize=False,
+                 beta1=0.9, beta2=0.999, eps=1e-8, a=10.0, shaping="centered"):
+        assert N % 2 == 0
+        self.problem, self.D, self.N = problem, D, N
+        self.sigma, self.lr = f32(sigma), f32(lr)
+        self.b1, self.b2, self.eps = f32(beta1), f32(beta2), f32(eps)
+        self.seed, self.s, self.maximize, self.a, self.shaping = seed, s, maximize, a, shaping
+        self.m = init_uniform(seed, D, lo, hi)
+        self.m1 = [0.0] * D
+        self.v = [0.0] * D
+        self.t = 0
+
+    def population(self):
+        """E (N x D): row j = +eps_j for j < N/2, -eps_{j-N/2} otherwise; x = m + sigma E."""
+        half = self.N // 2
+        E = []
+        for j in range(self.N):
+            e = eps_vector(self.seed, 0, j % half, self.t, self.D)
+            E.append(e if j < half else [-v for v in e])
+        X = [[fma32(self.sigma, E[j][d], self.m[d]) for d in range(self.D)] for j in range(self.N)]
+        return E, X
+
+    def generation(self, fit=None):
+        E, X = self.population()
+        f = fit if fit is not None else [fitness(self.problem, x, self.s, self.a) for x in X]
+        if self.shaping == "centered":
+            y = centered(f, self.maximize)
+        else:
+            y = [(-v if self.maximize else v) for v in f]
+        Ns = Fraction(self.N) * _q(self.sigma)
+        g = [f32(sum(_q(y[j]) * _q(E[j][d]) for j in range(self.N)) / Ns)
+             for d in range(self.D)]
+        tp = self.t + 1
+        bc1 = f32(1.0 - math.pow(self.b1, tp))
+        bc2 = f32(1.0 - math.pow(self.b2, tp))
+        omb1 = f32(1 - _q(self.b1))
+        omb2 = f32(1 - _q(self.b2))
+        for d in range(self.D):
+            a = f32(_q(omb1) * _q(g[d]))
+            m1 = fma32(self.b1, self.m1[d], a)
+            b = f32(_q(omb2) * _q(f32(_q(g[d]) ** 2)))
+            v = fma32(self.b2, self.v[d], b)
+            mhat = f32(_q(m1) / _q(bc1))
+            vhat = f32(_q(v) / _q(bc2))
+            den = f32(_q(f32(math.sqrt(vhat))) + _q(self.eps))
+            q = f32(_q(mhat) / _q(den))
+            self.m[d] = fma32(-self.lr, q, self.m[d])
+            self.m1[d], self.v[d] = m1, v
+        self.t += 1
+        return {"E": E, "X": X, "fitness": f, "y": y, "g": g}

@@ -1,0 +1,526 @@
+/*
+ * esoracle.c -- plain, slow CPU oracle for one OpenAI-ES generation.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may link, load or call
+ * this file; only the test-suite, the smoke check and the CPU-baseline leg of the
+ * benchmark use it.  It shares no code, header, table or constant generator with
+ * the HIP library: every step is written here again from its definition.
+ *
+ * What is computed (evosax report, arXiv 2212.04180):
+ *   - the ask / evaluate / tell loop of Sec. 2.1 (Listing 1), run for several
+ *     independent seeds as in Sec. 2.2 (Listing 3, vmap over keys);
+ *   - OpenAI-ES (Table 1, FDG class): isotropic Gaussian perturbations with
+ *     antithetic sampling, the finite-difference gradient estimator of Sec. 2.1
+ *     (grad_m E f(m + s*eps) = (1/s) E[f(m + s*eps) eps]), centered-rank fitness
+ *     shaping (Sec. 3.2; App. B, OpenAI-ES table) and an Adam update of the mean
+ *     (Sec. 2.1; App. B).  Minimisation is the default (Listing 1).
+ *   - The paper names no random-number generator, no rank formula and no Adam
+ *     formula.  The readings used here (Philox-4x32-10 with a fixed counter
+ *     layout, Box-Muller, the exact centered-rank fraction, Kingma & Ba Adam) are
+ *     stated at each function.
+ *
+ * Arithmetic: fp64 accumulation everywhere a sum appears; fp32 where the
+ * method's state is fp32.  Build with -ffp-contract=off so that no multiply-add
+ * is fused unless written as fmaf().
+ *
+ * Parity status per function is recorded in the test-suite; the only part that
+ * no outside fact pins is a free-running multi-generation trajectory (it is
+ * pinned only stage by stage), which the test-suite marks "parity unpinned".
+ */
+#define _GNU_SOURCE
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* Philox-4x32-10 (Salmon, Moraes, Dror, Shaw: "Parallel random numbers: as   */
+/* easy as 1, 2, 3", SC'11).  The paper uses JAX's splittable keys (Listing 1) */
+/* and names no generator; the counter-based Philox stream replaces them.     */
+/* ------------------------------------------------------------------------ */
+#define OR_TWO_PI 6.283185307179586476925286766559
+#define OR_PHILOX_M0 0xD2511F53u
+#define OR_PHILOX_M1 0xCD9E8D57u
+#define OR_PHILOX_W0 0x9E3779B9u
+#define OR_PHILOX_W1 0xBB67AE85u
+
+void or_philox4x32_10(uint32_t k0, uint32_t k1, const uint32_t ctr[4], uint32_t out[4])
+{
+    uint32_t c[4] = {ctr[0], ctr[1], ctr[2], ctr[3]};
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) { /* key schedule: bump the key between rounds */
+            k0 += OR_PHILOX_W0;
+            k1 += OR_PHILOX_W1;
+        }
+        uint64_t p0 = (uint64_t)OR_PHILOX_M0 * (uint64_t)c[0];
+        uint64_t p1 = (uint64_t)OR_PHILOX_M1 * (uint64_t)c[2];
+        uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        uint32_t n0 = hi1 ^ c[1] ^ k0;
+        uint32_t n1 = lo1;
+        uint32_t n2 = hi0 ^ c[3] ^ k1;
+        uint32_t n3 = lo0;
+        c[0] = n0; c[1] = n1; c[2] = n2; c[3] = n3;
+    }
+    out[0] = c[0]; out[1] = c[1]; out[2] = c[2]; out[3] = c[3];
+}
+
+/* Counter layout (reading): key = (lo32(seed_r), hi32(seed_r)),
+ * counter = (block = d/4, row, t, domain).                                  */
+enum { OR_DOM_NOISE = 0, OR_DOM_INIT = 1, OR_DOM_PROBLEM = 2, OR_DOM_EVAL = 3 };
+
+void or_words(uint64_t seed, uint32_t domain, uint32_t row, uint32_t t,
+              int64_t b0, int64_t nb, uint32_t* out)
+{
+    for (int64_t i = 0; i < nb; ++i) {
+        uint32_t ctr[4] = {(uint32_t)(b0 + i), row, t, domain};
+        or_philox4x32_10((uint32_t)seed, (uint32_t)(seed >> 32), ctr, out + 4 * i);
+    }
+}
+
+/* Uniforms (reading): exact multiples of 2^-24. */
+static double or_u_pos(uint32_t w) { return (double)((w >> 8) + 1u) * 0x1p-24; } /* (0,1] */
+static double or_u_half(uint32_t w) { return (double)(w >> 8) * 0x1p-24; }       /* [0,1) */
+
+/* Box-Muller (search distribution N(m, s^2 I) of Sec. 2.1): words (w0,w1)
+ * give two normals r*cos(2 pi th), r*sin(2 pi th) with r = sqrt(-2 ln u),
+ * computed in fp64 and rounded once to fp32.                               */
+static void or_box_muller(const uint32_t w[4], float out[4])
+{
+    for (int h = 0; h < 2; ++h) {
+        double r = sqrt(-2.0 * log(or_u_pos(w[2 * h])));
+        double a = OR_TWO_PI * or_u_half(w[2 * h + 1]);
+        out[2 * h] = (float)(r * cos(a));
+        out[2 * h + 1] = (float)(r * sin(a));
+    }
+}
+
+/* Normals for dims [d0, d0+nd) of the stream (seed, domain, row, t). */
+void or_normals(uint64_t seed, uint32_t domain, uint32_t row, uint32_t t,
+                int64_t d0, int64_t nd, float* out)
+{
+    int64_t d = d0;
+    while (d < d0 + nd) {
+        uint32_t w[4];
+        float z[4];
+        or_words(seed, domain, row, t, d / 4, 1, w);
+        or_box_muller(w, z);
+        for (int64_t k = d % 4; k < 4 && d < d0 + nd; ++k, ++d) out[d - d0] = z[k];
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Configuration (mirrors the fields of the library's config, declared here  */
+/* again on purpose: the oracle includes nothing from the library).         */
+/* ------------------------------------------------------------------------ */
+enum { OR_PROB_NONE = 0, OR_PROB_SPHERE = 1, OR_PROB_SHIFTED_SPHERE = 2,
+       OR_PROB_ROSENBROCK = 3, OR_PROB_RASTRIGIN = 4, OR_PROB_MLP = 5 };
+enum { OR_INIT_UNIFORM = 0, OR_INIT_ZERO = 1, OR_INIT_FANIN_NORMAL = 2 };
+enum { OR_SHAPE_CENTERED_RANK = 0, OR_SHAPE_RAW = 1 };
+
+typedef struct {
+    int64_t num_dims;   /* D */
+    int32_t popsize;    /* N, even */
+    int32_t num_runs;   /* R */
+    float sigma, lr, beta1, beta2, eps;
+    int32_t maximize;
+    int32_t shaping;
+    uint64_t seed;      /* run r uses seed + r */
+    int32_t init;
+    float init_lo, init_hi;
+    int32_t problem;
+    float rastrigin_a;
+    int32_t mlp_batch;  /* inputs per generation */
+    int32_t mlp_bf16;   /* 1: student forward rounds operands to bf16 */
+    int32_t mlp_tanh_out;
+} or_config;
+
+/* MLP 64-256-256-16 layer table, flattened [out][in] row-major weights, then
+ * bias, layer by layer (parameter reshaping, Sec. 3.2; flattening order is a
+ * reading).                                                                */
+#define OR_MLP_IN 64
+#define OR_MLP_H 256
+#define OR_MLP_OUT 16
+static const int64_t or_mlp_fan_in[3] = {OR_MLP_IN, OR_MLP_H, OR_MLP_H};
+static const int64_t or_mlp_fan_out[3] = {OR_MLP_H, OR_MLP_H, OR_MLP_OUT};
+
+int64_t or_mlp_num_params(void)
+{
+    int64_t n = 0;
+    for (int l = 0; l < 3; ++l) n += or_mlp_fan_in[l] * or_mlp_fan_out[l] + or_mlp_fan_out[l];
+    return n;
+}
+
+/* For flat index i: layer, and whether it is a weight (1) or a bias (0). */
+static int or_mlp_locate(int64_t i, int* layer)
+{
+    int64_t off = 0;
+    for (int l = 0; l < 3; ++l) {
+        int64_t nw = or_mlp_fan_in[l] * or_mlp_fan_out[l];
+        if (i < off + nw) { *layer = l; return 1; }
+        off += nw;
+        if (i < off + or_mlp_fan_out[l]) { *layer = l; return 0; }
+        off += or_mlp_fan_out[l];
+    }
+    *layer = -1;
+    return 0;
+}
+
+/* Fan-in normal vector: weights z/sqrt(fan_in), biases 0 (reading of
+ * "N(0, 1/fan_in) weights").                                                */
+static void or_fanin_normal(uint64_t seed, uint32_t domain, int64_t D, float* out)
+{
+    float* z = (float*)malloc(sizeof(float) * (size_t)D);
+    or_normals(seed, domain, 0, 0, 0, D, z);
+    for (int64_t i = 0; i < D; ++i) {
+        int l;
+        if (or_mlp_locate(i, &l))
+            out[i] = (float)((double)z[i] / sqrt((double)or_mlp_fan_in[l]));
+        else
+            out[i] = 0.0f;
+    }
+    free(z);
+}
+
+/* Initial mean of run r (reading: uniform from the INIT stream as
+ * lo + (hi - lo) * u, one fp32 rounding; zero; or fan-in normal).          */
+void or_init_mean(const or_config* c, int32_t run, float* m)
+{
+    uint64_t seed = c->seed + (uint64_t)run;
+    int64_t D = c->num_dims;
+    if (c->init == OR_INIT_ZERO) {
+        for (int64_t i = 0; i < D; ++i) m[i] = 0.0f;
+    } else if (c->init == OR_INIT_UNIFORM) {
+        float range = c->init_hi - c->init_lo;
+        for (int64_t i = 0; i < D; ++i) {
+            uint32_t w[4];
+            or_words(seed, OR_DOM_INIT, 0, 0, i / 4, 1, w);
+            m[i] = fmaf(range, (float)or_u_half(w[i % 4]), c->init_lo);
+        }
+    } else {
+        or_fanin_normal(seed, OR_DOM_INIT, D, m);
+    }
+}
+
+/* Problem data shared by all runs: the shift vector s (D floats) of the
+ * shifted sphere, or the teacher MLP (D floats) -- both from the base seed,
+ * PROBLEM stream.                                                           */
+void or_problem_data(const or_config* c, float* out)
+{
+    if (c->problem == OR_PROB_SHIFTED_SPHERE)
+        or_normals(c->seed, OR_DOM_PROBLEM, 0, 0, 0, c->num_dims, out);
+    else if (c->problem == OR_PROB_MLP)
+        or_fanin_normal(c->seed, OR_DOM_PROBLEM, c->num_dims, out);
+}
+
+/* ------------------------------------------------------------------------ */
+/* ask: antithetic population (Sec. 2.1 ask step; antithetic sampling named */
+/* in the FDG item).  Reading: members 0..N/2-1 use +eps_p, members          */
+/* N/2..N-1 use -eps_{j-N/2}; x = fmaf(+-sigma, eps, m), one rounding.       */
+/* ------------------------------------------------------------------------ */
+void or_member(const or_config* c, int32_t run, uint32_t t, const float* m, int32_t j, float* x)
+{
+    int32_t half = c->popsize / 2;
+    int32_t p = j < half ? j : j - half;
+    float sgn_sigma = j < half ? c->sigma : -c->sigma;
+    int64_t D = c->num_dims;
+    float* eps = (float*)malloc(sizeof(float) * (size_t)D);
+    or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)p, t, 0, D, eps);
+    for (int64_t d = 0; d < D; ++d) x[d] = fmaf(sgn_sigma, eps[d], m[d]);
+    free(eps);
+}
+
+void or_population(const or_config* c, int32_t run, uint32_t t, const float* m, float* x)
+{
+    for (int32_t j = 0; j < c->popsize; ++j) or_member(c, run, t, m, j, x + (int64_t)j * c->num_dims);
+}
+
+/* ------------------------------------------------------------------------ */
+/* evaluate: benchmark problems (BBOB family named in Sec. 3.2); formulas as  */
+/* the workloads state them; fp64 accumulation over fp32 x, rounded once.    */
+/* ------------------------------------------------------------------------ */
+float or_fitness_bbob(int32_t problem, const float* x, int64_t D, const float* s, float a)
+{
+    double acc = 0.0;
+    if (problem == OR_PROB_SPHERE) {
+        for (int64_t i = 0; i < D; ++i) acc += (double)x[i] * (double)x[i];
+    } else if (problem == OR_PROB_SHIFTED_SPHERE) {
+        for (int64_t i = 0; i < D; ++i) {
+            double d = (double)x[i] - (double)s[i];
+            acc += d * d;
+        }
+    } else if (problem == OR_PROB_ROSENBROCK) {
+        for (int64_t i = 0; i + 1 < D; ++i) {
+            double xi = x[i], xn = x[i + 1];
+            double q = xn - xi * xi;
+            acc += 100.0 * q * q + (1.0 - xi) * (1.0 - xi);
+        }
+    } else if (problem == OR_PROB_RASTRIGIN) {
+        acc = (double)a * (double)D;
+        for (int64_t i = 0; i < D; ++i) {
+            double xi = x[i];
+            acc += xi * xi - (double)a * cos(OR_TWO_PI * xi);
+        }
+    } else {
+        return NAN;
+    }
+    return (float)acc;
+}
+
+/* bf16 round-to-nearest-even of an fp32 value (NaN kept quiet). */
+static float or_bf16(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x7fffffu)) {
+        u |= 0x400000u;
+        u &= 0xffff0000u;
+    } else {
+        uint32_t lsb = (u >> 16) & 1u;
+        u += 0x7fffu + lsb;
+        u &= 0xffff0000u;
+    }
+    float r;
+    memcpy(&r, &u, 4);
+    return r;
+}
+
+/* Generation-t input batch X_t [B][64], N(0,1) from the EVAL stream of the
+ * base seed (shared by every member and run).                               */
+void or_mlp_inputs(const or_config* c, uint32_t t, float* X)
+{
+    or_normals(c->seed, OR_DOM_EVAL, 0, t, 0, (int64_t)c->mlp_batch * OR_MLP_IN, X);
+}
+
+/* Dense forward of the 64-256-256-16 MLP on B inputs.  bf16 = 1 rounds the
+ * input, every weight and every hidden activation to bf16 (RNE); dot products
+ * accumulate exactly in fp64 and the pre-activation is rounded to fp32.     */
+static void or_mlp_forward(const float* p, const float* X, int32_t B, int bf16, int tanh_out, float* Y)
+{
+    int64_t maxw = OR_MLP_H;
+    float* hin = (float*)malloc(sizeof(float) * (size_t)(B * maxw));
+    float* hout = (float*)malloc(sizeof(float) * (size_t)(B * maxw));
+    for (int64_t i = 0; i < (int64_t)B * OR_MLP_IN; ++i) hin[i] = bf16 ? or_bf16(X[i]) : X[i];
+    const float* q = p;
+    for (int l = 0; l < 3; ++l) {
+        int64_t fi = or_mlp_fan_in[l], fo = or_mlp_fan_out[l];
+        const float* W = q;
+        const float* bias = q + fi * fo;
+        for (int32_t n = 0; n < B; ++n) {
+            for (int64_t o = 0; o < fo; ++o) {
+                double acc = 0.0;
+                for (int64_t k = 0; k < fi; ++k) {
+                    float w = bf16 ? or_bf16(W[o * fi + k]) : W[o * fi + k];
+                    acc += (double)hin[n * fi + k] * (double)w;
+                }
+                float pre = (float)(acc + (double)bias[o]);
+                float h;
+                if (l < 2 || tanh_out) h = (float)tanh((double)pre);
+                else h = pre;
+                if (l < 2 && bf16) h = or_bf16(h);
+                hout[n * fo + o] = h;
+            }
+        }
+        float* tmp = hin; hin = hout; hout = tmp;
+        q += fi * fo + fo;
+    }
+    for (int64_t i = 0; i < (int64_t)B * OR_MLP_OUT; ++i) Y[i] = hin[i];
+    free(hin);
+    free(hout);
+}
+
+/* Teacher targets for generation t: fp32 teacher (no bf16) on X_t. */
+void or_mlp_teacher_out(const or_config* c, const float* teacher, uint32_t t, float* YT)
+{
+    float* X = (float*)malloc(sizeof(float) * (size_t)c->mlp_batch * OR_MLP_IN);
+    or_mlp_inputs(c, t, X);
+    or_mlp_forward(teacher, X, c->mlp_batch, 0, c->mlp_tanh_out, YT);
+    free(X);
+}
+
+/* MLP fitness of one parameter vector: -MSE against the teacher targets. */
+float or_mlp_fitness(const or_config* c, const float* x, uint32_t t, const float* YT)
+{
+    int32_t B = c->mlp_batch;
+    float* X = (float*)malloc(sizeof(float) * (size_t)B * OR_MLP_IN);
+    float* Y = (float*)malloc(sizeof(float) * (size_t)B * OR_MLP_OUT);
+    or_mlp_inputs(c, t, X);
+    or_mlp_forward(x, X, B, c->mlp_bf16, c->mlp_tanh_out, Y);
+    double acc = 0.0;
+    for (int64_t i = 0; i < (int64_t)B * OR_MLP_OUT; ++i) {
+        double d = (double)Y[i] - (double)YT[i];
+        acc += d * d;
+    }
+    free(X);
+    free(Y);
+    return (float)(-(acc / (double)((int64_t)B * OR_MLP_OUT)));
+}
+
+/* Fitness of the listed members js[0..nj) of run r at generation t. */
+void or_eval_members(const or_config* c, int32_t run, uint32_t t, const float* m,
+                     const float* pdata, const int32_t* js, int32_t nj, float* f)
+{
+    int64_t D = c->num_dims;
+    float* x = (float*)malloc(sizeof(float) * (size_t)D);
+    float* YT = NULL;
+    if (c->problem == OR_PROB_MLP) {
+        YT = (float*)malloc(sizeof(float) * (size_t)c->mlp_batch * OR_MLP_OUT);
+        or_mlp_teacher_out(c, pdata, t, YT);
+    }
+    for (int32_t i = 0; i < nj; ++i) {
+        or_member(c, run, t, m, js[i], x);
+        if (c->problem == OR_PROB_MLP) f[i] = or_mlp_fitness(c, x, t, YT);
+        else f[i] = or_fitness_bbob(c->problem, x, D, pdata, c->rastrigin_a);
+    }
+    free(x);
+    free(YT);
+}
+
+/* ------------------------------------------------------------------------ */
+/* tell, step 1: fitness shaping (Sec. 3.2 "centered rank"; App. B).         */
+/* Readings: key = f (minimise, Listing 1) or -f (maximise); NaN is the      */
+/* worst value (+inf key); -0 == +0.  rank = position in a stable ascending   */
+/* sort, i.e. ties broken by member index.                                   */
+/* ------------------------------------------------------------------------ */
+static double or_key(float f, int32_t maximize)
+{
+    double k = maximize ? -(double)f : (double)f;
+    if (isnan(k)) k = INFINITY;
+    return k;
+}
+
+void or_ranks(const float* f, int32_t N, int32_t maximize, int32_t* rank)
+{
+    for (int32_t j = 0; j < N; ++j) {
+        double kj = or_key(f[j], maximize);
+        int32_t r = 0;
+        for (int32_t k = 0; k < N; ++k) {
+            double kk = or_key(f[k], maximize);
+            if (kk < kj || (kk == kj && k < j)) ++r;
+        }
+        rank[j] = r;
+    }
+}
+
+/* Centered rank y = rank/(N-1) - 1/2, written as the single fp32 quotient
+ * (2 rank - (N-1)) / (2 (N-1)) of two exact integers (reading that fixes the
+ * bits).  RAW (test mode): y = key.                                         */
+void or_shape(const float* f, int32_t N, int32_t maximize, int32_t shaping, float* y)
+{
+    if (shaping == OR_SHAPE_RAW) {
+        for (int32_t j = 0; j < N; ++j) y[j] = maximize ? -f[j] : f[j];
+        return;
+    }
+    int32_t* rank = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
+    or_ranks(f, N, maximize, rank);
+    float den = (float)(2 * (N - 1));
+    for (int32_t j = 0; j < N; ++j) y[j] = (float)(2 * rank[j] - (N - 1)) / den;
+    free(rank);
+}
+
+/* ------------------------------------------------------------------------ */
+/* tell, step 2: FD gradient estimate (Sec. 2.1 estimator) over the whole    */
+/* population, g = E^T y / (N sigma), E the N x D matrix of perturbations    */
+/* (row j = +eps_j or -eps_{j-N/2}).  fp64 accumulation, one fp32 rounding.  */
+/* Computes dims [d0, d0+nd) only.                                           */
+/* ------------------------------------------------------------------------ */
+void or_grad(const or_config* c, int32_t run, uint32_t t, const float* y,
+             int64_t d0, int64_t nd, float* g)
+{
+    int32_t N = c->popsize, half = N / 2;
+    double* acc = (double*)calloc((size_t)nd, sizeof(double));
+    float* eps = (float*)malloc(sizeof(float) * (size_t)nd);
+    for (int32_t j = 0; j < N; ++j) {
+        int32_t p = j < half ? j : j - half;
+        double sgn = j < half ? 1.0 : -1.0;
+        or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)p, t, d0, nd, eps);
+        for (int64_t i = 0; i < nd; ++i) acc[i] += (double)y[j] * sgn * (double)eps[i];
+    }
+    double scale = (double)N * (double)c->sigma;
+    for (int64_t i = 0; i < nd; ++i) g[i] = (float)(acc[i] / scale);
+    free(acc);
+    free(eps);
+}
+
+/* ------------------------------------------------------------------------ */
+/* tell, step 3: Adam (Kingma & Ba 2015, Algorithm 1) on the mean; the paper  */
+/* names Adam as the optimiser (Sec. 2.1; App. B) without a formula.         */
+/* Reading: fp32 state, t' = t + 1 counted from 1, bias corrections          */
+/* bc = 1 - beta^t' evaluated in fp64 and rounded to fp32, eps outside sqrt,  */
+/* this exact fp32 operation order:                                          */
+/*   m1 = fmaf(b1, m1, (1-b1)*g);  v = fmaf(b2, v, (1-b2)*(g*g));           */
+/*   q = (m1/bc1) / (sqrt(v/bc2) + eps);  m = fmaf(-lr, q, m).               */
+/* ------------------------------------------------------------------------ */
+void or_adam(const or_config* c, int64_t t, const float* g, int64_t n, float* m, float* m1, float* v)
+{
+    double tp = (double)(t + 1);
+    float bc1 = (float)(1.0 - pow((double)c->beta1, tp));
+    float bc2 = (float)(1.0 - pow((double)c->beta2, tp));
+    float omb1 = (float)(1.0 - (double)c->beta1);
+    float omb2 = (float)(1.0 - (double)c->beta2);
+    for (int64_t i = 0; i < n; ++i) {
+        float gi = g[i];
+        float a = omb1 * gi;
+        float nm1 = fmaf(c->beta1, m1[i], a);
+        float gg = gi * gi;
+        float b = omb2 * gg;
+        float nv = fmaf(c->beta2, v[i], b);
+        float mhat = nm1 / bc1;
+        float vhat = nv / bc2;
+        float den = sqrtf(vhat) + c->eps;
+        float q = mhat / den;
+        m[i] = fmaf(-c->lr, q, m[i]);
+        m1[i] = nm1;
+        v[i] = nv;
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* One generation of one run (ask -> evaluate -> tell), the body of the      */
+/* scanned loop of Sec. 2.2 (Listing 2).  fit_in != NULL replaces the        */
+/* built-in evaluation (the user's own evaluate step).  Best-so-far member   */
+/* and fitness (state fields of Listing 1) are updated from the generation's */
+/* rank-0 member when it is strictly better.                                 */
+/* Outputs (any may be NULL): fit_out[N], y_out[N], g_out[D].                 */
+/* best_key / best_f / best_x carry the best-so-far state.                   */
+/* ------------------------------------------------------------------------ */
+void or_generation(const or_config* c, int32_t run, int64_t t, const float* pdata,
+                   float* m, float* m1, float* v, const float* fit_in,
+                   float* fit_out, float* y_out, float* g_out,
+                   double* best_key, float* best_f, float* best_x)
+{
+    int32_t N = c->popsize;
+    int64_t D = c->num_dims;
+    float* f = (float*)malloc(sizeof(float) * (size_t)N);
+    float* y = (float*)malloc(sizeof(float) * (size_t)N);
+    float* g = (float*)malloc(sizeof(float) * (size_t)D);
+    int32_t* rank = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
+    if (fit_in) {
+        memcpy(f, fit_in, sizeof(float) * (size_t)N);
+    } else {
+        int32_t* js = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
+        for (int32_t j = 0; j < N; ++j) js[j] = j;
+        or_eval_members(c, run, (uint32_t)t, m, pdata, js, N, f);
+        free(js);
+    }
+    or_ranks(f, N, c->maximize, rank);
+    int32_t jbest = 0;
+    for (int32_t j = 0; j < N; ++j)
+        if (rank[j] == 0) jbest = j;
+    double kb = or_key(f[jbest], c->maximize);
+    if (best_key && kb < *best_key) {
+        *best_key = kb;
+        if (best_f) *best_f = f[jbest];
+        if (best_x) or_member(c, run, (uint32_t)t, m, jbest, best_x);
+    }
+    or_shape(f, N, c->maximize, c->shaping, y);
+    or_grad(c, run, (uint32_t)t, y, 0, D, g);
+    or_adam(c, t, g, D, m, m1, v);
+    if (fit_out) memcpy(fit_out, f, sizeof(float) * (size_t)N);
+    if (y_out) memcpy(y_out, y, sizeof(float) * (size_t)N);
+    if (g_out) memcpy(g_out, g, sizeof(float) * (size_t)D);
+    free(f);
+    free(y);
+    free(g);
+    free(rank);
+}

@@ -1,0 +1,179 @@
+/*
+ * esmi.h -- C-ABI of the MI355X (gfx950) OpenAI-ES generation library.
+ *
+ * The library runs the ask / evaluate / tell loop of the evosax report
+ * (arXiv 2212.04180, Sec. 2.1, Listing 1) for OpenAI-ES (Table 1, FDG class)
+ * on R independent runs at once (the vmap over seeds of Sec. 2.2, Listing 3):
+ *   ask      antithetic Gaussian perturbations x = m +- sigma*eps, eps drawn
+ *            from a counter-based Philox-4x32-10 stream and regenerated on
+ *            demand -- never stored;
+ *   evaluate built-in benchmark problems (Sec. 3.2: sphere, shifted sphere,
+ *            Rosenbrock, Rastrigin; a teacher-student MLP), fused with ask;
+ *   tell     centered-rank fitness shaping (Sec. 3.2; App. B), the
+ *            finite-difference gradient estimate of Sec. 2.1,
+ *            g = E^T y / (N sigma), and an Adam step on the mean (App. B).
+ *
+ * Conventions shared by every entry point:
+ *   - Device pointers are HIP device addresses on the device that was
+ *     current when es_init ran; host pointers are ordinary memory.  Arrays
+ *     are dense, row-major, fp32 unless stated: a "[R][N]" array holds
+ *     element (r, j) at r*N + j.
+ *   - Every call only enqueues work on the stream given to es_init and
+ *     returns without waiting, except where "synchronous" is stated.
+ *     Outputs are valid once that stream has been synchronized (es_sync).
+ *   - The caller owns every buffer it passes; the handle owns its state
+ *     (mean, Adam moments, best-so-far, problem data, scratch).
+ *   - No call throws.  A negative es_status reports an error; the message
+ *     is available from es_last_error(h).  A failed call leaves the state
+ *     unchanged unless it is ES_ERR_HIP (then the handle should be
+ *     destroyed).
+ *   - A handle is not thread-safe; distinct handles are independent.
+ *   - Minimisation is the default (Listing 1); maximize = 1 negates keys.
+ */
+#ifndef ESMI_H
+#define ESMI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ES_OK = 0,
+    ES_ERR_ARG = -1,         /* invalid argument or configuration            */
+    ES_ERR_SEQUENCE = -2,    /* call out of ask -> (eval) -> tell order        */
+    ES_ERR_HIP = -3,         /* a HIP runtime call failed                     */
+    ES_ERR_OOM = -4,         /* device allocation failed                      */
+    ES_ERR_UNSUPPORTED = -5  /* valid request this build does not implement   */
+} es_status;
+
+typedef enum { ES_SHAPE_CENTERED_RANK = 0, ES_SHAPE_RAW = 1 } es_shaping;
+
+typedef enum {
+    ES_PROB_NONE = 0,           /* fitness only from the caller (es_tell)           */
+    ES_PROB_SPHERE = 1,         /* sum x_i^2                                        */
+    ES_PROB_SHIFTED_SPHERE = 2, /* sum (x_i - s_i)^2, s ~ N(0,1) from the base seed */
+    ES_PROB_ROSENBROCK = 3,     /* sum_{i<D-1} 100 (x_{i+1} - x_i^2)^2 + (1 - x_i)^2 */
+    ES_PROB_RASTRIGIN = 4,      /* A D + sum x_i^2 - A cos(2 pi x_i)                */
+    ES_PROB_MLP = 5             /* -MSE of a 64-256-256-16 tanh MLP vs a teacher    */
+} es_problem;
+
+typedef enum { ES_INIT_UNIFORM = 0, ES_INIT_ZERO = 1, ES_INIT_FANIN_NORMAL = 2 } es_init_kind;
+
+/* Flags (es_config.flags). */
+#define ES_FLAG_KEEP_GRAD 1u /* es_tell also stores g [R][D] for es_get_grad */
+
+/*
+ * Strategy parameters (the default_params of Listing 1; App. B, OpenAI-ES
+ * table).  Random streams: run r uses key seed + r; the shift vector, the
+ * teacher network and the MLP inputs come from the base seed and are shared
+ * by all runs.
+ */
+typedef struct es_config {
+    int64_t num_dims;   /* D >= 1                                           */
+    uint64_t seed;      /* base seed                                         */
+    int32_t popsize;    /* N >= 2, even: N/2 antithetic pairs                */
+    int32_t num_runs;   /* R >= 1 independent runs                           */
+    float sigma;        /* > 0, perturbation scale                           */
+    float lr;           /* Adam learning rate                                */
+    float beta1, beta2; /* Adam moment decays in [0, 1)                      */
+    float eps;          /* Adam epsilon (outside the square root)            */
+    int32_t maximize;   /* 0: minimise (default), 1: maximise               */
+    int32_t shaping;    /* es_shaping                                        */
+    int32_t init;       /* es_init_kind for the initial mean                 */
+    float init_lo, init_hi; /* ES_INIT_UNIFORM range [lo, hi)                */
+    int32_t problem;    /* es_problem used by es_eval / es_run               */
+    float rastrigin_a;  /* A of Rastrigin (10)                               */
+    int32_t mlp_batch;  /* ES_PROB_MLP: inputs per generation (256)          */
+    int32_t mlp_bf16;   /* ES_PROB_MLP: 1 = bf16 matrix-core forward         */
+    int32_t mlp_tanh_out; /* ES_PROB_MLP: 1 = tanh on the output layer       */
+    uint32_t flags;     /* ES_FLAG_*                                         */
+} es_config;
+
+typedef struct es_handle es_handle;
+
+/* Create a strategy: validates cfg, allocates device state and enqueues the
+ * initial mean (Listing 1 initialize), m1 = v = 0, t = 0, best = none.
+ * hip_stream: a hipStream_t (NULL = the default stream) used by every later
+ * call.  On success *out owns the handle (free with es_destroy). */
+es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out);
+
+/* ask (Sec. 2.1 step 1): starts generation t.  x_out: NULL (the population
+ * stays virtual and is regenerated where needed) or a device [R][N][D]
+ * buffer that receives x_j = m + sigma*eps_j (j < N/2) and
+ * m - sigma*eps_{j-N/2} (j >= N/2).  ES_ERR_SEQUENCE if the previous ask was
+ * not followed by es_tell. */
+es_status es_ask(es_handle* h, float* x_out);
+
+/* evaluate (Sec. 2.1 step 2) with the configured built-in problem, fused
+ * with the sampling: fitness_out device [R][N].  Requires a preceding es_ask
+ * for this generation; ES_ERR_UNSUPPORTED for ES_PROB_NONE. */
+es_status es_eval(es_handle* h, float* fitness_out);
+
+/* tell (Sec. 2.1 step 3): centered ranks (ties by member index, NaN worst),
+ * g = E^T y / (N sigma) with eps regenerated from the counter, Adam step on
+ * the mean, best-so-far update; t += 1.  fitness: device [R][N] from es_eval
+ * or from the caller's own evaluation of the asked population. */
+es_status es_tell(es_handle* h, const float* fitness);
+
+/* T fused generations (the scanned loop of Listing 2) with the built-in
+ * problem.  log: NULL or device [T][R] receiving each generation's best
+ * fitness (the member of rank 0).  Requires no open ask. */
+es_status es_run(es_handle* h, int32_t T, float* log);
+
+/* Copy out / replace the search state.  m, m1, v: device [R][D] (NULL to
+ * skip); t: number of completed generations.  es_set_state requires no open
+ * ask. */
+es_status es_get_state(es_handle* h, float* m, float* m1, float* v, int64_t* t);
+es_status es_set_state(es_handle* h, const float* m, const float* m1, const float* v, int64_t t);
+
+/* Best member and fitness seen so far (state fields of Listing 1).
+ * member: device [R][D], fitness: device [R] (NaN while none). */
+es_status es_get_best(es_handle* h, float* member, float* fitness);
+
+/* Diagnostics of the last es_tell: shaped weights y [R][N], ranks [R][N]
+ * (int32), and -- when ES_FLAG_KEEP_GRAD is set -- the gradient g [R][D].
+ * Device pointers; NULL to skip. */
+es_status es_get_shaped(es_handle* h, float* y, int32_t* rank);
+es_status es_get_grad(es_handle* h, float* g);
+
+/* Problem data shared by all runs: the shift vector s [D] (shifted sphere)
+ * or the flattened teacher network [D] (MLP).  Device pointer. */
+es_status es_get_problem_data(es_handle* h, float* out);
+
+/* Raw stream for one (run, generation t, pair): the Philox words
+ * words[4*ceil(D/4)] (uint32) and the normals eps[D].  Device pointers; NULL
+ * to skip.  Uses the same device code as ask, evaluate and tell. */
+es_status es_debug_noise(es_handle* h, int32_t run, int64_t t, int32_t pair,
+                         uint32_t* words, float* eps);
+
+/* Checkpoint (synchronous): with host_buf NULL, *bytes receives the size;
+ * otherwise the state (config, t, m, m1, v, best) is written to host_buf.
+ * es_load_state restores a checkpoint of a handle with the same config.
+ * The random stream is a pure function of (seed, t), so resuming continues
+ * the same trajectory bit for bit. */
+es_status es_save_state(es_handle* h, void* host_buf, size_t* bytes);
+es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes);
+
+/* Wait for all work enqueued by this handle (synchronous). */
+es_status es_sync(es_handle* h);
+
+/* Current generation counter t (host value; no device work). */
+int64_t es_generation(const es_handle* h);
+
+/* Message of the last failed call on h ("" if none); with h == NULL, the
+ * message of the last failed es_init on this thread.  Never NULL. */
+const char* es_last_error(const es_handle* h);
+
+/* Static description of a status code. */
+const char* es_status_string(es_status s);
+
+/* Release the handle and its device memory (waits for its stream). */
+void es_destroy(es_handle* h);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ESMI_H */

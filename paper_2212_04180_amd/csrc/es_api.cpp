@@ -1,0 +1,500 @@
+// es_api.cpp -- host runtime behind the C-ABI of esmi.h.
+//
+// Owns the handle (config, device state, scratch), validates arguments,
+// enforces the ask -> (evaluate) -> tell order of Sec. 2.1 / Listing 1 and
+// sequences the kernel launches on the caller's stream.  No call blocks
+// unless esmi.h says it is synchronous.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+
+#include "es_internal.hpp"
+#include "esmi.h"
+
+using namespace esmi;
+
+namespace {
+
+enum Phase { READY = 0, ASKED = 1 };
+
+constexpr uint32_t kCheckpointMagic = 0x45534d31u;  // "ESM1"
+
+thread_local char g_init_err[256] = {0};
+
+es_status init_fail(es_status s, const char* msg)
+{
+    std::snprintf(g_init_err, sizeof(g_init_err), "es_init: %s", msg);
+    return s;
+}
+
+}  // namespace
+
+struct es_handle {
+    es_config cfg;
+    Geometry g;
+    EvalPlan plan;
+    hipStream_t stream = nullptr;
+    int device = 0;
+    int64_t t = 0;
+    int phase = READY;
+    // state [R][Dp]
+    float* m = nullptr;
+    float* m1 = nullptr;
+    float* v = nullptr;
+    float* best_x = nullptr;
+    float* grad = nullptr;
+    // per-run scalars
+    uint32_t* best_okey = nullptr;
+    float* best_f = nullptr;
+    int32_t* best_j = nullptr;
+    // per-generation scratch
+    float* table = nullptr;  // centered weight per rank [N]
+    float* y = nullptr;      // [R][N]
+    int32_t* rank = nullptr; // [R][N]
+    float* wfold = nullptr;  // [R][P]
+    float* fit = nullptr;    // [R][N] fitness scratch for es_run
+    double* partial = nullptr;
+    float* pdata = nullptr;  // [Dp] shift vector or teacher
+    char err[512] = {0};
+};
+
+namespace {
+
+es_status fail(es_handle* h, es_status s, const char* fmt, ...)
+{
+    if (h) {
+        va_list ap;
+        va_start(ap, fmt);
+        vsnprintf(h->err, sizeof(h->err), fmt, ap);
+        va_end(ap);
+    }
+    return s;
+}
+
+es_status hip_fail(es_handle* h, hipError_t e, const char* what)
+{
+    return fail(h, e == hipErrorOutOfMemory ? ES_ERR_OOM : ES_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define ES_HIP(h, call, what)                                   \
+    do {                                                        \
+        hipError_t e__ = (call);                                \
+        if (e__ != hipSuccess) return hip_fail((h), e__, what); \
+    } while (0)
+
+template <typename T>
+hipError_t dalloc(T** p, size_t n)
+{
+    *p = nullptr;
+    if (n == 0) n = 1;
+    return hipMalloc(reinterpret_cast<void**>(p), n * sizeof(T));
+}
+
+const char* validate(const es_config& c)
+{
+    if (c.num_dims < 1) return "num_dims must be >= 1";
+    if (c.num_dims > ((int64_t)1 << 34)) return "num_dims exceeds 2^34";
+    if (c.popsize < 2 || (c.popsize & 1)) return "popsize must be even and >= 2";
+    if (c.popsize > RANK_MAX_N) return "popsize exceeds 16384";
+    if (c.num_runs < 1 || c.num_runs > 65535) return "num_runs must be in [1, 65535]";
+    if (!(c.sigma > 0.0f) || !std::isfinite(c.sigma)) return "sigma must be finite and > 0";
+    if (!std::isfinite(c.lr) || c.lr < 0.0f) return "lr must be finite and >= 0";
+    if (!(c.beta1 >= 0.0f && c.beta1 < 1.0f)) return "beta1 must be in [0, 1)";
+    if (!(c.beta2 >= 0.0f && c.beta2 < 1.0f)) return "beta2 must be in [0, 1)";
+    if (!(c.eps >= 0.0f) || !std::isfinite(c.eps)) return "eps must be finite and >= 0";
+    if (c.maximize != 0 && c.maximize != 1) return "maximize must be 0 or 1";
+    if (c.shaping != ES_SHAPE_CENTERED_RANK && c.shaping != ES_SHAPE_RAW) return "unknown shaping";
+    if (c.init < ES_INIT_UNIFORM || c.init > ES_INIT_FANIN_NORMAL) return "unknown init";
+    if (c.init == ES_INIT_UNIFORM && !(c.init_hi > c.init_lo)) return "init range must have hi > lo";
+    if (c.problem < ES_PROB_NONE || c.problem > ES_PROB_MLP) return "unknown problem";
+    if (c.init == ES_INIT_FANIN_NORMAL && c.num_dims != 86544)
+        return "fan-in normal init is defined for the 64-256-256-16 MLP (num_dims 86544)";
+    if (c.problem == ES_PROB_MLP && c.num_dims != 86544) return "MLP problem needs num_dims 86544";
+    if (c.problem == ES_PROB_RASTRIGIN && !std::isfinite(c.rastrigin_a)) return "rastrigin_a must be finite";
+    if ((c.flags & ~ES_FLAG_KEEP_GRAD) != 0) return "unknown flags";
+    return nullptr;
+}
+
+// Centered-rank weight of rank k: the fp32 quotient (2k - (N-1)) / (2(N-1)).
+void weight_table(int32_t N, float* out)
+{
+    const float den = (float)(2 * (N - 1));
+    for (int32_t k = 0; k < N; ++k) out[k] = (float)(2 * k - (N - 1)) / den;
+}
+
+AdamConsts adam_consts(const es_config& c, int64_t t)
+{
+    AdamConsts a;
+    const double tp = (double)(t + 1);
+    a.lr = c.lr;
+    a.beta1 = c.beta1;
+    a.beta2 = c.beta2;
+    a.omb1 = (float)(1.0 - (double)c.beta1);
+    a.omb2 = (float)(1.0 - (double)c.beta2);
+    a.bc1 = (float)(1.0 - std::pow((double)c.beta1, tp));
+    a.bc2 = (float)(1.0 - std::pow((double)c.beta2, tp));
+    a.eps = c.eps;
+    return a;
+}
+
+int64_t env_i64(const char* name, int64_t dflt)
+{
+    const char* s = std::getenv(name);
+    if (!s || !*s) return dflt;
+    return std::strtoll(s, nullptr, 10);
+}
+
+void free_all(es_handle* h)
+{
+    void* ptrs[] = {h->m, h->m1, h->v, h->best_x, h->grad, h->best_okey, h->best_f, h->best_j, h->table,
+                    h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata};
+    for (void* p : ptrs)
+        if (p) (void)hipFree(p);
+}
+
+es_status enqueue_tell(es_handle* h, const float* fitness, float* gen_best)
+{
+    const Geometry& g = h->g;
+    ES_HIP(h, launch_rank(g, h->cfg, fitness, h->table, h->y, h->rank, h->wfold, h->best_okey, h->best_f,
+                          h->best_j, gen_best, h->stream),
+           "rank kernel");
+    const AdamConsts a = adam_consts(h->cfg, h->t);
+    const double inv_ns = 1.0 / ((double)g.N * (double)h->cfg.sigma);
+    ES_HIP(h, launch_tell(g, h->cfg, (uint32_t)h->t, a, inv_ns, h->wfold, h->best_j, h->m, h->m1, h->v,
+                          h->grad, h->best_x, h->stream),
+           "tell kernel");
+    return ES_OK;
+}
+
+es_status enqueue_eval(es_handle* h, float* fit)
+{
+    if (h->cfg.problem == ES_PROB_NONE) return fail(h, ES_ERR_UNSUPPORTED, "no built-in problem configured");
+    if (h->cfg.problem == ES_PROB_MLP) return fail(h, ES_ERR_UNSUPPORTED, "MLP evaluation is not built");
+    ES_HIP(h, launch_eval_bbob(h->g, h->cfg, h->plan, (uint32_t)h->t, h->m, h->pdata, h->partial, fit, h->stream),
+           "evaluate kernel");
+    return ES_OK;
+}
+
+es_status copy_rows_out(es_handle* h, float* dst, const float* src)
+{
+    const Geometry& g = h->g;
+    ES_HIP(h, hipMemcpy2DAsync(dst, (size_t)g.D * 4, src, (size_t)g.Dp * 4, (size_t)g.D * 4, (size_t)g.R,
+                               hipMemcpyDeviceToDevice, h->stream),
+           "copy out");
+    return ES_OK;
+}
+
+es_status copy_rows_in(es_handle* h, float* dst, const float* src)
+{
+    const Geometry& g = h->g;
+    if (g.Dp != g.D)
+        ES_HIP(h, hipMemsetAsync(dst, 0, (size_t)g.Dp * g.R * 4, h->stream), "clear padding");
+    ES_HIP(h, hipMemcpy2DAsync(dst, (size_t)g.Dp * 4, src, (size_t)g.D * 4, (size_t)g.D * 4, (size_t)g.R,
+                               hipMemcpyDeviceToDevice, h->stream),
+           "copy in");
+    return ES_OK;
+}
+
+struct CkptHeader {
+    uint32_t magic;
+    uint32_t version;
+    es_config cfg;
+    int64_t t;
+    int64_t D, R;
+};
+
+}  // namespace
+
+extern "C" {
+
+const char* es_status_string(es_status s)
+{
+    switch (s) {
+    case ES_OK: return "ok";
+    case ES_ERR_ARG: return "invalid argument";
+    case ES_ERR_SEQUENCE: return "call out of ask/eval/tell order";
+    case ES_ERR_HIP: return "HIP runtime error";
+    case ES_ERR_OOM: return "device out of memory";
+    case ES_ERR_UNSUPPORTED: return "unsupported request";
+    }
+    return "unknown status";
+}
+
+const char* es_last_error(const es_handle* h) { return h ? h->err : g_init_err; }
+
+int64_t es_generation(const es_handle* h) { return h ? h->t : -1; }
+
+es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
+{
+    if (!cfg || !out) return init_fail(ES_ERR_ARG, "null argument");
+    *out = nullptr;
+    if (const char* why = validate(*cfg)) return init_fail(ES_ERR_ARG, why);
+    es_handle* h = new (std::nothrow) es_handle();
+    if (!h) return init_fail(ES_ERR_OOM, "host allocation failed");
+    h->cfg = *cfg;
+    h->stream = reinterpret_cast<hipStream_t>(hip_stream);
+    Geometry& g = h->g;
+    g.D = cfg->num_dims;
+    g.nb = (g.D + 3) / 4;
+    g.Dp = 4 * g.nb;
+    g.N = cfg->popsize;
+    g.P = cfg->popsize / 2;
+    g.R = cfg->num_runs;
+    h->plan = eval_plan(g, env_i64("ESMI_EVAL_BLOCKS_PER_CHUNK", 0));
+    hipError_t e = hipGetDevice(&h->device);
+    const size_t rows = (size_t)g.Dp * g.R;
+    if (e == hipSuccess) e = dalloc(&h->m, rows);
+    if (e == hipSuccess) e = dalloc(&h->m1, rows);
+    if (e == hipSuccess) e = dalloc(&h->v, rows);
+    if (e == hipSuccess) e = dalloc(&h->best_x, rows);
+    if (e == hipSuccess && (cfg->flags & ES_FLAG_KEEP_GRAD)) e = dalloc(&h->grad, rows);
+    if (e == hipSuccess) e = dalloc(&h->best_okey, (size_t)g.R);
+    if (e == hipSuccess) e = dalloc(&h->best_f, (size_t)g.R);
+    if (e == hipSuccess) e = dalloc(&h->best_j, (size_t)g.R);
+    if (e == hipSuccess) e = dalloc(&h->table, (size_t)g.N);
+    if (e == hipSuccess) e = dalloc(&h->y, (size_t)g.N * g.R);
+    if (e == hipSuccess) e = dalloc(&h->rank, (size_t)g.N * g.R);
+    if (e == hipSuccess) e = dalloc(&h->wfold, (size_t)g.P * g.R);
+    if (e == hipSuccess) e = dalloc(&h->fit, (size_t)g.N * g.R);
+    if (e == hipSuccess && cfg->problem != ES_PROB_NONE && cfg->problem != ES_PROB_MLP)
+        e = dalloc(&h->partial, (size_t)eval_partial_elems(g, h->plan));
+    if (e == hipSuccess && (cfg->problem == ES_PROB_SHIFTED_SPHERE || cfg->problem == ES_PROB_MLP))
+        e = dalloc(&h->pdata, (size_t)g.Dp);
+    if (e != hipSuccess) {
+        free_all(h);
+        delete h;
+        return init_fail(e == hipErrorOutOfMemory ? ES_ERR_OOM : ES_ERR_HIP, hipGetErrorString(e));
+    }
+    // weight table (host-computed, exact fp32 quotients) and best-so-far init
+    float* tab = static_cast<float*>(std::malloc(sizeof(float) * (size_t)g.N));
+    uint32_t* ok = static_cast<uint32_t*>(std::malloc(sizeof(uint32_t) * (size_t)g.R));
+    float* bf = static_cast<float*>(std::malloc(sizeof(float) * (size_t)g.R));
+    if (!tab || !ok || !bf) {
+        std::free(tab); std::free(ok); std::free(bf);
+        free_all(h);
+        delete h;
+        return init_fail(ES_ERR_OOM, "host allocation failed");
+    }
+    weight_table(g.N, tab);
+    for (int32_t r = 0; r < g.R; ++r) {
+        ok[r] = 0xFF800000u;  // order key of +inf: nothing is an improvement over it but a finite key
+        bf[r] = NAN;
+    }
+    e = hipMemcpyAsync(h->table, tab, sizeof(float) * (size_t)g.N, hipMemcpyHostToDevice, h->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(h->best_okey, ok, sizeof(uint32_t) * (size_t)g.R, hipMemcpyHostToDevice, h->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(h->best_f, bf, sizeof(float) * (size_t)g.R, hipMemcpyHostToDevice, h->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->stream);  // host staging buffers are freed next
+    std::free(tab); std::free(ok); std::free(bf);
+    if (e == hipSuccess) e = launch_init(g, *cfg, h->m, h->m1, h->v, h->best_x, h->stream);
+    if (e == hipSuccess && h->pdata) e = launch_problem_data(g, *cfg, h->pdata, h->stream);
+    if (e != hipSuccess) {
+        free_all(h);
+        delete h;
+        return init_fail(ES_ERR_HIP, hipGetErrorString(e));
+    }
+    g_init_err[0] = 0;
+    *out = h;
+    return ES_OK;
+}
+
+es_status es_ask(es_handle* h, float* x_out)
+{
+    if (!h) return ES_ERR_ARG;
+    if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_ask: previous generation was not told");
+    if (x_out) ES_HIP(h, launch_ask(h->g, h->cfg, (uint32_t)h->t, h->m, x_out, h->stream), "ask kernel");
+    h->phase = ASKED;
+    h->err[0] = 0;
+    return ES_OK;
+}
+
+es_status es_eval(es_handle* h, float* fitness_out)
+{
+    if (!h || !fitness_out) return h ? fail(h, ES_ERR_ARG, "es_eval: null fitness buffer") : ES_ERR_ARG;
+    if (h->phase != ASKED) return fail(h, ES_ERR_SEQUENCE, "es_eval: no open ask");
+    return enqueue_eval(h, fitness_out);
+}
+
+es_status es_tell(es_handle* h, const float* fitness)
+{
+    if (!h || !fitness) return h ? fail(h, ES_ERR_ARG, "es_tell: null fitness buffer") : ES_ERR_ARG;
+    if (h->phase != ASKED) return fail(h, ES_ERR_SEQUENCE, "es_tell: no open ask");
+    es_status s = enqueue_tell(h, fitness, nullptr);
+    if (s != ES_OK) return s;
+    h->t += 1;
+    h->phase = READY;
+    return ES_OK;
+}
+
+es_status es_run(es_handle* h, int32_t T, float* log)
+{
+    if (!h) return ES_ERR_ARG;
+    if (T < 0) return fail(h, ES_ERR_ARG, "es_run: T must be >= 0");
+    if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_run: an ask is open");
+    if (h->cfg.problem == ES_PROB_NONE) return fail(h, ES_ERR_UNSUPPORTED, "es_run needs a built-in problem");
+    for (int32_t i = 0; i < T; ++i) {
+        es_status s = enqueue_eval(h, h->fit);
+        if (s != ES_OK) return s;
+        s = enqueue_tell(h, h->fit, log ? log + (int64_t)i * h->g.R : nullptr);
+        if (s != ES_OK) return s;
+        h->t += 1;
+    }
+    return ES_OK;
+}
+
+es_status es_get_state(es_handle* h, float* m, float* m1, float* v, int64_t* t)
+{
+    if (!h) return ES_ERR_ARG;
+    es_status s = ES_OK;
+    if (m && (s = copy_rows_out(h, m, h->m)) != ES_OK) return s;
+    if (m1 && (s = copy_rows_out(h, m1, h->m1)) != ES_OK) return s;
+    if (v && (s = copy_rows_out(h, v, h->v)) != ES_OK) return s;
+    if (t) *t = h->t;
+    return ES_OK;
+}
+
+es_status es_set_state(es_handle* h, const float* m, const float* m1, const float* v, int64_t t)
+{
+    if (!h) return ES_ERR_ARG;
+    if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_set_state: an ask is open");
+    if (t < 0 || t > 0xFFFFFFFFll) return fail(h, ES_ERR_ARG, "es_set_state: t out of range");
+    es_status s = ES_OK;
+    if (m && (s = copy_rows_in(h, h->m, m)) != ES_OK) return s;
+    if (m1 && (s = copy_rows_in(h, h->m1, m1)) != ES_OK) return s;
+    if (v && (s = copy_rows_in(h, h->v, v)) != ES_OK) return s;
+    h->t = t;
+    return ES_OK;
+}
+
+es_status es_get_best(es_handle* h, float* member, float* fitness)
+{
+    if (!h) return ES_ERR_ARG;
+    if (member) {
+        es_status s = copy_rows_out(h, member, h->best_x);
+        if (s != ES_OK) return s;
+    }
+    if (fitness)
+        ES_HIP(h, hipMemcpyAsync(fitness, h->best_f, sizeof(float) * (size_t)h->g.R, hipMemcpyDeviceToDevice,
+                                 h->stream),
+               "copy best fitness");
+    return ES_OK;
+}
+
+es_status es_get_shaped(es_handle* h, float* y, int32_t* rank)
+{
+    if (!h) return ES_ERR_ARG;
+    const size_t n = (size_t)h->g.N * h->g.R;
+    if (y) ES_HIP(h, hipMemcpyAsync(y, h->y, n * 4, hipMemcpyDeviceToDevice, h->stream), "copy y");
+    if (rank) ES_HIP(h, hipMemcpyAsync(rank, h->rank, n * 4, hipMemcpyDeviceToDevice, h->stream), "copy ranks");
+    return ES_OK;
+}
+
+es_status es_get_grad(es_handle* h, float* g)
+{
+    if (!h || !g) return h ? fail(h, ES_ERR_ARG, "es_get_grad: null buffer") : ES_ERR_ARG;
+    if (!h->grad) return fail(h, ES_ERR_UNSUPPORTED, "es_get_grad needs ES_FLAG_KEEP_GRAD");
+    return copy_rows_out(h, g, h->grad);
+}
+
+es_status es_get_problem_data(es_handle* h, float* out)
+{
+    if (!h || !out) return h ? fail(h, ES_ERR_ARG, "es_get_problem_data: null buffer") : ES_ERR_ARG;
+    if (!h->pdata) return fail(h, ES_ERR_UNSUPPORTED, "this problem has no problem data");
+    ES_HIP(h, hipMemcpyAsync(out, h->pdata, sizeof(float) * (size_t)h->g.D, hipMemcpyDeviceToDevice, h->stream),
+           "copy problem data");
+    return ES_OK;
+}
+
+es_status es_debug_noise(es_handle* h, int32_t run, int64_t t, int32_t pair, uint32_t* words, float* eps)
+{
+    if (!h) return ES_ERR_ARG;
+    if (run < 0 || run >= h->g.R || pair < 0 || pair >= h->g.P || t < 0 || t > 0xFFFFFFFFll)
+        return fail(h, ES_ERR_ARG, "es_debug_noise: run, pair or t out of range");
+    ES_HIP(h, launch_debug_noise(h->g, h->cfg, run, (uint32_t)t, pair, words, eps, h->stream), "noise kernel");
+    return ES_OK;
+}
+
+es_status es_save_state(es_handle* h, void* host_buf, size_t* bytes)
+{
+    if (!h || !bytes) return ES_ERR_ARG;
+    const Geometry& g = h->g;
+    const size_t rows = (size_t)g.Dp * g.R * sizeof(float);
+    const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + sizeof(float));
+    if (!host_buf) {
+        *bytes = need;
+        return ES_OK;
+    }
+    if (*bytes < need) return fail(h, ES_ERR_ARG, "es_save_state: buffer too small (%zu < %zu)", *bytes, need);
+    if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_save_state: an ask is open");
+    char* p = static_cast<char*>(host_buf);
+    CkptHeader hd;
+    std::memset(&hd, 0, sizeof(hd));
+    hd.magic = kCheckpointMagic;
+    hd.version = 1;
+    hd.cfg = h->cfg;
+    hd.t = h->t;
+    hd.D = g.D;
+    hd.R = g.R;
+    std::memcpy(p, &hd, sizeof(hd));
+    p += sizeof(hd);
+    const float* srcs[4] = {h->m, h->m1, h->v, h->best_x};
+    for (const float* s : srcs) {
+        ES_HIP(h, hipMemcpyAsync(p, s, rows, hipMemcpyDeviceToHost, h->stream), "save state");
+        p += rows;
+    }
+    ES_HIP(h, hipMemcpyAsync(p, h->best_okey, g.R * sizeof(uint32_t), hipMemcpyDeviceToHost, h->stream), "save best");
+    p += g.R * sizeof(uint32_t);
+    ES_HIP(h, hipMemcpyAsync(p, h->best_f, g.R * sizeof(float), hipMemcpyDeviceToHost, h->stream), "save best");
+    ES_HIP(h, hipStreamSynchronize(h->stream), "save sync");
+    *bytes = need;
+    return ES_OK;
+}
+
+es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes)
+{
+    if (!h || !host_buf) return ES_ERR_ARG;
+    if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_load_state: an ask is open");
+    const Geometry& g = h->g;
+    const size_t rows = (size_t)g.Dp * g.R * sizeof(float);
+    const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + sizeof(float));
+    if (bytes < need) return fail(h, ES_ERR_ARG, "es_load_state: checkpoint too small");
+    CkptHeader hd;
+    std::memcpy(&hd, host_buf, sizeof(hd));
+    if (hd.magic != kCheckpointMagic || hd.version != 1)
+        return fail(h, ES_ERR_ARG, "es_load_state: not a checkpoint of this library");
+    if (std::memcmp(&hd.cfg, &h->cfg, sizeof(es_config)) != 0 || hd.D != g.D || hd.R != g.R)
+        return fail(h, ES_ERR_ARG, "es_load_state: checkpoint was written with another config");
+    const char* p = static_cast<const char*>(host_buf) + sizeof(hd);
+    float* dsts[4] = {h->m, h->m1, h->v, h->best_x};
+    for (float* d : dsts) {
+        ES_HIP(h, hipMemcpyAsync(d, p, rows, hipMemcpyHostToDevice, h->stream), "load state");
+        p += rows;
+    }
+    ES_HIP(h, hipMemcpyAsync(h->best_okey, p, g.R * sizeof(uint32_t), hipMemcpyHostToDevice, h->stream), "load best");
+    p += g.R * sizeof(uint32_t);
+    ES_HIP(h, hipMemcpyAsync(h->best_f, p, g.R * sizeof(float), hipMemcpyHostToDevice, h->stream), "load best");
+    ES_HIP(h, hipStreamSynchronize(h->stream), "load sync");
+    h->t = hd.t;
+    return ES_OK;
+}
+
+es_status es_sync(es_handle* h)
+{
+    if (!h) return ES_ERR_ARG;
+    ES_HIP(h, hipStreamSynchronize(h->stream), "stream synchronize");
+    return ES_OK;
+}
+
+void es_destroy(es_handle* h)
+{
+    if (!h) return;
+    (void)hipStreamSynchronize(h->stream);
+    free_all(h);
+    delete h;
+}
+
+}  // extern "C"

@@ -1,0 +1,97 @@
+// es_device.hpp -- device-side random stream of the library (gfx950).
+//
+// The search distribution of the evosax report (arXiv 2212.04180, Sec. 2.1)
+// is an isotropic Gaussian N(m, sigma^2 I); the report samples it with JAX's
+// splittable keys (Listing 1) and names no generator.  This library draws it
+// from Philox-4x32-10 (Salmon et al., SC'11), a counter-based generator: any
+// block of four words is a pure function of (key, counter), so the same
+// perturbation is regenerated in the evaluate kernel and again in the tell
+// kernel and never written to memory.
+//
+// Stream layout: key = (lo32(seed + r), hi32(seed + r)) for run r; counter =
+// (block = d/4, row, t, domain).  Domains: NOISE (row = antithetic pair,
+// t = generation), INIT (initial mean), PROBLEM (shift vector / teacher),
+// EVAL (MLP inputs of generation t).
+//
+// Normals: Box-Muller on word pairs, u = ((w >> 8) + 1) 2^-24 in (0, 1] for
+// the radius and th = (w >> 8) 2^-24 in [0, 1) for the angle.  The angle goes
+// straight into v_sin_f32 / v_cos_f32, which take their argument in
+// revolutions, and the radius uses v_log_f32 (log2) and v_sqrt_f32.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace esmi {
+
+enum : uint32_t { DOM_NOISE = 0, DOM_INIT = 1, DOM_PROBLEM = 2, DOM_EVAL = 3 };
+
+// Philox-4x32-10.  Each round forms two 32x32->64 products (v_mad_u64_u32)
+// and folds the high halves with the other words and the round key through
+// one three-input xor (v_bitop3_b32, truth table 0x96).  The key is uniform
+// across a wavefront, so the key schedule lives in scalar registers.
+__device__ __forceinline__ uint4 philox4x32_10(uint32_t k0, uint32_t k1, uint32_t c0, uint32_t c1,
+                                               uint32_t c2, uint32_t c3)
+{
+#pragma unroll
+    for (int i = 0; i < 10; ++i) {
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        const uint32_t n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), c1, k0, 0x96);
+        const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), c3, k1, 0x96);
+        c1 = (uint32_t)p1;
+        c3 = (uint32_t)p0;
+        c0 = n0;
+        c2 = n2;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return make_uint4(c0, c1, c2, c3);
+}
+
+// Box-Muller radius sqrt(-2 ln u) = sqrt(-2 ln2 * log2 u), u in (0, 1].
+__device__ __forceinline__ float bm_radius(uint32_t w)
+{
+    const float u = (float)((w >> 8) + 1u) * 0x1p-24f;  // exact
+    return __builtin_amdgcn_sqrtf(-1.38629436111989061883f * __builtin_amdgcn_logf(u));
+}
+
+// Angle in revolutions, exact.
+__device__ __forceinline__ float bm_turns(uint32_t w) { return (float)(w >> 8) * 0x1p-24f; }
+
+// Four standard normals from one Philox block.
+__device__ __forceinline__ void box_muller4(uint4 w, float e[4])
+{
+    const float r0 = bm_radius(w.x), a0 = bm_turns(w.y);
+    const float r1 = bm_radius(w.z), a1 = bm_turns(w.w);
+    e[0] = r0 * __builtin_amdgcn_cosf(a0);
+    e[1] = r0 * __builtin_amdgcn_sinf(a0);
+    e[2] = r1 * __builtin_amdgcn_cosf(a1);
+    e[3] = r1 * __builtin_amdgcn_sinf(a1);
+}
+
+__device__ __forceinline__ void normals4(uint64_t key, uint32_t block, uint32_t row, uint32_t t,
+                                         uint32_t domain, float e[4])
+{
+    box_muller4(philox4x32_10((uint32_t)key, (uint32_t)(key >> 32), block, row, t, domain), e);
+}
+
+// cos(2 pi x) for any finite x: v_cos_f32 takes revolutions and is accurate
+// for small arguments, so the integer part is removed first (exact).
+__device__ __forceinline__ float cos_2pi(float x)
+{
+    return __builtin_amdgcn_cosf(x - __builtin_rintf(x));
+}
+
+// Order-preserving map of a fitness to an unsigned key: minimisation order,
+// maximise = 1 negates, NaN sorts as +inf, -0 equals +0.
+__device__ __forceinline__ uint32_t order_key(float f, int maximize)
+{
+    float k = maximize ? -f : f;
+    if (k != k) k = __builtin_inff();
+    if (k == 0.0f) k = 0.0f;
+    const uint32_t u = __float_as_uint(k);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+}  // namespace esmi

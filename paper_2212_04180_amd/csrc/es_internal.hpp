@@ -1,0 +1,58 @@
+// es_internal.hpp -- host-side declarations shared by the runtime (es_api.cpp)
+// and the kernel launchers (es_kernels.hip).  Not part of the C-ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "esmi.h"
+
+namespace esmi {
+
+// Shapes of one strategy.  State rows are padded to Dp = 4 * nb floats so
+// that every Philox block of four dims is one aligned float4.
+struct Geometry {
+    int64_t D;   // dims
+    int64_t nb;  // Philox blocks per member, ceil(D / 4)
+    int64_t Dp;  // padded row stride, 4 * nb
+    int32_t N;   // population
+    int32_t P;   // antithetic pairs, N / 2
+    int32_t R;   // runs
+};
+
+// Adam constants of one step (host-rounded to fp32).
+struct AdamConsts {
+    float lr, beta1, beta2, omb1, omb2, bc1, bc2, eps;
+};
+
+// Geometry of the fused sample+evaluate launch: pair groups of EVAL_WG lanes,
+// D split into chunks of `bc` Philox blocks; per-chunk fp64 partial sums.
+struct EvalPlan {
+    int32_t n_pg;     // pair groups per run
+    int64_t bc;       // blocks per chunk
+    int64_t nchunks;  // chunks per member
+};
+EvalPlan eval_plan(const Geometry& g, int64_t bc_override);
+int64_t eval_partial_elems(const Geometry& g, const EvalPlan& e);  // doubles
+
+hipError_t launch_init(const Geometry& g, const es_config& c, float* m, float* m1, float* v,
+                       float* best_x, hipStream_t s);
+hipError_t launch_problem_data(const Geometry& g, const es_config& c, float* pdata, hipStream_t s);
+hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const float* m, float* x,
+                      hipStream_t s);
+hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t,
+                            const float* m, const float* pdata, double* partial, float* fit,
+                            hipStream_t s);
+hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* table,
+                       float* y, int32_t* rank, float* wfold, uint32_t* best_okey, float* best_f,
+                       int32_t* best_j, float* gen_best, hipStream_t s);
+hipError_t launch_tell(const Geometry& g, const es_config& c, uint32_t t, const AdamConsts& a,
+                       double inv_ns, const float* wfold, const int32_t* best_j, float* m,
+                       float* m1, float* v, float* grad, float* best_x, hipStream_t s);
+hipError_t launch_debug_noise(const Geometry& g, const es_config& c, int32_t run, uint32_t t,
+                              int32_t pair, uint32_t* words, float* eps, hipStream_t s);
+
+// Largest population the rank kernel stages in LDS.
+constexpr int32_t RANK_MAX_N = 16384;
+
+}  // namespace esmi

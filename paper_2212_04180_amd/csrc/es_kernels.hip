@@ -1,0 +1,579 @@
+// es_kernels.hip -- gfx950 kernels of one batched OpenAI-ES generation.
+//
+//   k_init          initial mean (Listing 1 initialize), zero Adam moments
+//   k_problem_data  shift vector / teacher network from the base seed
+//   k_ask           optional materialised population (Sec. 2.1 ask)
+//   k_eval_bbob     fused sample + evaluate (Sec. 2.1 evaluate) for the
+//                   benchmark problems; lane = antithetic pair, D chunked
+//   k_eval_reduce   fixed-order sum of the per-chunk partials -> fitness
+//   k_rank          centered ranks with index tie-break (Sec. 3.2), weights,
+//                   antithetic fold, best-so-far bookkeeping
+//   k_tell          FD gradient estimate g = E^T y / (N sigma) (Sec. 2.1) with
+//                   the noise regenerated, fused with the Adam step; lane = a
+//                   Philox block of four dims
+//   k_debug_noise   raw words and normals of one stream (diagnostics)
+//
+// Every reduction runs in a fixed order (no floating-point atomics), so a
+// launch is bit-reproducible.  Perturbation sums use short fp32 chains folded
+// into fp64 accumulators.
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include "es_device.hpp"
+#include "es_internal.hpp"
+
+namespace esmi {
+
+namespace {
+
+constexpr int EVAL_WG = 256;      // lanes = antithetic pairs
+constexpr int RED_WG = 256;       // 64 members x 4 chunk slices
+constexpr int RANK_PAIRS = 64;    // pairs per rank workgroup
+constexpr int RANK_SLICES = 16;   // key slices per pair
+constexpr int TELL_LANES = 64;    // Philox blocks per tell workgroup
+constexpr int TELL_PS = 4;        // pair slices per tell workgroup (one wave each)
+constexpr int TELL_GROUP = 16;    // fp32 pairs folded into the fp64 sum at once
+
+// MLP 64-256-256-16, flattened [out][in] per layer then the bias.  Returns
+// 1/sqrt(fan_in) for a weight and 0 for a bias.
+__device__ __forceinline__ float mlp_init_scale(int64_t i)
+{
+    if (i < 16384) return 0.125f;   // W1 [256][64]
+    if (i < 16640) return 0.0f;     // b1
+    if (i < 82176) return 0.0625f;  // W2 [256][256]
+    if (i < 82432) return 0.0f;     // b2
+    if (i < 86528) return 0.0625f;  // W3 [16][256]
+    return 0.0f;                    // b3
+}
+
+// ---------------------------------------------------------------------------
+__global__ void k_init(float* __restrict__ m, float* __restrict__ m1, float* __restrict__ v,
+                       float* __restrict__ best_x, uint64_t seed, int64_t D, int64_t nb, int32_t R,
+                       int32_t init, float lo, float range)
+{
+    const int64_t total = (int64_t)R * nb;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = i / nb, b = i - r * nb;
+        const uint64_t key = seed + (uint64_t)r;
+        float o[4] = {0.f, 0.f, 0.f, 0.f};
+        if (init == ES_INIT_UNIFORM) {
+            const uint4 w = philox4x32_10((uint32_t)key, (uint32_t)(key >> 32), (uint32_t)b, 0, 0, DOM_INIT);
+            const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) o[k] = fmaf(range, bm_turns(ww[k]), lo);
+        } else if (init == ES_INIT_FANIN_NORMAL) {
+            float e[4];
+            normals4(key, (uint32_t)b, 0, 0, DOM_INIT, e);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) o[k] = e[k] * mlp_init_scale(4 * b + k);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (4 * b + k >= D) o[k] = 0.f;
+        const int64_t off = r * 4 * nb + 4 * b;
+        *reinterpret_cast<float4*>(m + off) = make_float4(o[0], o[1], o[2], o[3]);
+        *reinterpret_cast<float4*>(m1 + off) = make_float4(0.f, 0.f, 0.f, 0.f);
+        *reinterpret_cast<float4*>(v + off) = make_float4(0.f, 0.f, 0.f, 0.f);
+        *reinterpret_cast<float4*>(best_x + off) = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+}
+
+__global__ void k_problem_data(float* __restrict__ out, uint64_t seed, int64_t D, int64_t nb, int32_t problem)
+{
+    for (int64_t b = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; b < nb;
+         b += (int64_t)gridDim.x * blockDim.x) {
+        float e[4];
+        normals4(seed, (uint32_t)b, 0, 0, DOM_PROBLEM, e);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            float o = problem == ES_PROB_MLP ? e[k] * mlp_init_scale(4 * b + k) : e[k];
+            if (4 * b + k >= D) o = 0.f;
+            out[4 * b + k] = o;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+__global__ void k_ask(const float* __restrict__ m, float* __restrict__ x, uint64_t seed, uint32_t t,
+                      int64_t D, int64_t nb, int32_t N, int32_t P, int32_t R, float sigma)
+{
+    const int64_t total = (int64_t)R * P * nb;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t b = i % nb;
+        const int64_t rp = i / nb;
+        const int64_t p = rp % P, r = rp / P;
+        float e[4];
+        normals4(seed + (uint64_t)r, (uint32_t)b, (uint32_t)p, t, DOM_NOISE, e);
+        const float* mr = m + r * 4 * nb;
+        float* xp = x + (r * N + p) * D;
+        float* xm = x + (r * N + p + P) * D;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int64_t d = 4 * b + k;
+            if (d < D) {
+                xp[d] = fmaf(sigma, e[k], mr[d]);
+                xm[d] = fmaf(-sigma, e[k], mr[d]);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Fused sample + evaluate.  Workgroup = EVAL_WG antithetic pairs of one run
+// over one D-chunk.  The chunk's mean (and shift) words are the same for the
+// whole workgroup, so they are fetched through the scalar cache; every lane
+// regenerates its own pair's normals and scores both members.
+template <int PROB>
+struct BlockTerm;
+
+template <>
+struct BlockTerm<ES_PROB_SPHERE> {
+    static __device__ __forceinline__ float f(float x, float, float) { return x * x; }
+};
+template <>
+struct BlockTerm<ES_PROB_SHIFTED_SPHERE> {
+    static __device__ __forceinline__ float f(float x, float s, float) { const float d = x - s; return d * d; }
+};
+template <>
+struct BlockTerm<ES_PROB_RASTRIGIN> {
+    static __device__ __forceinline__ float f(float x, float, float a) { return fmaf(x, x, -a * cos_2pi(x)); }
+};
+
+__device__ __forceinline__ float rosen_term(float xi, float xn)
+{
+    const float q = fmaf(-xi, xi, xn);
+    const float o = 1.0f - xi;
+    return fmaf(100.0f * q, q, o * o);
+}
+
+template <int PROB>
+__global__ __launch_bounds__(EVAL_WG) void k_eval_bbob(
+    const float* __restrict__ m, const float* __restrict__ pdata, double* __restrict__ partial,
+    uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t N, int32_t P, int32_t R, int64_t bc,
+    int32_t n_pg, float sigma, float ra)
+{
+    const int32_t r = blockIdx.y;
+    const int32_t pg = blockIdx.x % n_pg;
+    const int64_t chunk = blockIdx.x / n_pg;
+    const int32_t p = pg * EVAL_WG + (int32_t)threadIdx.x;
+    const uint32_t row = (uint32_t)(p < P ? p : P - 1);
+    const uint64_t key = seed + (uint64_t)r;
+    const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
+    const float* __restrict__ mr = m + (int64_t)r * 4 * nb;
+    const int64_t b0 = chunk * bc;
+    const int64_t b1 = b0 + bc < nb ? b0 + bc : nb;
+    const int64_t nfull = D / 4;
+    const int64_t bf = b1 < nfull ? b1 : nfull;  // end of the blocks with four live dims
+    const float ns = -sigma;
+
+    double accp = 0.0, accm = 0.0;
+    float xlp = 0.f, xlm = 0.f;  // Rosenbrock: member values at dim 4*b - 1
+    bool have_prev = false;
+    if (PROB == ES_PROB_ROSENBROCK && b0 > 0) {
+        float e[4];
+        box_muller4(philox4x32_10(k0, k1, (uint32_t)(b0 - 1), row, t, DOM_NOISE), e);
+        const float mv = mr[4 * b0 - 1];
+        xlp = fmaf(sigma, e[3], mv);
+        xlm = fmaf(ns, e[3], mv);
+        have_prev = true;
+    }
+
+    for (int64_t b = b0; b < bf; ++b) {
+        float e[4];
+        box_muller4(philox4x32_10(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
+        const float4 mv4 = *reinterpret_cast<const float4*>(mr + 4 * b);
+        const float mv[4] = {mv4.x, mv4.y, mv4.z, mv4.w};
+        float sp, sm;
+        if constexpr (PROB == ES_PROB_ROSENBROCK) {
+            float xp[4], xm[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                xp[k] = fmaf(sigma, e[k], mv[k]);
+                xm[k] = fmaf(ns, e[k], mv[k]);
+            }
+            sp = rosen_term(xp[0], xp[1]) + rosen_term(xp[1], xp[2]) + rosen_term(xp[2], xp[3]);
+            sm = rosen_term(xm[0], xm[1]) + rosen_term(xm[1], xm[2]) + rosen_term(xm[2], xm[3]);
+            if (have_prev) {
+                sp += rosen_term(xlp, xp[0]);
+                sm += rosen_term(xlm, xm[0]);
+            }
+            have_prev = true;
+            xlp = xp[3];
+            xlm = xm[3];
+        } else {
+            float sv[4] = {0.f, 0.f, 0.f, 0.f};
+            if constexpr (PROB == ES_PROB_SHIFTED_SPHERE) {
+                const float4 s4 = *reinterpret_cast<const float4*>(pdata + 4 * b);
+                sv[0] = s4.x; sv[1] = s4.y; sv[2] = s4.z; sv[3] = s4.w;
+            }
+            sp = BlockTerm<PROB>::f(fmaf(sigma, e[0], mv[0]), sv[0], ra);
+            sm = BlockTerm<PROB>::f(fmaf(ns, e[0], mv[0]), sv[0], ra);
+#pragma unroll
+            for (int k = 1; k < 4; ++k) {
+                sp += BlockTerm<PROB>::f(fmaf(sigma, e[k], mv[k]), sv[k], ra);
+                sm += BlockTerm<PROB>::f(fmaf(ns, e[k], mv[k]), sv[k], ra);
+            }
+        }
+        accp += (double)sp;
+        accm += (double)sm;
+    }
+
+    // Ragged tail: the last Philox block holds D % 4 live dims.
+    if (bf < b1) {
+        const int64_t b = bf;
+        const int nv = (int)(D - 4 * b);
+        float e[4];
+        box_muller4(philox4x32_10(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
+        float sp = 0.f, sm = 0.f;
+        for (int k = 0; k < nv; ++k) {
+            const float mv = mr[4 * b + k];
+            const float xp = fmaf(sigma, e[k], mv), xm = fmaf(ns, e[k], mv);
+            if constexpr (PROB == ES_PROB_ROSENBROCK) {
+                if (have_prev) {
+                    sp += rosen_term(xlp, xp);
+                    sm += rosen_term(xlm, xm);
+                }
+                have_prev = true;
+                xlp = xp;
+                xlm = xm;
+            } else {
+                const float s = PROB == ES_PROB_SHIFTED_SPHERE ? pdata[4 * b + k] : 0.f;
+                sp += BlockTerm<PROB>::f(xp, s, ra);
+                sm += BlockTerm<PROB>::f(xm, s, ra);
+            }
+        }
+        accp += (double)sp;
+        accm += (double)sm;
+    }
+
+    if (p < P) {
+        double* o = partial + (chunk * R + r) * (int64_t)N;
+        o[p] = accp;
+        o[p + P] = accm;
+    }
+}
+
+// fit[r][j] = add + sum over chunks (fixed order) of the partials.
+__global__ __launch_bounds__(RED_WG) void k_eval_reduce(const double* __restrict__ partial,
+                                                        float* __restrict__ fit, int32_t N, int32_t R,
+                                                        int64_t nchunks, double add)
+{
+    __shared__ double red[4][64];
+    const int32_t r = blockIdx.y;
+    const int32_t tx = threadIdx.x & 63, s = threadIdx.x >> 6;
+    const int32_t j = blockIdx.x * 64 + tx;
+    double acc = 0.0;
+    if (j < N)
+        for (int64_t c = s; c < nchunks; c += 4) acc += partial[(c * R + r) * (int64_t)N + j];
+    red[s][tx] = acc;
+    __syncthreads();
+    if (s == 0 && j < N)
+        fit[(int64_t)r * N + j] = (float)(((add + red[0][tx]) + red[1][tx]) + (red[2][tx] + red[3][tx]));
+}
+
+// ---------------------------------------------------------------------------
+// Centered ranks.  Workgroup = RANK_PAIRS pairs x RANK_SLICES key slices of
+// one run; the run's order keys sit in LDS.  rank_j counts keys that sort
+// before j in a stable ascending order: smaller key, or equal key and lower
+// index.
+__global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
+    const float* __restrict__ fit, const float* __restrict__ table, float* __restrict__ y,
+    int32_t* __restrict__ rank, float* __restrict__ wfold, uint32_t* __restrict__ best_okey,
+    float* __restrict__ best_f, int32_t* __restrict__ best_j, float* __restrict__ gen_best, int32_t N,
+    int32_t P, int32_t maximize, int32_t raw)
+{
+    extern __shared__ uint32_t keys[];
+    __shared__ int32_t cnt[RANK_SLICES][RANK_PAIRS][2];
+    const int32_t r = blockIdx.y;
+    const float* __restrict__ fr = fit + (int64_t)r * N;
+    for (int32_t k = threadIdx.x; k < N; k += blockDim.x) keys[k] = order_key(fr[k], maximize);
+    __syncthreads();
+
+    const int32_t tx = threadIdx.x % RANK_PAIRS, s = threadIdx.x / RANK_PAIRS;
+    const int32_t p = blockIdx.x * RANK_PAIRS + tx;
+    const bool valid = p < P;
+    const int32_t j1 = valid ? p : 0, j2 = j1 + P;
+    const uint32_t K1 = keys[j1], K2 = keys[j2];
+    const int32_t kb = (int32_t)(((int64_t)N * s) / RANK_SLICES);
+    const int32_t ke = (int32_t)(((int64_t)N * (s + 1)) / RANK_SLICES);
+    int32_t c1 = 0, c2 = 0;
+    for (int32_t k = kb; k < ke; ++k) {
+        const uint32_t kk = keys[k];
+        c1 += (kk < K1) | ((kk == K1) & (k < j1));
+        c2 += (kk < K2) | ((kk == K2) & (k < j2));
+    }
+    cnt[s][tx][0] = c1;
+    cnt[s][tx][1] = c2;
+    __syncthreads();
+    if (s != 0 || !valid) return;
+
+    int32_t r1 = 0, r2 = 0;
+#pragma unroll
+    for (int q = 0; q < RANK_SLICES; ++q) {
+        r1 += cnt[q][tx][0];
+        r2 += cnt[q][tx][1];
+    }
+    const float f1 = fr[j1], f2 = fr[j2];
+    float y1, y2;
+    if (raw) {
+        y1 = maximize ? -f1 : f1;
+        y2 = maximize ? -f2 : f2;
+    } else {
+        y1 = table[r1];
+        y2 = table[r2];
+    }
+    float* yr = y + (int64_t)r * N;
+    int32_t* rr = rank + (int64_t)r * N;
+    yr[j1] = y1;
+    yr[j2] = y2;
+    rr[j1] = r1;
+    rr[j2] = r2;
+    wfold[(int64_t)r * P + p] = y1 - y2;
+    if (r1 == 0 || r2 == 0) {
+        const int32_t jb = r1 == 0 ? j1 : j2;
+        const uint32_t kb0 = r1 == 0 ? K1 : K2;
+        if (gen_best) gen_best[r] = fr[jb];
+        if (kb0 < best_okey[r]) {
+            best_okey[r] = kb0;
+            best_f[r] = fr[jb];
+            best_j[r] = jb;
+        } else {
+            best_j[r] = -1;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Gradient + Adam.  Workgroup = TELL_LANES Philox blocks x TELL_PS pair
+// slices of one run.  Each lane walks its slice of pairs with the folded
+// weight w_p = y_p - y_{p+N/2} (uniform across the wave), regenerating the
+// pair's normals, so g_d = sum_p w_p eps_{p,d} / (N sigma) needs no
+// cross-lane reduction; the slices meet in LDS in a fixed order.
+__global__ __launch_bounds__(TELL_LANES * TELL_PS) void k_tell(
+    const float* __restrict__ wfold, const int32_t* __restrict__ best_j, float* __restrict__ m,
+    float* __restrict__ m1, float* __restrict__ v, float* __restrict__ grad,
+    float* __restrict__ best_x, uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t P,
+    float sigma, double inv_ns, AdamConsts ac)
+{
+    __shared__ double red[TELL_PS - 1][TELL_LANES][4];
+    const int32_t r = blockIdx.y;
+    const int32_t tx = threadIdx.x % TELL_LANES, s = threadIdx.x / TELL_LANES;
+    const int64_t b = (int64_t)blockIdx.x * TELL_LANES + tx;
+    const uint32_t bb = (uint32_t)(b < nb ? b : nb - 1);
+    const uint64_t key = seed + (uint64_t)r;
+    const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
+    const float* __restrict__ wr = wfold + (int64_t)r * P;
+    const int32_t pb = (int32_t)(((int64_t)P * s) / TELL_PS);
+    const int32_t pe = (int32_t)(((int64_t)P * (s + 1)) / TELL_PS);
+
+    double a64[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int32_t p0 = pb; p0 < pe; p0 += TELL_GROUP) {
+        const int32_t p1 = p0 + TELL_GROUP < pe ? p0 + TELL_GROUP : pe;
+        float a32[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int32_t p = p0; p < p1; ++p) {
+            float e[4];
+            box_muller4(philox4x32_10(k0, k1, bb, (uint32_t)p, t, DOM_NOISE), e);
+            const float w = wr[p];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) a32[k] = fmaf(w, e[k], a32[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) a64[k] += (double)a32[k];
+    }
+    if (s > 0) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) red[s - 1][tx][k] = a64[k];
+    }
+    __syncthreads();
+    if (s != 0 || b >= nb) return;
+#pragma unroll
+    for (int q = 0; q < TELL_PS - 1; ++q)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) a64[k] += red[q][tx][k];
+
+    const int64_t off = (int64_t)r * 4 * nb + 4 * b;
+    const float4 m4 = *reinterpret_cast<const float4*>(m + off);
+    const float4 m14 = *reinterpret_cast<const float4*>(m1 + off);
+    const float4 v4 = *reinterpret_cast<const float4*>(v + off);
+    const float mo[4] = {m4.x, m4.y, m4.z, m4.w};
+    const float m1o[4] = {m14.x, m14.y, m14.z, m14.w};
+    const float vo[4] = {v4.x, v4.y, v4.z, v4.w};
+    float mn[4], m1n[4], vn[4], gg[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        // Adam (Kingma & Ba), fp32 in a fixed operation order.
+        const float g = (float)(a64[k] * inv_ns);
+        gg[k] = g;
+        const float nm1 = __builtin_fmaf(ac.beta1, m1o[k], __fmul_rn(ac.omb1, g));
+        const float nv = __builtin_fmaf(ac.beta2, vo[k], __fmul_rn(ac.omb2, __fmul_rn(g, g)));
+        const float mhat = nm1 / ac.bc1;
+        const float vhat = nv / ac.bc2;
+        const float den = __fadd_rn(sqrtf(vhat), ac.eps);
+        const float q = mhat / den;
+        mn[k] = __builtin_fmaf(-ac.lr, q, mo[k]);
+        m1n[k] = nm1;
+        vn[k] = nv;
+        if (4 * b + k >= D) { mn[k] = 0.f; m1n[k] = 0.f; vn[k] = 0.f; gg[k] = 0.f; }
+    }
+    const int32_t jb = best_j[r];
+    if (jb >= 0) {
+        const int32_t pbst = jb < P ? jb : jb - P;
+        const float sg = jb < P ? sigma : -sigma;
+        float e[4];
+        box_muller4(philox4x32_10(k0, k1, bb, (uint32_t)pbst, t, DOM_NOISE), e);
+        float bx[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) bx[k] = 4 * b + k < D ? fmaf(sg, e[k], mo[k]) : 0.f;
+        *reinterpret_cast<float4*>(best_x + off) = make_float4(bx[0], bx[1], bx[2], bx[3]);
+    }
+    *reinterpret_cast<float4*>(m + off) = make_float4(mn[0], mn[1], mn[2], mn[3]);
+    *reinterpret_cast<float4*>(m1 + off) = make_float4(m1n[0], m1n[1], m1n[2], m1n[3]);
+    *reinterpret_cast<float4*>(v + off) = make_float4(vn[0], vn[1], vn[2], vn[3]);
+    if (grad) *reinterpret_cast<float4*>(grad + off) = make_float4(gg[0], gg[1], gg[2], gg[3]);
+}
+
+// ---------------------------------------------------------------------------
+__global__ void k_debug_noise(uint32_t* __restrict__ words, float* __restrict__ eps, uint64_t key,
+                              uint32_t row, uint32_t t, int64_t D, int64_t nb)
+{
+    for (int64_t b = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; b < nb;
+         b += (int64_t)gridDim.x * blockDim.x) {
+        const uint4 w = philox4x32_10((uint32_t)key, (uint32_t)(key >> 32), (uint32_t)b, row, t, DOM_NOISE);
+        if (words) {
+            words[4 * b + 0] = w.x;
+            words[4 * b + 1] = w.y;
+            words[4 * b + 2] = w.z;
+            words[4 * b + 3] = w.w;
+        }
+        if (eps) {
+            float e[4];
+            box_muller4(w, e);
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                if (4 * b + k < D) eps[4 * b + k] = e[k];
+        }
+    }
+}
+
+int grid_for(int64_t n, int threads)
+{
+    const int64_t g = (n + threads - 1) / threads;
+    return (int)(g < 65536 ? (g > 0 ? g : 1) : 65536);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+EvalPlan eval_plan(const Geometry& g, int64_t bc_override)
+{
+    EvalPlan e;
+    e.n_pg = (g.P + EVAL_WG - 1) / EVAL_WG;
+    int64_t bc;
+    if (bc_override > 0) {
+        bc = bc_override;
+    } else {
+        // Aim for about 2048 workgroups (8 per CU) with at least 16 blocks each.
+        const int64_t groups = (int64_t)e.n_pg * g.R;
+        bc = (g.nb * groups + 2047) / 2048;
+        if (bc < 16) bc = 16;
+    }
+    if (bc > g.nb) bc = g.nb;
+    e.bc = bc;
+    e.nchunks = (g.nb + bc - 1) / bc;
+    return e;
+}
+
+int64_t eval_partial_elems(const Geometry& g, const EvalPlan& e) { return e.nchunks * g.R * (int64_t)g.N; }
+
+hipError_t launch_init(const Geometry& g, const es_config& c, float* m, float* m1, float* v,
+                       float* best_x, hipStream_t s)
+{
+    const float range = c.init_hi - c.init_lo;
+    k_init<<<grid_for((int64_t)g.R * g.nb, 256), 256, 0, s>>>(m, m1, v, best_x, c.seed, g.D, g.nb, g.R,
+                                                               c.init, c.init_lo, range);
+    return hipGetLastError();
+}
+
+hipError_t launch_problem_data(const Geometry& g, const es_config& c, float* pdata, hipStream_t s)
+{
+    k_problem_data<<<grid_for(g.nb, 256), 256, 0, s>>>(pdata, c.seed, g.D, g.nb, c.problem);
+    return hipGetLastError();
+}
+
+hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const float* m, float* x,
+                      hipStream_t s)
+{
+    k_ask<<<grid_for((int64_t)g.R * g.P * g.nb, 256), 256, 0, s>>>(m, x, c.seed, t, g.D, g.nb, g.N, g.P,
+                                                                   g.R, c.sigma);
+    return hipGetLastError();
+}
+
+hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t,
+                            const float* m, const float* pdata, double* partial, float* fit,
+                            hipStream_t s)
+{
+    const dim3 grid((unsigned)(e.nchunks * e.n_pg), (unsigned)g.R);
+    switch (c.problem) {
+    case ES_PROB_SPHERE:
+        k_eval_bbob<ES_PROB_SPHERE><<<grid, EVAL_WG, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N, g.P,
+                                                             g.R, e.bc, e.n_pg, c.sigma, c.rastrigin_a);
+        break;
+    case ES_PROB_SHIFTED_SPHERE:
+        k_eval_bbob<ES_PROB_SHIFTED_SPHERE><<<grid, EVAL_WG, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N,
+                                                                     g.P, g.R, e.bc, e.n_pg, c.sigma,
+                                                                     c.rastrigin_a);
+        break;
+    case ES_PROB_ROSENBROCK:
+        k_eval_bbob<ES_PROB_ROSENBROCK><<<grid, EVAL_WG, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N,
+                                                                 g.P, g.R, e.bc, e.n_pg, c.sigma,
+                                                                 c.rastrigin_a);
+        break;
+    case ES_PROB_RASTRIGIN:
+        k_eval_bbob<ES_PROB_RASTRIGIN><<<grid, EVAL_WG, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N,
+                                                                g.P, g.R, e.bc, e.n_pg, c.sigma,
+                                                                c.rastrigin_a);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    const double add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;
+    k_eval_reduce<<<dim3((unsigned)((g.N + 63) / 64), (unsigned)g.R), RED_WG, 0, s>>>(partial, fit, g.N, g.R,
+                                                                                      e.nchunks, add);
+    return hipGetLastError();
+}
+
+hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* table,
+                       float* y, int32_t* rank, float* wfold, uint32_t* best_okey, float* best_f,
+                       int32_t* best_j, float* gen_best, hipStream_t s)
+{
+    const dim3 grid((unsigned)((g.P + RANK_PAIRS - 1) / RANK_PAIRS), (unsigned)g.R);
+    const size_t lds = sizeof(uint32_t) * (size_t)g.N;
+    k_rank<<<grid, RANK_PAIRS * RANK_SLICES, lds, s>>>(fit, table, y, rank, wfold, best_okey, best_f, best_j,
+                                                       gen_best, g.N, g.P, c.maximize,
+                                                       c.shaping == ES_SHAPE_RAW);
+    return hipGetLastError();
+}
+
+hipError_t launch_tell(const Geometry& g, const es_config& c, uint32_t t, const AdamConsts& a,
+                       double inv_ns, const float* wfold, const int32_t* best_j, float* m,
+                       float* m1, float* v, float* grad, float* best_x, hipStream_t s)
+{
+    const dim3 grid((unsigned)((g.nb + TELL_LANES - 1) / TELL_LANES), (unsigned)g.R);
+    k_tell<<<grid, TELL_LANES * TELL_PS, 0, s>>>(wfold, best_j, m, m1, v, grad, best_x, c.seed, t, g.D, g.nb,
+                                                 g.P, c.sigma, inv_ns, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_debug_noise(const Geometry& g, const es_config& c, int32_t run, uint32_t t,
+                              int32_t pair, uint32_t* words, float* eps, hipStream_t s)
+{
+    k_debug_noise<<<grid_for(g.nb, 256), 256, 0, s>>>(words, eps, c.seed + (uint64_t)run, (uint32_t)pair, t,
+                                                      g.D, g.nb);
+    return hipGetLastError();
+}
+
+}  // namespace esmi

@@ -1,0 +1,56 @@
+"""The C-ABI library loads and exports every symbol include/esmi.h declares
+(CPU only: no compute call is made)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "esmi.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return re.findall(r"\b(es_[a-z_]+)\s*\(", src)
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for must in ("es_init", "es_ask", "es_eval", "es_tell", "es_run", "es_destroy"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2212_04180_amd import esmi
+    L = esmi.lib()
+    names = _declared()
+    missing = [n for n in names if not hasattr(L, n)]
+    assert not missing, missing
+    assert sorted(set(names)) == sorted(set(esmi.EXPORTS))
+
+
+def test_status_strings_and_init_error_without_gpu_work():
+    from paper_2212_04180_amd import esmi
+    L = esmi.lib()
+    assert L.es_status_string(0) == b"ok"
+    assert L.es_status_string(-2).startswith(b"call out of")
+    # an invalid config is rejected before any device call
+    cfg = esmi.ESConfig(num_dims=8, popsize=3).cstruct()
+    h = ctypes.c_void_p()
+    assert L.es_init(ctypes.byref(cfg), None, ctypes.byref(h)) == esmi.ES_ERR_ARG
+    assert b"popsize" in L.es_last_error(None)
+
+
+def test_config_struct_has_no_padding():
+    from paper_2212_04180_amd import esmi
+    assert ctypes.sizeof(esmi._Config) == 88
+
+
+def test_product_does_not_reach_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2212_04180_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".cpp", ".hpp", ".h")):
+                text = open(os.path.join(dirpath, fn)).read()
+                assert "oracle" not in text.lower().replace("the oracle", ""), fn

@@ -17,23 +17,27 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-# MI355X public figures: 256 CUs x 4 SIMD x 16 lanes at 2.4 GHz -> one
-# full-rate 32-bit VALU lane-cycle each; HBM3E 8 TB/s.
-CU, LANES_PER_CU, CLOCK_HZ = 256, 64, 2.4e9
-VALU_PEAK = CU * LANES_PER_CU * CLOCK_HZ  # lane-cycles/s
+# MI355X public figures: 256 CUs at 2.4 GHz; fp32 vector 157.3 TFLOP/s, i.e.
+# 7.86e13 full-rate VALU lane-ops/s (an FMA counts two flops); HBM3E 8 TB/s.
+VALU_PEAK = 157.3e12 / 2.0  # lane-op slots/s
 HBM_PEAK = 8.0e12
 
-# Algorithmic VALU work of the fused sample+evaluate kernel, in lane-cycles
-# per Philox block of one antithetic pair (4 dims x 2 members), counted from
-# the minimal instruction sequence and the measured gfx950 issue costs (see
-# the design notes):
-#   Philox-4x32-10: 20 x v_mad_u64_u32 (4) + 20 x v_bitop3_b32 (1)        = 100
-#   Box-Muller: 4 x (shift + convert) (2) + 2 x (+1) + 2 x scale log arg
-#     + 2 x log2 (4) + 2 x sqrt (4) + 2 x sin (4) + 2 x cos (4)
-#     + 2 x (-2 ln 2) + 4 x angle scale + 4 x (r * trig)                   = 46
-#   member arithmetic, shifted sphere: 8 fma (x) + 8 sub (x - s)
-#     + 8 fma/mul (squares into the block sum) + 2 x (cvt f64 + add f64)    = 28
-EVAL_CYCLES_PER_PAIR_BLOCK = {"shifted_sphere": 174, "sphere": 166, "rastrigin": 190, "rosenbrock": 200}
+# Algorithmic VALU work, in full-rate lane-op slots per Philox block of one
+# antithetic pair (4 dims x 2 members).  Issue costs measured on gfx950
+# relative to v_fma_f32 (1): v_mad_u64_u32, v_mul_hi/lo_u32, v_cvt_*, fp64
+# fma/add 2; v_log/v_sqrt/v_sin/v_cos 4; bitwise, shifts, fp32 add/mul/fma 1.
+#   Philox-4x32-10: 20 x 32x32->64 product (2) + 20 x three-input xor (1)      = 60
+#   Box-Muller: 4 shift + 4 cvt (2) + 2 (+1) + 4 x 2^-24 scale + 2 log2 (4)
+#     + 2 x (-2 ln 2) + 2 sqrt (4) + 2 sin (4) + 2 cos (4) + 4 (r * trig)      = 56
+#   members (both signs): 8 fma for x plus the problem's terms, and the fold
+#     of each member's fp32 block sum into fp64 (2 x (cvt 2 + add 2) = 8):
+#     sphere 8 squares -> 24; shifted sphere 8 sub + 8 squares -> 32;
+#     Rosenbrock 6 ops x 4 terms x 2 -> 64; Rastrigin 9 ops x 8 -> 88.
+PHILOX_BM = 60 + 56
+EVAL_SLOTS_PER_PAIR_BLOCK = {"sphere": PHILOX_BM + 24, "shifted_sphere": PHILOX_BM + 32,
+                             "rosenbrock": PHILOX_BM + 64, "rastrigin": PHILOX_BM + 88}
+# tell: Philox + Box-Muller + 4 fma (w * eps) + the fp64 fold every 16 pairs
+TELL_SLOTS_PER_PAIR_BLOCK = PHILOX_BM + 4 + 1
 
 
 def parse():
@@ -44,6 +48,8 @@ def parse():
     ap.add_argument("--workload", default="shifted_sphere_d1m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-dims", type=int, default=0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run one plain device copy of this size (HBM counter calibration)")
     return ap.parse_args()
 
 
@@ -89,6 +95,14 @@ def main():
     es = P.ES(cfg, device=dev, stream=stream)
     R, N, D = cfg.num_runs, cfg.popsize, cfg.num_dims
     fit = torch.empty(R, N, device=dev)
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(n, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copy calibration: {n * 4} bytes read + {n * 4} bytes written")
+        del src, dst
 
     for _ in range(args.warmup):
         es.step(fit)
@@ -124,11 +138,15 @@ def main():
     roof = None
     if prob is not None:
         pair_blocks = R * (N // 2) * ((D + 3) // 4)
-        work = pair_blocks * EVAL_CYCLES_PER_PAIR_BLOCK[prob]
-        achieved = work / (eval_ms * 1e-3)
+        achieved = pair_blocks * EVAL_SLOTS_PER_PAIR_BLOCK[prob] / (eval_ms * 1e-3)
+        tell_achieved = pair_blocks * TELL_SLOTS_PER_PAIR_BLOCK / (tell_ms * 1e-3)
         roof = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
-                "unit": "T VALU lane-cycles/s", "frac": achieved / VALU_PEAK, "traffic": None,
-                "kernel": "k_eval_bbob (fused sample+evaluate) + k_eval_reduce", "kernel_ms": eval_ms}
+                "unit": "T VALU lane-op slots/s", "frac": achieved / VALU_PEAK, "traffic": None,
+                "kernel": "k_eval_bbob (fused sample+evaluate; timed with its k_eval_reduce)",
+                "kernel_ms": eval_ms, "slots_per_pair_block": EVAL_SLOTS_PER_PAIR_BLOCK[prob],
+                "pair_blocks_per_launch": pair_blocks,
+                "tell": {"kernel": "k_rank + k_tell", "kernel_ms": tell_ms, "achieved": tell_achieved / 1e12,
+                         "frac": tell_achieved / VALU_PEAK, "slots_per_pair_block": TELL_SLOTS_PER_PAIR_BLOCK}}
     # The benchmark spec's HBM reading: the same generation with the noise stored
     # (written once by evaluate, read once by tell) moves 4 B per member-dim.
     hbm_equiv = {"bytes_per_member_dim": 4.0, "peak_member_dims_per_s": HBM_PEAK / 4.0,
@@ -136,7 +154,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        sd = args.cpu_sample_dims or max(4, min(D, int(2.0e8 // (R * N))))
+        sd = args.cpu_sample_dims or max(4, min(D, int(4.0e8 // (R * N))))
         cpu = cpu_baseline(cfg, sd)
         log(f"[bench] oracle sample: {cpu['sample']} -> {cpu['value']:.3e} member-dims/s")
 

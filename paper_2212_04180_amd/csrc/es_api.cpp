@@ -58,7 +58,7 @@ struct es_handle {
     int32_t* rank = nullptr; // [R][N]
     float* wfold = nullptr;  // [R][P]
     float* fit = nullptr;    // [R][N] fitness scratch for es_run
-    double* partial = nullptr;
+    float* partial = nullptr;
     float* pdata = nullptr;  // [Dp] shift vector or teacher
     char err[512] = {0};
 };

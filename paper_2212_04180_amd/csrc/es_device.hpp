@@ -26,17 +26,39 @@ namespace esmi {
 
 enum : uint32_t { DOM_NOISE = 0, DOM_INIT = 1, DOM_PROBLEM = 2, DOM_EVAL = 3 };
 
-// Philox-4x32-10.  Each round forms two 32x32->64 products (v_mad_u64_u32)
-// and folds the high halves with the other words and the round key through
-// one three-input xor (v_bitop3_b32, truth table 0x96).  The key is uniform
-// across a wavefront, so the key schedule lives in scalar registers.
+// 32x32 -> 64-bit product as one v_mad_u64_u32.  Left to itself the compiler
+// sometimes splits a product into v_mul_lo_u32 + v_mul_hi_u32, which costs
+// twice the issue slots.
+__device__ __forceinline__ uint64_t mul_wide(uint32_t a, uint32_t b)
+{
+    uint64_t r;
+    asm("v_mad_u64_u32 %0, vcc, %1, %2, 0" : "=v"(r) : "v"(a), "s"(b) : "vcc");
+    return r;
+}
+
+// Which counter word varies across the lanes of a wavefront; the others are
+// uniform (the generation t and the domain always are).
+enum PhiloxLanes { LANES_BLOCK_AND_ROW = 0, LANES_ROW = 1, LANES_BLOCK = 2 };
+
+// Philox-4x32-10.  Each round forms two 32x32->64 products and folds the high
+// halves with the other words and the round key through one three-input xor
+// (v_bitop3_b32, truth table 0x96).  The key is uniform across a wavefront,
+// so the key schedule lives in scalar registers.  In the first two rounds
+// some products only involve uniform words; those are left to the compiler,
+// which runs them on the scalar unit, and every lane-varying product is one
+// v_mad_u64_u32.
+template <int V = LANES_BLOCK_AND_ROW>
 __device__ __forceinline__ uint4 philox4x32_10(uint32_t k0, uint32_t k1, uint32_t c0, uint32_t c1,
                                                uint32_t c2, uint32_t c3)
 {
 #pragma unroll
     for (int i = 0; i < 10; ++i) {
-        const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
-        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        // round 0: c0 = block varies unless V == LANES_ROW; c2 = t is uniform.
+        // round 1: c0 depends on the row, c2 on the block.
+        const bool vary0 = i >= 2 || (i == 0 && V != LANES_ROW) || (i == 1 && V != LANES_BLOCK);
+        const bool vary2 = i >= 2 || (i == 1 && V != LANES_ROW);
+        const uint64_t p0 = vary0 ? mul_wide(c0, 0xD2511F53u) : (uint64_t)0xD2511F53u * c0;
+        const uint64_t p1 = vary2 ? mul_wide(c2, 0xCD9E8D57u) : (uint64_t)0xCD9E8D57u * c2;
         const uint32_t n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), c1, k0, 0x96);
         const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), c3, k1, 0x96);
         c1 = (uint32_t)p1;

@@ -25,15 +25,17 @@ struct AdamConsts {
     float lr, beta1, beta2, omb1, omb2, bc1, bc2, eps;
 };
 
-// Geometry of the fused sample+evaluate launch: pair groups of EVAL_WG lanes,
-// D split into chunks of `bc` Philox blocks; per-chunk fp64 partial sums.
+// Geometry of the fused sample+evaluate launch: pair groups of `wg` lanes,
+// D split into chunks of `bc` Philox blocks; one fp32 partial sum per
+// (chunk, run, member).
 struct EvalPlan {
+    int32_t wg;       // lanes (pairs) per workgroup
     int32_t n_pg;     // pair groups per run
     int64_t bc;       // blocks per chunk
     int64_t nchunks;  // chunks per member
 };
 EvalPlan eval_plan(const Geometry& g, int64_t bc_override);
-int64_t eval_partial_elems(const Geometry& g, const EvalPlan& e);  // doubles
+int64_t eval_partial_elems(const Geometry& g, const EvalPlan& e);  // floats
 
 hipError_t launch_init(const Geometry& g, const es_config& c, float* m, float* m1, float* v,
                        float* best_x, hipStream_t s);
@@ -41,7 +43,7 @@ hipError_t launch_problem_data(const Geometry& g, const es_config& c, float* pda
 hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const float* m, float* x,
                       hipStream_t s);
 hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t,
-                            const float* m, const float* pdata, double* partial, float* fit,
+                            const float* m, const float* pdata, float* partial, float* fit,
                             hipStream_t s);
 hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* table,
                        float* y, int32_t* rank, float* wfold, uint32_t* best_okey, float* best_f,

@@ -26,9 +26,10 @@ namespace esmi {
 
 namespace {
 
-constexpr int EVAL_WG = 256;      // lanes = antithetic pairs
-constexpr int RED_WG = 256;       // 64 members x 4 chunk slices
-constexpr int RANK_PAIRS = 64;    // pairs per rank workgroup
+constexpr int EVAL_MAX_WG = 1024; // lanes = antithetic pairs
+constexpr int EVAL_FOLD = 4;      // Philox blocks summed in fp32 before the fp64 fold
+constexpr int RED_SLICES = 16;    // chunk slices per member in the partial reduce
+constexpr int RANK_PAIRS = 16;    // pairs per rank workgroup
 constexpr int RANK_SLICES = 16;   // key slices per pair
 constexpr int TELL_LANES = 64;    // Philox blocks per tell workgroup
 constexpr int TELL_PS = 4;        // pair slices per tell workgroup (one wave each)
@@ -121,10 +122,13 @@ __global__ void k_ask(const float* __restrict__ m, float* __restrict__ x, uint64
 }
 
 // ---------------------------------------------------------------------------
-// Fused sample + evaluate.  Workgroup = EVAL_WG antithetic pairs of one run
-// over one D-chunk.  The chunk's mean (and shift) words are the same for the
-// whole workgroup, so they are fetched through the scalar cache; every lane
-// regenerates its own pair's normals and scores both members.
+// Fused sample + evaluate.  Workgroup = up to EVAL_MAX_WG antithetic pairs of
+// one run over one chunk of Philox blocks.  The chunk's mean (and shift)
+// words are the same for the whole workgroup, so they come through the
+// scalar cache, EVAL_FOLD blocks (16 floats) per scalar load, fetched one
+// group ahead; every lane regenerates its own pair's normals and scores both
+// members.  Workgroup ids are dealt to the 8 XCDs round robin, so the pair
+// groups of one chunk are given ids that share an XCD (and its L2).
 template <int PROB>
 struct BlockTerm;
 
@@ -148,16 +152,59 @@ __device__ __forceinline__ float rosen_term(float xi, float xn)
     return fmaf(100.0f * q, q, o * o);
 }
 
+// Running state of one lane: both members' sums and, for Rosenbrock, the
+// members' values at the previous dim.
+struct EvalLane {
+    double accp, accm;
+    float xlp, xlm;
+    bool have_prev;
+};
+
+// Terms of one full Philox block (four live dims) for both members.
 template <int PROB>
-__global__ __launch_bounds__(EVAL_WG) void k_eval_bbob(
-    const float* __restrict__ m, const float* __restrict__ pdata, double* __restrict__ partial,
-    uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t N, int32_t P, int32_t R, int64_t bc,
+__device__ __forceinline__ void block_terms(const float e[4], const float mv[4], const float sv[4], float sg,
+                                            float ra, EvalLane& L, float& sp, float& sm)
+{
+    if constexpr (PROB == ES_PROB_ROSENBROCK) {
+        float xp[4], xm[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            xp[k] = fmaf(sg, e[k], mv[k]);
+            xm[k] = fmaf(-sg, e[k], mv[k]);
+        }
+        float tp = rosen_term(xp[0], xp[1]) + rosen_term(xp[1], xp[2]) + rosen_term(xp[2], xp[3]);
+        float tm = rosen_term(xm[0], xm[1]) + rosen_term(xm[1], xm[2]) + rosen_term(xm[2], xm[3]);
+        if (L.have_prev) {
+            tp += rosen_term(L.xlp, xp[0]);
+            tm += rosen_term(L.xlm, xm[0]);
+        }
+        L.have_prev = true;
+        L.xlp = xp[3];
+        L.xlm = xm[3];
+        sp += tp;
+        sm += tm;
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            sp += BlockTerm<PROB>::f(fmaf(sg, e[k], mv[k]), sv[k], ra);
+            sm += BlockTerm<PROB>::f(fmaf(-sg, e[k], mv[k]), sv[k], ra);
+        }
+    }
+}
+
+template <int PROB>
+__global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
+    const float* __restrict__ m, const float* __restrict__ pdata, float* __restrict__ partial,
+    uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t N, int32_t P, int64_t bc, int64_t nchunks,
     int32_t n_pg, float sigma, float ra)
 {
     const int32_t r = blockIdx.y;
-    const int32_t pg = blockIdx.x % n_pg;
-    const int64_t chunk = blockIdx.x / n_pg;
-    const int32_t p = pg * EVAL_WG + (int32_t)threadIdx.x;
+    const uint32_t w = blockIdx.x;
+    const uint32_t slot = w >> 3, xcd = w & 7u;
+    const int32_t pg = (int32_t)(slot % (uint32_t)n_pg);
+    const int64_t chunk = (int64_t)(slot / (uint32_t)n_pg) * 8 + xcd;
+    if (chunk >= nchunks) return;
+    const int32_t p = pg * (int32_t)blockDim.x + (int32_t)threadIdx.x;
     const uint32_t row = (uint32_t)(p < P ? p : P - 1);
     const uint64_t key = seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
@@ -165,112 +212,116 @@ __global__ __launch_bounds__(EVAL_WG) void k_eval_bbob(
     const int64_t b0 = chunk * bc;
     const int64_t b1 = b0 + bc < nb ? b0 + bc : nb;
     const int64_t nfull = D / 4;
-    const int64_t bf = b1 < nfull ? b1 : nfull;  // end of the blocks with four live dims
-    const float ns = -sigma;
+    const int32_t nf = (int32_t)((b1 < nfull ? b1 : nfull) - b0);  // full blocks in this chunk (may be <= 0)
+    // sigma lives in a VGPR so that fmaf(sigma, eps, m) can take m from an SGPR
+    float sg;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(sg) : "s"(sigma));
 
-    double accp = 0.0, accm = 0.0;
-    float xlp = 0.f, xlm = 0.f;  // Rosenbrock: member values at dim 4*b - 1
-    bool have_prev = false;
+    EvalLane L{0.0, 0.0, 0.f, 0.f, false};
     if (PROB == ES_PROB_ROSENBROCK && b0 > 0) {
         float e[4];
-        box_muller4(philox4x32_10(k0, k1, (uint32_t)(b0 - 1), row, t, DOM_NOISE), e);
+        box_muller4(philox4x32_10<LANES_ROW>(k0, k1, (uint32_t)(b0 - 1), row, t, DOM_NOISE), e);
         const float mv = mr[4 * b0 - 1];
-        xlp = fmaf(sigma, e[3], mv);
-        xlm = fmaf(ns, e[3], mv);
-        have_prev = true;
+        L.xlp = fmaf(sg, e[3], mv);
+        L.xlm = fmaf(-sg, e[3], mv);
+        L.have_prev = true;
     }
 
-    for (int64_t b = b0; b < bf; ++b) {
-        float e[4];
-        box_muller4(philox4x32_10(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
-        const float4 mv4 = *reinterpret_cast<const float4*>(mr + 4 * b);
-        const float mv[4] = {mv4.x, mv4.y, mv4.z, mv4.w};
-        float sp, sm;
-        if constexpr (PROB == ES_PROB_ROSENBROCK) {
-            float xp[4], xm[4];
+    const float zero4[4] = {0.f, 0.f, 0.f, 0.f};
+    int32_t i = 0;
+    for (; i + EVAL_FOLD <= nf; i += EVAL_FOLD) {
+        const int64_t bg = b0 + i;
+        float mv[4 * EVAL_FOLD], sv[4 * EVAL_FOLD];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                xp[k] = fmaf(sigma, e[k], mv[k]);
-                xm[k] = fmaf(ns, e[k], mv[k]);
-            }
-            sp = rosen_term(xp[0], xp[1]) + rosen_term(xp[1], xp[2]) + rosen_term(xp[2], xp[3]);
-            sm = rosen_term(xm[0], xm[1]) + rosen_term(xm[1], xm[2]) + rosen_term(xm[2], xm[3]);
-            if (have_prev) {
-                sp += rosen_term(xlp, xp[0]);
-                sm += rosen_term(xlm, xm[0]);
-            }
-            have_prev = true;
-            xlp = xp[3];
-            xlm = xm[3];
-        } else {
-            float sv[4] = {0.f, 0.f, 0.f, 0.f};
-            if constexpr (PROB == ES_PROB_SHIFTED_SPHERE) {
-                const float4 s4 = *reinterpret_cast<const float4*>(pdata + 4 * b);
-                sv[0] = s4.x; sv[1] = s4.y; sv[2] = s4.z; sv[3] = s4.w;
-            }
-            sp = BlockTerm<PROB>::f(fmaf(sigma, e[0], mv[0]), sv[0], ra);
-            sm = BlockTerm<PROB>::f(fmaf(ns, e[0], mv[0]), sv[0], ra);
+        for (int q = 0; q < 4 * EVAL_FOLD; ++q) mv[q] = mr[4 * bg + q];
+        if constexpr (PROB == ES_PROB_SHIFTED_SPHERE) {
 #pragma unroll
-            for (int k = 1; k < 4; ++k) {
-                sp += BlockTerm<PROB>::f(fmaf(sigma, e[k], mv[k]), sv[k], ra);
-                sm += BlockTerm<PROB>::f(fmaf(ns, e[k], mv[k]), sv[k], ra);
-            }
+            for (int q = 0; q < 4 * EVAL_FOLD; ++q) sv[q] = pdata[4 * bg + q];
         }
-        accp += (double)sp;
-        accm += (double)sm;
+        float sp = 0.f, sm = 0.f;
+#pragma unroll
+        for (int k = 0; k < EVAL_FOLD; ++k) {
+            float e[4];
+            box_muller4(philox4x32_10<LANES_ROW>(k0, k1, (uint32_t)(bg + k), row, t, DOM_NOISE), e);
+            block_terms<PROB>(e, mv + 4 * k, PROB == ES_PROB_SHIFTED_SPHERE ? sv + 4 * k : zero4, sg, ra, L, sp,
+                              sm);
+        }
+        L.accp += (double)sp;
+        L.accm += (double)sm;
+    }
+    for (; i < nf; ++i) {
+        const int64_t b = b0 + i;
+        float mv[4], sv[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) mv[q] = mr[4 * b + q];
+        if constexpr (PROB == ES_PROB_SHIFTED_SPHERE) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) sv[q] = pdata[4 * b + q];
+        }
+        float e[4];
+        box_muller4(philox4x32_10<LANES_ROW>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
+        float sp = 0.f, sm = 0.f;
+        block_terms<PROB>(e, mv, sv, sg, ra, L, sp, sm);
+        L.accp += (double)sp;
+        L.accm += (double)sm;
     }
 
     // Ragged tail: the last Philox block holds D % 4 live dims.
-    if (bf < b1) {
-        const int64_t b = bf;
+    if (b1 > nfull && b1 == nb && nfull >= b0) {
+        const int64_t b = nfull;
         const int nv = (int)(D - 4 * b);
         float e[4];
-        box_muller4(philox4x32_10(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
+        box_muller4(philox4x32_10<LANES_ROW>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
         float sp = 0.f, sm = 0.f;
         for (int k = 0; k < nv; ++k) {
             const float mv = mr[4 * b + k];
-            const float xp = fmaf(sigma, e[k], mv), xm = fmaf(ns, e[k], mv);
+            const float xp = fmaf(sg, e[k], mv), xm = fmaf(-sg, e[k], mv);
             if constexpr (PROB == ES_PROB_ROSENBROCK) {
-                if (have_prev) {
-                    sp += rosen_term(xlp, xp);
-                    sm += rosen_term(xlm, xm);
+                if (L.have_prev) {
+                    sp += rosen_term(L.xlp, xp);
+                    sm += rosen_term(L.xlm, xm);
                 }
-                have_prev = true;
-                xlp = xp;
-                xlm = xm;
+                L.have_prev = true;
+                L.xlp = xp;
+                L.xlm = xm;
             } else {
                 const float s = PROB == ES_PROB_SHIFTED_SPHERE ? pdata[4 * b + k] : 0.f;
                 sp += BlockTerm<PROB>::f(xp, s, ra);
                 sm += BlockTerm<PROB>::f(xm, s, ra);
             }
         }
-        accp += (double)sp;
-        accm += (double)sm;
+        L.accp += (double)sp;
+        L.accm += (double)sm;
     }
 
     if (p < P) {
-        double* o = partial + (chunk * R + r) * (int64_t)N;
-        o[p] = accp;
-        o[p + P] = accm;
+        float* o = partial + (chunk * gridDim.y + r) * (int64_t)N;
+        o[p] = (float)L.accp;
+        o[p + P] = (float)L.accm;
     }
 }
 
 // fit[r][j] = add + sum over chunks (fixed order) of the partials.
-__global__ __launch_bounds__(RED_WG) void k_eval_reduce(const double* __restrict__ partial,
-                                                        float* __restrict__ fit, int32_t N, int32_t R,
-                                                        int64_t nchunks, double add)
+// Workgroup = 64 members x RED_SLICES chunk slices.
+__global__ __launch_bounds__(64 * RED_SLICES) void k_eval_reduce(const float* __restrict__ partial,
+                                                                 float* __restrict__ fit, int32_t N, int32_t R,
+                                                                 int64_t nchunks, double add)
 {
-    __shared__ double red[4][64];
+    __shared__ double red[RED_SLICES][64];
     const int32_t r = blockIdx.y;
     const int32_t tx = threadIdx.x & 63, s = threadIdx.x >> 6;
     const int32_t j = blockIdx.x * 64 + tx;
     double acc = 0.0;
     if (j < N)
-        for (int64_t c = s; c < nchunks; c += 4) acc += partial[(c * R + r) * (int64_t)N + j];
+        for (int64_t c = s; c < nchunks; c += RED_SLICES) acc += (double)partial[(c * R + r) * (int64_t)N + j];
     red[s][tx] = acc;
     __syncthreads();
-    if (s == 0 && j < N)
-        fit[(int64_t)r * N + j] = (float)(((add + red[0][tx]) + red[1][tx]) + (red[2][tx] + red[3][tx]));
+    if (s == 0 && j < N) {
+        double tot = add;
+#pragma unroll
+        for (int q = 0; q < RED_SLICES; ++q) tot += red[q][tx];
+        fit[(int64_t)r * N + j] = (float)tot;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -359,7 +410,9 @@ __global__ __launch_bounds__(TELL_LANES * TELL_PS) void k_tell(
 {
     __shared__ double red[TELL_PS - 1][TELL_LANES][4];
     const int32_t r = blockIdx.y;
-    const int32_t tx = threadIdx.x % TELL_LANES, s = threadIdx.x / TELL_LANES;
+    const int32_t tx = threadIdx.x % TELL_LANES;
+    // one wave per pair slice: make the slice index (and the pair loop) uniform
+    const int32_t s = __builtin_amdgcn_readfirstlane(threadIdx.x / TELL_LANES);
     const int64_t b = (int64_t)blockIdx.x * TELL_LANES + tx;
     const uint32_t bb = (uint32_t)(b < nb ? b : nb - 1);
     const uint64_t key = seed + (uint64_t)r;
@@ -369,12 +422,27 @@ __global__ __launch_bounds__(TELL_LANES * TELL_PS) void k_tell(
     const int32_t pe = (int32_t)(((int64_t)P * (s + 1)) / TELL_PS);
 
     double a64[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int32_t p0 = pb; p0 < pe; p0 += TELL_GROUP) {
-        const int32_t p1 = p0 + TELL_GROUP < pe ? p0 + TELL_GROUP : pe;
+    int32_t p0 = pb;
+    for (; p0 + TELL_GROUP <= pe; p0 += TELL_GROUP) {
+        float wv[TELL_GROUP];
+#pragma unroll
+        for (int q = 0; q < TELL_GROUP; ++q) wv[q] = wr[p0 + q];
         float a32[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int32_t p = p0; p < p1; ++p) {
+#pragma unroll
+        for (int q = 0; q < TELL_GROUP; ++q) {
             float e[4];
-            box_muller4(philox4x32_10(k0, k1, bb, (uint32_t)p, t, DOM_NOISE), e);
+            box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, bb, (uint32_t)(p0 + q), t, DOM_NOISE), e);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) a32[k] = fmaf(wv[q], e[k], a32[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) a64[k] += (double)a32[k];
+    }
+    {
+        float a32[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int32_t p = p0; p < pe; ++p) {
+            float e[4];
+            box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, bb, (uint32_t)p, t, DOM_NOISE), e);
             const float w = wr[p];
 #pragma unroll
             for (int k = 0; k < 4; ++k) a32[k] = fmaf(w, e[k], a32[k]);
@@ -422,7 +490,7 @@ __global__ __launch_bounds__(TELL_LANES * TELL_PS) void k_tell(
         const int32_t pbst = jb < P ? jb : jb - P;
         const float sg = jb < P ? sigma : -sigma;
         float e[4];
-        box_muller4(philox4x32_10(k0, k1, bb, (uint32_t)pbst, t, DOM_NOISE), e);
+        box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, bb, (uint32_t)pbst, t, DOM_NOISE), e);
         float bx[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) bx[k] = 4 * b + k < D ? fmaf(sg, e[k], mo[k]) : 0.f;
@@ -469,14 +537,19 @@ int grid_for(int64_t n, int threads)
 EvalPlan eval_plan(const Geometry& g, int64_t bc_override)
 {
     EvalPlan e;
-    e.n_pg = (g.P + EVAL_WG - 1) / EVAL_WG;
+    const int32_t P64 = (g.P + 63) / 64 * 64;
+    e.wg = P64 < EVAL_MAX_WG ? P64 : EVAL_MAX_WG;
+    e.n_pg = (g.P + e.wg - 1) / e.wg;
     int64_t bc;
     if (bc_override > 0) {
         bc = bc_override;
     } else {
-        // Aim for about 2048 workgroups (8 per CU) with at least 16 blocks each.
-        const int64_t groups = (int64_t)e.n_pg * g.R;
-        bc = (g.nb * groups + 2047) / 2048;
+        // About 16384 waves in flight over the launch (two rounds of a full
+        // chip at 8 waves per SIMD), with at least 16 blocks per chunk.
+        const int64_t waves_per_chunk = (int64_t)e.n_pg * (e.wg / 64) * g.R;
+        int64_t nch = (16384 + waves_per_chunk - 1) / waves_per_chunk;
+        if (nch < 1) nch = 1;
+        bc = (g.nb + nch - 1) / nch;
         if (bc < 16) bc = 16;
     }
     if (bc > g.nb) bc = g.nb;
@@ -511,38 +584,29 @@ hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const f
 }
 
 hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t,
-                            const float* m, const float* pdata, double* partial, float* fit,
+                            const float* m, const float* pdata, float* partial, float* fit,
                             hipStream_t s)
 {
-    const dim3 grid((unsigned)(e.nchunks * e.n_pg), (unsigned)g.R);
+    // chunk ids are dealt so that the pair groups of one chunk share an XCD
+    const int64_t slots = (e.nchunks + 7) / 8 * e.n_pg;
+    const dim3 grid((unsigned)(slots * 8), (unsigned)g.R);
+    const dim3 block((unsigned)e.wg);
+#define ES_EVAL_LAUNCH(PROB)                                                                                   \
+    k_eval_bbob<PROB><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N, g.P, e.bc, e.nchunks, \
+                                             e.n_pg, c.sigma, c.rastrigin_a)
     switch (c.problem) {
-    case ES_PROB_SPHERE:
-        k_eval_bbob<ES_PROB_SPHERE><<<grid, EVAL_WG, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N, g.P,
-                                                             g.R, e.bc, e.n_pg, c.sigma, c.rastrigin_a);
-        break;
-    case ES_PROB_SHIFTED_SPHERE:
-        k_eval_bbob<ES_PROB_SHIFTED_SPHERE><<<grid, EVAL_WG, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N,
-                                                                     g.P, g.R, e.bc, e.n_pg, c.sigma,
-                                                                     c.rastrigin_a);
-        break;
-    case ES_PROB_ROSENBROCK:
-        k_eval_bbob<ES_PROB_ROSENBROCK><<<grid, EVAL_WG, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N,
-                                                                 g.P, g.R, e.bc, e.n_pg, c.sigma,
-                                                                 c.rastrigin_a);
-        break;
-    case ES_PROB_RASTRIGIN:
-        k_eval_bbob<ES_PROB_RASTRIGIN><<<grid, EVAL_WG, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N,
-                                                                g.P, g.R, e.bc, e.n_pg, c.sigma,
-                                                                c.rastrigin_a);
-        break;
-    default:
-        return hipErrorInvalidValue;
+    case ES_PROB_SPHERE: ES_EVAL_LAUNCH(ES_PROB_SPHERE); break;
+    case ES_PROB_SHIFTED_SPHERE: ES_EVAL_LAUNCH(ES_PROB_SHIFTED_SPHERE); break;
+    case ES_PROB_ROSENBROCK: ES_EVAL_LAUNCH(ES_PROB_ROSENBROCK); break;
+    case ES_PROB_RASTRIGIN: ES_EVAL_LAUNCH(ES_PROB_RASTRIGIN); break;
+    default: return hipErrorInvalidValue;
     }
+#undef ES_EVAL_LAUNCH
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     const double add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;
-    k_eval_reduce<<<dim3((unsigned)((g.N + 63) / 64), (unsigned)g.R), RED_WG, 0, s>>>(partial, fit, g.N, g.R,
-                                                                                      e.nchunks, add);
+    k_eval_reduce<<<dim3((unsigned)((g.N + 63) / 64), (unsigned)g.R), 64 * RED_SLICES, 0, s>>>(partial, fit, g.N,
+                                                                                            g.R, e.nchunks, add);
     return hipGetLastError();
 }
 

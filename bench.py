@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="shifted_sphere_d1m")
+    ap.add_argument("--path", choices=["percall", "run"], default="percall",
+                    help="percall: es_ask/es_eval/es_tell per generation; run: es_run over all K generations")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-dims", type=int, default=0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -115,20 +117,26 @@ def main():
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record(stream)
-    for k in range(K):
-        es.ask()
-        ev[k][0].record(stream)
-        es.eval(fit)
-        ev[k][1].record(stream)
-        es.tell(fit)
-        ev[k][2].record(stream)
+    if args.path == "run":
+        es.run(K, log=False)
+    else:
+        for k in range(K):
+            es.ask()
+            ev[k][0].record(stream)
+            es.eval(fit)
+            ev[k][1].record(stream)
+            es.tell(fit)
+            ev[k][2].record(stream)
     end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
     total_ms = start.elapsed_time(end)
     ms = total_ms / K
-    eval_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / K
-    tell_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / K
+    if args.path == "run":
+        eval_ms = tell_ms = float("nan")
+    else:
+        eval_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / K
+        tell_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / K
     value = R * N * D / (ms * 1e-3)
     log(f"[bench] {args.workload}: {ms:.4f} ms/gen (eval {eval_ms:.4f}, tell {tell_ms:.4f}), wall {wall:.3f}s "
         f"for {K} gens, {value:.4e} member-dims/s")
@@ -136,7 +144,7 @@ def main():
     prob = {P.PROB_SHIFTED_SPHERE: "shifted_sphere", P.PROB_SPHERE: "sphere", P.PROB_RASTRIGIN: "rastrigin",
             P.PROB_ROSENBROCK: "rosenbrock"}.get(cfg.problem)
     roof = None
-    if prob is not None:
+    if prob is not None and args.path == "percall":
         pair_blocks = R * (N // 2) * ((D + 3) // 4)
         achieved = pair_blocks * EVAL_SLOTS_PER_PAIR_BLOCK[prob] / (eval_ms * 1e-3)
         tell_achieved = pair_blocks * TELL_SLOTS_PER_PAIR_BLOCK / (tell_ms * 1e-3)
@@ -171,7 +179,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": args.workload, "num_runs": R, "popsize": N, "num_dims": D,
+        "config": {"workload": args.workload, "path": args.path, "num_runs": R, "popsize": N, "num_dims": D,
                    "problem": prob or "mlp", "sigma": cfg.sigma, "lr": cfg.lr,
                    "generations_per_s": 1e3 / ms, "eval_ms": eval_ms, "tell_ms": tell_ms},
         "roofline": roof,

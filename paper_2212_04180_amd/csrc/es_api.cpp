@@ -60,6 +60,13 @@ struct es_handle {
     float* fit = nullptr;    // [R][N] fitness scratch for es_run
     float* partial = nullptr;
     float* pdata = nullptr;  // [Dp] shift vector or teacher
+    // Adam constants of the generations of one fused es_run, staged in pinned
+    // host memory and copied on the stream; the event guards reuse.
+    AdamConsts* adam_host = nullptr;
+    AdamConsts* adam_dev = nullptr;
+    int32_t adam_cap = 0;
+    hipEvent_t adam_evt = nullptr;
+    int run_path = 0;  // 0 auto, 1 per-call kernels, 2 fused loop
     char err[512] = {0};
 };
 
@@ -152,9 +159,36 @@ int64_t env_i64(const char* name, int64_t dflt)
 void free_all(es_handle* h)
 {
     void* ptrs[] = {h->m, h->m1, h->v, h->best_x, h->grad, h->best_okey, h->best_f, h->best_j, h->table,
-                    h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata};
+                    h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->adam_dev};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
+    if (h->adam_host) (void)hipHostFree(h->adam_host);
+    if (h->adam_evt) (void)hipEventDestroy(h->adam_evt);
+}
+
+// Upload the Adam constants of generations t .. t+T-1 for the fused loop.
+es_status stage_adam(es_handle* h, int32_t T)
+{
+    if (h->adam_evt) ES_HIP(h, hipEventSynchronize(h->adam_evt), "wait for the previous constants upload");
+    if (T > h->adam_cap) {
+        if (h->adam_host) (void)hipHostFree(h->adam_host);
+        if (h->adam_dev) (void)hipFree(h->adam_dev);
+        h->adam_host = nullptr;
+        h->adam_dev = nullptr;
+        h->adam_cap = 0;
+        ES_HIP(h, hipHostMalloc(reinterpret_cast<void**>(&h->adam_host), sizeof(AdamConsts) * (size_t)T),
+               "pinned staging buffer");
+        ES_HIP(h, hipMalloc(reinterpret_cast<void**>(&h->adam_dev), sizeof(AdamConsts) * (size_t)T),
+               "Adam constants buffer");
+        h->adam_cap = T;
+    }
+    if (!h->adam_evt) ES_HIP(h, hipEventCreateWithFlags(&h->adam_evt, hipEventDisableTiming), "event");
+    for (int32_t i = 0; i < T; ++i) h->adam_host[i] = adam_consts(h->cfg, h->t + i);
+    ES_HIP(h, hipMemcpyAsync(h->adam_dev, h->adam_host, sizeof(AdamConsts) * (size_t)T, hipMemcpyHostToDevice,
+                             h->stream),
+           "upload Adam constants");
+    ES_HIP(h, hipEventRecord(h->adam_evt, h->stream), "record event");
+    return ES_OK;
 }
 
 es_status enqueue_tell(es_handle* h, const float* fitness, float* gen_best)
@@ -246,6 +280,7 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     g.P = cfg->popsize / 2;
     g.R = cfg->num_runs;
     h->plan = eval_plan(g, env_i64("ESMI_EVAL_BLOCKS_PER_CHUNK", 0));
+    h->run_path = (int)env_i64("ESMI_RUN_PATH", 0);
     hipError_t e = hipGetDevice(&h->device);
     const size_t rows = (size_t)g.Dp * g.R;
     if (e == hipSuccess) e = dalloc(&h->m, rows);
@@ -336,6 +371,23 @@ es_status es_run(es_handle* h, int32_t T, float* log)
     if (T < 0) return fail(h, ES_ERR_ARG, "es_run: T must be >= 0");
     if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_run: an ask is open");
     if (h->cfg.problem == ES_PROB_NONE) return fail(h, ES_ERR_UNSUPPORTED, "es_run needs a built-in problem");
+    if (T == 0) return ES_OK;
+    if (h->t + T > 0xFFFFFFFFll) return fail(h, ES_ERR_ARG, "es_run: generation counter would exceed 2^32");
+    const bool fused_ok = fused_supported(h->g, h->plan, h->cfg.problem);
+    // the fused loop pays off when each run is small: per-call launches then
+    // dominate, and the runs fill the chip one workgroup each
+    const bool fused = h->run_path == 2 ? fused_ok
+                       : h->run_path == 1 ? false
+                       : fused_ok && ((int64_t)h->g.P * h->g.nb <= 8192 || h->g.R >= 128);
+    if (fused) {
+        es_status s = stage_adam(h, T);
+        if (s != ES_OK) return s;
+        ES_HIP(h, launch_run_fused(h->g, h->cfg, h->plan, (uint32_t)h->t, T, h->adam_dev, h->m, h->m1, h->v,
+                                   h->best_x, h->best_okey, h->best_f, h->pdata, h->table, log, h->stream),
+               "fused generation loop");
+        h->t += T;
+        return ES_OK;
+    }
     for (int32_t i = 0; i < T; ++i) {
         es_status s = enqueue_eval(h, h->fit);
         if (s != ES_OK) return s;

@@ -54,6 +54,15 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, uint32_t t, const 
 hipError_t launch_debug_noise(const Geometry& g, const es_config& c, int32_t run, uint32_t t,
                               int32_t pair, uint32_t* words, float* eps, hipStream_t s);
 
+// Fused multi-generation loop (one workgroup per run, state in LDS).
+constexpr size_t FUSED_MAX_LDS = 60 * 1024;
+size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e);
+bool fused_supported(const Geometry& g, const EvalPlan& e, int problem);
+hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t0, int32_t T,
+                            const AdamConsts* adam, float* m, float* m1, float* v, float* best_x,
+                            uint32_t* best_okey, float* best_f, const float* pdata, const float* table, float* log,
+                            hipStream_t s);
+
 // Largest population the rank kernel stages in LDS.
 constexpr int32_t RANK_MAX_N = 16384;
 

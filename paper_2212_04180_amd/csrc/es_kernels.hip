@@ -34,6 +34,7 @@ constexpr int RANK_SLICES = 16;   // key slices per pair
 constexpr int TELL_LANES = 64;    // Philox blocks per tell workgroup
 constexpr int TELL_PS = 4;        // pair slices per tell workgroup (one wave each)
 constexpr int TELL_GROUP = 16;    // fp32 pairs folded into the fp64 sum at once
+constexpr int FUSED_WG = 256;     // threads of the fused multi-generation workgroup
 
 // MLP 64-256-256-16, flattened [out][in] per layer then the bias.  Returns
 // 1/sqrt(fan_in) for a weight and 0 for a bias.
@@ -192,35 +193,21 @@ __device__ __forceinline__ void block_terms(const float e[4], const float mv[4],
     }
 }
 
-template <int PROB>
-__global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
-    const float* __restrict__ m, const float* __restrict__ pdata, float* __restrict__ partial,
-    uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t N, int32_t P, int64_t bc, int64_t nchunks,
-    int32_t n_pg, float sigma, float ra)
+// Both members' sums of pair `row` over the Philox blocks [b0, b1) of one
+// run: fp32 sums of EVAL_FOLD blocks folded into fp64, in block order.  The
+// per-call kernel and the fused loop share this code, so both produce the
+// same bits.  V names the counter word that varies across the wave.
+template <int PROB, int V>
+__device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const float* __restrict__ pdata,
+                                           uint32_t k0, uint32_t k1, uint32_t row, uint32_t t, int64_t b0,
+                                           int64_t b1, int64_t D, float sg, float ra, double& accp, double& accm)
 {
-    const int32_t r = blockIdx.y;
-    const uint32_t w = blockIdx.x;
-    const uint32_t slot = w >> 3, xcd = w & 7u;
-    const int32_t pg = (int32_t)(slot % (uint32_t)n_pg);
-    const int64_t chunk = (int64_t)(slot / (uint32_t)n_pg) * 8 + xcd;
-    if (chunk >= nchunks) return;
-    const int32_t p = pg * (int32_t)blockDim.x + (int32_t)threadIdx.x;
-    const uint32_t row = (uint32_t)(p < P ? p : P - 1);
-    const uint64_t key = seed + (uint64_t)r;
-    const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
-    const float* __restrict__ mr = m + (int64_t)r * 4 * nb;
-    const int64_t b0 = chunk * bc;
-    const int64_t b1 = b0 + bc < nb ? b0 + bc : nb;
     const int64_t nfull = D / 4;
-    const int32_t nf = (int32_t)((b1 < nfull ? b1 : nfull) - b0);  // full blocks in this chunk (may be <= 0)
-    // sigma lives in a VGPR so that fmaf(sigma, eps, m) can take m from an SGPR
-    float sg;
-    asm volatile("v_mov_b32 %0, %1" : "=v"(sg) : "s"(sigma));
-
+    const int32_t nf = (int32_t)((b1 < nfull ? b1 : nfull) - b0);  // full blocks in [b0, b1) (may be <= 0)
     EvalLane L{0.0, 0.0, 0.f, 0.f, false};
     if (PROB == ES_PROB_ROSENBROCK && b0 > 0) {
         float e[4];
-        box_muller4(philox4x32_10<LANES_ROW>(k0, k1, (uint32_t)(b0 - 1), row, t, DOM_NOISE), e);
+        box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(b0 - 1), row, t, DOM_NOISE), e);
         const float mv = mr[4 * b0 - 1];
         L.xlp = fmaf(sg, e[3], mv);
         L.xlm = fmaf(-sg, e[3], mv);
@@ -242,7 +229,7 @@ __global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
 #pragma unroll
         for (int k = 0; k < EVAL_FOLD; ++k) {
             float e[4];
-            box_muller4(philox4x32_10<LANES_ROW>(k0, k1, (uint32_t)(bg + k), row, t, DOM_NOISE), e);
+            box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(bg + k), row, t, DOM_NOISE), e);
             block_terms<PROB>(e, mv + 4 * k, PROB == ES_PROB_SHIFTED_SPHERE ? sv + 4 * k : zero4, sg, ra, L, sp,
                               sm);
         }
@@ -259,7 +246,7 @@ __global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
             for (int q = 0; q < 4; ++q) sv[q] = pdata[4 * b + q];
         }
         float e[4];
-        box_muller4(philox4x32_10<LANES_ROW>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
+        box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
         float sp = 0.f, sm = 0.f;
         block_terms<PROB>(e, mv, sv, sg, ra, L, sp, sm);
         L.accp += (double)sp;
@@ -267,11 +254,11 @@ __global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
     }
 
     // Ragged tail: the last Philox block holds D % 4 live dims.
-    if (b1 > nfull && b1 == nb && nfull >= b0) {
+    if (b1 > nfull && nfull >= b0) {
         const int64_t b = nfull;
         const int nv = (int)(D - 4 * b);
         float e[4];
-        box_muller4(philox4x32_10<LANES_ROW>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
+        box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
         float sp = 0.f, sm = 0.f;
         for (int k = 0; k < nv; ++k) {
             const float mv = mr[4 * b + k];
@@ -293,11 +280,37 @@ __global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
         L.accp += (double)sp;
         L.accm += (double)sm;
     }
+    accp = L.accp;
+    accm = L.accm;
+}
 
+template <int PROB>
+__global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
+    const float* __restrict__ m, const float* __restrict__ pdata, float* __restrict__ partial,
+    uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t N, int32_t P, int64_t bc, int64_t nchunks,
+    int32_t n_pg, float sigma, float ra)
+{
+    const int32_t r = blockIdx.y;
+    const uint32_t w = blockIdx.x;
+    const uint32_t slot = w >> 3, xcd = w & 7u;
+    const int32_t pg = (int32_t)(slot % (uint32_t)n_pg);
+    const int64_t chunk = (int64_t)(slot / (uint32_t)n_pg) * 8 + xcd;
+    if (chunk >= nchunks) return;
+    const int32_t p = pg * (int32_t)blockDim.x + (int32_t)threadIdx.x;
+    const uint32_t row = (uint32_t)(p < P ? p : P - 1);
+    const uint64_t key = seed + (uint64_t)r;
+    const int64_t b0 = chunk * bc;
+    const int64_t b1 = b0 + bc < nb ? b0 + bc : nb;
+    // sigma lives in a VGPR so that fmaf(sigma, eps, m) can take m from an SGPR
+    float sg;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(sg) : "s"(sigma));
+    double accp, accm;
+    eval_chunk<PROB, LANES_ROW>(m + (int64_t)r * 4 * nb, pdata, (uint32_t)key, (uint32_t)(key >> 32), row, t, b0,
+                                b1, D, sg, ra, accp, accm);
     if (p < P) {
         float* o = partial + (chunk * gridDim.y + r) * (int64_t)N;
-        o[p] = (float)L.accp;
-        o[p + P] = (float)L.accm;
+        o[p] = (float)accp;
+        o[p + P] = (float)accm;
     }
 }
 
@@ -312,8 +325,20 @@ __global__ __launch_bounds__(64 * RED_SLICES) void k_eval_reduce(const float* __
     const int32_t tx = threadIdx.x & 63, s = threadIdx.x >> 6;
     const int32_t j = blockIdx.x * 64 + tx;
     double acc = 0.0;
-    if (j < N)
-        for (int64_t c = s; c < nchunks; c += RED_SLICES) acc += (double)partial[(c * R + r) * (int64_t)N + j];
+    if (j < N) {
+        const int64_t stride = (int64_t)RED_SLICES * R * N;
+        const float* __restrict__ q = partial + ((int64_t)s * R + r) * N + j;
+        int64_t c = s;
+        // eight loads in flight, summed in chunk order
+        for (; c + 7 * RED_SLICES < nchunks; c += 8 * RED_SLICES, q += 8 * stride) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = q[u * stride];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) acc += (double)v[u];
+        }
+        for (; c < nchunks; c += RED_SLICES, q += stride) acc += (double)*q;
+    }
     red[s][tx] = acc;
     __syncthreads();
     if (s == 0 && j < N) {
@@ -349,8 +374,20 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
     const uint32_t K1 = keys[j1], K2 = keys[j2];
     const int32_t kb = (int32_t)(((int64_t)N * s) / RANK_SLICES);
     const int32_t ke = (int32_t)(((int64_t)N * (s + 1)) / RANK_SLICES);
+    // rank_j = #{k : key_k < key_j} + #{k < j : key_k == key_j}
     int32_t c1 = 0, c2 = 0;
-    for (int32_t k = kb; k < ke; ++k) {
+    int32_t k = kb;
+    for (; k + 4 <= ke; k += 4) {
+        uint32_t kk[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) kk[u] = keys[k + u];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            c1 += (kk[u] < K1) | ((kk[u] == K1) & (k + u < j1));
+            c2 += (kk[u] < K2) | ((kk[u] == K2) & (k + u < j2));
+        }
+    }
+    for (; k < ke; ++k) {
         const uint32_t kk = keys[k];
         c1 += (kk < K1) | ((kk == K1) & (k < j1));
         c2 += (kk < K2) | ((kk == K2) & (k < j2));
@@ -397,6 +434,64 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
 }
 
 // ---------------------------------------------------------------------------
+// Weighted noise sum of one Philox block over the pairs [pb, pe):
+// a64[k] = sum_p w_p eps_{p, 4b+k}, fp32 over TELL_GROUP pairs folded into
+// fp64, in pair order.  Shared by the per-call and the fused kernels.
+template <int V>
+__device__ __forceinline__ void tell_slice(const float* __restrict__ wr, uint32_t k0, uint32_t k1, uint32_t bb,
+                                           uint32_t t, int32_t pb, int32_t pe, double a64[4])
+{
+    int32_t p0 = pb;
+    for (; p0 + TELL_GROUP <= pe; p0 += TELL_GROUP) {
+        float wv[TELL_GROUP];
+#pragma unroll
+        for (int q = 0; q < TELL_GROUP; ++q) wv[q] = wr[p0 + q];
+        float a32[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < TELL_GROUP; ++q) {
+            float e[4];
+            box_muller4(philox4x32_10<V>(k0, k1, bb, (uint32_t)(p0 + q), t, DOM_NOISE), e);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) a32[k] = fmaf(wv[q], e[k], a32[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) a64[k] += (double)a32[k];
+    }
+    float a32[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int32_t p = p0; p < pe; ++p) {
+        float e[4];
+        box_muller4(philox4x32_10<V>(k0, k1, bb, (uint32_t)p, t, DOM_NOISE), e);
+        const float w = wr[p];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) a32[k] = fmaf(w, e[k], a32[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) a64[k] += (double)a32[k];
+}
+
+// g = sum / (N sigma), then Adam (Kingma & Ba) in fp32 in a fixed operation
+// order on four dims; dims at or beyond D stay zero.
+__device__ __forceinline__ void adam_block(const double a64[4], double inv_ns, const AdamConsts& ac, int64_t d0,
+                                           int64_t D, const float mo[4], const float m1o[4], const float vo[4],
+                                           float mn[4], float m1n[4], float vn[4], float gg[4])
+{
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const float g = (float)(a64[k] * inv_ns);
+        gg[k] = g;
+        const float nm1 = __builtin_fmaf(ac.beta1, m1o[k], __fmul_rn(ac.omb1, g));
+        const float nv = __builtin_fmaf(ac.beta2, vo[k], __fmul_rn(ac.omb2, __fmul_rn(g, g)));
+        const float mhat = nm1 / ac.bc1;
+        const float vhat = nv / ac.bc2;
+        const float den = __fadd_rn(sqrtf(vhat), ac.eps);
+        const float q = mhat / den;
+        mn[k] = __builtin_fmaf(-ac.lr, q, mo[k]);
+        m1n[k] = nm1;
+        vn[k] = nv;
+        if (d0 + k >= D) { mn[k] = 0.f; m1n[k] = 0.f; vn[k] = 0.f; gg[k] = 0.f; }
+    }
+}
+
 // Gradient + Adam.  Workgroup = TELL_LANES Philox blocks x TELL_PS pair
 // slices of one run.  Each lane walks its slice of pairs with the folded
 // weight w_p = y_p - y_{p+N/2} (uniform across the wave), regenerating the
@@ -417,39 +512,11 @@ __global__ __launch_bounds__(TELL_LANES * TELL_PS) void k_tell(
     const uint32_t bb = (uint32_t)(b < nb ? b : nb - 1);
     const uint64_t key = seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
-    const float* __restrict__ wr = wfold + (int64_t)r * P;
     const int32_t pb = (int32_t)(((int64_t)P * s) / TELL_PS);
     const int32_t pe = (int32_t)(((int64_t)P * (s + 1)) / TELL_PS);
 
     double a64[4] = {0.0, 0.0, 0.0, 0.0};
-    int32_t p0 = pb;
-    for (; p0 + TELL_GROUP <= pe; p0 += TELL_GROUP) {
-        float wv[TELL_GROUP];
-#pragma unroll
-        for (int q = 0; q < TELL_GROUP; ++q) wv[q] = wr[p0 + q];
-        float a32[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int q = 0; q < TELL_GROUP; ++q) {
-            float e[4];
-            box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, bb, (uint32_t)(p0 + q), t, DOM_NOISE), e);
-#pragma unroll
-            for (int k = 0; k < 4; ++k) a32[k] = fmaf(wv[q], e[k], a32[k]);
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k) a64[k] += (double)a32[k];
-    }
-    {
-        float a32[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int32_t p = p0; p < pe; ++p) {
-            float e[4];
-            box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, bb, (uint32_t)p, t, DOM_NOISE), e);
-            const float w = wr[p];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) a32[k] = fmaf(w, e[k], a32[k]);
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k) a64[k] += (double)a32[k];
-    }
+    tell_slice<LANES_BLOCK>(wfold + (int64_t)r * P, k0, k1, bb, t, pb, pe, a64);
     if (s > 0) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) red[s - 1][tx][k] = a64[k];
@@ -469,22 +536,7 @@ __global__ __launch_bounds__(TELL_LANES * TELL_PS) void k_tell(
     const float m1o[4] = {m14.x, m14.y, m14.z, m14.w};
     const float vo[4] = {v4.x, v4.y, v4.z, v4.w};
     float mn[4], m1n[4], vn[4], gg[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        // Adam (Kingma & Ba), fp32 in a fixed operation order.
-        const float g = (float)(a64[k] * inv_ns);
-        gg[k] = g;
-        const float nm1 = __builtin_fmaf(ac.beta1, m1o[k], __fmul_rn(ac.omb1, g));
-        const float nv = __builtin_fmaf(ac.beta2, vo[k], __fmul_rn(ac.omb2, __fmul_rn(g, g)));
-        const float mhat = nm1 / ac.bc1;
-        const float vhat = nv / ac.bc2;
-        const float den = __fadd_rn(sqrtf(vhat), ac.eps);
-        const float q = mhat / den;
-        mn[k] = __builtin_fmaf(-ac.lr, q, mo[k]);
-        m1n[k] = nm1;
-        vn[k] = nv;
-        if (4 * b + k >= D) { mn[k] = 0.f; m1n[k] = 0.f; vn[k] = 0.f; gg[k] = 0.f; }
-    }
+    adam_block(a64, inv_ns, ac, 4 * b, D, mo, m1o, vo, mn, m1n, vn, gg);
     const int32_t jb = best_j[r];
     if (jb >= 0) {
         const int32_t pbst = jb < P ? jb : jb - P;
@@ -500,6 +552,165 @@ __global__ __launch_bounds__(TELL_LANES * TELL_PS) void k_tell(
     *reinterpret_cast<float4*>(m1 + off) = make_float4(m1n[0], m1n[1], m1n[2], m1n[3]);
     *reinterpret_cast<float4*>(v + off) = make_float4(vn[0], vn[1], vn[2], vn[3]);
     if (grad) *reinterpret_cast<float4*>(grad + off) = make_float4(gg[0], gg[1], gg[2], gg[3]);
+}
+
+// ---------------------------------------------------------------------------
+// T whole generations in one launch (the scanned loop of Listing 2) for
+// small strategies: one workgroup per run, the mean and Adam moments in LDS.
+// Each phase repeats the per-call kernels' arithmetic in the same order
+// (same chunking of the evaluation, same reduction order, same pair slices
+// of the gradient), so es_run gives the same bits on either path.
+struct FusedArgs {
+    float* m;
+    float* m1;
+    float* v;
+    float* best_x;
+    uint32_t* best_okey;
+    float* best_f;
+    const float* pdata;
+    const float* table;
+    const AdamConsts* adam;  // [T], for generations t0 .. t0+T-1
+    float* log;              // [T][R] or null
+    uint64_t seed;
+    uint32_t t0;
+    int32_t T;
+    int64_t D, nb;
+    int32_t N, P, R;
+    int64_t bc, nchunks;
+    float sigma, ra;
+    double add, inv_ns;
+    int32_t maximize, raw;
+};
+
+template <int PROB>
+__global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
+{
+    extern __shared__ double smem[];
+    const int32_t r = blockIdx.x;
+    const int64_t Dp = 4 * a.nb;
+    // LDS layout: tell slices (fp64) | m | m1 | v | partial | fit | y | wf | keys | best
+    double* red = smem;                                  // [TELL_PS][nb][4]
+    float* ms = reinterpret_cast<float*>(red + (int64_t)TELL_PS * a.nb * 4);
+    float* m1s = ms + Dp;
+    float* vs = m1s + Dp;
+    float* part = vs + Dp;                               // [nchunks][N]
+    float* fit = part + a.nchunks * a.N;                 // [N]
+    float* y = fit + a.N;                                // [N]
+    float* wf = y + a.N;                                 // [P]
+    uint32_t* keys = reinterpret_cast<uint32_t*>(wf + a.P);  // [N]
+    __shared__ int32_t best_j;
+
+    const uint64_t key = a.seed + (uint64_t)r;
+    const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
+    const int64_t goff = (int64_t)r * Dp;
+    for (int64_t i = threadIdx.x; i < Dp; i += blockDim.x) {
+        ms[i] = a.m[goff + i];
+        m1s[i] = a.m1[goff + i];
+        vs[i] = a.v[goff + i];
+    }
+    __syncthreads();
+
+    for (int32_t it = 0; it < a.T; ++it) {
+        const uint32_t t = a.t0 + (uint32_t)it;
+        // evaluate: items (pair, chunk)
+        const int64_t items = (int64_t)a.P * a.nchunks;
+        for (int64_t i = threadIdx.x; i < items; i += blockDim.x) {
+            const int32_t p = (int32_t)(i % a.P);
+            const int64_t c = i / a.P;
+            const int64_t b0 = c * a.bc, b1 = b0 + a.bc < a.nb ? b0 + a.bc : a.nb;
+            double accp, accm;
+            eval_chunk<PROB, LANES_BLOCK_AND_ROW>(ms, a.pdata, k0, k1, (uint32_t)p, t, b0, b1, a.D, a.sigma, a.ra,
+                                                  accp, accm);
+            part[c * a.N + p] = (float)accp;
+            part[c * a.N + p + a.P] = (float)accm;
+        }
+        __syncthreads();
+        // fitness in the reduce kernel's order, and order keys
+        for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) {
+            double tot = a.add;
+            for (int q = 0; q < RED_SLICES; ++q) {
+                double acc = 0.0;
+                for (int64_t c = q; c < a.nchunks; c += RED_SLICES) acc += (double)part[c * a.N + j];
+                tot += acc;
+            }
+            const float f = (float)tot;
+            fit[j] = f;
+            keys[j] = order_key(f, a.maximize);
+        }
+        __syncthreads();
+        // centered ranks, weights, best-so-far and the generation's log entry
+        for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) {
+            const uint32_t K = keys[j];
+            int32_t rk = 0;
+            for (int32_t k = 0; k < a.N; ++k) rk += (keys[k] < K) | ((keys[k] == K) & (k < j));
+            y[j] = a.raw ? (a.maximize ? -fit[j] : fit[j]) : a.table[rk];
+            if (rk == 0) {
+                if (a.log) a.log[(int64_t)it * a.R + r] = fit[j];
+                if (K < a.best_okey[r]) {
+                    a.best_okey[r] = K;
+                    a.best_f[r] = fit[j];
+                    best_j = j;
+                } else {
+                    best_j = -1;
+                }
+            }
+        }
+        __syncthreads();
+        for (int32_t p = threadIdx.x; p < a.P; p += blockDim.x) wf[p] = y[p] - y[p + a.P];
+        __syncthreads();
+        // tell: items (block, pair slice), slices summed in order, then Adam
+        const AdamConsts ac = a.adam[it];
+        for (int64_t i = threadIdx.x; i < (int64_t)TELL_PS * a.nb; i += blockDim.x) {
+            const int32_t s = (int32_t)(i / a.nb);
+            const int64_t b = i - (int64_t)s * a.nb;
+            const int32_t pb = (int32_t)(((int64_t)a.P * s) / TELL_PS);
+            const int32_t pe = (int32_t)(((int64_t)a.P * (s + 1)) / TELL_PS);
+            double a64[4] = {0.0, 0.0, 0.0, 0.0};
+            tell_slice<LANES_BLOCK_AND_ROW>(wf, k0, k1, (uint32_t)b, t, pb, pe, a64);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) red[((int64_t)s * a.nb + b) * 4 + k] = a64[k];
+        }
+        __syncthreads();
+        const int32_t jb = best_j;
+        for (int64_t b = threadIdx.x; b < a.nb; b += blockDim.x) {
+            double a64[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                a64[k] = red[b * 4 + k];
+#pragma unroll
+                for (int q = 1; q < TELL_PS; ++q) a64[k] += red[((int64_t)q * a.nb + b) * 4 + k];
+            }
+            float mo[4], m1o[4], vo[4], mn[4], m1n[4], vn[4], gg[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                mo[k] = ms[4 * b + k];
+                m1o[k] = m1s[4 * b + k];
+                vo[k] = vs[4 * b + k];
+            }
+            adam_block(a64, a.inv_ns, ac, 4 * b, a.D, mo, m1o, vo, mn, m1n, vn, gg);
+            if (jb >= 0) {
+                const int32_t pbst = jb < a.P ? jb : jb - a.P;
+                const float sg = jb < a.P ? a.sigma : -a.sigma;
+                float e[4];
+                box_muller4(philox4x32_10<LANES_BLOCK_AND_ROW>(k0, k1, (uint32_t)b, (uint32_t)pbst, t, DOM_NOISE),
+                            e);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) a.best_x[goff + 4 * b + k] = 4 * b + k < a.D ? fmaf(sg, e[k], mo[k]) : 0.f;
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                ms[4 * b + k] = mn[k];
+                m1s[4 * b + k] = m1n[k];
+                vs[4 * b + k] = vn[k];
+            }
+        }
+        __syncthreads();
+    }
+    for (int64_t i = threadIdx.x; i < Dp; i += blockDim.x) {
+        a.m[goff + i] = ms[i];
+        a.m1[goff + i] = m1s[i];
+        a.v[goff + i] = vs[i];
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -545,12 +756,12 @@ EvalPlan eval_plan(const Geometry& g, int64_t bc_override)
         bc = bc_override;
     } else {
         // About 16384 waves in flight over the launch (two rounds of a full
-        // chip at 8 waves per SIMD), with at least 16 blocks per chunk.
+        // chip at 8 waves per SIMD), with at least EVAL_FOLD blocks per chunk.
         const int64_t waves_per_chunk = (int64_t)e.n_pg * (e.wg / 64) * g.R;
         int64_t nch = (16384 + waves_per_chunk - 1) / waves_per_chunk;
         if (nch < 1) nch = 1;
         bc = (g.nb + nch - 1) / nch;
-        if (bc < 16) bc = 16;
+        if (bc < EVAL_FOLD) bc = EVAL_FOLD;
     }
     if (bc > g.nb) bc = g.nb;
     e.bc = bc;
@@ -629,6 +840,43 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, uint32_t t, const 
     const dim3 grid((unsigned)((g.nb + TELL_LANES - 1) / TELL_LANES), (unsigned)g.R);
     k_tell<<<grid, TELL_LANES * TELL_PS, 0, s>>>(wfold, best_j, m, m1, v, grad, best_x, c.seed, t, g.D, g.nb,
                                                  g.P, c.sigma, inv_ns, a);
+    return hipGetLastError();
+}
+
+size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e)
+{
+    const size_t red = sizeof(double) * (size_t)TELL_PS * g.nb * 4;
+    const size_t f32 = sizeof(float) * (size_t)(3 * g.Dp + e.nchunks * g.N + 2 * g.N + g.P + g.N);
+    return red + f32;
+}
+
+bool fused_supported(const Geometry& g, const EvalPlan& e, int problem)
+{
+    if (problem < ES_PROB_SPHERE || problem > ES_PROB_RASTRIGIN) return false;
+    return fused_lds_bytes(g, e) <= FUSED_MAX_LDS;
+}
+
+hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t0, int32_t T,
+                            const AdamConsts* adam, float* m, float* m1, float* v, float* best_x,
+                            uint32_t* best_okey, float* best_f, const float* pdata, const float* table, float* log,
+                            hipStream_t s)
+{
+    FusedArgs a;
+    a.m = m; a.m1 = m1; a.v = v; a.best_x = best_x; a.best_okey = best_okey; a.best_f = best_f;
+    a.pdata = pdata; a.table = table; a.adam = adam; a.log = log;
+    a.seed = c.seed; a.t0 = t0; a.T = T; a.D = g.D; a.nb = g.nb; a.N = g.N; a.P = g.P; a.R = g.R;
+    a.bc = e.bc; a.nchunks = e.nchunks; a.sigma = c.sigma; a.ra = c.rastrigin_a;
+    a.add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;
+    a.inv_ns = 1.0 / ((double)g.N * (double)c.sigma);
+    a.maximize = c.maximize; a.raw = c.shaping == ES_SHAPE_RAW;
+    const size_t lds = fused_lds_bytes(g, e);
+    switch (c.problem) {
+    case ES_PROB_SPHERE: k_run_fused<ES_PROB_SPHERE><<<g.R, FUSED_WG, lds, s>>>(a); break;
+    case ES_PROB_SHIFTED_SPHERE: k_run_fused<ES_PROB_SHIFTED_SPHERE><<<g.R, FUSED_WG, lds, s>>>(a); break;
+    case ES_PROB_ROSENBROCK: k_run_fused<ES_PROB_ROSENBROCK><<<g.R, FUSED_WG, lds, s>>>(a); break;
+    case ES_PROB_RASTRIGIN: k_run_fused<ES_PROB_RASTRIGIN><<<g.R, FUSED_WG, lds, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

@@ -185,3 +185,26 @@ def test_raw_shaping_linear_gradient_converges_to_a():
     g = _np(es.grad())[0]
     sd = np.sqrt((a @ a + a * a) / (N / 2))
     assert np.all(np.abs(g - a) <= 5 * sd)
+
+
+@pytest.mark.parametrize("prob,D,N,R,T", [("sphere", 16, 32, 1, 40), ("rastrigin", 100, 64, 8, 25),
+                                          ("rosenbrock", 37, 10, 3, 30), ("shifted", 1001, 8, 2, 6)])
+def test_fused_loop_matches_per_call_bits(prob, D, N, R, T, monkeypatch):
+    """The one-launch loop (one workgroup per run) repeats the per-call
+    kernels' arithmetic in the same order: identical bits."""
+    P = _P()
+    pmap = {"sphere": P.PROB_SPHERE, "shifted": P.PROB_SHIFTED_SPHERE, "rosenbrock": P.PROB_ROSENBROCK,
+            "rastrigin": P.PROB_RASTRIGIN}
+    cfg = P.ESConfig(num_dims=D, popsize=N, num_runs=R, sigma=0.2, lr=0.02, seed=17, init_lo=-3.0, init_hi=3.0,
+                     problem=pmap[prob], init=P.INIT_ZERO if prob == "shifted" else P.INIT_UNIFORM)
+    out = {}
+    for path in ("1", "2"):
+        monkeypatch.setenv("ESMI_RUN_PATH", path)
+        es = P.ES(cfg)
+        es.run(3)
+        log = _np(es.run(T))
+        st = es.get_state()
+        bx, bf = es.best()
+        out[path] = (log, _np(st["m"]), _np(st["m1"]), _np(st["v"]), _np(bx), _np(bf), st["t"])
+    for a, b in zip(out["1"], out["2"]):
+        np.testing.assert_array_equal(a, b)

@@ -40,6 +40,36 @@ EVAL_SLOTS_PER_PAIR_BLOCK = {"sphere": PHILOX_BM + 24, "shifted_sphere": PHILOX_
 TELL_SLOTS_PER_PAIR_BLOCK = PHILOX_BM + 4 + 1
 
 
+def kernel_source_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("es_device.hpp", "es_kernels.hip"):
+        with open(os.path.join(ROOT, "paper_2212_04180_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def profiled_traffic(workload):
+    """HBM bytes per launch of the evaluate kernel from the committed rocprofv3
+    counter summary of this workload, or None if there is none or the kernel
+    sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"k_eval_bbob_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256") != kernel_source_sha256():
+        return None
+    try:
+        return int(kv["eval_hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -149,7 +179,8 @@ def main():
         achieved = pair_blocks * EVAL_SLOTS_PER_PAIR_BLOCK[prob] / (eval_ms * 1e-3)
         tell_achieved = pair_blocks * TELL_SLOTS_PER_PAIR_BLOCK / (tell_ms * 1e-3)
         roof = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
-                "unit": "T VALU lane-op slots/s", "frac": achieved / VALU_PEAK, "traffic": None,
+                "unit": "T VALU lane-op slots/s", "frac": achieved / VALU_PEAK,
+                "traffic": profiled_traffic(args.workload),
                 "kernel": "k_eval_bbob (fused sample+evaluate; timed with its k_eval_reduce)",
                 "kernel_ms": eval_ms, "slots_per_pair_block": EVAL_SLOTS_PER_PAIR_BLOCK[prob],
                 "pair_blocks_per_launch": pair_blocks,

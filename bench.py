@@ -21,6 +21,9 @@ sys.path.insert(0, ROOT)
 # 7.86e13 full-rate VALU lane-ops/s (an FMA counts two flops); HBM3E 8 TB/s.
 VALU_PEAK = 157.3e12 / 2.0  # lane-op slots/s
 HBM_PEAK = 8.0e12
+BF16_MFMA_PEAK = 2.5e15  # dense bf16 matrix FLOP/s
+# Neuroevolution MLP 64-256-256-16 on 256 inputs: 2 flops per weight per input
+MLP_FLOPS_PER_MEMBER = 2 * 256 * (64 * 256 + 256 * 256 + 256 * 16)
 
 # Algorithmic VALU work, in full-rate lane-op slots per Philox block of one
 # antithetic pair (4 dims x 2 members).  Issue costs measured on gfx950
@@ -186,6 +189,18 @@ def main():
                 "pair_blocks_per_launch": pair_blocks,
                 "tell": {"kernel": "k_rank + k_tell", "kernel_ms": tell_ms, "achieved": tell_achieved / 1e12,
                          "frac": tell_achieved / VALU_PEAK, "slots_per_pair_block": TELL_SLOTS_PER_PAIR_BLOCK}}
+    if cfg.problem == P.PROB_MLP and args.path == "percall":
+        flops = R * N * MLP_FLOPS_PER_MEMBER
+        achieved = flops / (eval_ms * 1e-3)
+        pair_blocks = R * (N // 2) * ((D + 3) // 4)
+        tell_achieved = pair_blocks * TELL_SLOTS_PER_PAIR_BLOCK / (tell_ms * 1e-3)
+        roof = {"bound": "mfma", "achieved": achieved / 1e12, "peak": BF16_MFMA_PEAK / 1e12, "unit": "TFLOP/s",
+                "frac": achieved / BF16_MFMA_PEAK, "traffic": None,
+                "kernel": "k_mlp_inputs + k_mlp_teacher + k_eval_mlp (bf16 MFMA forward of every member)",
+                "kernel_ms": eval_ms, "flops_per_launch": flops,
+                "generation_frac": flops / (ms * 1e-3) / BF16_MFMA_PEAK,
+                "tell": {"kernel": "k_rank + k_tell", "kernel_ms": tell_ms, "achieved": tell_achieved / 1e12,
+                         "unit": "T VALU lane-op slots/s", "frac": tell_achieved / VALU_PEAK}}
     # The benchmark spec's HBM reading: the same generation with the noise stored
     # (written once by evaluate, read once by tell) moves 4 B per member-dim.
     hbm_equiv = {"bytes_per_member_dim": 4.0, "peak_member_dims_per_s": HBM_PEAK / 4.0,

@@ -60,6 +60,7 @@ struct es_handle {
     float* fit = nullptr;    // [R][N] fitness scratch for es_run
     float* partial = nullptr;
     float* pdata = nullptr;  // [Dp] shift vector or teacher
+    void* mlp_scratch = nullptr;  // MLP inputs and teacher outputs of the current generation
     // Adam constants of the generations of one fused es_run, staged in pinned
     // host memory and copied on the stream; the event guards reuse.
     AdamConsts* adam_host = nullptr;
@@ -119,9 +120,11 @@ const char* validate(const es_config& c)
     if (c.init < ES_INIT_UNIFORM || c.init > ES_INIT_FANIN_NORMAL) return "unknown init";
     if (c.init == ES_INIT_UNIFORM && !(c.init_hi > c.init_lo)) return "init range must have hi > lo";
     if (c.problem < ES_PROB_NONE || c.problem > ES_PROB_MLP) return "unknown problem";
-    if (c.init == ES_INIT_FANIN_NORMAL && c.num_dims != 86544)
+    if (c.init == ES_INIT_FANIN_NORMAL && c.num_dims != MLP_NUM_PARAMS)
         return "fan-in normal init is defined for the 64-256-256-16 MLP (num_dims 86544)";
-    if (c.problem == ES_PROB_MLP && c.num_dims != 86544) return "MLP problem needs num_dims 86544";
+    if (c.problem == ES_PROB_MLP && c.num_dims != MLP_NUM_PARAMS) return "MLP problem needs num_dims 86544";
+    if (c.problem == ES_PROB_MLP && c.mlp_batch != 256) return "MLP problem needs mlp_batch 256";
+    if (c.problem == ES_PROB_MLP && c.mlp_bf16 != 1) return "the MLP forward runs on bf16 matrix cores (mlp_bf16 = 1)";
     if (c.problem == ES_PROB_RASTRIGIN && !std::isfinite(c.rastrigin_a)) return "rastrigin_a must be finite";
     if ((c.flags & ~ES_FLAG_KEEP_GRAD) != 0) return "unknown flags";
     return nullptr;
@@ -159,7 +162,7 @@ int64_t env_i64(const char* name, int64_t dflt)
 void free_all(es_handle* h)
 {
     void* ptrs[] = {h->m, h->m1, h->v, h->best_x, h->grad, h->best_okey, h->best_f, h->best_j, h->table,
-                    h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->adam_dev};
+                    h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->adam_dev, h->mlp_scratch};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     if (h->adam_host) (void)hipHostFree(h->adam_host);
@@ -208,7 +211,11 @@ es_status enqueue_tell(es_handle* h, const float* fitness, float* gen_best)
 es_status enqueue_eval(es_handle* h, float* fit)
 {
     if (h->cfg.problem == ES_PROB_NONE) return fail(h, ES_ERR_UNSUPPORTED, "no built-in problem configured");
-    if (h->cfg.problem == ES_PROB_MLP) return fail(h, ES_ERR_UNSUPPORTED, "MLP evaluation is not built");
+    if (h->cfg.problem == ES_PROB_MLP) {
+        ES_HIP(h, launch_eval_mlp(h->g, h->cfg, (uint32_t)h->t, h->m, h->pdata, h->mlp_scratch, fit, h->stream),
+               "MLP evaluate kernels");
+        return ES_OK;
+    }
     ES_HIP(h, launch_eval_bbob(h->g, h->cfg, h->plan, (uint32_t)h->t, h->m, h->pdata, h->partial, fit, h->stream),
            "evaluate kernel");
     return ES_OK;
@@ -300,6 +307,8 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
         e = dalloc(&h->partial, (size_t)eval_partial_elems(g, h->plan));
     if (e == hipSuccess && (cfg->problem == ES_PROB_SHIFTED_SPHERE || cfg->problem == ES_PROB_MLP))
         e = dalloc(&h->pdata, (size_t)g.Dp);
+    if (e == hipSuccess && cfg->problem == ES_PROB_MLP)
+        e = dalloc(reinterpret_cast<char**>(&h->mlp_scratch), mlp_scratch_bytes());
     if (e != hipSuccess) {
         free_all(h);
         delete h;

@@ -54,6 +54,10 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, uint32_t t, const 
 hipError_t launch_debug_noise(const Geometry& g, const es_config& c, int32_t run, uint32_t t,
                               int32_t pair, uint32_t* words, float* eps, hipStream_t s);
 
+// Pair slices of the gradient kernel (one wave each); the fused loop uses
+// the same split so that both paths sum in the same order.
+int32_t tell_slices(const Geometry& g);
+
 // Fused multi-generation loop (one workgroup per run, state in LDS).
 constexpr size_t FUSED_MAX_LDS = 60 * 1024;
 size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e);
@@ -62,6 +66,13 @@ hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPla
                             const AdamConsts* adam, float* m, float* m1, float* v, float* best_x,
                             uint32_t* best_okey, float* best_f, const float* pdata, const float* table, float* log,
                             hipStream_t s);
+
+// Neuroevolution problem (64-256-256-16 MLP vs a teacher).
+constexpr int64_t MLP_NUM_PARAMS = 86544;
+size_t mlp_scratch_bytes();  // X_t (fp32 and bf16) and teacher outputs
+size_t mlp_lds_bytes();
+hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, const float* m, const float* teacher,
+                           void* scratch, float* fit, hipStream_t s);
 
 // Largest population the rank kernel stages in LDS.
 constexpr int32_t RANK_MAX_N = 16384;

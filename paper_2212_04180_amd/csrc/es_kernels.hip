@@ -32,7 +32,7 @@ constexpr int RED_SLICES = 16;    // chunk slices per member in the partial redu
 constexpr int RANK_PAIRS = 16;    // pairs per rank workgroup
 constexpr int RANK_SLICES = 16;   // key slices per pair
 constexpr int TELL_LANES = 64;    // Philox blocks per tell workgroup
-constexpr int TELL_PS = 4;        // pair slices per tell workgroup (one wave each)
+constexpr int TELL_MAX_PS = 16;   // pair slices per tell workgroup (one wave each)
 constexpr int TELL_GROUP = 16;    // fp32 pairs folded into the fp64 sum at once
 constexpr int FUSED_WG = 256;     // threads of the fused multi-generation workgroup
 
@@ -492,18 +492,18 @@ __device__ __forceinline__ void adam_block(const double a64[4], double inv_ns, c
     }
 }
 
-// Gradient + Adam.  Workgroup = TELL_LANES Philox blocks x TELL_PS pair
-// slices of one run.  Each lane walks its slice of pairs with the folded
+// Gradient + Adam.  Workgroup = TELL_LANES Philox blocks x ps pair slices
+// (ps <= TELL_MAX_PS, chosen per geometry) of one run.  Each lane walks its slice of pairs with the folded
 // weight w_p = y_p - y_{p+N/2} (uniform across the wave), regenerating the
 // pair's normals, so g_d = sum_p w_p eps_{p,d} / (N sigma) needs no
 // cross-lane reduction; the slices meet in LDS in a fixed order.
-__global__ __launch_bounds__(TELL_LANES * TELL_PS) void k_tell(
+__global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(
     const float* __restrict__ wfold, const int32_t* __restrict__ best_j, float* __restrict__ m,
     float* __restrict__ m1, float* __restrict__ v, float* __restrict__ grad,
-    float* __restrict__ best_x, uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t P,
+    float* __restrict__ best_x, uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t P, int32_t ps,
     float sigma, double inv_ns, AdamConsts ac)
 {
-    __shared__ double red[TELL_PS - 1][TELL_LANES][4];
+    __shared__ double red[TELL_MAX_PS - 1][TELL_LANES][4];
     const int32_t r = blockIdx.y;
     const int32_t tx = threadIdx.x % TELL_LANES;
     // one wave per pair slice: make the slice index (and the pair loop) uniform
@@ -512,8 +512,8 @@ __global__ __launch_bounds__(TELL_LANES * TELL_PS) void k_tell(
     const uint32_t bb = (uint32_t)(b < nb ? b : nb - 1);
     const uint64_t key = seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
-    const int32_t pb = (int32_t)(((int64_t)P * s) / TELL_PS);
-    const int32_t pe = (int32_t)(((int64_t)P * (s + 1)) / TELL_PS);
+    const int32_t pb = (int32_t)(((int64_t)P * s) / ps);
+    const int32_t pe = (int32_t)(((int64_t)P * (s + 1)) / ps);
 
     double a64[4] = {0.0, 0.0, 0.0, 0.0};
     tell_slice<LANES_BLOCK>(wfold + (int64_t)r * P, k0, k1, bb, t, pb, pe, a64);
@@ -523,8 +523,7 @@ __global__ __launch_bounds__(TELL_LANES * TELL_PS) void k_tell(
     }
     __syncthreads();
     if (s != 0 || b >= nb) return;
-#pragma unroll
-    for (int q = 0; q < TELL_PS - 1; ++q)
+    for (int q = 0; q < ps - 1; ++q)
 #pragma unroll
         for (int k = 0; k < 4; ++k) a64[k] += red[q][tx][k];
 
@@ -577,6 +576,7 @@ struct FusedArgs {
     int64_t D, nb;
     int32_t N, P, R;
     int64_t bc, nchunks;
+    int32_t ps;
     float sigma, ra;
     double add, inv_ns;
     int32_t maximize, raw;
@@ -589,8 +589,8 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
     const int32_t r = blockIdx.x;
     const int64_t Dp = 4 * a.nb;
     // LDS layout: tell slices (fp64) | m | m1 | v | partial | fit | y | wf | keys | best
-    double* red = smem;                                  // [TELL_PS][nb][4]
-    float* ms = reinterpret_cast<float*>(red + (int64_t)TELL_PS * a.nb * 4);
+    double* red = smem;                                  // [ps][nb][4]
+    float* ms = reinterpret_cast<float*>(red + (int64_t)a.ps * a.nb * 4);
     float* m1s = ms + Dp;
     float* vs = m1s + Dp;
     float* part = vs + Dp;                               // [nchunks][N]
@@ -660,11 +660,11 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         __syncthreads();
         // tell: items (block, pair slice), slices summed in order, then Adam
         const AdamConsts ac = a.adam[it];
-        for (int64_t i = threadIdx.x; i < (int64_t)TELL_PS * a.nb; i += blockDim.x) {
+        for (int64_t i = threadIdx.x; i < (int64_t)a.ps * a.nb; i += blockDim.x) {
             const int32_t s = (int32_t)(i / a.nb);
             const int64_t b = i - (int64_t)s * a.nb;
-            const int32_t pb = (int32_t)(((int64_t)a.P * s) / TELL_PS);
-            const int32_t pe = (int32_t)(((int64_t)a.P * (s + 1)) / TELL_PS);
+            const int32_t pb = (int32_t)(((int64_t)a.P * s) / a.ps);
+            const int32_t pe = (int32_t)(((int64_t)a.P * (s + 1)) / a.ps);
             double a64[4] = {0.0, 0.0, 0.0, 0.0};
             tell_slice<LANES_BLOCK_AND_ROW>(wf, k0, k1, (uint32_t)b, t, pb, pe, a64);
 #pragma unroll
@@ -678,7 +678,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             for (int k = 0; k < 4; ++k) {
                 a64[k] = red[b * 4 + k];
 #pragma unroll
-                for (int q = 1; q < TELL_PS; ++q) a64[k] += red[((int64_t)q * a.nb + b) * 4 + k];
+                for (int q = 1; q < a.ps; ++q) a64[k] += red[((int64_t)q * a.nb + b) * 4 + k];
             }
             float mo[4], m1o[4], vo[4], mn[4], m1n[4], vn[4], gg[4];
 #pragma unroll
@@ -837,15 +837,27 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, uint32_t t, const 
                        double inv_ns, const float* wfold, const int32_t* best_j, float* m,
                        float* m1, float* v, float* grad, float* best_x, hipStream_t s)
 {
+    const int32_t ps = tell_slices(g);
     const dim3 grid((unsigned)((g.nb + TELL_LANES - 1) / TELL_LANES), (unsigned)g.R);
-    k_tell<<<grid, TELL_LANES * TELL_PS, 0, s>>>(wfold, best_j, m, m1, v, grad, best_x, c.seed, t, g.D, g.nb,
-                                                 g.P, c.sigma, inv_ns, a);
+    k_tell<<<grid, TELL_LANES * ps, 0, s>>>(wfold, best_j, m, m1, v, grad, best_x, c.seed, t, g.D, g.nb, g.P, ps,
+                                            c.sigma, inv_ns, a);
     return hipGetLastError();
+}
+
+int32_t tell_slices(const Geometry& g)
+{
+    // about 4096 waves over the launch, at least 4 slices, at most one per pair
+    const int64_t groups = (g.nb + TELL_LANES - 1) / TELL_LANES * g.R;
+    int64_t ps = (4096 + groups - 1) / groups;
+    if (ps < 4) ps = 4;
+    if (ps > TELL_MAX_PS) ps = TELL_MAX_PS;
+    if (ps > g.P) ps = g.P;
+    return (int32_t)ps;
 }
 
 size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e)
 {
-    const size_t red = sizeof(double) * (size_t)TELL_PS * g.nb * 4;
+    const size_t red = sizeof(double) * (size_t)tell_slices(g) * g.nb * 4;
     const size_t f32 = sizeof(float) * (size_t)(3 * g.Dp + e.nchunks * g.N + 2 * g.N + g.P + g.N);
     return red + f32;
 }
@@ -865,7 +877,7 @@ hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPla
     a.m = m; a.m1 = m1; a.v = v; a.best_x = best_x; a.best_okey = best_okey; a.best_f = best_f;
     a.pdata = pdata; a.table = table; a.adam = adam; a.log = log;
     a.seed = c.seed; a.t0 = t0; a.T = T; a.D = g.D; a.nb = g.nb; a.N = g.N; a.P = g.P; a.R = g.R;
-    a.bc = e.bc; a.nchunks = e.nchunks; a.sigma = c.sigma; a.ra = c.rastrigin_a;
+    a.bc = e.bc; a.nchunks = e.nchunks; a.ps = tell_slices(g); a.sigma = c.sigma; a.ra = c.rastrigin_a;
     a.add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;
     a.inv_ns = 1.0 / ((double)g.N * (double)c.sigma);
     a.maximize = c.maximize; a.raw = c.shaping == ES_SHAPE_RAW;

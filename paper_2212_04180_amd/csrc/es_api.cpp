@@ -336,6 +336,7 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     std::free(tab); std::free(ok); std::free(bf);
     if (e == hipSuccess) e = launch_init(g, *cfg, h->m, h->m1, h->v, h->best_x, h->stream);
     if (e == hipSuccess && h->pdata) e = launch_problem_data(g, *cfg, h->pdata, h->stream);
+    if (e == hipSuccess && h->mlp_scratch) e = launch_mlp_setup(h->pdata, h->mlp_scratch, h->stream);
     if (e != hipSuccess) {
         free_all(h);
         delete h;

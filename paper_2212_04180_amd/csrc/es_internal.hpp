@@ -69,7 +69,8 @@ hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPla
 
 // Neuroevolution problem (64-256-256-16 MLP vs a teacher).
 constexpr int64_t MLP_NUM_PARAMS = 86544;
-size_t mlp_scratch_bytes();  // X_t (fp32 and bf16) and teacher outputs
+size_t mlp_scratch_bytes();  // X_t (fp32 and bf16), teacher outputs, transposed teacher
+hipError_t launch_mlp_setup(const float* teacher, void* scratch, hipStream_t s);
 size_t mlp_lds_bytes();
 hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, const float* m, const float* teacher,
                            void* scratch, float* fit, hipStream_t s);

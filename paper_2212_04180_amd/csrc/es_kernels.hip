@@ -442,10 +442,17 @@ __device__ __forceinline__ void tell_slice(const float* __restrict__ wr, uint32_
                                            uint32_t t, int32_t pb, int32_t pe, double a64[4])
 {
     int32_t p0 = pb;
-    for (; p0 + TELL_GROUP <= pe; p0 += TELL_GROUP) {
-        float wv[TELL_GROUP];
+    float wv[TELL_GROUP];
+    if (p0 + TELL_GROUP <= pe) {
 #pragma unroll
         for (int q = 0; q < TELL_GROUP; ++q) wv[q] = wr[p0 + q];
+    }
+    for (; p0 + TELL_GROUP <= pe; p0 += TELL_GROUP) {
+        // fetch the next group's weights while this group's noise is generated
+        float wn[TELL_GROUP];
+        const int32_t pn = p0 + 2 * TELL_GROUP <= pe ? p0 + TELL_GROUP : p0;  // stays in bounds
+#pragma unroll
+        for (int q = 0; q < TELL_GROUP; ++q) wn[q] = wr[pn + q];
         float a32[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int q = 0; q < TELL_GROUP; ++q) {
@@ -456,6 +463,8 @@ __device__ __forceinline__ void tell_slice(const float* __restrict__ wr, uint32_
         }
 #pragma unroll
         for (int k = 0; k < 4; ++k) a64[k] += (double)a32[k];
+#pragma unroll
+        for (int q = 0; q < TELL_GROUP; ++q) wv[q] = wn[q];
     }
     float a32[4] = {0.f, 0.f, 0.f, 0.f};
     for (int32_t p = p0; p < pe; ++p) {
@@ -852,6 +861,9 @@ int32_t tell_slices(const Geometry& g)
     if (ps < 4) ps = 4;
     if (ps > TELL_MAX_PS) ps = TELL_MAX_PS;
     if (ps > g.P) ps = g.P;
+    // round up to a slice count that splits the pairs into whole groups
+    for (int64_t q = ps; q <= TELL_MAX_PS && q <= g.P; ++q)
+        if (g.P % q == 0 && (g.P / q) % TELL_GROUP == 0) return (int32_t)q;
     return (int32_t)ps;
 }
 

@@ -3,9 +3,9 @@
 // parameter reshaping, Sec. 3.2 of the evosax report), scored by -MSE
 // against a fixed random teacher network of the same shape.
 //
-//   k_mlp_inputs   X_t [256][64] ~ N(0,1) from the EVAL stream of the base
-//                  seed: fp32 for the teacher, bf16 for the students
-//   k_mlp_teacher  fp32 teacher forward on X_t -> Y_T [256][16]
+//   k_mlp_teacher  X_t [256][64] ~ N(0,1) from the EVAL stream of the base
+//                  seed (fp32 for the teacher, bf16 for the students) and
+//                  the fp32 teacher forward on it -> Y_T [256][16]
 //   k_eval_mlp     one workgroup per antithetic pair: the pair's noise is
 //                  regenerated once and turned into both members' weights
 //                  (bf16(m +- sigma*eps), biases fp32) in LDS; the forward
@@ -41,20 +41,32 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int MLP_IN = 64, MLP_H = 256, MLP_OUT = 16, MLP_BATCH = 256;
 constexpr int64_t OFF_W1 = 0, OFF_B1 = 16384, OFF_W2 = 16640, OFF_B2 = 82176, OFF_W3 = 82432, OFF_B3 = 86528;
-constexpr int MLP_WAVES = 8;           // 8 x 32 batch columns = 256 inputs
+constexpr int MLP_WAVES = 16;          // per member: 8 waves x 32 batch columns = 256 inputs
 constexpr int MLP_THREADS = 64 * MLP_WAVES;
-constexpr int W2_ROWS = 64;            // W2 rows generated per LDS round
-// LDS row strides (bf16 elements), padded against bank conflicts
+constexpr int W2_ROWS = 32;            // W2 rows per LDS chunk (one K-step of layer 3)
+constexpr int W2_CHUNKS = MLP_H / W2_ROWS;
+constexpr int W2_BLOCKS_PER_THREAD = W2_ROWS * MLP_H / 4 / MLP_THREADS;  // Philox blocks per lane per chunk
+static_assert(W2_BLOCKS_PER_THREAD * MLP_THREADS * 4 == W2_ROWS * MLP_H, "W2 chunk must split evenly");
+static_assert(8 % W2_BLOCKS_PER_THREAD == 0, "generation steps must divide the K loop");
+// LDS row strides (bf16 elements), padded so that the A-operand reads of a
+// 16-lane group hit distinct banks
 constexpr int W1S = MLP_IN + 8;        // W1 tile [256][64]
-constexpr int W2S = MLP_H + 8;         // W2 chunk [64][256]
-constexpr int W3S = MLP_H + 8;         // W3 [16][256]
-constexpr int WTILE = (MLP_H * W1S > W2_ROWS * W2S) ? MLP_H * W1S : W2_ROWS * W2S;
+constexpr int W2S = MLP_H + 4;         // W2 chunk [32][256]
+constexpr int W3S = MLP_H + 4;         // W3 [16][256]
+constexpr int W1_TILE = MLP_H * W1S;
+constexpr int W2_TILE = W2_ROWS * W2S;
 
+// The W1 tiles are dead once layer 1 is done, so the second W2 chunk buffer
+// reuses their space.
 struct MlpSmem {
-    __bf16 w[2][WTILE];            // member +, member -: W1 or the current W2 chunk
+    union {
+        __bf16 w1[2][W1_TILE];     // member +, member -
+        __bf16 w2b[2][W2_TILE];    // W2 chunk buffer 1
+    } a;
+    __bf16 w2a[2][W2_TILE];        // W2 chunk buffer 0
     __bf16 w3[2][MLP_OUT * W3S];
     float b1[2][MLP_H], b2[2][MLP_H], b3[2][MLP_OUT];
-    double red[MLP_WAVES][2];
+    double red[MLP_WAVES];
 };
 
 // tanh x = 1 - 2 / (e^{2x} + 1): v_exp_f32 and v_rcp_f32, saturating to +-1.
@@ -72,10 +84,8 @@ __device__ __forceinline__ void gen_weights(const float* __restrict__ mr, uint32
                                             __bf16* wm, int ld)
 {
     const int nblk = rows * cols / 4;
-    for (int i = threadIdx.x; i < nblk; i += blockDim.x) {
+    auto one = [&](int i, const float e[4]) {
         const int64_t b = off / 4 + i;
-        float e[4];
-        box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)b, pair, t, DOM_NOISE), e);
         const float4 m4 = *reinterpret_cast<const float4*>(mr + 4 * b);
         const float mv[4] = {m4.x, m4.y, m4.z, m4.w};
         bf16x4 vp, vm;
@@ -87,6 +97,24 @@ __device__ __forceinline__ void gen_weights(const float* __restrict__ mr, uint32
         const int row = (4 * i) / cols, col = (4 * i) % cols;
         *reinterpret_cast<bf16x4*>(wp + row * ld + col) = vp;
         *reinterpret_cast<bf16x4*>(wm + row * ld + col) = vm;
+    };
+    const int step = (int)blockDim.x;
+    int i = threadIdx.x;
+    // two independent Philox chains in flight per lane (latency hiding at
+    // two waves per SIMD)
+    for (; i + step < nblk; i += 2 * step) {
+        float e0[4], e1[4];
+        const uint4 w0 = philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)(off / 4 + i), pair, t, DOM_NOISE);
+        const uint4 w1 = philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)(off / 4 + i + step), pair, t, DOM_NOISE);
+        box_muller4(w0, e0);
+        box_muller4(w1, e1);
+        one(i, e0);
+        one(i + step, e1);
+    }
+    if (i < nblk) {
+        float e[4];
+        box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)(off / 4 + i), pair, t, DOM_NOISE), e);
+        one(i, e);
     }
 }
 
@@ -130,6 +158,66 @@ __device__ __forceinline__ bf16x8 activate(const floatx4& lo, const floatx4& hi,
     return h;
 }
 
+// One Philox block (4 weights) of W2 chunk `chunk` into the chunk buffers.
+__device__ __forceinline__ void gen_w2_block(const float* __restrict__ mr, uint32_t k0, uint32_t k1, uint32_t pair,
+                                             uint32_t t, int chunk, int i, float sigma, __bf16* wp, __bf16* wm)
+{
+    const int64_t b = (OFF_W2 + (int64_t)chunk * W2_ROWS * MLP_H) / 4 + i;
+    float e[4];
+    box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)b, pair, t, DOM_NOISE), e);
+    const float4 m4 = *reinterpret_cast<const float4*>(mr + 4 * b);
+    const float mv[4] = {m4.x, m4.y, m4.z, m4.w};
+    bf16x4 vp, vm;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        vp[k] = (__bf16)fmaf(sigma, e[k], mv[k]);
+        vm[k] = (__bf16)fmaf(-sigma, e[k], mv[k]);
+    }
+    const int row = (4 * i) / MLP_H, col = (4 * i) % MLP_H;
+    *reinterpret_cast<bf16x4*>(wp + row * W2S + col) = vp;
+    *reinterpret_cast<bf16x4*>(wm + row * W2S + col) = vm;
+}
+
+// Layer 2 on one W2 chunk (rows [W2_ROWS*c, +W2_ROWS)) for this wave's
+// member: acc = W2[chunk] . H1^T.
+__device__ __forceinline__ void layer2_mfma(const __bf16* wc, const bf16x8 (&h1)[8][2], floatx4 (&acc)[2][2], int q,
+                                            int l16)
+{
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int g = 0; g < 8; ++g)
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) {
+            const __bf16* row = wc + (16 * mt + l16) * W2S + 32 * g;
+            const bf16x8 A = cat(*reinterpret_cast<const bf16x4*>(row + 4 * q),
+                                 *reinterpret_cast<const bf16x4*>(row + 16 + 4 * q));
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt)
+                acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, h1[g][nt], acc[mt][nt], 0, 0, 0);
+        }
+}
+
+// Bias + tanh + bf16 of the chunk's layer-2 rows, then that chunk's share of
+// layer 3 (the chunk's rows are layer 3's K range).
+__device__ __forceinline__ void layer2_act(const MlpSmem& S, const floatx4 (&acc)[2][2], int c, int mem,
+                                           floatx4 (&y)[2], int q, int l16)
+{
+    const int r0 = W2_ROWS * c;
+    const __bf16* w3row = S.w3[mem] + l16 * W3S + r0;
+    const bf16x8 A3 = cat(*reinterpret_cast<const bf16x4*>(w3row + 4 * q),
+                          *reinterpret_cast<const bf16x4*>(w3row + 16 + 4 * q));
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+        const bf16x8 hb = activate(acc[0][nt], acc[1][nt], S.b2[mem], r0, q);
+        y[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A3, hb, y[nt], 0, 0, 0);
+    }
+}
+
+// One workgroup per antithetic pair: waves 0-7 evaluate member p (+eps),
+// waves 8-15 member p + N/2 (-eps); each wave owns 32 batch columns.
 __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restrict__ m, const __bf16* __restrict__ xb,
                                                           const float* __restrict__ yt, float* __restrict__ fit,
                                                           uint64_t seed, uint32_t t, int64_t Dp, int32_t N,
@@ -139,17 +227,19 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
     MlpSmem& S = *reinterpret_cast<MlpSmem*>(smem_raw);
     const int32_t p = blockIdx.x, r = blockIdx.y;
     const int wave = threadIdx.x / 64, lane = threadIdx.x % 64, q = lane / 16, l16 = lane % 16;
+    const int mem = wave / 8;                 // 0: +eps, 1: -eps
+    const int nbase = 32 * (wave % 8);        // this wave's batch columns
     const uint64_t key = seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
     const float* __restrict__ mr = m + (int64_t)r * Dp;
-    const int nbase = 32 * wave;  // this wave's batch columns
 
     // ---- layer 1 weights, all biases, layer 3 weights
-    gen_weights(mr, k0, k1, (uint32_t)p, t, OFF_W1, MLP_H, MLP_IN, sigma, S.w[0], S.w[1], W1S);
+    gen_weights(mr, k0, k1, (uint32_t)p, t, OFF_W1, MLP_H, MLP_IN, sigma, S.a.w1[0], S.a.w1[1], W1S);
     gen_weights(mr, k0, k1, (uint32_t)p, t, OFF_W3, MLP_OUT, MLP_H, sigma, S.w3[0], S.w3[1], W3S);
     gen_bias(mr, k0, k1, (uint32_t)p, t, OFF_B1, MLP_H, sigma, S.b1[0], S.b1[1]);
     gen_bias(mr, k0, k1, (uint32_t)p, t, OFF_B2, MLP_H, sigma, S.b2[0], S.b2[1]);
     gen_bias(mr, k0, k1, (uint32_t)p, t, OFF_B3, MLP_OUT, sigma, S.b3[0], S.b3[1]);
+    gen_weights(mr, k0, k1, (uint32_t)p, t, OFF_W2, W2_ROWS, MLP_H, sigma, S.w2a[0], S.w2a[1], W2S);  // chunk 0
 
     // input B operands: X[n][32ks + 8q + i] for batch column n of tile nt
     bf16x8 xop[2][2];
@@ -160,148 +250,137 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
             xop[ks][nt] = *reinterpret_cast<const bf16x8*>(xb + (nbase + 16 * nt + l16) * MLP_IN + 32 * ks + 8 * q);
     __syncthreads();
 
-    // ---- layer 1: H1^T (256 x 32) per member, kept as layer-2 B operands
-    bf16x8 h1[2][8][2];
+    // ---- layer 1: H1^T (256 x 32), kept as layer-2 B operands
+    bf16x8 h1[8][2];
+    const __bf16* W1 = S.a.w1[mem];
 #pragma unroll
-    for (int mem = 0; mem < 2; ++mem) {
-        const __bf16* W = S.w[mem];
+    for (int g = 0; g < 8; ++g) {
+        floatx4 cc[2][2];
 #pragma unroll
-        for (int g = 0; g < 8; ++g) {
-            floatx4 c[2][2];
+        for (int a = 0; a < 2; ++a)
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
+            for (int nt = 0; nt < 2; ++nt) cc[a][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int nt = 0; nt < 2; ++nt) c[a][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int a = 0; a < 2; ++a)
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
+            for (int ks = 0; ks < 2; ++ks) {
+                const bf16x8 A = *reinterpret_cast<const bf16x8*>(W1 + (32 * g + 16 * a + l16) * W1S + 32 * ks + 8 * q);
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    const bf16x8 A = *reinterpret_cast<const bf16x8*>(W + (32 * g + 16 * a + l16) * W1S + 32 * ks + 8 * q);
-#pragma unroll
-                    for (int nt = 0; nt < 2; ++nt)
-                        c[a][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, xop[ks][nt], c[a][nt], 0, 0, 0);
-                }
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt) h1[mem][g][nt] = activate(c[0][nt], c[1][nt], S.b1[mem], 32 * g, q);
-        }
-    }
-    __syncthreads();  // W1 tiles are reused for W2
-
-    // ---- layer 2 in chunks of W2_ROWS output rows, each followed by its
-    // share of layer 3 (the chunk's rows are layer 3's K range)
-    floatx4 y[2][2];
-#pragma unroll
-    for (int mem = 0; mem < 2; ++mem)
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) y[mem][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < MLP_H / W2_ROWS; ++c) {
-        gen_weights(mr, k0, k1, (uint32_t)p, t, OFF_W2 + (int64_t)c * W2_ROWS * MLP_H, W2_ROWS, MLP_H, sigma, S.w[0],
-                    S.w[1], W2S);
-        __syncthreads();
-#pragma unroll
-        for (int mem = 0; mem < 2; ++mem) {
-            const __bf16* W = S.w[mem];
-            floatx4 acc[4][2];
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-                for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int g = 0; g < 8; ++g)
-#pragma unroll
-                for (int mt = 0; mt < 4; ++mt) {
-                    const __bf16* row = W + (16 * mt + l16) * W2S + 32 * g;
-                    const bf16x8 A = cat(*reinterpret_cast<const bf16x4*>(row + 4 * q),
-                                         *reinterpret_cast<const bf16x4*>(row + 16 + 4 * q));
-#pragma unroll
-                    for (int nt = 0; nt < 2; ++nt)
-                        acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, h1[mem][g][nt], acc[mt][nt], 0, 0, 0);
-                }
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int r0 = W2_ROWS * c + 32 * h;  // layer-2 output rows = layer-3 K range
-                const __bf16* w3row = S.w3[mem] + l16 * W3S + r0;
-                const bf16x8 A3 = cat(*reinterpret_cast<const bf16x4*>(w3row + 4 * q),
-                                      *reinterpret_cast<const bf16x4*>(w3row + 16 + 4 * q));
-#pragma unroll
-                for (int nt = 0; nt < 2; ++nt) {
-                    const bf16x8 hb = activate(acc[2 * h][nt], acc[2 * h + 1][nt], S.b2[mem], r0, q);
-                    y[mem][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A3, hb, y[mem][nt], 0, 0, 0);
-                }
+                for (int nt = 0; nt < 2; ++nt)
+                    cc[a][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, xop[ks][nt], cc[a][nt], 0, 0, 0);
             }
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) h1[g][nt] = activate(cc[0][nt], cc[1][nt], S.b1[mem], 32 * g, q);
+    }
+    __syncthreads();  // W1 is dead from here on; its space holds chunk buffer 1
+
+    // ---- layer 2 chunk by chunk, generating the next chunk meanwhile
+    floatx4 y[2] = {floatx4{0.f, 0.f, 0.f, 0.f}, floatx4{0.f, 0.f, 0.f, 0.f}};
+    for (int c = 0; c < W2_CHUNKS; ++c) {
+        // Even chunks live in buffer 0, odd ones in buffer 1.  Each lane also
+        // generates its share of chunk c+1 into the other buffer: the waves of
+        // member + do that before their matrix work, those of member - after
+        // it, so that every SIMD has VALU and MFMA work in flight together.
+        __bf16* nb_p = (c & 1) ? S.w2a[0] : S.a.w2b[0];
+        __bf16* nb_m = (c & 1) ? S.w2a[1] : S.a.w2b[1];
+        const __bf16* wc = (c & 1) ? S.a.w2b[mem] : S.w2a[mem];
+        const bool gen = c + 1 < W2_CHUNKS;
+        if (mem == 0 && gen)
+            for (int j = 0; j < W2_BLOCKS_PER_THREAD; ++j)
+                gen_w2_block(mr, k0, k1, (uint32_t)p, t, c + 1, (int)threadIdx.x + j * MLP_THREADS, sigma, nb_p, nb_m);
+        {
+            floatx4 acc[2][2];
+            layer2_mfma(wc, h1, acc, q, l16);
+            layer2_act(S, acc, c, mem, y, q, l16);
         }
-        __syncthreads();  // before the next chunk overwrites the tiles
+        if (mem == 1 && gen)
+            for (int j = 0; j < W2_BLOCKS_PER_THREAD; ++j)
+                gen_w2_block(mr, k0, k1, (uint32_t)p, t, c + 1, (int)threadIdx.x + j * MLP_THREADS, sigma, nb_p, nb_m);
+        __syncthreads();
     }
 
     // ---- output layer bias, squared error against the teacher
-    double se[2] = {0.0, 0.0};
+    double se = 0.0;
 #pragma unroll
-    for (int mem = 0; mem < 2; ++mem)
+    for (int nt = 0; nt < 2; ++nt) {
+        const int n = nbase + 16 * nt + l16;
+        float sq = 0.f;
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-            const int n = nbase + 16 * nt + l16;
-            float s = 0.f;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int o = 4 * q + i;
-                float v = y[mem][nt][i] + S.b3[mem][o];
-                if (tanh_out) v = tanh_fast(v);
-                const float d = v - yt[n * MLP_OUT + o];
-                s = fmaf(d, d, s);
-            }
-            se[mem] += (double)s;
+        for (int i = 0; i < 4; ++i) {
+            const int o = 4 * q + i;
+            float v = y[nt][i] + S.b3[mem][o];
+            if (tanh_out) v = tanh_fast(v);
+            const float d = v - yt[n * MLP_OUT + o];
+            sq = fmaf(d, d, sq);
         }
-#pragma unroll
-    for (int mem = 0; mem < 2; ++mem)
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) se[mem] += __shfl_xor(se[mem], off);
-    if (lane == 0) {
-        S.red[wave][0] = se[0];
-        S.red[wave][1] = se[1];
+        se += (double)sq;
     }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) se += __shfl_xor(se, off);
+    if (lane == 0) S.red[wave] = se;
     __syncthreads();
     if (threadIdx.x < 2) {
         double tot = 0.0;
-        for (int w = 0; w < MLP_WAVES; ++w) tot += S.red[w][threadIdx.x];
+        for (int w = 0; w < 8; ++w) tot += S.red[8 * threadIdx.x + w];
         const double mse = tot / (double)(MLP_BATCH * MLP_OUT);
         fit[(int64_t)r * N + p + (threadIdx.x ? P : 0)] = (float)(-mse);
     }
 }
 
-// X_t: 256 x 64 normals from the EVAL stream (row 0, counter block = flat/4).
-__global__ void k_mlp_inputs(float* __restrict__ xf, __bf16* __restrict__ xb, uint64_t seed, uint32_t t)
+// The teacher's weights transposed once at set-up: W1^T [64][256],
+// W2^T [256][256], W3^T [256][16] (the biases are not copied), so that the
+// per-generation forward reads them coalesced.
+__global__ void k_mlp_transpose(const float* __restrict__ w, float* __restrict__ wt)
 {
-    const int b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= MLP_BATCH * MLP_IN / 4) return;
-    float e[4];
-    normals4(seed, (uint32_t)b, 0, t, DOM_EVAL, e);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        xf[4 * b + k] = e[k];
-        xb[4 * b + k] = (__bf16)e[k];
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;  // destination index
+    if (i < MLP_IN * MLP_H) {
+        const int k = i / MLP_H, o = i % MLP_H;
+        wt[OFF_W1 + i] = w[OFF_W1 + o * MLP_IN + k];
+    } else if (i < MLP_IN * MLP_H + MLP_H * MLP_H) {
+        const int j = i - MLP_IN * MLP_H, k = j / MLP_H, o = j % MLP_H;
+        wt[OFF_W2 + j] = w[OFF_W2 + o * MLP_H + k];
+    } else if (i < MLP_IN * MLP_H + MLP_H * MLP_H + MLP_H * MLP_OUT) {
+        const int j = i - MLP_IN * MLP_H - MLP_H * MLP_H, k = j / MLP_OUT, o = j % MLP_OUT;
+        wt[OFF_W3 + j] = w[OFF_W3 + o * MLP_H + k];
     }
 }
 
-// Teacher forward in fp32: one workgroup per input row, one thread per
-// hidden unit; Y_T[n][o].
-__global__ __launch_bounds__(MLP_H) void k_mlp_teacher(const float* __restrict__ w, const float* __restrict__ xf,
-                                                       float* __restrict__ yt, int32_t tanh_out)
+// Per generation: input row n of X_t (64 normals from the EVAL stream of the
+// base seed, counter block = flat index / 4) in fp32 and bf16, and the fp32
+// teacher forward of that row -> Y_T[n][:].  One workgroup per input row, one
+// thread per hidden unit, sequential fp32 sums over the inputs.
+__global__ __launch_bounds__(MLP_H) void k_mlp_teacher(const float* __restrict__ w, const float* __restrict__ wt,
+                                                       float* __restrict__ xf, __bf16* __restrict__ xb,
+                                                       float* __restrict__ yt, uint64_t seed, uint32_t t,
+                                                       int32_t tanh_out)
 {
     __shared__ float x[MLP_IN], h1[MLP_H], h2[MLP_H];
     const int n = blockIdx.x, o = threadIdx.x;
-    if (o < MLP_IN) x[o] = xf[n * MLP_IN + o];
+    if (o < MLP_IN / 4) {
+        float e[4];
+        normals4(seed, (uint32_t)(n * (MLP_IN / 4) + o), 0, t, DOM_EVAL, e);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            x[4 * o + k] = e[k];
+            xf[n * MLP_IN + 4 * o + k] = e[k];
+            xb[n * MLP_IN + 4 * o + k] = (__bf16)e[k];
+        }
+    }
     __syncthreads();
     float a = 0.f;
-    for (int k = 0; k < MLP_IN; ++k) a = fmaf(x[k], w[OFF_W1 + o * MLP_IN + k], a);
+#pragma unroll 8
+    for (int k = 0; k < MLP_IN; ++k) a = fmaf(x[k], wt[OFF_W1 + k * MLP_H + o], a);
     h1[o] = tanhf(a + w[OFF_B1 + o]);
     __syncthreads();
     a = 0.f;
-    for (int k = 0; k < MLP_H; ++k) a = fmaf(h1[k], w[OFF_W2 + o * MLP_H + k], a);
+#pragma unroll 8
+    for (int k = 0; k < MLP_H; ++k) a = fmaf(h1[k], wt[OFF_W2 + k * MLP_H + o], a);
     h2[o] = tanhf(a + w[OFF_B2 + o]);
     __syncthreads();
     if (o < MLP_OUT) {
         a = 0.f;
-        for (int k = 0; k < MLP_H; ++k) a = fmaf(h2[k], w[OFF_W3 + o * MLP_H + k], a);
+#pragma unroll 8
+        for (int k = 0; k < MLP_H; ++k) a = fmaf(h2[k], wt[OFF_W3 + k * MLP_OUT + o], a);
         a += w[OFF_B3 + o];
         yt[n * MLP_OUT + o] = tanh_out ? tanhf(a) : a;
     }
@@ -311,7 +390,17 @@ __global__ __launch_bounds__(MLP_H) void k_mlp_teacher(const float* __restrict__
 
 size_t mlp_scratch_bytes()
 {
-    return sizeof(float) * MLP_BATCH * MLP_IN + sizeof(__bf16) * MLP_BATCH * MLP_IN + sizeof(float) * MLP_BATCH * MLP_OUT;
+    // X_t fp32, X_t bf16, Y_T, transposed teacher
+    return sizeof(float) * MLP_BATCH * MLP_IN + sizeof(__bf16) * MLP_BATCH * MLP_IN + sizeof(float) * MLP_BATCH * MLP_OUT +
+           sizeof(float) * MLP_NUM_PARAMS;
+}
+
+hipError_t launch_mlp_setup(const float* teacher, void* scratch, hipStream_t s)
+{
+    float* wt = reinterpret_cast<float*>(static_cast<char*>(scratch) + mlp_scratch_bytes() - sizeof(float) * MLP_NUM_PARAMS);
+    const int n = MLP_IN * MLP_H + MLP_H * MLP_H + MLP_H * MLP_OUT;
+    k_mlp_transpose<<<(n + 255) / 256, 256, 0, s>>>(teacher, wt);
+    return hipGetLastError();
 }
 
 size_t mlp_lds_bytes() { return sizeof(MlpSmem); }
@@ -322,11 +411,10 @@ hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, co
     float* xf = static_cast<float*>(scratch);
     __bf16* xb = reinterpret_cast<__bf16*>(xf + MLP_BATCH * MLP_IN);
     float* yt = reinterpret_cast<float*>(xb + MLP_BATCH * MLP_IN);
-    k_mlp_inputs<<<(MLP_BATCH * MLP_IN / 4 + 255) / 256, 256, 0, s>>>(xf, xb, c.seed, t);
+    const float* wt = reinterpret_cast<const float*>(static_cast<const char*>(scratch) + mlp_scratch_bytes() -
+                                                     sizeof(float) * MLP_NUM_PARAMS);
+    k_mlp_teacher<<<MLP_BATCH, MLP_H, 0, s>>>(teacher, wt, xf, xb, yt, c.seed, t, c.mlp_tanh_out);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    k_mlp_teacher<<<MLP_BATCH, MLP_H, 0, s>>>(teacher, xf, yt, c.mlp_tanh_out);
-    e = hipGetLastError();
     if (e != hipSuccess) return e;
     static bool lds_attr_set = false;  // more than 64 KB of LDS per workgroup
     if (!lds_attr_set) {

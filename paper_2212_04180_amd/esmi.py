@@ -14,7 +14,8 @@ from dataclasses import dataclass, fields
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libesmi.so")
+# ESMI_LIB may point at another build of the same library (A/B timing)
+LIB_PATH = os.environ.get("ESMI_LIB") or os.path.join(_PKG, "libesmi.so")
 
 ES_OK, ES_ERR_ARG, ES_ERR_SEQUENCE, ES_ERR_HIP, ES_ERR_OOM, ES_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 SHAPE_CENTERED_RANK, SHAPE_RAW = 0, 1

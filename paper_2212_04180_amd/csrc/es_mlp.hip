@@ -347,42 +347,71 @@ __global__ void k_mlp_transpose(const float* __restrict__ w, float* __restrict__
 
 // Per generation: input row n of X_t (64 normals from the EVAL stream of the
 // base seed, counter block = flat index / 4) in fp32 and bf16, and the fp32
-// teacher forward of that row -> Y_T[n][:].  One workgroup per input row, one
-// thread per hidden unit, sequential fp32 sums over the inputs.
-__global__ __launch_bounds__(MLP_H) void k_mlp_teacher(const float* __restrict__ w, const float* __restrict__ wt,
-                                                       float* __restrict__ xf, __bf16* __restrict__ xb,
-                                                       float* __restrict__ yt, uint64_t seed, uint32_t t,
-                                                       int32_t tanh_out)
+// teacher forward on it -> Y_T[n][:].  One workgroup per input row; each
+// layer's inner sum is split into TEACHER_SLICES contiguous K ranges (one per
+// group of 256 threads, coalesced reads of the transposed weights) whose fp32
+// partials are added in slice order.
+constexpr int TEACHER_SLICES = 4;
+constexpr int TEACHER_THREADS = TEACHER_SLICES * MLP_H;
+constexpr int L3_SLICES = TEACHER_THREADS / MLP_OUT;  // layer 3: 64 K ranges of 4
+
+__global__ __launch_bounds__(TEACHER_THREADS) void k_mlp_teacher(const float* __restrict__ w,
+                                                                 const float* __restrict__ wt,
+                                                                 float* __restrict__ xf, __bf16* __restrict__ xb,
+                                                                 float* __restrict__ yt, uint64_t seed, uint32_t t,
+                                                                 int32_t tanh_out)
 {
-    __shared__ float x[MLP_IN], h1[MLP_H], h2[MLP_H];
-    const int n = blockIdx.x, o = threadIdx.x;
-    if (o < MLP_IN / 4) {
+    __shared__ float x[MLP_IN], h1[MLP_H], h2[MLP_H], part[TEACHER_THREADS];
+    const int n = blockIdx.x, o = threadIdx.x % MLP_H, ks = threadIdx.x / MLP_H;
+    if (threadIdx.x < MLP_IN / 4) {
+        const int c4 = threadIdx.x;
         float e[4];
-        normals4(seed, (uint32_t)(n * (MLP_IN / 4) + o), 0, t, DOM_EVAL, e);
+        normals4(seed, (uint32_t)(n * (MLP_IN / 4) + c4), 0, t, DOM_EVAL, e);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            x[4 * o + k] = e[k];
-            xf[n * MLP_IN + 4 * o + k] = e[k];
-            xb[n * MLP_IN + 4 * o + k] = (__bf16)e[k];
+            x[4 * c4 + k] = e[k];
+            xf[n * MLP_IN + 4 * c4 + k] = e[k];
+            xb[n * MLP_IN + 4 * c4 + k] = (__bf16)e[k];
         }
     }
     __syncthreads();
+    constexpr int K1 = MLP_IN / TEACHER_SLICES, K2 = MLP_H / TEACHER_SLICES, K3 = MLP_H / L3_SLICES;
     float a = 0.f;
-#pragma unroll 8
-    for (int k = 0; k < MLP_IN; ++k) a = fmaf(x[k], wt[OFF_W1 + k * MLP_H + o], a);
-    h1[o] = tanhf(a + w[OFF_B1 + o]);
+#pragma unroll
+    for (int k = ks * K1; k < (ks + 1) * K1; ++k) a = fmaf(x[k], wt[OFF_W1 + k * MLP_H + o], a);
+    part[threadIdx.x] = a;
+    __syncthreads();
+    if (ks == 0) {
+        float z = part[o];
+        for (int j = 1; j < TEACHER_SLICES; ++j) z += part[j * MLP_H + o];
+        h1[o] = tanhf(z + w[OFF_B1 + o]);
+    }
     __syncthreads();
     a = 0.f;
-#pragma unroll 8
-    for (int k = 0; k < MLP_H; ++k) a = fmaf(h1[k], wt[OFF_W2 + k * MLP_H + o], a);
-    h2[o] = tanhf(a + w[OFF_B2 + o]);
+#pragma unroll 16
+    for (int k = ks * K2; k < (ks + 1) * K2; ++k) a = fmaf(h1[k], wt[OFF_W2 + k * MLP_H + o], a);
+    part[threadIdx.x] = a;
     __syncthreads();
-    if (o < MLP_OUT) {
+    if (ks == 0) {
+        float z = part[o];
+        for (int j = 1; j < TEACHER_SLICES; ++j) z += part[j * MLP_H + o];
+        h2[o] = tanhf(z + w[OFF_B2 + o]);
+    }
+    __syncthreads();
+    {
+        const int o3 = threadIdx.x % MLP_OUT, k3 = threadIdx.x / MLP_OUT;
         a = 0.f;
-#pragma unroll 8
-        for (int k = 0; k < MLP_H; ++k) a = fmaf(h2[k], wt[OFF_W3 + k * MLP_OUT + o], a);
-        a += w[OFF_B3 + o];
-        yt[n * MLP_OUT + o] = tanh_out ? tanhf(a) : a;
+#pragma unroll
+        for (int k = k3 * K3; k < (k3 + 1) * K3; ++k) a = fmaf(h2[k], wt[OFF_W3 + k * MLP_OUT + o3], a);
+        part[threadIdx.x] = a;
+    }
+    __syncthreads();
+    if (threadIdx.x < MLP_OUT) {
+        const int o3 = threadIdx.x;
+        float z = part[o3];
+        for (int j = 1; j < L3_SLICES; ++j) z += part[j * MLP_OUT + o3];
+        z += w[OFF_B3 + o3];
+        yt[n * MLP_OUT + o3] = tanh_out ? tanhf(z) : z;
     }
 }
 
@@ -413,7 +442,7 @@ hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, co
     float* yt = reinterpret_cast<float*>(xb + MLP_BATCH * MLP_IN);
     const float* wt = reinterpret_cast<const float*>(static_cast<const char*>(scratch) + mlp_scratch_bytes() -
                                                      sizeof(float) * MLP_NUM_PARAMS);
-    k_mlp_teacher<<<MLP_BATCH, MLP_H, 0, s>>>(teacher, wt, xf, xb, yt, c.seed, t, c.mlp_tanh_out);
+    k_mlp_teacher<<<MLP_BATCH, TEACHER_THREADS, 0, s>>>(teacher, wt, xf, xb, yt, c.seed, t, c.mlp_tanh_out);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     static bool lds_attr_set = false;  // more than 64 KB of LDS per workgroup

@@ -59,6 +59,8 @@ struct es_handle {
     float* wfold = nullptr;  // [R][P]
     float* fit = nullptr;    // [R][N] fitness scratch for es_run
     float* partial = nullptr;
+    TellPlan tell;               // pair slices of the gradient kernel
+    double* tell_part = nullptr; // per-workgroup gradient sums when tell.nsplit > 1
     float* pdata = nullptr;  // [Dp] shift vector or teacher
     void* mlp_scratch = nullptr;  // MLP inputs and teacher outputs of the current generation
     // Adam constants of the generations of one fused es_run, staged in pinned
@@ -162,7 +164,8 @@ int64_t env_i64(const char* name, int64_t dflt)
 void free_all(es_handle* h)
 {
     void* ptrs[] = {h->m, h->m1, h->v, h->best_x, h->grad, h->best_okey, h->best_f, h->best_j, h->table,
-                    h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->adam_dev, h->mlp_scratch};
+                    h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->adam_dev, h->mlp_scratch,
+                    h->tell_part};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     if (h->adam_host) (void)hipHostFree(h->adam_host);
@@ -202,8 +205,8 @@ es_status enqueue_tell(es_handle* h, const float* fitness, float* gen_best)
            "rank kernel");
     const AdamConsts a = adam_consts(h->cfg, h->t);
     const double inv_ns = 1.0 / ((double)g.N * (double)h->cfg.sigma);
-    ES_HIP(h, launch_tell(g, h->cfg, (uint32_t)h->t, a, inv_ns, h->wfold, h->best_j, h->m, h->m1, h->v,
-                          h->grad, h->best_x, h->stream),
+    ES_HIP(h, launch_tell(g, h->cfg, h->tell, (uint32_t)h->t, a, inv_ns, h->wfold, h->best_j, h->m, h->m1, h->v,
+                          h->grad, h->best_x, h->tell_part, h->stream),
            "tell kernel");
     return ES_OK;
 }
@@ -287,6 +290,9 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     g.P = cfg->popsize / 2;
     g.R = cfg->num_runs;
     h->plan = eval_plan(g, env_i64("ESMI_EVAL_BLOCKS_PER_CHUNK", 0));
+    // es_run may take the fused loop for this geometry; then the per-call
+    // gradient kernel must sum in the fused loop's order
+    h->tell = tell_plan(g, fused_supported(g, h->plan, cfg->problem), env_i64("ESMI_TELL_SPLIT", 0));
     h->run_path = (int)env_i64("ESMI_RUN_PATH", 0);
     hipError_t e = hipGetDevice(&h->device);
     const size_t rows = (size_t)g.Dp * g.R;
@@ -309,6 +315,7 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
         e = dalloc(&h->pdata, (size_t)g.Dp);
     if (e == hipSuccess && cfg->problem == ES_PROB_MLP)
         e = dalloc(reinterpret_cast<char**>(&h->mlp_scratch), mlp_scratch_bytes());
+    if (e == hipSuccess && h->tell.nsplit > 1) e = dalloc(&h->tell_part, tell_part_elems(g, h->tell));
     if (e != hipSuccess) {
         free_all(h);
         delete h;

@@ -48,9 +48,19 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
 hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* table,
                        float* y, int32_t* rank, float* wfold, uint32_t* best_okey, float* best_f,
                        int32_t* best_j, float* gen_best, hipStream_t s);
-hipError_t launch_tell(const Geometry& g, const es_config& c, uint32_t t, const AdamConsts& a,
+// Split of the gradient kernel's pairs: ps pair slices (one wave each) per
+// workgroup, nsplit workgroups per group of 64 Philox blocks.  With nsplit > 1
+// every workgroup stores its partial sums (part, fp64 [R][nsplit][nb][4]) and
+// a second kernel adds them in split order and applies Adam.
+struct TellPlan {
+    int32_t ps = 1;
+    int32_t nsplit = 1;
+};
+TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit);
+size_t tell_part_elems(const Geometry& g, const TellPlan& tp);
+hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp, uint32_t t, const AdamConsts& a,
                        double inv_ns, const float* wfold, const int32_t* best_j, float* m,
-                       float* m1, float* v, float* grad, float* best_x, hipStream_t s);
+                       float* m1, float* v, float* grad, float* best_x, double* part, hipStream_t s);
 hipError_t launch_debug_noise(const Geometry& g, const es_config& c, int32_t run, uint32_t t,
                               int32_t pair, uint32_t* words, float* eps, hipStream_t s);
 

@@ -501,41 +501,15 @@ __device__ __forceinline__ void adam_block(const double a64[4], double inv_ns, c
     }
 }
 
-// Gradient + Adam.  Workgroup = TELL_LANES Philox blocks x ps pair slices
-// (ps <= TELL_MAX_PS, chosen per geometry) of one run.  Each lane walks its slice of pairs with the folded
-// weight w_p = y_p - y_{p+N/2} (uniform across the wave), regenerating the
-// pair's normals, so g_d = sum_p w_p eps_{p,d} / (N sigma) needs no
-// cross-lane reduction; the slices meet in LDS in a fixed order.
-__global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(
-    const float* __restrict__ wfold, const int32_t* __restrict__ best_j, float* __restrict__ m,
-    float* __restrict__ m1, float* __restrict__ v, float* __restrict__ grad,
-    float* __restrict__ best_x, uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t P, int32_t ps,
-    float sigma, double inv_ns, AdamConsts ac)
+// Adam step of one Philox block from its gradient sum, the best member's
+// parameters when the generation improved on the best so far, and the
+// gradient itself when asked for.
+__device__ __forceinline__ void tell_finish(const double a64[4], int64_t b, int32_t r, uint32_t k0, uint32_t k1,
+                                            uint32_t t, int64_t D, int64_t nb, int32_t P, float sigma, double inv_ns,
+                                            const AdamConsts& ac, const int32_t* __restrict__ best_j,
+                                            float* __restrict__ m, float* __restrict__ m1, float* __restrict__ v,
+                                            float* __restrict__ grad, float* __restrict__ best_x)
 {
-    __shared__ double red[TELL_MAX_PS - 1][TELL_LANES][4];
-    const int32_t r = blockIdx.y;
-    const int32_t tx = threadIdx.x % TELL_LANES;
-    // one wave per pair slice: make the slice index (and the pair loop) uniform
-    const int32_t s = __builtin_amdgcn_readfirstlane(threadIdx.x / TELL_LANES);
-    const int64_t b = (int64_t)blockIdx.x * TELL_LANES + tx;
-    const uint32_t bb = (uint32_t)(b < nb ? b : nb - 1);
-    const uint64_t key = seed + (uint64_t)r;
-    const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
-    const int32_t pb = (int32_t)(((int64_t)P * s) / ps);
-    const int32_t pe = (int32_t)(((int64_t)P * (s + 1)) / ps);
-
-    double a64[4] = {0.0, 0.0, 0.0, 0.0};
-    tell_slice<LANES_BLOCK>(wfold + (int64_t)r * P, k0, k1, bb, t, pb, pe, a64);
-    if (s > 0) {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) red[s - 1][tx][k] = a64[k];
-    }
-    __syncthreads();
-    if (s != 0 || b >= nb) return;
-    for (int q = 0; q < ps - 1; ++q)
-#pragma unroll
-        for (int k = 0; k < 4; ++k) a64[k] += red[q][tx][k];
-
     const int64_t off = (int64_t)r * 4 * nb + 4 * b;
     const float4 m4 = *reinterpret_cast<const float4*>(m + off);
     const float4 m14 = *reinterpret_cast<const float4*>(m1 + off);
@@ -550,7 +524,7 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(
         const int32_t pbst = jb < P ? jb : jb - P;
         const float sg = jb < P ? sigma : -sigma;
         float e[4];
-        box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, bb, (uint32_t)pbst, t, DOM_NOISE), e);
+        box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)b, (uint32_t)pbst, t, DOM_NOISE), e);
         float bx[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) bx[k] = 4 * b + k < D ? fmaf(sg, e[k], mo[k]) : 0.f;
@@ -560,6 +534,77 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(
     *reinterpret_cast<float4*>(m1 + off) = make_float4(m1n[0], m1n[1], m1n[2], m1n[3]);
     *reinterpret_cast<float4*>(v + off) = make_float4(vn[0], vn[1], vn[2], vn[3]);
     if (grad) *reinterpret_cast<float4*>(grad + off) = make_float4(gg[0], gg[1], gg[2], gg[3]);
+}
+
+// Gradient + Adam.  Workgroup = TELL_LANES Philox blocks x ps pair slices
+// (ps <= TELL_MAX_PS, chosen per geometry) of one run.  Each lane walks its
+// slice of pairs with the folded weight w_p = y_p - y_{p+N/2} (uniform across
+// the wave), regenerating the pair's normals, so g_d = sum_p w_p eps_{p,d} /
+// (N sigma) needs no cross-lane reduction; the slices meet in LDS in a fixed
+// order.  With nsplit > 1, grid.z = nsplit workgroups share a block group
+// (workgroup z takes global slices z*ps .. z*ps+ps-1 of ps*nsplit equal
+// slices of the pairs) and store their sums to part; k_tell_fold adds them in
+// split order and applies Adam.
+__global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(
+    const float* __restrict__ wfold, const int32_t* __restrict__ best_j, float* __restrict__ m,
+    float* __restrict__ m1, float* __restrict__ v, float* __restrict__ grad,
+    float* __restrict__ best_x, uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t P, int32_t ps,
+    int32_t nsplit, double* __restrict__ part, float sigma, double inv_ns, AdamConsts ac)
+{
+    __shared__ double red[TELL_MAX_PS - 1][TELL_LANES][4];
+    const int32_t r = blockIdx.y, z = blockIdx.z;
+    const int32_t tx = threadIdx.x % TELL_LANES;
+    // one wave per pair slice: make the slice index (and the pair loop) uniform
+    const int32_t s = __builtin_amdgcn_readfirstlane(threadIdx.x / TELL_LANES);
+    const int64_t b = (int64_t)blockIdx.x * TELL_LANES + tx;
+    const uint32_t bb = (uint32_t)(b < nb ? b : nb - 1);
+    const uint64_t key = seed + (uint64_t)r;
+    const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
+    const int64_t S = (int64_t)ps * nsplit, gs = (int64_t)z * ps + s;
+    const int32_t pb = (int32_t)(((int64_t)P * gs) / S);
+    const int32_t pe = (int32_t)(((int64_t)P * (gs + 1)) / S);
+
+    double a64[4] = {0.0, 0.0, 0.0, 0.0};
+    tell_slice<LANES_BLOCK>(wfold + (int64_t)r * P, k0, k1, bb, t, pb, pe, a64);
+    if (s > 0) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) red[s - 1][tx][k] = a64[k];
+    }
+    __syncthreads();
+    if (s != 0 || b >= nb) return;
+    for (int q = 0; q < ps - 1; ++q)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) a64[k] += red[q][tx][k];
+    if (nsplit > 1) {
+        *reinterpret_cast<double4*>(part + (((int64_t)r * nsplit + z) * nb + b) * 4) =
+            make_double4(a64[0], a64[1], a64[2], a64[3]);
+        return;
+    }
+    tell_finish(a64, b, r, k0, k1, t, D, nb, P, sigma, inv_ns, ac, best_j, m, m1, v, grad, best_x);
+}
+
+// Second half of a split gradient: the nsplit workgroup sums of each Philox
+// block added in split order, then Adam.  One lane per block.
+__global__ __launch_bounds__(256) void k_tell_fold(const double* __restrict__ part, const int32_t* __restrict__ best_j,
+                                                   float* __restrict__ m, float* __restrict__ m1,
+                                                   float* __restrict__ v, float* __restrict__ grad,
+                                                   float* __restrict__ best_x, uint64_t seed, uint32_t t, int64_t D,
+                                                   int64_t nb, int32_t P, int32_t nsplit, float sigma,
+                                                   double inv_ns, AdamConsts ac)
+{
+    const int32_t r = blockIdx.y;
+    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= nb) return;
+    const uint64_t key = seed + (uint64_t)r;
+    const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
+    const double* p0 = part + ((int64_t)r * nsplit * nb + b) * 4;
+    const double4 q0 = *reinterpret_cast<const double4*>(p0);
+    double a64[4] = {q0.x, q0.y, q0.z, q0.w};
+    for (int32_t q = 1; q < nsplit; ++q) {
+        const double4 qq = *reinterpret_cast<const double4*>(p0 + (int64_t)q * nb * 4);
+        a64[0] += qq.x; a64[1] += qq.y; a64[2] += qq.z; a64[3] += qq.w;
+    }
+    tell_finish(a64, b, r, k0, k1, t, D, nb, P, sigma, inv_ns, ac, best_j, m, m1, v, grad, best_x);
 }
 
 // ---------------------------------------------------------------------------
@@ -842,15 +887,41 @@ hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, 
     return hipGetLastError();
 }
 
-hipError_t launch_tell(const Geometry& g, const es_config& c, uint32_t t, const AdamConsts& a,
+hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp, uint32_t t, const AdamConsts& a,
                        double inv_ns, const float* wfold, const int32_t* best_j, float* m,
-                       float* m1, float* v, float* grad, float* best_x, hipStream_t s)
+                       float* m1, float* v, float* grad, float* best_x, double* part, hipStream_t s)
 {
-    const int32_t ps = tell_slices(g);
-    const dim3 grid((unsigned)((g.nb + TELL_LANES - 1) / TELL_LANES), (unsigned)g.R);
-    k_tell<<<grid, TELL_LANES * ps, 0, s>>>(wfold, best_j, m, m1, v, grad, best_x, c.seed, t, g.D, g.nb, g.P, ps,
-                                            c.sigma, inv_ns, a);
+    const dim3 grid((unsigned)((g.nb + TELL_LANES - 1) / TELL_LANES), (unsigned)g.R, (unsigned)tp.nsplit);
+    k_tell<<<grid, TELL_LANES * tp.ps, 0, s>>>(wfold, best_j, m, m1, v, grad, best_x, c.seed, t, g.D, g.nb, g.P,
+                                               tp.ps, tp.nsplit, part, c.sigma, inv_ns, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || tp.nsplit == 1) return e;
+    const dim3 fgrid((unsigned)((g.nb + 255) / 256), (unsigned)g.R);
+    k_tell_fold<<<fgrid, 256, 0, s>>>(part, best_j, m, m1, v, grad, best_x, c.seed, t, g.D, g.nb, g.P, tp.nsplit,
+                                      c.sigma, inv_ns, a);
     return hipGetLastError();
+}
+
+TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit)
+{
+    TellPlan tp;
+    tp.ps = tell_slices(g);
+    if (fused_path) return tp;  // the fused loop sums all slices in one workgroup
+    // Few block groups (under four workgroups per CU) leave the CUs unevenly
+    // loaded; then split each group's pairs over more, smaller workgroups
+    // (four slices each), as long as every slice keeps two whole pair groups.
+    const int64_t groups = (g.nb + TELL_LANES - 1) / TELL_LANES * g.R;
+    int64_t nsplit = force_nsplit > 0 ? force_nsplit : groups >= 1024 ? 1 : (1024 + groups - 1) / groups;
+    while (nsplit > 1 && g.P / (4 * nsplit) < 2 * TELL_GROUP) --nsplit;
+    if (nsplit <= 1 || nsplit > 65535) return tp;
+    tp.ps = 4;
+    tp.nsplit = (int32_t)nsplit;
+    return tp;
+}
+
+size_t tell_part_elems(const Geometry& g, const TellPlan& tp)
+{
+    return tp.nsplit > 1 ? (size_t)g.R * tp.nsplit * g.nb * 4 : 0;
 }
 
 int32_t tell_slices(const Geometry& g)

@@ -206,3 +206,38 @@ def test_tell_matches_oracle(D, N, R, t):
         np.testing.assert_array_equal(mg[r], ma)
         np.testing.assert_array_equal(m1g[r], m1a)
         np.testing.assert_array_equal(vg[r], va)
+
+
+def test_split_tell_repeated_and_deterministic():
+    """A geometry with few groups of Philox blocks (D = 4099, N = 2048, two
+    runs), whose pairs the gradient kernel spreads over several workgroups per
+    block group: three consecutive tells, each checked against the oracle from
+    the state the GPU reached, and bit-identical across two handles (the
+    workgroups' partial sums meet in a fixed order whichever arrives last)."""
+    P = _es()
+    D, N, R = 4099, 2048, 2
+    cfg = _cfg(num_dims=D, popsize=N, num_runs=R, problem=P.PROB_NONE, sigma=0.05, lr=0.005,
+               flags=P.FLAG_KEEP_GRAD, seed=5)
+    a, b = P.ES(cfg), P.ES(cfg)
+    oc = to_oracle(cfg)
+    for t in range(3):
+        f = fitness_with_ties(100 + t, R, N, ties=False)
+        st0 = a.get_state()
+        m0, m10, v0 = _np(st0["m"]), _np(st0["m1"]), _np(st0["v"])
+        for es in (a, b):
+            es.ask()
+            es.tell(torch.tensor(f, device="cuda"))
+        ga, gb = _np(a.grad()), _np(b.grad())
+        np.testing.assert_array_equal(ga, gb)
+        sa, sb = a.get_state(), b.get_state()
+        for k in ("m", "m1", "v"):
+            np.testing.assert_array_equal(_np(sa[k]), _np(sb[k]))
+        mg = _np(sa["m"])
+        for r in range(R):
+            y = O.shape(f[r])
+            gref = O.grad(oc, r, t, y)
+            assert np.max(np.abs(ga[r] - gref)) <= 1e-4 * np.max(np.abs(gref)), (t, r)
+            mr, _, _ = O.adam(oc, t, gref, m0[r], m10[r], v0[r])
+            assert np.max(np.abs(mg[r] - mr) / np.maximum(np.abs(mr), cfg.lr)) <= 1e-5, (t, r)
+            ma, _, _ = O.adam(oc, t, ga[r], m0[r], m10[r], v0[r])
+            np.testing.assert_array_equal(mg[r], ma)

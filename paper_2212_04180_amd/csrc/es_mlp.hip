@@ -65,74 +65,21 @@ struct MlpSmem {
     } a;
     __bf16 w2a[2][W2_TILE];        // W2 chunk buffer 0
     __bf16 w3[2][MLP_OUT * W3S];
-    float b1[2][MLP_H], b2[2][MLP_H], b3[2][MLP_OUT];
+    float b1[2][MLP_H], b2[2][MLP_H], b3[2][MLP_OUT];  // b1, b2 times 2 log2(e)
     double red[MLP_WAVES];
 };
 
-// tanh x = 1 - 2 / (e^{2x} + 1): v_exp_f32 and v_rcp_f32, saturating to +-1.
-__device__ __forceinline__ float tanh_fast(float x)
+// tanh x = 1 - 2 / (2^u + 1) with u = 2 log2(e) x: v_exp_f32 and v_rcp_f32,
+// saturating to +-1.  The hidden layers keep their biases pre-multiplied by
+// 2 log2(e) so that u = fma(z, 2 log2(e), that product) is one instruction.
+constexpr float TWO_LOG2E = 2.88539008177792681472f;
+
+__device__ __forceinline__ float tanh_scaled(float u)
 {
-    const float e = __builtin_amdgcn_exp2f(x * 2.88539008177792681472f);
-    return fmaf(-2.0f, __builtin_amdgcn_rcpf(e + 1.0f), 1.0f);
+    return fmaf(-2.0f, __builtin_amdgcn_rcpf(__builtin_amdgcn_exp2f(u) + 1.0f), 1.0f);
 }
 
-// Perturbed weights of flat range [off, off + rows*cols) (a [rows][cols]
-// block of one tensor), written as bf16 to two LDS tiles with row stride ld.
-// Lanes vary in the Philox block; the pair is uniform.
-__device__ __forceinline__ void gen_weights(const float* __restrict__ mr, uint32_t k0, uint32_t k1, uint32_t pair,
-                                            uint32_t t, int64_t off, int rows, int cols, float sigma, __bf16* wp,
-                                            __bf16* wm, int ld)
-{
-    const int nblk = rows * cols / 4;
-    auto one = [&](int i, const float e[4]) {
-        const int64_t b = off / 4 + i;
-        const float4 m4 = *reinterpret_cast<const float4*>(mr + 4 * b);
-        const float mv[4] = {m4.x, m4.y, m4.z, m4.w};
-        bf16x4 vp, vm;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            vp[k] = (__bf16)fmaf(sigma, e[k], mv[k]);
-            vm[k] = (__bf16)fmaf(-sigma, e[k], mv[k]);
-        }
-        const int row = (4 * i) / cols, col = (4 * i) % cols;
-        *reinterpret_cast<bf16x4*>(wp + row * ld + col) = vp;
-        *reinterpret_cast<bf16x4*>(wm + row * ld + col) = vm;
-    };
-    const int step = (int)blockDim.x;
-    int i = threadIdx.x;
-    // two independent Philox chains in flight per lane (latency hiding at
-    // two waves per SIMD)
-    for (; i + step < nblk; i += 2 * step) {
-        float e0[4], e1[4];
-        const uint4 w0 = philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)(off / 4 + i), pair, t, DOM_NOISE);
-        const uint4 w1 = philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)(off / 4 + i + step), pair, t, DOM_NOISE);
-        box_muller4(w0, e0);
-        box_muller4(w1, e1);
-        one(i, e0);
-        one(i + step, e1);
-    }
-    if (i < nblk) {
-        float e[4];
-        box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)(off / 4 + i), pair, t, DOM_NOISE), e);
-        one(i, e);
-    }
-}
-
-// Perturbed biases of flat range [off, off + n), fp32.
-__device__ __forceinline__ void gen_bias(const float* __restrict__ mr, uint32_t k0, uint32_t k1, uint32_t pair,
-                                         uint32_t t, int64_t off, int n, float sigma, float* bp, float* bm)
-{
-    for (int i = threadIdx.x; i < n / 4; i += blockDim.x) {
-        const int64_t b = off / 4 + i;
-        float e[4];
-        box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)b, pair, t, DOM_NOISE), e);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            bp[4 * i + k] = fmaf(sigma, e[k], mr[4 * b + k]);
-            bm[4 * i + k] = fmaf(-sigma, e[k], mr[4 * b + k]);
-        }
-    }
-}
+__device__ __forceinline__ float tanh_fast(float x) { return tanh_scaled(x * TWO_LOG2E); }
 
 __device__ __forceinline__ bf16x8 cat(bf16x4 lo, bf16x4 hi)
 {
@@ -146,14 +93,15 @@ __device__ __forceinline__ bf16x8 cat(bf16x4 lo, bf16x4 hi)
 }
 
 // Bias, activation and bf16 rounding of two stacked accumulator tiles
-// (rows r0+4q+i and r0+16+4q+i) into one B operand of the next layer.
-__device__ __forceinline__ bf16x8 activate(const floatx4& lo, const floatx4& hi, const float* bias, int r0, int q)
+// (rows r0+4q+i and r0+16+4q+i) into one B operand of the next layer;
+// biasK holds the layer's biases times 2 log2(e).
+__device__ __forceinline__ bf16x8 activate(const floatx4& lo, const floatx4& hi, const float* biasK, int r0, int q)
 {
     bf16x8 h;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        h[i] = (__bf16)tanh_fast(lo[i] + bias[r0 + 4 * q + i]);
-        h[4 + i] = (__bf16)tanh_fast(hi[i] + bias[r0 + 16 + 4 * q + i]);
+        h[i] = (__bf16)tanh_scaled(fmaf(lo[i], TWO_LOG2E, biasK[r0 + 4 * q + i]));
+        h[4 + i] = (__bf16)tanh_scaled(fmaf(hi[i], TWO_LOG2E, biasK[r0 + 16 + 4 * q + i]));
     }
     return h;
 }
@@ -233,13 +181,75 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
     const float* __restrict__ mr = m + (int64_t)r * Dp;
 
-    // ---- layer 1 weights, all biases, layer 3 weights
-    gen_weights(mr, k0, k1, (uint32_t)p, t, OFF_W1, MLP_H, MLP_IN, sigma, S.a.w1[0], S.a.w1[1], W1S);
-    gen_weights(mr, k0, k1, (uint32_t)p, t, OFF_W3, MLP_OUT, MLP_H, sigma, S.w3[0], S.w3[1], W3S);
-    gen_bias(mr, k0, k1, (uint32_t)p, t, OFF_B1, MLP_H, sigma, S.b1[0], S.b1[1]);
-    gen_bias(mr, k0, k1, (uint32_t)p, t, OFF_B2, MLP_H, sigma, S.b2[0], S.b2[1]);
-    gen_bias(mr, k0, k1, (uint32_t)p, t, OFF_B3, MLP_OUT, sigma, S.b3[0], S.b3[1]);
-    gen_weights(mr, k0, k1, (uint32_t)p, t, OFF_W2, W2_ROWS, MLP_H, sigma, S.w2a[0], S.w2a[1], W2S);  // chunk 0
+    // ---- layer 1 and layer 3 weights, W2 chunk 0, all biases.  Each thread
+    // owns seven weight blocks (W1: tid + 1024k, W3: tid, W2 chunk 0: tid and
+    // tid + 1024); the 132 bias blocks go to the last threads.  All mean
+    // words are fetched before the first Philox block is generated.
+    {
+        const int tid = (int)threadIdx.x;
+        constexpr int NB1 = MLP_H * MLP_IN / 4, NB3 = MLP_OUT * MLP_H / 4;
+        static_assert(NB1 == 4 * MLP_THREADS && NB3 == MLP_THREADS && W2_ROWS * MLP_H / 4 == 2 * MLP_THREADS,
+                      "prologue block split");
+        constexpr int NBIAS = (2 * MLP_H + MLP_OUT) / 4;
+        const int64_t blk[7] = {OFF_W1 / 4 + tid, OFF_W1 / 4 + tid + MLP_THREADS, OFF_W1 / 4 + tid + 2 * MLP_THREADS,
+                                OFF_W1 / 4 + tid + 3 * MLP_THREADS, OFF_W3 / 4 + tid, OFF_W2 / 4 + tid,
+                                OFF_W2 / 4 + tid + MLP_THREADS};
+        float4 mw[7];
+#pragma unroll
+        for (int k = 0; k < 7; ++k) mw[k] = *reinterpret_cast<const float4*>(mr + 4 * blk[k]);
+        const int jb = tid - (MLP_THREADS - NBIAS);  // bias block of this thread, if >= 0
+        const int64_t bblk = jb < MLP_H / 4 ? OFF_B1 / 4 + jb : jb < MLP_H / 2 ? OFF_B2 / 4 + (jb - MLP_H / 4)
+                                                                                : OFF_B3 / 4 + (jb - MLP_H / 2);
+        float4 mb = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (jb >= 0) mb = *reinterpret_cast<const float4*>(mr + 4 * bblk);
+#pragma unroll
+        for (int k = 0; k < 7; ++k) {
+            float e[4];
+            box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)blk[k], (uint32_t)p, t, DOM_NOISE), e);
+            const float mv[4] = {mw[k].x, mw[k].y, mw[k].z, mw[k].w};
+            bf16x4 vp, vm;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                vp[i] = (__bf16)fmaf(sigma, e[i], mv[i]);
+                vm[i] = (__bf16)fmaf(-sigma, e[i], mv[i]);
+            }
+            __bf16 *dp, *dm;
+            if (k < 4) {  // W1 [256][64]
+                const int i4 = 4 * (tid + k * MLP_THREADS);
+                dp = S.a.w1[0] + (i4 / MLP_IN) * W1S + i4 % MLP_IN;
+                dm = S.a.w1[1] + (i4 / MLP_IN) * W1S + i4 % MLP_IN;
+            } else if (k == 4) {  // W3 [16][256]
+                const int i4 = 4 * tid;
+                dp = S.w3[0] + (i4 / MLP_H) * W3S + i4 % MLP_H;
+                dm = S.w3[1] + (i4 / MLP_H) * W3S + i4 % MLP_H;
+            } else {  // W2 chunk 0 [32][256]
+                const int i4 = 4 * (tid + (k - 5) * MLP_THREADS);
+                dp = S.w2a[0] + (i4 / MLP_H) * W2S + i4 % MLP_H;
+                dm = S.w2a[1] + (i4 / MLP_H) * W2S + i4 % MLP_H;
+            }
+            *reinterpret_cast<bf16x4*>(dp) = vp;
+            *reinterpret_cast<bf16x4*>(dm) = vm;
+        }
+        if (jb >= 0) {
+            float e[4];
+            box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)bblk, (uint32_t)p, t, DOM_NOISE), e);
+            const float mv[4] = {mb.x, mb.y, mb.z, mb.w};
+            float *bp, *bm;
+            if (jb < MLP_H / 4) {
+                bp = S.b1[0] + 4 * jb; bm = S.b1[1] + 4 * jb;
+            } else if (jb < MLP_H / 2) {
+                bp = S.b2[0] + 4 * (jb - MLP_H / 4); bm = S.b2[1] + 4 * (jb - MLP_H / 4);
+            } else {
+                bp = S.b3[0] + 4 * (jb - MLP_H / 2); bm = S.b3[1] + 4 * (jb - MLP_H / 2);
+            }
+            const float sc = jb < MLP_H / 2 ? TWO_LOG2E : 1.0f;  // hidden-layer biases pre-scaled
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                bp[i] = fmaf(sigma, e[i], mv[i]) * sc;
+                bm[i] = fmaf(-sigma, e[i], mv[i]) * sc;
+            }
+        }
+    }
 
     // input B operands: X[n][32ks + 8q + i] for batch column n of tile nt
     bf16x8 xop[2][2];
@@ -274,6 +284,13 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
     }
     __syncthreads();  // W1 is dead from here on; its space holds chunk buffer 1
 
+    // teacher outputs of this lane's (batch column, output) entries, fetched
+    // early: Y_T[n][4q .. 4q+3] for n = nbase + 16 nt + l16
+    float4 yref[2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+        yref[nt] = *reinterpret_cast<const float4*>(yt + (nbase + 16 * nt + l16) * MLP_OUT + 4 * q);
+
     // ---- layer 2 chunk by chunk, generating the next chunk meanwhile
     floatx4 y[2] = {floatx4{0.f, 0.f, 0.f, 0.f}, floatx4{0.f, 0.f, 0.f, 0.f}};
     for (int c = 0; c < W2_CHUNKS; ++c) {
@@ -303,14 +320,14 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
     double se = 0.0;
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
-        const int n = nbase + 16 * nt + l16;
+        const float yr[4] = {yref[nt].x, yref[nt].y, yref[nt].z, yref[nt].w};
         float sq = 0.f;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int o = 4 * q + i;
             float v = y[nt][i] + S.b3[mem][o];
             if (tanh_out) v = tanh_fast(v);
-            const float d = v - yt[n * MLP_OUT + o];
+            const float d = v - yr[i];
             sq = fmaf(d, d, sq);
         }
         se += (double)sq;

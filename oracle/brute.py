@@ -133,14 +133,57 @@ def centered(f, maximize=False):
     return [f32(Fraction(2 * r - (N - 1), 2 * (N - 1))) for r in ranks(f, maximize)]
 
 
+def shaped_keys(f, pen, maximize, w_decay):
+    """Minimisation keys with the weight-decay penalty added in fp32:
+    k = f or -f, then fl32(k + fl32(w * pen)) for finite k; NaN is +inf."""
+    out = []
+    for j, v in enumerate(f):
+        k = -v if maximize else v
+        if math.isnan(k):
+            out.append(math.inf)
+        elif w_decay and math.isfinite(k):
+            out.append(f32(_q(k) + _q(f32(_q(w_decay) * _q(pen[j])))))
+        else:
+            out.append(k)
+    return out
+
+
+def zscore(keys):
+    """(k - mean) / (population sd + 1e-10) over the finite keys, from the exact
+    rational mean and variance and a 60-digit square root, rounded once to fp32;
+    non-finite keys give 0."""
+    from decimal import Decimal, getcontext
+    getcontext().prec = 60
+    fin = [_q(k) for k in keys if math.isfinite(k)]
+    n = len(fin)
+    mu = sum(fin) / n if n else Fraction(0)
+    var = sum((k - mu) ** 2 for k in fin) / n if n else Fraction(0)
+    sd = (Decimal(var.numerator) / Decimal(var.denominator)).sqrt()
+    den = sd + Decimal(1e-10)
+    out = []
+    for k in keys:
+        if not math.isfinite(k):
+            out.append(0.0)
+            continue
+        num = _q(k) - mu
+        z = Decimal(num.numerator) / Decimal(num.denominator) / den
+        out.append(f32(Fraction(z)))
+    return out
+
+
 class BruteES:
-    """R=1 OpenAI-ES with antithetic pairs (+eps first half, -eps second half)."""
+    """R=1 OpenAI-ES with antithetic pairs (+eps first half, -eps second half).
+    sigma and lr follow the App. B schedules, max(x * decay, final) after each
+    generation; shaping "centered", "raw" or "zscore", optional weight decay."""
 
     def __init__(self, problem, D, N, sigma, lr, seed, lo, hi, s=None, maximize=False,
-                 beta1=0.9, beta2=0.999, eps=1e-8, a=10.0, shaping="centered"):
+                 beta1=0.9, beta2=0.999, eps=1e-8, a=10.0, shaping="centered",
+                 sigma_decay=1.0, sigma_final=0.0, lr_decay=1.0, lr_final=0.0, w_decay=0.0):
         assert N % 2 == 0
         self.problem, self.D, self.N = problem, D, N
         self.sigma, self.lr = f32(sigma), f32(lr)
+        self.sd, self.sf, self.ld, self.lf = f32(sigma_decay), f32(sigma_final), f32(lr_decay), f32(lr_final)
+        self.w_decay = f32(w_decay)
         self.b1, self.b2, self.eps = f32(beta1), f32(beta2), f32(eps)
         self.seed, self.s, self.maximize, self.a, self.shaping = seed, s, maximize, a, shaping
         self.m = init_uniform(seed, D, lo, hi)
@@ -161,10 +204,17 @@ class BruteES:
     def generation(self, fit=None):
         E, X = self.population()
         f = fit if fit is not None else [fitness(self.problem, x, self.s, self.a) for x in X]
+        pen = [f32(sum(_q(v) ** 2 for v in x) / self.D) for x in X]
+        keys = shaped_keys(f, pen, self.maximize, self.w_decay)
         if self.shaping == "centered":
-            y = centered(f, self.maximize)
+            N = self.N
+            rk = [sum(1 for k in range(N) if keys[k] < keys[j] or (keys[k] == keys[j] and k < j))
+                  for j in range(N)]
+            y = [f32(Fraction(2 * r - (N - 1), 2 * (N - 1))) for r in rk]
+        elif self.shaping == "zscore":
+            y = zscore(keys)
         else:
-            y = [(-v if self.maximize else v) for v in f]
+            y = keys
         Ns = Fraction(self.N) * _q(self.sigma)
         g = [f32(sum(_q(y[j]) * _q(E[j][d]) for j in range(self.N)) / Ns)
              for d in range(self.D)]
@@ -185,4 +235,7 @@ class BruteES:
             self.m[d] = fma32(-self.lr, q, self.m[d])
             self.m1[d], self.v[d] = m1, v
         self.t += 1
-        return {"E": E, "X": X, "fitness": f, "y": y, "g": g}
+        used = (self.sigma, self.lr)
+        self.sigma = max(f32(_q(self.sigma) * _q(self.sd)), self.sf)
+        self.lr = max(f32(_q(self.lr) * _q(self.ld)), self.lf)
+        return {"E": E, "X": X, "fitness": f, "y": y, "g": g, "pen": pen, "sigma_lr": used}

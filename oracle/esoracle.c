@@ -116,7 +116,7 @@ void or_normals(uint64_t seed, uint32_t domain, uint32_t row, uint32_t t,
 enum { OR_PROB_NONE = 0, OR_PROB_SPHERE = 1, OR_PROB_SHIFTED_SPHERE = 2,
        OR_PROB_ROSENBROCK = 3, OR_PROB_RASTRIGIN = 4, OR_PROB_MLP = 5 };
 enum { OR_INIT_UNIFORM = 0, OR_INIT_ZERO = 1, OR_INIT_FANIN_NORMAL = 2 };
-enum { OR_SHAPE_CENTERED_RANK = 0, OR_SHAPE_RAW = 1 };
+enum { OR_SHAPE_CENTERED_RANK = 0, OR_SHAPE_RAW = 1, OR_SHAPE_Z_SCORE = 2 };
 
 typedef struct {
     int64_t num_dims;   /* D */
@@ -133,6 +133,11 @@ typedef struct {
     int32_t mlp_batch;  /* inputs per generation */
     int32_t mlp_bf16;   /* 1: student forward rounds operands to bf16 */
     int32_t mlp_tanh_out;
+    /* schedules (App. B tables: init / decay / final): after each tell       */
+    /* sigma <- max(sigma * decay, final), lr likewise; 1 and 0 keep them      */
+    /* constant.  sigma and lr above are the values of the current generation. */
+    float sigma_decay, sigma_final, lr_decay, lr_final;
+    float w_decay;      /* weight-decay coefficient of the fitness shaping   */
 } or_config;
 
 /* MLP 64-256-256-16 layer table, flattened [out][in] row-major weights, then
@@ -418,6 +423,75 @@ void or_shape(const float* f, int32_t N, int32_t maximize, int32_t shaping, floa
     free(rank);
 }
 
+/* The other shaping transformations Sec. 3.2 names next to centered ranks:
+ * z-scoring and weight-decay regularisation.
+ * Readings.  Weight decay penalises the mean square parameter of a member in
+ * the minimisation sense: with pen_j = (1/D) sum_d x_jd^2 (fp32),
+ *   key_j = fl32(k_j + fl32(w_decay * pen_j)),  k_j = f_j or -f_j (maximise);
+ * a NaN fitness stays the worst key (+inf).  Ranks and raw shaping then use
+ * these keys.  z-score: over the n finite keys, mean mu and population
+ * standard deviation sd in fp64, y_j = fl32((key_j - mu) / (sd + 1e-10));
+ * members with a non-finite key get y = 0.                                  */
+float or_shaped_key(float f, float pen, int32_t maximize, float w_decay)
+{
+    float k = maximize ? -f : f;
+    if (isnan(k)) return INFINITY;
+    if (w_decay != 0.0f && isfinite(k)) k = k + w_decay * pen;
+    return k;
+}
+
+void or_shape_full(const float* f, const float* pen, int32_t N, int32_t maximize, int32_t shaping,
+                   float w_decay, float* y)
+{
+    float* key = (float*)malloc(sizeof(float) * (size_t)N);
+    for (int32_t j = 0; j < N; ++j) key[j] = or_shaped_key(f[j], pen ? pen[j] : 0.0f, maximize, w_decay);
+    if (shaping == OR_SHAPE_RAW) {
+        for (int32_t j = 0; j < N; ++j) y[j] = key[j];
+    } else if (shaping == OR_SHAPE_Z_SCORE) {
+        double sum = 0.0, n = 0.0;
+        for (int32_t j = 0; j < N; ++j)
+            if (isfinite(key[j])) { sum += (double)key[j]; n += 1.0; }
+        double mu = n > 0.0 ? sum / n : 0.0, ss = 0.0;
+        for (int32_t j = 0; j < N; ++j)
+            if (isfinite(key[j])) ss += ((double)key[j] - mu) * ((double)key[j] - mu);
+        double sd = n > 0.0 ? sqrt(ss / n) : 0.0;
+        for (int32_t j = 0; j < N; ++j)
+            y[j] = isfinite(key[j]) ? (float)(((double)key[j] - mu) / (sd + 1e-10)) : 0.0f;
+    } else {
+        /* centered ranks of the keys: key already minimisation-oriented */
+        float den = (float)(2 * (N - 1));
+        for (int32_t j = 0; j < N; ++j) {
+            int32_t r = 0;
+            for (int32_t k = 0; k < N; ++k)
+                if (key[k] < key[j] || (key[k] == key[j] && k < j)) ++r;
+            y[j] = (float)(2 * r - (N - 1)) / den;
+        }
+    }
+    free(key);
+}
+
+/* Mean square parameter of every member of run r at generation t,
+ * pen_j = fl32((sum_d x_jd^2 in fp64) / D).                                 */
+void or_penalty(const or_config* c, int32_t run, uint32_t t, const float* m, float* pen)
+{
+    int64_t D = c->num_dims;
+    float* x = (float*)malloc(sizeof(float) * (size_t)D);
+    for (int32_t j = 0; j < c->popsize; ++j) {
+        or_member(c, run, t, m, j, x);
+        double acc = 0.0;
+        for (int64_t d = 0; d < D; ++d) acc += (double)x[d] * (double)x[d];
+        pen[j] = (float)(acc / (double)D);
+    }
+    free(x);
+}
+
+/* Exponential decay with a floor (App. B schedules), fp32: max(x*decay, final). */
+float or_decay(float x, float decay, float final)
+{
+    float y = x * decay;
+    return y > final ? y : final;
+}
+
 /* ------------------------------------------------------------------------ */
 /* tell, step 2: FD gradient estimate (Sec. 2.1 estimator) over the whole    */
 /* population, g = E^T y / (N sigma), E the N x D matrix of perturbations    */
@@ -513,7 +587,17 @@ void or_generation(const or_config* c, int32_t run, int64_t t, const float* pdat
         if (best_f) *best_f = f[jbest];
         if (best_x) or_member(c, run, (uint32_t)t, m, jbest, best_x);
     }
-    or_shape(f, N, c->maximize, c->shaping, y);
+    if (c->w_decay != 0.0f || c->shaping == OR_SHAPE_Z_SCORE) {
+        float* pen = NULL;
+        if (c->w_decay != 0.0f) {
+            pen = (float*)malloc(sizeof(float) * (size_t)N);
+            or_penalty(c, run, (uint32_t)t, m, pen);
+        }
+        or_shape_full(f, pen, N, c->maximize, c->shaping, c->w_decay, y);
+        free(pen);
+    } else {
+        or_shape(f, N, c->maximize, c->shaping, y);
+    }
     or_grad(c, run, (uint32_t)t, y, 0, D, g);
     or_adam(c, t, g, D, m, m1, v);
     if (fit_out) memcpy(fit_out, f, sizeof(float) * (size_t)N);

@@ -13,7 +13,7 @@ import ctypes
 import math
 import os
 import subprocess
-from dataclasses import dataclass
+from dataclasses import dataclass, replace
 
 import numpy as np
 
@@ -23,7 +23,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 PROB_NONE, PROB_SPHERE, PROB_SHIFTED_SPHERE, PROB_ROSENBROCK, PROB_RASTRIGIN, PROB_MLP = range(6)
 INIT_UNIFORM, INIT_ZERO, INIT_FANIN_NORMAL = range(3)
-SHAPE_CENTERED_RANK, SHAPE_RAW = range(2)
+SHAPE_CENTERED_RANK, SHAPE_RAW, SHAPE_Z_SCORE = range(3)
 DOM_NOISE, DOM_INIT, DOM_PROBLEM, DOM_EVAL = range(4)
 MLP_IN, MLP_H, MLP_OUT = 64, 256, 16
 
@@ -60,6 +60,11 @@ class _Cfg(ctypes.Structure):
         ("mlp_batch", ctypes.c_int32),
         ("mlp_bf16", ctypes.c_int32),
         ("mlp_tanh_out", ctypes.c_int32),
+        ("sigma_decay", ctypes.c_float),
+        ("sigma_final", ctypes.c_float),
+        ("lr_decay", ctypes.c_float),
+        ("lr_final", ctypes.c_float),
+        ("w_decay", ctypes.c_float),
     ]
 
 
@@ -85,12 +90,19 @@ class OracleConfig:
     mlp_batch: int = 256
     mlp_bf16: int = 1
     mlp_tanh_out: int = 0
+    # App. B schedules (init = sigma / lr above, then decay and floor per tell)
+    sigma_decay: float = 1.0
+    sigma_final: float = 0.0
+    lr_decay: float = 1.0
+    lr_final: float = 0.0
+    w_decay: float = 0.0  # weight-decay fitness regularisation (Sec. 3.2)
 
     def cstruct(self) -> _Cfg:
         return _Cfg(self.num_dims, self.popsize, self.num_runs, self.sigma, self.lr, self.beta1,
                     self.beta2, self.eps, self.maximize, self.shaping, self.seed, self.init,
                     self.init_lo, self.init_hi, self.problem, self.rastrigin_a, self.mlp_batch,
-                    self.mlp_bf16, self.mlp_tanh_out)
+                    self.mlp_bf16, self.mlp_tanh_out, self.sigma_decay, self.sigma_final,
+                    self.lr_decay, self.lr_final, self.w_decay)
 
 
 _lib = None
@@ -118,6 +130,10 @@ def lib():
             "or_mlp_fitness": (f32, [pc, P(f32), u32, P(f32)]),
             "or_eval_members": (None, [pc, i32, u32, P(f32), P(f32), P(i32), i32, P(f32)]),
             "or_ranks": (None, [P(f32), i32, i32, P(i32)]),
+            "or_shaped_key": (f32, [f32, f32, i32, f32]),
+            "or_shape_full": (None, [P(f32), P(f32), i32, i32, i32, f32, P(f32)]),
+            "or_penalty": (None, [pc, i32, u32, P(f32), P(f32)]),
+            "or_decay": (f32, [f32, f32, f32]),
             "or_shape": (None, [P(f32), i32, i32, i32, P(f32)]),
             "or_grad": (None, [pc, i32, u32, P(f32), i64, i64, P(f32)]),
             "or_adam": (None, [pc, i64, P(f32), i64, P(f32), P(f32), P(f32)]),
@@ -251,6 +267,29 @@ def shape(f, maximize=0, shaping=SHAPE_CENTERED_RANK):
     return y
 
 
+def shape_full(f, pen=None, maximize=0, shaping=SHAPE_CENTERED_RANK, w_decay=0.0):
+    """Fitness shaping with the z-score and weight-decay options of Sec. 3.2
+    (readings in ``or_shape_full``); ``pen`` = per-member mean square."""
+    f = _f32(f)
+    y = np.zeros(f.shape[0], dtype=np.float32)
+    pp = _f32(pen) if pen is not None else None
+    lib().or_shape_full(_p(f), _p(pp), f.shape[0], maximize, shaping, w_decay, _p(y))
+    return y
+
+
+def penalty(cfg, run, t, m):
+    """Per-member mean square parameter (1/D) sum_d x_jd^2 of run r at generation t."""
+    m = _f32(m)
+    pen = np.zeros(cfg.popsize, dtype=np.float32)
+    lib().or_penalty(cfg.cstruct(), run, t, _p(m), _p(pen))
+    return pen
+
+
+def decay(x, rate, final):
+    """One step of the App. B schedule: max(x * rate, final) in fp32."""
+    return float(lib().or_decay(x, rate, final))
+
+
 def grad(cfg, run, t, y, d0=0, nd=None):
     """FD gradient estimate g = E^T y / (N sigma) (Sec. 2.1) for dims [d0, d0+nd)."""
     nd = cfg.num_dims - d0 if nd is None else nd
@@ -272,6 +311,10 @@ def adam(cfg, t, g, m, m1, v):
 # over R independent seeds (Listing 3).
 # --------------------------------------------------------------------------
 class OracleES:
+    """Batched OpenAI-ES state and loop (Listing 1 / Listing 2 / Listing 3).
+    Per-run sigma and learning rate (the vmap over hyper-parameters of
+    Sec. 2.2) start from the config and follow the App. B schedules."""
+
     def __init__(self, cfg: OracleConfig):
         self.cfg = cfg
         R, D = cfg.num_runs, cfg.num_dims
@@ -283,13 +326,25 @@ class OracleES:
         self.best_key = np.full(R, math.inf, dtype=np.float64)
         self.best_f = np.full(R, math.nan, dtype=np.float32)
         self.best_x = np.zeros((R, D), np.float32)
+        self.sigma = np.full(R, cfg.sigma, dtype=np.float32)
+        self.lr = np.full(R, cfg.lr, dtype=np.float32)
+
+    def set_hparams(self, sigma=None, lr=None):
+        if sigma is not None:
+            self.sigma = _f32(sigma).copy()
+        if lr is not None:
+            self.lr = _f32(lr).copy()
+
+    def run_cfg(self, r) -> OracleConfig:
+        """The config of run r at the current generation (its sigma and lr)."""
+        return replace(self.cfg, sigma=float(self.sigma[r]), lr=float(self.lr[r]))
 
     def ask(self):
-        return np.stack([population(self.cfg, r, self.t, self.m[r]) for r in range(self.cfg.num_runs)])
+        return np.stack([population(self.run_cfg(r), r, self.t, self.m[r]) for r in range(self.cfg.num_runs)])
 
     def eval(self):
         js = np.arange(self.cfg.popsize, dtype=np.int32)
-        return np.stack([eval_members(self.cfg, r, self.t, self.m[r], self.pdata, js)
+        return np.stack([eval_members(self.run_cfg(r), r, self.t, self.m[r], self.pdata, js)
                          for r in range(self.cfg.num_runs)])
 
     def tell(self, fitness=None):
@@ -300,9 +355,9 @@ class OracleES:
         out_f = np.zeros((R, N), np.float32)
         out_y = np.zeros((R, N), np.float32)
         out_g = np.zeros((R, D), np.float32)
-        c = cfg.cstruct()
         pd = _f32(self.pdata) if self.pdata is not None else None
         for r in range(R):
+            c = self.run_cfg(r).cstruct()
             m, m1, v = self.m[r].copy(), self.m1[r].copy(), self.v[r].copy()
             fin = _f32(fitness[r]) if fitness is not None else None
             bk = ctypes.c_double(self.best_key[r])
@@ -314,6 +369,8 @@ class OracleES:
             self.m[r], self.m1[r], self.v[r] = m, m1, v
             self.best_key[r], self.best_f[r], self.best_x[r] = bk.value, bf[0], bx
             out_f[r], out_y[r], out_g[r] = fo, yo, go
+            self.sigma[r] = decay(float(self.sigma[r]), cfg.sigma_decay, cfg.sigma_final)
+            self.lr[r] = decay(float(self.lr[r]), cfg.lr_decay, cfg.lr_final)
         self.t += 1
         return {"fitness": out_f, "y": out_y, "g": out_g}
 
@@ -332,7 +389,8 @@ class OracleES:
         return log
 
     def get_state(self):
-        return {"m": self.m.copy(), "m1": self.m1.copy(), "v": self.v.copy(), "t": self.t}
+        return {"m": self.m.copy(), "m1": self.m1.copy(), "v": self.v.copy(), "t": self.t,
+                "sigma": self.sigma.copy(), "lr": self.lr.copy()}
 
     def set_state(self, m, m1, v, t):
         self.m, self.m1, self.v = _f32(m).copy(), _f32(m1).copy(), _f32(v).copy()

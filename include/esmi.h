@@ -9,9 +9,12 @@
  *            demand -- never stored;
  *   evaluate built-in benchmark problems (Sec. 3.2: sphere, shifted sphere,
  *            Rosenbrock, Rastrigin; a teacher-student MLP), fused with ask;
- *   tell     centered-rank fitness shaping (Sec. 3.2; App. B), the
- *            finite-difference gradient estimate of Sec. 2.1,
- *            g = E^T y / (N sigma), and an Adam step on the mean (App. B).
+ *   tell     fitness shaping (Sec. 3.2: centered ranks as in App. B,
+ *            z-scores, weight-decay regularisation), the finite-difference
+ *            gradient estimate of Sec. 2.1, g = E^T y / (N sigma), and an
+ *            Adam step on the mean (App. B); sigma and the learning rate
+ *            then follow the exponential schedules of the App. B tables,
+ *            per run (the vmap over hyper-parameters of Sec. 2.2).
  *
  * Conventions shared by every entry point:
  *   - Device pointers are HIP device addresses on the device that was
@@ -49,7 +52,18 @@ typedef enum {
     ES_ERR_UNSUPPORTED = -5  /* valid request this build does not implement   */
 } es_status;
 
-typedef enum { ES_SHAPE_CENTERED_RANK = 0, ES_SHAPE_RAW = 1 } es_shaping;
+/* Fitness shaping (Sec. 3.2).  With key_j = f_j (minimise) or -f_j
+ * (maximise), NaN the worst key (+inf), and -- when w_decay != 0 -- the
+ * weight-decay penalty key_j = fl32(key_j + fl32(w_decay * pen_j)) for finite
+ * keys, pen_j = (1/D) sum_d x_jd^2:
+ *   CENTERED_RANK  y_j = (2 rank_j - (N-1)) / (2 (N-1)), one fp32 division of
+ *                  exact integers; rank = position in a stable ascending sort
+ *                  of the keys (ties by member index);
+ *   RAW            y_j = key_j;
+ *   Z_SCORE        y_j = fl32((key_j - mu) / (sd + 1e-10)), mu and sd the
+ *                  fp64 mean and population standard deviation of the finite
+ *                  keys; y_j = 0 for a non-finite key. */
+typedef enum { ES_SHAPE_CENTERED_RANK = 0, ES_SHAPE_RAW = 1, ES_SHAPE_Z_SCORE = 2 } es_shaping;
 
 typedef enum {
     ES_PROB_NONE = 0,           /* fitness only from the caller (es_tell)           */
@@ -90,6 +104,15 @@ typedef struct es_config {
     int32_t mlp_bf16;   /* ES_PROB_MLP: 1 = bf16 matrix-core forward         */
     int32_t mlp_tanh_out; /* ES_PROB_MLP: 1 = tanh on the output layer       */
     uint32_t flags;     /* ES_FLAG_*                                         */
+    /* Schedules (App. B, OpenAI-ES and PGPE tables: init / decay / final):
+     * after every tell sigma <- max(fl32(sigma * sigma_decay), sigma_final)
+     * and lr likewise, per run.  decay 1 and final 0 keep them constant. */
+    float sigma_decay;  /* > 0                                               */
+    float sigma_final;  /* >= 0                                              */
+    float lr_decay;     /* > 0                                               */
+    float lr_final;     /* >= 0                                              */
+    float w_decay;      /* >= 0, weight-decay coefficient of the shaping     */
+    uint32_t reserved;  /* must be 0                                         */
 } es_config;
 
 typedef struct es_handle es_handle;
@@ -112,10 +135,12 @@ es_status es_ask(es_handle* h, float* x_out);
  * for this generation; ES_ERR_UNSUPPORTED for ES_PROB_NONE. */
 es_status es_eval(es_handle* h, float* fitness_out);
 
-/* tell (Sec. 2.1 step 3): centered ranks (ties by member index, NaN worst),
- * g = E^T y / (N sigma) with eps regenerated from the counter, Adam step on
- * the mean, best-so-far update; t += 1.  fitness: device [R][N] from es_eval
- * or from the caller's own evaluation of the asked population. */
+/* tell (Sec. 2.1 step 3): fitness shaping (es_shaping; with weight decay the
+ * penalty pass regenerates the population once more), g = E^T y / (N sigma)
+ * with eps regenerated from the counter, Adam step on the mean, best-so-far
+ * update on the raw fitness, schedule step of sigma and lr; t += 1.
+ * fitness: device [R][N] from es_eval or from the caller's own evaluation
+ * of the asked population. */
 es_status es_tell(es_handle* h, const float* fitness);
 
 /* T fused generations (the scanned loop of Listing 2) with the built-in
@@ -139,6 +164,19 @@ es_status es_get_best(es_handle* h, float* member, float* fitness);
 es_status es_get_shaped(es_handle* h, float* y, int32_t* rank);
 es_status es_get_grad(es_handle* h, float* g);
 
+/* Per-run hyper-parameters (the vmap over hyper-parameters of Sec. 2.2):
+ * sigma and lr of the next generation of every run.  Host arrays [R];
+ * either may be NULL (left unchanged).  es_init sets every run to
+ * cfg.sigma and cfg.lr; the schedules continue from the values set here.
+ * Requires no open ask; sigma must be finite and > 0, lr finite and >= 0
+ * (ES_ERR_ARG otherwise).  es_get_hparams is synchronous. */
+es_status es_set_hparams(es_handle* h, const float* sigma, const float* lr);
+es_status es_get_hparams(es_handle* h, float* sigma, float* lr);
+
+/* Weight-decay penalty of the last es_tell: pen [R][N] = (1/D) sum_d x_jd^2
+ * of every member (device pointer).  ES_ERR_UNSUPPORTED when w_decay = 0. */
+es_status es_get_penalty(es_handle* h, float* pen);
+
 /* Problem data shared by all runs: the shift vector s [D] (shifted sphere)
  * or the flattened teacher network [D] (MLP).  Device pointer. */
 es_status es_get_problem_data(es_handle* h, float* out);
@@ -150,7 +188,8 @@ es_status es_debug_noise(es_handle* h, int32_t run, int64_t t, int32_t pair,
                          uint32_t* words, float* eps);
 
 /* Checkpoint (synchronous): with host_buf NULL, *bytes receives the size;
- * otherwise the state (config, t, m, m1, v, best) is written to host_buf.
+ * otherwise the state (config, t, m, m1, v, best, per-run sigma and lr) is
+ * written to host_buf.
  * es_load_state restores a checkpoint of a handle with the same config.
  * The random stream is a pure function of (seed, t), so resuming continues
  * the same trajectory bit for bit. */

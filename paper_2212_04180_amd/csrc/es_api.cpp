@@ -22,7 +22,7 @@ namespace {
 
 enum Phase { READY = 0, ASKED = 1 };
 
-constexpr uint32_t kCheckpointMagic = 0x45534d31u;  // "ESM1"
+constexpr uint32_t kCheckpointMagic = 0x45534d32u;  // "ESM2"
 
 thread_local char g_init_err[256] = {0};
 
@@ -59,6 +59,11 @@ struct es_handle {
     float* wfold = nullptr;  // [R][P]
     float* fit = nullptr;    // [R][N] fitness scratch for es_run
     float* partial = nullptr;
+    // per-run sigma and lr ([2][R]) of the current generation and the next;
+    // the rank kernel writes the schedule step into the other buffer
+    float* hp[2] = {nullptr, nullptr};
+    int hp_cur = 0;
+    float* pen = nullptr;        // [R][N] weight-decay mean square of the last tell
     TellPlan tell;               // pair slices of the gradient kernel
     double* tell_part = nullptr; // per-workgroup gradient sums when tell.nsplit > 1
     float* pdata = nullptr;  // [Dp] shift vector or teacher
@@ -118,7 +123,8 @@ const char* validate(const es_config& c)
     if (!(c.beta2 >= 0.0f && c.beta2 < 1.0f)) return "beta2 must be in [0, 1)";
     if (!(c.eps >= 0.0f) || !std::isfinite(c.eps)) return "eps must be finite and >= 0";
     if (c.maximize != 0 && c.maximize != 1) return "maximize must be 0 or 1";
-    if (c.shaping != ES_SHAPE_CENTERED_RANK && c.shaping != ES_SHAPE_RAW) return "unknown shaping";
+    if (c.shaping != ES_SHAPE_CENTERED_RANK && c.shaping != ES_SHAPE_RAW && c.shaping != ES_SHAPE_Z_SCORE)
+        return "unknown shaping";
     if (c.init < ES_INIT_UNIFORM || c.init > ES_INIT_FANIN_NORMAL) return "unknown init";
     if (c.init == ES_INIT_UNIFORM && !(c.init_hi > c.init_lo)) return "init range must have hi > lo";
     if (c.problem < ES_PROB_NONE || c.problem > ES_PROB_MLP) return "unknown problem";
@@ -129,6 +135,12 @@ const char* validate(const es_config& c)
     if (c.problem == ES_PROB_MLP && c.mlp_bf16 != 1) return "the MLP forward runs on bf16 matrix cores (mlp_bf16 = 1)";
     if (c.problem == ES_PROB_RASTRIGIN && !std::isfinite(c.rastrigin_a)) return "rastrigin_a must be finite";
     if ((c.flags & ~ES_FLAG_KEEP_GRAD) != 0) return "unknown flags";
+    if (!(c.sigma_decay > 0.0f) || !std::isfinite(c.sigma_decay)) return "sigma_decay must be finite and > 0";
+    if (!(c.lr_decay > 0.0f) || !std::isfinite(c.lr_decay)) return "lr_decay must be finite and > 0";
+    if (!(c.sigma_final >= 0.0f) || !std::isfinite(c.sigma_final)) return "sigma_final must be finite and >= 0";
+    if (!(c.lr_final >= 0.0f) || !std::isfinite(c.lr_final)) return "lr_final must be finite and >= 0";
+    if (!(c.w_decay >= 0.0f) || !std::isfinite(c.w_decay)) return "w_decay must be finite and >= 0";
+    if (c.reserved != 0) return "reserved must be 0";
     return nullptr;
 }
 
@@ -143,7 +155,6 @@ AdamConsts adam_consts(const es_config& c, int64_t t)
 {
     AdamConsts a;
     const double tp = (double)(t + 1);
-    a.lr = c.lr;
     a.beta1 = c.beta1;
     a.beta2 = c.beta2;
     a.omb1 = (float)(1.0 - (double)c.beta1);
@@ -165,7 +176,7 @@ void free_all(es_handle* h)
 {
     void* ptrs[] = {h->m, h->m1, h->v, h->best_x, h->grad, h->best_okey, h->best_f, h->best_j, h->table,
                     h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->adam_dev, h->mlp_scratch,
-                    h->tell_part};
+                    h->tell_part, h->hp[0], h->hp[1], h->pen};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     if (h->adam_host) (void)hipHostFree(h->adam_host);
@@ -200,14 +211,24 @@ es_status stage_adam(es_handle* h, int32_t T)
 es_status enqueue_tell(es_handle* h, const float* fitness, float* gen_best)
 {
     const Geometry& g = h->g;
-    ES_HIP(h, launch_rank(g, h->cfg, fitness, h->table, h->y, h->rank, h->wfold, h->best_okey, h->best_f,
-                          h->best_j, gen_best, h->stream),
+    const float* hp = h->hp[h->hp_cur];
+    if (h->cfg.w_decay != 0.0f) {
+        // weight decay: the mean square of every member, one more pass of the
+        // sampler through the sphere evaluation, divided by D in its reduction
+        es_config sq = h->cfg;
+        sq.problem = ES_PROB_SPHERE;
+        ES_HIP(h, launch_eval_bbob(g, sq, h->plan, (uint32_t)h->t, h->m, nullptr, h->partial, h->pen, hp,
+                                   (double)g.D, h->stream),
+               "weight-decay penalty pass");
+    }
+    ES_HIP(h, launch_rank(g, h->cfg, fitness, h->pen, h->table, h->y, h->rank, h->wfold, h->best_okey, h->best_f,
+                          h->best_j, gen_best, hp, h->hp[1 - h->hp_cur], h->stream),
            "rank kernel");
     const AdamConsts a = adam_consts(h->cfg, h->t);
-    const double inv_ns = 1.0 / ((double)g.N * (double)h->cfg.sigma);
-    ES_HIP(h, launch_tell(g, h->cfg, h->tell, (uint32_t)h->t, a, inv_ns, h->wfold, h->best_j, h->m, h->m1, h->v,
-                          h->grad, h->best_x, h->tell_part, h->stream),
+    ES_HIP(h, launch_tell(g, h->cfg, h->tell, (uint32_t)h->t, a, h->wfold, h->best_j, h->m, h->m1, h->v, h->grad,
+                          h->best_x, h->tell_part, hp, h->stream),
            "tell kernel");
+    h->hp_cur = 1 - h->hp_cur;  // the schedule step is next generation's sigma and lr
     return ES_OK;
 }
 
@@ -215,11 +236,13 @@ es_status enqueue_eval(es_handle* h, float* fit)
 {
     if (h->cfg.problem == ES_PROB_NONE) return fail(h, ES_ERR_UNSUPPORTED, "no built-in problem configured");
     if (h->cfg.problem == ES_PROB_MLP) {
-        ES_HIP(h, launch_eval_mlp(h->g, h->cfg, (uint32_t)h->t, h->m, h->pdata, h->mlp_scratch, fit, h->stream),
+        ES_HIP(h, launch_eval_mlp(h->g, h->cfg, (uint32_t)h->t, h->m, h->pdata, h->mlp_scratch, fit,
+                                  h->hp[h->hp_cur], h->stream),
                "MLP evaluate kernels");
         return ES_OK;
     }
-    ES_HIP(h, launch_eval_bbob(h->g, h->cfg, h->plan, (uint32_t)h->t, h->m, h->pdata, h->partial, fit, h->stream),
+    ES_HIP(h, launch_eval_bbob(h->g, h->cfg, h->plan, (uint32_t)h->t, h->m, h->pdata, h->partial, fit,
+                               h->hp[h->hp_cur], 1.0, h->stream),
            "evaluate kernel");
     return ES_OK;
 }
@@ -292,7 +315,7 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     h->plan = eval_plan(g, env_i64("ESMI_EVAL_BLOCKS_PER_CHUNK", 0));
     // es_run may take the fused loop for this geometry; then the per-call
     // gradient kernel must sum in the fused loop's order
-    h->tell = tell_plan(g, fused_supported(g, h->plan, cfg->problem), env_i64("ESMI_TELL_SPLIT", 0));
+    h->tell = tell_plan(g, fused_supported(g, h->plan, *cfg), env_i64("ESMI_TELL_SPLIT", 0));
     h->run_path = (int)env_i64("ESMI_RUN_PATH", 0);
     hipError_t e = hipGetDevice(&h->device);
     const size_t rows = (size_t)g.Dp * g.R;
@@ -309,8 +332,11 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     if (e == hipSuccess) e = dalloc(&h->rank, (size_t)g.N * g.R);
     if (e == hipSuccess) e = dalloc(&h->wfold, (size_t)g.P * g.R);
     if (e == hipSuccess) e = dalloc(&h->fit, (size_t)g.N * g.R);
-    if (e == hipSuccess && cfg->problem != ES_PROB_NONE && cfg->problem != ES_PROB_MLP)
+    if (e == hipSuccess && ((cfg->problem != ES_PROB_NONE && cfg->problem != ES_PROB_MLP) || cfg->w_decay != 0.0f))
         e = dalloc(&h->partial, (size_t)eval_partial_elems(g, h->plan));
+    if (e == hipSuccess && cfg->w_decay != 0.0f) e = dalloc(&h->pen, (size_t)g.N * g.R);
+    if (e == hipSuccess) e = dalloc(&h->hp[0], 2 * (size_t)g.R);
+    if (e == hipSuccess) e = dalloc(&h->hp[1], 2 * (size_t)g.R);
     if (e == hipSuccess && (cfg->problem == ES_PROB_SHIFTED_SPHERE || cfg->problem == ES_PROB_MLP))
         e = dalloc(&h->pdata, (size_t)g.Dp);
     if (e == hipSuccess && cfg->problem == ES_PROB_MLP)
@@ -325,8 +351,9 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     float* tab = static_cast<float*>(std::malloc(sizeof(float) * (size_t)g.N));
     uint32_t* ok = static_cast<uint32_t*>(std::malloc(sizeof(uint32_t) * (size_t)g.R));
     float* bf = static_cast<float*>(std::malloc(sizeof(float) * (size_t)g.R));
-    if (!tab || !ok || !bf) {
-        std::free(tab); std::free(ok); std::free(bf);
+    float* hp = static_cast<float*>(std::malloc(sizeof(float) * 2 * (size_t)g.R));
+    if (!tab || !ok || !bf || !hp) {
+        std::free(tab); std::free(ok); std::free(bf); std::free(hp);
         free_all(h);
         delete h;
         return init_fail(ES_ERR_OOM, "host allocation failed");
@@ -335,12 +362,15 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     for (int32_t r = 0; r < g.R; ++r) {
         ok[r] = 0xFF800000u;  // order key of +inf: nothing is an improvement over it but a finite key
         bf[r] = NAN;
+        hp[r] = cfg->sigma;
+        hp[g.R + r] = cfg->lr;
     }
     e = hipMemcpyAsync(h->table, tab, sizeof(float) * (size_t)g.N, hipMemcpyHostToDevice, h->stream);
     if (e == hipSuccess) e = hipMemcpyAsync(h->best_okey, ok, sizeof(uint32_t) * (size_t)g.R, hipMemcpyHostToDevice, h->stream);
     if (e == hipSuccess) e = hipMemcpyAsync(h->best_f, bf, sizeof(float) * (size_t)g.R, hipMemcpyHostToDevice, h->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(h->hp[0], hp, sizeof(float) * 2 * (size_t)g.R, hipMemcpyHostToDevice, h->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);  // host staging buffers are freed next
-    std::free(tab); std::free(ok); std::free(bf);
+    std::free(tab); std::free(ok); std::free(bf); std::free(hp);
     if (e == hipSuccess) e = launch_init(g, *cfg, h->m, h->m1, h->v, h->best_x, h->stream);
     if (e == hipSuccess && h->pdata) e = launch_problem_data(g, *cfg, h->pdata, h->stream);
     if (e == hipSuccess && h->mlp_scratch) e = launch_mlp_setup(h->pdata, h->mlp_scratch, h->stream);
@@ -358,7 +388,8 @@ es_status es_ask(es_handle* h, float* x_out)
 {
     if (!h) return ES_ERR_ARG;
     if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_ask: previous generation was not told");
-    if (x_out) ES_HIP(h, launch_ask(h->g, h->cfg, (uint32_t)h->t, h->m, x_out, h->stream), "ask kernel");
+    if (x_out)
+        ES_HIP(h, launch_ask(h->g, h->cfg, (uint32_t)h->t, h->m, x_out, h->hp[h->hp_cur], h->stream), "ask kernel");
     h->phase = ASKED;
     h->err[0] = 0;
     return ES_OK;
@@ -390,7 +421,7 @@ es_status es_run(es_handle* h, int32_t T, float* log)
     if (h->cfg.problem == ES_PROB_NONE) return fail(h, ES_ERR_UNSUPPORTED, "es_run needs a built-in problem");
     if (T == 0) return ES_OK;
     if (h->t + T > 0xFFFFFFFFll) return fail(h, ES_ERR_ARG, "es_run: generation counter would exceed 2^32");
-    const bool fused_ok = fused_supported(h->g, h->plan, h->cfg.problem);
+    const bool fused_ok = fused_supported(h->g, h->plan, h->cfg);
     // the fused loop pays off when each run is small: per-call launches then
     // dominate, and the runs fill the chip one workgroup each
     const bool fused = h->run_path == 2 ? fused_ok
@@ -400,7 +431,8 @@ es_status es_run(es_handle* h, int32_t T, float* log)
         es_status s = stage_adam(h, T);
         if (s != ES_OK) return s;
         ES_HIP(h, launch_run_fused(h->g, h->cfg, h->plan, (uint32_t)h->t, T, h->adam_dev, h->m, h->m1, h->v,
-                                   h->best_x, h->best_okey, h->best_f, h->pdata, h->table, log, h->stream),
+                                   h->best_x, h->best_okey, h->best_f, h->pdata, h->table, log,
+                                   h->hp[h->hp_cur], h->stream),
                "fused generation loop");
         h->t += T;
         return ES_OK;
@@ -469,6 +501,46 @@ es_status es_get_grad(es_handle* h, float* g)
     return copy_rows_out(h, g, h->grad);
 }
 
+es_status es_set_hparams(es_handle* h, const float* sigma, const float* lr)
+{
+    if (!h) return ES_ERR_ARG;
+    if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_set_hparams: an ask is open");
+    const int32_t R = h->g.R;
+    for (int32_t r = 0; r < R; ++r) {
+        if (sigma && (!(sigma[r] > 0.0f) || !std::isfinite(sigma[r])))
+            return fail(h, ES_ERR_ARG, "es_set_hparams: sigma[%d] must be finite and > 0", r);
+        if (lr && (!(lr[r] >= 0.0f) || !std::isfinite(lr[r])))
+            return fail(h, ES_ERR_ARG, "es_set_hparams: lr[%d] must be finite and >= 0", r);
+    }
+    float* d = h->hp[h->hp_cur];
+    // synchronous copies: the caller's host arrays may be reused on return
+    if (sigma) ES_HIP(h, hipMemcpyAsync(d, sigma, sizeof(float) * R, hipMemcpyHostToDevice, h->stream), "set sigma");
+    if (lr) ES_HIP(h, hipMemcpyAsync(d + R, lr, sizeof(float) * R, hipMemcpyHostToDevice, h->stream), "set lr");
+    ES_HIP(h, hipStreamSynchronize(h->stream), "set hparams");
+    return ES_OK;
+}
+
+es_status es_get_hparams(es_handle* h, float* sigma, float* lr)
+{
+    if (!h) return ES_ERR_ARG;
+    const int32_t R = h->g.R;
+    const float* d = h->hp[h->hp_cur];
+    if (sigma) ES_HIP(h, hipMemcpyAsync(sigma, d, sizeof(float) * R, hipMemcpyDeviceToHost, h->stream), "get sigma");
+    if (lr) ES_HIP(h, hipMemcpyAsync(lr, d + R, sizeof(float) * R, hipMemcpyDeviceToHost, h->stream), "get lr");
+    ES_HIP(h, hipStreamSynchronize(h->stream), "get hparams");
+    return ES_OK;
+}
+
+es_status es_get_penalty(es_handle* h, float* pen)
+{
+    if (!h || !pen) return h ? fail(h, ES_ERR_ARG, "es_get_penalty: null buffer") : ES_ERR_ARG;
+    if (!h->pen) return fail(h, ES_ERR_UNSUPPORTED, "es_get_penalty needs w_decay > 0");
+    ES_HIP(h, hipMemcpyAsync(pen, h->pen, sizeof(float) * (size_t)h->g.N * h->g.R, hipMemcpyDeviceToDevice,
+                             h->stream),
+           "copy penalty");
+    return ES_OK;
+}
+
 es_status es_get_problem_data(es_handle* h, float* out)
 {
     if (!h || !out) return h ? fail(h, ES_ERR_ARG, "es_get_problem_data: null buffer") : ES_ERR_ARG;
@@ -492,7 +564,7 @@ es_status es_save_state(es_handle* h, void* host_buf, size_t* bytes)
     if (!h || !bytes) return ES_ERR_ARG;
     const Geometry& g = h->g;
     const size_t rows = (size_t)g.Dp * g.R * sizeof(float);
-    const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + sizeof(float));
+    const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + 3 * sizeof(float));
     if (!host_buf) {
         *bytes = need;
         return ES_OK;
@@ -518,6 +590,9 @@ es_status es_save_state(es_handle* h, void* host_buf, size_t* bytes)
     ES_HIP(h, hipMemcpyAsync(p, h->best_okey, g.R * sizeof(uint32_t), hipMemcpyDeviceToHost, h->stream), "save best");
     p += g.R * sizeof(uint32_t);
     ES_HIP(h, hipMemcpyAsync(p, h->best_f, g.R * sizeof(float), hipMemcpyDeviceToHost, h->stream), "save best");
+    p += g.R * sizeof(float);
+    ES_HIP(h, hipMemcpyAsync(p, h->hp[h->hp_cur], 2 * g.R * sizeof(float), hipMemcpyDeviceToHost, h->stream),
+           "save sigma and lr");
     ES_HIP(h, hipStreamSynchronize(h->stream), "save sync");
     *bytes = need;
     return ES_OK;
@@ -529,7 +604,7 @@ es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes)
     if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_load_state: an ask is open");
     const Geometry& g = h->g;
     const size_t rows = (size_t)g.Dp * g.R * sizeof(float);
-    const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + sizeof(float));
+    const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + 3 * sizeof(float));
     if (bytes < need) return fail(h, ES_ERR_ARG, "es_load_state: checkpoint too small");
     CkptHeader hd;
     std::memcpy(&hd, host_buf, sizeof(hd));
@@ -546,6 +621,9 @@ es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes)
     ES_HIP(h, hipMemcpyAsync(h->best_okey, p, g.R * sizeof(uint32_t), hipMemcpyHostToDevice, h->stream), "load best");
     p += g.R * sizeof(uint32_t);
     ES_HIP(h, hipMemcpyAsync(h->best_f, p, g.R * sizeof(float), hipMemcpyHostToDevice, h->stream), "load best");
+    p += g.R * sizeof(float);
+    ES_HIP(h, hipMemcpyAsync(h->hp[h->hp_cur], p, 2 * g.R * sizeof(float), hipMemcpyHostToDevice, h->stream),
+           "load sigma and lr");
     ES_HIP(h, hipStreamSynchronize(h->stream), "load sync");
     h->t = hd.t;
     return ES_OK;

@@ -21,8 +21,9 @@ struct Geometry {
 };
 
 // Adam constants of one step (host-rounded to fp32).
+// Adam constants of one generation (the learning rate is per run, beside sigma).
 struct AdamConsts {
-    float lr, beta1, beta2, omb1, omb2, bc1, bc2, eps;
+    float beta1, beta2, omb1, omb2, bc1, bc2, eps;
 };
 
 // Geometry of the fused sample+evaluate launch: pair groups of `wg` lanes,
@@ -40,14 +41,16 @@ int64_t eval_partial_elems(const Geometry& g, const EvalPlan& e);  // floats
 hipError_t launch_init(const Geometry& g, const es_config& c, float* m, float* m1, float* v,
                        float* best_x, hipStream_t s);
 hipError_t launch_problem_data(const Geometry& g, const es_config& c, float* pdata, hipStream_t s);
+// hp: device [2][R], sigma then lr of every run for the current generation.
 hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const float* m, float* x,
-                      hipStream_t s);
+                      const float* hp, hipStream_t s);
 hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t,
                             const float* m, const float* pdata, float* partial, float* fit,
-                            hipStream_t s);
-hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* table,
-                       float* y, int32_t* rank, float* wfold, uint32_t* best_okey, float* best_f,
-                       int32_t* best_j, float* gen_best, hipStream_t s);
+                            const float* hp, double div, hipStream_t s);
+hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* pen,
+                       const float* table, float* y, int32_t* rank, float* wfold, uint32_t* best_okey,
+                       float* best_f, int32_t* best_j, float* gen_best, const float* hp_cur, float* hp_next,
+                       hipStream_t s);
 // Split of the gradient kernel's pairs: ps pair slices (one wave each) per
 // workgroup, nsplit workgroups per group of 64 Philox blocks.  With nsplit > 1
 // every workgroup stores its partial sums (part, fp64 [R][nsplit][nb][4]) and
@@ -59,8 +62,8 @@ struct TellPlan {
 TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit);
 size_t tell_part_elems(const Geometry& g, const TellPlan& tp);
 hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp, uint32_t t, const AdamConsts& a,
-                       double inv_ns, const float* wfold, const int32_t* best_j, float* m,
-                       float* m1, float* v, float* grad, float* best_x, double* part, hipStream_t s);
+                       const float* wfold, const int32_t* best_j, float* m, float* m1, float* v, float* grad,
+                       float* best_x, double* part, const float* hp, hipStream_t s);
 hipError_t launch_debug_noise(const Geometry& g, const es_config& c, int32_t run, uint32_t t,
                               int32_t pair, uint32_t* words, float* eps, hipStream_t s);
 
@@ -71,11 +74,11 @@ int32_t tell_slices(const Geometry& g);
 // Fused multi-generation loop (one workgroup per run, state in LDS).
 constexpr size_t FUSED_MAX_LDS = 60 * 1024;
 size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e);
-bool fused_supported(const Geometry& g, const EvalPlan& e, int problem);
+bool fused_supported(const Geometry& g, const EvalPlan& e, const es_config& c);
 hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t0, int32_t T,
                             const AdamConsts* adam, float* m, float* m1, float* v, float* best_x,
                             uint32_t* best_okey, float* best_f, const float* pdata, const float* table, float* log,
-                            hipStream_t s);
+                            float* hp, hipStream_t s);
 
 // Neuroevolution problem (64-256-256-16 MLP vs a teacher).
 constexpr int64_t MLP_NUM_PARAMS = 86544;
@@ -83,7 +86,7 @@ size_t mlp_scratch_bytes();  // X_t (fp32 and bf16), teacher outputs, transposed
 hipError_t launch_mlp_setup(const float* teacher, void* scratch, hipStream_t s);
 size_t mlp_lds_bytes();
 hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, const float* m, const float* teacher,
-                           void* scratch, float* fit, hipStream_t s);
+                           void* scratch, float* fit, const float* hp, hipStream_t s);
 
 // Largest population the rank kernel stages in LDS.
 constexpr int32_t RANK_MAX_N = 16384;

@@ -98,7 +98,7 @@ __global__ void k_problem_data(float* __restrict__ out, uint64_t seed, int64_t D
 
 // ---------------------------------------------------------------------------
 __global__ void k_ask(const float* __restrict__ m, float* __restrict__ x, uint64_t seed, uint32_t t,
-                      int64_t D, int64_t nb, int32_t N, int32_t P, int32_t R, float sigma)
+                      int64_t D, int64_t nb, int32_t N, int32_t P, int32_t R, const float* __restrict__ hp)
 {
     const int64_t total = (int64_t)R * P * nb;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
@@ -111,6 +111,7 @@ __global__ void k_ask(const float* __restrict__ m, float* __restrict__ x, uint64
         const float* mr = m + r * 4 * nb;
         float* xp = x + (r * N + p) * D;
         float* xm = x + (r * N + p + P) * D;
+        const float sigma = hp[r];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int64_t d = 4 * b + k;
@@ -288,9 +289,10 @@ template <int PROB>
 __global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
     const float* __restrict__ m, const float* __restrict__ pdata, float* __restrict__ partial,
     uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t N, int32_t P, int64_t bc, int64_t nchunks,
-    int32_t n_pg, float sigma, float ra)
+    int32_t n_pg, const float* __restrict__ hp, float ra)
 {
     const int32_t r = blockIdx.y;
+    const float sigma = hp[r];
     const uint32_t w = blockIdx.x;
     const uint32_t slot = w >> 3, xcd = w & 7u;
     const int32_t pg = (int32_t)(slot % (uint32_t)n_pg);
@@ -314,11 +316,12 @@ __global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
     }
 }
 
-// fit[r][j] = add + sum over chunks (fixed order) of the partials.
+// fit[r][j] = (add + sum over chunks (fixed order) of the partials) / div
+// (div = 1 for fitness, D for the weight-decay mean square).
 // Workgroup = 64 members x RED_SLICES chunk slices.
 __global__ __launch_bounds__(64 * RED_SLICES) void k_eval_reduce(const float* __restrict__ partial,
                                                                  float* __restrict__ fit, int32_t N, int32_t R,
-                                                                 int64_t nchunks, double add)
+                                                                 int64_t nchunks, double add, double div)
 {
     __shared__ double red[RED_SLICES][64];
     const int32_t r = blockIdx.y;
@@ -345,27 +348,119 @@ __global__ __launch_bounds__(64 * RED_SLICES) void k_eval_reduce(const float* __
         double tot = add;
 #pragma unroll
         for (int q = 0; q < RED_SLICES; ++q) tot += red[q][tx];
-        fit[(int64_t)r * N + j] = (float)tot;
+        fit[(int64_t)r * N + j] = (float)(tot / div);
     }
 }
 
 // ---------------------------------------------------------------------------
-// Centered ranks.  Workgroup = RANK_PAIRS pairs x RANK_SLICES key slices of
-// one run; the run's order keys sit in LDS.  rank_j counts keys that sort
-// before j in a stable ascending order: smaller key, or equal key and lower
-// index.
+// Fitness shaping (Sec. 3.2).  Workgroup = RANK_PAIRS pairs x RANK_SLICES key
+// slices of one run; the run's order keys sit in LDS.  The shaped key is the
+// fitness (negated when maximising, NaN the worst) plus, with weight decay,
+// fl32(w * pen_j) for a finite key.  rank_j counts keys that sort before j in
+// a stable ascending order: smaller key, or equal key and lower index.
+// y_j: centered-rank table entry, the key itself (raw), or its z-score over
+// the finite keys (fp64 mean and population deviation, reduced in a fixed
+// order that every workgroup of the run repeats).  The first workgroup of a
+// run also steps the run's sigma and learning-rate schedules.
+struct ShapeArgs {
+    const float* pen;       // [R][N] mean-square penalty or null
+    const float* hp_cur;    // [2][R]: sigma, lr of this generation
+    float* hp_next;         // [2][R]: after the schedule step
+    float w_decay;
+    float sigma_decay, sigma_final, lr_decay, lr_final;
+    int32_t shaping;        // es_shaping
+    int32_t maximize;
+};
+
+__device__ __forceinline__ float shaped_key(float f, float pen, int maximize, float w_decay)
+{
+    float k = maximize ? -f : f;
+    if (k != k) return __builtin_inff();
+    if (w_decay != 0.0f && __builtin_isfinite(k)) k = __fadd_rn(k, __fmul_rn(w_decay, pen));
+    return k;
+}
+
+__device__ __forceinline__ float key_value(uint32_t K)
+{
+    return __uint_as_float((K & 0x80000000u) ? (K & 0x7FFFFFFFu) : ~K);
+}
+
+__device__ __forceinline__ float schedule_step(float x, float decay, float final)
+{
+    const float y = __fmul_rn(x, decay);
+    return y > final ? y : final;
+}
+
+// Sum of v over the workgroup in a fixed tree order (blockDim.x = 256).
+__device__ __forceinline__ double block_sum(double v, double* red)
+{
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int w = RANK_PAIRS * RANK_SLICES / 2; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    const double out = red[0];
+    __syncthreads();
+    return out;
+}
+
 __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
     const float* __restrict__ fit, const float* __restrict__ table, float* __restrict__ y,
     int32_t* __restrict__ rank, float* __restrict__ wfold, uint32_t* __restrict__ best_okey,
     float* __restrict__ best_f, int32_t* __restrict__ best_j, float* __restrict__ gen_best, int32_t N,
-    int32_t P, int32_t maximize, int32_t raw)
+    int32_t P, int32_t R, ShapeArgs sa)
 {
     extern __shared__ uint32_t keys[];
     __shared__ int32_t cnt[RANK_SLICES][RANK_PAIRS][2];
+    __shared__ double red[RANK_PAIRS * RANK_SLICES];
+    __shared__ uint32_t raw_best[2];
     const int32_t r = blockIdx.y;
     const float* __restrict__ fr = fit + (int64_t)r * N;
-    for (int32_t k = threadIdx.x; k < N; k += blockDim.x) keys[k] = order_key(fr[k], maximize);
+    const float* __restrict__ pr = sa.pen ? sa.pen + (int64_t)r * N : nullptr;
+    for (int32_t k = threadIdx.x; k < N; k += blockDim.x)
+        keys[k] = order_key(shaped_key(fr[k], pr ? pr[k] : 0.0f, sa.maximize, sa.w_decay), 0);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        sa.hp_next[r] = schedule_step(sa.hp_cur[r], sa.sigma_decay, sa.sigma_final);
+        sa.hp_next[R + r] = schedule_step(sa.hp_cur[R + r], sa.lr_decay, sa.lr_final);
+    }
     __syncthreads();
+
+    double mu = 0.0, inv_sd = 0.0;
+    if (sa.shaping == ES_SHAPE_Z_SCORE) {
+        double sum = 0.0, n = 0.0;
+        for (int32_t k = threadIdx.x; k < N; k += blockDim.x) {
+            const float v = key_value(keys[k]);
+            if (__builtin_isfinite(v)) { sum += (double)v; n += 1.0; }
+        }
+        sum = block_sum(sum, red);
+        n = block_sum(n, red);
+        mu = n > 0.0 ? sum / n : 0.0;
+        double ss = 0.0;
+        for (int32_t k = threadIdx.x; k < N; k += blockDim.x) {
+            const float v = key_value(keys[k]);
+            if (__builtin_isfinite(v)) ss += ((double)v - mu) * ((double)v - mu);
+        }
+        ss = block_sum(ss, red);
+        const double sd = n > 0.0 ? sqrt(ss / n) : 0.0;
+        inv_sd = sd + 1e-10;
+    }
+    // With weight decay the best-so-far still follows the raw fitness: the
+    // smallest raw key, lowest index first.
+    const bool penalised = sa.w_decay != 0.0f;
+    if (penalised) {
+        if (threadIdx.x == 0) { raw_best[0] = 0xFFFFFFFFu; raw_best[1] = 0xFFFFFFFFu; }
+        __syncthreads();
+        uint32_t bk = 0xFFFFFFFFu, bj = 0xFFFFFFFFu;
+        for (int32_t k = threadIdx.x; k < N; k += blockDim.x) {
+            const uint32_t K = order_key(fr[k], sa.maximize);
+            if (K < bk) { bk = K; bj = (uint32_t)k; }
+        }
+        atomicMin(&raw_best[0], bk);
+        __syncthreads();
+        if (bk == raw_best[0]) atomicMin(&raw_best[1], bj);
+        __syncthreads();
+    }
 
     const int32_t tx = threadIdx.x % RANK_PAIRS, s = threadIdx.x / RANK_PAIRS;
     const int32_t p = blockIdx.x * RANK_PAIRS + tx;
@@ -405,9 +500,14 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
     }
     const float f1 = fr[j1], f2 = fr[j2];
     float y1, y2;
-    if (raw) {
-        y1 = maximize ? -f1 : f1;
-        y2 = maximize ? -f2 : f2;
+    if (sa.shaping == ES_SHAPE_RAW) {
+        // the key itself; without weight decay the fitness keeps its NaN and sign of zero
+        y1 = penalised ? shaped_key(f1, pr[j1], sa.maximize, sa.w_decay) : (sa.maximize ? -f1 : f1);
+        y2 = penalised ? shaped_key(f2, pr[j2], sa.maximize, sa.w_decay) : (sa.maximize ? -f2 : f2);
+    } else if (sa.shaping == ES_SHAPE_Z_SCORE) {
+        const float v1 = key_value(K1), v2 = key_value(K2);
+        y1 = __builtin_isfinite(v1) ? (float)(((double)v1 - mu) / inv_sd) : 0.0f;
+        y2 = __builtin_isfinite(v2) ? (float)(((double)v2 - mu) / inv_sd) : 0.0f;
     } else {
         y1 = table[r1];
         y2 = table[r2];
@@ -419,9 +519,15 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
     rr[j1] = r1;
     rr[j2] = r2;
     wfold[(int64_t)r * P + p] = y1 - y2;
-    if (r1 == 0 || r2 == 0) {
-        const int32_t jb = r1 == 0 ? j1 : j2;
-        const uint32_t kb0 = r1 == 0 ? K1 : K2;
+    int32_t jb = -1;
+    if (penalised) {
+        if ((uint32_t)j1 == raw_best[1]) jb = j1;
+        if ((uint32_t)j2 == raw_best[1]) jb = j2;
+    } else if (r1 == 0 || r2 == 0) {
+        jb = r1 == 0 ? j1 : j2;
+    }
+    if (jb >= 0) {
+        const uint32_t kb0 = order_key(fr[jb], sa.maximize);
         if (gen_best) gen_best[r] = fr[jb];
         if (kb0 < best_okey[r]) {
             best_okey[r] = kb0;
@@ -480,7 +586,7 @@ __device__ __forceinline__ void tell_slice(const float* __restrict__ wr, uint32_
 
 // g = sum / (N sigma), then Adam (Kingma & Ba) in fp32 in a fixed operation
 // order on four dims; dims at or beyond D stay zero.
-__device__ __forceinline__ void adam_block(const double a64[4], double inv_ns, const AdamConsts& ac, int64_t d0,
+__device__ __forceinline__ void adam_block(const double a64[4], double inv_ns, const AdamConsts& ac, float lr, int64_t d0,
                                            int64_t D, const float mo[4], const float m1o[4], const float vo[4],
                                            float mn[4], float m1n[4], float vn[4], float gg[4])
 {
@@ -494,7 +600,7 @@ __device__ __forceinline__ void adam_block(const double a64[4], double inv_ns, c
         const float vhat = nv / ac.bc2;
         const float den = __fadd_rn(sqrtf(vhat), ac.eps);
         const float q = mhat / den;
-        mn[k] = __builtin_fmaf(-ac.lr, q, mo[k]);
+        mn[k] = __builtin_fmaf(-lr, q, mo[k]);
         m1n[k] = nm1;
         vn[k] = nv;
         if (d0 + k >= D) { mn[k] = 0.f; m1n[k] = 0.f; vn[k] = 0.f; gg[k] = 0.f; }
@@ -505,7 +611,7 @@ __device__ __forceinline__ void adam_block(const double a64[4], double inv_ns, c
 // parameters when the generation improved on the best so far, and the
 // gradient itself when asked for.
 __device__ __forceinline__ void tell_finish(const double a64[4], int64_t b, int32_t r, uint32_t k0, uint32_t k1,
-                                            uint32_t t, int64_t D, int64_t nb, int32_t P, float sigma, double inv_ns,
+                                            uint32_t t, int64_t D, int64_t nb, int32_t P, float sigma, float lr,
                                             const AdamConsts& ac, const int32_t* __restrict__ best_j,
                                             float* __restrict__ m, float* __restrict__ m1, float* __restrict__ v,
                                             float* __restrict__ grad, float* __restrict__ best_x)
@@ -518,7 +624,8 @@ __device__ __forceinline__ void tell_finish(const double a64[4], int64_t b, int3
     const float m1o[4] = {m14.x, m14.y, m14.z, m14.w};
     const float vo[4] = {v4.x, v4.y, v4.z, v4.w};
     float mn[4], m1n[4], vn[4], gg[4];
-    adam_block(a64, inv_ns, ac, 4 * b, D, mo, m1o, vo, mn, m1n, vn, gg);
+    const double inv_ns = 1.0 / (2.0 * (double)P * (double)sigma);  // 1 / (N sigma)
+    adam_block(a64, inv_ns, ac, lr, 4 * b, D, mo, m1o, vo, mn, m1n, vn, gg);
     const int32_t jb = best_j[r];
     if (jb >= 0) {
         const int32_t pbst = jb < P ? jb : jb - P;
@@ -549,7 +656,7 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(
     const float* __restrict__ wfold, const int32_t* __restrict__ best_j, float* __restrict__ m,
     float* __restrict__ m1, float* __restrict__ v, float* __restrict__ grad,
     float* __restrict__ best_x, uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t P, int32_t ps,
-    int32_t nsplit, double* __restrict__ part, float sigma, double inv_ns, AdamConsts ac)
+    int32_t nsplit, double* __restrict__ part, const float* __restrict__ hp, int32_t R, AdamConsts ac)
 {
     __shared__ double red[TELL_MAX_PS - 1][TELL_LANES][4];
     const int32_t r = blockIdx.y, z = blockIdx.z;
@@ -580,7 +687,7 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(
             make_double4(a64[0], a64[1], a64[2], a64[3]);
         return;
     }
-    tell_finish(a64, b, r, k0, k1, t, D, nb, P, sigma, inv_ns, ac, best_j, m, m1, v, grad, best_x);
+    tell_finish(a64, b, r, k0, k1, t, D, nb, P, hp[r], hp[R + r], ac, best_j, m, m1, v, grad, best_x);
 }
 
 // Second half of a split gradient: the nsplit workgroup sums of each Philox
@@ -589,8 +696,8 @@ __global__ __launch_bounds__(256) void k_tell_fold(const double* __restrict__ pa
                                                    float* __restrict__ m, float* __restrict__ m1,
                                                    float* __restrict__ v, float* __restrict__ grad,
                                                    float* __restrict__ best_x, uint64_t seed, uint32_t t, int64_t D,
-                                                   int64_t nb, int32_t P, int32_t nsplit, float sigma,
-                                                   double inv_ns, AdamConsts ac)
+                                                   int64_t nb, int32_t P, int32_t nsplit,
+                                                   const float* __restrict__ hp, int32_t R, AdamConsts ac)
 {
     const int32_t r = blockIdx.y;
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -604,7 +711,7 @@ __global__ __launch_bounds__(256) void k_tell_fold(const double* __restrict__ pa
         const double4 qq = *reinterpret_cast<const double4*>(p0 + (int64_t)q * nb * 4);
         a64[0] += qq.x; a64[1] += qq.y; a64[2] += qq.z; a64[3] += qq.w;
     }
-    tell_finish(a64, b, r, k0, k1, t, D, nb, P, sigma, inv_ns, ac, best_j, m, m1, v, grad, best_x);
+    tell_finish(a64, b, r, k0, k1, t, D, nb, P, hp[r], hp[R + r], ac, best_j, m, m1, v, grad, best_x);
 }
 
 // ---------------------------------------------------------------------------
@@ -631,9 +738,11 @@ struct FusedArgs {
     int32_t N, P, R;
     int64_t bc, nchunks;
     int32_t ps;
-    float sigma, ra;
-    double add, inv_ns;
+    float ra;
+    double add;
     int32_t maximize, raw;
+    float* hp;               // [2][R] sigma, lr: read at the start, the schedule's values written at the end
+    float sigma_decay, sigma_final, lr_decay, lr_final;
 };
 
 template <int PROB>
@@ -657,6 +766,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
     const uint64_t key = a.seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
     const int64_t goff = (int64_t)r * Dp;
+    float sigma = a.hp[r], lr = a.hp[a.R + r];
     for (int64_t i = threadIdx.x; i < Dp; i += blockDim.x) {
         ms[i] = a.m[goff + i];
         m1s[i] = a.m1[goff + i];
@@ -673,7 +783,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             const int64_t c = i / a.P;
             const int64_t b0 = c * a.bc, b1 = b0 + a.bc < a.nb ? b0 + a.bc : a.nb;
             double accp, accm;
-            eval_chunk<PROB, LANES_BLOCK_AND_ROW>(ms, a.pdata, k0, k1, (uint32_t)p, t, b0, b1, a.D, a.sigma, a.ra,
+            eval_chunk<PROB, LANES_BLOCK_AND_ROW>(ms, a.pdata, k0, k1, (uint32_t)p, t, b0, b1, a.D, sigma, a.ra,
                                                   accp, accm);
             part[c * a.N + p] = (float)accp;
             part[c * a.N + p + a.P] = (float)accm;
@@ -726,6 +836,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         }
         __syncthreads();
         const int32_t jb = best_j;
+        const double inv_ns = 1.0 / (2.0 * (double)a.P * (double)sigma);  // 1 / (N sigma)
         for (int64_t b = threadIdx.x; b < a.nb; b += blockDim.x) {
             double a64[4];
 #pragma unroll
@@ -741,10 +852,10 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
                 m1o[k] = m1s[4 * b + k];
                 vo[k] = vs[4 * b + k];
             }
-            adam_block(a64, a.inv_ns, ac, 4 * b, a.D, mo, m1o, vo, mn, m1n, vn, gg);
+            adam_block(a64, inv_ns, ac, lr, 4 * b, a.D, mo, m1o, vo, mn, m1n, vn, gg);
             if (jb >= 0) {
                 const int32_t pbst = jb < a.P ? jb : jb - a.P;
-                const float sg = jb < a.P ? a.sigma : -a.sigma;
+                const float sg = jb < a.P ? sigma : -sigma;
                 float e[4];
                 box_muller4(philox4x32_10<LANES_BLOCK_AND_ROW>(k0, k1, (uint32_t)b, (uint32_t)pbst, t, DOM_NOISE),
                             e);
@@ -759,6 +870,12 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             }
         }
         __syncthreads();
+        sigma = schedule_step(sigma, a.sigma_decay, a.sigma_final);
+        lr = schedule_step(lr, a.lr_decay, a.lr_final);
+    }
+    if (threadIdx.x == 0) {
+        a.hp[r] = sigma;
+        a.hp[a.R + r] = lr;
     }
     for (int64_t i = threadIdx.x; i < Dp; i += blockDim.x) {
         a.m[goff + i] = ms[i];
@@ -841,16 +958,16 @@ hipError_t launch_problem_data(const Geometry& g, const es_config& c, float* pda
 }
 
 hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const float* m, float* x,
-                      hipStream_t s)
+                      const float* hp, hipStream_t s)
 {
     k_ask<<<grid_for((int64_t)g.R * g.P * g.nb, 256), 256, 0, s>>>(m, x, c.seed, t, g.D, g.nb, g.N, g.P,
-                                                                   g.R, c.sigma);
+                                                                   g.R, hp);
     return hipGetLastError();
 }
 
 hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t,
                             const float* m, const float* pdata, float* partial, float* fit,
-                            hipStream_t s)
+                            const float* hp, double div, hipStream_t s)
 {
     // chunk ids are dealt so that the pair groups of one chunk share an XCD
     const int64_t slots = (e.nchunks + 7) / 8 * e.n_pg;
@@ -858,7 +975,7 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
     const dim3 block((unsigned)e.wg);
 #define ES_EVAL_LAUNCH(PROB)                                                                                   \
     k_eval_bbob<PROB><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N, g.P, e.bc, e.nchunks, \
-                                             e.n_pg, c.sigma, c.rastrigin_a)
+                                             e.n_pg, hp, c.rastrigin_a)
     switch (c.problem) {
     case ES_PROB_SPHERE: ES_EVAL_LAUNCH(ES_PROB_SPHERE); break;
     case ES_PROB_SHIFTED_SPHERE: ES_EVAL_LAUNCH(ES_PROB_SHIFTED_SPHERE); break;
@@ -871,34 +988,45 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
     if (err != hipSuccess) return err;
     const double add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;
     k_eval_reduce<<<dim3((unsigned)((g.N + 63) / 64), (unsigned)g.R), 64 * RED_SLICES, 0, s>>>(partial, fit, g.N,
-                                                                                            g.R, e.nchunks, add);
+                                                                                            g.R, e.nchunks, add, div);
     return hipGetLastError();
 }
 
-hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* table,
-                       float* y, int32_t* rank, float* wfold, uint32_t* best_okey, float* best_f,
-                       int32_t* best_j, float* gen_best, hipStream_t s)
+hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* pen,
+                       const float* table, float* y, int32_t* rank, float* wfold, uint32_t* best_okey,
+                       float* best_f, int32_t* best_j, float* gen_best, const float* hp_cur, float* hp_next,
+                       hipStream_t s)
 {
     const dim3 grid((unsigned)((g.P + RANK_PAIRS - 1) / RANK_PAIRS), (unsigned)g.R);
     const size_t lds = sizeof(uint32_t) * (size_t)g.N;
+    ShapeArgs sa;
+    sa.pen = c.w_decay != 0.0f ? pen : nullptr;
+    sa.hp_cur = hp_cur;
+    sa.hp_next = hp_next;
+    sa.w_decay = c.w_decay;
+    sa.sigma_decay = c.sigma_decay;
+    sa.sigma_final = c.sigma_final;
+    sa.lr_decay = c.lr_decay;
+    sa.lr_final = c.lr_final;
+    sa.shaping = c.shaping;
+    sa.maximize = c.maximize;
     k_rank<<<grid, RANK_PAIRS * RANK_SLICES, lds, s>>>(fit, table, y, rank, wfold, best_okey, best_f, best_j,
-                                                       gen_best, g.N, g.P, c.maximize,
-                                                       c.shaping == ES_SHAPE_RAW);
+                                                       gen_best, g.N, g.P, g.R, sa);
     return hipGetLastError();
 }
 
 hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp, uint32_t t, const AdamConsts& a,
-                       double inv_ns, const float* wfold, const int32_t* best_j, float* m,
-                       float* m1, float* v, float* grad, float* best_x, double* part, hipStream_t s)
+                       const float* wfold, const int32_t* best_j, float* m, float* m1, float* v, float* grad,
+                       float* best_x, double* part, const float* hp, hipStream_t s)
 {
     const dim3 grid((unsigned)((g.nb + TELL_LANES - 1) / TELL_LANES), (unsigned)g.R, (unsigned)tp.nsplit);
     k_tell<<<grid, TELL_LANES * tp.ps, 0, s>>>(wfold, best_j, m, m1, v, grad, best_x, c.seed, t, g.D, g.nb, g.P,
-                                               tp.ps, tp.nsplit, part, c.sigma, inv_ns, a);
+                                               tp.ps, tp.nsplit, part, hp, g.R, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || tp.nsplit == 1) return e;
     const dim3 fgrid((unsigned)((g.nb + 255) / 256), (unsigned)g.R);
     k_tell_fold<<<fgrid, 256, 0, s>>>(part, best_j, m, m1, v, grad, best_x, c.seed, t, g.D, g.nb, g.P, tp.nsplit,
-                                      c.sigma, inv_ns, a);
+                                      hp, g.R, a);
     return hipGetLastError();
 }
 
@@ -945,25 +1073,28 @@ size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e)
     return red + f32;
 }
 
-bool fused_supported(const Geometry& g, const EvalPlan& e, int problem)
+bool fused_supported(const Geometry& g, const EvalPlan& e, const es_config& c)
 {
-    if (problem < ES_PROB_SPHERE || problem > ES_PROB_RASTRIGIN) return false;
+    if (c.problem < ES_PROB_SPHERE || c.problem > ES_PROB_RASTRIGIN) return false;
+    // the fused loop shapes by centered ranks or raw keys, without weight decay
+    if (c.shaping == ES_SHAPE_Z_SCORE || c.w_decay != 0.0f) return false;
     return fused_lds_bytes(g, e) <= FUSED_MAX_LDS;
 }
 
 hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t0, int32_t T,
                             const AdamConsts* adam, float* m, float* m1, float* v, float* best_x,
                             uint32_t* best_okey, float* best_f, const float* pdata, const float* table, float* log,
-                            hipStream_t s)
+                            float* hp, hipStream_t s)
 {
     FusedArgs a;
     a.m = m; a.m1 = m1; a.v = v; a.best_x = best_x; a.best_okey = best_okey; a.best_f = best_f;
     a.pdata = pdata; a.table = table; a.adam = adam; a.log = log;
     a.seed = c.seed; a.t0 = t0; a.T = T; a.D = g.D; a.nb = g.nb; a.N = g.N; a.P = g.P; a.R = g.R;
-    a.bc = e.bc; a.nchunks = e.nchunks; a.ps = tell_slices(g); a.sigma = c.sigma; a.ra = c.rastrigin_a;
+    a.bc = e.bc; a.nchunks = e.nchunks; a.ps = tell_slices(g); a.ra = c.rastrigin_a;
     a.add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;
-    a.inv_ns = 1.0 / ((double)g.N * (double)c.sigma);
     a.maximize = c.maximize; a.raw = c.shaping == ES_SHAPE_RAW;
+    a.hp = hp;
+    a.sigma_decay = c.sigma_decay; a.sigma_final = c.sigma_final; a.lr_decay = c.lr_decay; a.lr_final = c.lr_final;
     const size_t lds = fused_lds_bytes(g, e);
     switch (c.problem) {
     case ES_PROB_SPHERE: k_run_fused<ES_PROB_SPHERE><<<g.R, FUSED_WG, lds, s>>>(a); break;

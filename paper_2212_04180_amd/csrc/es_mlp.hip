@@ -169,7 +169,7 @@ __device__ __forceinline__ void layer2_act(const MlpSmem& S, const floatx4 (&acc
 __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restrict__ m, const __bf16* __restrict__ xb,
                                                           const float* __restrict__ yt, float* __restrict__ fit,
                                                           uint64_t seed, uint32_t t, int64_t Dp, int32_t N,
-                                                          int32_t P, float sigma, int32_t tanh_out)
+                                                          int32_t P, const float* __restrict__ hp, int32_t tanh_out)
 {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     MlpSmem& S = *reinterpret_cast<MlpSmem*>(smem_raw);
@@ -180,6 +180,7 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
     const uint64_t key = seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
     const float* __restrict__ mr = m + (int64_t)r * Dp;
+    const float sigma = hp[r];
 
     // ---- layer 1 and layer 3 weights, W2 chunk 0, all biases.  Each thread
     // owns seven weight blocks (W1: tid + 1024k, W3: tid, W2 chunk 0: tid and
@@ -452,7 +453,7 @@ hipError_t launch_mlp_setup(const float* teacher, void* scratch, hipStream_t s)
 size_t mlp_lds_bytes() { return sizeof(MlpSmem); }
 
 hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, const float* m, const float* teacher,
-                           void* scratch, float* fit, hipStream_t s)
+                           void* scratch, float* fit, const float* hp, hipStream_t s)
 {
     float* xf = static_cast<float*>(scratch);
     __bf16* xb = reinterpret_cast<__bf16*>(xf + MLP_BATCH * MLP_IN);
@@ -470,7 +471,7 @@ hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, co
         lds_attr_set = true;
     }
     k_eval_mlp<<<dim3((unsigned)g.P, (unsigned)g.R), MLP_THREADS, sizeof(MlpSmem), s>>>(
-        m, xb, yt, fit, c.seed, t, g.Dp, g.N, g.P, c.sigma, c.mlp_tanh_out);
+        m, xb, yt, fit, c.seed, t, g.Dp, g.N, g.P, hp, c.mlp_tanh_out);
     return hipGetLastError();
 }
 

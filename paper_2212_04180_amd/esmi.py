@@ -18,14 +18,15 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("ESMI_LIB") or os.path.join(_PKG, "libesmi.so")
 
 ES_OK, ES_ERR_ARG, ES_ERR_SEQUENCE, ES_ERR_HIP, ES_ERR_OOM, ES_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
-SHAPE_CENTERED_RANK, SHAPE_RAW = 0, 1
+SHAPE_CENTERED_RANK, SHAPE_RAW, SHAPE_Z_SCORE = 0, 1, 2
 PROB_NONE, PROB_SPHERE, PROB_SHIFTED_SPHERE, PROB_ROSENBROCK, PROB_RASTRIGIN, PROB_MLP = range(6)
 INIT_UNIFORM, INIT_ZERO, INIT_FANIN_NORMAL = range(3)
 FLAG_KEEP_GRAD = 1
 
 # Every symbol include/esmi.h declares, in declaration order.
 EXPORTS = ("es_init", "es_ask", "es_eval", "es_tell", "es_run", "es_get_state", "es_set_state",
-           "es_get_best", "es_get_shaped", "es_get_grad", "es_get_problem_data", "es_debug_noise",
+           "es_get_best", "es_get_shaped", "es_get_grad", "es_set_hparams", "es_get_hparams", "es_get_penalty",
+           "es_get_problem_data", "es_debug_noise",
            "es_save_state", "es_load_state", "es_sync", "es_generation", "es_last_error",
            "es_status_string", "es_destroy")
 
@@ -58,6 +59,12 @@ class _Config(ctypes.Structure):
         ("mlp_bf16", ctypes.c_int32),
         ("mlp_tanh_out", ctypes.c_int32),
         ("flags", ctypes.c_uint32),
+        ("sigma_decay", ctypes.c_float),
+        ("sigma_final", ctypes.c_float),
+        ("lr_decay", ctypes.c_float),
+        ("lr_final", ctypes.c_float),
+        ("w_decay", ctypes.c_float),
+        ("reserved", ctypes.c_uint32),
     ]
 
 
@@ -84,6 +91,13 @@ class ESConfig:
     mlp_bf16: int = 1
     mlp_tanh_out: int = 0
     flags: int = 0
+    # App. B schedules: after each tell x <- max(x * decay, final)
+    sigma_decay: float = 1.0
+    sigma_final: float = 0.0
+    lr_decay: float = 1.0
+    lr_final: float = 0.0
+    w_decay: float = 0.0  # weight-decay fitness regularisation (Sec. 3.2)
+    reserved: int = 0
 
     def cstruct(self) -> _Config:
         c = _Config()
@@ -117,6 +131,9 @@ def lib() -> ctypes.CDLL:
         "es_get_best": (i32, [vp, vp, vp]),
         "es_get_shaped": (i32, [vp, vp, vp]),
         "es_get_grad": (i32, [vp, vp]),
+        "es_set_hparams": (i32, [vp, vp, vp]),
+        "es_get_hparams": (i32, [vp, vp, vp]),
+        "es_get_penalty": (i32, [vp, vp]),
         "es_get_problem_data": (i32, [vp, vp]),
         "es_debug_noise": (i32, [vp, i32, i64, i32, vp, vp]),
         "es_save_state": (i32, [vp, vp, P(ctypes.c_size_t)]),
@@ -236,6 +253,30 @@ class ES:
         g = self._empty(self.R, self.D)
         self._check(lib().es_get_grad(self._h, _ptr(g)))
         return g
+
+    def set_hparams(self, sigma=None, lr=None):
+        """Per-run sigma and learning rate of the next generation (host arrays [R])."""
+        import numpy as np
+        bufs = []
+        for a in (sigma, lr):
+            if a is None:
+                bufs.append(None)
+            else:
+                b = np.ascontiguousarray(np.asarray(a, dtype=np.float32).reshape(self.R))
+                bufs.append(b)
+        ptr = [None if b is None else ctypes.c_void_p(b.ctypes.data) for b in bufs]
+        self._check(lib().es_set_hparams(self._h, ptr[0], ptr[1]))
+
+    def get_hparams(self):
+        import numpy as np
+        sg, lr = np.zeros(self.R, np.float32), np.zeros(self.R, np.float32)
+        self._check(lib().es_get_hparams(self._h, ctypes.c_void_p(sg.ctypes.data), ctypes.c_void_p(lr.ctypes.data)))
+        return sg, lr
+
+    def penalty(self):
+        out = self._empty(self.R, self.N)
+        self._check(lib().es_get_penalty(self._h, _ptr(out)))
+        return out
 
     def problem_data(self):
         out = self._empty(self.D)

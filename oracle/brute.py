@@ -239,3 +239,96 @@ class BruteES:
         self.sigma = max(f32(_q(self.sigma) * _q(self.sd)), self.sf)
         self.lr = max(f32(_q(self.lr) * _q(self.ld)), self.lf)
         return {"E": E, "X": X, "fitness": f, "y": y, "g": g, "pen": pen, "sigma_lr": used}
+
+
+def _dsqrt(q):
+    """60-digit square root of an exact rational, as a Fraction."""
+    from decimal import Decimal, getcontext
+    getcontext().prec = 60
+    q = _q(q)
+    return Fraction((Decimal(q.numerator) / Decimal(q.denominator)).sqrt())
+
+
+class BruteFamily:
+    """R=1 PGPE / SNES / OpenAI-ES+ClipUp generation with per-dimension sigma,
+    in exact rationals: the sums over pairs are exact, every fp32 result is
+    rounded once (``f32``); square roots to 60 digits, exp in fp64."""
+
+    def __init__(self, strategy, problem, D, N, sigma, lr, seed, lo, hi, sigma_lr=0.2, max_change=0.2,
+                 optimizer="adam", max_speed=0.3, momentum=0.9, beta=12.0, b1=0.9, b2=0.999, eps=1e-8):
+        self.strategy, self.problem, self.D, self.N = strategy, problem, D, N
+        self.sig = [f32(sigma)] * D
+        self.lr, self.seed = f32(lr), seed
+        self.slr, self.mc = f32(sigma_lr), f32(max_change)
+        self.opt, self.vmax, self.mom, self.beta = optimizer, f32(max_speed), f32(momentum), beta
+        self.b1, self.b2, self.eps = f32(b1), f32(b2), f32(eps)
+        self.m = init_uniform(seed, D, lo, hi)
+        self.m1, self.v, self.vel = [0.0] * D, [0.0] * D, [0.0] * D
+        self.t = 0
+
+    def _adam(self, g):
+        tp = self.t + 1
+        bc1, bc2 = f32(1.0 - math.pow(self.b1, tp)), f32(1.0 - math.pow(self.b2, tp))
+        omb1, omb2 = f32(1 - _q(self.b1)), f32(1 - _q(self.b2))
+        for d in range(self.D):
+            m1 = fma32(self.b1, self.m1[d], f32(_q(omb1) * _q(g[d])))
+            v = fma32(self.b2, self.v[d], f32(_q(omb2) * _q(f32(_q(g[d]) ** 2))))
+            den = f32(_q(f32(math.sqrt(f32(_q(v) / _q(bc2))))) + _q(self.eps))
+            self.m[d] = fma32(-self.lr, f32(_q(f32(_q(m1) / _q(bc1))) / _q(den)), self.m[d])
+            self.m1[d], self.v[d] = m1, v
+
+    def _clipup(self, g):
+        gg = sum(_q(x) ** 2 for x in g)
+        inv = f32(1 / _dsqrt(gg)) if gg > 0 else 0.0
+        vel = [fma32(self.lr, f32(_q(g[d]) * _q(inv)), f32(_q(self.mom) * _q(self.vel[d]))) for d in range(self.D)]
+        nv = _dsqrt(sum(_q(x) ** 2 for x in vel))
+        if nv > _q(self.vmax):
+            sc = f32(_q(self.vmax) / nv)
+            vel = [f32(_q(x) * _q(sc)) for x in vel]
+        self.vel = vel
+        self.m = [f32(_q(self.m[d]) - _q(vel[d])) for d in range(self.D)]
+
+    def generation(self):
+        P, D, N = self.N // 2, self.D, self.N
+        Z = [eps_vector(self.seed, 0, p, self.t, D) for p in range(P)]
+        X = [[fma32(self.sig[d] if j < P else -self.sig[d], Z[j % P][d], self.m[d]) for d in range(D)]
+             for j in range(N)]
+        f = [fitness(self.problem, x) for x in X]
+        rk = ranks(f)
+        if self.strategy == "snes":
+            S = math.fsum(math.exp(self.beta * (k / N - 0.5)) for k in range(N))
+            tab = [f32(math.exp(self.beta * (k / N - 0.5)) / S) for k in range(N)]
+            w = [tab[N - 1 - r] for r in rk]
+            a = [f32(_q(w[p]) - _q(w[p + P])) for p in range(P)]
+            b = [f32(_q(w[p]) + _q(w[p + P])) for p in range(P)]
+        else:
+            y = [f32(Fraction(2 * r - (N - 1), 2 * (N - 1))) for r in rk]
+            ybar = sum(_q(v) for v in y) / N
+            a = [f32(_q(y[p]) - _q(y[p + P])) for p in range(P)]
+            b = [f32(Fraction(1, 2) * (_q(y[p]) + _q(y[p + P])) - ybar) for p in range(P)]
+        A = [sum(_q(a[p]) * _q(Z[p][d]) for p in range(P)) for d in range(D)]
+        B = [sum(_q(b[p]) * (_q(Z[p][d]) ** 2 - 1) for p in range(P)) for d in range(D)]
+        if self.strategy == "snes":
+            h = f32(Fraction(1, 2) * _q(self.slr))
+            for d in range(D):
+                self.m[d] = fma32(f32(_q(self.lr) * _q(self.sig[d])), f32(A[d]), self.m[d])
+                self.sig[d] = f32(_q(self.sig[d]) * _q(f32(math.exp(f32(_q(h) * _q(f32(B[d])))))))
+            g = None
+        else:
+            if self.strategy == "pgpe":
+                g = [f32(_q(self.sig[d]) * A[d] / N) for d in range(D)]
+            else:  # OpenAI-ES: g = E^T y / (N sigma) over the unfolded population
+                g = [f32(A[d] / (N * _q(self.sig[d]))) for d in range(D)]
+            if self.opt == "clipup":
+                self._clipup(g)
+            else:
+                self._adam(g)
+            if self.strategy == "pgpe":
+                for d in range(D):
+                    sg = f32(_q(self.sig[d]) * B[d] / P)
+                    dlt = -f32(_q(self.slr) * _q(sg))
+                    lim = f32(_q(self.mc) * _q(self.sig[d]))
+                    dlt = min(max(dlt, -lim), lim)
+                    self.sig[d] = f32(_q(self.sig[d]) + _q(dlt))
+        self.t += 1
+        return {"X": X, "fitness": f, "g": g, "A": A, "B": B}

@@ -117,6 +117,8 @@ enum { OR_PROB_NONE = 0, OR_PROB_SPHERE = 1, OR_PROB_SHIFTED_SPHERE = 2,
        OR_PROB_ROSENBROCK = 3, OR_PROB_RASTRIGIN = 4, OR_PROB_MLP = 5 };
 enum { OR_INIT_UNIFORM = 0, OR_INIT_ZERO = 1, OR_INIT_FANIN_NORMAL = 2 };
 enum { OR_SHAPE_CENTERED_RANK = 0, OR_SHAPE_RAW = 1, OR_SHAPE_Z_SCORE = 2 };
+enum { OR_STRAT_OPENAI_ES = 0, OR_STRAT_PGPE = 1, OR_STRAT_SNES = 2 };
+enum { OR_OPT_ADAM = 0, OR_OPT_CLIPUP = 1 };
 
 typedef struct {
     int64_t num_dims;   /* D */
@@ -138,6 +140,16 @@ typedef struct {
     /* constant.  sigma and lr above are the values of the current generation. */
     float sigma_decay, sigma_final, lr_decay, lr_final;
     float w_decay;      /* weight-decay coefficient of the fitness shaping   */
+    /* Strategies of Table 1 beside OpenAI-ES (PGPE, SNES) and the ClipUp     */
+    /* optimiser named in Sec. 3.1; parameters from the App. B tables.        */
+    int32_t strategy;        /* OR_STRAT_*                                   */
+    int32_t optimizer;       /* OR_OPT_* for the mean (OpenAI-ES, PGPE)       */
+    float sigma_lr;          /* PGPE / SNES learning rate of sigma            */
+    float sigma_max_change;  /* PGPE: bound of |d sigma| / sigma per step     */
+    float clipup_max_speed;  /* ClipUp: bound of the velocity norm            */
+    float clipup_momentum;   /* ClipUp: velocity decay                        */
+    float snes_temperature;  /* SNES: beta of the softmax rank utilities      */
+    const float* sigma_vec;  /* per-dimension sigma of this run (PGPE, SNES)  */
 } or_config;
 
 /* MLP 64-256-256-16 layer table, flattened [out][in] row-major weights, then
@@ -227,11 +239,14 @@ void or_member(const or_config* c, int32_t run, uint32_t t, const float* m, int3
 {
     int32_t half = c->popsize / 2;
     int32_t p = j < half ? j : j - half;
-    float sgn_sigma = j < half ? c->sigma : -c->sigma;
     int64_t D = c->num_dims;
     float* eps = (float*)malloc(sizeof(float) * (size_t)D);
     or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)p, t, 0, D, eps);
-    for (int64_t d = 0; d < D; ++d) x[d] = fmaf(sgn_sigma, eps[d], m[d]);
+    for (int64_t d = 0; d < D; ++d) {
+        /* PGPE / SNES: a diagonal Gaussian, per-dimension sigma */
+        float sd = c->sigma_vec ? c->sigma_vec[d] : c->sigma;
+        x[d] = fmaf(j < half ? sd : -sd, eps[d], m[d]);
+    }
     free(eps);
 }
 
@@ -550,6 +565,171 @@ void or_adam(const or_config* c, int64_t t, const float* g, int64_t n, float* m,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Two weighted noise sums over the pairs, fp64:                             */
+/*   A_d = sum_p a_p z_pd,   B_d = sum_p b_p (z_pd^2 - 1).                    */
+/* ------------------------------------------------------------------------ */
+void or_noise_sums(const or_config* c, int32_t run, uint32_t t, const float* a, const float* b,
+                   double* A, double* B)
+{
+    int32_t P = c->popsize / 2;
+    int64_t D = c->num_dims;
+    float* z = (float*)malloc(sizeof(float) * (size_t)D);
+    for (int64_t d = 0; d < D; ++d) { A[d] = 0.0; B[d] = 0.0; }
+    for (int32_t p = 0; p < P; ++p) {
+        or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)p, t, 0, D, z);
+        for (int64_t d = 0; d < D; ++d) {
+            double zd = (double)z[d];
+            A[d] += (double)a[p] * zd;
+            B[d] += (double)b[p] * (zd * zd - 1.0);
+        }
+    }
+    free(z);
+}
+
+/* ClipUp (Toklu et al. 2020), the ES-adapted optimiser named in Sec. 3.1,
+ * for minimisation.  Reading: with the fp64 norms |g| and |v'|,
+ *   gh_d = fl32(g_d * fl32(1/|g|))          (0 when |g| = 0)
+ *   v'_d = fmaf(lr, gh_d, fl32(momentum * v_d))
+ *   v_d  = |v'| > max_speed ? fl32(v'_d * fl32(max_speed / |v'|)) : v'_d
+ *   m_d  = m_d - v_d.                                                       */
+void or_clipup(const or_config* c, float lr, const float* g, int64_t n, float* m, float* vel)
+{
+    double gg = 0.0;
+    for (int64_t i = 0; i < n; ++i) gg += (double)g[i] * (double)g[i];
+    float inv = gg > 0.0 ? (float)(1.0 / sqrt(gg)) : 0.0f;
+    double vv = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+        float gh = g[i] * inv;
+        float mv = c->clipup_momentum * vel[i];
+        vel[i] = fmaf(lr, gh, mv);
+        vv += (double)vel[i] * (double)vel[i];
+    }
+    double nv = sqrt(vv);
+    if (nv > (double)c->clipup_max_speed) {
+        float sc = (float)((double)c->clipup_max_speed / nv);
+        for (int64_t i = 0; i < n; ++i) vel[i] = vel[i] * sc;
+    }
+    for (int64_t i = 0; i < n; ++i) m[i] = m[i] - vel[i];
+}
+
+/* SNES utilities (App. B, SNES table): w_j = softmax(beta (rank'_j/N - 1/2))
+ * with rank'_j = N - 1 - rank_j, so that the best member (rank 0 of the
+ * minimisation keys) has the largest weight.  rank' is a permutation of
+ * 0..N-1, so the weights form a table indexed by rank'; fp64, one fp32
+ * rounding each.                                                           */
+void or_snes_table(int32_t N, float beta, float* w)
+{
+    double S = 0.0;
+    for (int32_t k = 0; k < N; ++k) S += exp((double)beta * ((double)k / (double)N - 0.5));
+    for (int32_t k = 0; k < N; ++k) w[k] = (float)(exp((double)beta * ((double)k / (double)N - 0.5)) / S);
+}
+
+/* Ranks of the shaped minimisation keys (weight decay included). */
+static void or_key_ranks(const float* f, const float* pen, int32_t N, int32_t maximize, float w_decay,
+                         int32_t* rank)
+{
+    float* key = (float*)malloc(sizeof(float) * (size_t)N);
+    for (int32_t j = 0; j < N; ++j) key[j] = or_shaped_key(f[j], pen ? pen[j] : 0.0f, maximize, w_decay);
+    for (int32_t j = 0; j < N; ++j) {
+        int32_t r = 0;
+        for (int32_t k = 0; k < N; ++k)
+            if (key[k] < key[j] || (key[k] == key[j] && k < j)) ++r;
+        rank[j] = r;
+    }
+    free(key);
+}
+
+/* PGPE tell (Sehnke et al. 2010, symmetric sampling; FDG row of Table 1;
+ * App. B PGPE table: sigma learning rate and maximum change).  Readings, for
+ * shaped weights y (low = good) and pairs p with x = m +- sigma (.) z_p:
+ *   mean gradient  g_d = fl32(sigma_d A_d / N),  a_p = y_p - y_{p+P};
+ *   sigma gradient s_d = fl32(sigma_d B_d / P),  b_p = fl32((y_p + y_{p+P})/2 - ybar),
+ *                  ybar the fp64 mean of y;
+ *   mean step: the optimiser (Adam, or ClipUp) on g with learning rate lr;
+ *   sigma step: dlt = -(sigma_lr * s_d), clipped to +- fl32(max_change * sigma_d),
+ *                  sigma_d + dlt, then the schedule max(fl32(sigma*decay), final). */
+void or_pgpe_update(const or_config* c, int32_t run, int64_t t, float lr, const float* y, float* m,
+                    float* m1, float* v, float* vel, float* sig, float* g_out)
+{
+    int32_t N = c->popsize, P = N / 2;
+    int64_t D = c->num_dims;
+    double ybar = 0.0;
+    for (int32_t j = 0; j < N; ++j) ybar += (double)y[j];
+    ybar /= (double)N;
+    float* a = (float*)malloc(sizeof(float) * (size_t)P);
+    float* b = (float*)malloc(sizeof(float) * (size_t)P);
+    for (int32_t p = 0; p < P; ++p) {
+        a[p] = y[p] - y[p + P];
+        b[p] = (float)(0.5 * ((double)y[p] + (double)y[p + P]) - ybar);
+    }
+    double* A = (double*)malloc(sizeof(double) * (size_t)D);
+    double* B = (double*)malloc(sizeof(double) * (size_t)D);
+    or_noise_sums(c, run, (uint32_t)t, a, b, A, B);
+    float* g = (float*)malloc(sizeof(float) * (size_t)D);
+    for (int64_t d = 0; d < D; ++d) g[d] = (float)((double)sig[d] * A[d] / (double)N);
+    if (c->optimizer == OR_OPT_CLIPUP) {
+        or_clipup(c, lr, g, D, m, vel);
+    } else {
+        or_config cc = *c;
+        cc.lr = lr;
+        or_adam(&cc, t, g, D, m, m1, v);
+    }
+    for (int64_t d = 0; d < D; ++d) {
+        float sg = (float)((double)sig[d] * B[d] / (double)P);
+        float dlt = -(c->sigma_lr * sg);
+        float lim = c->sigma_max_change * sig[d];
+        if (dlt > lim) dlt = lim;
+        if (dlt < -lim) dlt = -lim;
+        float ns = sig[d] + dlt;
+        sig[d] = or_decay(ns, c->sigma_decay, c->sigma_final);
+    }
+    if (g_out) memcpy(g_out, g, sizeof(float) * (size_t)D);
+    free(a); free(b); free(A); free(B); free(g);
+}
+
+/* SNES tell (Schaul et al. 2011; PFD row of Table 1) with the softmax rank
+ * utilities of App. B.  Readings: w_j from or_snes_table over rank'_j (ranks
+ * of the shaped keys, weight decay included); a_p = w_p - w_{p+P},
+ * b_p = w_p + w_{p+P};
+ *   m_d     = fmaf(fl32(lr * sigma_d), fl32(A_d), m_d)            (lr = eta_m)
+ *   sigma_d = fl32(sigma_d * expf(fl32(fl32(sigma_lr / 2) * fl32(B_d)))),
+ * then the sigma schedule.                                                 */
+void or_snes_update(const or_config* c, int32_t run, int64_t t, float lr, const float* f, const float* pen,
+                    float* m, float* sig, float* w_out)
+{
+    int32_t N = c->popsize, P = N / 2;
+    int64_t D = c->num_dims;
+    int32_t* rank = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
+    or_key_ranks(f, pen, N, c->maximize, c->w_decay, rank);
+    float* tab = (float*)malloc(sizeof(float) * (size_t)N);
+    or_snes_table(N, c->snes_temperature, tab);
+    float* w = (float*)malloc(sizeof(float) * (size_t)N);
+    for (int32_t j = 0; j < N; ++j) w[j] = tab[N - 1 - rank[j]];
+    float* a = (float*)malloc(sizeof(float) * (size_t)P);
+    float* b = (float*)malloc(sizeof(float) * (size_t)P);
+    for (int32_t p = 0; p < P; ++p) {
+        a[p] = w[p] - w[p + P];
+        b[p] = w[p] + w[p + P];
+    }
+    double* A = (double*)malloc(sizeof(double) * (size_t)D);
+    double* B = (double*)malloc(sizeof(double) * (size_t)D);
+    or_noise_sums(c, run, (uint32_t)t, a, b, A, B);
+    float h = 0.5f * c->sigma_lr;
+    for (int64_t d = 0; d < D; ++d) {
+        m[d] = fmaf(lr * sig[d], (float)A[d], m[d]);
+        float ns = sig[d] * expf(h * (float)B[d]);
+        sig[d] = or_decay(ns, c->sigma_decay, c->sigma_final);
+    }
+    if (w_out) memcpy(w_out, w, sizeof(float) * (size_t)N);
+    free(rank); free(tab); free(w); free(a); free(b); free(A); free(B);
+}
+
+void or_generation_ex(const or_config* c0, int32_t run, int64_t t, const float* pdata,
+                      float* m, float* m1, float* v, float* vel, float* sig, const float* fit_in,
+                      float* fit_out, float* y_out, float* g_out,
+                      double* best_key, float* best_f, float* best_x);
+
+/* ------------------------------------------------------------------------ */
 /* One generation of one run (ask -> evaluate -> tell), the body of the      */
 /* scanned loop of Sec. 2.2 (Listing 2).  fit_in != NULL replaces the        */
 /* built-in evaluation (the user's own evaluate step).  Best-so-far member   */
@@ -563,6 +743,21 @@ void or_generation(const or_config* c, int32_t run, int64_t t, const float* pdat
                    float* fit_out, float* y_out, float* g_out,
                    double* best_key, float* best_f, float* best_x)
 {
+    or_generation_ex(c, run, t, pdata, m, m1, v, NULL, NULL, fit_in, fit_out, y_out, g_out, best_key, best_f,
+                     best_x);
+}
+
+/* As or_generation, for every strategy: vel = ClipUp velocity (or NULL),
+ * sig = per-dimension sigma (PGPE, SNES; updated in place, and used as
+ * c->sigma_vec for the sampling).                                          */
+void or_generation_ex(const or_config* c0, int32_t run, int64_t t, const float* pdata,
+                      float* m, float* m1, float* v, float* vel, float* sig, const float* fit_in,
+                      float* fit_out, float* y_out, float* g_out,
+                      double* best_key, float* best_f, float* best_x)
+{
+    or_config cfg = *c0;
+    const or_config* c = &cfg;
+    if (cfg.strategy != OR_STRAT_OPENAI_ES) cfg.sigma_vec = sig;
     int32_t N = c->popsize;
     int64_t D = c->num_dims;
     float* f = (float*)malloc(sizeof(float) * (size_t)N);
@@ -587,19 +782,37 @@ void or_generation(const or_config* c, int32_t run, int64_t t, const float* pdat
         if (best_f) *best_f = f[jbest];
         if (best_x) or_member(c, run, (uint32_t)t, m, jbest, best_x);
     }
-    if (c->w_decay != 0.0f || c->shaping == OR_SHAPE_Z_SCORE) {
-        float* pen = NULL;
-        if (c->w_decay != 0.0f) {
-            pen = (float*)malloc(sizeof(float) * (size_t)N);
-            or_penalty(c, run, (uint32_t)t, m, pen);
-        }
-        or_shape_full(f, pen, N, c->maximize, c->shaping, c->w_decay, y);
-        free(pen);
-    } else {
-        or_shape(f, N, c->maximize, c->shaping, y);
+    float* pen = NULL;
+    if (c->w_decay != 0.0f) {
+        pen = (float*)malloc(sizeof(float) * (size_t)N);
+        or_penalty(c, run, (uint32_t)t, m, pen);
     }
-    or_grad(c, run, (uint32_t)t, y, 0, D, g);
-    or_adam(c, t, g, D, m, m1, v);
+    if (c->strategy == OR_STRAT_SNES) {
+        /* m and sigma move together; sig is also c->sigma_vec */
+        float* snew = (float*)malloc(sizeof(float) * (size_t)D);
+        memcpy(snew, sig, sizeof(float) * (size_t)D);
+        or_snes_update(c, run, t, c->lr, f, pen, m, snew, y);
+        memcpy(sig, snew, sizeof(float) * (size_t)D);
+        free(snew);
+        for (int64_t d = 0; d < D; ++d) g[d] = 0.0f;
+    } else {
+        if (c->w_decay != 0.0f || c->shaping == OR_SHAPE_Z_SCORE)
+            or_shape_full(f, pen, N, c->maximize, c->shaping, c->w_decay, y);
+        else
+            or_shape(f, N, c->maximize, c->shaping, y);
+        if (c->strategy == OR_STRAT_PGPE) {
+            float* snew = (float*)malloc(sizeof(float) * (size_t)D);
+            memcpy(snew, sig, sizeof(float) * (size_t)D);
+            or_pgpe_update(c, run, t, c->lr, y, m, m1, v, vel, snew, g);
+            memcpy(sig, snew, sizeof(float) * (size_t)D);
+            free(snew);
+        } else {
+            or_grad(c, run, (uint32_t)t, y, 0, D, g);
+            if (c->optimizer == OR_OPT_CLIPUP) or_clipup(c, c->lr, g, D, m, vel);
+            else or_adam(c, t, g, D, m, m1, v);
+        }
+    }
+    free(pen);
     if (fit_out) memcpy(fit_out, f, sizeof(float) * (size_t)N);
     if (y_out) memcpy(y_out, y, sizeof(float) * (size_t)N);
     if (g_out) memcpy(g_out, g, sizeof(float) * (size_t)D);

@@ -24,6 +24,8 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 PROB_NONE, PROB_SPHERE, PROB_SHIFTED_SPHERE, PROB_ROSENBROCK, PROB_RASTRIGIN, PROB_MLP = range(6)
 INIT_UNIFORM, INIT_ZERO, INIT_FANIN_NORMAL = range(3)
 SHAPE_CENTERED_RANK, SHAPE_RAW, SHAPE_Z_SCORE = range(3)
+STRAT_OPENAI_ES, STRAT_PGPE, STRAT_SNES = range(3)
+OPT_ADAM, OPT_CLIPUP = range(2)
 DOM_NOISE, DOM_INIT, DOM_PROBLEM, DOM_EVAL = range(4)
 MLP_IN, MLP_H, MLP_OUT = 64, 256, 16
 
@@ -65,6 +67,14 @@ class _Cfg(ctypes.Structure):
         ("lr_decay", ctypes.c_float),
         ("lr_final", ctypes.c_float),
         ("w_decay", ctypes.c_float),
+        ("strategy", ctypes.c_int32),
+        ("optimizer", ctypes.c_int32),
+        ("sigma_lr", ctypes.c_float),
+        ("sigma_max_change", ctypes.c_float),
+        ("clipup_max_speed", ctypes.c_float),
+        ("clipup_momentum", ctypes.c_float),
+        ("snes_temperature", ctypes.c_float),
+        ("sigma_vec", ctypes.c_void_p),
     ]
 
 
@@ -96,13 +106,28 @@ class OracleConfig:
     lr_decay: float = 1.0
     lr_final: float = 0.0
     w_decay: float = 0.0  # weight-decay fitness regularisation (Sec. 3.2)
+    # Table 1 strategies beside OpenAI-ES and the ClipUp optimiser (Sec. 3.1);
+    # defaults from the App. B PGPE / SNES tables
+    strategy: int = STRAT_OPENAI_ES
+    optimizer: int = OPT_ADAM
+    sigma_lr: float = 0.2
+    sigma_max_change: float = 0.2
+    clipup_max_speed: float = 0.3
+    clipup_momentum: float = 0.9
+    snes_temperature: float = 12.0
 
-    def cstruct(self) -> _Cfg:
-        return _Cfg(self.num_dims, self.popsize, self.num_runs, self.sigma, self.lr, self.beta1,
-                    self.beta2, self.eps, self.maximize, self.shaping, self.seed, self.init,
-                    self.init_lo, self.init_hi, self.problem, self.rastrigin_a, self.mlp_batch,
-                    self.mlp_bf16, self.mlp_tanh_out, self.sigma_decay, self.sigma_final,
-                    self.lr_decay, self.lr_final, self.w_decay)
+    def cstruct(self, sigma_vec=None) -> _Cfg:
+        c = _Cfg(self.num_dims, self.popsize, self.num_runs, self.sigma, self.lr, self.beta1,
+                 self.beta2, self.eps, self.maximize, self.shaping, self.seed, self.init,
+                 self.init_lo, self.init_hi, self.problem, self.rastrigin_a, self.mlp_batch,
+                 self.mlp_bf16, self.mlp_tanh_out, self.sigma_decay, self.sigma_final,
+                 self.lr_decay, self.lr_final, self.w_decay, self.strategy, self.optimizer,
+                 self.sigma_lr, self.sigma_max_change, self.clipup_max_speed, self.clipup_momentum,
+                 self.snes_temperature, None)
+        if sigma_vec is not None:
+            c.sigma_vec = sigma_vec.ctypes.data
+            c._keep = sigma_vec  # the C side reads through this pointer
+        return c
 
 
 _lib = None
@@ -134,6 +159,11 @@ def lib():
             "or_shape_full": (None, [P(f32), P(f32), i32, i32, i32, f32, P(f32)]),
             "or_penalty": (None, [pc, i32, u32, P(f32), P(f32)]),
             "or_decay": (f32, [f32, f32, f32]),
+            "or_noise_sums": (None, [pc, i32, u32, P(f32), P(f32), P(ctypes.c_double), P(ctypes.c_double)]),
+            "or_clipup": (None, [pc, f32, P(f32), i64, P(f32), P(f32)]),
+            "or_snes_table": (None, [i32, f32, P(f32)]),
+            "or_generation_ex": (None, [pc, i32, i64, P(f32), P(f32), P(f32), P(f32), P(f32), P(f32), P(f32),
+                                        P(f32), P(f32), P(f32), P(ctypes.c_double), P(f32), P(f32)]),
             "or_shape": (None, [P(f32), i32, i32, i32, P(f32)]),
             "or_grad": (None, [pc, i32, u32, P(f32), i64, i64, P(f32)]),
             "or_adam": (None, [pc, i64, P(f32), i64, P(f32), P(f32), P(f32)]),
@@ -203,18 +233,18 @@ def problem_data(cfg: OracleConfig):
     return out
 
 
-def member(cfg, run, t, m, j):
+def member(cfg, run, t, m, j, sig=None):
     x = np.zeros(cfg.num_dims, dtype=np.float32)
     m = _f32(m)
-    lib().or_member(cfg.cstruct(), run, t, _p(m), j, _p(x))
+    lib().or_member(cfg.cstruct(None if sig is None else _f32(sig)), run, t, _p(m), j, _p(x))
     return x
 
 
-def population(cfg, run, t, m):
+def population(cfg, run, t, m, sig=None):
     """ask (Sec. 2.1): all N members of run ``run`` at generation t, [N][D]."""
     x = np.zeros((cfg.popsize, cfg.num_dims), dtype=np.float32)
     m = _f32(m)
-    lib().or_population(cfg.cstruct(), run, t, _p(m), _p(x))
+    lib().or_population(cfg.cstruct(None if sig is None else _f32(sig)), run, t, _p(m), _p(x))
     return x
 
 
@@ -242,13 +272,13 @@ def mlp_fitness(cfg, x, t, YT):
     return float(lib().or_mlp_fitness(cfg.cstruct(), _p(x), t, _p(YT)))
 
 
-def eval_members(cfg, run, t, m, pdata, js):
+def eval_members(cfg, run, t, m, pdata, js, sig=None):
     """evaluate (Sec. 2.1) for the listed members only."""
     js = np.ascontiguousarray(js, dtype=np.int32)
     f = np.zeros(len(js), dtype=np.float32)
     m = _f32(m)
     pd = _f32(pdata) if pdata is not None else None
-    lib().or_eval_members(cfg.cstruct(), run, t, _p(m), _p(pd), _p(js, ctypes.c_int32), len(js), _p(f))
+    lib().or_eval_members(cfg.cstruct(None if sig is None else _f32(sig)), run, t, _p(m), _p(pd), _p(js, ctypes.c_int32), len(js), _p(f))
     return f
 
 
@@ -277,17 +307,40 @@ def shape_full(f, pen=None, maximize=0, shaping=SHAPE_CENTERED_RANK, w_decay=0.0
     return y
 
 
-def penalty(cfg, run, t, m):
+def penalty(cfg, run, t, m, sig=None):
     """Per-member mean square parameter (1/D) sum_d x_jd^2 of run r at generation t."""
     m = _f32(m)
     pen = np.zeros(cfg.popsize, dtype=np.float32)
-    lib().or_penalty(cfg.cstruct(), run, t, _p(m), _p(pen))
+    lib().or_penalty(cfg.cstruct(None if sig is None else _f32(sig)), run, t, _p(m), _p(pen))
     return pen
 
 
 def decay(x, rate, final):
     """One step of the App. B schedule: max(x * rate, final) in fp32."""
     return float(lib().or_decay(x, rate, final))
+
+
+def noise_sums(cfg, run, t, a, b):
+    """A_d = sum_p a_p z_pd and B_d = sum_p b_p (z_pd^2 - 1), fp64."""
+    a, b = _f32(a), _f32(b)
+    A = np.zeros(cfg.num_dims, np.float64)
+    B = np.zeros(cfg.num_dims, np.float64)
+    lib().or_noise_sums(cfg.cstruct(), run, t, _p(a), _p(b), _p(A, ctypes.c_double), _p(B, ctypes.c_double))
+    return A, B
+
+
+def clipup(cfg, lr, g, m, vel):
+    """One ClipUp step (Toklu et al. 2020) on copies of m and the velocity."""
+    g, m, vel = _f32(g), _f32(m).copy(), _f32(vel).copy()
+    lib().or_clipup(cfg.cstruct(), lr, _p(g), g.shape[0], _p(m), _p(vel))
+    return m, vel
+
+
+def snes_table(N, beta):
+    """SNES softmax rank utilities indexed by rank' (best = N - 1)."""
+    w = np.zeros(N, np.float32)
+    lib().or_snes_table(N, beta, _p(w))
+    return w
 
 
 def grad(cfg, run, t, y, d0=0, nd=None):
@@ -328,6 +381,9 @@ class OracleES:
         self.best_x = np.zeros((R, D), np.float32)
         self.sigma = np.full(R, cfg.sigma, dtype=np.float32)
         self.lr = np.full(R, cfg.lr, dtype=np.float32)
+        # per-dimension sigma (PGPE, SNES) and ClipUp velocity
+        self.sig = np.full((R, D), cfg.sigma, dtype=np.float32)
+        self.vel = np.zeros((R, D), np.float32)
 
     def set_hparams(self, sigma=None, lr=None):
         if sigma is not None:
@@ -339,13 +395,27 @@ class OracleES:
         """The config of run r at the current generation (its sigma and lr)."""
         return replace(self.cfg, sigma=float(self.sigma[r]), lr=float(self.lr[r]))
 
+    def _cs(self, r):
+        """C config of run r, with its sigma vector for PGPE / SNES."""
+        vec = self.sig[r] if self.cfg.strategy != STRAT_OPENAI_ES else None
+        return self.run_cfg(r).cstruct(vec)
+
     def ask(self):
-        return np.stack([population(self.run_cfg(r), r, self.t, self.m[r]) for r in range(self.cfg.num_runs)])
+        R, N, D = self.cfg.num_runs, self.cfg.popsize, self.cfg.num_dims
+        out = np.zeros((R, N, D), np.float32)
+        for r in range(R):
+            lib().or_population(self._cs(r), r, self.t, _p(_f32(self.m[r])), _p(out[r]))
+        return out
 
     def eval(self):
         js = np.arange(self.cfg.popsize, dtype=np.int32)
-        return np.stack([eval_members(self.run_cfg(r), r, self.t, self.m[r], self.pdata, js)
-                         for r in range(self.cfg.num_runs)])
+        R, N = self.cfg.num_runs, self.cfg.popsize
+        out = np.zeros((R, N), np.float32)
+        pd = _f32(self.pdata) if self.pdata is not None else None
+        for r in range(R):
+            lib().or_eval_members(self._cs(r), r, self.t, _p(_f32(self.m[r])), _p(pd), _p(js, ctypes.c_int32), N,
+                                  _p(out[r]))
+        return out
 
     def tell(self, fitness=None):
         """One generation; ``fitness`` [R][N] replaces the built-in evaluation.
@@ -359,17 +429,20 @@ class OracleES:
         for r in range(R):
             c = self.run_cfg(r).cstruct()
             m, m1, v = self.m[r].copy(), self.m1[r].copy(), self.v[r].copy()
+            vel, sig = self.vel[r].copy(), self.sig[r].copy()
             fin = _f32(fitness[r]) if fitness is not None else None
             bk = ctypes.c_double(self.best_key[r])
             bf = np.array([self.best_f[r]], np.float32)
             bx = self.best_x[r].copy()
             fo, yo, go = np.zeros(N, np.float32), np.zeros(N, np.float32), np.zeros(D, np.float32)
-            lib().or_generation(c, r, self.t, _p(pd), _p(m), _p(m1), _p(v), _p(fin), _p(fo), _p(yo),
-                                _p(go), ctypes.byref(bk), _p(bf), _p(bx))
+            lib().or_generation_ex(c, r, self.t, _p(pd), _p(m), _p(m1), _p(v), _p(vel), _p(sig), _p(fin), _p(fo),
+                                   _p(yo), _p(go), ctypes.byref(bk), _p(bf), _p(bx))
             self.m[r], self.m1[r], self.v[r] = m, m1, v
+            self.vel[r], self.sig[r] = vel, sig
             self.best_key[r], self.best_f[r], self.best_x[r] = bk.value, bf[0], bx
             out_f[r], out_y[r], out_g[r] = fo, yo, go
-            self.sigma[r] = decay(float(self.sigma[r]), cfg.sigma_decay, cfg.sigma_final)
+            if cfg.strategy == STRAT_OPENAI_ES:
+                self.sigma[r] = decay(float(self.sigma[r]), cfg.sigma_decay, cfg.sigma_final)
             self.lr[r] = decay(float(self.lr[r]), cfg.lr_decay, cfg.lr_final)
         self.t += 1
         return {"fitness": out_f, "y": out_y, "g": out_g}
@@ -390,8 +463,12 @@ class OracleES:
 
     def get_state(self):
         return {"m": self.m.copy(), "m1": self.m1.copy(), "v": self.v.copy(), "t": self.t,
-                "sigma": self.sigma.copy(), "lr": self.lr.copy()}
+                "sigma": self.sigma.copy(), "lr": self.lr.copy(), "sig": self.sig.copy(), "vel": self.vel.copy()}
 
-    def set_state(self, m, m1, v, t):
+    def set_state(self, m, m1, v, t, sig=None, vel=None):
         self.m, self.m1, self.v = _f32(m).copy(), _f32(m1).copy(), _f32(v).copy()
         self.t = int(t)
+        if sig is not None:
+            self.sig = _f32(sig).copy()
+        if vel is not None:
+            self.vel = _f32(vel).copy()

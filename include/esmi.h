@@ -76,6 +76,26 @@ typedef enum {
 
 typedef enum { ES_INIT_UNIFORM = 0, ES_INIT_ZERO = 1, ES_INIT_FANIN_NORMAL = 2 } es_init_kind;
 
+/* Strategies (Table 1).  All sample antithetic pairs x = m +- s (.) z_p with
+ * z_p the Philox normals of pair p; s = sigma (OpenAI-ES) or a per-dimension
+ * sigma vector (PGPE, SNES).  With a_p = y_p - y_{p+P}, b_p the second folded
+ * weight, A_d = sum_p a_p z_pd and B_d = sum_p b_p (z_pd^2 - 1):
+ *   OPENAI_ES  g = A / (N sigma); the optimiser steps the mean.
+ *   PGPE       (Sehnke et al. 2010, symmetric sampling) b_p = (y_p +
+ *              y_{p+P})/2 - mean(y); g = sigma_d A / N for the optimiser;
+ *              sigma_d += clip(-sigma_lr sigma_d B / P, +-max_change sigma_d).
+ *   SNES       (Schaul et al. 2011) y = softmax rank utilities of App. B,
+ *              w = softmax(beta (rank'/N - 1/2)), rank' = N-1-rank (best
+ *              largest), b_p = y_p + y_{p+P}; m += fl32(lr sigma_d) A,
+ *              sigma_d *= exp(sigma_lr/2 B); the shaping field is ignored.
+ * After each tell the sigma (vector) follows the schedule. */
+typedef enum { ES_STRAT_OPENAI_ES = 0, ES_STRAT_PGPE = 1, ES_STRAT_SNES = 2 } es_strategy;
+
+/* Optimiser of the mean (OpenAI-ES, PGPE): Adam, or ClipUp (Toklu et al.
+ * 2020, the ES optimiser named in Sec. 3.1): v = momentum v + lr g/|g|,
+ * clipped to |v| <= clipup_max_speed, m -= v (norms in fp64 over the run). */
+typedef enum { ES_OPT_ADAM = 0, ES_OPT_CLIPUP = 1 } es_optimizer;
+
 /* Flags (es_config.flags). */
 #define ES_FLAG_KEEP_GRAD 1u /* es_tell also stores g [R][D] for es_get_grad */
 
@@ -112,7 +132,13 @@ typedef struct es_config {
     float lr_decay;     /* > 0                                               */
     float lr_final;     /* >= 0                                              */
     float w_decay;      /* >= 0, weight-decay coefficient of the shaping     */
-    uint32_t reserved;  /* must be 0                                         */
+    int32_t strategy;   /* es_strategy                                       */
+    int32_t optimizer;  /* es_optimizer (ignored by SNES)                    */
+    float sigma_lr;     /* PGPE / SNES learning rate of sigma (> 0)          */
+    float sigma_max_change; /* PGPE: |d sigma| <= max_change sigma, (0, 1)   */
+    float clipup_max_speed; /* ClipUp velocity bound (> 0)                   */
+    float clipup_momentum;  /* ClipUp velocity decay in [0, 1)               */
+    float snes_temperature; /* SNES utility temperature beta (>= 0)          */
 } es_config;
 
 typedef struct es_handle es_handle;
@@ -173,6 +199,13 @@ es_status es_get_grad(es_handle* h, float* g);
 es_status es_set_hparams(es_handle* h, const float* sigma, const float* lr);
 es_status es_get_hparams(es_handle* h, float* sigma, float* lr);
 
+/* Per-dimension sigma (PGPE, SNES) and ClipUp velocity of every run:
+ * device [R][D] each; NULL to skip.  ES_ERR_UNSUPPORTED for a state the
+ * configured strategy and optimiser do not keep.  es_set_strategy_state
+ * requires no open ask. */
+es_status es_get_strategy_state(es_handle* h, float* sigma_vec, float* velocity);
+es_status es_set_strategy_state(es_handle* h, const float* sigma_vec, const float* velocity);
+
 /* Weight-decay penalty of the last es_tell: pen [R][N] = (1/D) sum_d x_jd^2
  * of every member (device pointer).  ES_ERR_UNSUPPORTED when w_decay = 0. */
 es_status es_get_penalty(es_handle* h, float* pen);
@@ -188,8 +221,8 @@ es_status es_debug_noise(es_handle* h, int32_t run, int64_t t, int32_t pair,
                          uint32_t* words, float* eps);
 
 /* Checkpoint (synchronous): with host_buf NULL, *bytes receives the size;
- * otherwise the state (config, t, m, m1, v, best, per-run sigma and lr) is
- * written to host_buf.
+ * otherwise the state (config, t, m, m1, v, best, per-run sigma and lr, the
+ * sigma vector and velocity where kept) is written to host_buf.
  * es_load_state restores a checkpoint of a handle with the same config.
  * The random stream is a pure function of (seed, t), so resuming continues
  * the same trajectory bit for bit. */

@@ -64,6 +64,13 @@ struct es_handle {
     float* hp[2] = {nullptr, nullptr};
     int hp_cur = 0;
     float* pen = nullptr;        // [R][N] weight-decay mean square of the last tell
+    double ybar_table = 0.0;     // mean of the shaping table
+    float* bfold = nullptr;      // [R][P] second folded weight (PGPE, SNES)
+    float* sig = nullptr;        // [R][Dp] per-dimension sigma (PGPE, SNES)
+    float* vel = nullptr;        // [R][Dp] ClipUp velocity
+    float* gbuf = nullptr;       // [R][Dp] ClipUp gradient
+    double* gpart = nullptr;     // [R][groups] ClipUp partial norms
+    double* vpart = nullptr;
     TellPlan tell;               // pair slices of the gradient kernel
     double* tell_part = nullptr; // per-workgroup gradient sums when tell.nsplit > 1
     float* pdata = nullptr;  // [Dp] shift vector or teacher
@@ -140,15 +147,40 @@ const char* validate(const es_config& c)
     if (!(c.sigma_final >= 0.0f) || !std::isfinite(c.sigma_final)) return "sigma_final must be finite and >= 0";
     if (!(c.lr_final >= 0.0f) || !std::isfinite(c.lr_final)) return "lr_final must be finite and >= 0";
     if (!(c.w_decay >= 0.0f) || !std::isfinite(c.w_decay)) return "w_decay must be finite and >= 0";
-    if (c.reserved != 0) return "reserved must be 0";
+    if (c.strategy < ES_STRAT_OPENAI_ES || c.strategy > ES_STRAT_SNES) return "unknown strategy";
+    if (c.optimizer != ES_OPT_ADAM && c.optimizer != ES_OPT_CLIPUP) return "unknown optimizer";
+    if (c.strategy != ES_STRAT_OPENAI_ES && (!(c.sigma_lr > 0.0f) || !std::isfinite(c.sigma_lr)))
+        return "sigma_lr must be finite and > 0";
+    if (c.strategy == ES_STRAT_PGPE && !(c.sigma_max_change > 0.0f && c.sigma_max_change < 1.0f))
+        return "sigma_max_change must be in (0, 1)";
+    if (c.strategy != ES_STRAT_SNES && c.optimizer == ES_OPT_CLIPUP) {
+        if (!(c.clipup_max_speed > 0.0f) || !std::isfinite(c.clipup_max_speed))
+            return "clipup_max_speed must be finite and > 0";
+        if (!(c.clipup_momentum >= 0.0f && c.clipup_momentum < 1.0f)) return "clipup_momentum must be in [0, 1)";
+    }
+    if (c.strategy == ES_STRAT_SNES && (!(c.snes_temperature >= 0.0f) || !std::isfinite(c.snes_temperature)))
+        return "snes_temperature must be finite and >= 0";
     return nullptr;
 }
 
-// Centered-rank weight of rank k: the fp32 quotient (2k - (N-1)) / (2(N-1)).
-void weight_table(int32_t N, float* out)
+// Shaping weight of rank k.  Centered ranks: the fp32 quotient
+// (2k - (N-1)) / (2(N-1)).  SNES: the softmax utility of rank' = N-1-k,
+// exp(beta (rank'/N - 1/2)) / sum, in fp64 rounded once.  Returns the
+// table's fp64 mean.
+double weight_table(const es_config& c, int32_t N, float* out)
 {
-    const float den = (float)(2 * (N - 1));
-    for (int32_t k = 0; k < N; ++k) out[k] = (float)(2 * k - (N - 1)) / den;
+    if (c.strategy == ES_STRAT_SNES) {
+        double S = 0.0;
+        for (int32_t k = 0; k < N; ++k) S += std::exp((double)c.snes_temperature * ((double)k / (double)N - 0.5));
+        for (int32_t k = 0; k < N; ++k)
+            out[k] = (float)(std::exp((double)c.snes_temperature * ((double)(N - 1 - k) / (double)N - 0.5)) / S);
+    } else {
+        const float den = (float)(2 * (N - 1));
+        for (int32_t k = 0; k < N; ++k) out[k] = (float)(2 * k - (N - 1)) / den;
+    }
+    double sum = 0.0;
+    for (int32_t k = 0; k < N; ++k) sum += (double)out[k];
+    return sum / (double)N;
 }
 
 AdamConsts adam_consts(const es_config& c, int64_t t)
@@ -176,7 +208,8 @@ void free_all(es_handle* h)
 {
     void* ptrs[] = {h->m, h->m1, h->v, h->best_x, h->grad, h->best_okey, h->best_f, h->best_j, h->table,
                     h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->adam_dev, h->mlp_scratch,
-                    h->tell_part, h->hp[0], h->hp[1], h->pen};
+                    h->tell_part, h->hp[0], h->hp[1], h->pen, h->bfold, h->sig, h->vel, h->gbuf,
+                    h->gpart, h->vpart};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     if (h->adam_host) (void)hipHostFree(h->adam_host);
@@ -217,17 +250,20 @@ es_status enqueue_tell(es_handle* h, const float* fitness, float* gen_best)
         // sampler through the sphere evaluation, divided by D in its reduction
         es_config sq = h->cfg;
         sq.problem = ES_PROB_SPHERE;
-        ES_HIP(h, launch_eval_bbob(g, sq, h->plan, (uint32_t)h->t, h->m, nullptr, h->partial, h->pen, hp,
+        ES_HIP(h, launch_eval_bbob(g, sq, h->plan, (uint32_t)h->t, h->m, nullptr, h->partial, h->pen, hp, h->sig,
                                    (double)g.D, h->stream),
                "weight-decay penalty pass");
     }
-    ES_HIP(h, launch_rank(g, h->cfg, fitness, h->pen, h->table, h->y, h->rank, h->wfold, h->best_okey, h->best_f,
-                          h->best_j, gen_best, hp, h->hp[1 - h->hp_cur], h->stream),
+    ES_HIP(h, launch_rank(g, h->cfg, fitness, h->pen, h->table, h->ybar_table, h->y, h->rank, h->wfold, h->bfold,
+                          h->best_okey, h->best_f, h->best_j, gen_best, hp, h->hp[1 - h->hp_cur], h->stream),
            "rank kernel");
     const AdamConsts a = adam_consts(h->cfg, h->t);
-    ES_HIP(h, launch_tell(g, h->cfg, h->tell, (uint32_t)h->t, a, h->wfold, h->best_j, h->m, h->m1, h->v, h->grad,
-                          h->best_x, h->tell_part, hp, h->stream),
-           "tell kernel");
+    TellBuffers tb;
+    tb.wfold = h->wfold; tb.bfold = h->bfold; tb.best_j = h->best_j;
+    tb.m = h->m; tb.m1 = h->m1; tb.v = h->v; tb.grad = h->grad; tb.best_x = h->best_x;
+    tb.sig = h->sig; tb.vel = h->vel; tb.gbuf = h->gbuf; tb.gpart = h->gpart; tb.vpart = h->vpart;
+    tb.part = h->tell_part; tb.hp = hp;
+    ES_HIP(h, launch_tell(g, h->cfg, h->tell, (uint32_t)h->t, a, tb, h->stream), "tell kernel");
     h->hp_cur = 1 - h->hp_cur;  // the schedule step is next generation's sigma and lr
     return ES_OK;
 }
@@ -237,12 +273,12 @@ es_status enqueue_eval(es_handle* h, float* fit)
     if (h->cfg.problem == ES_PROB_NONE) return fail(h, ES_ERR_UNSUPPORTED, "no built-in problem configured");
     if (h->cfg.problem == ES_PROB_MLP) {
         ES_HIP(h, launch_eval_mlp(h->g, h->cfg, (uint32_t)h->t, h->m, h->pdata, h->mlp_scratch, fit,
-                                  h->hp[h->hp_cur], h->stream),
+                                  h->hp[h->hp_cur], h->sig, h->stream),
                "MLP evaluate kernels");
         return ES_OK;
     }
     ES_HIP(h, launch_eval_bbob(h->g, h->cfg, h->plan, (uint32_t)h->t, h->m, h->pdata, h->partial, fit,
-                               h->hp[h->hp_cur], 1.0, h->stream),
+                               h->hp[h->hp_cur], h->sig, 1.0, h->stream),
            "evaluate kernel");
     return ES_OK;
 }
@@ -341,7 +377,15 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
         e = dalloc(&h->pdata, (size_t)g.Dp);
     if (e == hipSuccess && cfg->problem == ES_PROB_MLP)
         e = dalloc(reinterpret_cast<char**>(&h->mlp_scratch), mlp_scratch_bytes());
-    if (e == hipSuccess && h->tell.nsplit > 1) e = dalloc(&h->tell_part, tell_part_elems(g, h->tell));
+    if (e == hipSuccess && h->tell.nsplit > 1)
+        e = dalloc(&h->tell_part, tell_part_elems(g, h->tell, cfg->strategy));
+    if (e == hipSuccess && cfg->strategy != ES_STRAT_OPENAI_ES) e = dalloc(&h->bfold, (size_t)g.P * g.R);
+    if (e == hipSuccess && cfg->strategy != ES_STRAT_OPENAI_ES) e = dalloc(&h->sig, rows);
+    const bool clipup = cfg->strategy != ES_STRAT_SNES && cfg->optimizer == ES_OPT_CLIPUP;
+    if (e == hipSuccess && clipup) e = dalloc(&h->vel, rows);
+    if (e == hipSuccess && clipup) e = dalloc(&h->gbuf, rows);
+    if (e == hipSuccess && clipup) e = dalloc(&h->gpart, tell_groups(g) * g.R);
+    if (e == hipSuccess && clipup) e = dalloc(&h->vpart, tell_groups(g) * g.R);
     if (e != hipSuccess) {
         free_all(h);
         delete h;
@@ -358,7 +402,7 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
         delete h;
         return init_fail(ES_ERR_OOM, "host allocation failed");
     }
-    weight_table(g.N, tab);
+    h->ybar_table = weight_table(*cfg, g.N, tab);
     for (int32_t r = 0; r < g.R; ++r) {
         ok[r] = 0xFF800000u;  // order key of +inf: nothing is an improvement over it but a finite key
         bf[r] = NAN;
@@ -372,6 +416,8 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);  // host staging buffers are freed next
     std::free(tab); std::free(ok); std::free(bf); std::free(hp);
     if (e == hipSuccess) e = launch_init(g, *cfg, h->m, h->m1, h->v, h->best_x, h->stream);
+    if (e == hipSuccess && h->sig) e = launch_fill_rows(g, h->sig, cfg->sigma, h->stream);
+    if (e == hipSuccess && h->vel) e = launch_fill_rows(g, h->vel, 0.0f, h->stream);
     if (e == hipSuccess && h->pdata) e = launch_problem_data(g, *cfg, h->pdata, h->stream);
     if (e == hipSuccess && h->mlp_scratch) e = launch_mlp_setup(h->pdata, h->mlp_scratch, h->stream);
     if (e != hipSuccess) {
@@ -389,7 +435,8 @@ es_status es_ask(es_handle* h, float* x_out)
     if (!h) return ES_ERR_ARG;
     if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_ask: previous generation was not told");
     if (x_out)
-        ES_HIP(h, launch_ask(h->g, h->cfg, (uint32_t)h->t, h->m, x_out, h->hp[h->hp_cur], h->stream), "ask kernel");
+        ES_HIP(h, launch_ask(h->g, h->cfg, (uint32_t)h->t, h->m, x_out, h->hp[h->hp_cur], h->sig, h->stream),
+               "ask kernel");
     h->phase = ASKED;
     h->err[0] = 0;
     return ES_OK;
@@ -531,6 +578,29 @@ es_status es_get_hparams(es_handle* h, float* sigma, float* lr)
     return ES_OK;
 }
 
+es_status es_get_strategy_state(es_handle* h, float* sigma_vec, float* velocity)
+{
+    if (!h) return ES_ERR_ARG;
+    if ((sigma_vec && !h->sig) || (velocity && !h->vel))
+        return fail(h, ES_ERR_UNSUPPORTED, "es_get_strategy_state: the strategy keeps no such state");
+    es_status s = ES_OK;
+    if (sigma_vec && (s = copy_rows_out(h, sigma_vec, h->sig)) != ES_OK) return s;
+    if (velocity && (s = copy_rows_out(h, velocity, h->vel)) != ES_OK) return s;
+    return ES_OK;
+}
+
+es_status es_set_strategy_state(es_handle* h, const float* sigma_vec, const float* velocity)
+{
+    if (!h) return ES_ERR_ARG;
+    if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_set_strategy_state: an ask is open");
+    if ((sigma_vec && !h->sig) || (velocity && !h->vel))
+        return fail(h, ES_ERR_UNSUPPORTED, "es_set_strategy_state: the strategy keeps no such state");
+    es_status s = ES_OK;
+    if (sigma_vec && (s = copy_rows_in(h, h->sig, sigma_vec)) != ES_OK) return s;
+    if (velocity && (s = copy_rows_in(h, h->vel, velocity)) != ES_OK) return s;
+    return ES_OK;
+}
+
 es_status es_get_penalty(es_handle* h, float* pen)
 {
     if (!h || !pen) return h ? fail(h, ES_ERR_ARG, "es_get_penalty: null buffer") : ES_ERR_ARG;
@@ -564,7 +634,8 @@ es_status es_save_state(es_handle* h, void* host_buf, size_t* bytes)
     if (!h || !bytes) return ES_ERR_ARG;
     const Geometry& g = h->g;
     const size_t rows = (size_t)g.Dp * g.R * sizeof(float);
-    const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + 3 * sizeof(float));
+    const size_t extra = (h->sig ? rows : 0) + (h->vel ? rows : 0);
+    const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + 3 * sizeof(float)) + extra;
     if (!host_buf) {
         *bytes = need;
         return ES_OK;
@@ -593,6 +664,12 @@ es_status es_save_state(es_handle* h, void* host_buf, size_t* bytes)
     p += g.R * sizeof(float);
     ES_HIP(h, hipMemcpyAsync(p, h->hp[h->hp_cur], 2 * g.R * sizeof(float), hipMemcpyDeviceToHost, h->stream),
            "save sigma and lr");
+    p += 2 * g.R * sizeof(float);
+    for (const float* src : {static_cast<const float*>(h->sig), static_cast<const float*>(h->vel)}) {
+        if (!src) continue;
+        ES_HIP(h, hipMemcpyAsync(p, src, rows, hipMemcpyDeviceToHost, h->stream), "save strategy state");
+        p += rows;
+    }
     ES_HIP(h, hipStreamSynchronize(h->stream), "save sync");
     *bytes = need;
     return ES_OK;
@@ -604,7 +681,8 @@ es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes)
     if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_load_state: an ask is open");
     const Geometry& g = h->g;
     const size_t rows = (size_t)g.Dp * g.R * sizeof(float);
-    const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + 3 * sizeof(float));
+    const size_t extra = (h->sig ? rows : 0) + (h->vel ? rows : 0);
+    const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + 3 * sizeof(float)) + extra;
     if (bytes < need) return fail(h, ES_ERR_ARG, "es_load_state: checkpoint too small");
     CkptHeader hd;
     std::memcpy(&hd, host_buf, sizeof(hd));
@@ -624,6 +702,12 @@ es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes)
     p += g.R * sizeof(float);
     ES_HIP(h, hipMemcpyAsync(h->hp[h->hp_cur], p, 2 * g.R * sizeof(float), hipMemcpyHostToDevice, h->stream),
            "load sigma and lr");
+    p += 2 * g.R * sizeof(float);
+    for (float* dst : {h->sig, h->vel}) {
+        if (!dst) continue;
+        ES_HIP(h, hipMemcpyAsync(dst, p, rows, hipMemcpyHostToDevice, h->stream), "load strategy state");
+        p += rows;
+    }
     ES_HIP(h, hipStreamSynchronize(h->stream), "load sync");
     h->t = hd.t;
     return ES_OK;

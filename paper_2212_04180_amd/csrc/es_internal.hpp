@@ -41,16 +41,20 @@ int64_t eval_partial_elems(const Geometry& g, const EvalPlan& e);  // floats
 hipError_t launch_init(const Geometry& g, const es_config& c, float* m, float* m1, float* v,
                        float* best_x, hipStream_t s);
 hipError_t launch_problem_data(const Geometry& g, const es_config& c, float* pdata, hipStream_t s);
+hipError_t launch_fill_rows(const Geometry& g, float* p, float value, hipStream_t s);  // [R][Dp], padding 0
 // hp: device [2][R], sigma then lr of every run for the current generation.
+// svec: per-dimension sigma [R][Dp] (PGPE, SNES) or null.
 hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const float* m, float* x,
-                      const float* hp, hipStream_t s);
+                      const float* hp, const float* svec, hipStream_t s);
 hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t,
                             const float* m, const float* pdata, float* partial, float* fit,
-                            const float* hp, double div, hipStream_t s);
+                            const float* hp, const float* svec, double div, hipStream_t s);
+// table: the shaping table indexed by rank (centered ranks, or SNES
+// utilities by rank), ybar_table its mean; bfold: PGPE / SNES second weight.
 hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* pen,
-                       const float* table, float* y, int32_t* rank, float* wfold, uint32_t* best_okey,
-                       float* best_f, int32_t* best_j, float* gen_best, const float* hp_cur, float* hp_next,
-                       hipStream_t s);
+                       const float* table, double ybar_table, float* y, int32_t* rank, float* wfold, float* bfold,
+                       uint32_t* best_okey, float* best_f, int32_t* best_j, float* gen_best, const float* hp_cur,
+                       float* hp_next, hipStream_t s);
 // Split of the gradient kernel's pairs: ps pair slices (one wave each) per
 // workgroup, nsplit workgroups per group of 64 Philox blocks.  With nsplit > 1
 // every workgroup stores its partial sums (part, fp64 [R][nsplit][nb][4]) and
@@ -60,10 +64,29 @@ struct TellPlan {
     int32_t nsplit = 1;
 };
 TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit);
-size_t tell_part_elems(const Geometry& g, const TellPlan& tp);
+size_t tell_part_elems(const Geometry& g, const TellPlan& tp, int strategy);  // doubles
+size_t tell_groups(const Geometry& g);  // groups of 64 Philox blocks per run
+
+// Device buffers of one tell (null where the strategy has none).
+struct TellBuffers {
+    const float* wfold;    // [R][P]
+    const float* bfold;    // [R][P] PGPE / SNES
+    const int32_t* best_j; // [R]
+    float* m;
+    float* m1;
+    float* v;
+    float* grad;           // [R][Dp] with ES_FLAG_KEEP_GRAD
+    float* best_x;
+    float* sig;            // [R][Dp] PGPE / SNES per-dimension sigma
+    float* vel;            // [R][Dp] ClipUp velocity
+    float* gbuf;           // [R][Dp] ClipUp gradient
+    double* gpart;         // [R][groups] ClipUp |g|^2 partials
+    double* vpart;         // [R][groups] ClipUp |v|^2 partials
+    double* part;          // split partial sums
+    const float* hp;       // [2][R] sigma, lr
+};
 hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp, uint32_t t, const AdamConsts& a,
-                       const float* wfold, const int32_t* best_j, float* m, float* m1, float* v, float* grad,
-                       float* best_x, double* part, const float* hp, hipStream_t s);
+                       const TellBuffers& tb, hipStream_t s);
 hipError_t launch_debug_noise(const Geometry& g, const es_config& c, int32_t run, uint32_t t,
                               int32_t pair, uint32_t* words, float* eps, hipStream_t s);
 
@@ -86,7 +109,7 @@ size_t mlp_scratch_bytes();  // X_t (fp32 and bf16), teacher outputs, transposed
 hipError_t launch_mlp_setup(const float* teacher, void* scratch, hipStream_t s);
 size_t mlp_lds_bytes();
 hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, const float* m, const float* teacher,
-                           void* scratch, float* fit, const float* hp, hipStream_t s);
+                           void* scratch, float* fit, const float* hp, const float* svec, hipStream_t s);
 
 // Largest population the rank kernel stages in LDS.
 constexpr int32_t RANK_MAX_N = 16384;

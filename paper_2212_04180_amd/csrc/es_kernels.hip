@@ -98,7 +98,8 @@ __global__ void k_problem_data(float* __restrict__ out, uint64_t seed, int64_t D
 
 // ---------------------------------------------------------------------------
 __global__ void k_ask(const float* __restrict__ m, float* __restrict__ x, uint64_t seed, uint32_t t,
-                      int64_t D, int64_t nb, int32_t N, int32_t P, int32_t R, const float* __restrict__ hp)
+                      int64_t D, int64_t nb, int32_t N, int32_t P, int32_t R, const float* __restrict__ hp,
+                      const float* __restrict__ svec)
 {
     const int64_t total = (int64_t)R * P * nb;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
@@ -116,8 +117,9 @@ __global__ void k_ask(const float* __restrict__ m, float* __restrict__ x, uint64
         for (int k = 0; k < 4; ++k) {
             const int64_t d = 4 * b + k;
             if (d < D) {
-                xp[d] = fmaf(sigma, e[k], mr[d]);
-                xm[d] = fmaf(-sigma, e[k], mr[d]);
+                const float g = svec ? svec[r * 4 * nb + d] : sigma;
+                xp[d] = fmaf(g, e[k], mr[d]);
+                xm[d] = fmaf(-g, e[k], mr[d]);
             }
         }
     }
@@ -162,17 +164,19 @@ struct EvalLane {
     bool have_prev;
 };
 
-// Terms of one full Philox block (four live dims) for both members.
-template <int PROB>
-__device__ __forceinline__ void block_terms(const float e[4], const float mv[4], const float sv[4], float sg,
-                                            float ra, EvalLane& L, float& sp, float& sm)
+// Terms of one full Philox block (four live dims) for both members.  VEC:
+// per-dimension sigma gv[] (PGPE, SNES) instead of the run's scalar sg.
+template <int PROB, bool VEC>
+__device__ __forceinline__ void block_terms(const float e[4], const float mv[4], const float sv[4], const float* gv,
+                                            float sg, float ra, EvalLane& L, float& sp, float& sm)
 {
     if constexpr (PROB == ES_PROB_ROSENBROCK) {
         float xp[4], xm[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            xp[k] = fmaf(sg, e[k], mv[k]);
-            xm[k] = fmaf(-sg, e[k], mv[k]);
+            const float g = VEC ? gv[k] : sg;
+            xp[k] = fmaf(g, e[k], mv[k]);
+            xm[k] = fmaf(-g, e[k], mv[k]);
         }
         float tp = rosen_term(xp[0], xp[1]) + rosen_term(xp[1], xp[2]) + rosen_term(xp[2], xp[3]);
         float tm = rosen_term(xm[0], xm[1]) + rosen_term(xm[1], xm[2]) + rosen_term(xm[2], xm[3]);
@@ -188,8 +192,9 @@ __device__ __forceinline__ void block_terms(const float e[4], const float mv[4],
     } else {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            sp += BlockTerm<PROB>::f(fmaf(sg, e[k], mv[k]), sv[k], ra);
-            sm += BlockTerm<PROB>::f(fmaf(-sg, e[k], mv[k]), sv[k], ra);
+            const float g = VEC ? gv[k] : sg;
+            sp += BlockTerm<PROB>::f(fmaf(g, e[k], mv[k]), sv[k], ra);
+            sm += BlockTerm<PROB>::f(fmaf(-g, e[k], mv[k]), sv[k], ra);
         }
     }
 }
@@ -198,10 +203,11 @@ __device__ __forceinline__ void block_terms(const float e[4], const float mv[4],
 // run: fp32 sums of EVAL_FOLD blocks folded into fp64, in block order.  The
 // per-call kernel and the fused loop share this code, so both produce the
 // same bits.  V names the counter word that varies across the wave.
-template <int PROB, int V>
+template <int PROB, int V, bool VEC = false>
 __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const float* __restrict__ pdata,
                                            uint32_t k0, uint32_t k1, uint32_t row, uint32_t t, int64_t b0,
-                                           int64_t b1, int64_t D, float sg, float ra, double& accp, double& accm)
+                                           int64_t b1, int64_t D, float sg, float ra, double& accp, double& accm,
+                                           const float* __restrict__ gr = nullptr)
 {
     const int64_t nfull = D / 4;
     const int32_t nf = (int32_t)((b1 < nfull ? b1 : nfull) - b0);  // full blocks in [b0, b1) (may be <= 0)
@@ -210,8 +216,9 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         float e[4];
         box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(b0 - 1), row, t, DOM_NOISE), e);
         const float mv = mr[4 * b0 - 1];
-        L.xlp = fmaf(sg, e[3], mv);
-        L.xlm = fmaf(-sg, e[3], mv);
+        const float g = VEC ? gr[4 * b0 - 1] : sg;
+        L.xlp = fmaf(g, e[3], mv);
+        L.xlm = fmaf(-g, e[3], mv);
         L.have_prev = true;
     }
 
@@ -219,9 +226,13 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
     int32_t i = 0;
     for (; i + EVAL_FOLD <= nf; i += EVAL_FOLD) {
         const int64_t bg = b0 + i;
-        float mv[4 * EVAL_FOLD], sv[4 * EVAL_FOLD];
+        float mv[4 * EVAL_FOLD], sv[4 * EVAL_FOLD], gv[VEC ? 4 * EVAL_FOLD : 1];
 #pragma unroll
         for (int q = 0; q < 4 * EVAL_FOLD; ++q) mv[q] = mr[4 * bg + q];
+        if constexpr (VEC) {
+#pragma unroll
+            for (int q = 0; q < 4 * EVAL_FOLD; ++q) gv[q] = gr[4 * bg + q];
+        }
         if constexpr (PROB == ES_PROB_SHIFTED_SPHERE) {
 #pragma unroll
             for (int q = 0; q < 4 * EVAL_FOLD; ++q) sv[q] = pdata[4 * bg + q];
@@ -231,17 +242,21 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         for (int k = 0; k < EVAL_FOLD; ++k) {
             float e[4];
             box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(bg + k), row, t, DOM_NOISE), e);
-            block_terms<PROB>(e, mv + 4 * k, PROB == ES_PROB_SHIFTED_SPHERE ? sv + 4 * k : zero4, sg, ra, L, sp,
-                              sm);
+            block_terms<PROB, VEC>(e, mv + 4 * k, PROB == ES_PROB_SHIFTED_SPHERE ? sv + 4 * k : zero4,
+                                   VEC ? gv + 4 * k : nullptr, sg, ra, L, sp, sm);
         }
         L.accp += (double)sp;
         L.accm += (double)sm;
     }
     for (; i < nf; ++i) {
         const int64_t b = b0 + i;
-        float mv[4], sv[4] = {0.f, 0.f, 0.f, 0.f};
+        float mv[4], sv[4] = {0.f, 0.f, 0.f, 0.f}, gv[4] = {sg, sg, sg, sg};
 #pragma unroll
         for (int q = 0; q < 4; ++q) mv[q] = mr[4 * b + q];
+        if constexpr (VEC) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) gv[q] = gr[4 * b + q];
+        }
         if constexpr (PROB == ES_PROB_SHIFTED_SPHERE) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) sv[q] = pdata[4 * b + q];
@@ -249,7 +264,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         float e[4];
         box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
         float sp = 0.f, sm = 0.f;
-        block_terms<PROB>(e, mv, sv, sg, ra, L, sp, sm);
+        block_terms<PROB, VEC>(e, mv, sv, gv, sg, ra, L, sp, sm);
         L.accp += (double)sp;
         L.accm += (double)sm;
     }
@@ -263,7 +278,8 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         float sp = 0.f, sm = 0.f;
         for (int k = 0; k < nv; ++k) {
             const float mv = mr[4 * b + k];
-            const float xp = fmaf(sg, e[k], mv), xm = fmaf(-sg, e[k], mv);
+            const float g = VEC ? gr[4 * b + k] : sg;
+            const float xp = fmaf(g, e[k], mv), xm = fmaf(-g, e[k], mv);
             if constexpr (PROB == ES_PROB_ROSENBROCK) {
                 if (L.have_prev) {
                     sp += rosen_term(L.xlp, xp);
@@ -285,11 +301,11 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
     accm = L.accm;
 }
 
-template <int PROB>
+template <int PROB, bool VEC>
 __global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
     const float* __restrict__ m, const float* __restrict__ pdata, float* __restrict__ partial,
     uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t N, int32_t P, int64_t bc, int64_t nchunks,
-    int32_t n_pg, const float* __restrict__ hp, float ra)
+    int32_t n_pg, const float* __restrict__ hp, float ra, const float* __restrict__ svec)
 {
     const int32_t r = blockIdx.y;
     const float sigma = hp[r];
@@ -307,8 +323,8 @@ __global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
     float sg;
     asm volatile("v_mov_b32 %0, %1" : "=v"(sg) : "s"(sigma));
     double accp, accm;
-    eval_chunk<PROB, LANES_ROW>(m + (int64_t)r * 4 * nb, pdata, (uint32_t)key, (uint32_t)(key >> 32), row, t, b0,
-                                b1, D, sg, ra, accp, accm);
+    eval_chunk<PROB, LANES_ROW, VEC>(m + (int64_t)r * 4 * nb, pdata, (uint32_t)key, (uint32_t)(key >> 32), row, t,
+                                     b0, b1, D, sg, ra, accp, accm, VEC ? svec + (int64_t)r * 4 * nb : nullptr);
     if (p < P) {
         float* o = partial + (chunk * gridDim.y + r) * (int64_t)N;
         o[p] = (float)accp;
@@ -370,6 +386,11 @@ struct ShapeArgs {
     float sigma_decay, sigma_final, lr_decay, lr_final;
     int32_t shaping;        // es_shaping
     int32_t maximize;
+    // second folded weight per pair for the sigma-adapting strategies:
+    // PGPE b_p = (y_p + y_{p+P})/2 - mean(y), SNES b_p = y_p + y_{p+P}
+    float* bfold;           // [R][P] or null
+    int32_t bmode;          // 0 none, 1 PGPE, 2 SNES
+    double ybar_table;      // mean of the shaping table (table shaping)
 };
 
 __device__ __forceinline__ float shaped_key(float f, float pen, int maximize, float w_decay)
@@ -445,6 +466,24 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
         const double sd = n > 0.0 ? sqrt(ss / n) : 0.0;
         inv_sd = sd + 1e-10;
     }
+    // PGPE baseline: the mean of y over the run (table shaping: the table's
+    // own mean, as the ranks are a permutation)
+    double ybar = sa.ybar_table;
+    if (sa.bmode == 1 && sa.shaping != ES_SHAPE_CENTERED_RANK) {
+        double acc = 0.0;
+        for (int32_t k = threadIdx.x; k < N; k += blockDim.x) {
+            float yk;
+            if (sa.shaping == ES_SHAPE_RAW) {
+                yk = sa.w_decay != 0.0f ? shaped_key(fr[k], pr[k], sa.maximize, sa.w_decay)
+                                        : (sa.maximize ? -fr[k] : fr[k]);
+            } else {
+                const float v = key_value(keys[k]);
+                yk = __builtin_isfinite(v) ? (float)(((double)v - mu) / inv_sd) : 0.0f;
+            }
+            acc += (double)yk;
+        }
+        ybar = block_sum(acc, red) / (double)N;
+    }
     // With weight decay the best-so-far still follows the raw fitness: the
     // smallest raw key, lowest index first.
     const bool penalised = sa.w_decay != 0.0f;
@@ -519,6 +558,8 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
     rr[j1] = r1;
     rr[j2] = r2;
     wfold[(int64_t)r * P + p] = y1 - y2;
+    if (sa.bmode == 1) sa.bfold[(int64_t)r * P + p] = (float)(0.5 * ((double)y1 + (double)y2) - ybar);
+    if (sa.bmode == 2) sa.bfold[(int64_t)r * P + p] = y1 + y2;
     int32_t jb = -1;
     if (penalised) {
         if ((uint32_t)j1 == raw_best[1]) jb = j1;
@@ -584,6 +625,57 @@ __device__ __forceinline__ void tell_slice(const float* __restrict__ wr, uint32_
     for (int k = 0; k < 4; ++k) a64[k] += (double)a32[k];
 }
 
+// Both sums of one Philox block over the pairs [pb, pe) for the strategies
+// that adapt a per-dimension sigma: a64[k] = sum_p a_p z_{p,4b+k} and
+// b64[k] = sum_p b_p (z^2 - 1), fp32 over TELL_GROUP pairs folded into fp64.
+template <int V>
+__device__ __forceinline__ void tell_slice2(const float* __restrict__ ar, const float* __restrict__ br, uint32_t k0,
+                                            uint32_t k1, uint32_t bb, uint32_t t, int32_t pb, int32_t pe,
+                                            double a64[4], double b64[4])
+{
+    int32_t p0 = pb;
+    for (; p0 + TELL_GROUP <= pe; p0 += TELL_GROUP) {
+        float av[TELL_GROUP], bv[TELL_GROUP];
+#pragma unroll
+        for (int q = 0; q < TELL_GROUP; ++q) {
+            av[q] = ar[p0 + q];
+            bv[q] = br[p0 + q];
+        }
+        float a32[4] = {0.f, 0.f, 0.f, 0.f}, b32[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < TELL_GROUP; ++q) {
+            float e[4];
+            box_muller4(philox4x32_10<V>(k0, k1, bb, (uint32_t)(p0 + q), t, DOM_NOISE), e);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                a32[k] = fmaf(av[q], e[k], a32[k]);
+                b32[k] = fmaf(bv[q], fmaf(e[k], e[k], -1.0f), b32[k]);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            a64[k] += (double)a32[k];
+            b64[k] += (double)b32[k];
+        }
+    }
+    float a32[4] = {0.f, 0.f, 0.f, 0.f}, b32[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int32_t p = p0; p < pe; ++p) {
+        float e[4];
+        box_muller4(philox4x32_10<V>(k0, k1, bb, (uint32_t)p, t, DOM_NOISE), e);
+        const float a = ar[p], b = br[p];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            a32[k] = fmaf(a, e[k], a32[k]);
+            b32[k] = fmaf(b, fmaf(e[k], e[k], -1.0f), b32[k]);
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        a64[k] += (double)a32[k];
+        b64[k] += (double)b32[k];
+    }
+}
+
 // g = sum / (N sigma), then Adam (Kingma & Ba) in fp32 in a fixed operation
 // order on four dims; dims at or beyond D stay zero.
 __device__ __forceinline__ void adam_block(const double a64[4], double inv_ns, const AdamConsts& ac, float lr, int64_t d0,
@@ -607,111 +699,293 @@ __device__ __forceinline__ void adam_block(const double a64[4], double inv_ns, c
     }
 }
 
-// Adam step of one Philox block from its gradient sum, the best member's
-// parameters when the generation improved on the best so far, and the
-// gradient itself when asked for.
-__device__ __forceinline__ void tell_finish(const double a64[4], int64_t b, int32_t r, uint32_t k0, uint32_t k1,
-                                            uint32_t t, int64_t D, int64_t nb, int32_t P, float sigma, float lr,
-                                            const AdamConsts& ac, const int32_t* __restrict__ best_j,
-                                            float* __restrict__ m, float* __restrict__ m1, float* __restrict__ v,
-                                            float* __restrict__ grad, float* __restrict__ best_x)
+// Everything the gradient kernels need besides the geometry.
+struct TellArgs {
+    const float* wfold;    // [R][P] a_p = y_p - y_{p+P}
+    const float* bfold;    // [R][P] second weight (PGPE, SNES) or null
+    const int32_t* best_j; // [R]
+    float* m;
+    float* m1;
+    float* v;
+    float* grad;           // [R][Dp] or null
+    float* best_x;
+    float* sig;            // [R][Dp] per-dimension sigma (PGPE, SNES) or null
+    float* gbuf;           // [R][Dp] ClipUp: the gradient, stepped by the ClipUp kernels
+    double* gpart;         // [R][groups] ClipUp: |g|^2 of each group of 64 blocks
+    double* part;          // split partial sums [R][nsplit][nb][4 or 8]
+    const float* hp;       // [2][R] sigma, lr
+    uint64_t seed;
+    uint32_t t;
+    int64_t D, nb;
+    int32_t P, R, ps, nsplit;
+    int32_t strategy, optimizer;
+    float sigma_lr, max_change, sigma_decay, sigma_final;
+    AdamConsts ac;
+};
+
+__device__ __forceinline__ double wave_sum(double v)
 {
-    const int64_t off = (int64_t)r * 4 * nb + 4 * b;
-    const float4 m4 = *reinterpret_cast<const float4*>(m + off);
-    const float4 m14 = *reinterpret_cast<const float4*>(m1 + off);
-    const float4 v4 = *reinterpret_cast<const float4*>(v + off);
-    const float mo[4] = {m4.x, m4.y, m4.z, m4.w};
-    const float m1o[4] = {m14.x, m14.y, m14.z, m14.w};
-    const float vo[4] = {v4.x, v4.y, v4.z, v4.w};
-    float mn[4], m1n[4], vn[4], gg[4];
-    const double inv_ns = 1.0 / (2.0 * (double)P * (double)sigma);  // 1 / (N sigma)
-    adam_block(a64, inv_ns, ac, lr, 4 * b, D, mo, m1o, vo, mn, m1n, vn, gg);
-    const int32_t jb = best_j[r];
-    if (jb >= 0) {
-        const int32_t pbst = jb < P ? jb : jb - P;
-        const float sg = jb < P ? sigma : -sigma;
-        float e[4];
-        box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)b, (uint32_t)pbst, t, DOM_NOISE), e);
-        float bx[4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) bx[k] = 4 * b + k < D ? fmaf(sg, e[k], mo[k]) : 0.f;
-        *reinterpret_cast<float4*>(best_x + off) = make_float4(bx[0], bx[1], bx[2], bx[3]);
-    }
-    *reinterpret_cast<float4*>(m + off) = make_float4(mn[0], mn[1], mn[2], mn[3]);
-    *reinterpret_cast<float4*>(m1 + off) = make_float4(m1n[0], m1n[1], m1n[2], m1n[3]);
-    *reinterpret_cast<float4*>(v + off) = make_float4(vn[0], vn[1], vn[2], vn[3]);
-    if (grad) *reinterpret_cast<float4*>(grad + off) = make_float4(gg[0], gg[1], gg[2], gg[3]);
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
 }
 
-// Gradient + Adam.  Workgroup = TELL_LANES Philox blocks x ps pair slices
-// (ps <= TELL_MAX_PS, chosen per geometry) of one run.  Each lane walks its
-// slice of pairs with the folded weight w_p = y_p - y_{p+N/2} (uniform across
-// the wave), regenerating the pair's normals, so g_d = sum_p w_p eps_{p,d} /
-// (N sigma) needs no cross-lane reduction; the slices meet in LDS in a fixed
-// order.  With nsplit > 1, grid.z = nsplit workgroups share a block group
-// (workgroup z takes global slices z*ps .. z*ps+ps-1 of ps*nsplit equal
-// slices of the pairs) and store their sums to part; k_tell_fold adds them in
-// split order and applies Adam.
-__global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(
-    const float* __restrict__ wfold, const int32_t* __restrict__ best_j, float* __restrict__ m,
-    float* __restrict__ m1, float* __restrict__ v, float* __restrict__ grad,
-    float* __restrict__ best_x, uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t P, int32_t ps,
-    int32_t nsplit, double* __restrict__ part, const float* __restrict__ hp, int32_t R, AdamConsts ac)
+// Update of one Philox block from its noise sums a64 (and b64):
+//   OpenAI-ES  g = a / (N sigma), Adam (or ClipUp, stepped later);
+//   PGPE       g = sigma_d a / N, Adam or ClipUp on the mean;
+//              s = sigma_d b / P, sigma += clip(-sigma_lr s, +-max_change sigma), schedule;
+//   SNES       m += fl32(lr sigma_d) a, sigma *= exp(fl32(sigma_lr/2) b), schedule.
+// Also the best member's parameters when the generation improved on the
+// best so far (old mean and sigma), and the gradient when asked for.
+// Returns this lane's share of |g|^2 (ClipUp), else 0.
+__device__ __forceinline__ double tell_finish(const TellArgs& a, const double a64[4], const double b64[4], int64_t b,
+                                              int32_t r, uint32_t k0, uint32_t k1)
 {
-    __shared__ double red[TELL_MAX_PS - 1][TELL_LANES][4];
+    const int64_t off = (int64_t)r * 4 * a.nb + 4 * b;
+    const float sigma = a.hp[r], lr = a.hp[a.R + r];
+    const float4 m4 = *reinterpret_cast<const float4*>(a.m + off);
+    const float mo[4] = {m4.x, m4.y, m4.z, m4.w};
+    float so[4] = {sigma, sigma, sigma, sigma};
+    if (a.sig) {
+        const float4 s4 = *reinterpret_cast<const float4*>(a.sig + off);
+        so[0] = s4.x; so[1] = s4.y; so[2] = s4.z; so[3] = s4.w;
+    }
+    const int32_t N = 2 * a.P;
+    float mn[4] = {mo[0], mo[1], mo[2], mo[3]}, gg[4] = {0.f, 0.f, 0.f, 0.f}, sn[4] = {so[0], so[1], so[2], so[3]};
+    double g2 = 0.0;
+    if (a.strategy == ES_STRAT_SNES) {
+        const float h = 0.5f * a.sigma_lr;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const float A = (float)a64[k], B = (float)b64[k];
+            if (4 * b + k < a.D) {
+                mn[k] = fmaf(__fmul_rn(lr, so[k]), A, mo[k]);
+                sn[k] = schedule_step(__fmul_rn(so[k], expf(__fmul_rn(h, B))), a.sigma_decay, a.sigma_final);
+                gg[k] = __fmul_rn(so[k], A);
+            } else {
+                mn[k] = 0.f; sn[k] = 0.f;
+            }
+        }
+    } else {
+        const double inv_ns = 1.0 / ((double)N * (double)sigma);  // 1 / (N sigma)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            gg[k] = a.strategy == ES_STRAT_PGPE ? (float)((double)so[k] * a64[k] / (double)N) : (float)(a64[k] * inv_ns);
+            if (4 * b + k >= a.D) gg[k] = 0.f;
+        }
+        if (a.optimizer == ES_OPT_CLIPUP) {
+            *reinterpret_cast<float4*>(a.gbuf + off) = make_float4(gg[0], gg[1], gg[2], gg[3]);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) g2 += (double)gg[k] * (double)gg[k];
+        } else {
+            const float4 m14 = *reinterpret_cast<const float4*>(a.m1 + off);
+            const float4 v4 = *reinterpret_cast<const float4*>(a.v + off);
+            const float m1o[4] = {m14.x, m14.y, m14.z, m14.w};
+            const float vo[4] = {v4.x, v4.y, v4.z, v4.w};
+            float m1n[4], vn[4], gd[4];
+            const double a1[4] = {(double)gg[0], (double)gg[1], (double)gg[2], (double)gg[3]};
+            adam_block(a1, 1.0, a.ac, lr, 4 * b, a.D, mo, m1o, vo, mn, m1n, vn, gd);
+            *reinterpret_cast<float4*>(a.m1 + off) = make_float4(m1n[0], m1n[1], m1n[2], m1n[3]);
+            *reinterpret_cast<float4*>(a.v + off) = make_float4(vn[0], vn[1], vn[2], vn[3]);
+        }
+        if (a.strategy == ES_STRAT_PGPE) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float sg = (float)((double)so[k] * b64[k] / (double)a.P);
+                float dlt = -__fmul_rn(a.sigma_lr, sg);
+                const float lim = __fmul_rn(a.max_change, so[k]);
+                dlt = dlt > lim ? lim : dlt;
+                dlt = dlt < -lim ? -lim : dlt;
+                sn[k] = 4 * b + k < a.D ? schedule_step(__fadd_rn(so[k], dlt), a.sigma_decay, a.sigma_final) : 0.f;
+            }
+        }
+    }
+    const int32_t jb = a.best_j[r];
+    if (jb >= 0) {
+        const int32_t pbst = jb < a.P ? jb : jb - a.P;
+        float e[4];
+        box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)b, (uint32_t)pbst, a.t, DOM_NOISE), e);
+        float bx[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) bx[k] = 4 * b + k < a.D ? fmaf(jb < a.P ? so[k] : -so[k], e[k], mo[k]) : 0.f;
+        *reinterpret_cast<float4*>(a.best_x + off) = make_float4(bx[0], bx[1], bx[2], bx[3]);
+    }
+    if (a.strategy == ES_STRAT_SNES || a.optimizer != ES_OPT_CLIPUP)
+        *reinterpret_cast<float4*>(a.m + off) = make_float4(mn[0], mn[1], mn[2], mn[3]);
+    if (a.sig) *reinterpret_cast<float4*>(a.sig + off) = make_float4(sn[0], sn[1], sn[2], sn[3]);
+    if (a.grad) *reinterpret_cast<float4*>(a.grad + off) = make_float4(gg[0], gg[1], gg[2], gg[3]);
+    return g2;
+}
+
+// Gradient + update.  Workgroup = TELL_LANES Philox blocks x ps pair slices
+// (ps <= TELL_MAX_PS, chosen per geometry) of one run.  Each lane walks its
+// slice of pairs with the folded weights (uniform across the wave),
+// regenerating the pair's normals, so the sums over pairs need no
+// cross-lane reduction; the slices meet in LDS in a fixed order.  With
+// nsplit > 1, grid.z = nsplit workgroups share a block group (workgroup z
+// takes global slices z*ps .. z*ps+ps-1 of ps*nsplit equal slices of the
+// pairs) and store their sums to part; k_tell_fold adds them in split order
+// and applies the update.  TWO: the second sum b (PGPE, SNES).
+template <bool TWO>
+__global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
+{
+    __shared__ double red[TELL_MAX_PS - 1][TELL_LANES][TWO ? 8 : 4];
     const int32_t r = blockIdx.y, z = blockIdx.z;
     const int32_t tx = threadIdx.x % TELL_LANES;
     // one wave per pair slice: make the slice index (and the pair loop) uniform
     const int32_t s = __builtin_amdgcn_readfirstlane(threadIdx.x / TELL_LANES);
     const int64_t b = (int64_t)blockIdx.x * TELL_LANES + tx;
-    const uint32_t bb = (uint32_t)(b < nb ? b : nb - 1);
-    const uint64_t key = seed + (uint64_t)r;
+    const uint32_t bb = (uint32_t)(b < a.nb ? b : a.nb - 1);
+    const uint64_t key = a.seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
-    const int64_t S = (int64_t)ps * nsplit, gs = (int64_t)z * ps + s;
-    const int32_t pb = (int32_t)(((int64_t)P * gs) / S);
-    const int32_t pe = (int32_t)(((int64_t)P * (gs + 1)) / S);
+    const int64_t S = (int64_t)a.ps * a.nsplit, gs = (int64_t)z * a.ps + s;
+    const int32_t pb = (int32_t)(((int64_t)a.P * gs) / S);
+    const int32_t pe = (int32_t)(((int64_t)a.P * (gs + 1)) / S);
 
-    double a64[4] = {0.0, 0.0, 0.0, 0.0};
-    tell_slice<LANES_BLOCK>(wfold + (int64_t)r * P, k0, k1, bb, t, pb, pe, a64);
+    double a64[4] = {0.0, 0.0, 0.0, 0.0}, b64[4] = {0.0, 0.0, 0.0, 0.0};
+    if constexpr (TWO)
+        tell_slice2<LANES_BLOCK>(a.wfold + (int64_t)r * a.P, a.bfold + (int64_t)r * a.P, k0, k1, bb, a.t, pb, pe,
+                                 a64, b64);
+    else
+        tell_slice<LANES_BLOCK>(a.wfold + (int64_t)r * a.P, k0, k1, bb, a.t, pb, pe, a64);
     if (s > 0) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) red[s - 1][tx][k] = a64[k];
+        for (int k = 0; k < 4; ++k) {
+            red[s - 1][tx][k] = a64[k];
+            if constexpr (TWO) red[s - 1][tx][4 + k] = b64[k];
+        }
     }
     __syncthreads();
-    if (s != 0 || b >= nb) return;
-    for (int q = 0; q < ps - 1; ++q)
+    if (s != 0) return;
+    for (int q = 0; q < a.ps - 1; ++q)
 #pragma unroll
-        for (int k = 0; k < 4; ++k) a64[k] += red[q][tx][k];
-    if (nsplit > 1) {
-        *reinterpret_cast<double4*>(part + (((int64_t)r * nsplit + z) * nb + b) * 4) =
-            make_double4(a64[0], a64[1], a64[2], a64[3]);
+        for (int k = 0; k < 4; ++k) {
+            a64[k] += red[q][tx][k];
+            if constexpr (TWO) b64[k] += red[q][tx][4 + k];
+        }
+    if (a.nsplit > 1) {
+        if (b < a.nb) {
+            double* o = a.part + (((int64_t)r * a.nsplit + z) * a.nb + b) * (TWO ? 8 : 4);
+            *reinterpret_cast<double4*>(o) = make_double4(a64[0], a64[1], a64[2], a64[3]);
+            if constexpr (TWO) *reinterpret_cast<double4*>(o + 4) = make_double4(b64[0], b64[1], b64[2], b64[3]);
+        }
         return;
     }
-    tell_finish(a64, b, r, k0, k1, t, D, nb, P, hp[r], hp[R + r], ac, best_j, m, m1, v, grad, best_x);
+    const double g2 = b < a.nb ? tell_finish(a, a64, b64, b, r, k0, k1) : 0.0;
+    if (a.gpart) {
+        const double tot = wave_sum(g2);
+        if (tx == 0) a.gpart[(int64_t)r * gridDim.x + blockIdx.x] = tot;
+    }
 }
 
 // Second half of a split gradient: the nsplit workgroup sums of each Philox
-// block added in split order, then Adam.  One lane per block.
-__global__ __launch_bounds__(256) void k_tell_fold(const double* __restrict__ part, const int32_t* __restrict__ best_j,
-                                                   float* __restrict__ m, float* __restrict__ m1,
-                                                   float* __restrict__ v, float* __restrict__ grad,
-                                                   float* __restrict__ best_x, uint64_t seed, uint32_t t, int64_t D,
-                                                   int64_t nb, int32_t P, int32_t nsplit,
-                                                   const float* __restrict__ hp, int32_t R, AdamConsts ac)
+// block added in split order, then the update.  One lane per block; each
+// wave covers one group of 64 blocks.
+template <bool TWO>
+__global__ __launch_bounds__(256) void k_tell_fold(TellArgs a)
 {
     const int32_t r = blockIdx.y;
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= nb) return;
-    const uint64_t key = seed + (uint64_t)r;
+    const uint64_t key = a.seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
-    const double* p0 = part + ((int64_t)r * nsplit * nb + b) * 4;
-    const double4 q0 = *reinterpret_cast<const double4*>(p0);
-    double a64[4] = {q0.x, q0.y, q0.z, q0.w};
-    for (int32_t q = 1; q < nsplit; ++q) {
-        const double4 qq = *reinterpret_cast<const double4*>(p0 + (int64_t)q * nb * 4);
-        a64[0] += qq.x; a64[1] += qq.y; a64[2] += qq.z; a64[3] += qq.w;
+    double g2 = 0.0;
+    if (b < a.nb) {
+        constexpr int W = TWO ? 8 : 4;
+        const double* p0 = a.part + ((int64_t)r * a.nsplit * a.nb + b) * W;
+        double a64[4], b64[4] = {0.0, 0.0, 0.0, 0.0};
+        const double4 q0 = *reinterpret_cast<const double4*>(p0);
+        a64[0] = q0.x; a64[1] = q0.y; a64[2] = q0.z; a64[3] = q0.w;
+        if constexpr (TWO) {
+            const double4 r0 = *reinterpret_cast<const double4*>(p0 + 4);
+            b64[0] = r0.x; b64[1] = r0.y; b64[2] = r0.z; b64[3] = r0.w;
+        }
+        for (int32_t q = 1; q < a.nsplit; ++q) {
+            const double* pq = p0 + (int64_t)q * a.nb * W;
+            const double4 qq = *reinterpret_cast<const double4*>(pq);
+            a64[0] += qq.x; a64[1] += qq.y; a64[2] += qq.z; a64[3] += qq.w;
+            if constexpr (TWO) {
+                const double4 rr = *reinterpret_cast<const double4*>(pq + 4);
+                b64[0] += rr.x; b64[1] += rr.y; b64[2] += rr.z; b64[3] += rr.w;
+            }
+        }
+        g2 = tell_finish(a, a64, b64, b, r, k0, k1);
     }
-    tell_finish(a64, b, r, k0, k1, t, D, nb, P, hp[r], hp[R + r], ac, best_j, m, m1, v, grad, best_x);
+    if (a.gpart) {
+        const double tot = wave_sum(g2);
+        const int64_t groups = (a.nb + TELL_LANES - 1) / TELL_LANES;
+        if ((threadIdx.x & 63) == 0 && (b >> 6) < groups) a.gpart[(int64_t)r * groups + (b >> 6)] = tot;
+    }
+}
+
+// ClipUp (Toklu et al. 2020) after the gradient kernel, two passes over the
+// run's dims.  Each workgroup sums the per-group partials of |g|^2 (then
+// |v'|^2) in the same fixed order, so every workgroup sees the same norm.
+__device__ __forceinline__ double group_total(const double* __restrict__ part, int64_t n, double* red)
+{
+    double acc = 0.0;
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) acc += part[i];
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    const double tot = red[0];
+    __syncthreads();
+    return tot;
+}
+
+// v' = fmaf(lr, g * fl32(1/|g|), momentum * v); stores v' and |v'|^2 per group.
+__global__ __launch_bounds__(256) void k_clipup_velocity(const float* __restrict__ gbuf, float* __restrict__ vel,
+                                                         const double* __restrict__ gpart, double* __restrict__ vpart,
+                                                         const float* __restrict__ hp, int32_t R, int64_t nb,
+                                                         int64_t groups, float momentum)
+{
+    __shared__ double red[256];
+    const int32_t r = blockIdx.y;
+    const double gg = group_total(gpart + (int64_t)r * groups, groups, red);
+    const float inv = gg > 0.0 ? (float)(1.0 / sqrt(gg)) : 0.0f;
+    const float lr = hp[R + r];
+    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    double v2 = 0.0;
+    if (b < nb) {
+        const int64_t off = (int64_t)r * 4 * nb + 4 * b;
+        const float4 g4 = *reinterpret_cast<const float4*>(gbuf + off);
+        const float4 v4 = *reinterpret_cast<const float4*>(vel + off);
+        const float g[4] = {g4.x, g4.y, g4.z, g4.w}, vo[4] = {v4.x, v4.y, v4.z, v4.w};
+        float vn[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            vn[k] = fmaf(lr, __fmul_rn(g[k], inv), __fmul_rn(momentum, vo[k]));
+            v2 += (double)vn[k] * (double)vn[k];
+        }
+        *reinterpret_cast<float4*>(vel + off) = make_float4(vn[0], vn[1], vn[2], vn[3]);
+    }
+    const double tot = wave_sum(v2);
+    if ((threadIdx.x & 63) == 0 && (b >> 6) < groups) vpart[(int64_t)r * groups + (b >> 6)] = tot;
+}
+
+// v = v' * fl32(max_speed / |v'|) when |v'| > max_speed; m -= v.
+__global__ __launch_bounds__(256) void k_clipup_apply(float* __restrict__ vel, float* __restrict__ m,
+                                                      const double* __restrict__ vpart, int64_t nb, int64_t groups,
+                                                      float max_speed)
+{
+    __shared__ double red[256];
+    const int32_t r = blockIdx.y;
+    const double nv = sqrt(group_total(vpart + (int64_t)r * groups, groups, red));
+    const bool clip = nv > (double)max_speed;
+    const float sc = clip ? (float)((double)max_speed / nv) : 1.0f;
+    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= nb) return;
+    const int64_t off = (int64_t)r * 4 * nb + 4 * b;
+    float4 v4 = *reinterpret_cast<const float4*>(vel + off);
+    float4 m4 = *reinterpret_cast<const float4*>(m + off);
+    if (clip) {
+        v4.x = __fmul_rn(v4.x, sc); v4.y = __fmul_rn(v4.y, sc); v4.z = __fmul_rn(v4.z, sc); v4.w = __fmul_rn(v4.w, sc);
+        *reinterpret_cast<float4*>(vel + off) = v4;
+    }
+    m4.x = __fsub_rn(m4.x, v4.x); m4.y = __fsub_rn(m4.y, v4.y); m4.z = __fsub_rn(m4.z, v4.z); m4.w = __fsub_rn(m4.w, v4.w);
+    *reinterpret_cast<float4*>(m + off) = m4;
 }
 
 // ---------------------------------------------------------------------------
@@ -907,6 +1181,13 @@ __global__ void k_debug_noise(uint32_t* __restrict__ words, float* __restrict__ 
     }
 }
 
+// rows [R][Dp]: value on the live dims, 0 on the padding
+__global__ void k_fill_rows(float* __restrict__ p, float value, int64_t D, int64_t Dp, int64_t total)
+{
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = (i % Dp) < D ? value : 0.0f;
+}
+
 int grid_for(int64_t n, int threads)
 {
     const int64_t g = (n + threads - 1) / threads;
@@ -951,6 +1232,13 @@ hipError_t launch_init(const Geometry& g, const es_config& c, float* m, float* m
     return hipGetLastError();
 }
 
+hipError_t launch_fill_rows(const Geometry& g, float* p, float value, hipStream_t s)
+{
+    const int64_t total = g.Dp * (int64_t)g.R;
+    k_fill_rows<<<grid_for(total, 256), 256, 0, s>>>(p, value, g.D, g.Dp, total);
+    return hipGetLastError();
+}
+
 hipError_t launch_problem_data(const Geometry& g, const es_config& c, float* pdata, hipStream_t s)
 {
     k_problem_data<<<grid_for(g.nb, 256), 256, 0, s>>>(pdata, c.seed, g.D, g.nb, c.problem);
@@ -958,24 +1246,30 @@ hipError_t launch_problem_data(const Geometry& g, const es_config& c, float* pda
 }
 
 hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const float* m, float* x,
-                      const float* hp, hipStream_t s)
+                      const float* hp, const float* svec, hipStream_t s)
 {
     k_ask<<<grid_for((int64_t)g.R * g.P * g.nb, 256), 256, 0, s>>>(m, x, c.seed, t, g.D, g.nb, g.N, g.P,
-                                                                   g.R, hp);
+                                                                   g.R, hp, svec);
     return hipGetLastError();
 }
 
 hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t,
                             const float* m, const float* pdata, float* partial, float* fit,
-                            const float* hp, double div, hipStream_t s)
+                            const float* hp, const float* svec, double div, hipStream_t s)
 {
     // chunk ids are dealt so that the pair groups of one chunk share an XCD
     const int64_t slots = (e.nchunks + 7) / 8 * e.n_pg;
     const dim3 grid((unsigned)(slots * 8), (unsigned)g.R);
     const dim3 block((unsigned)e.wg);
 #define ES_EVAL_LAUNCH(PROB)                                                                                   \
-    k_eval_bbob<PROB><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N, g.P, e.bc, e.nchunks, \
-                                             e.n_pg, hp, c.rastrigin_a)
+    do {                                                                                                       \
+        if (svec)                                                                                              \
+            k_eval_bbob<PROB, true><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N, g.P,   \
+                                                           e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, svec);  \
+        else                                                                                                   \
+            k_eval_bbob<PROB, false><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N, g.P,  \
+                                                            e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, nullptr); \
+    } while (0)
     switch (c.problem) {
     case ES_PROB_SPHERE: ES_EVAL_LAUNCH(ES_PROB_SPHERE); break;
     case ES_PROB_SHIFTED_SPHERE: ES_EVAL_LAUNCH(ES_PROB_SHIFTED_SPHERE); break;
@@ -993,9 +1287,9 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
 }
 
 hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* pen,
-                       const float* table, float* y, int32_t* rank, float* wfold, uint32_t* best_okey,
-                       float* best_f, int32_t* best_j, float* gen_best, const float* hp_cur, float* hp_next,
-                       hipStream_t s)
+                       const float* table, double ybar_table, float* y, int32_t* rank, float* wfold, float* bfold,
+                       uint32_t* best_okey, float* best_f, int32_t* best_j, float* gen_best, const float* hp_cur,
+                       float* hp_next, hipStream_t s)
 {
     const dim3 grid((unsigned)((g.P + RANK_PAIRS - 1) / RANK_PAIRS), (unsigned)g.R);
     const size_t lds = sizeof(uint32_t) * (size_t)g.N;
@@ -1008,26 +1302,54 @@ hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, 
     sa.sigma_final = c.sigma_final;
     sa.lr_decay = c.lr_decay;
     sa.lr_final = c.lr_final;
-    sa.shaping = c.shaping;
+    // SNES shapes by its utility table (host-made, indexed by rank)
+    sa.shaping = c.strategy == ES_STRAT_SNES ? ES_SHAPE_CENTERED_RANK : c.shaping;
     sa.maximize = c.maximize;
+    sa.bmode = c.strategy == ES_STRAT_PGPE ? 1 : c.strategy == ES_STRAT_SNES ? 2 : 0;
+    sa.bfold = bfold;
+    sa.ybar_table = ybar_table;
     k_rank<<<grid, RANK_PAIRS * RANK_SLICES, lds, s>>>(fit, table, y, rank, wfold, best_okey, best_f, best_j,
                                                        gen_best, g.N, g.P, g.R, sa);
     return hipGetLastError();
 }
 
-hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp, uint32_t t, const AdamConsts& a,
-                       const float* wfold, const int32_t* best_j, float* m, float* m1, float* v, float* grad,
-                       float* best_x, double* part, const float* hp, hipStream_t s)
+hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp, uint32_t t, const AdamConsts& ac,
+                       const TellBuffers& tb, hipStream_t s)
 {
-    const dim3 grid((unsigned)((g.nb + TELL_LANES - 1) / TELL_LANES), (unsigned)g.R, (unsigned)tp.nsplit);
-    k_tell<<<grid, TELL_LANES * tp.ps, 0, s>>>(wfold, best_j, m, m1, v, grad, best_x, c.seed, t, g.D, g.nb, g.P,
-                                               tp.ps, tp.nsplit, part, hp, g.R, a);
+    TellArgs a;
+    a.wfold = tb.wfold; a.bfold = tb.bfold; a.best_j = tb.best_j;
+    a.m = tb.m; a.m1 = tb.m1; a.v = tb.v; a.grad = tb.grad; a.best_x = tb.best_x;
+    a.sig = tb.sig; a.gbuf = tb.gbuf; a.gpart = tb.gpart; a.part = tb.part; a.hp = tb.hp;
+    a.seed = c.seed; a.t = t; a.D = g.D; a.nb = g.nb; a.P = g.P; a.R = g.R; a.ps = tp.ps; a.nsplit = tp.nsplit;
+    a.strategy = c.strategy; a.optimizer = c.optimizer;
+    a.sigma_lr = c.sigma_lr; a.max_change = c.sigma_max_change;
+    a.sigma_decay = c.sigma_decay; a.sigma_final = c.sigma_final;
+    a.ac = ac;
+    const bool two = c.strategy != ES_STRAT_OPENAI_ES;
+    const bool clipup = c.strategy != ES_STRAT_SNES && c.optimizer == ES_OPT_CLIPUP;
+    if (!clipup) a.gpart = nullptr;
+    const int64_t groups = (g.nb + TELL_LANES - 1) / TELL_LANES;
+    const dim3 grid((unsigned)groups, (unsigned)g.R, (unsigned)tp.nsplit);
+    if (two) k_tell<true><<<grid, TELL_LANES * tp.ps, 0, s>>>(a);
+    else k_tell<false><<<grid, TELL_LANES * tp.ps, 0, s>>>(a);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || tp.nsplit == 1) return e;
+    if (e != hipSuccess) return e;
     const dim3 fgrid((unsigned)((g.nb + 255) / 256), (unsigned)g.R);
-    k_tell_fold<<<fgrid, 256, 0, s>>>(part, best_j, m, m1, v, grad, best_x, c.seed, t, g.D, g.nb, g.P, tp.nsplit,
-                                      hp, g.R, a);
-    return hipGetLastError();
+    if (tp.nsplit > 1) {
+        if (two) k_tell_fold<true><<<fgrid, 256, 0, s>>>(a);
+        else k_tell_fold<false><<<fgrid, 256, 0, s>>>(a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (clipup) {
+        k_clipup_velocity<<<fgrid, 256, 0, s>>>(tb.gbuf, tb.vel, tb.gpart, tb.vpart, tb.hp, g.R, g.nb, groups,
+                                                 c.clipup_momentum);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        k_clipup_apply<<<fgrid, 256, 0, s>>>(tb.vel, tb.m, tb.vpart, g.nb, groups, c.clipup_max_speed);
+        e = hipGetLastError();
+    }
+    return e;
 }
 
 TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit)
@@ -1047,10 +1369,13 @@ TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit)
     return tp;
 }
 
-size_t tell_part_elems(const Geometry& g, const TellPlan& tp)
+size_t tell_part_elems(const Geometry& g, const TellPlan& tp, int strategy)
 {
-    return tp.nsplit > 1 ? (size_t)g.R * tp.nsplit * g.nb * 4 : 0;
+    const size_t w = strategy == ES_STRAT_OPENAI_ES ? 4 : 8;
+    return tp.nsplit > 1 ? (size_t)g.R * tp.nsplit * g.nb * w : 0;
 }
+
+size_t tell_groups(const Geometry& g) { return (size_t)((g.nb + TELL_LANES - 1) / TELL_LANES); }
 
 int32_t tell_slices(const Geometry& g)
 {
@@ -1076,6 +1401,8 @@ size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e)
 bool fused_supported(const Geometry& g, const EvalPlan& e, const es_config& c)
 {
     if (c.problem < ES_PROB_SPHERE || c.problem > ES_PROB_RASTRIGIN) return false;
+    // the fused loop runs OpenAI-ES with Adam
+    if (c.strategy != ES_STRAT_OPENAI_ES || c.optimizer != ES_OPT_ADAM) return false;
     // the fused loop shapes by centered ranks or raw keys, without weight decay
     if (c.shaping == ES_SHAPE_Z_SCORE || c.w_decay != 0.0f) return false;
     return fused_lds_bytes(g, e) <= FUSED_MAX_LDS;

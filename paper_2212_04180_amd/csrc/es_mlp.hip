@@ -107,19 +107,27 @@ __device__ __forceinline__ bf16x8 activate(const floatx4& lo, const floatx4& hi,
 }
 
 // One Philox block (4 weights) of W2 chunk `chunk` into the chunk buffers.
-__device__ __forceinline__ void gen_w2_block(const float* __restrict__ mr, uint32_t k0, uint32_t k1, uint32_t pair,
-                                             uint32_t t, int chunk, int i, float sigma, __bf16* wp, __bf16* wm)
+// VEC: per-dimension sigma from sr (PGPE, SNES).
+template <bool VEC>
+__device__ __forceinline__ void gen_w2_block(const float* __restrict__ mr, const float* __restrict__ sr, uint32_t k0,
+                                             uint32_t k1, uint32_t pair, uint32_t t, int chunk, int i, float sigma,
+                                             __bf16* wp, __bf16* wm)
 {
     const int64_t b = (OFF_W2 + (int64_t)chunk * W2_ROWS * MLP_H) / 4 + i;
     float e[4];
     box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)b, pair, t, DOM_NOISE), e);
     const float4 m4 = *reinterpret_cast<const float4*>(mr + 4 * b);
     const float mv[4] = {m4.x, m4.y, m4.z, m4.w};
+    float sv[4] = {sigma, sigma, sigma, sigma};
+    if constexpr (VEC) {
+        const float4 s4 = *reinterpret_cast<const float4*>(sr + 4 * b);
+        sv[0] = s4.x; sv[1] = s4.y; sv[2] = s4.z; sv[3] = s4.w;
+    }
     bf16x4 vp, vm;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-        vp[k] = (__bf16)fmaf(sigma, e[k], mv[k]);
-        vm[k] = (__bf16)fmaf(-sigma, e[k], mv[k]);
+        vp[k] = (__bf16)fmaf(sv[k], e[k], mv[k]);
+        vm[k] = (__bf16)fmaf(-sv[k], e[k], mv[k]);
     }
     const int row = (4 * i) / MLP_H, col = (4 * i) % MLP_H;
     *reinterpret_cast<bf16x4*>(wp + row * W2S + col) = vp;
@@ -166,10 +174,12 @@ __device__ __forceinline__ void layer2_act(const MlpSmem& S, const floatx4 (&acc
 
 // One workgroup per antithetic pair: waves 0-7 evaluate member p (+eps),
 // waves 8-15 member p + N/2 (-eps); each wave owns 32 batch columns.
+template <bool VEC>
 __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restrict__ m, const __bf16* __restrict__ xb,
                                                           const float* __restrict__ yt, float* __restrict__ fit,
                                                           uint64_t seed, uint32_t t, int64_t Dp, int32_t N,
-                                                          int32_t P, const float* __restrict__ hp, int32_t tanh_out)
+                                                          int32_t P, const float* __restrict__ hp, int32_t tanh_out,
+                                                          const float* __restrict__ svec)
 {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     MlpSmem& S = *reinterpret_cast<MlpSmem*>(smem_raw);
@@ -180,6 +190,7 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
     const uint64_t key = seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
     const float* __restrict__ mr = m + (int64_t)r * Dp;
+    const float* __restrict__ sr = VEC ? svec + (int64_t)r * Dp : nullptr;
     const float sigma = hp[r];
 
     // ---- layer 1 and layer 3 weights, W2 chunk 0, all biases.  Each thread
@@ -195,9 +206,13 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
         const int64_t blk[7] = {OFF_W1 / 4 + tid, OFF_W1 / 4 + tid + MLP_THREADS, OFF_W1 / 4 + tid + 2 * MLP_THREADS,
                                 OFF_W1 / 4 + tid + 3 * MLP_THREADS, OFF_W3 / 4 + tid, OFF_W2 / 4 + tid,
                                 OFF_W2 / 4 + tid + MLP_THREADS};
-        float4 mw[7];
+        float4 mw[7], sw[VEC ? 7 : 1];
 #pragma unroll
         for (int k = 0; k < 7; ++k) mw[k] = *reinterpret_cast<const float4*>(mr + 4 * blk[k]);
+        if constexpr (VEC) {
+#pragma unroll
+            for (int k = 0; k < 7; ++k) sw[k] = *reinterpret_cast<const float4*>(sr + 4 * blk[k]);
+        }
         const int jb = tid - (MLP_THREADS - NBIAS);  // bias block of this thread, if >= 0
         const int64_t bblk = jb < MLP_H / 4 ? OFF_B1 / 4 + jb : jb < MLP_H / 2 ? OFF_B2 / 4 + (jb - MLP_H / 4)
                                                                                 : OFF_B3 / 4 + (jb - MLP_H / 2);
@@ -208,11 +223,15 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
             float e[4];
             box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)blk[k], (uint32_t)p, t, DOM_NOISE), e);
             const float mv[4] = {mw[k].x, mw[k].y, mw[k].z, mw[k].w};
+            float sv[4] = {sigma, sigma, sigma, sigma};
+            if constexpr (VEC) {
+                sv[0] = sw[k].x; sv[1] = sw[k].y; sv[2] = sw[k].z; sv[3] = sw[k].w;
+            }
             bf16x4 vp, vm;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                vp[i] = (__bf16)fmaf(sigma, e[i], mv[i]);
-                vm[i] = (__bf16)fmaf(-sigma, e[i], mv[i]);
+                vp[i] = (__bf16)fmaf(sv[i], e[i], mv[i]);
+                vm[i] = (__bf16)fmaf(-sv[i], e[i], mv[i]);
             }
             __bf16 *dp, *dm;
             if (k < 4) {  // W1 [256][64]
@@ -235,6 +254,11 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
             float e[4];
             box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)bblk, (uint32_t)p, t, DOM_NOISE), e);
             const float mv[4] = {mb.x, mb.y, mb.z, mb.w};
+            float sv[4] = {sigma, sigma, sigma, sigma};
+            if constexpr (VEC) {
+                const float4 s4 = *reinterpret_cast<const float4*>(sr + 4 * bblk);
+                sv[0] = s4.x; sv[1] = s4.y; sv[2] = s4.z; sv[3] = s4.w;
+            }
             float *bp, *bm;
             if (jb < MLP_H / 4) {
                 bp = S.b1[0] + 4 * jb; bm = S.b1[1] + 4 * jb;
@@ -246,8 +270,8 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
             const float sc = jb < MLP_H / 2 ? TWO_LOG2E : 1.0f;  // hidden-layer biases pre-scaled
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                bp[i] = fmaf(sigma, e[i], mv[i]) * sc;
-                bm[i] = fmaf(-sigma, e[i], mv[i]) * sc;
+                bp[i] = fmaf(sv[i], e[i], mv[i]) * sc;
+                bm[i] = fmaf(-sv[i], e[i], mv[i]) * sc;
             }
         }
     }
@@ -305,7 +329,8 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
         const bool gen = c + 1 < W2_CHUNKS;
         if (mem == 0 && gen)
             for (int j = 0; j < W2_BLOCKS_PER_THREAD; ++j)
-                gen_w2_block(mr, k0, k1, (uint32_t)p, t, c + 1, (int)threadIdx.x + j * MLP_THREADS, sigma, nb_p, nb_m);
+                gen_w2_block<VEC>(mr, sr, k0, k1, (uint32_t)p, t, c + 1, (int)threadIdx.x + j * MLP_THREADS, sigma, nb_p,
+                                  nb_m);
         {
             floatx4 acc[2][2];
             layer2_mfma(wc, h1, acc, q, l16);
@@ -313,7 +338,8 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
         }
         if (mem == 1 && gen)
             for (int j = 0; j < W2_BLOCKS_PER_THREAD; ++j)
-                gen_w2_block(mr, k0, k1, (uint32_t)p, t, c + 1, (int)threadIdx.x + j * MLP_THREADS, sigma, nb_p, nb_m);
+                gen_w2_block<VEC>(mr, sr, k0, k1, (uint32_t)p, t, c + 1, (int)threadIdx.x + j * MLP_THREADS, sigma, nb_p,
+                                  nb_m);
         __syncthreads();
     }
 
@@ -453,7 +479,7 @@ hipError_t launch_mlp_setup(const float* teacher, void* scratch, hipStream_t s)
 size_t mlp_lds_bytes() { return sizeof(MlpSmem); }
 
 hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, const float* m, const float* teacher,
-                           void* scratch, float* fit, const float* hp, hipStream_t s)
+                           void* scratch, float* fit, const float* hp, const float* svec, hipStream_t s)
 {
     float* xf = static_cast<float*>(scratch);
     __bf16* xb = reinterpret_cast<__bf16*>(xf + MLP_BATCH * MLP_IN);
@@ -463,15 +489,18 @@ hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, co
     k_mlp_teacher<<<MLP_BATCH, TEACHER_THREADS, 0, s>>>(teacher, wt, xf, xb, yt, c.seed, t, c.mlp_tanh_out);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    static bool lds_attr_set = false;  // more than 64 KB of LDS per workgroup
-    if (!lds_attr_set) {
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_eval_mlp),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(MlpSmem));
-        if (e != hipSuccess) return e;
-        lds_attr_set = true;
-    }
-    k_eval_mlp<<<dim3((unsigned)g.P, (unsigned)g.R), MLP_THREADS, sizeof(MlpSmem), s>>>(
-        m, xb, yt, fit, c.seed, t, g.Dp, g.N, g.P, hp, c.mlp_tanh_out);
+    // more than 64 KB of LDS per workgroup: allowed per kernel (cheap to repeat)
+    const void* kern = svec ? reinterpret_cast<const void*>(&k_eval_mlp<true>)
+                            : reinterpret_cast<const void*>(&k_eval_mlp<false>);
+    e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(MlpSmem));
+    if (e != hipSuccess) return e;
+    const dim3 grid((unsigned)g.P, (unsigned)g.R);
+    if (svec)
+        k_eval_mlp<true><<<grid, MLP_THREADS, sizeof(MlpSmem), s>>>(m, xb, yt, fit, c.seed, t, g.Dp, g.N, g.P, hp,
+                                                                     c.mlp_tanh_out, svec);
+    else
+        k_eval_mlp<false><<<grid, MLP_THREADS, sizeof(MlpSmem), s>>>(m, xb, yt, fit, c.seed, t, g.Dp, g.N, g.P, hp,
+                                                                      c.mlp_tanh_out, nullptr);
     return hipGetLastError();
 }
 

@@ -22,10 +22,13 @@ SHAPE_CENTERED_RANK, SHAPE_RAW, SHAPE_Z_SCORE = 0, 1, 2
 PROB_NONE, PROB_SPHERE, PROB_SHIFTED_SPHERE, PROB_ROSENBROCK, PROB_RASTRIGIN, PROB_MLP = range(6)
 INIT_UNIFORM, INIT_ZERO, INIT_FANIN_NORMAL = range(3)
 FLAG_KEEP_GRAD = 1
+STRAT_OPENAI_ES, STRAT_PGPE, STRAT_SNES = range(3)
+OPT_ADAM, OPT_CLIPUP = range(2)
 
 # Every symbol include/esmi.h declares, in declaration order.
 EXPORTS = ("es_init", "es_ask", "es_eval", "es_tell", "es_run", "es_get_state", "es_set_state",
-           "es_get_best", "es_get_shaped", "es_get_grad", "es_set_hparams", "es_get_hparams", "es_get_penalty",
+           "es_get_best", "es_get_shaped", "es_get_grad", "es_set_hparams", "es_get_hparams",
+           "es_get_strategy_state", "es_set_strategy_state", "es_get_penalty",
            "es_get_problem_data", "es_debug_noise",
            "es_save_state", "es_load_state", "es_sync", "es_generation", "es_last_error",
            "es_status_string", "es_destroy")
@@ -64,7 +67,13 @@ class _Config(ctypes.Structure):
         ("lr_decay", ctypes.c_float),
         ("lr_final", ctypes.c_float),
         ("w_decay", ctypes.c_float),
-        ("reserved", ctypes.c_uint32),
+        ("strategy", ctypes.c_int32),
+        ("optimizer", ctypes.c_int32),
+        ("sigma_lr", ctypes.c_float),
+        ("sigma_max_change", ctypes.c_float),
+        ("clipup_max_speed", ctypes.c_float),
+        ("clipup_momentum", ctypes.c_float),
+        ("snes_temperature", ctypes.c_float),
     ]
 
 
@@ -97,7 +106,14 @@ class ESConfig:
     lr_decay: float = 1.0
     lr_final: float = 0.0
     w_decay: float = 0.0  # weight-decay fitness regularisation (Sec. 3.2)
-    reserved: int = 0
+    # Table 1 strategy and the mean's optimiser; App. B PGPE / SNES defaults
+    strategy: int = STRAT_OPENAI_ES
+    optimizer: int = OPT_ADAM
+    sigma_lr: float = 0.2
+    sigma_max_change: float = 0.2
+    clipup_max_speed: float = 0.3
+    clipup_momentum: float = 0.9
+    snes_temperature: float = 12.0
 
     def cstruct(self) -> _Config:
         c = _Config()
@@ -134,6 +150,8 @@ def lib() -> ctypes.CDLL:
         "es_set_hparams": (i32, [vp, vp, vp]),
         "es_get_hparams": (i32, [vp, vp, vp]),
         "es_get_penalty": (i32, [vp, vp]),
+        "es_get_strategy_state": (i32, [vp, vp, vp]),
+        "es_set_strategy_state": (i32, [vp, vp, vp]),
         "es_get_problem_data": (i32, [vp, vp]),
         "es_debug_noise": (i32, [vp, i32, i64, i32, vp, vp]),
         "es_save_state": (i32, [vp, vp, P(ctypes.c_size_t)]),
@@ -272,6 +290,16 @@ class ES:
         sg, lr = np.zeros(self.R, np.float32), np.zeros(self.R, np.float32)
         self._check(lib().es_get_hparams(self._h, ctypes.c_void_p(sg.ctypes.data), ctypes.c_void_p(lr.ctypes.data)))
         return sg, lr
+
+    def strategy_state(self, sigma=True, velocity=False):
+        """Per-dimension sigma (PGPE, SNES) and/or ClipUp velocity, [R][D] each."""
+        sg = self._empty(self.R, self.D) if sigma else None
+        ve = self._empty(self.R, self.D) if velocity else None
+        self._check(lib().es_get_strategy_state(self._h, _ptr(sg), _ptr(ve)))
+        return sg, ve
+
+    def set_strategy_state(self, sigma=None, velocity=None):
+        self._check(lib().es_set_strategy_state(self._h, _ptr(sigma), _ptr(velocity)))
 
     def penalty(self):
         out = self._empty(self.R, self.N)

@@ -41,6 +41,10 @@ EVAL_SLOTS_PER_PAIR_BLOCK = {"sphere": PHILOX_BM + 24, "shifted_sphere": PHILOX_
                              "rosenbrock": PHILOX_BM + 64, "rastrigin": PHILOX_BM + 88}
 # tell: Philox + Box-Muller + 4 fma (w * eps) + the fp64 fold every 16 pairs
 TELL_SLOTS_PER_PAIR_BLOCK = PHILOX_BM + 4 + 1
+# per-dimension sigma (PGPE, SNES): evaluate moves each dim's sigma into a
+# VGPR (4 movs per block); tell adds the second sum, 4 fma (z*z - 1) + 4 fma
+EVAL_VEC_EXTRA = 4
+TELL_TWO_EXTRA = 8
 
 
 def kernel_source_sha256():
@@ -101,7 +105,12 @@ def cpu_baseline(cfg, sample_dims):
                         lr=cfg.lr, beta1=cfg.beta1, beta2=cfg.beta2, eps=cfg.eps, maximize=cfg.maximize,
                         shaping=cfg.shaping, seed=cfg.seed, init=cfg.init, init_lo=cfg.init_lo,
                         init_hi=cfg.init_hi, problem=cfg.problem, rastrigin_a=cfg.rastrigin_a,
-                        mlp_batch=cfg.mlp_batch, mlp_bf16=cfg.mlp_bf16, mlp_tanh_out=cfg.mlp_tanh_out)
+                        mlp_batch=cfg.mlp_batch, mlp_bf16=cfg.mlp_bf16, mlp_tanh_out=cfg.mlp_tanh_out,
+                        sigma_decay=cfg.sigma_decay, sigma_final=cfg.sigma_final, lr_decay=cfg.lr_decay,
+                        lr_final=cfg.lr_final, w_decay=cfg.w_decay, strategy=cfg.strategy,
+                        optimizer=cfg.optimizer, sigma_lr=cfg.sigma_lr, sigma_max_change=cfg.sigma_max_change,
+                        clipup_max_speed=cfg.clipup_max_speed, clipup_momentum=cfg.clipup_momentum,
+                        snes_temperature=cfg.snes_temperature)
     es = O.OracleES(oc)
     t0 = time.perf_counter()
     es.step()
@@ -179,16 +188,19 @@ def main():
     roof = None
     if prob is not None and args.path == "percall":
         pair_blocks = R * (N // 2) * ((D + 3) // 4)
-        achieved = pair_blocks * EVAL_SLOTS_PER_PAIR_BLOCK[prob] / (eval_ms * 1e-3)
-        tell_achieved = pair_blocks * TELL_SLOTS_PER_PAIR_BLOCK / (tell_ms * 1e-3)
+        vec = cfg.strategy != P.STRAT_OPENAI_ES
+        eval_slots = EVAL_SLOTS_PER_PAIR_BLOCK[prob] + (EVAL_VEC_EXTRA if vec else 0)
+        tell_slots = TELL_SLOTS_PER_PAIR_BLOCK + (TELL_TWO_EXTRA if vec else 0)
+        achieved = pair_blocks * eval_slots / (eval_ms * 1e-3)
+        tell_achieved = pair_blocks * tell_slots / (tell_ms * 1e-3)
         roof = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                 "unit": "T VALU lane-op slots/s", "frac": achieved / VALU_PEAK,
                 "traffic": profiled_traffic(args.workload),
                 "kernel": "k_eval_bbob (fused sample+evaluate; timed with its k_eval_reduce)",
-                "kernel_ms": eval_ms, "slots_per_pair_block": EVAL_SLOTS_PER_PAIR_BLOCK[prob],
+                "kernel_ms": eval_ms, "slots_per_pair_block": eval_slots,
                 "pair_blocks_per_launch": pair_blocks,
                 "tell": {"kernel": "k_rank + k_tell", "kernel_ms": tell_ms, "achieved": tell_achieved / 1e12,
-                         "frac": tell_achieved / VALU_PEAK, "slots_per_pair_block": TELL_SLOTS_PER_PAIR_BLOCK}}
+                         "frac": tell_achieved / VALU_PEAK, "slots_per_pair_block": tell_slots}}
     if cfg.problem == P.PROB_MLP and args.path == "percall":
         flops = R * N * MLP_FLOPS_PER_MEMBER
         achieved = flops / (eval_ms * 1e-3)
@@ -227,6 +239,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "path": args.path, "num_runs": R, "popsize": N, "num_dims": D,
                    "problem": prob or "mlp", "sigma": cfg.sigma, "lr": cfg.lr,
+                   "strategy": {0: "openai_es", 1: "pgpe", 2: "snes"}[cfg.strategy],
+                   "optimizer": "clipup" if cfg.optimizer == P.OPT_CLIPUP and cfg.strategy != P.STRAT_SNES else
+                   ("adam" if cfg.strategy != P.STRAT_SNES else "snes natural gradient"),
                    "generations_per_s": 1e3 / ms, "eval_ms": eval_ms, "tell_ms": tell_ms},
         "roofline": roof,
         "hbm_equivalent": hbm_equiv,

@@ -332,3 +332,57 @@ class BruteFamily:
                     self.sig[d] = f32(_q(self.sig[d]) + _q(dlt))
         self.t += 1
         return {"X": X, "fitness": f, "g": g, "A": A, "B": B}
+
+
+class BruteSepCMA:
+    """R=1 Sep-CMA-ES generation (Ros & Hansen 2008) with independent members
+    (row = member index): exact rational recombination sums, fp64 updates, one
+    fp32 rounding per stored value.  Settings as the oracle's readings."""
+
+    def __init__(self, problem, D, N, sigma, seed, lo, hi, elite_ratio=0.5):
+        self.problem, self.D, self.N, self.seed = problem, D, N, seed
+        self.mu = max(1, int(math.floor(elite_ratio * N)))
+        wr = [math.log(self.mu + 0.5) - math.log(i + 1) for i in range(self.mu)]
+        sw = math.fsum(wr)
+        self.w = [v / sw for v in wr]
+        self.sigma = f32(sigma)
+        self.m = init_uniform(seed, D, lo, hi)
+        self.C, self.ps, self.pc = [1.0] * D, [0.0] * D, [0.0] * D
+        self.t = 0
+
+    def generation(self):
+        D, N, mu, w = self.D, self.N, self.mu, self.w
+        mu_eff = 1.0 / math.fsum(v * v for v in w)
+        c_s = (mu_eff + 2.0) / (D + mu_eff + 5.0)
+        d_s = 1.0 + 2.0 * max(0.0, math.sqrt((mu_eff - 1.0) / (D + 1.0)) - 1.0) + c_s
+        c_c = (4.0 + mu_eff / D) / (D + 4.0 + 2.0 * mu_eff / D)
+        c1 = 2.0 / ((D + 1.3) ** 2 + mu_eff)
+        cmu = min(1.0 - c1, 2.0 * (mu_eff - 2.0 + 1.0 / mu_eff) / ((D + 2.0) ** 2 + mu_eff))
+        c1 = min(1.0, c1 * (D + 2.0) / 3.0)
+        cmu = min(1.0 - c1, cmu * (D + 2.0) / 3.0)
+        chi = math.sqrt(D) * (1.0 - 1.0 / (4.0 * D) + 1.0 / (21.0 * D * D))
+        s = [f32(_q(self.sigma) * _q(f32(math.sqrt(self.C[d])))) for d in range(D)]
+        Z = [eps_vector(self.seed, 0, j, self.t, D) for j in range(N)]
+        X = [[fma32(s[d], Z[j][d], self.m[d]) for d in range(D)] for j in range(N)]
+        f = [fitness(self.problem, x) for x in X]
+        rk = ranks(f)
+        elite = [0] * mu
+        for j in range(N):
+            if rk[j] < mu:
+                elite[rk[j]] = j
+        zw = [float(sum(_q(w[i]) * _q(Z[elite[i]][d]) for i in range(mu))) for d in range(D)]
+        q = [float(sum(_q(w[i]) * _q(Z[elite[i]][d]) ** 2 for i in range(mu))) for d in range(D)]
+        a_s = math.sqrt(c_s * (2.0 - c_s) * mu_eff)
+        self.m = [f32(self.m[d] + s[d] * zw[d]) for d in range(D)]
+        self.ps = [f32((1.0 - c_s) * self.ps[d] + a_s * zw[d]) for d in range(D)]
+        nps = math.sqrt(math.fsum(v * v for v in self.ps))
+        h = 1.0 if nps / math.sqrt(1.0 - (1.0 - c_s) ** (2.0 * (self.t + 1))) < (1.4 + 2.0 / (D + 1.0)) * chi else 0.0
+        a_c = math.sqrt(c_c * (2.0 - c_c) * mu_eff)
+        for d in range(D):
+            Cd = self.C[d]
+            self.pc[d] = f32((1.0 - c_c) * self.pc[d] + h * a_c * math.sqrt(Cd) * zw[d])
+            self.C[d] = f32((1.0 - c1 - cmu) * Cd + c1 * (self.pc[d] ** 2 + (1.0 - h) * c_c * (2.0 - c_c) * Cd)
+                            + cmu * Cd * q[d])
+        self.sigma = f32(self.sigma * math.exp((c_s / d_s) * (nps / chi - 1.0)))
+        self.t += 1
+        return {"X": X, "fitness": f, "elite": elite, "h": h}

@@ -117,7 +117,7 @@ enum { OR_PROB_NONE = 0, OR_PROB_SPHERE = 1, OR_PROB_SHIFTED_SPHERE = 2,
        OR_PROB_ROSENBROCK = 3, OR_PROB_RASTRIGIN = 4, OR_PROB_MLP = 5 };
 enum { OR_INIT_UNIFORM = 0, OR_INIT_ZERO = 1, OR_INIT_FANIN_NORMAL = 2 };
 enum { OR_SHAPE_CENTERED_RANK = 0, OR_SHAPE_RAW = 1, OR_SHAPE_Z_SCORE = 2 };
-enum { OR_STRAT_OPENAI_ES = 0, OR_STRAT_PGPE = 1, OR_STRAT_SNES = 2 };
+enum { OR_STRAT_OPENAI_ES = 0, OR_STRAT_PGPE = 1, OR_STRAT_SNES = 2, OR_STRAT_SEP_CMA = 3 };
 enum { OR_OPT_ADAM = 0, OR_OPT_CLIPUP = 1 };
 
 typedef struct {
@@ -149,7 +149,9 @@ typedef struct {
     float clipup_max_speed;  /* ClipUp: bound of the velocity norm            */
     float clipup_momentum;   /* ClipUp: velocity decay                        */
     float snes_temperature;  /* SNES: beta of the softmax rank utilities      */
-    const float* sigma_vec;  /* per-dimension sigma of this run (PGPE, SNES)  */
+    const float* sigma_vec;  /* per-dimension sigma of this run (PGPE, SNES);   */
+                             /* Sep-CMA-ES: the sampling scale sigma*sqrt(C)  */
+    float elite_ratio;       /* Sep-CMA-ES: mu = max(1, floor(ratio * N))     */
 } or_config;
 
 /* MLP 64-256-256-16 layer table, flattened [out][in] row-major weights, then
@@ -238,9 +240,16 @@ void or_problem_data(const or_config* c, float* out)
 void or_member(const or_config* c, int32_t run, uint32_t t, const float* m, int32_t j, float* x)
 {
     int32_t half = c->popsize / 2;
-    int32_t p = j < half ? j : j - half;
     int64_t D = c->num_dims;
     float* eps = (float*)malloc(sizeof(float) * (size_t)D);
+    if (c->strategy == OR_STRAT_SEP_CMA) {
+        /* independent samples, row = member: x = m + s (.) z_j */
+        or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)j, t, 0, D, eps);
+        for (int64_t d = 0; d < D; ++d) x[d] = fmaf(c->sigma_vec[d], eps[d], m[d]);
+        free(eps);
+        return;
+    }
+    int32_t p = j < half ? j : j - half;
     or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)p, t, 0, D, eps);
     for (int64_t d = 0; d < D; ++d) {
         /* PGPE / SNES: a diagonal Gaussian, per-dimension sigma */
@@ -724,8 +733,132 @@ void or_snes_update(const or_config* c, int32_t run, int64_t t, float lr, const 
     free(rank); free(tab); free(w); free(a); free(b); free(A); free(B);
 }
 
+/* ------------------------------------------------------------------------ */
+/* Sep-CMA-ES (Ros & Hansen 2008; EOD row of Table 1, App. B table: sigma    */
+/* init and elite ratio).  Readings (the paper gives no formula; these are   */
+/* the standard CMA-ES settings of Hansen's tutorial with the separable      */
+/* learning-rate scaling (D+2)/3 of Ros & Hansen):                           */
+/*   mu = max(1, floor(ratio N)); w_i = (ln(mu + 1/2) - ln(i+1)) / sum,      */
+/*   i = 0..mu-1 by rank; mu_eff = 1/sum w^2;                                */
+/*   c_s = (mu_eff + 2)/(D + mu_eff + 5);                                    */
+/*   d_s = 1 + 2 max(0, sqrt((mu_eff-1)/(D+1)) - 1) + c_s;                   */
+/*   c_c = (4 + mu_eff/D)/(D + 4 + 2 mu_eff/D);                              */
+/*   c1 = 2/((D+1.3)^2 + mu_eff);                                            */
+/*   cmu = min(1 - c1, 2 (mu_eff - 2 + 1/mu_eff)/((D+2)^2 + mu_eff));        */
+/*   separable: c1s = min(1, c1 (D+2)/3), cmus = min(1 - c1s, cmu (D+2)/3);  */
+/*   chi = sqrt(D) (1 - 1/(4D) + 1/(21 D^2)).                                */
+/* Sampling: s_d = fl32(sigma sqrtf(C_d)), x_j = fmaf(s, z_j, m) with z_j    */
+/* the Philox normals of row j (independent members, no mirroring).          */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    int32_t mu;
+    double mu_eff, c_s, d_s, c_c, c1, cmu, chi;
+} or_cma_consts;
+
+int32_t or_cma_mu(const or_config* c)
+{
+    int32_t mu = (int32_t)floor((double)c->elite_ratio * (double)c->popsize);
+    return mu < 1 ? 1 : mu;
+}
+
+void or_cma_weights(const or_config* c, double* w)
+{
+    int32_t mu = or_cma_mu(c);
+    double s = 0.0;
+    for (int32_t i = 0; i < mu; ++i) {
+        w[i] = log((double)mu + 0.5) - log((double)(i + 1));
+        s += w[i];
+    }
+    for (int32_t i = 0; i < mu; ++i) w[i] /= s;
+}
+
+static or_cma_consts or_cma_setup(const or_config* c, const double* w)
+{
+    or_cma_consts k;
+    double D = (double)c->num_dims, s2 = 0.0;
+    k.mu = or_cma_mu(c);
+    for (int32_t i = 0; i < k.mu; ++i) s2 += w[i] * w[i];
+    k.mu_eff = 1.0 / s2;
+    k.c_s = (k.mu_eff + 2.0) / (D + k.mu_eff + 5.0);
+    double q = sqrt((k.mu_eff - 1.0) / (D + 1.0)) - 1.0;
+    k.d_s = 1.0 + 2.0 * (q > 0.0 ? q : 0.0) + k.c_s;
+    k.c_c = (4.0 + k.mu_eff / D) / (D + 4.0 + 2.0 * k.mu_eff / D);
+    double c1 = 2.0 / ((D + 1.3) * (D + 1.3) + k.mu_eff);
+    double cmu = 2.0 * (k.mu_eff - 2.0 + 1.0 / k.mu_eff) / ((D + 2.0) * (D + 2.0) + k.mu_eff);
+    if (cmu > 1.0 - c1) cmu = 1.0 - c1;
+    k.c1 = c1 * (D + 2.0) / 3.0;
+    if (k.c1 > 1.0) k.c1 = 1.0;
+    k.cmu = cmu * (D + 2.0) / 3.0;
+    if (k.cmu > 1.0 - k.c1) k.cmu = 1.0 - k.c1;
+    k.chi = sqrt(D) * (1.0 - 1.0 / (4.0 * D) + 1.0 / (21.0 * D * D));
+    return k;
+}
+
+void or_cma_scale(int64_t D, float sigma, const float* C, float* s)
+{
+    for (int64_t d = 0; d < D; ++d) s[d] = sigma * sqrtf(C[d]);
+}
+
+/* One Sep-CMA-ES tell.  Elites e_i = the member of rank i (shaped keys,
+ * weight decay included); zw_d = sum_i w_i z_{e_i,d}, q_d = sum_i w_i
+ * z_{e_i,d}^2 (fp64).  Then, in fp64 from the fp32 state, one rounding per
+ * stored value, with s the generation's sampling scale:
+ *   m_d   = m_d + s_d zw_d
+ *   ps_d  = (1 - c_s) ps_d + sqrt(c_s (2 - c_s) mu_eff) zw_d
+ *   h     = |ps| / sqrt(1 - (1 - c_s)^(2(t+1))) < (1.4 + 2/(D+1)) chi
+ *   pc_d  = (1 - c_c) pc_d + h sqrt(c_c (2 - c_c) mu_eff) sqrt(C_d) zw_d
+ *   C_d   = (1 - c1s - cmus) C_d + c1s (pc_d^2 + (1 - h) c_c (2 - c_c) C_d)
+ *           + cmus C_d q_d
+ *   sigma = sigma exp((c_s / d_s) (|ps| / chi - 1)).                       */
+void or_sepcma_update(const or_config* c, int32_t run, int64_t t, const float* f, const float* pen, float* m,
+                      float* sigma, float* C, float* ps, float* pc, const float* s, float* w_out)
+{
+    int32_t N = c->popsize;
+    int64_t D = c->num_dims;
+    double* w = (double*)malloc(sizeof(double) * (size_t)N);
+    or_cma_weights(c, w);
+    or_cma_consts k = or_cma_setup(c, w);
+    int32_t* rank = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
+    or_key_ranks(f, pen, N, c->maximize, c->w_decay, rank);
+    int32_t* elite = (int32_t*)malloc(sizeof(int32_t) * (size_t)k.mu);
+    for (int32_t j = 0; j < N; ++j)
+        if (rank[j] < k.mu) elite[rank[j]] = j;
+    double* zw = (double*)calloc((size_t)D, sizeof(double));
+    double* q = (double*)calloc((size_t)D, sizeof(double));
+    float* z = (float*)malloc(sizeof(float) * (size_t)D);
+    for (int32_t i = 0; i < k.mu; ++i) {
+        or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)elite[i], (uint32_t)t, 0, D, z);
+        for (int64_t d = 0; d < D; ++d) {
+            zw[d] += w[i] * (double)z[d];
+            q[d] += w[i] * (double)z[d] * (double)z[d];
+        }
+    }
+    double a_s = sqrt(k.c_s * (2.0 - k.c_s) * k.mu_eff), n2 = 0.0;
+    for (int64_t d = 0; d < D; ++d) {
+        m[d] = (float)((double)m[d] + (double)s[d] * zw[d]);
+        ps[d] = (float)((1.0 - k.c_s) * (double)ps[d] + a_s * zw[d]);
+        n2 += (double)ps[d] * (double)ps[d];
+    }
+    double nps = sqrt(n2);
+    double hth = nps / sqrt(1.0 - pow(1.0 - k.c_s, 2.0 * (double)(t + 1)));
+    double h = hth < (1.4 + 2.0 / ((double)D + 1.0)) * k.chi ? 1.0 : 0.0;
+    double a_c = sqrt(k.c_c * (2.0 - k.c_c) * k.mu_eff);
+    for (int64_t d = 0; d < D; ++d) {
+        double Cd = (double)C[d];
+        pc[d] = (float)((1.0 - k.c_c) * (double)pc[d] + h * a_c * sqrt(Cd) * zw[d]);
+        double pcd = (double)pc[d];
+        C[d] = (float)((1.0 - k.c1 - k.cmu) * Cd + k.c1 * (pcd * pcd + (1.0 - h) * k.c_c * (2.0 - k.c_c) * Cd)
+                       + k.cmu * Cd * q[d]);
+    }
+    *sigma = (float)((double)*sigma * exp((k.c_s / k.d_s) * (nps / k.chi - 1.0)));
+    if (w_out)
+        for (int32_t j = 0; j < N; ++j) w_out[j] = rank[j] < k.mu ? (float)w[rank[j]] : 0.0f;
+    free(w); free(rank); free(elite); free(zw); free(q); free(z);
+}
+
 void or_generation_ex(const or_config* c0, int32_t run, int64_t t, const float* pdata,
-                      float* m, float* m1, float* v, float* vel, float* sig, const float* fit_in,
+                      float* m, float* m1, float* v, float* vel, float* sig, float* sigma_out,
+                      const float* fit_in,
                       float* fit_out, float* y_out, float* g_out,
                       double* best_key, float* best_f, float* best_x);
 
@@ -743,21 +876,31 @@ void or_generation(const or_config* c, int32_t run, int64_t t, const float* pdat
                    float* fit_out, float* y_out, float* g_out,
                    double* best_key, float* best_f, float* best_x)
 {
-    or_generation_ex(c, run, t, pdata, m, m1, v, NULL, NULL, fit_in, fit_out, y_out, g_out, best_key, best_f,
-                     best_x);
+    or_generation_ex(c, run, t, pdata, m, m1, v, NULL, NULL, NULL, fit_in, fit_out, y_out, g_out, best_key,
+                     best_f, best_x);
 }
 
 /* As or_generation, for every strategy: vel = ClipUp velocity (or NULL),
  * sig = per-dimension sigma (PGPE, SNES; updated in place, and used as
- * c->sigma_vec for the sampling).                                          */
+ * c->sigma_vec for the sampling).  Sep-CMA-ES keeps C in sig, p_sigma in
+ * m1 and p_c in v, and returns the run's new sigma in *sigma_out.          */
 void or_generation_ex(const or_config* c0, int32_t run, int64_t t, const float* pdata,
-                      float* m, float* m1, float* v, float* vel, float* sig, const float* fit_in,
+                      float* m, float* m1, float* v, float* vel, float* sig, float* sigma_out,
+                      const float* fit_in,
                       float* fit_out, float* y_out, float* g_out,
                       double* best_key, float* best_f, float* best_x)
 {
     or_config cfg = *c0;
     const or_config* c = &cfg;
-    if (cfg.strategy != OR_STRAT_OPENAI_ES) cfg.sigma_vec = sig;
+    float* scale = NULL;
+    if (cfg.strategy == OR_STRAT_SEP_CMA) {
+        /* state: sig = C, m1 = p_sigma, v = p_c; sampling scale sigma sqrt(C) */
+        scale = (float*)malloc(sizeof(float) * (size_t)cfg.num_dims);
+        or_cma_scale(cfg.num_dims, cfg.sigma, sig, scale);
+        cfg.sigma_vec = scale;
+    } else if (cfg.strategy != OR_STRAT_OPENAI_ES) {
+        cfg.sigma_vec = sig;
+    }
     int32_t N = c->popsize;
     int64_t D = c->num_dims;
     float* f = (float*)malloc(sizeof(float) * (size_t)N);
@@ -787,7 +930,12 @@ void or_generation_ex(const or_config* c0, int32_t run, int64_t t, const float* 
         pen = (float*)malloc(sizeof(float) * (size_t)N);
         or_penalty(c, run, (uint32_t)t, m, pen);
     }
-    if (c->strategy == OR_STRAT_SNES) {
+    if (c->strategy == OR_STRAT_SEP_CMA) {
+        float sg = c->sigma;
+        or_sepcma_update(c, run, t, f, pen, m, &sg, sig, m1, v, scale, y);
+        if (sigma_out) *sigma_out = sg;
+        for (int64_t d = 0; d < D; ++d) g[d] = 0.0f;
+    } else if (c->strategy == OR_STRAT_SNES) {
         /* m and sigma move together; sig is also c->sigma_vec */
         float* snew = (float*)malloc(sizeof(float) * (size_t)D);
         memcpy(snew, sig, sizeof(float) * (size_t)D);
@@ -813,6 +961,7 @@ void or_generation_ex(const or_config* c0, int32_t run, int64_t t, const float* 
         }
     }
     free(pen);
+    free(scale);
     if (fit_out) memcpy(fit_out, f, sizeof(float) * (size_t)N);
     if (y_out) memcpy(y_out, y, sizeof(float) * (size_t)N);
     if (g_out) memcpy(g_out, g, sizeof(float) * (size_t)D);

@@ -24,7 +24,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 PROB_NONE, PROB_SPHERE, PROB_SHIFTED_SPHERE, PROB_ROSENBROCK, PROB_RASTRIGIN, PROB_MLP = range(6)
 INIT_UNIFORM, INIT_ZERO, INIT_FANIN_NORMAL = range(3)
 SHAPE_CENTERED_RANK, SHAPE_RAW, SHAPE_Z_SCORE = range(3)
-STRAT_OPENAI_ES, STRAT_PGPE, STRAT_SNES = range(3)
+STRAT_OPENAI_ES, STRAT_PGPE, STRAT_SNES, STRAT_SEP_CMA = range(4)
 OPT_ADAM, OPT_CLIPUP = range(2)
 DOM_NOISE, DOM_INIT, DOM_PROBLEM, DOM_EVAL = range(4)
 MLP_IN, MLP_H, MLP_OUT = 64, 256, 16
@@ -75,6 +75,7 @@ class _Cfg(ctypes.Structure):
         ("clipup_momentum", ctypes.c_float),
         ("snes_temperature", ctypes.c_float),
         ("sigma_vec", ctypes.c_void_p),
+        ("elite_ratio", ctypes.c_float),
     ]
 
 
@@ -115,6 +116,7 @@ class OracleConfig:
     clipup_max_speed: float = 0.3
     clipup_momentum: float = 0.9
     snes_temperature: float = 12.0
+    elite_ratio: float = 0.5  # Sep-CMA-ES (App. B table)
 
     def cstruct(self, sigma_vec=None) -> _Cfg:
         c = _Cfg(self.num_dims, self.popsize, self.num_runs, self.sigma, self.lr, self.beta1,
@@ -123,7 +125,7 @@ class OracleConfig:
                  self.mlp_bf16, self.mlp_tanh_out, self.sigma_decay, self.sigma_final,
                  self.lr_decay, self.lr_final, self.w_decay, self.strategy, self.optimizer,
                  self.sigma_lr, self.sigma_max_change, self.clipup_max_speed, self.clipup_momentum,
-                 self.snes_temperature, None)
+                 self.snes_temperature, None, self.elite_ratio)
         if sigma_vec is not None:
             c.sigma_vec = sigma_vec.ctypes.data
             c._keep = sigma_vec  # the C side reads through this pointer
@@ -163,7 +165,10 @@ def lib():
             "or_clipup": (None, [pc, f32, P(f32), i64, P(f32), P(f32)]),
             "or_snes_table": (None, [i32, f32, P(f32)]),
             "or_generation_ex": (None, [pc, i32, i64, P(f32), P(f32), P(f32), P(f32), P(f32), P(f32), P(f32),
-                                        P(f32), P(f32), P(f32), P(ctypes.c_double), P(f32), P(f32)]),
+                                        P(f32), P(f32), P(f32), P(f32), P(ctypes.c_double), P(f32), P(f32)]),
+            "or_cma_mu": (i32, [pc]),
+            "or_cma_weights": (None, [pc, P(ctypes.c_double)]),
+            "or_cma_scale": (None, [i64, f32, P(f32), P(f32)]),
             "or_shape": (None, [P(f32), i32, i32, i32, P(f32)]),
             "or_grad": (None, [pc, i32, u32, P(f32), i64, i64, P(f32)]),
             "or_adam": (None, [pc, i64, P(f32), i64, P(f32), P(f32), P(f32)]),
@@ -336,6 +341,14 @@ def clipup(cfg, lr, g, m, vel):
     return m, vel
 
 
+def cma_weights(cfg):
+    """Sep-CMA-ES recombination weights by rank (fp64), length mu."""
+    mu = int(lib().or_cma_mu(cfg.cstruct()))
+    w = np.zeros(mu, np.float64)
+    lib().or_cma_weights(cfg.cstruct(), _p(w, ctypes.c_double))
+    return w
+
+
 def snes_table(N, beta):
     """SNES softmax rank utilities indexed by rank' (best = N - 1)."""
     w = np.zeros(N, np.float32)
@@ -382,7 +395,9 @@ class OracleES:
         self.sigma = np.full(R, cfg.sigma, dtype=np.float32)
         self.lr = np.full(R, cfg.lr, dtype=np.float32)
         # per-dimension sigma (PGPE, SNES) and ClipUp velocity
-        self.sig = np.full((R, D), cfg.sigma, dtype=np.float32)
+        # Sep-CMA-ES keeps its diagonal covariance C (init 1) in sig, p_sigma
+        # in m1 and p_c in v
+        self.sig = np.full((R, D), 1.0 if cfg.strategy == STRAT_SEP_CMA else cfg.sigma, dtype=np.float32)
         self.vel = np.zeros((R, D), np.float32)
 
     def set_hparams(self, sigma=None, lr=None):
@@ -395,10 +410,17 @@ class OracleES:
         """The config of run r at the current generation (its sigma and lr)."""
         return replace(self.cfg, sigma=float(self.sigma[r]), lr=float(self.lr[r]))
 
+    def scale(self, r):
+        """Sampling scale of run r: sigma vector (PGPE, SNES), sigma sqrt(C) (Sep-CMA-ES)."""
+        if self.cfg.strategy == STRAT_SEP_CMA:
+            s = np.zeros(self.cfg.num_dims, np.float32)
+            lib().or_cma_scale(self.cfg.num_dims, float(self.sigma[r]), _p(_f32(self.sig[r])), _p(s))
+            return s
+        return self.sig[r] if self.cfg.strategy != STRAT_OPENAI_ES else None
+
     def _cs(self, r):
-        """C config of run r, with its sigma vector for PGPE / SNES."""
-        vec = self.sig[r] if self.cfg.strategy != STRAT_OPENAI_ES else None
-        return self.run_cfg(r).cstruct(vec)
+        """C config of run r, with its sampling scale vector where there is one."""
+        return self.run_cfg(r).cstruct(self.scale(r))
 
     def ask(self):
         R, N, D = self.cfg.num_runs, self.cfg.popsize, self.cfg.num_dims
@@ -435,14 +457,18 @@ class OracleES:
             bf = np.array([self.best_f[r]], np.float32)
             bx = self.best_x[r].copy()
             fo, yo, go = np.zeros(N, np.float32), np.zeros(N, np.float32), np.zeros(D, np.float32)
-            lib().or_generation_ex(c, r, self.t, _p(pd), _p(m), _p(m1), _p(v), _p(vel), _p(sig), _p(fin), _p(fo),
-                                   _p(yo), _p(go), ctypes.byref(bk), _p(bf), _p(bx))
+            so = np.array([self.sigma[r]], np.float32)
+            lib().or_generation_ex(c, r, self.t, _p(pd), _p(m), _p(m1), _p(v), _p(vel), _p(sig), _p(so), _p(fin),
+                                   _p(fo), _p(yo), _p(go), ctypes.byref(bk), _p(bf), _p(bx))
+            if cfg.strategy == STRAT_SEP_CMA:
+                self.sigma[r] = so[0]
             self.m[r], self.m1[r], self.v[r] = m, m1, v
             self.vel[r], self.sig[r] = vel, sig
             self.best_key[r], self.best_f[r], self.best_x[r] = bk.value, bf[0], bx
             out_f[r], out_y[r], out_g[r] = fo, yo, go
             if cfg.strategy == STRAT_OPENAI_ES:
                 self.sigma[r] = decay(float(self.sigma[r]), cfg.sigma_decay, cfg.sigma_final)
+            # (Sep-CMA-ES adapts sigma by path length instead of a schedule)
             self.lr[r] = decay(float(self.lr[r]), cfg.lr_decay, cfg.lr_final)
         self.t += 1
         return {"fitness": out_f, "y": out_y, "g": out_g}

@@ -88,8 +88,18 @@ typedef enum { ES_INIT_UNIFORM = 0, ES_INIT_ZERO = 1, ES_INIT_FANIN_NORMAL = 2 }
  *              w = softmax(beta (rank'/N - 1/2)), rank' = N-1-rank (best
  *              largest), b_p = y_p + y_{p+P}; m += fl32(lr sigma_d) A,
  *              sigma_d *= exp(sigma_lr/2 B); the shaping field is ignored.
- * After each tell the sigma (vector) follows the schedule. */
-typedef enum { ES_STRAT_OPENAI_ES = 0, ES_STRAT_PGPE = 1, ES_STRAT_SNES = 2 } es_strategy;
+ * After each tell the sigma (vector) follows the schedule.
+ *   SEP_CMA    Sep-CMA-ES (Ros & Hansen 2008): independent members
+ *              x_j = m + s (.) z_j (Philox row j), s_d = fl32(sigma sqrtf(C_d));
+ *              the mu = max(1, floor(elite_ratio N)) best members recombine
+ *              with weights ln(mu + 1/2) - ln(i + 1) (normalised);
+ *              evolution paths p_sigma, p_c, diagonal covariance C and
+ *              path-length control of sigma with the standard CMA-ES
+ *              settings and the separable rate factor (D + 2)/3.  m1 and v
+ *              of es_get_state hold p_sigma and p_c; es_get_strategy_state's
+ *              sigma_vec holds C; sigma is per run (es_get_hparams) and has
+ *              no schedule.  The shaping field is ignored. */
+typedef enum { ES_STRAT_OPENAI_ES = 0, ES_STRAT_PGPE = 1, ES_STRAT_SNES = 2, ES_STRAT_SEP_CMA = 3 } es_strategy;
 
 /* Optimiser of the mean (OpenAI-ES, PGPE): Adam, or ClipUp (Toklu et al.
  * 2020, the ES optimiser named in Sec. 3.1): v = momentum v + lr g/|g|,
@@ -139,6 +149,8 @@ typedef struct es_config {
     float clipup_max_speed; /* ClipUp velocity bound (> 0)                   */
     float clipup_momentum;  /* ClipUp velocity decay in [0, 1)               */
     float snes_temperature; /* SNES utility temperature beta (>= 0)          */
+    float elite_ratio;  /* Sep-CMA-ES: share of the population recombined, (0, 1] */
+    int32_t reserved;   /* must be 0                                         */
 } es_config;
 
 typedef struct es_handle es_handle;
@@ -199,7 +211,8 @@ es_status es_get_grad(es_handle* h, float* g);
 es_status es_set_hparams(es_handle* h, const float* sigma, const float* lr);
 es_status es_get_hparams(es_handle* h, float* sigma, float* lr);
 
-/* Per-dimension sigma (PGPE, SNES) and ClipUp velocity of every run:
+/* Per-dimension sigma (PGPE, SNES) -- for Sep-CMA-ES the diagonal
+ * covariance C -- and ClipUp velocity of every run:
  * device [R][D] each; NULL to skip.  ES_ERR_UNSUPPORTED for a state the
  * configured strategy and optimiser do not keep.  es_set_strategy_state
  * requires no open ask. */

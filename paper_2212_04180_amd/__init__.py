@@ -5,10 +5,10 @@ this package is its thin Python binding and the synthetic workload presets.
 """
 from .esmi import (ES, ESConfig, EsError, FLAG_KEEP_GRAD, INIT_FANIN_NORMAL, INIT_UNIFORM, INIT_ZERO,
                    PROB_MLP, PROB_NONE, PROB_RASTRIGIN, PROB_ROSENBROCK, PROB_SHIFTED_SPHERE, PROB_SPHERE,
-                   SHAPE_CENTERED_RANK, SHAPE_RAW, SHAPE_Z_SCORE, STRAT_OPENAI_ES, STRAT_PGPE, STRAT_SNES,
+                   SHAPE_CENTERED_RANK, SHAPE_RAW, SHAPE_Z_SCORE, STRAT_OPENAI_ES, STRAT_PGPE, STRAT_SNES, STRAT_SEP_CMA,
                    OPT_ADAM, OPT_CLIPUP, lib)
 
 __all__ = ["ES", "ESConfig", "EsError", "lib", "FLAG_KEEP_GRAD", "INIT_FANIN_NORMAL", "INIT_UNIFORM",
            "INIT_ZERO", "PROB_MLP", "PROB_NONE", "PROB_RASTRIGIN", "PROB_ROSENBROCK", "PROB_SHIFTED_SPHERE",
            "PROB_SPHERE", "SHAPE_CENTERED_RANK", "SHAPE_RAW", "SHAPE_Z_SCORE", "STRAT_OPENAI_ES", "STRAT_PGPE",
-           "STRAT_SNES", "OPT_ADAM", "OPT_CLIPUP"]
+           "STRAT_SNES", "STRAT_SEP_CMA", "OPT_ADAM", "OPT_CLIPUP"]

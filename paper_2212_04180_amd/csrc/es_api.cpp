@@ -10,7 +10,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <algorithm>
 #include <cstring>
+#include <vector>
 #include <new>
 
 #include "es_internal.hpp"
@@ -69,8 +71,15 @@ struct es_handle {
     float* sig = nullptr;        // [R][Dp] per-dimension sigma (PGPE, SNES)
     float* vel = nullptr;        // [R][Dp] ClipUp velocity
     float* gbuf = nullptr;       // [R][Dp] ClipUp gradient
-    double* gpart = nullptr;     // [R][groups] ClipUp partial norms
+    double* gpart = nullptr;     // [R][groups] ClipUp / Sep-CMA-ES partial norms
     double* vpart = nullptr;
+    // Sep-CMA-ES
+    CmaConsts cma{};
+    int32_t* elite = nullptr;    // [R][N]
+    float* cw = nullptr;         // [mu]
+    float* cmaC = nullptr;       // [R][Dp]
+    double* zw = nullptr;        // [R][Dp]
+    double* qd = nullptr;        // [R][Dp]
     TellPlan tell;               // pair slices of the gradient kernel
     double* tell_part = nullptr; // per-workgroup gradient sums when tell.nsplit > 1
     float* pdata = nullptr;  // [Dp] shift vector or teacher
@@ -147,13 +156,19 @@ const char* validate(const es_config& c)
     if (!(c.sigma_final >= 0.0f) || !std::isfinite(c.sigma_final)) return "sigma_final must be finite and >= 0";
     if (!(c.lr_final >= 0.0f) || !std::isfinite(c.lr_final)) return "lr_final must be finite and >= 0";
     if (!(c.w_decay >= 0.0f) || !std::isfinite(c.w_decay)) return "w_decay must be finite and >= 0";
-    if (c.strategy < ES_STRAT_OPENAI_ES || c.strategy > ES_STRAT_SNES) return "unknown strategy";
+    if (c.strategy < ES_STRAT_OPENAI_ES || c.strategy > ES_STRAT_SEP_CMA) return "unknown strategy";
+    if (c.strategy == ES_STRAT_SEP_CMA && !(c.elite_ratio > 0.0f && c.elite_ratio <= 1.0f))
+        return "elite_ratio must be in (0, 1]";
+    if (c.reserved != 0) return "reserved must be 0";
+    if (c.strategy == ES_STRAT_SEP_CMA && c.problem == ES_PROB_MLP)
+        return "Sep-CMA-ES takes the benchmark problems or the caller's fitness (the MLP evaluate kernel samples "
+               "antithetic pairs)";
     if (c.optimizer != ES_OPT_ADAM && c.optimizer != ES_OPT_CLIPUP) return "unknown optimizer";
-    if (c.strategy != ES_STRAT_OPENAI_ES && (!(c.sigma_lr > 0.0f) || !std::isfinite(c.sigma_lr)))
+    if ((c.strategy == ES_STRAT_PGPE || c.strategy == ES_STRAT_SNES) && (!(c.sigma_lr > 0.0f) || !std::isfinite(c.sigma_lr)))
         return "sigma_lr must be finite and > 0";
     if (c.strategy == ES_STRAT_PGPE && !(c.sigma_max_change > 0.0f && c.sigma_max_change < 1.0f))
         return "sigma_max_change must be in (0, 1)";
-    if (c.strategy != ES_STRAT_SNES && c.optimizer == ES_OPT_CLIPUP) {
+    if ((c.strategy == ES_STRAT_OPENAI_ES || c.strategy == ES_STRAT_PGPE) && c.optimizer == ES_OPT_CLIPUP) {
         if (!(c.clipup_max_speed > 0.0f) || !std::isfinite(c.clipup_max_speed))
             return "clipup_max_speed must be finite and > 0";
         if (!(c.clipup_momentum >= 0.0f && c.clipup_momentum < 1.0f)) return "clipup_momentum must be in [0, 1)";
@@ -167,9 +182,51 @@ const char* validate(const es_config& c)
 // (2k - (N-1)) / (2(N-1)).  SNES: the softmax utility of rank' = N-1-k,
 // exp(beta (rank'/N - 1/2)) / sum, in fp64 rounded once.  Returns the
 // table's fp64 mean.
+int32_t cma_mu(const es_config& c)
+{
+    const int32_t mu = (int32_t)std::floor((double)c.elite_ratio * (double)c.popsize);
+    return mu < 1 ? 1 : mu;
+}
+
+// Sep-CMA-ES settings (standard CMA-ES values, separable rate factor (D+2)/3)
+// and recombination weights ln(mu + 1/2) - ln(i + 1), normalised in fp64.
+CmaConsts cma_consts(const es_config& c, std::vector<double>& w)
+{
+    CmaConsts k{};
+    const double D = (double)c.num_dims;
+    k.mu = cma_mu(c);
+    w.assign((size_t)k.mu, 0.0);
+    double sum = 0.0, s2 = 0.0;
+    for (int32_t i = 0; i < k.mu; ++i) sum += (w[i] = std::log((double)k.mu + 0.5) - std::log((double)(i + 1)));
+    for (int32_t i = 0; i < k.mu; ++i) {
+        w[i] /= sum;
+        s2 += w[i] * w[i];
+    }
+    k.mu_eff = 1.0 / s2;
+    k.c_s = (k.mu_eff + 2.0) / (D + k.mu_eff + 5.0);
+    const double q = std::sqrt((k.mu_eff - 1.0) / (D + 1.0)) - 1.0;
+    k.d_s = 1.0 + 2.0 * (q > 0.0 ? q : 0.0) + k.c_s;
+    k.c_c = (4.0 + k.mu_eff / D) / (D + 4.0 + 2.0 * k.mu_eff / D);
+    const double c1 = 2.0 / ((D + 1.3) * (D + 1.3) + k.mu_eff);
+    double cmu = 2.0 * (k.mu_eff - 2.0 + 1.0 / k.mu_eff) / ((D + 2.0) * (D + 2.0) + k.mu_eff);
+    if (cmu > 1.0 - c1) cmu = 1.0 - c1;
+    k.c1 = std::min(1.0, c1 * (D + 2.0) / 3.0);
+    k.cmu = std::min(1.0 - k.c1, cmu * (D + 2.0) / 3.0);
+    k.chi = std::sqrt(D) * (1.0 - 1.0 / (4.0 * D) + 1.0 / (21.0 * D * D));
+    k.a_s = std::sqrt(k.c_s * (2.0 - k.c_s) * k.mu_eff);
+    k.a_c = std::sqrt(k.c_c * (2.0 - k.c_c) * k.mu_eff);
+    k.wsum = 0.0;
+    for (int32_t i = 0; i < k.mu; ++i) k.wsum += (double)(float)w[i];
+    return k;
+}
+
 double weight_table(const es_config& c, int32_t N, float* out)
 {
-    if (c.strategy == ES_STRAT_SNES) {
+    if (c.strategy == ES_STRAT_SEP_CMA) {
+        std::vector<double> w;
+        const CmaConsts k = cma_consts(c, w);
+        for (int32_t r = 0; r < N; ++r) out[r] = r < k.mu ? (float)w[r] : 0.0f;
+    } else if (c.strategy == ES_STRAT_SNES) {
         double S = 0.0;
         for (int32_t k = 0; k < N; ++k) S += std::exp((double)c.snes_temperature * ((double)k / (double)N - 0.5));
         for (int32_t k = 0; k < N; ++k)
@@ -209,7 +266,7 @@ void free_all(es_handle* h)
     void* ptrs[] = {h->m, h->m1, h->v, h->best_x, h->grad, h->best_okey, h->best_f, h->best_j, h->table,
                     h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->adam_dev, h->mlp_scratch,
                     h->tell_part, h->hp[0], h->hp[1], h->pen, h->bfold, h->sig, h->vel, h->gbuf,
-                    h->gpart, h->vpart};
+                    h->gpart, h->vpart, h->elite, h->cw, h->cmaC, h->zw, h->qd};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     if (h->adam_host) (void)hipHostFree(h->adam_host);
@@ -255,14 +312,16 @@ es_status enqueue_tell(es_handle* h, const float* fitness, float* gen_best)
                "weight-decay penalty pass");
     }
     ES_HIP(h, launch_rank(g, h->cfg, fitness, h->pen, h->table, h->ybar_table, h->y, h->rank, h->wfold, h->bfold,
-                          h->best_okey, h->best_f, h->best_j, gen_best, hp, h->hp[1 - h->hp_cur], h->stream),
+                          h->elite, h->cma.mu, h->best_okey, h->best_f, h->best_j, gen_best, hp, h->hp[1 - h->hp_cur],
+                          h->stream),
            "rank kernel");
     const AdamConsts a = adam_consts(h->cfg, h->t);
     TellBuffers tb;
     tb.wfold = h->wfold; tb.bfold = h->bfold; tb.best_j = h->best_j;
     tb.m = h->m; tb.m1 = h->m1; tb.v = h->v; tb.grad = h->grad; tb.best_x = h->best_x;
     tb.sig = h->sig; tb.vel = h->vel; tb.gbuf = h->gbuf; tb.gpart = h->gpart; tb.vpart = h->vpart;
-    tb.part = h->tell_part; tb.hp = hp;
+    tb.part = h->tell_part; tb.hp = hp; tb.hp_next = h->hp[1 - h->hp_cur];
+    tb.elite = h->elite; tb.cw = h->cw; tb.zw = h->zw; tb.qd = h->qd; tb.cmaC = h->cmaC; tb.cma = h->cma;
     ES_HIP(h, launch_tell(g, h->cfg, h->tell, (uint32_t)h->t, a, tb, h->stream), "tell kernel");
     h->hp_cur = 1 - h->hp_cur;  // the schedule step is next generation's sigma and lr
     return ES_OK;
@@ -379,9 +438,20 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
         e = dalloc(reinterpret_cast<char**>(&h->mlp_scratch), mlp_scratch_bytes());
     if (e == hipSuccess && h->tell.nsplit > 1)
         e = dalloc(&h->tell_part, tell_part_elems(g, h->tell, cfg->strategy));
-    if (e == hipSuccess && cfg->strategy != ES_STRAT_OPENAI_ES) e = dalloc(&h->bfold, (size_t)g.P * g.R);
-    if (e == hipSuccess && cfg->strategy != ES_STRAT_OPENAI_ES) e = dalloc(&h->sig, rows);
-    const bool clipup = cfg->strategy != ES_STRAT_SNES && cfg->optimizer == ES_OPT_CLIPUP;
+    const bool pgpe_snes = cfg->strategy == ES_STRAT_PGPE || cfg->strategy == ES_STRAT_SNES;
+    const bool cma = cfg->strategy == ES_STRAT_SEP_CMA;
+    if (e == hipSuccess && pgpe_snes) e = dalloc(&h->bfold, (size_t)g.P * g.R);
+    if (e == hipSuccess && (pgpe_snes || cma)) e = dalloc(&h->sig, rows);
+    std::vector<double> cma_w;
+    if (cma) h->cma = cma_consts(*cfg, cma_w);
+    if (e == hipSuccess && cma) e = dalloc(&h->elite, (size_t)g.N * g.R);
+    if (e == hipSuccess && cma) e = dalloc(&h->cw, (size_t)h->cma.mu);
+    if (e == hipSuccess && cma) e = dalloc(&h->cmaC, rows);
+    if (e == hipSuccess && cma) e = dalloc(&h->zw, rows);
+    if (e == hipSuccess && cma) e = dalloc(&h->qd, rows);
+    if (e == hipSuccess && cma) e = dalloc(&h->gpart, tell_groups(g) * g.R);
+    const bool clipup = (cfg->strategy == ES_STRAT_OPENAI_ES || cfg->strategy == ES_STRAT_PGPE) &&
+                        cfg->optimizer == ES_OPT_CLIPUP;
     if (e == hipSuccess && clipup) e = dalloc(&h->vel, rows);
     if (e == hipSuccess && clipup) e = dalloc(&h->gbuf, rows);
     if (e == hipSuccess && clipup) e = dalloc(&h->gpart, tell_groups(g) * g.R);
@@ -417,6 +487,13 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     std::free(tab); std::free(ok); std::free(bf); std::free(hp);
     if (e == hipSuccess) e = launch_init(g, *cfg, h->m, h->m1, h->v, h->best_x, h->stream);
     if (e == hipSuccess && h->sig) e = launch_fill_rows(g, h->sig, cfg->sigma, h->stream);
+    if (e == hipSuccess && h->cmaC) e = launch_fill_rows(g, h->cmaC, 1.0f, h->stream);
+    if (e == hipSuccess && h->cw) {
+        std::vector<float> w32(cma_w.size());
+        for (size_t i = 0; i < cma_w.size(); ++i) w32[i] = (float)cma_w[i];
+        e = hipMemcpyAsync(h->cw, w32.data(), sizeof(float) * w32.size(), hipMemcpyHostToDevice, h->stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(h->stream);  // w32 is freed next
+    }
     if (e == hipSuccess && h->vel) e = launch_fill_rows(g, h->vel, 0.0f, h->stream);
     if (e == hipSuccess && h->pdata) e = launch_problem_data(g, *cfg, h->pdata, h->stream);
     if (e == hipSuccess && h->mlp_scratch) e = launch_mlp_setup(h->pdata, h->mlp_scratch, h->stream);
@@ -563,6 +640,7 @@ es_status es_set_hparams(es_handle* h, const float* sigma, const float* lr)
     // synchronous copies: the caller's host arrays may be reused on return
     if (sigma) ES_HIP(h, hipMemcpyAsync(d, sigma, sizeof(float) * R, hipMemcpyHostToDevice, h->stream), "set sigma");
     if (lr) ES_HIP(h, hipMemcpyAsync(d + R, lr, sizeof(float) * R, hipMemcpyHostToDevice, h->stream), "set lr");
+    if (sigma && h->cmaC) ES_HIP(h, launch_cma_scale(h->g, h->sig, h->cmaC, d, h->stream), "Sep-CMA-ES scale");
     ES_HIP(h, hipStreamSynchronize(h->stream), "set hparams");
     return ES_OK;
 }
@@ -584,7 +662,8 @@ es_status es_get_strategy_state(es_handle* h, float* sigma_vec, float* velocity)
     if ((sigma_vec && !h->sig) || (velocity && !h->vel))
         return fail(h, ES_ERR_UNSUPPORTED, "es_get_strategy_state: the strategy keeps no such state");
     es_status s = ES_OK;
-    if (sigma_vec && (s = copy_rows_out(h, sigma_vec, h->sig)) != ES_OK) return s;
+    // Sep-CMA-ES: the diagonal covariance (its sampling scale is derived)
+    if (sigma_vec && (s = copy_rows_out(h, sigma_vec, h->cmaC ? h->cmaC : h->sig)) != ES_OK) return s;
     if (velocity && (s = copy_rows_out(h, velocity, h->vel)) != ES_OK) return s;
     return ES_OK;
 }
@@ -596,8 +675,10 @@ es_status es_set_strategy_state(es_handle* h, const float* sigma_vec, const floa
     if ((sigma_vec && !h->sig) || (velocity && !h->vel))
         return fail(h, ES_ERR_UNSUPPORTED, "es_set_strategy_state: the strategy keeps no such state");
     es_status s = ES_OK;
-    if (sigma_vec && (s = copy_rows_in(h, h->sig, sigma_vec)) != ES_OK) return s;
+    if (sigma_vec && (s = copy_rows_in(h, h->cmaC ? h->cmaC : h->sig, sigma_vec)) != ES_OK) return s;
     if (velocity && (s = copy_rows_in(h, h->vel, velocity)) != ES_OK) return s;
+    if (sigma_vec && h->cmaC)
+        ES_HIP(h, launch_cma_scale(h->g, h->sig, h->cmaC, h->hp[h->hp_cur], h->stream), "Sep-CMA-ES scale");
     return ES_OK;
 }
 
@@ -634,7 +715,7 @@ es_status es_save_state(es_handle* h, void* host_buf, size_t* bytes)
     if (!h || !bytes) return ES_ERR_ARG;
     const Geometry& g = h->g;
     const size_t rows = (size_t)g.Dp * g.R * sizeof(float);
-    const size_t extra = (h->sig ? rows : 0) + (h->vel ? rows : 0);
+    const size_t extra = (h->sig ? rows : 0) + (h->vel ? rows : 0) + (h->cmaC ? rows : 0);
     const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + 3 * sizeof(float)) + extra;
     if (!host_buf) {
         *bytes = need;
@@ -665,7 +746,8 @@ es_status es_save_state(es_handle* h, void* host_buf, size_t* bytes)
     ES_HIP(h, hipMemcpyAsync(p, h->hp[h->hp_cur], 2 * g.R * sizeof(float), hipMemcpyDeviceToHost, h->stream),
            "save sigma and lr");
     p += 2 * g.R * sizeof(float);
-    for (const float* src : {static_cast<const float*>(h->sig), static_cast<const float*>(h->vel)}) {
+    for (const float* src : {static_cast<const float*>(h->sig), static_cast<const float*>(h->vel),
+                             static_cast<const float*>(h->cmaC)}) {
         if (!src) continue;
         ES_HIP(h, hipMemcpyAsync(p, src, rows, hipMemcpyDeviceToHost, h->stream), "save strategy state");
         p += rows;
@@ -681,7 +763,7 @@ es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes)
     if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_load_state: an ask is open");
     const Geometry& g = h->g;
     const size_t rows = (size_t)g.Dp * g.R * sizeof(float);
-    const size_t extra = (h->sig ? rows : 0) + (h->vel ? rows : 0);
+    const size_t extra = (h->sig ? rows : 0) + (h->vel ? rows : 0) + (h->cmaC ? rows : 0);
     const size_t need = sizeof(CkptHeader) + 4 * rows + g.R * (sizeof(uint32_t) + 3 * sizeof(float)) + extra;
     if (bytes < need) return fail(h, ES_ERR_ARG, "es_load_state: checkpoint too small");
     CkptHeader hd;
@@ -703,7 +785,7 @@ es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes)
     ES_HIP(h, hipMemcpyAsync(h->hp[h->hp_cur], p, 2 * g.R * sizeof(float), hipMemcpyHostToDevice, h->stream),
            "load sigma and lr");
     p += 2 * g.R * sizeof(float);
-    for (float* dst : {h->sig, h->vel}) {
+    for (float* dst : {h->sig, h->vel, h->cmaC}) {
         if (!dst) continue;
         ES_HIP(h, hipMemcpyAsync(dst, p, rows, hipMemcpyHostToDevice, h->stream), "load strategy state");
         p += rows;

@@ -21,6 +21,14 @@ struct Geometry {
 };
 
 // Adam constants of one step (host-rounded to fp32).
+// Sep-CMA-ES settings (host-computed in fp64 from D, N and the elite ratio).
+struct CmaConsts {
+    int32_t mu;
+    double mu_eff, c_s, d_s, c_c, c1, cmu, chi;
+    double a_s, a_c;  // sqrt(c_s (2 - c_s) mu_eff), sqrt(c_c (2 - c_c) mu_eff)
+    double wsum;      // sum of the fp32 recombination weights
+};
+
 // Adam constants of one generation (the learning rate is per run, beside sigma).
 struct AdamConsts {
     float beta1, beta2, omb1, omb2, bc1, bc2, eps;
@@ -42,6 +50,7 @@ hipError_t launch_init(const Geometry& g, const es_config& c, float* m, float* m
                        float* best_x, hipStream_t s);
 hipError_t launch_problem_data(const Geometry& g, const es_config& c, float* pdata, hipStream_t s);
 hipError_t launch_fill_rows(const Geometry& g, float* p, float value, hipStream_t s);  // [R][Dp], padding 0
+hipError_t launch_cma_scale(const Geometry& g, float* svec, const float* C, const float* hp, hipStream_t s);
 // hp: device [2][R], sigma then lr of every run for the current generation.
 // svec: per-dimension sigma [R][Dp] (PGPE, SNES) or null.
 hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const float* m, float* x,
@@ -53,8 +62,8 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
 // utilities by rank), ybar_table its mean; bfold: PGPE / SNES second weight.
 hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* pen,
                        const float* table, double ybar_table, float* y, int32_t* rank, float* wfold, float* bfold,
-                       uint32_t* best_okey, float* best_f, int32_t* best_j, float* gen_best, const float* hp_cur,
-                       float* hp_next, hipStream_t s);
+                       int32_t* elite, int32_t mu, uint32_t* best_okey, float* best_f, int32_t* best_j,
+                       float* gen_best, const float* hp_cur, float* hp_next, hipStream_t s);
 // Split of the gradient kernel's pairs: ps pair slices (one wave each) per
 // workgroup, nsplit workgroups per group of 64 Philox blocks.  With nsplit > 1
 // every workgroup stores its partial sums (part, fp64 [R][nsplit][nb][4]) and
@@ -84,6 +93,13 @@ struct TellBuffers {
     double* vpart;         // [R][groups] ClipUp |v|^2 partials
     double* part;          // split partial sums
     const float* hp;       // [2][R] sigma, lr
+    float* hp_next;        // [2][R] next generation's (Sep-CMA-ES stores sigma')
+    const int32_t* elite;  // [R][N] Sep-CMA-ES elites by rank
+    const float* cw;       // [mu] recombination weights
+    double* zw;            // [R][Dp]
+    double* qd;            // [R][Dp]
+    float* cmaC;           // [R][Dp] diagonal covariance
+    CmaConsts cma;
 };
 hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp, uint32_t t, const AdamConsts& a,
                        const TellBuffers& tb, hipStream_t s);

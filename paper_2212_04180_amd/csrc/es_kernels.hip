@@ -99,7 +99,7 @@ __global__ void k_problem_data(float* __restrict__ out, uint64_t seed, int64_t D
 // ---------------------------------------------------------------------------
 __global__ void k_ask(const float* __restrict__ m, float* __restrict__ x, uint64_t seed, uint32_t t,
                       int64_t D, int64_t nb, int32_t N, int32_t P, int32_t R, const float* __restrict__ hp,
-                      const float* __restrict__ svec)
+                      const float* __restrict__ svec, int32_t indep)
 {
     const int64_t total = (int64_t)R * P * nb;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
@@ -107,8 +107,10 @@ __global__ void k_ask(const float* __restrict__ m, float* __restrict__ x, uint64
         const int64_t b = i % nb;
         const int64_t rp = i / nb;
         const int64_t p = rp % P, r = rp / P;
-        float e[4];
+        float e[4], e2[4];
         normals4(seed + (uint64_t)r, (uint32_t)b, (uint32_t)p, t, DOM_NOISE, e);
+        // independent members (Sep-CMA-ES): the second member has its own row
+        if (indep) normals4(seed + (uint64_t)r, (uint32_t)b, (uint32_t)(p + P), t, DOM_NOISE, e2);
         const float* mr = m + r * 4 * nb;
         float* xp = x + (r * N + p) * D;
         float* xm = x + (r * N + p + P) * D;
@@ -119,7 +121,7 @@ __global__ void k_ask(const float* __restrict__ m, float* __restrict__ x, uint64
             if (d < D) {
                 const float g = svec ? svec[r * 4 * nb + d] : sigma;
                 xp[d] = fmaf(g, e[k], mr[d]);
-                xm[d] = fmaf(-g, e[k], mr[d]);
+                xm[d] = indep ? fmaf(g, e2[k], mr[d]) : fmaf(-g, e[k], mr[d]);
             }
         }
     }
@@ -164,19 +166,25 @@ struct EvalLane {
     bool have_prev;
 };
 
-// Terms of one full Philox block (four live dims) for both members.  VEC:
-// per-dimension sigma gv[] (PGPE, SNES) instead of the run's scalar sg.
-template <int PROB, bool VEC>
-__device__ __forceinline__ void block_terms(const float e[4], const float mv[4], const float sv[4], const float* gv,
-                                            float sg, float ra, EvalLane& L, float& sp, float& sm)
+// Sampling modes of the evaluate kernels: antithetic with the run's scalar
+// sigma (OpenAI-ES), antithetic with a per-dimension sigma (PGPE, SNES), and
+// independent members with a per-dimension scale (Sep-CMA-ES: the lane's
+// second member uses Philox row p + P and the plus sign).
+enum SampleMode { SM_SCALAR = 0, SM_VEC = 1, SM_INDEP = 2 };
+
+// Terms of one full Philox block (four live dims) for both members: the
+// first from normals e, the second from -e (antithetic) or e2 (independent).
+template <int PROB, int SM>
+__device__ __forceinline__ void block_terms(const float e[4], const float e2[4], const float mv[4], const float sv[4],
+                                            const float* gv, float sg, float ra, EvalLane& L, float& sp, float& sm)
 {
     if constexpr (PROB == ES_PROB_ROSENBROCK) {
         float xp[4], xm[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const float g = VEC ? gv[k] : sg;
+            const float g = SM != SM_SCALAR ? gv[k] : sg;
             xp[k] = fmaf(g, e[k], mv[k]);
-            xm[k] = fmaf(-g, e[k], mv[k]);
+            xm[k] = SM == SM_INDEP ? fmaf(g, e2[k], mv[k]) : fmaf(-g, e[k], mv[k]);
         }
         float tp = rosen_term(xp[0], xp[1]) + rosen_term(xp[1], xp[2]) + rosen_term(xp[2], xp[3]);
         float tm = rosen_term(xm[0], xm[1]) + rosen_term(xm[1], xm[2]) + rosen_term(xm[2], xm[3]);
@@ -192,9 +200,9 @@ __device__ __forceinline__ void block_terms(const float e[4], const float mv[4],
     } else {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const float g = VEC ? gv[k] : sg;
+            const float g = SM != SM_SCALAR ? gv[k] : sg;
             sp += BlockTerm<PROB>::f(fmaf(g, e[k], mv[k]), sv[k], ra);
-            sm += BlockTerm<PROB>::f(fmaf(-g, e[k], mv[k]), sv[k], ra);
+            sm += BlockTerm<PROB>::f(SM == SM_INDEP ? fmaf(g, e2[k], mv[k]) : fmaf(-g, e[k], mv[k]), sv[k], ra);
         }
     }
 }
@@ -203,22 +211,24 @@ __device__ __forceinline__ void block_terms(const float e[4], const float mv[4],
 // run: fp32 sums of EVAL_FOLD blocks folded into fp64, in block order.  The
 // per-call kernel and the fused loop share this code, so both produce the
 // same bits.  V names the counter word that varies across the wave.
-template <int PROB, int V, bool VEC = false>
+template <int PROB, int V, int SM = SM_SCALAR>
 __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const float* __restrict__ pdata,
                                            uint32_t k0, uint32_t k1, uint32_t row, uint32_t t, int64_t b0,
                                            int64_t b1, int64_t D, float sg, float ra, double& accp, double& accm,
-                                           const float* __restrict__ gr = nullptr)
+                                           const float* __restrict__ gr = nullptr, uint32_t row2 = 0)
 {
+    constexpr bool VEC = SM != SM_SCALAR;
     const int64_t nfull = D / 4;
     const int32_t nf = (int32_t)((b1 < nfull ? b1 : nfull) - b0);  // full blocks in [b0, b1) (may be <= 0)
     EvalLane L{0.0, 0.0, 0.f, 0.f, false};
     if (PROB == ES_PROB_ROSENBROCK && b0 > 0) {
-        float e[4];
+        float e[4], e2[4] = {0.f, 0.f, 0.f, 0.f};
         box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(b0 - 1), row, t, DOM_NOISE), e);
+        if constexpr (SM == SM_INDEP) box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(b0 - 1), row2, t, DOM_NOISE), e2);
         const float mv = mr[4 * b0 - 1];
         const float g = VEC ? gr[4 * b0 - 1] : sg;
         L.xlp = fmaf(g, e[3], mv);
-        L.xlm = fmaf(-g, e[3], mv);
+        L.xlm = SM == SM_INDEP ? fmaf(g, e2[3], mv) : fmaf(-g, e[3], mv);
         L.have_prev = true;
     }
 
@@ -240,10 +250,12 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         float sp = 0.f, sm = 0.f;
 #pragma unroll
         for (int k = 0; k < EVAL_FOLD; ++k) {
-            float e[4];
+            float e[4], e2[4] = {0.f, 0.f, 0.f, 0.f};
             box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(bg + k), row, t, DOM_NOISE), e);
-            block_terms<PROB, VEC>(e, mv + 4 * k, PROB == ES_PROB_SHIFTED_SPHERE ? sv + 4 * k : zero4,
-                                   VEC ? gv + 4 * k : nullptr, sg, ra, L, sp, sm);
+            if constexpr (SM == SM_INDEP)
+                box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(bg + k), row2, t, DOM_NOISE), e2);
+            block_terms<PROB, SM>(e, e2, mv + 4 * k, PROB == ES_PROB_SHIFTED_SPHERE ? sv + 4 * k : zero4,
+                                  VEC ? gv + 4 * k : nullptr, sg, ra, L, sp, sm);
         }
         L.accp += (double)sp;
         L.accm += (double)sm;
@@ -261,10 +273,11 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
 #pragma unroll
             for (int q = 0; q < 4; ++q) sv[q] = pdata[4 * b + q];
         }
-        float e[4];
+        float e[4], e2[4] = {0.f, 0.f, 0.f, 0.f};
         box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
+        if constexpr (SM == SM_INDEP) box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row2, t, DOM_NOISE), e2);
         float sp = 0.f, sm = 0.f;
-        block_terms<PROB, VEC>(e, mv, sv, gv, sg, ra, L, sp, sm);
+        block_terms<PROB, SM>(e, e2, mv, sv, gv, sg, ra, L, sp, sm);
         L.accp += (double)sp;
         L.accm += (double)sm;
     }
@@ -273,13 +286,14 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
     if (b1 > nfull && nfull >= b0) {
         const int64_t b = nfull;
         const int nv = (int)(D - 4 * b);
-        float e[4];
+        float e[4], e2[4] = {0.f, 0.f, 0.f, 0.f};
         box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
+        if constexpr (SM == SM_INDEP) box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row2, t, DOM_NOISE), e2);
         float sp = 0.f, sm = 0.f;
         for (int k = 0; k < nv; ++k) {
             const float mv = mr[4 * b + k];
             const float g = VEC ? gr[4 * b + k] : sg;
-            const float xp = fmaf(g, e[k], mv), xm = fmaf(-g, e[k], mv);
+            const float xp = fmaf(g, e[k], mv), xm = SM == SM_INDEP ? fmaf(g, e2[k], mv) : fmaf(-g, e[k], mv);
             if constexpr (PROB == ES_PROB_ROSENBROCK) {
                 if (L.have_prev) {
                     sp += rosen_term(L.xlp, xp);
@@ -301,7 +315,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
     accm = L.accm;
 }
 
-template <int PROB, bool VEC>
+template <int PROB, int SM>
 __global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
     const float* __restrict__ m, const float* __restrict__ pdata, float* __restrict__ partial,
     uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t N, int32_t P, int64_t bc, int64_t nchunks,
@@ -323,8 +337,9 @@ __global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
     float sg;
     asm volatile("v_mov_b32 %0, %1" : "=v"(sg) : "s"(sigma));
     double accp, accm;
-    eval_chunk<PROB, LANES_ROW, VEC>(m + (int64_t)r * 4 * nb, pdata, (uint32_t)key, (uint32_t)(key >> 32), row, t,
-                                     b0, b1, D, sg, ra, accp, accm, VEC ? svec + (int64_t)r * 4 * nb : nullptr);
+    eval_chunk<PROB, LANES_ROW, SM>(m + (int64_t)r * 4 * nb, pdata, (uint32_t)key, (uint32_t)(key >> 32), row, t, b0,
+                                    b1, D, sg, ra, accp, accm, SM != SM_SCALAR ? svec + (int64_t)r * 4 * nb : nullptr,
+                                    row + (uint32_t)P);
     if (p < P) {
         float* o = partial + (chunk * gridDim.y + r) * (int64_t)N;
         o[p] = (float)accp;
@@ -389,8 +404,10 @@ struct ShapeArgs {
     // second folded weight per pair for the sigma-adapting strategies:
     // PGPE b_p = (y_p + y_{p+P})/2 - mean(y), SNES b_p = y_p + y_{p+P}
     float* bfold;           // [R][P] or null
-    int32_t bmode;          // 0 none, 1 PGPE, 2 SNES
+    int32_t bmode;          // 0 none, 1 PGPE, 2 SNES, 3 Sep-CMA-ES (elite list)
     double ybar_table;      // mean of the shaping table (table shaping)
+    int32_t* elite;         // [R][N] Sep-CMA-ES: member of rank i, i < mu
+    int32_t mu;
 };
 
 __device__ __forceinline__ float shaped_key(float f, float pen, int maximize, float w_decay)
@@ -560,6 +577,10 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
     wfold[(int64_t)r * P + p] = y1 - y2;
     if (sa.bmode == 1) sa.bfold[(int64_t)r * P + p] = (float)(0.5 * ((double)y1 + (double)y2) - ybar);
     if (sa.bmode == 2) sa.bfold[(int64_t)r * P + p] = y1 + y2;
+    if (sa.bmode == 3) {
+        if (r1 < sa.mu) sa.elite[(int64_t)r * N + r1] = j1;
+        if (r2 < sa.mu) sa.elite[(int64_t)r * N + r2] = j2;
+    }
     int32_t jb = -1;
     if (penalised) {
         if ((uint32_t)j1 == raw_best[1]) jb = j1;
@@ -628,10 +649,12 @@ __device__ __forceinline__ void tell_slice(const float* __restrict__ wr, uint32_
 // Both sums of one Philox block over the pairs [pb, pe) for the strategies
 // that adapt a per-dimension sigma: a64[k] = sum_p a_p z_{p,4b+k} and
 // b64[k] = sum_p b_p (z^2 - 1), fp32 over TELL_GROUP pairs folded into fp64.
+// rows: Philox row of each item (Sep-CMA-ES: the elite members), else the
+// item index (the pair).
 template <int V>
 __device__ __forceinline__ void tell_slice2(const float* __restrict__ ar, const float* __restrict__ br, uint32_t k0,
                                             uint32_t k1, uint32_t bb, uint32_t t, int32_t pb, int32_t pe,
-                                            double a64[4], double b64[4])
+                                            double a64[4], double b64[4], const int32_t* __restrict__ rows = nullptr)
 {
     int32_t p0 = pb;
     for (; p0 + TELL_GROUP <= pe; p0 += TELL_GROUP) {
@@ -645,7 +668,8 @@ __device__ __forceinline__ void tell_slice2(const float* __restrict__ ar, const 
 #pragma unroll
         for (int q = 0; q < TELL_GROUP; ++q) {
             float e[4];
-            box_muller4(philox4x32_10<V>(k0, k1, bb, (uint32_t)(p0 + q), t, DOM_NOISE), e);
+            const uint32_t row = rows ? (uint32_t)rows[p0 + q] : (uint32_t)(p0 + q);
+            box_muller4(philox4x32_10<V>(k0, k1, bb, row, t, DOM_NOISE), e);
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 a32[k] = fmaf(av[q], e[k], a32[k]);
@@ -661,7 +685,7 @@ __device__ __forceinline__ void tell_slice2(const float* __restrict__ ar, const 
     float a32[4] = {0.f, 0.f, 0.f, 0.f}, b32[4] = {0.f, 0.f, 0.f, 0.f};
     for (int32_t p = p0; p < pe; ++p) {
         float e[4];
-        box_muller4(philox4x32_10<V>(k0, k1, bb, (uint32_t)p, t, DOM_NOISE), e);
+        box_muller4(philox4x32_10<V>(k0, k1, bb, rows ? (uint32_t)rows[p] : (uint32_t)p, t, DOM_NOISE), e);
         const float a = ar[p], b = br[p];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -714,10 +738,18 @@ struct TellArgs {
     double* gpart;         // [R][groups] ClipUp: |g|^2 of each group of 64 blocks
     double* part;          // split partial sums [R][nsplit][nb][4 or 8]
     const float* hp;       // [2][R] sigma, lr
+    // Sep-CMA-ES: elite members by rank, recombination weights, the weighted
+    // noise sums kept for the second pass
+    const int32_t* elite;  // [R][N]
+    const float* cw;       // [mu]
+    double* zw;            // [R][Dp] sum_i w_i z_i
+    double* qd;            // [R][Dp] sum_i w_i z_i^2
+    CmaConsts cma;
     uint64_t seed;
     uint32_t t;
     int64_t D, nb;
     int32_t P, R, ps, nsplit;
+    int32_t nitems;        // items the slices split: P pairs, or mu elites
     int32_t strategy, optimizer;
     float sigma_lr, max_change, sigma_decay, sigma_final;
     AdamConsts ac;
@@ -753,6 +785,38 @@ __device__ __forceinline__ double tell_finish(const TellArgs& a, const double a6
     const int32_t N = 2 * a.P;
     float mn[4] = {mo[0], mo[1], mo[2], mo[3]}, gg[4] = {0.f, 0.f, 0.f, 0.f}, sn[4] = {so[0], so[1], so[2], so[3]};
     double g2 = 0.0;
+    if (a.strategy == ES_STRAT_SEP_CMA) {
+        // first pass: mean, p_sigma (in m1), the sums for the second pass and
+        // this lane's share of |p_sigma|^2; the best member (row = member, + sign)
+        const float4 p4 = *reinterpret_cast<const float4*>(a.m1 + off);
+        const float po[4] = {p4.x, p4.y, p4.z, p4.w};
+        float pn[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const bool live = 4 * b + k < a.D;
+            mn[k] = live ? (float)((double)mo[k] + (double)so[k] * a64[k]) : 0.f;
+            pn[k] = live ? (float)((1.0 - a.cma.c_s) * (double)po[k] + a.cma.a_s * a64[k]) : 0.f;
+            g2 += (double)pn[k] * (double)pn[k];
+        }
+        *reinterpret_cast<double4*>(a.zw + off) = make_double4(a64[0], a64[1], a64[2], a64[3]);
+        *reinterpret_cast<double4*>(a.qd + off) =
+            make_double4(b64[0] + a.cma.wsum, b64[1] + a.cma.wsum, b64[2] + a.cma.wsum, b64[3] + a.cma.wsum);
+        *reinterpret_cast<float4*>(a.m1 + off) = make_float4(pn[0], pn[1], pn[2], pn[3]);
+        const int32_t jb = a.best_j[r];
+        if (jb >= 0) {
+            float e[4];
+            box_muller4(philox4x32_10<LANES_BLOCK>(k0, k1, (uint32_t)b, (uint32_t)jb, a.t, DOM_NOISE), e);
+            float bx[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) bx[k] = 4 * b + k < a.D ? fmaf(so[k], e[k], mo[k]) : 0.f;
+            *reinterpret_cast<float4*>(a.best_x + off) = make_float4(bx[0], bx[1], bx[2], bx[3]);
+        }
+        *reinterpret_cast<float4*>(a.m + off) = make_float4(mn[0], mn[1], mn[2], mn[3]);
+        if (a.grad)
+            *reinterpret_cast<float4*>(a.grad + off) =
+                make_float4((float)a64[0], (float)a64[1], (float)a64[2], (float)a64[3]);
+        return g2;
+    }
     if (a.strategy == ES_STRAT_SNES) {
         const float h = 0.5f * a.sigma_lr;
 #pragma unroll
@@ -839,14 +903,17 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
     const uint64_t key = a.seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
     const int64_t S = (int64_t)a.ps * a.nsplit, gs = (int64_t)z * a.ps + s;
-    const int32_t pb = (int32_t)(((int64_t)a.P * gs) / S);
-    const int32_t pe = (int32_t)(((int64_t)a.P * (gs + 1)) / S);
+    const int32_t pb = (int32_t)(((int64_t)a.nitems * gs) / S);
+    const int32_t pe = (int32_t)(((int64_t)a.nitems * (gs + 1)) / S);
 
     double a64[4] = {0.0, 0.0, 0.0, 0.0}, b64[4] = {0.0, 0.0, 0.0, 0.0};
-    if constexpr (TWO)
-        tell_slice2<LANES_BLOCK>(a.wfold + (int64_t)r * a.P, a.bfold + (int64_t)r * a.P, k0, k1, bb, a.t, pb, pe,
-                                 a64, b64);
-    else
+    if constexpr (TWO) {
+        if (a.strategy == ES_STRAT_SEP_CMA)
+            tell_slice2<LANES_BLOCK>(a.cw, a.cw, k0, k1, bb, a.t, pb, pe, a64, b64, a.elite + (int64_t)r * 2 * a.P);
+        else
+            tell_slice2<LANES_BLOCK>(a.wfold + (int64_t)r * a.P, a.bfold + (int64_t)r * a.P, k0, k1, bb, a.t, pb,
+                                     pe, a64, b64);
+    } else
         tell_slice<LANES_BLOCK>(a.wfold + (int64_t)r * a.P, k0, k1, bb, a.t, pb, pe, a64);
     if (s > 0) {
 #pragma unroll
@@ -963,6 +1030,57 @@ __global__ __launch_bounds__(256) void k_clipup_velocity(const float* __restrict
     }
     const double tot = wave_sum(v2);
     if ((threadIdx.x & 63) == 0 && (b >> 6) < groups) vpart[(int64_t)r * groups + (b >> 6)] = tot;
+}
+
+// Sep-CMA-ES second pass: |p_sigma| from the groups' partials (fixed order),
+// then per dim p_c (in v), C, and the next generation's sampling scale
+// s = fl32(sigma' sqrtf(C)); the first workgroup stores the run's sigma'.
+__global__ __launch_bounds__(256) void k_sepcma_finish(float* __restrict__ v, float* __restrict__ C,
+                                                       float* __restrict__ svec, const double* __restrict__ zw,
+                                                       const double* __restrict__ qd, const double* __restrict__ gpart,
+                                                       const float* __restrict__ hp, float* __restrict__ hp_next,
+                                                       int64_t D, int64_t nb, int64_t groups, uint32_t t, CmaConsts k)
+{
+    __shared__ double red[256];
+    const int32_t r = blockIdx.y;
+    const double nps = sqrt(group_total(gpart + (int64_t)r * groups, groups, red));
+    const double hth = nps / sqrt(1.0 - pow(1.0 - k.c_s, 2.0 * ((double)t + 1.0)));
+    const double h = hth < (1.4 + 2.0 / ((double)D + 1.0)) * k.chi ? 1.0 : 0.0;
+    const float sig_new = (float)((double)hp[r] * exp((k.c_s / k.d_s) * (nps / k.chi - 1.0)));
+    if (blockIdx.x == 0 && threadIdx.x == 0) hp_next[r] = sig_new;
+    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= nb) return;
+    const int64_t off = (int64_t)r * 4 * nb + 4 * b;
+    const float4 pc4 = *reinterpret_cast<const float4*>(v + off);
+    const float4 c4 = *reinterpret_cast<const float4*>(C + off);
+    const double4 z4 = *reinterpret_cast<const double4*>(zw + off);
+    const double4 q4 = *reinterpret_cast<const double4*>(qd + off);
+    const float pco[4] = {pc4.x, pc4.y, pc4.z, pc4.w}, co[4] = {c4.x, c4.y, c4.z, c4.w};
+    const double zv[4] = {z4.x, z4.y, z4.z, z4.w}, qv[4] = {q4.x, q4.y, q4.z, q4.w};
+    float pcn[4], cn[4], sn[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (4 * b + j >= D) { pcn[j] = 0.f; cn[j] = 0.f; sn[j] = 0.f; continue; }
+        const double Cd = (double)co[j];
+        pcn[j] = (float)((1.0 - k.c_c) * (double)pco[j] + h * k.a_c * sqrt(Cd) * zv[j]);
+        const double pcd = (double)pcn[j];
+        cn[j] = (float)((1.0 - k.c1 - k.cmu) * Cd + k.c1 * (pcd * pcd + (1.0 - h) * k.c_c * (2.0 - k.c_c) * Cd) +
+                        k.cmu * Cd * qv[j]);
+        sn[j] = __fmul_rn(sig_new, sqrtf(cn[j]));
+    }
+    *reinterpret_cast<float4*>(v + off) = make_float4(pcn[0], pcn[1], pcn[2], pcn[3]);
+    *reinterpret_cast<float4*>(C + off) = make_float4(cn[0], cn[1], cn[2], cn[3]);
+    *reinterpret_cast<float4*>(svec + off) = make_float4(sn[0], sn[1], sn[2], sn[3]);
+}
+
+// s = fl32(sigma sqrtf(C)) for every run (after a change of sigma or C).
+__global__ void k_cma_scale(float* __restrict__ svec, const float* __restrict__ C, const float* __restrict__ hp,
+                            int64_t D, int64_t Dp, int64_t total)
+{
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = i / Dp;
+        svec[i] = (i % Dp) < D ? __fmul_rn(hp[r], sqrtf(C[i])) : 0.0f;
+    }
 }
 
 // v = v' * fl32(max_speed / |v'|) when |v'| > max_speed; m -= v.
@@ -1232,6 +1350,13 @@ hipError_t launch_init(const Geometry& g, const es_config& c, float* m, float* m
     return hipGetLastError();
 }
 
+hipError_t launch_cma_scale(const Geometry& g, float* svec, const float* C, const float* hp, hipStream_t s)
+{
+    const int64_t total = g.Dp * (int64_t)g.R;
+    k_cma_scale<<<grid_for(total, 256), 256, 0, s>>>(svec, C, hp, g.D, g.Dp, total);
+    return hipGetLastError();
+}
+
 hipError_t launch_fill_rows(const Geometry& g, float* p, float value, hipStream_t s)
 {
     const int64_t total = g.Dp * (int64_t)g.R;
@@ -1249,7 +1374,7 @@ hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const f
                       const float* hp, const float* svec, hipStream_t s)
 {
     k_ask<<<grid_for((int64_t)g.R * g.P * g.nb, 256), 256, 0, s>>>(m, x, c.seed, t, g.D, g.nb, g.N, g.P,
-                                                                   g.R, hp, svec);
+                                                                   g.R, hp, svec, c.strategy == ES_STRAT_SEP_CMA);
     return hipGetLastError();
 }
 
@@ -1263,12 +1388,17 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
     const dim3 block((unsigned)e.wg);
 #define ES_EVAL_LAUNCH(PROB)                                                                                   \
     do {                                                                                                       \
-        if (svec)                                                                                              \
-            k_eval_bbob<PROB, true><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N, g.P,   \
-                                                           e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, svec);  \
+        if (c.strategy == ES_STRAT_SEP_CMA)                                                                    \
+            k_eval_bbob<PROB, SM_INDEP><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N,    \
+                                                               g.P, e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, \
+                                                               svec);                                          \
+        else if (svec)                                                                                         \
+            k_eval_bbob<PROB, SM_VEC><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N, g.P, \
+                                                             e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, svec); \
         else                                                                                                   \
-            k_eval_bbob<PROB, false><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N, g.P,  \
-                                                            e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, nullptr); \
+            k_eval_bbob<PROB, SM_SCALAR><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N,   \
+                                                                g.P, e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, \
+                                                                nullptr);                                      \
     } while (0)
     switch (c.problem) {
     case ES_PROB_SPHERE: ES_EVAL_LAUNCH(ES_PROB_SPHERE); break;
@@ -1288,8 +1418,8 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
 
 hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* pen,
                        const float* table, double ybar_table, float* y, int32_t* rank, float* wfold, float* bfold,
-                       uint32_t* best_okey, float* best_f, int32_t* best_j, float* gen_best, const float* hp_cur,
-                       float* hp_next, hipStream_t s)
+                       int32_t* elite, int32_t mu, uint32_t* best_okey, float* best_f, int32_t* best_j,
+                       float* gen_best, const float* hp_cur, float* hp_next, hipStream_t s)
 {
     const dim3 grid((unsigned)((g.P + RANK_PAIRS - 1) / RANK_PAIRS), (unsigned)g.R);
     const size_t lds = sizeof(uint32_t) * (size_t)g.N;
@@ -1302,12 +1432,14 @@ hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, 
     sa.sigma_final = c.sigma_final;
     sa.lr_decay = c.lr_decay;
     sa.lr_final = c.lr_final;
-    // SNES shapes by its utility table (host-made, indexed by rank)
-    sa.shaping = c.strategy == ES_STRAT_SNES ? ES_SHAPE_CENTERED_RANK : c.shaping;
+    // SNES and Sep-CMA-ES shape by their weight tables (host-made, by rank)
+    sa.shaping = c.strategy == ES_STRAT_SNES || c.strategy == ES_STRAT_SEP_CMA ? ES_SHAPE_CENTERED_RANK : c.shaping;
     sa.maximize = c.maximize;
-    sa.bmode = c.strategy == ES_STRAT_PGPE ? 1 : c.strategy == ES_STRAT_SNES ? 2 : 0;
+    sa.bmode = c.strategy == ES_STRAT_PGPE ? 1 : c.strategy == ES_STRAT_SNES ? 2 : c.strategy == ES_STRAT_SEP_CMA ? 3 : 0;
     sa.bfold = bfold;
     sa.ybar_table = ybar_table;
+    sa.elite = elite;
+    sa.mu = mu;
     k_rank<<<grid, RANK_PAIRS * RANK_SLICES, lds, s>>>(fit, table, y, rank, wfold, best_okey, best_f, best_j,
                                                        gen_best, g.N, g.P, g.R, sa);
     return hipGetLastError();
@@ -1320,14 +1452,17 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp
     a.wfold = tb.wfold; a.bfold = tb.bfold; a.best_j = tb.best_j;
     a.m = tb.m; a.m1 = tb.m1; a.v = tb.v; a.grad = tb.grad; a.best_x = tb.best_x;
     a.sig = tb.sig; a.gbuf = tb.gbuf; a.gpart = tb.gpart; a.part = tb.part; a.hp = tb.hp;
+    a.elite = tb.elite; a.cw = tb.cw; a.zw = tb.zw; a.qd = tb.qd; a.cma = tb.cma;
+    a.nitems = c.strategy == ES_STRAT_SEP_CMA ? tb.cma.mu : g.P;
     a.seed = c.seed; a.t = t; a.D = g.D; a.nb = g.nb; a.P = g.P; a.R = g.R; a.ps = tp.ps; a.nsplit = tp.nsplit;
     a.strategy = c.strategy; a.optimizer = c.optimizer;
     a.sigma_lr = c.sigma_lr; a.max_change = c.sigma_max_change;
     a.sigma_decay = c.sigma_decay; a.sigma_final = c.sigma_final;
     a.ac = ac;
     const bool two = c.strategy != ES_STRAT_OPENAI_ES;
-    const bool clipup = c.strategy != ES_STRAT_SNES && c.optimizer == ES_OPT_CLIPUP;
-    if (!clipup) a.gpart = nullptr;
+    const bool cma = c.strategy == ES_STRAT_SEP_CMA;
+    const bool clipup = c.strategy != ES_STRAT_SNES && !cma && c.optimizer == ES_OPT_CLIPUP;
+    if (!clipup && !cma) a.gpart = nullptr;
     const int64_t groups = (g.nb + TELL_LANES - 1) / TELL_LANES;
     const dim3 grid((unsigned)groups, (unsigned)g.R, (unsigned)tp.nsplit);
     if (two) k_tell<true><<<grid, TELL_LANES * tp.ps, 0, s>>>(a);
@@ -1340,6 +1475,11 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp
         else k_tell_fold<false><<<fgrid, 256, 0, s>>>(a);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
+    }
+    if (cma) {
+        k_sepcma_finish<<<fgrid, 256, 0, s>>>(tb.v, tb.cmaC, tb.sig, tb.zw, tb.qd, tb.gpart, tb.hp, tb.hp_next, g.D,
+                                               g.nb, groups, t, tb.cma);
+        e = hipGetLastError();
     }
     if (clipup) {
         k_clipup_velocity<<<fgrid, 256, 0, s>>>(tb.gbuf, tb.vel, tb.gpart, tb.vpart, tb.hp, g.R, g.nb, groups,
@@ -1401,7 +1541,7 @@ size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e)
 bool fused_supported(const Geometry& g, const EvalPlan& e, const es_config& c)
 {
     if (c.problem < ES_PROB_SPHERE || c.problem > ES_PROB_RASTRIGIN) return false;
-    // the fused loop runs OpenAI-ES with Adam
+    // the fused loop runs OpenAI-ES with Adam (not PGPE, SNES, Sep-CMA-ES)
     if (c.strategy != ES_STRAT_OPENAI_ES || c.optimizer != ES_OPT_ADAM) return false;
     // the fused loop shapes by centered ranks or raw keys, without weight decay
     if (c.shaping == ES_SHAPE_Z_SCORE || c.w_decay != 0.0f) return false;

@@ -22,7 +22,7 @@ SHAPE_CENTERED_RANK, SHAPE_RAW, SHAPE_Z_SCORE = 0, 1, 2
 PROB_NONE, PROB_SPHERE, PROB_SHIFTED_SPHERE, PROB_ROSENBROCK, PROB_RASTRIGIN, PROB_MLP = range(6)
 INIT_UNIFORM, INIT_ZERO, INIT_FANIN_NORMAL = range(3)
 FLAG_KEEP_GRAD = 1
-STRAT_OPENAI_ES, STRAT_PGPE, STRAT_SNES = range(3)
+STRAT_OPENAI_ES, STRAT_PGPE, STRAT_SNES, STRAT_SEP_CMA = range(4)
 OPT_ADAM, OPT_CLIPUP = range(2)
 
 # Every symbol include/esmi.h declares, in declaration order.
@@ -74,6 +74,8 @@ class _Config(ctypes.Structure):
         ("clipup_max_speed", ctypes.c_float),
         ("clipup_momentum", ctypes.c_float),
         ("snes_temperature", ctypes.c_float),
+        ("elite_ratio", ctypes.c_float),
+        ("reserved", ctypes.c_int32),
     ]
 
 
@@ -114,6 +116,8 @@ class ESConfig:
     clipup_max_speed: float = 0.3
     clipup_momentum: float = 0.9
     snes_temperature: float = 12.0
+    elite_ratio: float = 0.5  # Sep-CMA-ES (App. B table)
+    reserved: int = 0
 
     def cstruct(self) -> _Config:
         c = _Config()

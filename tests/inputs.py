@@ -16,7 +16,7 @@ def to_oracle(cfg) -> O.OracleConfig:
     keys = ["num_dims", "popsize", "num_runs", "sigma", "lr", "beta1", "beta2", "eps", "maximize", "shaping",
             "seed", "init", "init_lo", "init_hi", "problem", "rastrigin_a", "mlp_batch", "mlp_bf16", "mlp_tanh_out",
             "sigma_decay", "sigma_final", "lr_decay", "lr_final", "w_decay", "strategy", "optimizer", "sigma_lr",
-            "sigma_max_change", "clipup_max_speed", "clipup_momentum", "snes_temperature"]
+            "sigma_max_change", "clipup_max_speed", "clipup_momentum", "snes_temperature", "elite_ratio"]
     return O.OracleConfig(**{k: getattr(cfg, k) for k in keys})
 
 

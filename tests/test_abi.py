@@ -44,7 +44,7 @@ def test_status_strings_and_init_error_without_gpu_work():
 
 def test_config_struct_has_no_padding():
     from paper_2212_04180_amd import esmi
-    assert ctypes.sizeof(esmi._Config) == 136
+    assert ctypes.sizeof(esmi._Config) == 144
 
 
 def test_product_does_not_reach_the_oracle():

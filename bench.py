@@ -191,8 +191,15 @@ def main():
         vec = cfg.strategy != P.STRAT_OPENAI_ES
         eval_slots = EVAL_SLOTS_PER_PAIR_BLOCK[prob] + (EVAL_VEC_EXTRA if vec else 0)
         tell_slots = TELL_SLOTS_PER_PAIR_BLOCK + (TELL_TWO_EXTRA if vec else 0)
+        tell_items = pair_blocks
+        if cfg.strategy == P.STRAT_SEP_CMA:
+            # independent members: a second Philox block and Box-Muller per
+            # pair-block; the gradient sums run over the mu elites
+            eval_slots += PHILOX_BM
+            mu = max(1, int(cfg.elite_ratio * N))
+            tell_items = R * mu * ((D + 3) // 4)
         achieved = pair_blocks * eval_slots / (eval_ms * 1e-3)
-        tell_achieved = pair_blocks * tell_slots / (tell_ms * 1e-3)
+        tell_achieved = tell_items * tell_slots / (tell_ms * 1e-3)
         roof = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                 "unit": "T VALU lane-op slots/s", "frac": achieved / VALU_PEAK,
                 "traffic": profiled_traffic(args.workload),
@@ -239,9 +246,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "path": args.path, "num_runs": R, "popsize": N, "num_dims": D,
                    "problem": prob or "mlp", "sigma": cfg.sigma, "lr": cfg.lr,
-                   "strategy": {0: "openai_es", 1: "pgpe", 2: "snes"}[cfg.strategy],
+                   "strategy": {0: "openai_es", 1: "pgpe", 2: "snes", 3: "sep_cma_es"}[cfg.strategy],
                    "optimizer": "clipup" if cfg.optimizer == P.OPT_CLIPUP and cfg.strategy != P.STRAT_SNES else
-                   ("adam" if cfg.strategy != P.STRAT_SNES else "snes natural gradient"),
+                   ({0: "adam", 1: "adam", 2: "snes natural gradient", 3: "cma recombination"}[cfg.strategy]),
                    "generations_per_s": 1e3 / ms, "eval_ms": eval_ms, "tell_ms": tell_ms},
         "roofline": roof,
         "hbm_equivalent": hbm_equiv,

@@ -9,7 +9,7 @@ The values are plain numbers: no arithmetic of the method lives here.
 from __future__ import annotations
 
 from .esmi import (ESConfig, INIT_FANIN_NORMAL, INIT_UNIFORM, INIT_ZERO, OPT_CLIPUP, PROB_MLP, PROB_RASTRIGIN,
-                   PROB_ROSENBROCK, PROB_SHIFTED_SPHERE, PROB_SPHERE, STRAT_PGPE, STRAT_SNES)
+                   PROB_ROSENBROCK, PROB_SHIFTED_SPHERE, PROB_SPHERE, STRAT_PGPE, STRAT_SEP_CMA, STRAT_SNES)
 
 # name -> (config, generations)
 WORKLOADS = {
@@ -42,6 +42,10 @@ WORKLOADS = {
     "snes_shifted_sphere_d1m": (ESConfig(num_dims=1_000_000, popsize=2048, num_runs=1, sigma=0.01, lr=1.0,
                                          seed=2, init=INIT_ZERO, problem=PROB_SHIFTED_SPHERE, strategy=STRAT_SNES,
                                          sigma_lr=0.00336, snes_temperature=12.0), 20),
+    # Sep-CMA-ES (App. B table: elite ratio 0.5), independent members
+    "sepcma_shifted_sphere_d1m": (ESConfig(num_dims=1_000_000, popsize=2048, num_runs=1, sigma=0.01, lr=0.0,
+                                           seed=2, init=INIT_ZERO, problem=PROB_SHIFTED_SPHERE,
+                                           strategy=STRAT_SEP_CMA, elite_ratio=0.5), 20),
 }
 
 

@@ -1140,10 +1140,10 @@ struct FusedArgs {
 template <int PROB>
 __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
 {
-    extern __shared__ double smem[];
+    extern __shared__ __align__(16) double smem[];
     const int32_t r = blockIdx.x;
     const int64_t Dp = 4 * a.nb;
-    // LDS layout: tell slices (fp64) | m | m1 | v | partial | fit | y | wf | keys | best
+    // LDS layout: tell slices (fp64) | m | m1 | v | partial | fit | y | wf | keys (N rounded up to 4) | table
     double* red = smem;                                  // [ps][nb][4]
     float* ms = reinterpret_cast<float*>(red + (int64_t)a.ps * a.nb * 4);
     float* m1s = ms + Dp;
@@ -1152,8 +1152,17 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
     float* fit = part + a.nchunks * a.N;                 // [N]
     float* y = fit + a.N;                                // [N]
     float* wf = y + a.N;                                 // [P]
-    uint32_t* keys = reinterpret_cast<uint32_t*>(wf + a.P);  // [N]
+    // keys start on a 16-byte boundary (they are read four at a time)
+    uint32_t* keys = reinterpret_cast<uint32_t*>(ms + ((3 * Dp + a.nchunks * a.N + 2 * a.N + a.P + 3) & ~(int64_t)3));
+    float* tab = reinterpret_cast<float*>(keys + ((a.N + 3) & ~3));  // [N] shaping table
+    // best-so-far of the run, kept on chip for the whole loop
     __shared__ int32_t best_j;
+    __shared__ uint32_t best_k;
+    __shared__ float best_fv;
+    // the last improvement of the loop: generation, member, sigma
+    __shared__ uint32_t best_t;
+    __shared__ int32_t best_jj;
+    __shared__ float best_sg;
 
     const uint64_t key = a.seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
@@ -1164,10 +1173,18 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         m1s[i] = a.m1[goff + i];
         vs[i] = a.v[goff + i];
     }
+    for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) tab[j] = a.table[j];
+    if (threadIdx.x == 0) {
+        best_k = a.best_okey[r];
+        best_fv = a.best_f[r];
+        best_jj = -1;
+    }
     __syncthreads();
 
     for (int32_t it = 0; it < a.T; ++it) {
         const uint32_t t = a.t0 + (uint32_t)it;
+        // this generation's Adam constants, fetched while the population is scored
+        const AdamConsts ac = a.adam[it];
         // evaluate: items (pair, chunk)
         const int64_t items = (int64_t)a.P * a.nchunks;
         for (int64_t i = threadIdx.x; i < items; i += blockDim.x) {
@@ -1182,9 +1199,10 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         }
         __syncthreads();
         // fitness in the reduce kernel's order, and order keys
+        const int nq = a.nchunks < RED_SLICES ? (int)a.nchunks : RED_SLICES;  // slices beyond add 0
         for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) {
             double tot = a.add;
-            for (int q = 0; q < RED_SLICES; ++q) {
+            for (int q = 0; q < nq; ++q) {
                 double acc = 0.0;
                 for (int64_t c = q; c < a.nchunks; c += RED_SLICES) acc += (double)part[c * a.N + j];
                 tot += acc;
@@ -1197,14 +1215,21 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         // centered ranks, weights, best-so-far and the generation's log entry
         for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) {
             const uint32_t K = keys[j];
-            int32_t rk = 0;
-            for (int32_t k = 0; k < a.N; ++k) rk += (keys[k] < K) | ((keys[k] == K) & (k < j));
-            y[j] = a.raw ? (a.maximize ? -fit[j] : fit[j]) : a.table[rk];
+            int32_t rk = 0, k = 0;
+            for (; k + 4 <= a.N; k += 4) {
+                const uint4 q4 = *reinterpret_cast<const uint4*>(keys + k);
+                rk += (q4.x < K) | ((q4.x == K) & (k < j));
+                rk += (q4.y < K) | ((q4.y == K) & (k + 1 < j));
+                rk += (q4.z < K) | ((q4.z == K) & (k + 2 < j));
+                rk += (q4.w < K) | ((q4.w == K) & (k + 3 < j));
+            }
+            for (; k < a.N; ++k) rk += (keys[k] < K) | ((keys[k] == K) & (k < j));
+            y[j] = a.raw ? (a.maximize ? -fit[j] : fit[j]) : tab[rk];
             if (rk == 0) {
                 if (a.log) a.log[(int64_t)it * a.R + r] = fit[j];
-                if (K < a.best_okey[r]) {
-                    a.best_okey[r] = K;
-                    a.best_f[r] = fit[j];
+                if (K < best_k) {
+                    best_k = K;
+                    best_fv = fit[j];
                     best_j = j;
                 } else {
                     best_j = -1;
@@ -1215,7 +1240,6 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         for (int32_t p = threadIdx.x; p < a.P; p += blockDim.x) wf[p] = y[p] - y[p + a.P];
         __syncthreads();
         // tell: items (block, pair slice), slices summed in order, then Adam
-        const AdamConsts ac = a.adam[it];
         for (int64_t i = threadIdx.x; i < (int64_t)a.ps * a.nb; i += blockDim.x) {
             const int32_t s = (int32_t)(i / a.nb);
             const int64_t b = i - (int64_t)s * a.nb;
@@ -1230,12 +1254,15 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         const int32_t jb = best_j;
         const double inv_ns = 1.0 / (2.0 * (double)a.P * (double)sigma);  // 1 / (N sigma)
         for (int64_t b = threadIdx.x; b < a.nb; b += blockDim.x) {
-            double a64[4];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                a64[k] = red[b * 4 + k];
-#pragma unroll
-                for (int q = 1; q < a.ps; ++q) a64[k] += red[((int64_t)q * a.nb + b) * 4 + k];
+            // slices in order, the four dims' chains side by side
+            const double4 r0 = *reinterpret_cast<const double4*>(red + b * 4);
+            double a64[4] = {r0.x, r0.y, r0.z, r0.w};
+            for (int q = 1; q < a.ps; ++q) {
+                const double4 rq = *reinterpret_cast<const double4*>(red + ((int64_t)q * a.nb + b) * 4);
+                a64[0] += rq.x;
+                a64[1] += rq.y;
+                a64[2] += rq.z;
+                a64[3] += rq.w;
             }
             float mo[4], m1o[4], vo[4], mn[4], m1n[4], vn[4], gg[4];
 #pragma unroll
@@ -1245,14 +1272,11 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
                 vo[k] = vs[4 * b + k];
             }
             adam_block(a64, inv_ns, ac, lr, 4 * b, a.D, mo, m1o, vo, mn, m1n, vn, gg);
+            // a new best: keep the mean it was sampled around; its noise is
+            // added once, after the loop (same arithmetic as the per-call path)
             if (jb >= 0) {
-                const int32_t pbst = jb < a.P ? jb : jb - a.P;
-                const float sg = jb < a.P ? sigma : -sigma;
-                float e[4];
-                box_muller4(philox4x32_10<LANES_BLOCK_AND_ROW>(k0, k1, (uint32_t)b, (uint32_t)pbst, t, DOM_NOISE),
-                            e);
 #pragma unroll
-                for (int k = 0; k < 4; ++k) a.best_x[goff + 4 * b + k] = 4 * b + k < a.D ? fmaf(sg, e[k], mo[k]) : 0.f;
+                for (int k = 0; k < 4; ++k) a.best_x[goff + 4 * b + k] = mo[k];
             }
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -1261,13 +1285,33 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
                 vs[4 * b + k] = vn[k];
             }
         }
+        if (jb >= 0 && threadIdx.x == 0) {
+            best_t = t;
+            best_jj = jb;
+            best_sg = sigma;
+        }
         __syncthreads();
         sigma = schedule_step(sigma, a.sigma_decay, a.sigma_final);
         lr = schedule_step(lr, a.lr_decay, a.lr_final);
     }
+    if (best_jj >= 0) {
+        const int32_t pbst = best_jj < a.P ? best_jj : best_jj - a.P;
+        const float sg = best_jj < a.P ? best_sg : -best_sg;
+        for (int64_t b = threadIdx.x; b < a.nb; b += blockDim.x) {
+            float e[4];
+            box_muller4(philox4x32_10<LANES_BLOCK_AND_ROW>(k0, k1, (uint32_t)b, (uint32_t)pbst, best_t, DOM_NOISE), e);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int64_t d = goff + 4 * b + k;
+                a.best_x[d] = 4 * b + k < a.D ? fmaf(sg, e[k], a.best_x[d]) : 0.f;
+            }
+        }
+    }
     if (threadIdx.x == 0) {
         a.hp[r] = sigma;
         a.hp[a.R + r] = lr;
+        a.best_okey[r] = best_k;
+        a.best_f[r] = best_fv;
     }
     for (int64_t i = threadIdx.x; i < Dp; i += blockDim.x) {
         a.m[goff + i] = ms[i];
@@ -1534,8 +1578,11 @@ int32_t tell_slices(const Geometry& g)
 size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e)
 {
     const size_t red = sizeof(double) * (size_t)tell_slices(g) * g.nb * 4;
-    const size_t f32 = sizeof(float) * (size_t)(3 * g.Dp + e.nchunks * g.N + 2 * g.N + g.P + g.N);
-    return red + f32;
+    // m, m1, v | partials | fit, y | wf | keys (padded to 4) | table
+    size_t f32 = (size_t)(3 * g.Dp + e.nchunks * g.N + 2 * g.N + g.P);
+    f32 = (f32 + 3) & ~(size_t)3;  // the keys are read four at a time
+    f32 += (size_t)((g.N + 3) & ~3) + (size_t)g.N;
+    return red + sizeof(float) * f32;
 }
 
 bool fused_supported(const Geometry& g, const EvalPlan& e, const es_config& c)

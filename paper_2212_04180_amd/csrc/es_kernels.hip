@@ -635,6 +635,8 @@ __device__ __forceinline__ void tell_slice(const float* __restrict__ wr, uint32_
         for (int q = 0; q < TELL_GROUP; ++q) wv[q] = wn[q];
     }
     float a32[4] = {0.f, 0.f, 0.f, 0.f};
+    // the pairs past the last whole group: independent noise blocks, summed in order
+#pragma unroll 4
     for (int32_t p = p0; p < pe; ++p) {
         float e[4];
         box_muller4(philox4x32_10<V>(k0, k1, bb, (uint32_t)p, t, DOM_NOISE), e);
@@ -649,9 +651,9 @@ __device__ __forceinline__ void tell_slice(const float* __restrict__ wr, uint32_
 // Both sums of one Philox block over the pairs [pb, pe) for the strategies
 // that adapt a per-dimension sigma: a64[k] = sum_p a_p z_{p,4b+k} and
 // b64[k] = sum_p b_p (z^2 - 1), fp32 over TELL_GROUP pairs folded into fp64.
-// rows: Philox row of each item (Sep-CMA-ES: the elite members), else the
-// item index (the pair).
-template <int V>
+// ROWS: the Philox row of each item comes from rows[] (Sep-CMA-ES: the
+// elite members), else it is the item index (the pair).
+template <int V, bool ROWS = false>
 __device__ __forceinline__ void tell_slice2(const float* __restrict__ ar, const float* __restrict__ br, uint32_t k0,
                                             uint32_t k1, uint32_t bb, uint32_t t, int32_t pb, int32_t pe,
                                             double a64[4], double b64[4], const int32_t* __restrict__ rows = nullptr)
@@ -668,7 +670,7 @@ __device__ __forceinline__ void tell_slice2(const float* __restrict__ ar, const 
 #pragma unroll
         for (int q = 0; q < TELL_GROUP; ++q) {
             float e[4];
-            const uint32_t row = rows ? (uint32_t)rows[p0 + q] : (uint32_t)(p0 + q);
+            const uint32_t row = ROWS ? (uint32_t)rows[p0 + q] : (uint32_t)(p0 + q);
             box_muller4(philox4x32_10<V>(k0, k1, bb, row, t, DOM_NOISE), e);
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -685,7 +687,7 @@ __device__ __forceinline__ void tell_slice2(const float* __restrict__ ar, const 
     float a32[4] = {0.f, 0.f, 0.f, 0.f}, b32[4] = {0.f, 0.f, 0.f, 0.f};
     for (int32_t p = p0; p < pe; ++p) {
         float e[4];
-        box_muller4(philox4x32_10<V>(k0, k1, bb, rows ? (uint32_t)rows[p] : (uint32_t)p, t, DOM_NOISE), e);
+        box_muller4(philox4x32_10<V>(k0, k1, bb, ROWS ? (uint32_t)rows[p] : (uint32_t)p, t, DOM_NOISE), e);
         const float a = ar[p], b = br[p];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -889,8 +891,9 @@ __device__ __forceinline__ double tell_finish(const TellArgs& a, const double a6
 // nsplit > 1, grid.z = nsplit workgroups share a block group (workgroup z
 // takes global slices z*ps .. z*ps+ps-1 of ps*nsplit equal slices of the
 // pairs) and store their sums to part; k_tell_fold adds them in split order
-// and applies the update.  TWO: the second sum b (PGPE, SNES).
-template <bool TWO>
+// and applies the update.  TWO: the second sum b (PGPE, SNES, Sep-CMA-ES);
+// ROWS: items are the elites (Sep-CMA-ES) rather than the pairs.
+template <bool TWO, bool ROWS = false>
 __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
 {
     __shared__ double red[TELL_MAX_PS - 1][TELL_LANES][TWO ? 8 : 4];
@@ -907,13 +910,12 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
     const int32_t pe = (int32_t)(((int64_t)a.nitems * (gs + 1)) / S);
 
     double a64[4] = {0.0, 0.0, 0.0, 0.0}, b64[4] = {0.0, 0.0, 0.0, 0.0};
-    if constexpr (TWO) {
-        if (a.strategy == ES_STRAT_SEP_CMA)
-            tell_slice2<LANES_BLOCK>(a.cw, a.cw, k0, k1, bb, a.t, pb, pe, a64, b64, a.elite + (int64_t)r * 2 * a.P);
-        else
-            tell_slice2<LANES_BLOCK>(a.wfold + (int64_t)r * a.P, a.bfold + (int64_t)r * a.P, k0, k1, bb, a.t, pb,
-                                     pe, a64, b64);
-    } else
+    if constexpr (ROWS)
+        tell_slice2<LANES_BLOCK, true>(a.cw, a.cw, k0, k1, bb, a.t, pb, pe, a64, b64, a.elite + (int64_t)r * 2 * a.P);
+    else if constexpr (TWO)
+        tell_slice2<LANES_BLOCK>(a.wfold + (int64_t)r * a.P, a.bfold + (int64_t)r * a.P, k0, k1, bb, a.t, pb, pe,
+                                 a64, b64);
+    else
         tell_slice<LANES_BLOCK>(a.wfold + (int64_t)r * a.P, k0, k1, bb, a.t, pb, pe, a64);
     if (s > 0) {
 #pragma unroll
@@ -1216,6 +1218,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) {
             const uint32_t K = keys[j];
             int32_t rk = 0, k = 0;
+#pragma unroll 4
             for (; k + 4 <= a.N; k += 4) {
                 const uint4 q4 = *reinterpret_cast<const uint4*>(keys + k);
                 rk += (q4.x < K) | ((q4.x == K) & (k < j));
@@ -1509,7 +1512,8 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp
     if (!clipup && !cma) a.gpart = nullptr;
     const int64_t groups = (g.nb + TELL_LANES - 1) / TELL_LANES;
     const dim3 grid((unsigned)groups, (unsigned)g.R, (unsigned)tp.nsplit);
-    if (two) k_tell<true><<<grid, TELL_LANES * tp.ps, 0, s>>>(a);
+    if (cma) k_tell<true, true><<<grid, TELL_LANES * tp.ps, 0, s>>>(a);
+    else if (two) k_tell<true><<<grid, TELL_LANES * tp.ps, 0, s>>>(a);
     else k_tell<false><<<grid, TELL_LANES * tp.ps, 0, s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -88,7 +88,9 @@ typedef enum { ES_INIT_UNIFORM = 0, ES_INIT_ZERO = 1, ES_INIT_FANIN_NORMAL = 2 }
  *              w = softmax(beta (rank'/N - 1/2)), rank' = N-1-rank (best
  *              largest), b_p = y_p + y_{p+P}; m += fl32(lr sigma_d) A,
  *              sigma_d *= exp(sigma_lr/2 B); the shaping field is ignored.
- * After each tell the sigma (vector) follows the schedule.
+ * After each tell the sigma (vector) follows the schedule.  For PGPE and
+ * SNES the run's sigma (cfg.sigma, es_get_hparams) is the value every
+ * dimension starts from at es_init and stays fixed.
  *   SEP_CMA    Sep-CMA-ES (Ros & Hansen 2008): independent members
  *              x_j = m + s (.) z_j (Philox row j), s_d = fl32(sigma sqrtf(C_d));
  *              the mu = max(1, floor(elite_ratio N)) best members recombine
@@ -207,7 +209,9 @@ es_status es_get_grad(es_handle* h, float* g);
  * either may be NULL (left unchanged).  es_init sets every run to
  * cfg.sigma and cfg.lr; the schedules continue from the values set here.
  * Requires no open ask; sigma must be finite and > 0, lr finite and >= 0
- * (ES_ERR_ARG otherwise).  es_get_hparams is synchronous. */
+ * (ES_ERR_ARG otherwise).  PGPE and SNES refuse a sigma (ES_ERR_UNSUPPORTED:
+ * they sample with the per-dimension sigma of es_set_strategy_state).
+ * es_get_hparams is synchronous. */
 es_status es_set_hparams(es_handle* h, const float* sigma, const float* lr);
 es_status es_get_hparams(es_handle* h, float* sigma, float* lr);
 

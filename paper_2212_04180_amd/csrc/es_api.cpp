@@ -629,6 +629,9 @@ es_status es_set_hparams(es_handle* h, const float* sigma, const float* lr)
 {
     if (!h) return ES_ERR_ARG;
     if (h->phase != READY) return fail(h, ES_ERR_SEQUENCE, "es_set_hparams: an ask is open");
+    if (sigma && (h->cfg.strategy == ES_STRAT_PGPE || h->cfg.strategy == ES_STRAT_SNES))
+        return fail(h, ES_ERR_UNSUPPORTED, "es_set_hparams: PGPE and SNES sample with a per-dimension sigma "
+                                           "(es_set_strategy_state)");
     const int32_t R = h->g.R;
     for (int32_t r = 0; r < R; ++r) {
         if (sigma && (!(sigma[r] > 0.0f) || !std::isfinite(sigma[r])))

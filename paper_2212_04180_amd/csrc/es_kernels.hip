@@ -1475,8 +1475,11 @@ hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, 
     sa.hp_cur = hp_cur;
     sa.hp_next = hp_next;
     sa.w_decay = c.w_decay;
-    sa.sigma_decay = c.sigma_decay;
-    sa.sigma_final = c.sigma_final;
+    // PGPE and SNES: the schedule acts on every dimension's sigma in the
+    // tell; the run's sigma only seeded them and stays as it is
+    const bool vec = c.strategy == ES_STRAT_PGPE || c.strategy == ES_STRAT_SNES;
+    sa.sigma_decay = vec ? 1.0f : c.sigma_decay;
+    sa.sigma_final = vec ? 0.0f : c.sigma_final;
     sa.lr_decay = c.lr_decay;
     sa.lr_final = c.lr_final;
     // SNES and Sep-CMA-ES shape by their weight tables (host-made, by rank)

@@ -150,3 +150,9 @@ def test_strategy_config_errors():
     es = P.ES(_cfg(P.STRAT_OPENAI_ES, P.OPT_ADAM))
     with pytest.raises(P.EsError):
         es.strategy_state()
+    for strategy in (P.STRAT_PGPE, P.STRAT_SNES):
+        es = P.ES(_cfg(strategy, 0))
+        with pytest.raises(P.EsError):
+            es.set_hparams([0.2, 0.2], None)
+        es.set_hparams(None, [0.01, 0.02])
+        np.testing.assert_array_equal(es.get_hparams()[1], np.float32([0.01, 0.02]))

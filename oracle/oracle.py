@@ -349,6 +349,13 @@ def cma_weights(cfg):
     return w
 
 
+def cma_scale(D, sigma, C):
+    """Sep-CMA-ES sampling scale s_d = fl32(sigma sqrtf(C_d))."""
+    s = np.zeros(D, np.float32)
+    lib().or_cma_scale(D, float(sigma), _p(_f32(C)), _p(s))
+    return s
+
+
 def snes_table(N, beta):
     """SNES softmax rank utilities indexed by rank' (best = N - 1)."""
     w = np.zeros(N, np.float32)
@@ -413,9 +420,7 @@ class OracleES:
     def scale(self, r):
         """Sampling scale of run r: sigma vector (PGPE, SNES), sigma sqrt(C) (Sep-CMA-ES)."""
         if self.cfg.strategy == STRAT_SEP_CMA:
-            s = np.zeros(self.cfg.num_dims, np.float32)
-            lib().or_cma_scale(self.cfg.num_dims, float(self.sigma[r]), _p(_f32(self.sig[r])), _p(s))
-            return s
+            return cma_scale(self.cfg.num_dims, self.sigma[r], self.sig[r])
         return self.sig[r] if self.cfg.strategy != STRAT_OPENAI_ES else None
 
     def _cs(self, r):

@@ -1,0 +1,185 @@
+"""Parity at the full D = 1e6, N = 2048 shifted-sphere geometry, in the
+launch configuration the benchmark times (marked gpu).
+
+The oracle cannot run a whole generation at this size in seconds, so these
+tests check what it can compute one by one: the fitness of sampled members,
+ranks and shaped weights (exact, from the GPU's fitness vector), the gradient
+and the Adam step on windows of dimensions (a first block, one in the
+middle, the ragged tail), and for the other strategies the properties that
+hold at any size."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+from inputs import to_oracle
+from oracle import oracle as O
+
+pytestmark = pytest.mark.gpu
+
+EPS_REL, EPS_ABS = 3e-7, 8e-7
+MEMBERS = [0, 1, 777, 1023, 1024, 1500, 2047]
+
+
+def _P():
+    import paper_2212_04180_amd as P
+    return P
+
+
+def _np(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def _workload(name, **kw):
+    from paper_2212_04180_amd import workloads
+    cfg, _ = workloads.get(name)
+    return dataclasses.replace(cfg, **kw)
+
+
+def _windows(D):
+    return [(0, 64), (D // 2 - 32, 64), (D - 37, 37)]
+
+
+def _check_fitness(es, oc, t, pdata, f, sig=None):
+    m = _np(es.get_state()["m"])[0]
+    ref = O.eval_members(oc, 0, t, m, pdata, np.array(MEMBERS), sig=sig)
+    got = f[0, MEMBERS]
+    assert np.all(np.abs(got - ref) <= 1e-5 * np.abs(ref)), (t, got, ref)
+
+
+def test_openai_es_adam_full_size_sampled():
+    P = _P()
+    cfg = _workload("shifted_sphere_d1m", flags=P.FLAG_KEEP_GRAD)
+    D, N = cfg.num_dims, cfg.popsize
+    es = P.ES(cfg)
+    oc = to_oracle(cfg)
+    pdata = O.problem_data(oc)
+    s_gpu = _np(es.problem_data())
+    err = np.abs(s_gpu.astype(np.float64) - pdata)
+    assert np.all(err <= EPS_REL * np.abs(pdata) + EPS_ABS)
+    assert not np.any(_np(es.get_state()["m"]))
+    for t in range(2):
+        st = es.get_state()
+        m0, m10, v0 = _np(st["m"])[0], _np(st["m1"])[0], _np(st["v"])[0]
+        es.ask()
+        f = _np(es.eval())
+        print("full-size openai-es t", t, flush=True)
+        _check_fitness(es, oc, t, pdata, f)
+        es.tell(torch.tensor(f, device="cuda"))
+        y, rk = es.shaped()
+        y, rk = _np(y)[0], _np(rk)[0]
+        np.testing.assert_array_equal(rk, O.ranks(f[0]))
+        np.testing.assert_array_equal(y, O.shape(f[0]))
+        g = _np(es.grad())[0]
+        st = es.get_state()
+        mg, m1g, vg = _np(st["m"])[0], _np(st["m1"])[0], _np(st["v"])[0]
+        w = y[: N // 2].astype(np.float64) - y[N // 2:]
+        ns = N * np.float64(np.float32(cfg.sigma))
+        for d0, nd in _windows(D):
+            sl = slice(d0, d0 + nd)
+            gref = O.grad(oc, 0, t, y, d0, nd)
+            E = np.stack([O.noise(oc, 0, t, p, d0, nd) for p in range(N // 2)]).astype(np.float64)
+            bound = (np.abs(w) @ (EPS_REL * np.abs(E) + EPS_ABS) + 1e-6 * (np.abs(w) @ np.abs(E))) / ns
+            assert np.all(np.abs(g[sl] - gref) <= bound + 1e-12), (t, d0)
+            mr, _, _ = O.adam(oc, t, gref, m0[sl], m10[sl], v0[sl])
+            assert np.max(np.abs(mg[sl] - mr) / np.maximum(np.abs(mr), cfg.lr)) <= 1e-5, (t, d0)
+            ma, m1a, va = O.adam(oc, t, g[sl], m0[sl], m10[sl], v0[sl])
+            np.testing.assert_array_equal(mg[sl], ma)
+            np.testing.assert_array_equal(m1g[sl], m1a)
+            np.testing.assert_array_equal(vg[sl], va)
+
+
+def test_openai_es_clipup_full_size_sampled():
+    P = _P()
+    cfg = _workload("clipup_shifted_sphere_d1m", flags=P.FLAG_KEEP_GRAD)
+    D, N = cfg.num_dims, cfg.popsize
+    es = P.ES(cfg)
+    oc = to_oracle(cfg)
+    pdata = O.problem_data(oc)
+    for t in range(2):
+        es.ask()
+        f = _np(es.eval())
+        print("full-size clipup t", t, flush=True)
+        _check_fitness(es, oc, t, pdata, f)
+        m0 = _np(es.get_state()["m"])[0]
+        v0 = _np(es.strategy_state(sigma=False, velocity=True)[1])[0].astype(np.float64)
+        es.tell(torch.tensor(f, device="cuda"))
+        y = O.shape(f[0])
+        g = _np(es.grad())[0].astype(np.float64)
+        vel = _np(es.strategy_state(sigma=False, velocity=True)[1])[0].astype(np.float64)
+        m = _np(es.get_state()["m"])[0]
+        for d0, nd in _windows(D):
+            sl = slice(d0, d0 + nd)
+            gref = O.grad(oc, 0, t, y, d0, nd).astype(np.float64)
+            assert np.max(np.abs(g[sl] - gref)) <= 1e-4 * np.max(np.abs(gref)), (t, d0)
+            # m moves by exactly the stored velocity
+            np.testing.assert_array_equal(m[sl], (m0[sl] - vel[sl].astype(np.float32)).astype(np.float32))
+        # v' = momentum v + lr g/|g|, then clipped to the maximum speed
+        gn = np.linalg.norm(g)
+        raw = cfg.clipup_momentum * v0 + cfg.lr * g / gn
+        scale = min(1.0, cfg.clipup_max_speed / np.linalg.norm(raw))
+        assert np.max(np.abs(vel - raw * scale)) <= 1e-5 * np.max(np.abs(raw * scale))
+        assert np.linalg.norm(vel) <= cfg.clipup_max_speed * (1 + 1e-5)
+
+
+@pytest.mark.parametrize("name", ["pgpe_shifted_sphere_d1m", "snes_shifted_sphere_d1m"])
+def test_per_dimension_sigma_strategies_full_size(name):
+    P = _P()
+    cfg = _workload(name)
+    es = P.ES(cfg)
+    twin = P.ES(cfg)
+    oc = to_oracle(cfg)
+    pdata = O.problem_data(oc)
+    for t in range(3):
+        sig0 = _np(es.strategy_state()[0])[0]
+        es.ask()
+        twin.ask()
+        f = _np(es.eval())
+        print("full-size", name, "t", t, flush=True)
+        np.testing.assert_array_equal(f, _np(twin.eval()))
+        _check_fitness(es, oc, t, pdata, f, sig=sig0)
+        es.tell(torch.tensor(f, device="cuda"))
+        twin.tell(torch.tensor(f, device="cuda"))
+        sig = _np(es.strategy_state()[0])[0]
+        np.testing.assert_array_equal(sig, _np(twin.strategy_state()[0])[0])
+        np.testing.assert_array_equal(_np(es.get_state()["m"]), _np(twin.get_state()["m"]))
+        assert np.all(np.isfinite(sig)) and np.all(sig > 0)
+        if cfg.strategy == P.STRAT_PGPE:
+            # the sigma step is clipped to max_change of the old sigma
+            r = sig.astype(np.float64) / sig0
+            assert np.all(r >= 1 - cfg.sigma_max_change - 1e-6) and np.all(r <= 1 + cfg.sigma_max_change + 1e-6)
+        else:
+            # sigma_d *= exp(sigma_lr/2 B_d) with |B_d| <= max(w) * P * max(z^2 - 1)
+            r = np.log(sig.astype(np.float64) / sig0)
+            assert np.all(np.abs(r) <= cfg.sigma_lr / 2 * 2 * 5.77 ** 2)
+
+
+def test_sepcma_full_size_sampled_and_elites():
+    P = _P()
+    cfg = _workload("sepcma_shifted_sphere_d1m")
+    es = P.ES(cfg)
+    oc = to_oracle(cfg)
+    pdata = O.problem_data(oc)
+    w = O.cma_weights(oc).astype(np.float32)
+    for t in range(2):
+        C = _np(es.strategy_state()[0])[0]
+        sg = float(es.get_hparams()[0][0])
+        es.ask()
+        f = _np(es.eval())
+        print("full-size sep-cma-es t", t, flush=True)
+        m = _np(es.get_state()["m"])[0]
+        ref = O.eval_members(dataclasses.replace(oc, sigma=sg), 0, t, m, pdata, np.array(MEMBERS),
+                             sig=O.cma_scale(oc.num_dims, sg, C))
+        got = f[0, MEMBERS]
+        assert np.all(np.abs(got - ref) <= 1e-5 * np.abs(ref)), (t, got, ref)
+        es.tell(torch.tensor(f, device="cuda"))
+        y, rk = es.shaped()
+        y, rk = _np(y)[0], _np(rk)[0]
+        np.testing.assert_array_equal(rk, O.ranks(f[0]))
+        np.testing.assert_array_equal(y, np.where(rk < len(w), w[np.minimum(rk, len(w) - 1)], np.float32(0)))
+        C1 = _np(es.strategy_state()[0])[0]
+        assert np.all(np.isfinite(C1)) and np.all(C1 > 0)
+        sg1 = float(es.get_hparams()[0][0])
+        assert np.isfinite(sg1) and sg1 > 0

@@ -183,3 +183,37 @@ def test_sepcma_full_size_sampled_and_elites():
         assert np.all(np.isfinite(C1)) and np.all(C1 > 0)
         sg1 = float(es.get_hparams()[0][0])
         assert np.isfinite(sg1) and sg1 > 0
+
+
+@pytest.mark.parametrize("name", ["sphere_d16", "rosenbrock_d1000", "rastrigin_r1024"])
+def test_run_workloads_full_size(name, monkeypatch):
+    """The es_run workloads at their full shapes: the first generation of
+    every run against the oracle, then es_run as the benchmark calls it (the
+    fused loop where the geometry takes it) bit-identical to per-call steps."""
+    P = _P()
+    from paper_2212_04180_amd import workloads
+    cfg, _ = workloads.get(name)
+    R = cfg.num_runs
+    es = P.ES(cfg)
+    ref = O.OracleES(to_oracle(cfg))
+    np.testing.assert_array_equal(_np(es.get_state()["m"]), ref.m)
+    es.ask()
+    f = _np(es.eval())
+    print("full-size", name, flush=True)
+    fr = ref.eval()
+    assert np.all(np.abs(f - fr) <= 1e-5 * np.maximum(np.abs(fr), 1e-30))
+    es.tell(torch.tensor(f, device="cuda"))
+    ref.tell(f)
+    m = _np(es.get_state()["m"])
+    assert np.max(np.abs(m - ref.m) / np.maximum(np.abs(ref.m), cfg.lr)) <= 1e-5
+    out = {}
+    for path in ("0", "1"):
+        monkeypatch.setenv("ESMI_RUN_PATH", path)
+        h = P.ES(cfg)
+        log = _np(h.run(12))
+        st = h.get_state()
+        bx, bf = h.best()
+        out[path] = (log, _np(st["m"]), _np(st["m1"]), _np(st["v"]), _np(bx), _np(bf))
+        assert log.shape == (12, R)
+    for a, b in zip(out["0"], out["1"]):
+        np.testing.assert_array_equal(a, b)

@@ -49,7 +49,7 @@ typedef enum {
     ES_ERR_SEQUENCE = -2,    /* call out of ask -> (eval) -> tell order        */
     ES_ERR_HIP = -3,         /* a HIP runtime call failed                     */
     ES_ERR_OOM = -4,         /* device allocation failed                      */
-    ES_ERR_UNSUPPORTED = -5  /* valid request this build does not implement   */
+    ES_ERR_UNSUPPORTED = -5  /* valid request the library does not implement  */
 } es_status;
 
 /* Fitness shaping (Sec. 3.2).  With key_j = f_j (minimise) or -f_j

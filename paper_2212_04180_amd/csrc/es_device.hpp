@@ -43,24 +43,43 @@ enum PhiloxLanes { LANES_BLOCK_AND_ROW = 0, LANES_ROW = 1, LANES_BLOCK = 2 };
 // Philox-4x32-10.  Each round forms two 32x32->64 products and folds the high
 // halves with the other words and the round key through one three-input xor
 // (v_bitop3_b32, truth table 0x96).  The key is uniform across a wavefront,
-// so the key schedule lives in scalar registers.  In the first two rounds
-// some products only involve uniform words; those are left to the compiler,
-// which runs them on the scalar unit, and every lane-varying product is one
-// v_mad_u64_u32.
+// so the key schedule lives in scalar registers.  In the first rounds some
+// words only depend on uniform inputs (the generation, the domain, and the
+// block or the row when it is the same across the wavefront): those products
+// and xors are written as plain integer arithmetic, which the compiler runs
+// on the scalar unit, and every lane-varying product is one v_mad_u64_u32.
+//
+// Uniformity of the counter words at the start of round i for lane layout V:
+// bit k set = word k is the same across the wavefront.
+template <int V>
+struct PhiloxUniform {
+    static constexpr unsigned at(int i)
+    {
+        // round 0: the block (word 0) varies unless V == LANES_ROW, the row
+        // (word 1) unless V == LANES_BLOCK; t and the domain never vary
+        unsigned u = (V == LANES_ROW ? 1u : 0u) | (V == LANES_BLOCK ? 2u : 0u) | 4u | 8u;
+        for (int r = 0; r < i; ++r) {
+            const bool p0 = u & 1u, p1 = u & 4u;             // products of words 0 and 2
+            const bool n0 = p1 && (u & 2u), n2 = p0 && (u & 8u);
+            u = (n0 ? 1u : 0u) | (p1 ? 2u : 0u) | (n2 ? 4u : 0u) | (p0 ? 8u : 0u);
+        }
+        return u;
+    }
+};
+
 template <int V = LANES_BLOCK_AND_ROW>
 __device__ __forceinline__ uint4 philox4x32_10(uint32_t k0, uint32_t k1, uint32_t c0, uint32_t c1,
                                                uint32_t c2, uint32_t c3)
 {
 #pragma unroll
     for (int i = 0; i < 10; ++i) {
-        // round 0: c0 = block varies unless V == LANES_ROW; c2 = t is uniform.
-        // round 1: c0 depends on the row, c2 on the block.
-        const bool vary0 = i >= 2 || (i == 0 && V != LANES_ROW) || (i == 1 && V != LANES_BLOCK);
-        const bool vary2 = i >= 2 || (i == 1 && V != LANES_ROW);
-        const uint64_t p0 = vary0 ? mul_wide(c0, 0xD2511F53u) : (uint64_t)0xD2511F53u * c0;
-        const uint64_t p1 = vary2 ? mul_wide(c2, 0xCD9E8D57u) : (uint64_t)0xCD9E8D57u * c2;
-        const uint32_t n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), c1, k0, 0x96);
-        const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), c3, k1, 0x96);
+        const unsigned u = PhiloxUniform<V>::at(i);
+        const bool u0 = u & 1u, u1 = u & 2u, u2 = u & 4u, u3 = u & 8u;
+        const uint64_t p0 = u0 ? (uint64_t)0xD2511F53u * c0 : mul_wide(c0, 0xD2511F53u);
+        const uint64_t p1 = u2 ? (uint64_t)0xCD9E8D57u * c2 : mul_wide(c2, 0xCD9E8D57u);
+        const uint32_t h1 = (uint32_t)(p1 >> 32), h0 = (uint32_t)(p0 >> 32);
+        const uint32_t n0 = u2 && u1 ? h1 ^ c1 ^ k0 : __builtin_amdgcn_bitop3_b32(h1, c1, k0, 0x96);
+        const uint32_t n2 = u0 && u3 ? h0 ^ c3 ^ k1 : __builtin_amdgcn_bitop3_b32(h0, c3, k1, 0x96);
         c1 = (uint32_t)p1;
         c3 = (uint32_t)p0;
         c0 = n0;

@@ -315,8 +315,10 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
     accm = L.accm;
 }
 
+// Eight waves per SIMD (two 16-wave workgroups per CU): the compiler then
+// keeps the kernel within the scalar register budget of that occupancy.
 template <int PROB, int SM>
-__global__ __launch_bounds__(EVAL_MAX_WG) void k_eval_bbob(
+__global__ __launch_bounds__(EVAL_MAX_WG) __attribute__((amdgpu_waves_per_eu(8, 8))) void k_eval_bbob(
     const float* __restrict__ m, const float* __restrict__ pdata, float* __restrict__ partial,
     uint64_t seed, uint32_t t, int64_t D, int64_t nb, int32_t N, int32_t P, int64_t bc, int64_t nchunks,
     int32_t n_pg, const float* __restrict__ hp, float ra, const float* __restrict__ svec)

@@ -705,26 +705,32 @@ __device__ __forceinline__ void tell_slice2(const float* __restrict__ ar, const 
 }
 
 // g = sum / (N sigma), then Adam (Kingma & Ba) in fp32 in a fixed operation
-// order on four dims; dims at or beyond D stay zero.
+// order on one dim; a dim at or beyond D stays zero.
+__device__ __forceinline__ void adam_dim(double a64, double inv_ns, const AdamConsts& ac, float lr, int64_t d,
+                                         int64_t D, float mo, float m1o, float vo, float& mn, float& m1n,
+                                         float& vn, float& gg)
+{
+    const float g = (float)(a64 * inv_ns);
+    gg = g;
+    const float nm1 = __builtin_fmaf(ac.beta1, m1o, __fmul_rn(ac.omb1, g));
+    const float nv = __builtin_fmaf(ac.beta2, vo, __fmul_rn(ac.omb2, __fmul_rn(g, g)));
+    const float mhat = nm1 / ac.bc1;
+    const float vhat = nv / ac.bc2;
+    const float den = __fadd_rn(sqrtf(vhat), ac.eps);
+    const float q = mhat / den;
+    mn = __builtin_fmaf(-lr, q, mo);
+    m1n = nm1;
+    vn = nv;
+    if (d >= D) { mn = 0.f; m1n = 0.f; vn = 0.f; gg = 0.f; }
+}
+
+// The same on the four dims of a Philox block.
 __device__ __forceinline__ void adam_block(const double a64[4], double inv_ns, const AdamConsts& ac, float lr, int64_t d0,
                                            int64_t D, const float mo[4], const float m1o[4], const float vo[4],
                                            float mn[4], float m1n[4], float vn[4], float gg[4])
 {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const float g = (float)(a64[k] * inv_ns);
-        gg[k] = g;
-        const float nm1 = __builtin_fmaf(ac.beta1, m1o[k], __fmul_rn(ac.omb1, g));
-        const float nv = __builtin_fmaf(ac.beta2, vo[k], __fmul_rn(ac.omb2, __fmul_rn(g, g)));
-        const float mhat = nm1 / ac.bc1;
-        const float vhat = nv / ac.bc2;
-        const float den = __fadd_rn(sqrtf(vhat), ac.eps);
-        const float q = mhat / den;
-        mn[k] = __builtin_fmaf(-lr, q, mo[k]);
-        m1n[k] = nm1;
-        vn[k] = nv;
-        if (d0 + k >= D) { mn[k] = 0.f; m1n[k] = 0.f; vn[k] = 0.f; gg[k] = 0.f; }
-    }
+    for (int k = 0; k < 4; ++k) adam_dim(a64[k], inv_ns, ac, lr, d0 + k, D, mo[k], m1o[k], vo[k], mn[k], m1n[k], vn[k], gg[k]);
 }
 
 // Everything the gradient kernels need besides the geometry.
@@ -1216,33 +1222,51 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             keys[j] = order_key(f, a.maximize);
         }
         __syncthreads();
-        // centered ranks, weights, best-so-far and the generation's log entry
-        for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) {
-            const uint32_t K = keys[j];
-            int32_t rk = 0, k = 0;
-#pragma unroll 4
-            for (; k + 4 <= a.N; k += 4) {
-                const uint4 q4 = *reinterpret_cast<const uint4*>(keys + k);
-                rk += (q4.x < K) | ((q4.x == K) & (k < j));
-                rk += (q4.y < K) | ((q4.y == K) & (k + 1 < j));
-                rk += (q4.z < K) | ((q4.z == K) & (k + 2 < j));
-                rk += (q4.w < K) | ((q4.w == K) & (k + 3 < j));
-            }
-            for (; k < a.N; ++k) rk += (keys[k] < K) | ((keys[k] == K) & (k < j));
-            y[j] = a.raw ? (a.maximize ? -fit[j] : fit[j]) : tab[rk];
-            if (rk == 0) {
-                if (a.log) a.log[(int64_t)it * a.R + r] = fit[j];
-                if (K < best_k) {
-                    best_k = K;
-                    best_fv = fit[j];
-                    best_j = j;
-                } else {
-                    best_j = -1;
+        // centered ranks, the folded weights, best-so-far and the generation's
+        // log entry.  Eight lanes per pair: lanes 4*mem + q count the keys of
+        // slice q below member p + mem*P (ties by index); the quad adds its
+        // counts and the two members' weights meet across the group.
+        {
+            const int32_t cs = ((a.N + 15) / 16) * 4;  // keys per slice, a multiple of 4
+            const int32_t lg = threadIdx.x & 7, mem = lg >> 2, q = lg & 3;
+            for (int32_t pb = 0; pb < a.P; pb += FUSED_WG / 8) {
+                const int32_t p = pb + (int32_t)(threadIdx.x >> 3);
+                int32_t rk = 0, j = 0;
+                uint32_t K = 0;
+                if (p < a.P) {
+                    j = p + mem * a.P;
+                    K = keys[j];
+                    const int32_t s0 = q * cs, s1 = s0 + cs < a.N ? s0 + cs : a.N;
+                    int32_t k = s0;
+                    for (; k + 4 <= s1; k += 4) {
+                        const uint4 q4 = *reinterpret_cast<const uint4*>(keys + k);
+                        rk += (q4.x < K) | ((q4.x == K) & (k < j));
+                        rk += (q4.y < K) | ((q4.y == K) & (k + 1 < j));
+                        rk += (q4.z < K) | ((q4.z == K) & (k + 2 < j));
+                        rk += (q4.w < K) | ((q4.w == K) & (k + 3 < j));
+                    }
+                    for (; k < s1; ++k) rk += (keys[k] < K) | ((keys[k] == K) & (k < j));
+                }
+                // every lane of the wave takes part in the exchanges
+                rk += __shfl_xor(rk, 1);
+                rk += __shfl_xor(rk, 2);
+                const float yj = p < a.P ? (a.raw ? (a.maximize ? -fit[j] : fit[j]) : tab[rk]) : 0.f;
+                const float yo = __shfl_xor(yj, 4);
+                if (p < a.P && q == 0) {
+                    if (mem == 0) wf[p] = yj - yo;
+                    if (rk == 0) {
+                        if (a.log) a.log[(int64_t)it * a.R + r] = fit[j];
+                        if (K < best_k) {
+                            best_k = K;
+                            best_fv = fit[j];
+                            best_j = j;
+                        } else {
+                            best_j = -1;
+                        }
+                    }
                 }
             }
         }
-        __syncthreads();
-        for (int32_t p = threadIdx.x; p < a.P; p += blockDim.x) wf[p] = y[p] - y[p + a.P];
         __syncthreads();
         // tell: items (block, pair slice), slices summed in order, then Adam
         for (int64_t i = threadIdx.x; i < (int64_t)a.ps * a.nb; i += blockDim.x) {
@@ -1258,37 +1282,19 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         __syncthreads();
         const int32_t jb = best_j;
         const double inv_ns = 1.0 / (2.0 * (double)a.P * (double)sigma);  // 1 / (N sigma)
-        for (int64_t b = threadIdx.x; b < a.nb; b += blockDim.x) {
-            // slices in order, the four dims' chains side by side
-            const double4 r0 = *reinterpret_cast<const double4*>(red + b * 4);
-            double a64[4] = {r0.x, r0.y, r0.z, r0.w};
-            for (int q = 1; q < a.ps; ++q) {
-                const double4 rq = *reinterpret_cast<const double4*>(red + ((int64_t)q * a.nb + b) * 4);
-                a64[0] += rq.x;
-                a64[1] += rq.y;
-                a64[2] += rq.z;
-                a64[3] += rq.w;
-            }
-            float mo[4], m1o[4], vo[4], mn[4], m1n[4], vn[4], gg[4];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                mo[k] = ms[4 * b + k];
-                m1o[k] = m1s[4 * b + k];
-                vo[k] = vs[4 * b + k];
-            }
-            adam_block(a64, inv_ns, ac, lr, 4 * b, a.D, mo, m1o, vo, mn, m1n, vn, gg);
+        for (int64_t i = threadIdx.x; i < 4 * a.nb; i += blockDim.x) {
+            // one dim per lane: the slices in order, then Adam
+            double s64 = red[i];
+            for (int q = 1; q < a.ps; ++q) s64 += red[(int64_t)q * 4 * a.nb + i];
+            const float mo = ms[i];
+            float mn, m1n, vn, gg;
+            adam_dim(s64, inv_ns, ac, lr, i, a.D, mo, m1s[i], vs[i], mn, m1n, vn, gg);
             // a new best: keep the mean it was sampled around; its noise is
             // added once, after the loop (same arithmetic as the per-call path)
-            if (jb >= 0) {
-#pragma unroll
-                for (int k = 0; k < 4; ++k) a.best_x[goff + 4 * b + k] = mo[k];
-            }
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                ms[4 * b + k] = mn[k];
-                m1s[4 * b + k] = m1n[k];
-                vs[4 * b + k] = vn[k];
-            }
+            if (jb >= 0) a.best_x[goff + i] = mo;
+            ms[i] = mn;
+            m1s[i] = m1n;
+            vs[i] = vn;
         }
         if (jb >= 0 && threadIdx.x == 0) {
             best_t = t;

@@ -84,6 +84,32 @@ def test_deterministic_and_fused_equals_per_call():
         np.testing.assert_array_equal(_np(a.get_state()[k]), _np(c.get_state()[k]))
 
 
+@pytest.mark.parametrize("D,N,R,prob", [(5, 6, 3, "sphere"), (16, 34, 2, "rastrigin"), (37, 64, 5, "sphere"),
+                                        (3, 2, 1, "rastrigin")])
+def test_fused_loop_equals_per_call_with_ties(D, N, R, prob, monkeypatch):
+    """With the mean at 0 on a symmetric problem every antithetic pair ties in
+    the first generation, so ranks are decided by index: the fused loop's
+    sliced rank count and its per-dimension Adam give the per-call bits."""
+    P = _P()
+    cfg = P.ESConfig(num_dims=D, popsize=N, num_runs=R, sigma=0.3, lr=0.05, seed=12, init=P.INIT_ZERO,
+                     problem=P.PROB_SPHERE if prob == "sphere" else P.PROB_RASTRIGIN)
+    out = {}
+    for path in ("1", "2"):
+        monkeypatch.setenv("ESMI_RUN_PATH", path)
+        es = P.ES(cfg)
+        log = _np(es.run(10))
+        st = es.get_state()
+        bx, bf = es.best()
+        out[path] = (log, _np(st["m"]), _np(st["m1"]), _np(st["v"]), _np(bx), _np(bf))
+    for a, b in zip(out["1"], out["2"]):
+        np.testing.assert_array_equal(a, b)
+    # the first generation really ties: f(m + s) = f(m - s) at m = 0
+    es = P.ES(cfg)
+    es.ask()
+    f = _np(es.eval())
+    np.testing.assert_array_equal(f[:, : N // 2], f[:, N // 2:])
+
+
 def test_best_so_far_tracks_rank0_member():
     P = _P()
     cfg = P.ESConfig(num_dims=16, popsize=32, sigma=0.1, lr=0.01, seed=0, problem=P.PROB_SPHERE)

@@ -1285,6 +1285,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         for (int64_t i = threadIdx.x; i < 4 * a.nb; i += blockDim.x) {
             // one dim per lane: the slices in order, then Adam
             double s64 = red[i];
+#pragma unroll 4
             for (int q = 1; q < a.ps; ++q) s64 += red[(int64_t)q * 4 * a.nb + i];
             const float mo = ms[i];
             float mn, m1n, vn, gg;

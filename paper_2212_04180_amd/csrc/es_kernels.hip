@@ -1388,6 +1388,13 @@ EvalPlan eval_plan(const Geometry& g, int64_t bc_override)
         if (nch < 1) nch = 1;
         bc = (g.nb + nch - 1) / nch;
         if (bc < EVAL_FOLD) bc = EVAL_FOLD;
+        // a small run: chunks short enough that the fused loop's workgroup
+        // takes every (pair, chunk) item at once
+        if ((int64_t)g.P * g.nb <= (int64_t)FUSED_WG * EVAL_FOLD) {
+            const int64_t per = FUSED_WG / g.P > 1 ? FUSED_WG / g.P : 1;  // chunks per pair in one pass
+            const int64_t bs = (g.nb + per - 1) / per;
+            if (bs < bc) bc = bs;
+        }
     }
     if (bc > g.nb) bc = g.nb;
     e.bc = bc;
@@ -1583,6 +1590,8 @@ int32_t tell_slices(const Geometry& g)
     const int64_t groups = (g.nb + TELL_LANES - 1) / TELL_LANES * g.R;
     int64_t ps = (4096 + groups - 1) / groups;
     if (ps < 4) ps = 4;
+    // small runs: enough slices to keep a fused-loop workgroup's lanes busy
+    if (ps * g.nb < FUSED_WG) ps = FUSED_WG / g.nb;
     if (ps > TELL_MAX_PS) ps = TELL_MAX_PS;
     if (ps > g.P) ps = g.P;
     // round up to a slice count that splits the pairs into whole groups

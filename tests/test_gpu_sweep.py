@@ -1,0 +1,58 @@
+"""Seeded random configurations of every strategy, optimiser, problem and
+shaping on the GPU (marked gpu), three generations each, stage by stage
+against the oracle (the bars of the per-strategy tests, via stagecheck).
+
+The sizes are drawn log-uniformly (D from 1 to 20000, N even from 2 to 512,
+R from 1 to 4) and capped so that the oracle finishes each case in about a
+second; they land on every remainder of D modulo the Philox block and on
+pair counts that are and are not whole pair groups."""
+import numpy as np
+import pytest
+
+import stagecheck
+
+pytestmark = pytest.mark.gpu
+
+CASES = 48
+
+
+def _P():
+    import paper_2212_04180_amd as P
+    return P
+
+
+def _draw(i):
+    P = _P()
+    rng = np.random.default_rng(1000 + i)
+    while True:
+        D = int(np.exp(rng.uniform(0.0, np.log(20000.0))))
+        N = 2 * int(np.exp(rng.uniform(0.0, np.log(256.0))))
+        R = int(rng.integers(1, 5))
+        if R * N * D <= 3_000_000:
+            break
+    strategy = int(rng.integers(0, 4))
+    optimizer = int(rng.integers(0, 2)) if strategy in (P.STRAT_OPENAI_ES, P.STRAT_PGPE) else P.OPT_ADAM
+    problem = int(rng.integers(P.PROB_SPHERE, P.PROB_RASTRIGIN + 1))
+    shaping = int(rng.integers(0, 3))
+    decay = bool(rng.integers(0, 2))
+    kw = dict(num_dims=D, popsize=N, num_runs=R, sigma=float(rng.uniform(0.05, 0.5)),
+              lr=float(rng.uniform(0.005, 0.05)), seed=int(rng.integers(0, 1 << 40)), init_lo=-2.0, init_hi=2.0,
+              problem=problem, strategy=strategy, optimizer=optimizer, shaping=shaping,
+              maximize=int(rng.integers(0, 2)), sigma_lr=0.2, sigma_max_change=0.2, clipup_max_speed=0.3,
+              clipup_momentum=0.9, snes_temperature=12.0, elite_ratio=float(rng.uniform(0.2, 0.6)),
+              flags=P.FLAG_KEEP_GRAD)
+    if decay:
+        kw.update(sigma_decay=0.95, sigma_final=0.02, lr_decay=0.9, lr_final=0.001)
+    if strategy == P.STRAT_SNES:
+        kw.update(lr=1.0, sigma_lr=0.3)
+    if strategy == P.STRAT_SEP_CMA:
+        kw.update(lr=0.0, sigma_decay=1.0, sigma_final=0.0)
+    return P.ESConfig(**kw)
+
+
+@pytest.mark.parametrize("i", range(CASES))
+def test_random_configuration_matches_oracle(i):
+    P = _P()
+    cfg = _draw(i)
+    print("case", i, cfg, flush=True)
+    stagecheck.run(P, cfg, 3)

@@ -29,8 +29,8 @@ namespace {
 constexpr int EVAL_MAX_WG = 1024; // lanes = antithetic pairs
 constexpr int EVAL_FOLD = 4;      // Philox blocks summed in fp32 before the fp64 fold
 constexpr int RED_SLICES = 16;    // chunk slices per member in the partial reduce
-constexpr int RANK_PAIRS = 16;    // pairs per rank workgroup
-constexpr int RANK_SLICES = 16;   // key slices per pair
+constexpr int RANK_PAIRS = 4;     // pairs per rank workgroup
+constexpr int RANK_SLICES = 64;   // key slices per pair
 constexpr int TELL_LANES = 64;    // Philox blocks per tell workgroup
 constexpr int TELL_MAX_PS = 16;   // pair slices per tell workgroup (one wave each)
 constexpr int TELL_GROUP = 16;    // fp32 pairs folded into the fp64 sum at once
@@ -458,8 +458,28 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
     const int32_t r = blockIdx.y;
     const float* __restrict__ fr = fit + (int64_t)r * N;
     const float* __restrict__ pr = sa.pen ? sa.pen + (int64_t)r * N : nullptr;
-    for (int32_t k = threadIdx.x; k < N; k += blockDim.x)
-        keys[k] = order_key(shaped_key(fr[k], pr ? pr[k] : 0.0f, sa.maximize, sa.w_decay), 0);
+    // this workgroup's own members, fetched first (used after the count)
+    const int32_t tx = threadIdx.x % RANK_PAIRS, s = threadIdx.x / RANK_PAIRS;
+    const int32_t p = blockIdx.x * RANK_PAIRS + tx;
+    const bool valid = p < P;
+    const int32_t j1 = valid ? p : 0, j2 = j1 + P;
+    const float f1 = fr[j1], f2 = fr[j2];
+    // the run's keys: eight loads per lane in flight at once
+    constexpr int KU = 8;
+    for (int32_t k0 = threadIdx.x; k0 < N; k0 += KU * (int32_t)blockDim.x) {
+        float fv[KU], pv[KU];
+#pragma unroll
+        for (int u = 0; u < KU; ++u) {
+            const int32_t k = k0 + u * (int32_t)blockDim.x;
+            fv[u] = k < N ? fr[k] : 0.0f;
+            pv[u] = pr && k < N ? pr[k] : 0.0f;
+        }
+#pragma unroll
+        for (int u = 0; u < KU; ++u) {
+            const int32_t k = k0 + u * (int32_t)blockDim.x;
+            if (k < N) keys[k] = order_key(shaped_key(fv[u], pv[u], sa.maximize, sa.w_decay), 0);
+        }
+    }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         sa.hp_next[r] = schedule_step(sa.hp_cur[r], sa.sigma_decay, sa.sigma_final);
         sa.hp_next[R + r] = schedule_step(sa.hp_cur[R + r], sa.lr_decay, sa.lr_final);
@@ -520,10 +540,6 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
         __syncthreads();
     }
 
-    const int32_t tx = threadIdx.x % RANK_PAIRS, s = threadIdx.x / RANK_PAIRS;
-    const int32_t p = blockIdx.x * RANK_PAIRS + tx;
-    const bool valid = p < P;
-    const int32_t j1 = valid ? p : 0, j2 = j1 + P;
     const uint32_t K1 = keys[j1], K2 = keys[j2];
     const int32_t kb = (int32_t)(((int64_t)N * s) / RANK_SLICES);
     const int32_t ke = (int32_t)(((int64_t)N * (s + 1)) / RANK_SLICES);
@@ -556,7 +572,6 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
         r1 += cnt[q][tx][0];
         r2 += cnt[q][tx][1];
     }
-    const float f1 = fr[j1], f2 = fr[j2];
     float y1, y2;
     if (sa.shaping == ES_SHAPE_RAW) {
         // the key itself; without weight decay the fitness keeps its NaN and sign of zero
@@ -591,11 +606,12 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
         jb = r1 == 0 ? j1 : j2;
     }
     if (jb >= 0) {
-        const uint32_t kb0 = order_key(fr[jb], sa.maximize);
-        if (gen_best) gen_best[r] = fr[jb];
+        const float fb = jb == j1 ? f1 : f2;
+        const uint32_t kb0 = order_key(fb, sa.maximize);
+        if (gen_best) gen_best[r] = fb;
         if (kb0 < best_okey[r]) {
             best_okey[r] = kb0;
-            best_f[r] = fr[jb];
+            best_f[r] = fb;
             best_j[r] = jb;
         } else {
             best_j[r] = -1;

@@ -178,10 +178,7 @@ const char* validate(const es_config& c)
     return nullptr;
 }
 
-// Shaping weight of rank k.  Centered ranks: the fp32 quotient
-// (2k - (N-1)) / (2(N-1)).  SNES: the softmax utility of rank' = N-1-k,
-// exp(beta (rank'/N - 1/2)) / sum, in fp64 rounded once.  Returns the
-// table's fp64 mean.
+// Sep-CMA-ES parent count: max(1, floor(elite_ratio N)).
 int32_t cma_mu(const es_config& c)
 {
     const int32_t mu = (int32_t)std::floor((double)c.elite_ratio * (double)c.popsize);
@@ -220,6 +217,10 @@ CmaConsts cma_consts(const es_config& c, std::vector<double>& w)
     return k;
 }
 
+// Shaping weight of rank k.  Centered ranks: the fp32 quotient
+// (2k - (N-1)) / (2(N-1)).  SNES: the softmax utility of rank' = N-1-k,
+// exp(beta (rank'/N - 1/2)) / sum, in fp64 rounded once.  Sep-CMA-ES: the
+// recombination weight of rank k < mu, else 0.  Returns the table's fp64 mean.
 double weight_table(const es_config& c, int32_t N, float* out)
 {
     if (c.strategy == ES_STRAT_SEP_CMA) {

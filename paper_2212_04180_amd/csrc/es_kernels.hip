@@ -920,7 +920,9 @@ __device__ __forceinline__ double tell_finish(const TellArgs& a, const double a6
 template <bool TWO, bool ROWS = false>
 __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
 {
-    __shared__ double red[TELL_MAX_PS - 1][TELL_LANES][TWO ? 8 : 4];
+    // slices 1 .. ps-1 of every lane, sized by the launch: [ps-1][TELL_LANES][W]
+    extern __shared__ double red[];
+    constexpr int W = TWO ? 8 : 4;
     const int32_t r = blockIdx.y, z = blockIdx.z;
     const int32_t tx = threadIdx.x % TELL_LANES;
     // one wave per pair slice: make the slice index (and the pair loop) uniform
@@ -944,8 +946,8 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
     if (s > 0) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            red[s - 1][tx][k] = a64[k];
-            if constexpr (TWO) red[s - 1][tx][4 + k] = b64[k];
+            red[((s - 1) * TELL_LANES + tx) * W + k] = a64[k];
+            if constexpr (TWO) red[((s - 1) * TELL_LANES + tx) * W + 4 + k] = b64[k];
         }
     }
     __syncthreads();
@@ -953,8 +955,8 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
     for (int q = 0; q < a.ps - 1; ++q)
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            a64[k] += red[q][tx][k];
-            if constexpr (TWO) b64[k] += red[q][tx][4 + k];
+            a64[k] += red[(q * TELL_LANES + tx) * W + k];
+            if constexpr (TWO) b64[k] += red[(q * TELL_LANES + tx) * W + 4 + k];
         }
     if (a.nsplit > 1) {
         if (b < a.nb) {
@@ -1547,9 +1549,10 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp
     if (!clipup && !cma) a.gpart = nullptr;
     const int64_t groups = (g.nb + TELL_LANES - 1) / TELL_LANES;
     const dim3 grid((unsigned)groups, (unsigned)g.R, (unsigned)tp.nsplit);
-    if (cma) k_tell<true, true><<<grid, TELL_LANES * tp.ps, 0, s>>>(a);
-    else if (two) k_tell<true><<<grid, TELL_LANES * tp.ps, 0, s>>>(a);
-    else k_tell<false><<<grid, TELL_LANES * tp.ps, 0, s>>>(a);
+    const size_t lds = sizeof(double) * (size_t)(tp.ps - 1) * TELL_LANES * (two || cma ? 8 : 4);
+    if (cma) k_tell<true, true><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
+    else if (two) k_tell<true><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
+    else k_tell<false><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const dim3 fgrid((unsigned)((g.nb + 255) / 256), (unsigned)g.R);

@@ -1,17 +1,27 @@
-// es_kernels.hip -- gfx950 kernels of one batched OpenAI-ES generation.
+// es_kernels.hip -- gfx950 kernels of one batched ES generation (OpenAI-ES,
+// and the PGPE, SNES and Sep-CMA-ES strategies of Table 1 on the same path).
 //
-//   k_init          initial mean (Listing 1 initialize), zero Adam moments
-//   k_problem_data  shift vector / teacher network from the base seed
-//   k_ask           optional materialised population (Sec. 2.1 ask)
-//   k_eval_bbob     fused sample + evaluate (Sec. 2.1 evaluate) for the
-//                   benchmark problems; lane = antithetic pair, D chunked
-//   k_eval_reduce   fixed-order sum of the per-chunk partials -> fitness
-//   k_rank          centered ranks with index tie-break (Sec. 3.2), weights,
-//                   antithetic fold, best-so-far bookkeeping
-//   k_tell          FD gradient estimate g = E^T y / (N sigma) (Sec. 2.1) with
-//                   the noise regenerated, fused with the Adam step; lane = a
-//                   Philox block of four dims
-//   k_debug_noise   raw words and normals of one stream (diagnostics)
+//   k_init            initial mean (Listing 1 initialize), zero Adam moments
+//   k_problem_data    shift vector / teacher network from the base seed
+//   k_fill_rows       per-dimension state rows (sigma vector, C) at init
+//   k_ask             optional materialised population (Sec. 2.1 ask)
+//   k_eval_bbob       fused sample + evaluate (Sec. 2.1 evaluate) for the
+//                     benchmark problems; lane = antithetic pair (or member
+//                     pair for independent sampling), D chunked
+//   k_eval_reduce     fixed-order sum of the per-chunk partials -> fitness
+//   k_rank            fitness shaping (Sec. 3.2): centered ranks with index
+//                     tie-break, raw keys, z-scores, weight decay, the rank
+//                     tables of SNES and Sep-CMA-ES; antithetic fold,
+//                     best-so-far, the schedule step of sigma and lr
+//   k_tell            noise sums over the pairs regenerated per Philox block
+//                     (g = E^T y / (N sigma) for OpenAI-ES, Sec. 2.1), fused
+//                     with the strategy's update; lane = a block of four dims
+//   k_tell_fold       the split gradient's partial sums in split order, then
+//                     the update
+//   k_clipup_velocity, k_clipup_apply   ClipUp's two norm passes
+//   k_sepcma_finish, k_cma_scale        Sep-CMA-ES second pass, sampling scale
+//   k_run_fused       T whole generations in one launch for small runs
+//   k_debug_noise     raw words and normals of one stream (diagnostics)
 //
 // Every reduction runs in a fixed order (no floating-point atomics), so a
 // launch is bit-reproducible.  Perturbation sums use short fp32 chains folded

@@ -1595,9 +1595,10 @@ TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit)
     if (fused_path) return tp;  // the fused loop sums all slices in one workgroup
     // Few block groups (under four workgroups per CU) leave the CUs unevenly
     // loaded; then split each group's pairs over more, smaller workgroups
-    // (four slices each), as long as every slice keeps two whole pair groups.
+    // (four slices each; about 1024 workgroups, which all fit on the chip at
+    // once), as long as every slice keeps two whole pair groups.
     const int64_t groups = (g.nb + TELL_LANES - 1) / TELL_LANES * g.R;
-    int64_t nsplit = force_nsplit > 0 ? force_nsplit : groups >= 1024 ? 1 : (1024 + groups - 1) / groups;
+    int64_t nsplit = force_nsplit > 0 ? force_nsplit : groups >= 1024 ? 1 : (1024 + groups / 2) / groups;
     while (nsplit > 1 && g.P / (4 * nsplit) < 2 * TELL_GROUP) --nsplit;
     if (nsplit <= 1 || nsplit > 65535) return tp;
     tp.ps = 4;

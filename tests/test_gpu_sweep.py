@@ -56,3 +56,39 @@ def test_random_configuration_matches_oracle(i):
     cfg = _draw(i)
     print("case", i, cfg, flush=True)
     stagecheck.run(P, cfg, 3)
+
+
+def _draw_fused(i):
+    P = _P()
+    rng = np.random.default_rng(2000 + i)
+    D = int(np.exp(rng.uniform(0.0, np.log(400.0))))
+    N = 2 * int(np.exp(rng.uniform(0.0, np.log(96.0))))
+    R = int(rng.integers(1, 9))
+    kw = dict(num_dims=D, popsize=N, num_runs=R, sigma=float(rng.uniform(0.05, 0.5)),
+              lr=float(rng.uniform(0.005, 0.05)), seed=int(rng.integers(0, 1 << 40)), init_lo=-2.0, init_hi=2.0,
+              problem=int(rng.integers(P.PROB_SPHERE, P.PROB_RASTRIGIN + 1)), shaping=int(rng.integers(0, 2)),
+              maximize=int(rng.integers(0, 2)))
+    if rng.integers(0, 2):
+        kw.update(sigma_decay=0.97, sigma_final=0.05, lr_decay=0.95, lr_final=0.002)
+    return P.ESConfig(**kw)
+
+
+@pytest.mark.parametrize("i", range(16))
+def test_random_fused_loop_equals_per_call(i, monkeypatch):
+    """es_run through the fused loop (forced) and through the per-call kernels
+    give the same bits: log, mean, moments, best-so-far, sigma and lr."""
+    import torch
+    P = _P()
+    cfg = _draw_fused(i)
+    print("case", i, cfg, flush=True)
+    out = {}
+    for path in ("1", "2"):
+        monkeypatch.setenv("ESMI_RUN_PATH", path)
+        es = P.ES(cfg)
+        log = es.run(7)
+        st = es.get_state()
+        bx, bf = es.best()
+        torch.cuda.synchronize()
+        out[path] = [t.cpu().numpy() for t in (log, st["m"], st["m1"], st["v"], bx, bf)] + list(es.get_hparams())
+    for a, b in zip(out["1"], out["2"]):
+        np.testing.assert_array_equal(a, b)

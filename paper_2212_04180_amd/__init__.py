@@ -1,4 +1,5 @@
-"""MI355X-native batched OpenAI-ES generation (ask / evaluate / tell).
+"""MI355X-native batched ES generations (ask / evaluate / tell): OpenAI-ES, PGPE,
+SNES and Sep-CMA-ES.
 
 The hot path is the HIP library ``libesmi.so`` (C-ABI in ``include/esmi.h``);
 this package is its thin Python binding and the synthetic workload presets.

@@ -1,8 +1,9 @@
 /*
- * esmi.h -- C-ABI of the MI355X (gfx950) OpenAI-ES generation library.
+ * esmi.h -- C-ABI of the MI355X (gfx950) evolution-strategy generation library.
  *
  * The library runs the ask / evaluate / tell loop of the evosax report
  * (arXiv 2212.04180, Sec. 2.1, Listing 1) for OpenAI-ES (Table 1, FDG class)
+ * -- and PGPE, SNES and Sep-CMA-ES on the same path (es_strategy below) --
  * on R independent runs at once (the vmap over seeds of Sec. 2.2, Listing 3):
  *   ask      antithetic Gaussian perturbations x = m +- sigma*eps, eps drawn
  *            from a counter-based Philox-4x32-10 stream and regenerated on
@@ -12,7 +13,7 @@
  *   tell     fitness shaping (Sec. 3.2: centered ranks as in App. B,
  *            z-scores, weight-decay regularisation), the finite-difference
  *            gradient estimate of Sec. 2.1, g = E^T y / (N sigma), and an
- *            Adam step on the mean (App. B); sigma and the learning rate
+ *            Adam (or ClipUp) step on the mean (App. B); sigma and the learning rate
  *            then follow the exponential schedules of the App. B tables,
  *            per run (the vmap over hyper-parameters of Sec. 2.2).
  *

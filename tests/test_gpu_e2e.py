@@ -234,3 +234,32 @@ def test_fused_loop_matches_per_call_bits(prob, D, N, R, T, monkeypatch):
         out[path] = (log, _np(st["m"]), _np(st["m1"]), _np(st["v"]), _np(bx), _np(bf), st["t"])
     for a, b in zip(out["1"], out["2"]):
         np.testing.assert_array_equal(a, b)
+
+
+def test_two_handles_on_their_own_streams():
+    """Handles are independent: two runs interleaved on two streams give the
+    bits of each run alone on the default stream."""
+    P = _P()
+    cfgs = [P.ESConfig(num_dims=300, popsize=64, num_runs=2, sigma=0.1, lr=0.01, seed=70 + i, init_lo=-2.0,
+                       init_hi=2.0, problem=P.PROB_RASTRIGIN if i else P.PROB_ROSENBROCK) for i in range(2)]
+    solo = []
+    for cfg in cfgs:
+        es = P.ES(cfg)
+        for _ in range(6):
+            es.step()
+        solo.append(_np(es.get_state()["m"]))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    hs = [P.ES(cfg, stream=s) for cfg, s in zip(cfgs, streams)]
+    for _ in range(6):
+        for h, s in zip(hs, streams):
+            with torch.cuda.stream(s):
+                f = torch.empty((h.R, h.N), device="cuda")
+                h.ask()
+                h.eval(f)
+                h.tell(f)
+    torch.cuda.synchronize()
+    for h, s, ref in zip(hs, streams, solo):
+        with torch.cuda.stream(s):
+            m = h.get_state()["m"]
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(m.cpu().numpy(), ref)

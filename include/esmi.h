@@ -32,6 +32,11 @@
  *     unchanged unless it is ES_ERR_HIP (then the handle should be
  *     destroyed).
  *   - A handle is not thread-safe; distinct handles are independent.
+ *   - The generation counter, sigma / lr buffer selection and sequence
+ *     checks live on the host and the kernels take them as launch
+ *     arguments, so a stream capture of es_ask / es_eval / es_tell records
+ *     that one generation; a replay repeats it.  For many generations per
+ *     launch use es_run.
  *   - Minimisation is the default (Listing 1); maximize = 1 negates keys.
  */
 #ifndef ESMI_H

@@ -56,10 +56,13 @@ def kernel_source_sha256():
     return h.hexdigest()
 
 
-def profiled_traffic(workload):
+def profiled_traffic(workload, key="eval_hbm_bytes_per_launch"):
     """HBM bytes per launch of the evaluate kernel from the committed rocprofv3
     counter summary of this workload, or None if there is none or the kernel
-    sources changed since the counters were taken."""
+    sources changed since the counters were taken.  The default key is the
+    copy-calibrated FETCH_SIZE + WRITE_SIZE; eval_hbm_bytes_request_sized
+    prices each read request at its size (the evaluate kernel's scalar-cache
+    reads are 64-B requests, the copy's 128-B)."""
     path = os.path.join(ROOT, "profiles", f"k_eval_bbob_{workload}.txt")
     if not os.path.exists(path):
         return None
@@ -72,7 +75,7 @@ def profiled_traffic(workload):
     if kv.get("kernel_source_sha256") != kernel_source_sha256():
         return None
     try:
-        return int(kv["eval_hbm_bytes_per_launch"])
+        return int(kv[key])
     except (KeyError, ValueError):
         return None
 
@@ -204,6 +207,7 @@ def main():
         roof = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                 "unit": "T VALU lane-op slots/s", "frac": achieved / VALU_PEAK,
                 "traffic": profiled_traffic(args.workload),
+                "traffic_request_sized": profiled_traffic(args.workload, "eval_hbm_bytes_request_sized"),
                 "kernel": "k_eval_bbob (fused sample+evaluate; timed with its k_eval_reduce)",
                 "kernel_ms": eval_ms, "slots_per_pair_block": eval_slots,
                 "pair_blocks_per_launch": pair_blocks,

@@ -255,6 +255,13 @@ AdamConsts adam_consts(const es_config& c, int64_t t)
     return a;
 }
 
+// es_run's choice: the fused loop pays off when each run is small (per-call
+// launches then dominate) or when the runs fill the chip one workgroup each.
+bool fused_by_default(const Geometry& g, const EvalPlan& e, const es_config& c)
+{
+    return fused_supported(g, e, c) && ((int64_t)g.P * g.nb <= 8192 || g.R >= 128);
+}
+
 int64_t env_i64(const char* name, int64_t dflt)
 {
     const char* s = std::getenv(name);
@@ -409,9 +416,9 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     g.P = cfg->popsize / 2;
     g.R = cfg->num_runs;
     h->plan = eval_plan(g, env_i64("ESMI_EVAL_BLOCKS_PER_CHUNK", 0));
-    // es_run may take the fused loop for this geometry; then the per-call
-    // gradient kernel must sum in the fused loop's order
-    h->tell = tell_plan(g, fused_supported(g, h->plan, *cfg), env_i64("ESMI_TELL_SPLIT", 0));
+    // where es_run takes the fused loop (the rule of es_run), the per-call
+    // gradient kernel sums in the fused loop's order, so both give the same bits
+    h->tell = tell_plan(g, fused_by_default(g, h->plan, *cfg), env_i64("ESMI_TELL_SPLIT", 0));
     h->run_path = (int)env_i64("ESMI_RUN_PATH", 0);
     hipError_t e = hipGetDevice(&h->device);
     const size_t rows = (size_t)g.Dp * g.R;
@@ -547,11 +554,9 @@ es_status es_run(es_handle* h, int32_t T, float* log)
     if (T == 0) return ES_OK;
     if (h->t + T > 0xFFFFFFFFll) return fail(h, ES_ERR_ARG, "es_run: generation counter would exceed 2^32");
     const bool fused_ok = fused_supported(h->g, h->plan, h->cfg);
-    // the fused loop pays off when each run is small: per-call launches then
-    // dominate, and the runs fill the chip one workgroup each
-    const bool fused = h->run_path == 2 ? fused_ok
-                       : h->run_path == 1 ? false
-                       : fused_ok && ((int64_t)h->g.P * h->g.nb <= 8192 || h->g.R >= 128);
+    // ESMI_RUN_PATH forces a path (1 per-call kernels, 2 fused loop); a forced
+    // fused loop on a geometry es_run would not fuse sums in its own order
+    const bool fused = h->run_path == 2 ? fused_ok : h->run_path == 1 ? false : fused_by_default(h->g, h->plan, h->cfg);
     if (fused) {
         es_status s = stage_adam(h, T);
         if (s != ES_OK) return s;

@@ -71,6 +71,7 @@ hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, 
 struct TellPlan {
     int32_t ps = 1;
     int32_t nsplit = 1;
+    int32_t sub = 1;  // lanes per Philox block (4: sub-slices of the pairs)
 };
 TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit);
 size_t tell_part_elems(const Geometry& g, const TellPlan& tp, int strategy);  // doubles

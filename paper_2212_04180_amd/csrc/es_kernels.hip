@@ -785,6 +785,7 @@ struct TellArgs {
     uint32_t t;
     int64_t D, nb;
     int32_t P, R, ps, nsplit;
+    int32_t sub;           // lanes per block (1, or 4 for runs with few block groups)
     int32_t nitems;        // items the slices split: P pairs, or mu elites
     int32_t strategy, optimizer;
     float sigma_lr, max_change, sigma_decay, sigma_final;
@@ -937,11 +938,14 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
     const int32_t tx = threadIdx.x % TELL_LANES;
     // one wave per pair slice: make the slice index (and the pair loop) uniform
     const int32_t s = __builtin_amdgcn_readfirstlane(threadIdx.x / TELL_LANES);
-    const int64_t b = (int64_t)blockIdx.x * TELL_LANES + tx;
+    // sub > 1: sub neighbouring lanes share a block, each with a sub-slice of
+    // the wave's pairs (a run with few block groups spread over more CUs)
+    const int32_t sub = a.sub, si = tx % sub;
+    const int64_t b = (int64_t)blockIdx.x * (TELL_LANES / sub) + tx / sub;
     const uint32_t bb = (uint32_t)(b < a.nb ? b : a.nb - 1);
     const uint64_t key = a.seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
-    const int64_t S = (int64_t)a.ps * a.nsplit, gs = (int64_t)z * a.ps + s;
+    const int64_t S = (int64_t)a.ps * a.nsplit * sub, gs = ((int64_t)z * a.ps + s) * sub + si;
     const int32_t pb = (int32_t)(((int64_t)a.nitems * gs) / S);
     const int32_t pe = (int32_t)(((int64_t)a.nitems * (gs + 1)) / S);
 
@@ -953,6 +957,14 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
                                  a64, b64);
     else
         tell_slice<LANES_BLOCK>(a.wfold + (int64_t)r * a.P, k0, k1, bb, a.t, pb, pe, a64);
+    // sub-slices of one block: ((l0 + l1) + (l2 + l3)) in every lane of the group
+    for (int off = 1; off < sub; off <<= 1) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            a64[k] += __shfl_xor(a64[k], off);
+            if constexpr (TWO) b64[k] += __shfl_xor(b64[k], off);
+        }
+    }
     if (s > 0) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -976,6 +988,7 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
         }
         return;
     }
+    if (si != 0) return;  // sub > 1 only where no per-wave norm partials are kept
     const double g2 = b < a.nb ? tell_finish(a, a64, b64, b, r, k0, k1) : 0.0;
     if (a.gpart) {
         const double tot = wave_sum(g2);
@@ -1557,7 +1570,9 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp
     const bool cma = c.strategy == ES_STRAT_SEP_CMA;
     const bool clipup = c.strategy != ES_STRAT_SNES && !cma && c.optimizer == ES_OPT_CLIPUP;
     if (!clipup && !cma) a.gpart = nullptr;
-    const int64_t groups = (g.nb + TELL_LANES - 1) / TELL_LANES;
+    // ClipUp and Sep-CMA-ES reduce per-wave norm partials: one lane per block
+    a.sub = (!clipup && !cma) ? tp.sub : 1;
+    const int64_t groups = (g.nb + TELL_LANES / a.sub - 1) / (TELL_LANES / a.sub);
     const dim3 grid((unsigned)groups, (unsigned)g.R, (unsigned)tp.nsplit);
     const size_t lds = sizeof(double) * (size_t)(tp.ps - 1) * TELL_LANES * (two || cma ? 8 : 4);
     if (cma) k_tell<true, true><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
@@ -1593,6 +1608,13 @@ TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit)
     TellPlan tp;
     tp.ps = tell_slices(g);
     if (fused_path) return tp;  // the fused loop sums all slices in one workgroup
+    // A run with few block groups: four lanes per block, so the groups of
+    // 16 blocks spread the run over four times the CUs (no split launch).
+    const int64_t groups64 = (g.nb + TELL_LANES - 1) / TELL_LANES * g.R;
+    if (groups64 < 64 && g.P >= 8 * tp.ps) {
+        tp.sub = 4;
+        return tp;
+    }
     // Few block groups (under four workgroups per CU) leave the CUs unevenly
     // loaded; then split each group's pairs over more, smaller workgroups
     // (four slices each; about 1024 workgroups, which all fit on the chip at

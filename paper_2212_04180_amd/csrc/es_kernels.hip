@@ -785,7 +785,6 @@ struct TellArgs {
     uint32_t t;
     int64_t D, nb;
     int32_t P, R, ps, nsplit;
-    int32_t sub;           // lanes per block (1, or 4 for runs with few block groups)
     int32_t nitems;        // items the slices split: P pairs, or mu elites
     int32_t strategy, optimizer;
     float sigma_lr, max_change, sigma_decay, sigma_final;
@@ -928,7 +927,7 @@ __device__ __forceinline__ double tell_finish(const TellArgs& a, const double a6
 // pairs) and store their sums to part; k_tell_fold adds them in split order
 // and applies the update.  TWO: the second sum b (PGPE, SNES, Sep-CMA-ES);
 // ROWS: items are the elites (Sep-CMA-ES) rather than the pairs.
-template <bool TWO, bool ROWS = false>
+template <bool TWO, bool ROWS = false, int SUB = 1>
 __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
 {
     // slices 1 .. ps-1 of every lane, sized by the launch: [ps-1][TELL_LANES][W]
@@ -938,9 +937,12 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
     const int32_t tx = threadIdx.x % TELL_LANES;
     // one wave per pair slice: make the slice index (and the pair loop) uniform
     const int32_t s = __builtin_amdgcn_readfirstlane(threadIdx.x / TELL_LANES);
-    // sub > 1: sub neighbouring lanes share a block, each with a sub-slice of
-    // the wave's pairs (a run with few block groups spread over more CUs)
-    const int32_t sub = a.sub, si = tx % sub;
+    // SUB > 1: SUB neighbouring lanes share a block, each with a sub-slice of
+    // the wave's pairs (a run with few block groups spread over more CUs);
+    // SUB = 1 keeps the pair range uniform, so the weights come through the
+    // scalar cache
+    constexpr int32_t sub = SUB;
+    const int32_t si = tx % sub;
     const int64_t b = (int64_t)blockIdx.x * (TELL_LANES / sub) + tx / sub;
     const uint32_t bb = (uint32_t)(b < a.nb ? b : a.nb - 1);
     const uint64_t key = a.seed + (uint64_t)r;
@@ -958,6 +960,7 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
     else
         tell_slice<LANES_BLOCK>(a.wfold + (int64_t)r * a.P, k0, k1, bb, a.t, pb, pe, a64);
     // sub-slices of one block: ((l0 + l1) + (l2 + l3)) in every lane of the group
+#pragma unroll
     for (int off = 1; off < sub; off <<= 1) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -988,7 +991,7 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
         }
         return;
     }
-    if (si != 0) return;  // sub > 1 only where no per-wave norm partials are kept
+    if (SUB > 1 && si != 0) return;  // SUB > 1 only where no per-wave norm partials are kept
     const double g2 = b < a.nb ? tell_finish(a, a64, b64, b, r, k0, k1) : 0.0;
     if (a.gpart) {
         const double tot = wave_sum(g2);
@@ -1571,12 +1574,14 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp
     const bool clipup = c.strategy != ES_STRAT_SNES && !cma && c.optimizer == ES_OPT_CLIPUP;
     if (!clipup && !cma) a.gpart = nullptr;
     // ClipUp and Sep-CMA-ES reduce per-wave norm partials: one lane per block
-    a.sub = (!clipup && !cma) ? tp.sub : 1;
-    const int64_t groups = (g.nb + TELL_LANES / a.sub - 1) / (TELL_LANES / a.sub);
+    const int sub = (!clipup && !cma && tp.nsplit == 1) ? tp.sub : 1;
+    const int64_t groups = (g.nb + TELL_LANES / sub - 1) / (TELL_LANES / sub);
     const dim3 grid((unsigned)groups, (unsigned)g.R, (unsigned)tp.nsplit);
     const size_t lds = sizeof(double) * (size_t)(tp.ps - 1) * TELL_LANES * (two || cma ? 8 : 4);
     if (cma) k_tell<true, true><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
+    else if (two && sub == 4) k_tell<true, false, 4><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
     else if (two) k_tell<true><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
+    else if (sub == 4) k_tell<false, false, 4><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
     else k_tell<false><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

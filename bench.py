@@ -156,11 +156,17 @@ def main():
     torch.cuda.synchronize()
 
     K = args.steps
-    # two events per generation, around the evaluate phase (the dominant
-    # kernel's duration); the tell phase runs from one generation's second
-    # event to the next one's first (each event record leaves the stream idle
-    # for a few microseconds, so no third one is placed after the tell)
+    # Two HIP events per generation time the evaluate phase (the dominant
+    # kernel): es_eval_timed has the evaluate's first and last kernel
+    # dispatches record them (hipExtLaunchKernel), so the timed stream holds
+    # no marker packets (an event record between kernels leaves the stream
+    # idle for a few microseconds).  The tell phase runs from one generation's
+    # stop event to the next one's start event.  Each event is recorded once
+    # here, outside the timed region, so that it exists.
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    for pair in ev:
+        for e in pair:
+            e.record(stream)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
@@ -170,9 +176,7 @@ def main():
     else:
         for k in range(K):
             es.ask()
-            ev[k][0].record(stream)
-            es.eval(fit)
-            ev[k][1].record(stream)
+            es.eval(fit, events=ev[k])
             es.tell(fit)
     end.record(stream)
     torch.cuda.synchronize()

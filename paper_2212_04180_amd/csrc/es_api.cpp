@@ -335,17 +335,17 @@ es_status enqueue_tell(es_handle* h, const float* fitness, float* gen_best)
     return ES_OK;
 }
 
-es_status enqueue_eval(es_handle* h, float* fit)
+es_status enqueue_eval(es_handle* h, float* fit, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr)
 {
     if (h->cfg.problem == ES_PROB_NONE) return fail(h, ES_ERR_UNSUPPORTED, "no built-in problem configured");
     if (h->cfg.problem == ES_PROB_MLP) {
         ES_HIP(h, launch_eval_mlp(h->g, h->cfg, (uint32_t)h->t, h->m, h->pdata, h->mlp_scratch, fit,
-                                  h->hp[h->hp_cur], h->sig, h->stream),
+                                  h->hp[h->hp_cur], h->sig, h->stream, ev_start, ev_stop),
                "MLP evaluate kernels");
         return ES_OK;
     }
     ES_HIP(h, launch_eval_bbob(h->g, h->cfg, h->plan, (uint32_t)h->t, h->m, h->pdata, h->partial, fit,
-                               h->hp[h->hp_cur], h->sig, 1.0, h->stream),
+                               h->hp[h->hp_cur], h->sig, 1.0, h->stream, ev_start, ev_stop),
            "evaluate kernel");
     return ES_OK;
 }
@@ -532,6 +532,14 @@ es_status es_eval(es_handle* h, float* fitness_out)
     if (!h || !fitness_out) return h ? fail(h, ES_ERR_ARG, "es_eval: null fitness buffer") : ES_ERR_ARG;
     if (h->phase != ASKED) return fail(h, ES_ERR_SEQUENCE, "es_eval: no open ask");
     return enqueue_eval(h, fitness_out);
+}
+
+es_status es_eval_timed(es_handle* h, float* fitness_out, void* start_event, void* stop_event)
+{
+    if (!h || !fitness_out) return h ? fail(h, ES_ERR_ARG, "es_eval_timed: null fitness buffer") : ES_ERR_ARG;
+    if (h->phase != ASKED) return fail(h, ES_ERR_SEQUENCE, "es_eval_timed: no open ask");
+    return enqueue_eval(h, fitness_out, reinterpret_cast<hipEvent_t>(start_event),
+                        reinterpret_cast<hipEvent_t>(stop_event));
 }
 
 es_status es_tell(es_handle* h, const float* fitness)

@@ -2,6 +2,7 @@
 // and the kernel launchers (es_kernels.hip).  Not part of the C-ABI.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -55,9 +56,12 @@ hipError_t launch_cma_scale(const Geometry& g, float* svec, const float* C, cons
 // svec: per-dimension sigma [R][Dp] (PGPE, SNES) or null.
 hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const float* m, float* x,
                       const float* hp, const float* svec, hipStream_t s);
+// ev_start / ev_stop (either may be null): events that record the dispatch of
+// the first kernel and the end of the last one (es_eval_timed).
 hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t,
                             const float* m, const float* pdata, float* partial, float* fit,
-                            const float* hp, const float* svec, double div, hipStream_t s);
+                            const float* hp, const float* svec, double div, hipStream_t s,
+                            hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 // table: the shaping table indexed by rank (centered ranks, or SNES
 // utilities by rank), ybar_table its mean; bfold: PGPE / SNES second weight.
 hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* pen,
@@ -126,7 +130,19 @@ size_t mlp_scratch_bytes();  // X_t (fp32 and bf16), teacher outputs, transposed
 hipError_t launch_mlp_setup(const float* teacher, void* scratch, hipStream_t s);
 size_t mlp_lds_bytes();
 hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, const float* m, const float* teacher,
-                           void* scratch, float* fit, const float* hp, const float* svec, hipStream_t s);
+                           void* scratch, float* fit, const float* hp, const float* svec, hipStream_t s,
+                           hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+
+// A kernel launch that, given events, has the dispatch itself record its start
+// and end (hipExtLaunchKernel), so no marker packet sits between kernels.
+template <typename... KArgs, typename... Args>
+hipError_t launch_timed(void (*k)(KArgs...), dim3 grid, dim3 block, uint32_t lds, hipStream_t s, hipEvent_t ev_start,
+                        hipEvent_t ev_stop, Args... args)
+{
+    if (!ev_start && !ev_stop) k<<<grid, block, lds, s>>>(args...);
+    else hipExtLaunchKernelGGL(k, grid, block, lds, s, ev_start, ev_stop, 0u, args...);
+    return hipGetLastError();
+}
 
 // Largest population the rank kernel stages in LDS.
 constexpr int32_t RANK_MAX_N = 16384;

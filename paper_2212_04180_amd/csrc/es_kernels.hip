@@ -1487,40 +1487,35 @@ hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const f
 
 hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t,
                             const float* m, const float* pdata, float* partial, float* fit,
-                            const float* hp, const float* svec, double div, hipStream_t s)
+                            const float* hp, const float* svec, double div, hipStream_t s, hipEvent_t ev_start,
+                            hipEvent_t ev_stop)
 {
     // chunk ids are dealt so that the pair groups of one chunk share an XCD
     const int64_t slots = (e.nchunks + 7) / 8 * e.n_pg;
     const dim3 grid((unsigned)(slots * 8), (unsigned)g.R);
     const dim3 block((unsigned)e.wg);
-#define ES_EVAL_LAUNCH(PROB)                                                                                   \
-    do {                                                                                                       \
-        if (c.strategy == ES_STRAT_SEP_CMA)                                                                    \
-            k_eval_bbob<PROB, SM_INDEP><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N,    \
-                                                               g.P, e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, \
-                                                               svec);                                          \
-        else if (svec)                                                                                         \
-            k_eval_bbob<PROB, SM_VEC><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N, g.P, \
-                                                             e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, svec); \
-        else                                                                                                   \
-            k_eval_bbob<PROB, SM_SCALAR><<<grid, block, 0, s>>>(m, pdata, partial, c.seed, t, g.D, g.nb, g.N,   \
-                                                                g.P, e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, \
-                                                                nullptr);                                      \
-    } while (0)
+    const int sm = c.strategy == ES_STRAT_SEP_CMA ? SM_INDEP : svec ? SM_VEC : SM_SCALAR;
+    const float* sv = sm == SM_SCALAR ? nullptr : svec;
+#define ES_EVAL_LAUNCH(PROB, SM)                                                                                \
+    launch_timed(k_eval_bbob<PROB, SM>, grid, block, 0, s, ev_start, nullptr, m, pdata, partial, c.seed, t, g.D, \
+                 g.nb, g.N, g.P, e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, sv)
+#define ES_EVAL_PROB(PROB)                                                                                      \
+    (sm == SM_INDEP ? ES_EVAL_LAUNCH(PROB, SM_INDEP) : sm == SM_VEC ? ES_EVAL_LAUNCH(PROB, SM_VEC)               \
+                                                                    : ES_EVAL_LAUNCH(PROB, SM_SCALAR))
+    hipError_t err;
     switch (c.problem) {
-    case ES_PROB_SPHERE: ES_EVAL_LAUNCH(ES_PROB_SPHERE); break;
-    case ES_PROB_SHIFTED_SPHERE: ES_EVAL_LAUNCH(ES_PROB_SHIFTED_SPHERE); break;
-    case ES_PROB_ROSENBROCK: ES_EVAL_LAUNCH(ES_PROB_ROSENBROCK); break;
-    case ES_PROB_RASTRIGIN: ES_EVAL_LAUNCH(ES_PROB_RASTRIGIN); break;
+    case ES_PROB_SPHERE: err = ES_EVAL_PROB(ES_PROB_SPHERE); break;
+    case ES_PROB_SHIFTED_SPHERE: err = ES_EVAL_PROB(ES_PROB_SHIFTED_SPHERE); break;
+    case ES_PROB_ROSENBROCK: err = ES_EVAL_PROB(ES_PROB_ROSENBROCK); break;
+    case ES_PROB_RASTRIGIN: err = ES_EVAL_PROB(ES_PROB_RASTRIGIN); break;
     default: return hipErrorInvalidValue;
     }
+#undef ES_EVAL_PROB
 #undef ES_EVAL_LAUNCH
-    hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     const double add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;
-    k_eval_reduce<<<dim3((unsigned)((g.N + 63) / 64), (unsigned)g.R), 64 * RED_SLICES, 0, s>>>(partial, fit, g.N,
-                                                                                            g.R, e.nchunks, add, div);
-    return hipGetLastError();
+    return launch_timed(k_eval_reduce, dim3((unsigned)((g.N + 63) / 64), (unsigned)g.R), dim3(64 * RED_SLICES), 0, s,
+                        nullptr, ev_stop, (const float*)partial, fit, g.N, g.R, e.nchunks, add, div);
 }
 
 hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* pen,

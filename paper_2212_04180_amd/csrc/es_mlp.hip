@@ -479,15 +479,16 @@ hipError_t launch_mlp_setup(const float* teacher, void* scratch, hipStream_t s)
 size_t mlp_lds_bytes() { return sizeof(MlpSmem); }
 
 hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, const float* m, const float* teacher,
-                           void* scratch, float* fit, const float* hp, const float* svec, hipStream_t s)
+                           void* scratch, float* fit, const float* hp, const float* svec, hipStream_t s,
+                           hipEvent_t ev_start, hipEvent_t ev_stop)
 {
     float* xf = static_cast<float*>(scratch);
     __bf16* xb = reinterpret_cast<__bf16*>(xf + MLP_BATCH * MLP_IN);
     float* yt = reinterpret_cast<float*>(xb + MLP_BATCH * MLP_IN);
     const float* wt = reinterpret_cast<const float*>(static_cast<const char*>(scratch) + mlp_scratch_bytes() -
                                                      sizeof(float) * MLP_NUM_PARAMS);
-    k_mlp_teacher<<<MLP_BATCH, TEACHER_THREADS, 0, s>>>(teacher, wt, xf, xb, yt, c.seed, t, c.mlp_tanh_out);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_timed(k_mlp_teacher, dim3(MLP_BATCH), dim3(TEACHER_THREADS), 0, s, ev_start, nullptr, teacher,
+                                wt, xf, xb, yt, c.seed, t, c.mlp_tanh_out);
     if (e != hipSuccess) return e;
     // more than 64 KB of LDS per workgroup: allowed per kernel (cheap to repeat)
     const void* kern = svec ? reinterpret_cast<const void*>(&k_eval_mlp<true>)
@@ -495,13 +496,13 @@ hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, co
     e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(MlpSmem));
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)g.P, (unsigned)g.R);
+    const __bf16* xbc = xb;
+    const float* ytc = yt;
     if (svec)
-        k_eval_mlp<true><<<grid, MLP_THREADS, sizeof(MlpSmem), s>>>(m, xb, yt, fit, c.seed, t, g.Dp, g.N, g.P, hp,
-                                                                     c.mlp_tanh_out, svec);
-    else
-        k_eval_mlp<false><<<grid, MLP_THREADS, sizeof(MlpSmem), s>>>(m, xb, yt, fit, c.seed, t, g.Dp, g.N, g.P, hp,
-                                                                      c.mlp_tanh_out, nullptr);
-    return hipGetLastError();
+        return launch_timed(k_eval_mlp<true>, grid, dim3(MLP_THREADS), (uint32_t)sizeof(MlpSmem), s, nullptr, ev_stop,
+                            m, xbc, ytc, fit, c.seed, t, g.Dp, g.N, g.P, hp, c.mlp_tanh_out, svec);
+    return launch_timed(k_eval_mlp<false>, grid, dim3(MLP_THREADS), (uint32_t)sizeof(MlpSmem), s, nullptr, ev_stop, m,
+                        xbc, ytc, fit, c.seed, t, g.Dp, g.N, g.P, hp, c.mlp_tanh_out, (const float*)nullptr);
 }
 
 }  // namespace esmi

@@ -26,7 +26,7 @@ STRAT_OPENAI_ES, STRAT_PGPE, STRAT_SNES, STRAT_SEP_CMA = range(4)
 OPT_ADAM, OPT_CLIPUP = range(2)
 
 # Every symbol include/esmi.h declares, in declaration order.
-EXPORTS = ("es_init", "es_ask", "es_eval", "es_tell", "es_run", "es_get_state", "es_set_state",
+EXPORTS = ("es_init", "es_ask", "es_eval", "es_eval_timed", "es_tell", "es_run", "es_get_state", "es_set_state",
            "es_get_best", "es_get_shaped", "es_get_grad", "es_set_hparams", "es_get_hparams",
            "es_get_strategy_state", "es_set_strategy_state", "es_get_penalty",
            "es_get_problem_data", "es_debug_noise",
@@ -144,6 +144,7 @@ def lib() -> ctypes.CDLL:
         "es_init": (i32, [P(_Config), vp, P(vp)]),
         "es_ask": (i32, [vp, vp]),
         "es_eval": (i32, [vp, vp]),
+        "es_eval_timed": (i32, [vp, vp, vp, vp]),
         "es_tell": (i32, [vp, vp]),
         "es_run": (i32, [vp, i32, vp]),
         "es_get_state": (i32, [vp, vp, vp, vp, P(i64)]),
@@ -229,9 +230,19 @@ class ES:
         self._check(lib().es_ask(self._h, _ptr(x)))
         return x
 
-    def eval(self, out=None):
+    def eval(self, out=None, events=None):
+        """Fitness of the asked population.  events: None, or a (start, stop)
+        pair of timing torch.cuda.Event objects, each recorded once before so
+        that it exists, which the evaluate kernels then record themselves
+        (es_eval_timed)."""
         out = self._empty(self.R, self.N) if out is None else out
-        self._check(lib().es_eval(self._h, _ptr(out)))
+        if events is None:
+            self._check(lib().es_eval(self._h, _ptr(out)))
+            return out
+        hs, he = (int(e.cuda_event) for e in events)
+        if not hs or not he:
+            raise ValueError("es_eval_timed takes created events: record each one once beforehand")
+        self._check(lib().es_eval_timed(self._h, _ptr(out), ctypes.c_void_p(hs), ctypes.c_void_p(he)))
         return out
 
     def tell(self, fitness):

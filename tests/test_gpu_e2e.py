@@ -263,3 +263,35 @@ def test_two_handles_on_their_own_streams():
             m = h.get_state()["m"]
         torch.cuda.synchronize()
         np.testing.assert_array_equal(m.cpu().numpy(), ref)
+
+
+@pytest.mark.parametrize("name", ["rosenbrock_d1000", "mlp_teacher"])
+def test_eval_timed_equals_eval_and_times_the_kernels(name):
+    """es_eval_timed: the same fitness bits as es_eval, and its events (recorded
+    by the first and last evaluate dispatch) span a positive time that fits
+    inside events recorded on the stream around the call."""
+    from paper_2212_04180_amd import workloads
+    P = _P()
+    cfg, _ = workloads.get(name)
+    a, b = P.ES(cfg), P.ES(cfg)
+    s = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in ev:
+        e.record(s)
+    b.ask()
+    with pytest.raises(ValueError):
+        b.eval(events=(torch.cuda.Event(enable_timing=True), ev[1]))  # never recorded: no event yet
+    b.tell(b.eval())
+    a.ask()
+    a.tell(a.eval())
+    # generation 1 of both: plain and timed evaluate
+    a.ask()
+    fa = a.eval()
+    b.ask()
+    ev[0].record(s)
+    fb = b.eval(events=(ev[1], ev[2]))
+    ev[3].record(s)
+    torch.cuda.synchronize()
+    assert torch.equal(fa, fb)
+    inner, outer = ev[1].elapsed_time(ev[2]), ev[0].elapsed_time(ev[3])
+    assert 0.0 < inner <= outer, (inner, outer)

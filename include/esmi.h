@@ -35,8 +35,9 @@
  *   - The generation counter, sigma / lr buffer selection and sequence
  *     checks live on the host and the kernels take them as launch
  *     arguments, so a stream capture of es_ask / es_eval / es_tell records
- *     that one generation; a replay repeats it.  For many generations per
- *     launch use es_run.
+ *     that one generation; a replay repeats it (for ES_PROB_MLP with
+ *     OpenAI-ES on the inputs the replayed es_tell made for the generation
+ *     after it).  For many generations per launch use es_run.
  *   - Minimisation is the default (Listing 1); maximize = 1 negates keys.
  */
 #ifndef ESMI_H
@@ -194,7 +195,9 @@ es_status es_eval_timed(es_handle* h, float* fitness_out, void* start_event, voi
  * with eps regenerated from the counter, Adam step on the mean, best-so-far
  * update on the raw fitness, schedule step of sigma and lr; t += 1.
  * fitness: device [R][N] from es_eval or from the caller's own evaluation
- * of the asked population. */
+ * of the asked population.  ES_PROB_MLP with OpenAI-ES: the same launch also
+ * makes the next generation's inputs and teacher outputs, which the next
+ * es_eval then uses. */
 es_status es_tell(es_handle* h, const float* fitness);
 
 /* T fused generations (the scanned loop of Listing 2) with the built-in

@@ -84,6 +84,7 @@ struct es_handle {
     double* tell_part = nullptr; // per-workgroup gradient sums when tell.nsplit > 1
     float* pdata = nullptr;  // [Dp] shift vector or teacher
     void* mlp_scratch = nullptr;  // MLP inputs and teacher outputs of the current generation
+    int64_t teacher_t = -1;       // generation whose inputs and teacher outputs are in mlp_scratch
     // Adam constants of the generations of one fused es_run, staged in pinned
     // host memory and copied on the stream; the event guards reuse.
     AdamConsts* adam_host = nullptr;
@@ -330,7 +331,14 @@ es_status enqueue_tell(es_handle* h, const float* fitness, float* gen_best)
     tb.sig = h->sig; tb.vel = h->vel; tb.gbuf = h->gbuf; tb.gpart = h->gpart; tb.vpart = h->vpart;
     tb.part = h->tell_part; tb.hp = hp; tb.hp_next = h->hp[1 - h->hp_cur];
     tb.elite = h->elite; tb.cw = h->cw; tb.zw = h->zw; tb.qd = h->qd; tb.cmaC = h->cmaC; tb.cma = h->cma;
+    // MLP: where the gradient kernel can carry them (OpenAI-ES), the next
+    // generation's inputs and teacher outputs ride in the gradient launch (the
+    // evaluate kernel of this generation has read them); otherwise the next
+    // evaluate makes them
+    const bool teach = h->mlp_scratch && tell_carries_teacher(h->cfg, h->tell) && h->t + 1 <= 0xFFFFFFFFll;
+    if (teach) tb.teacher = mlp_teacher_job(h->cfg, h->pdata, h->mlp_scratch, (uint32_t)(h->t + 1));
     ES_HIP(h, launch_tell(g, h->cfg, h->tell, (uint32_t)h->t, a, tb, h->stream), "tell kernel");
+    h->teacher_t = teach ? h->t + 1 : -1;
     h->hp_cur = 1 - h->hp_cur;  // the schedule step is next generation's sigma and lr
     return ES_OK;
 }
@@ -340,8 +348,9 @@ es_status enqueue_eval(es_handle* h, float* fit, hipEvent_t ev_start = nullptr, 
     if (h->cfg.problem == ES_PROB_NONE) return fail(h, ES_ERR_UNSUPPORTED, "no built-in problem configured");
     if (h->cfg.problem == ES_PROB_MLP) {
         ES_HIP(h, launch_eval_mlp(h->g, h->cfg, (uint32_t)h->t, h->m, h->pdata, h->mlp_scratch, fit,
-                                  h->hp[h->hp_cur], h->sig, h->stream, ev_start, ev_stop),
+                                  h->hp[h->hp_cur], h->sig, h->teacher_t != h->t, h->stream, ev_start, ev_stop),
                "MLP evaluate kernels");
+        h->teacher_t = h->t;
         return ES_OK;
     }
     ES_HIP(h, launch_eval_bbob(h->g, h->cfg, h->plan, (uint32_t)h->t, h->m, h->pdata, h->partial, fit,
@@ -605,6 +614,7 @@ es_status es_set_state(es_handle* h, const float* m, const float* m1, const floa
     if (m && (s = copy_rows_in(h, h->m, m)) != ES_OK) return s;
     if (m1 && (s = copy_rows_in(h, h->m1, m1)) != ES_OK) return s;
     if (v && (s = copy_rows_in(h, h->v, v)) != ES_OK) return s;
+    if (t != h->t) h->teacher_t = -1;
     h->t = t;
     return ES_OK;
 }
@@ -808,6 +818,7 @@ es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes)
         p += rows;
     }
     ES_HIP(h, hipStreamSynchronize(h->stream), "load sync");
+    if (hd.t != h->t) h->teacher_t = -1;
     h->t = hd.t;
     return ES_OK;
 }

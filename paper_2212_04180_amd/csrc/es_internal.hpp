@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "es_teacher.hpp"
 #include "esmi.h"
 
 namespace esmi {
@@ -105,9 +106,14 @@ struct TellBuffers {
     double* qd;            // [R][Dp]
     float* cmaC;           // [R][Dp] diagonal covariance
     CmaConsts cma;
+    // MLP: the next generation's teacher work, run by MLP_BATCH extra
+    // workgroups of the gradient launch (teacher.w null: none)
+    TeacherJob teacher{};
 };
 hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp, uint32_t t, const AdamConsts& a,
                        const TellBuffers& tb, hipStream_t s);
+// Whether the gradient launch of this plan can run teacher rows (tb.teacher).
+bool tell_carries_teacher(const es_config& c, const TellPlan& tp);
 hipError_t launch_debug_noise(const Geometry& g, const es_config& c, int32_t run, uint32_t t,
                               int32_t pair, uint32_t* words, float* eps, hipStream_t s);
 
@@ -129,9 +135,13 @@ constexpr int64_t MLP_NUM_PARAMS = 86544;
 size_t mlp_scratch_bytes();  // X_t (fp32 and bf16), teacher outputs, transposed teacher
 hipError_t launch_mlp_setup(const float* teacher, void* scratch, hipStream_t s);
 size_t mlp_lds_bytes();
+// run_teacher: also compute X_t and Y_T first (else the gradient launch of
+// the previous generation left them in scratch).
 hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, const float* m, const float* teacher,
-                           void* scratch, float* fit, const float* hp, const float* svec, hipStream_t s,
-                           hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+                           void* scratch, float* fit, const float* hp, const float* svec, bool run_teacher,
+                           hipStream_t s, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+// The teacher work of generation t (X_t, Y_T into scratch).
+TeacherJob mlp_teacher_job(const es_config& c, const float* teacher, void* scratch, uint32_t t);
 
 // A kernel launch that, given events, has the dispatch itself record its start
 // and end (hipExtLaunchKernel), so no marker packet sits between kernels.

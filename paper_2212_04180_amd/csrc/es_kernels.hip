@@ -15,7 +15,9 @@
 //                     best-so-far, the schedule step of sigma and lr
 //   k_tell            noise sums over the pairs regenerated per Philox block
 //                     (g = E^T y / (N sigma) for OpenAI-ES, Sec. 2.1), fused
-//                     with the strategy's update; lane = a block of four dims
+//                     with the strategy's update; lane = a block of four dims;
+//                     for the MLP problem its launch also runs the next
+//                     generation's teacher rows (es_teacher.hpp)
 //   k_tell_fold       the split gradient's partial sums in split order, then
 //                     the update
 //   k_clipup_velocity, k_clipup_apply   ClipUp's two norm passes
@@ -789,6 +791,10 @@ struct TellArgs {
     int32_t strategy, optimizer;
     float sigma_lr, max_change, sigma_decay, sigma_final;
     AdamConsts ac;
+    // MLP: workgroups x < tshift of the launch (y = z = 0) run the next
+    // generation's teacher rows; the gradient's workgroups follow them
+    TeacherJob teacher;
+    int32_t tshift;
 };
 
 __device__ __forceinline__ double wave_sum(double v)
@@ -927,9 +933,21 @@ __device__ __forceinline__ double tell_finish(const TellArgs& a, const double a6
 // pairs) and store their sums to part; k_tell_fold adds them in split order
 // and applies the update.  TWO: the second sum b (PGPE, SNES, Sep-CMA-ES);
 // ROWS: items are the elites (Sep-CMA-ES) rather than the pairs.
-template <bool TWO, bool ROWS = false, int SUB = 1>
+template <bool TWO, bool ROWS = false, int SUB = 1, bool TEACH = false>
 __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
 {
+    if constexpr (TEACH) {
+        // the next generation's teacher rows, dispatched ahead of the gradient
+        // workgroups so that they run in the shadow of the gradient's VALU work
+        // (their own instantiation: the teacher's registers would otherwise
+        // lower every gradient kernel's occupancy)
+        if ((int32_t)blockIdx.x < a.tshift) {
+            if (blockIdx.y == 0 && blockIdx.z == 0) teacher_row(a.teacher, blockIdx.x);
+            return;
+        }
+    }
+    const int32_t tsh = TEACH ? a.tshift : 0;
+    const int32_t gx = (int32_t)blockIdx.x - tsh, gn = (int32_t)gridDim.x - tsh;
     // slices 1 .. ps-1 of every lane, sized by the launch: [ps-1][TELL_LANES][W]
     extern __shared__ double red[];
     constexpr int W = TWO ? 8 : 4;
@@ -943,7 +961,7 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
     // scalar cache
     constexpr int32_t sub = SUB;
     const int32_t si = tx % sub;
-    const int64_t b = (int64_t)blockIdx.x * (TELL_LANES / sub) + tx / sub;
+    const int64_t b = (int64_t)gx * (TELL_LANES / sub) + tx / sub;
     const uint32_t bb = (uint32_t)(b < a.nb ? b : a.nb - 1);
     const uint64_t key = a.seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
@@ -995,7 +1013,7 @@ __global__ __launch_bounds__(TELL_LANES * TELL_MAX_PS) void k_tell(TellArgs a)
     const double g2 = b < a.nb ? tell_finish(a, a64, b64, b, r, k0, k1) : 0.0;
     if (a.gpart) {
         const double tot = wave_sum(g2);
-        if (tx == 0) a.gpart[(int64_t)r * gridDim.x + blockIdx.x] = tot;
+        if (tx == 0) a.gpart[(int64_t)r * gn + gx] = tot;
     }
 }
 
@@ -1564,6 +1582,8 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp
     a.sigma_lr = c.sigma_lr; a.max_change = c.sigma_max_change;
     a.sigma_decay = c.sigma_decay; a.sigma_final = c.sigma_final;
     a.ac = ac;
+    a.teacher = tb.teacher;
+    a.tshift = tb.teacher.w ? MLP_BATCH : 0;
     const bool two = c.strategy != ES_STRAT_OPENAI_ES;
     const bool cma = c.strategy == ES_STRAT_SEP_CMA;
     const bool clipup = c.strategy != ES_STRAT_SNES && !cma && c.optimizer == ES_OPT_CLIPUP;
@@ -1571,9 +1591,11 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp
     // ClipUp and Sep-CMA-ES reduce per-wave norm partials: one lane per block
     const int sub = (!clipup && !cma && tp.nsplit == 1) ? tp.sub : 1;
     const int64_t groups = (g.nb + TELL_LANES / sub - 1) / (TELL_LANES / sub);
-    const dim3 grid((unsigned)groups, (unsigned)g.R, (unsigned)tp.nsplit);
+    if (a.tshift && !tell_carries_teacher(c, tp)) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)(groups + a.tshift), (unsigned)g.R, (unsigned)tp.nsplit);
     const size_t lds = sizeof(double) * (size_t)(tp.ps - 1) * TELL_LANES * (two || cma ? 8 : 4);
-    if (cma) k_tell<true, true><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
+    if (a.tshift) k_tell<false, false, 1, true><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
+    else if (cma) k_tell<true, true><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
     else if (two && sub == 4) k_tell<true, false, 4><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
     else if (two) k_tell<true><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
     else if (sub == 4) k_tell<false, false, 4><<<grid, TELL_LANES * tp.ps, lds, s>>>(a);
@@ -1601,6 +1623,15 @@ hipError_t launch_tell(const Geometry& g, const es_config& c, const TellPlan& tp
         e = hipGetLastError();
     }
     return e;
+}
+
+bool tell_carries_teacher(const es_config& c, const TellPlan& tp)
+{
+    // the one-sum kernel with one lane per block, in workgroups of at least
+    // the teacher's thread count
+    const bool clipup = c.optimizer == ES_OPT_CLIPUP;
+    const int sub = (!clipup && tp.nsplit == 1) ? tp.sub : 1;
+    return c.strategy == ES_STRAT_OPENAI_ES && sub == 1 && TELL_LANES * tp.ps >= TEACHER_THREADS;
 }
 
 TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit)

@@ -5,7 +5,9 @@
 //
 //   k_mlp_teacher  X_t [256][64] ~ N(0,1) from the EVAL stream of the base
 //                  seed (fp32 for the teacher, bf16 for the students) and
-//                  the fp32 teacher forward on it -> Y_T [256][16]
+//                  the fp32 teacher forward on it -> Y_T [256][16]; after
+//                  the first generation the gradient launch of generation
+//                  t computes them for t+1 (es_teacher.hpp)
 //   k_eval_mlp     one workgroup per antithetic pair: the pair's noise is
 //                  regenerated once and turned into both members' weights
 //                  (bf16(m +- sigma*eps), biases fp32) in LDS; the forward
@@ -30,6 +32,7 @@
 
 #include "es_device.hpp"
 #include "es_internal.hpp"
+#include "es_teacher.hpp"
 
 namespace esmi {
 
@@ -39,8 +42,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int MLP_IN = 64, MLP_H = 256, MLP_OUT = 16, MLP_BATCH = 256;
-constexpr int64_t OFF_W1 = 0, OFF_B1 = 16384, OFF_W2 = 16640, OFF_B2 = 82176, OFF_W3 = 82432, OFF_B3 = 86528;
 constexpr int MLP_WAVES = 16;          // per member: 8 waves x 32 batch columns = 256 inputs
 constexpr int MLP_THREADS = 64 * MLP_WAVES;
 constexpr int W2_ROWS = 32;            // W2 rows per LDS chunk (one K-step of layer 3)
@@ -389,75 +390,8 @@ __global__ void k_mlp_transpose(const float* __restrict__ w, float* __restrict__
     }
 }
 
-// Per generation: input row n of X_t (64 normals from the EVAL stream of the
-// base seed, counter block = flat index / 4) in fp32 and bf16, and the fp32
-// teacher forward on it -> Y_T[n][:].  One workgroup per input row; each
-// layer's inner sum is split into TEACHER_SLICES contiguous K ranges (one per
-// group of 256 threads, coalesced reads of the transposed weights) whose fp32
-// partials are added in slice order.
-constexpr int TEACHER_SLICES = 4;
-constexpr int TEACHER_THREADS = TEACHER_SLICES * MLP_H;
-constexpr int L3_SLICES = TEACHER_THREADS / MLP_OUT;  // layer 3: 64 K ranges of 4
-
-__global__ __launch_bounds__(TEACHER_THREADS) void k_mlp_teacher(const float* __restrict__ w,
-                                                                 const float* __restrict__ wt,
-                                                                 float* __restrict__ xf, __bf16* __restrict__ xb,
-                                                                 float* __restrict__ yt, uint64_t seed, uint32_t t,
-                                                                 int32_t tanh_out)
-{
-    __shared__ float x[MLP_IN], h1[MLP_H], h2[MLP_H], part[TEACHER_THREADS];
-    const int n = blockIdx.x, o = threadIdx.x % MLP_H, ks = threadIdx.x / MLP_H;
-    if (threadIdx.x < MLP_IN / 4) {
-        const int c4 = threadIdx.x;
-        float e[4];
-        normals4(seed, (uint32_t)(n * (MLP_IN / 4) + c4), 0, t, DOM_EVAL, e);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            x[4 * c4 + k] = e[k];
-            xf[n * MLP_IN + 4 * c4 + k] = e[k];
-            xb[n * MLP_IN + 4 * c4 + k] = (__bf16)e[k];
-        }
-    }
-    __syncthreads();
-    constexpr int K1 = MLP_IN / TEACHER_SLICES, K2 = MLP_H / TEACHER_SLICES, K3 = MLP_H / L3_SLICES;
-    float a = 0.f;
-#pragma unroll
-    for (int k = ks * K1; k < (ks + 1) * K1; ++k) a = fmaf(x[k], wt[OFF_W1 + k * MLP_H + o], a);
-    part[threadIdx.x] = a;
-    __syncthreads();
-    if (ks == 0) {
-        float z = part[o];
-        for (int j = 1; j < TEACHER_SLICES; ++j) z += part[j * MLP_H + o];
-        h1[o] = tanhf(z + w[OFF_B1 + o]);
-    }
-    __syncthreads();
-    a = 0.f;
-#pragma unroll 16
-    for (int k = ks * K2; k < (ks + 1) * K2; ++k) a = fmaf(h1[k], wt[OFF_W2 + k * MLP_H + o], a);
-    part[threadIdx.x] = a;
-    __syncthreads();
-    if (ks == 0) {
-        float z = part[o];
-        for (int j = 1; j < TEACHER_SLICES; ++j) z += part[j * MLP_H + o];
-        h2[o] = tanhf(z + w[OFF_B2 + o]);
-    }
-    __syncthreads();
-    {
-        const int o3 = threadIdx.x % MLP_OUT, k3 = threadIdx.x / MLP_OUT;
-        a = 0.f;
-#pragma unroll
-        for (int k = k3 * K3; k < (k3 + 1) * K3; ++k) a = fmaf(h2[k], wt[OFF_W3 + k * MLP_OUT + o3], a);
-        part[threadIdx.x] = a;
-    }
-    __syncthreads();
-    if (threadIdx.x < MLP_OUT) {
-        const int o3 = threadIdx.x;
-        float z = part[o3];
-        for (int j = 1; j < L3_SLICES; ++j) z += part[j * MLP_OUT + o3];
-        z += w[OFF_B3 + o3];
-        yt[n * MLP_OUT + o3] = tanh_out ? tanhf(z) : z;
-    }
-}
+// Per generation: X_t and Y_T, one workgroup per input row.
+__global__ __launch_bounds__(TEACHER_THREADS) void k_mlp_teacher(TeacherJob j) { teacher_row(j, blockIdx.x); }
 
 }  // namespace
 
@@ -478,31 +412,44 @@ hipError_t launch_mlp_setup(const float* teacher, void* scratch, hipStream_t s)
 
 size_t mlp_lds_bytes() { return sizeof(MlpSmem); }
 
-hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, const float* m, const float* teacher,
-                           void* scratch, float* fit, const float* hp, const float* svec, hipStream_t s,
-                           hipEvent_t ev_start, hipEvent_t ev_stop)
+TeacherJob mlp_teacher_job(const es_config& c, const float* teacher, void* scratch, uint32_t t)
 {
-    float* xf = static_cast<float*>(scratch);
-    __bf16* xb = reinterpret_cast<__bf16*>(xf + MLP_BATCH * MLP_IN);
-    float* yt = reinterpret_cast<float*>(xb + MLP_BATCH * MLP_IN);
-    const float* wt = reinterpret_cast<const float*>(static_cast<const char*>(scratch) + mlp_scratch_bytes() -
-                                                     sizeof(float) * MLP_NUM_PARAMS);
-    hipError_t e = launch_timed(k_mlp_teacher, dim3(MLP_BATCH), dim3(TEACHER_THREADS), 0, s, ev_start, nullptr, teacher,
-                                wt, xf, xb, yt, c.seed, t, c.mlp_tanh_out);
-    if (e != hipSuccess) return e;
+    TeacherJob j;
+    j.xf = static_cast<float*>(scratch);
+    j.xb = reinterpret_cast<__bf16*>(j.xf + MLP_BATCH * MLP_IN);
+    j.yt = reinterpret_cast<float*>(j.xb + MLP_BATCH * MLP_IN);
+    j.wt = reinterpret_cast<const float*>(static_cast<const char*>(scratch) + mlp_scratch_bytes() -
+                                          sizeof(float) * MLP_NUM_PARAMS);
+    j.w = teacher;
+    j.seed = c.seed;
+    j.t = t;
+    j.tanh_out = c.mlp_tanh_out;
+    return j;
+}
+
+hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, const float* m, const float* teacher,
+                           void* scratch, float* fit, const float* hp, const float* svec, bool run_teacher,
+                           hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop)
+{
+    const TeacherJob j = mlp_teacher_job(c, teacher, scratch, t);
+    const __bf16* xb = j.xb;
+    const float* yt = j.yt;
+    if (run_teacher) {
+        hipError_t e = launch_timed(k_mlp_teacher, dim3(MLP_BATCH), dim3(TEACHER_THREADS), 0, s, ev_start, nullptr, j);
+        if (e != hipSuccess) return e;
+        ev_start = nullptr;
+    }
     // more than 64 KB of LDS per workgroup: allowed per kernel (cheap to repeat)
     const void* kern = svec ? reinterpret_cast<const void*>(&k_eval_mlp<true>)
                             : reinterpret_cast<const void*>(&k_eval_mlp<false>);
-    e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(MlpSmem));
+    const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(MlpSmem));
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)g.P, (unsigned)g.R);
-    const __bf16* xbc = xb;
-    const float* ytc = yt;
     if (svec)
-        return launch_timed(k_eval_mlp<true>, grid, dim3(MLP_THREADS), (uint32_t)sizeof(MlpSmem), s, nullptr, ev_stop,
-                            m, xbc, ytc, fit, c.seed, t, g.Dp, g.N, g.P, hp, c.mlp_tanh_out, svec);
-    return launch_timed(k_eval_mlp<false>, grid, dim3(MLP_THREADS), (uint32_t)sizeof(MlpSmem), s, nullptr, ev_stop, m,
-                        xbc, ytc, fit, c.seed, t, g.Dp, g.N, g.P, hp, c.mlp_tanh_out, (const float*)nullptr);
+        return launch_timed(k_eval_mlp<true>, grid, dim3(MLP_THREADS), (uint32_t)sizeof(MlpSmem), s, ev_start, ev_stop,
+                            m, xb, yt, fit, c.seed, t, g.Dp, g.N, g.P, hp, c.mlp_tanh_out, svec);
+    return launch_timed(k_eval_mlp<false>, grid, dim3(MLP_THREADS), (uint32_t)sizeof(MlpSmem), s, ev_start, ev_stop,
+                        m, xb, yt, fit, c.seed, t, g.Dp, g.N, g.P, hp, c.mlp_tanh_out, (const float*)nullptr);
 }
 
 }  // namespace esmi

@@ -98,3 +98,32 @@ def test_mlp_rejects_fp32_mode():
     import paper_2212_04180_amd as P
     with pytest.raises(P.EsError):
         P.ES(_cfg(mlp_bf16=0))
+
+
+@pytest.mark.parametrize("strategy,popsize,runs", [(0, 1024, 1), (0, 8, 3), (1, 8, 1)])
+def test_teacher_in_gradient_launch_equals_standalone(strategy, popsize, runs):
+    """After the first generation the gradient launch also computes the next
+    generation's inputs and teacher outputs (OpenAI-ES; PGPE keeps the
+    separate teacher kernel).  A second handle restored to the same state,
+    whose evaluate therefore runs the teacher kernel, gives the same fitness
+    bits: the teacher's sums do not depend on the workgroup that runs them."""
+    import paper_2212_04180_amd as P
+    cfg = _cfg(popsize=popsize, num_runs=runs, strategy=strategy, sigma_lr=0.2, sigma_max_change=0.2)
+    a, b = P.ES(cfg), P.ES(cfg)
+    for _ in range(3):
+        a.step()
+    st = a.get_state()
+    b.set_state(st["m"], st["m1"], st["v"], st["t"])
+    if strategy == 1:
+        b.set_strategy_state(sigma=a.strategy_state()[0])
+    a.ask()
+    fa = a.eval()
+    b.ask()
+    fb = b.eval()
+    assert torch.equal(fa, fb)
+    # and the next generation, after a gradient launch on both handles
+    a.tell(fa)
+    b.tell(fb)
+    a.ask()
+    b.ask()
+    assert torch.equal(a.eval(), b.eval())

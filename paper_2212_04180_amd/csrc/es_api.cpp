@@ -85,12 +85,6 @@ struct es_handle {
     float* pdata = nullptr;  // [Dp] shift vector or teacher
     void* mlp_scratch = nullptr;  // MLP inputs and teacher outputs of the current generation
     int64_t teacher_t = -1;       // generation whose inputs and teacher outputs are in mlp_scratch
-    // Adam constants of the generations of one fused es_run, staged in pinned
-    // host memory and copied on the stream; the event guards reuse.
-    AdamConsts* adam_host = nullptr;
-    AdamConsts* adam_dev = nullptr;
-    int32_t adam_cap = 0;
-    hipEvent_t adam_evt = nullptr;
     int run_path = 0;  // 0 auto, 1 per-call kernels, 2 fused loop
     char err[512] = {0};
 };
@@ -273,38 +267,11 @@ int64_t env_i64(const char* name, int64_t dflt)
 void free_all(es_handle* h)
 {
     void* ptrs[] = {h->m, h->m1, h->v, h->best_x, h->grad, h->best_okey, h->best_f, h->best_j, h->table,
-                    h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->adam_dev, h->mlp_scratch,
+                    h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->mlp_scratch,
                     h->tell_part, h->hp[0], h->hp[1], h->pen, h->bfold, h->sig, h->vel, h->gbuf,
                     h->gpart, h->vpart, h->elite, h->cw, h->cmaC, h->zw, h->qd};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
-    if (h->adam_host) (void)hipHostFree(h->adam_host);
-    if (h->adam_evt) (void)hipEventDestroy(h->adam_evt);
-}
-
-// Upload the Adam constants of generations t .. t+T-1 for the fused loop.
-es_status stage_adam(es_handle* h, int32_t T)
-{
-    if (h->adam_evt) ES_HIP(h, hipEventSynchronize(h->adam_evt), "wait for the previous constants upload");
-    if (T > h->adam_cap) {
-        if (h->adam_host) (void)hipHostFree(h->adam_host);
-        if (h->adam_dev) (void)hipFree(h->adam_dev);
-        h->adam_host = nullptr;
-        h->adam_dev = nullptr;
-        h->adam_cap = 0;
-        ES_HIP(h, hipHostMalloc(reinterpret_cast<void**>(&h->adam_host), sizeof(AdamConsts) * (size_t)T),
-               "pinned staging buffer");
-        ES_HIP(h, hipMalloc(reinterpret_cast<void**>(&h->adam_dev), sizeof(AdamConsts) * (size_t)T),
-               "Adam constants buffer");
-        h->adam_cap = T;
-    }
-    if (!h->adam_evt) ES_HIP(h, hipEventCreateWithFlags(&h->adam_evt, hipEventDisableTiming), "event");
-    for (int32_t i = 0; i < T; ++i) h->adam_host[i] = adam_consts(h->cfg, h->t + i);
-    ES_HIP(h, hipMemcpyAsync(h->adam_dev, h->adam_host, sizeof(AdamConsts) * (size_t)T, hipMemcpyHostToDevice,
-                             h->stream),
-           "upload Adam constants");
-    ES_HIP(h, hipEventRecord(h->adam_evt, h->stream), "record event");
-    return ES_OK;
 }
 
 es_status enqueue_tell(es_handle* h, const float* fitness, float* gen_best)
@@ -575,13 +542,23 @@ es_status es_run(es_handle* h, int32_t T, float* log)
     // fused loop on a geometry es_run would not fuse sums in its own order
     const bool fused = h->run_path == 2 ? fused_ok : h->run_path == 1 ? false : fused_by_default(h->g, h->plan, h->cfg);
     if (fused) {
-        es_status s = stage_adam(h, T);
-        if (s != ES_OK) return s;
-        ES_HIP(h, launch_run_fused(h->g, h->cfg, h->plan, (uint32_t)h->t, T, h->adam_dev, h->m, h->m1, h->v,
-                                   h->best_x, h->best_okey, h->best_f, h->pdata, h->table, log,
-                                   h->hp[h->hp_cur], h->stream),
-               "fused generation loop");
-        h->t += T;
+        // launches of up to FUSED_MAX_T generations, each with its generations'
+        // Adam bias corrections in the kernel arguments
+        float bcorr[FUSED_MAX_T][2];
+        for (int32_t done = 0; done < T;) {
+            const int32_t Tc = std::min(T - done, FUSED_MAX_T);
+            for (int32_t i = 0; i < Tc; ++i) {
+                const AdamConsts a = adam_consts(h->cfg, h->t + i);
+                bcorr[i][0] = a.bc1;
+                bcorr[i][1] = a.bc2;
+            }
+            ES_HIP(h, launch_run_fused(h->g, h->cfg, h->plan, (uint32_t)h->t, Tc, adam_consts(h->cfg, h->t), bcorr,
+                                       h->m, h->m1, h->v, h->best_x, h->best_okey, h->best_f, h->pdata, h->table,
+                                       log ? log + (int64_t)done * h->g.R : nullptr, h->hp[h->hp_cur], h->stream),
+                   "fused generation loop");
+            h->t += Tc;
+            done += Tc;
+        }
         return ES_OK;
     }
     for (int32_t i = 0; i < T; ++i) {

@@ -125,10 +125,14 @@ int32_t tell_slices(const Geometry& g);
 constexpr size_t FUSED_MAX_LDS = 60 * 1024;
 size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e);
 bool fused_supported(const Geometry& g, const EvalPlan& e, const es_config& c);
+// Generations per fused launch: their Adam bias corrections (bcorr[i] =
+// {bc1, bc2} of generation t0 + i) travel in the kernel arguments, so a
+// launch needs no staging buffer; es_run splits longer runs into launches.
+constexpr int32_t FUSED_MAX_T = 256;
 hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t0, int32_t T,
-                            const AdamConsts* adam, float* m, float* m1, float* v, float* best_x,
-                            uint32_t* best_okey, float* best_f, const float* pdata, const float* table, float* log,
-                            float* hp, hipStream_t s);
+                            const AdamConsts& ac, const float (*bcorr)[2], float* m, float* m1, float* v,
+                            float* best_x, uint32_t* best_okey, float* best_f, const float* pdata, const float* table,
+                            float* log, float* hp, hipStream_t s);
 
 // Neuroevolution problem (64-256-256-16 MLP vs a teacher).
 constexpr int64_t MLP_NUM_PARAMS = 86544;

@@ -30,6 +30,9 @@
 // into fp64 accumulators.
 #include <hip/hip_runtime.h>
 #include <math.h>
+#include <stddef.h>
+
+#include <type_traits>
 
 #include "es_device.hpp"
 #include "es_internal.hpp"
@@ -1193,7 +1196,6 @@ struct FusedArgs {
     float* best_f;
     const float* pdata;
     const float* table;
-    const AdamConsts* adam;  // [T], for generations t0 .. t0+T-1
     float* log;              // [T][R] or null
     uint64_t seed;
     uint32_t t0;
@@ -1207,7 +1209,10 @@ struct FusedArgs {
     int32_t maximize, raw;
     float* hp;               // [2][R] sigma, lr: read at the start, the schedule's values written at the end
     float sigma_decay, sigma_final, lr_decay, lr_final;
+    AdamConsts ac;           // the generation-independent Adam constants
+    float bcorr[FUSED_MAX_T][2];  // bias corrections bc1, bc2 of generations t0 .. t0+T-1
 };
+static_assert(std::is_standard_layout<FusedArgs>::value, "offsetof(FusedArgs, bcorr) is used on the device");
 
 template <int PROB>
 __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
@@ -1255,8 +1260,18 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
 
     for (int32_t it = 0; it < a.T; ++it) {
         const uint32_t t = a.t0 + (uint32_t)it;
-        // this generation's Adam constants, fetched while the population is scored
-        const AdamConsts ac = a.adam[it];
+        // this generation's Adam constants, from the kernel arguments: the
+        // bias corrections are read through the kernarg segment pointer (the
+        // launch's only explicit argument starts at its offset 0), because a
+        // dynamic index into the by-value argument made the compiler hold the
+        // array in VGPRs (92 -> 155 per lane, five waves per SIMD -> three)
+        AdamConsts ac = a.ac;
+        {
+            const float* kb = reinterpret_cast<const float*>((const char*)__builtin_amdgcn_kernarg_segment_ptr() +
+                                                             offsetof(FusedArgs, bcorr));
+            ac.bc1 = kb[2 * it];
+            ac.bc2 = kb[2 * it + 1];
+        }
         // evaluate: items (pair, chunk)
         const int64_t items = (int64_t)a.P * a.nchunks;
         for (int64_t i = threadIdx.x; i < items; i += blockDim.x) {
@@ -1704,13 +1719,19 @@ bool fused_supported(const Geometry& g, const EvalPlan& e, const es_config& c)
 }
 
 hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t0, int32_t T,
-                            const AdamConsts* adam, float* m, float* m1, float* v, float* best_x,
-                            uint32_t* best_okey, float* best_f, const float* pdata, const float* table, float* log,
-                            float* hp, hipStream_t s)
+                            const AdamConsts& ac, const float (*bcorr)[2], float* m, float* m1, float* v,
+                            float* best_x, uint32_t* best_okey, float* best_f, const float* pdata, const float* table,
+                            float* log, float* hp, hipStream_t s)
 {
+    if (T < 1 || T > FUSED_MAX_T) return hipErrorInvalidValue;
     FusedArgs a;
     a.m = m; a.m1 = m1; a.v = v; a.best_x = best_x; a.best_okey = best_okey; a.best_f = best_f;
-    a.pdata = pdata; a.table = table; a.adam = adam; a.log = log;
+    a.pdata = pdata; a.table = table; a.log = log;
+    a.ac = ac;
+    for (int32_t i = 0; i < T; ++i) {
+        a.bcorr[i][0] = bcorr[i][0];
+        a.bcorr[i][1] = bcorr[i][1];
+    }
     a.seed = c.seed; a.t0 = t0; a.T = T; a.D = g.D; a.nb = g.nb; a.N = g.N; a.P = g.P; a.R = g.R;
     a.bc = e.bc; a.nchunks = e.nchunks; a.ps = tell_slices(g); a.ra = c.rastrigin_a;
     a.add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;

@@ -214,10 +214,13 @@ def test_raw_shaping_linear_gradient_converges_to_a():
 
 
 @pytest.mark.parametrize("prob,D,N,R,T", [("sphere", 16, 32, 1, 40), ("rastrigin", 100, 64, 8, 25),
-                                          ("rosenbrock", 37, 10, 3, 30), ("shifted", 1001, 8, 2, 6)])
+                                          ("rosenbrock", 37, 10, 3, 30), ("shifted", 1001, 8, 2, 6),
+                                          ("sphere", 16, 32, 2, 600)])
 def test_fused_loop_matches_per_call_bits(prob, D, N, R, T, monkeypatch):
     """The one-launch loop (one workgroup per run) repeats the per-call
-    kernels' arithmetic in the same order: identical bits."""
+    kernels' arithmetic in the same order: identical bits.  T = 600 takes
+    three launches (at most 256 generations each, their Adam bias
+    corrections in the kernel arguments) and the log of each."""
     P = _P()
     pmap = {"sphere": P.PROB_SPHERE, "shifted": P.PROB_SHIFTED_SPHERE, "rosenbrock": P.PROB_ROSENBROCK,
             "rastrigin": P.PROB_RASTRIGIN}

@@ -100,15 +100,18 @@ def test_mlp_rejects_fp32_mode():
         P.ES(_cfg(mlp_bf16=0))
 
 
-@pytest.mark.parametrize("strategy,popsize,runs", [(0, 1024, 1), (0, 8, 3), (1, 8, 1)])
-def test_teacher_in_gradient_launch_equals_standalone(strategy, popsize, runs):
+@pytest.mark.parametrize("strategy,popsize,runs,optimizer", [(0, 1024, 1, 0), (0, 8, 3, 0), (0, 8, 2, 1), (1, 8, 1, 0),
+                                                        (0, 4, 1, 0)])
+def test_teacher_in_gradient_launch_equals_standalone(strategy, popsize, runs, optimizer):
     """After the first generation the gradient launch also computes the next
-    generation's inputs and teacher outputs (OpenAI-ES; PGPE keeps the
-    separate teacher kernel).  A second handle restored to the same state,
-    whose evaluate therefore runs the teacher kernel, gives the same fitness
-    bits: the teacher's sums do not depend on the workgroup that runs them."""
+    generation's inputs and teacher outputs (OpenAI-ES with Adam or ClipUp;
+    PGPE, and workgroups under 256 threads (N = 4), keep the separate teacher
+    kernel).  A second handle restored to the same state, whose evaluate
+    therefore runs the teacher kernel, gives the same fitness bits: the
+    teacher's sums do not depend on the workgroup that runs them."""
     import paper_2212_04180_amd as P
-    cfg = _cfg(popsize=popsize, num_runs=runs, strategy=strategy, sigma_lr=0.2, sigma_max_change=0.2)
+    cfg = _cfg(popsize=popsize, num_runs=runs, strategy=strategy, optimizer=optimizer, sigma_lr=0.2,
+               sigma_max_change=0.2, clipup_max_speed=0.05, clipup_momentum=0.9)
     a, b = P.ES(cfg), P.ES(cfg)
     for _ in range(3):
         a.step()
@@ -116,6 +119,8 @@ def test_teacher_in_gradient_launch_equals_standalone(strategy, popsize, runs):
     b.set_state(st["m"], st["m1"], st["v"], st["t"])
     if strategy == 1:
         b.set_strategy_state(sigma=a.strategy_state()[0])
+    if optimizer == 1:
+        b.set_strategy_state(velocity=a.strategy_state(sigma=False, velocity=True)[1])
     a.ask()
     fa = a.eval()
     b.ask()

@@ -44,3 +44,39 @@ def test_tiny_and_ragged_geometries_match_oracle(name, geom):
     strategy, optimizer = STRATS[name]
     print("case", name, geom, flush=True)
     stagecheck.run(P, _cfg(strategy, optimizer, *geom), 6)
+
+
+def test_largest_run_count_fused_and_per_call(monkeypatch):
+    """num_runs = 65535, the largest accepted (runs are the y dimension of the
+    per-call grids): es_run through the fused loop (one workgroup per run) and
+    through the per-call kernels gives the same bits, and sampled runs score
+    as standalone oracle runs with key seed + r."""
+    import dataclasses
+
+    import numpy as np
+    import torch
+
+    from inputs import to_oracle
+    from oracle import oracle as O
+    P = _P()
+    cfg = P.ESConfig(num_dims=5, popsize=2, num_runs=65535, sigma=0.3, lr=0.05, seed=0, init_lo=-2.0, init_hi=2.0,
+                     problem=P.PROB_ROSENBROCK)
+    out = {}
+    for path in ("1", "2"):
+        monkeypatch.setenv("ESMI_RUN_PATH", path)
+        es = P.ES(cfg)
+        log = es.run(3)
+        st = es.get_state()
+        torch.cuda.synchronize()
+        out[path] = [t.cpu().numpy() for t in (log, st["m"], st["m1"], st["v"])]
+    for a, b in zip(out["1"], out["2"]):
+        np.testing.assert_array_equal(a, b)
+    es = P.ES(cfg)
+    es.ask()
+    f = es.eval()
+    torch.cuda.synchronize()
+    f = f.cpu().numpy()
+    for r in (0, 1, 40000, 65534):
+        oc = dataclasses.replace(to_oracle(cfg), num_runs=1, seed=r)
+        fr = O.OracleES(oc).eval()[0]
+        assert np.all(np.abs(f[r] - fr) <= 1e-5 * np.abs(fr)), (r, f[r], fr)

@@ -326,12 +326,31 @@ es_status enqueue_eval(es_handle* h, float* fit, hipEvent_t ev_start = nullptr, 
     return ES_OK;
 }
 
+// Device rows [R][D] <-> state rows [R][Dp]: one copy when the rows are
+// contiguous on both sides (Dp = D, or one run), one 2D copy for pitches the
+// runtime takes (under 2 GiB), else a copy per row.
+constexpr size_t kMaxCopyPitch = ((size_t)1 << 31) - 1;
+
+hipError_t copy_rows(const Geometry& g, float* dst, size_t dpitch, const float* src, size_t spitch, hipStream_t s)
+{
+    const size_t width = (size_t)g.D * 4;
+    if (g.R == 1 || g.Dp == g.D)
+        return hipMemcpyAsync(dst, src, width * (size_t)g.R, hipMemcpyDeviceToDevice, s);
+    if (dpitch <= kMaxCopyPitch && spitch <= kMaxCopyPitch)
+        return hipMemcpy2DAsync(dst, dpitch, src, spitch, width, (size_t)g.R, hipMemcpyDeviceToDevice, s);
+    for (int32_t r = 0; r < g.R; ++r) {
+        const hipError_t e = hipMemcpyAsync(reinterpret_cast<char*>(dst) + (size_t)r * dpitch,
+                                            reinterpret_cast<const char*>(src) + (size_t)r * spitch, width,
+                                            hipMemcpyDeviceToDevice, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 es_status copy_rows_out(es_handle* h, float* dst, const float* src)
 {
     const Geometry& g = h->g;
-    ES_HIP(h, hipMemcpy2DAsync(dst, (size_t)g.D * 4, src, (size_t)g.Dp * 4, (size_t)g.D * 4, (size_t)g.R,
-                               hipMemcpyDeviceToDevice, h->stream),
-           "copy out");
+    ES_HIP(h, copy_rows(g, dst, (size_t)g.D * 4, src, (size_t)g.Dp * 4, h->stream), "copy out");
     return ES_OK;
 }
 
@@ -340,9 +359,7 @@ es_status copy_rows_in(es_handle* h, float* dst, const float* src)
     const Geometry& g = h->g;
     if (g.Dp != g.D)
         ES_HIP(h, hipMemsetAsync(dst, 0, (size_t)g.Dp * g.R * 4, h->stream), "clear padding");
-    ES_HIP(h, hipMemcpy2DAsync(dst, (size_t)g.Dp * 4, src, (size_t)g.D * 4, (size_t)g.D * 4, (size_t)g.R,
-                               hipMemcpyDeviceToDevice, h->stream),
-           "copy in");
+    ES_HIP(h, copy_rows(g, dst, (size_t)g.Dp * 4, src, (size_t)g.D * 4, h->stream), "copy in");
     return ES_OK;
 }
 

@@ -80,3 +80,14 @@ def test_largest_run_count_fused_and_per_call(monkeypatch):
         oc = dataclasses.replace(to_oracle(cfg), num_runs=1, seed=r)
         fr = O.OracleES(oc).eval()[0]
         assert np.all(np.abs(f[r] - fr) <= 1e-5 * np.abs(fr)), (r, f[r], fr)
+
+
+@pytest.mark.parametrize("name", list(STRATS))
+def test_largest_population_matches_oracle(name):
+    """N = 16384, the largest accepted (the rank kernel's keys fill 64 KB of
+    LDS), D = 37 (ragged), two runs, stage by stage."""
+    P = _P()
+    strategy, optimizer = STRATS[name]
+    cfg = _cfg(strategy, optimizer, 37, 16384, 2)
+    print("case", name, flush=True)
+    stagecheck.run(P, cfg, 2)

@@ -182,12 +182,14 @@ es_status es_ask(es_handle* h, float* x_out);
  * for this generation; ES_ERR_UNSUPPORTED for ES_PROB_NONE. */
 es_status es_eval(es_handle* h, float* fitness_out);
 
-/* es_eval that also times itself: start_event and stop_event (hipEvent_t
- * handles the caller created with timing enabled; either may be NULL) are
- * recorded by the dispatches themselves (hipExtLaunchKernel), at the start
- * of the evaluate's first kernel and at the end of its last one, so the
- * stream carries no marker between kernels.  hipEventElapsedTime of the two
- * gives the evaluate kernels' time.  Same results as es_eval. */
+/* es_eval that also times its main kernel: start_event and stop_event
+ * (hipEvent_t handles the caller created with timing enabled; either may be
+ * NULL) are recorded by that kernel's dispatch itself (hipExtLaunchKernel),
+ * at its start and at its end, so the stream carries no marker packet.  The
+ * main kernel is the fused sample + evaluate (the benchmark problems; the
+ * per-chunk sums are reduced by a second kernel after it) or the MLP forward
+ * (a teacher kernel, when one runs, goes before it).  hipEventElapsedTime of
+ * the two gives that kernel's time.  Same results as es_eval. */
 es_status es_eval_timed(es_handle* h, float* fitness_out, void* start_event, void* stop_event);
 
 /* tell (Sec. 2.1 step 3): fitness shaping (es_shaping; with weight decay the

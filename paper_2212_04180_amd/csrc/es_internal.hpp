@@ -57,8 +57,8 @@ hipError_t launch_cma_scale(const Geometry& g, float* svec, const float* C, cons
 // svec: per-dimension sigma [R][Dp] (PGPE, SNES) or null.
 hipError_t launch_ask(const Geometry& g, const es_config& c, uint32_t t, const float* m, float* x,
                       const float* hp, const float* svec, hipStream_t s);
-// ev_start / ev_stop (either may be null): events that record the dispatch of
-// the first kernel and the end of the last one (es_eval_timed).
+// ev_start / ev_stop (either may be null): events that record the start and
+// the end of the main evaluate kernel (es_eval_timed).
 hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t,
                             const float* m, const float* pdata, float* partial, float* fit,
                             const float* hp, const float* svec, double div, hipStream_t s,

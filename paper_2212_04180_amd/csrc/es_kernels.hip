@@ -1530,7 +1530,7 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
     const int sm = c.strategy == ES_STRAT_SEP_CMA ? SM_INDEP : svec ? SM_VEC : SM_SCALAR;
     const float* sv = sm == SM_SCALAR ? nullptr : svec;
 #define ES_EVAL_LAUNCH(PROB, SM)                                                                                \
-    launch_timed(k_eval_bbob<PROB, SM>, grid, block, 0, s, ev_start, nullptr, m, pdata, partial, c.seed, t, g.D, \
+    launch_timed(k_eval_bbob<PROB, SM>, grid, block, 0, s, ev_start, ev_stop, m, pdata, partial, c.seed, t, g.D, \
                  g.nb, g.N, g.P, e.bc, e.nchunks, e.n_pg, hp, c.rastrigin_a, sv)
 #define ES_EVAL_PROB(PROB)                                                                                      \
     (sm == SM_INDEP ? ES_EVAL_LAUNCH(PROB, SM_INDEP) : sm == SM_VEC ? ES_EVAL_LAUNCH(PROB, SM_VEC)               \
@@ -1548,7 +1548,7 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
     if (err != hipSuccess) return err;
     const double add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;
     return launch_timed(k_eval_reduce, dim3((unsigned)((g.N + 63) / 64), (unsigned)g.R), dim3(64 * RED_SLICES), 0, s,
-                        nullptr, ev_stop, (const float*)partial, fit, g.N, g.R, e.nchunks, add, div);
+                        nullptr, nullptr, (const float*)partial, fit, g.N, g.R, e.nchunks, add, div);
 }
 
 hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* pen,

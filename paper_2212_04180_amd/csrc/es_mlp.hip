@@ -435,9 +435,8 @@ hipError_t launch_eval_mlp(const Geometry& g, const es_config& c, uint32_t t, co
     const __bf16* xb = j.xb;
     const float* yt = j.yt;
     if (run_teacher) {
-        hipError_t e = launch_timed(k_mlp_teacher, dim3(MLP_BATCH), dim3(TEACHER_THREADS), 0, s, ev_start, nullptr, j);
+        hipError_t e = launch_timed(k_mlp_teacher, dim3(MLP_BATCH), dim3(TEACHER_THREADS), 0, s, nullptr, nullptr, j);
         if (e != hipSuccess) return e;
-        ev_start = nullptr;
     }
     // more than 64 KB of LDS per workgroup: allowed per kernel (cheap to repeat)
     const void* kern = svec ? reinterpret_cast<const void*>(&k_eval_mlp<true>)

@@ -271,7 +271,7 @@ def test_two_handles_on_their_own_streams():
 @pytest.mark.parametrize("name", ["rosenbrock_d1000", "mlp_teacher"])
 def test_eval_timed_equals_eval_and_times_the_kernels(name):
     """es_eval_timed: the same fitness bits as es_eval, and its events (recorded
-    by the first and last evaluate dispatch) span a positive time that fits
+    by the main evaluate kernel's dispatch) span a positive time that fits
     inside events recorded on the stream around the call."""
     from paper_2212_04180_amd import workloads
     P = _P()

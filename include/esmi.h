@@ -189,7 +189,8 @@ es_status es_eval(es_handle* h, float* fitness_out);
  * main kernel is the fused sample + evaluate (the benchmark problems; the
  * per-chunk sums are reduced by a second kernel after it) or the MLP forward
  * (a teacher kernel, when one runs, goes before it).  hipEventElapsedTime of
- * the two gives that kernel's time.  Same results as es_eval. */
+ * the two gives that kernel's time.  Same results as es_eval.  A timing
+ * aid: not meant for a stream under capture. */
 es_status es_eval_timed(es_handle* h, float* fitness_out, void* start_event, void* stop_event);
 
 /* tell (Sec. 2.1 step 3): fitness shaping (es_shaping; with weight decay the

@@ -50,6 +50,7 @@ constexpr int TELL_LANES = 64;    // Philox blocks per tell workgroup
 constexpr int TELL_MAX_PS = 16;   // pair slices per tell workgroup (one wave each)
 constexpr int TELL_GROUP = 16;    // fp32 pairs folded into the fp64 sum at once
 constexpr int FUSED_WG = 256;     // threads of the fused multi-generation workgroup
+constexpr int FUSED_PRIO = 1;     // wave priority of the fused loop's short phases
 
 // MLP 64-256-256-16, flattened [out][in] per layer then the bias.  Returns
 // 1/sqrt(fan_in) for a weight and 0 for a bias.
@@ -1272,7 +1273,12 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             ac.bc1 = kb[2 * it];
             ac.bc2 = kb[2 * it + 1];
         }
-        // evaluate: items (pair, chunk)
+        // evaluate: items (pair, chunk).  The evaluate and gradient phases run
+        // at the base wave priority, the short phases between them (fitness,
+        // ranks, update: latency chains on a few lanes) at a raised one, so
+        // that the long phases of the other runs' workgroups on the same CU
+        // fill the issue slots around them instead of delaying them.
+        __builtin_amdgcn_s_setprio(0);
         const int64_t items = (int64_t)a.P * a.nchunks;
         for (int64_t i = threadIdx.x; i < items; i += blockDim.x) {
             const int32_t p = (int32_t)(i % a.P);
@@ -1285,6 +1291,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             part[c * a.N + p + a.P] = (float)accm;
         }
         __syncthreads();
+        __builtin_amdgcn_s_setprio(FUSED_PRIO);
         // fitness in the reduce kernel's order, and order keys
         const int nq = a.nchunks < RED_SLICES ? (int)a.nchunks : RED_SLICES;  // slices beyond add 0
         for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) {
@@ -1345,6 +1352,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             }
         }
         __syncthreads();
+        __builtin_amdgcn_s_setprio(0);
         // tell: items (block, pair slice), slices summed in order, then Adam
         for (int64_t i = threadIdx.x; i < (int64_t)a.ps * a.nb; i += blockDim.x) {
             const int32_t s = (int32_t)(i / a.nb);
@@ -1357,6 +1365,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             for (int k = 0; k < 4; ++k) red[((int64_t)s * a.nb + b) * 4 + k] = a64[k];
         }
         __syncthreads();
+        __builtin_amdgcn_s_setprio(FUSED_PRIO);
         const int32_t jb = best_j;
         const double inv_ns = 1.0 / (2.0 * (double)a.P * (double)sigma);  // 1 / (N sigma)
         for (int64_t i = threadIdx.x; i < 4 * a.nb; i += blockDim.x) {

@@ -138,7 +138,9 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        _lib = ctypes.CDLL(build())
+        # ESMI_ORACLE_LIB: an alternative build of the same source (the
+        # sanitizer test loads one compiled with ASan/UBSan)
+        _lib = ctypes.CDLL(os.environ.get("ESMI_ORACLE_LIB") or build())
         P = ctypes.POINTER
         f32, u32, i32, i64, u64 = ctypes.c_float, ctypes.c_uint32, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
         pc = P(_Cfg)

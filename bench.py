@@ -30,13 +30,14 @@ MLP_FLOPS_PER_MEMBER = 2 * 256 * (64 * 256 + 256 * 256 + 256 * 16)
 # relative to v_fma_f32 (1): v_mad_u64_u32, v_mul_hi/lo_u32, v_cvt_*, fp64
 # fma/add 2; v_log/v_sqrt/v_sin/v_cos 4; bitwise, shifts, fp32 add/mul/fma 1.
 #   Philox-4x32-10: 20 x 32x32->64 product (2) + 20 x three-input xor (1)      = 60
-#   Box-Muller: 4 shift + 4 cvt (2) + 2 (+1) + 4 x 2^-24 scale + 2 log2 (4)
-#     + 2 x (-2 ln 2) + 2 sqrt (4) + 2 sin (4) + 2 cos (4) + 4 (r * trig)      = 56
+#   Box-Muller: 4 shift + 4 cvt (2) + 4 x 2^-24 scale (the radius words'
+#     +1 folded into their scale as one fma) + 2 log2 (4) + 2 x (-2 ln 2)
+#     + 2 sqrt (4) + 2 sin (4) + 2 cos (4) + 4 (r * trig)                      = 54
 #   members (both signs): 8 fma for x plus the problem's terms, and the fold
 #     of each member's fp32 block sum into fp64 (2 x (cvt 2 + add 2) = 8):
 #     sphere 8 squares -> 24; shifted sphere 8 sub + 8 squares -> 32;
 #     Rosenbrock 6 ops x 4 terms x 2 -> 64; Rastrigin 9 ops x 8 -> 88.
-PHILOX_BM = 60 + 56
+PHILOX_BM = 60 + 54
 EVAL_SLOTS_PER_PAIR_BLOCK = {"sphere": PHILOX_BM + 24, "shifted_sphere": PHILOX_BM + 32,
                              "rosenbrock": PHILOX_BM + 64, "rastrigin": PHILOX_BM + 88}
 # tell: Philox + Box-Muller + 4 fma (w * eps) + the fp64 fold every 16 pairs

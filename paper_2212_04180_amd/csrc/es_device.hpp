@@ -91,9 +91,12 @@ __device__ __forceinline__ uint4 philox4x32_10(uint32_t k0, uint32_t k1, uint32_
 }
 
 // Box-Muller radius sqrt(-2 ln u) = sqrt(-2 ln2 * log2 u), u in (0, 1].
+// u = ((w >> 8) + 1) 2^-24 is formed as one fma of the integer w >> 8 (exact
+// in fp32, below 2^24): the exact product plus 2^-24 is at most 1 and a
+// multiple of 2^-24, so the fma rounds nothing and no integer add is needed.
 __device__ __forceinline__ float bm_radius(uint32_t w)
 {
-    const float u = (float)((w >> 8) + 1u) * 0x1p-24f;  // exact
+    const float u = __builtin_fmaf((float)(w >> 8), 0x1p-24f, 0x1p-24f);
     return __builtin_amdgcn_sqrtf(-1.38629436111989061883f * __builtin_amdgcn_logf(u));
 }
 

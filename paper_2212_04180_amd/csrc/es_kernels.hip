@@ -1467,10 +1467,13 @@ EvalPlan eval_plan(const Geometry& g, int64_t bc_override)
     if (bc_override > 0) {
         bc = bc_override;
     } else {
-        // About 16384 waves in flight over the launch (two rounds of a full
-        // chip at 8 waves per SIMD), with at least EVAL_FOLD blocks per chunk.
+        // About 24576 waves over the launch (three rounds of a full chip at
+        // 8 waves per SIMD), with at least EVAL_FOLD blocks per chunk: the
+        // shorter workgroups of three rounds leave a shorter tail while the
+        // last round drains than those of two (D = 1e6, N = 2048: evaluate
+        // 536 -> 524 us; four rounds gain no more and add partials to sum).
         const int64_t waves_per_chunk = (int64_t)e.n_pg * (e.wg / 64) * g.R;
-        int64_t nch = (16384 + waves_per_chunk - 1) / waves_per_chunk;
+        int64_t nch = (24576 + waves_per_chunk - 1) / waves_per_chunk;
         if (nch < 1) nch = 1;
         bc = (g.nb + nch - 1) / nch;
         if (bc < EVAL_FOLD) bc = EVAL_FOLD;

@@ -1,10 +1,15 @@
 """Throughput of one batched OpenAI-ES generation (ask + evaluate + tell) on one MI355X.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+                [--no-other-workloads]
 
 A step is one whole generation of the per-call path (es_ask, es_eval,
 es_tell) on the synthetic workload (default: shifted sphere, D = 1e6,
-N = 2048, R = 1).  Prints ONE JSON line on stdout; diagnostics go to stderr.
+N = 2048, R = 1).  With the default workload the same run also times the
+other four workloads (the neuroevolution MLP through the per-call path; the
+sphere D = 16, Rosenbrock D = 1000 and R = 1024 Rastrigin runs through
+es_run) under "other_workloads".  Prints ONE JSON line on stdout;
+diagnostics go to stderr.
 """
 from __future__ import annotations
 
@@ -57,13 +62,15 @@ def kernel_source_sha256():
     return h.hexdigest()
 
 
-def profiled_traffic(workload, key="eval_hbm_bytes_per_launch"):
-    """HBM bytes per launch of the evaluate kernel from the committed rocprofv3
-    counter summary of this workload, or None if there is none or the kernel
-    sources changed since the counters were taken.  The default key is the
-    copy-calibrated FETCH_SIZE + WRITE_SIZE; eval_hbm_bytes_request_sized
-    prices each read request at its size (the evaluate kernel's scalar-cache
-    reads are 64-B requests, the copy's 128-B)."""
+def profiled_traffic(workload, key="eval_hbm_bytes_request_sized", cast=int):
+    """A figure of the evaluate kernel from the committed rocprofv3 counter
+    summary of this workload, or None if there is none or the kernel sources
+    changed since the counters were taken.  The default key is the HBM bytes
+    per launch with each read request priced at its size (the evaluate
+    kernel's scalar-cache reads are 64-B requests, the copy's 128-B);
+    eval_hbm_bytes_per_launch is the copy-calibrated FETCH_SIZE + WRITE_SIZE,
+    eval_valu_issued_slots_per_pair_block the issued VALU slots read from
+    SQ_INSTS_VALU and the instruction mix."""
     path = os.path.join(ROOT, "profiles", f"k_eval_bbob_{workload}.txt")
     if not os.path.exists(path):
         return None
@@ -76,7 +83,7 @@ def profiled_traffic(workload, key="eval_hbm_bytes_per_launch"):
     if kv.get("kernel_source_sha256") != kernel_source_sha256():
         return None
     try:
-        return int(kv[key])
+        return cast(kv[key])
     except (KeyError, ValueError):
         return None
 
@@ -90,6 +97,8 @@ def parse():
     ap.add_argument("--path", choices=["percall", "run"], default="percall",
                     help="percall: es_ask/es_eval/es_tell per generation; run: es_run over all K generations")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="time only --workload (the default workload also times the other four)")
     ap.add_argument("--cpu-sample-dims", type=int, default=0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter calibration)")
@@ -103,8 +112,29 @@ def log(*a):
 def cpu_baseline(cfg, sample_dims):
     """The oracle as it stands, on the host cores, on a bounded sample of the
     workload: one whole generation of the same strategy restricted to its
-    first `sample_dims` dims (same N, R, problem).  Scaled to member-dims/s."""
+    first `sample_dims` dims (same N, R, problem), once on one thread and
+    once on all the threads OpenMP is given (the oracle's parallel loops give
+    the same bits).  Scaled to member-dims/s; the all-threads figure is the
+    value, `cores` the threads it used, `host_cores` the cores this process
+    may run on."""
     from oracle import oracle as O
+    legs = {}
+    for threads in (1, 0):
+        O.set_threads(threads)
+        used = O.get_threads()
+        legs[threads] = (used, _oracle_generation(O, cfg, sample_dims))
+    O.set_threads(0)
+    md = cfg.num_runs * cfg.popsize * sample_dims
+    (n1, dt1), (nt, dtn) = legs[1], legs[0]
+    return {"value": md / dtn, "unit": "member-dims/s", "cores": nt, "kind": "oracle",
+            "host_cores": len(os.sched_getaffinity(0)),
+            "single_thread": {"value": md / dt1, "seconds": dt1},
+            "sample": f"1 generation (ask+eval+tell) of the same workload on its first {sample_dims} dims "
+                      f"(R={cfg.num_runs}, N={cfg.popsize}): {dtn:.2f} s on {nt} threads, "
+                      f"{dt1:.2f} s on one"}
+
+
+def _oracle_generation(O, cfg, sample_dims):
     oc = O.OracleConfig(num_dims=sample_dims, popsize=cfg.popsize, num_runs=cfg.num_runs, sigma=cfg.sigma,
                         lr=cfg.lr, beta1=cfg.beta1, beta2=cfg.beta2, eps=cfg.eps, maximize=cfg.maximize,
                         shaping=cfg.shaping, seed=cfg.seed, init=cfg.init, init_lo=cfg.init_lo,
@@ -118,33 +148,19 @@ def cpu_baseline(cfg, sample_dims):
     es = O.OracleES(oc)
     t0 = time.perf_counter()
     es.step()
-    dt = time.perf_counter() - t0
-    md = cfg.num_runs * cfg.popsize * sample_dims
-    return {"value": md / dt, "unit": "member-dims/s", "cores": 1, "kind": "oracle",
-            "sample": f"1 generation (ask+eval+tell) of the same workload on its first {sample_dims} dims "
-                      f"(R={cfg.num_runs}, N={cfg.popsize}), single-threaded, {dt:.1f} s"}
+    return time.perf_counter() - t0
 
 
-def main():
-    args = parse()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: the library runs every strategy on a single MI355X and "
-              "sharding over several GPUs is not implemented", file=sys.stderr)
-        sys.exit(2)
-    import torch
-
-    import paper_2212_04180_amd as P
+def time_workload(P, torch, name, K, W, path, dev, stream, copy_mib=0):
+    """Times K generations of workload `name` (after W warm-up generations)
+    through the per-call path or es_run; returns the timings and roofline."""
     from paper_2212_04180_amd import workloads
-
-    cfg, gens = workloads.get(args.workload)
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    stream = torch.cuda.current_stream(dev)
+    cfg, _ = workloads.get(name)
     es = P.ES(cfg, device=dev, stream=stream)
     R, N, D = cfg.num_runs, cfg.popsize, cfg.num_dims
     fit = torch.empty(R, N, device=dev)
-    if args.copy_calibration_mib:
-        n = args.copy_calibration_mib * (1 << 20) // 4
+    if copy_mib:
+        n = copy_mib * (1 << 20) // 4
         src = torch.ones(n, device=dev)
         dst = torch.empty_like(src)
         dst.copy_(src)
@@ -152,11 +168,13 @@ def main():
         log(f"[bench] copy calibration: {n * 4} bytes read + {n * 4} bytes written")
         del src, dst
 
-    for _ in range(args.warmup):
-        es.step(fit)
+    if path == "run":
+        es.run(W, log=False)
+    else:
+        for _ in range(W):
+            es.step(fit)
     torch.cuda.synchronize()
 
-    K = args.steps
     # Two HIP events per generation time the dominant kernel, the main
     # evaluate kernel: es_eval_timed has its dispatch record them
     # (hipExtLaunchKernel), so the timed stream holds no marker packets (an
@@ -173,7 +191,7 @@ def main():
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record(stream)
-    if args.path == "run":
+    if path == "run":
         es.run(K, log=False)
     else:
         for k in range(K):
@@ -183,23 +201,23 @@ def main():
     end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
-    total_ms = start.elapsed_time(end)
-    ms = total_ms / K
-    if args.path == "run":
+    ms = start.elapsed_time(end) / K
+    if path == "run":
         eval_ms = rest_ms = None  # es_run has no phase boundaries to time
     else:
         eval_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / K
         rest_ms = sum(ev[k][1].elapsed_time(ev[k + 1][0] if k + 1 < K else end) for k in range(K)) / K
+    es.close()
     value = R * N * D / (ms * 1e-3)
     phases = f" (eval kernel {eval_ms:.4f}, rest {rest_ms:.4f})" if eval_ms is not None else ""
-    log(f"[bench] {args.workload}: {ms:.4f} ms/gen{phases}, wall {wall:.3f}s "
-        f"for {K} gens, {value:.4e} member-dims/s")
+    log(f"[bench] {name} ({path}): {ms:.4f} ms/gen{phases}, wall {wall:.3f}s for {K} gens, "
+        f"{value:.4e} member-dims/s")
 
     prob = {P.PROB_SHIFTED_SPHERE: "shifted_sphere", P.PROB_SPHERE: "sphere", P.PROB_RASTRIGIN: "rastrigin",
             P.PROB_ROSENBROCK: "rosenbrock"}.get(cfg.problem)
+    pair_blocks = R * (N // 2) * ((D + 3) // 4)
     roof = None
-    if prob is not None and args.path == "percall":
-        pair_blocks = R * (N // 2) * ((D + 3) // 4)
+    if prob is not None and path == "percall":
         vec = cfg.strategy != P.STRAT_OPENAI_ES
         eval_slots = EVAL_SLOTS_PER_PAIR_BLOCK[prob] + (EVAL_VEC_EXTRA if vec else 0)
         tell_slots = TELL_SLOTS_PER_PAIR_BLOCK + (TELL_TWO_EXTRA if vec else 0)
@@ -212,29 +230,30 @@ def main():
             tell_items = R * mu * ((D + 3) // 4)
         achieved = pair_blocks * eval_slots / (eval_ms * 1e-3)
         tell_achieved = tell_items * tell_slots / (rest_ms * 1e-3)
+        issued = profiled_traffic(name, "eval_valu_issued_slots_per_pair_block", float)
         roof = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                 "unit": "T VALU lane-op slots/s", "frac": achieved / VALU_PEAK,
-                "traffic": profiled_traffic(args.workload),
-                "traffic_request_sized": profiled_traffic(args.workload, "eval_hbm_bytes_request_sized"),
+                "traffic": profiled_traffic(name),
+                "traffic_copy_scaled": profiled_traffic(name, "eval_hbm_bytes_per_launch"),
                 "kernel": "k_eval_bbob (fused sample+evaluate)",
                 "kernel_ms": eval_ms, "slots_per_pair_block": eval_slots,
                 "pair_blocks_per_launch": pair_blocks,
+                "issued_slots_per_pair_block": issued,
+                "issued_frac": None if issued is None else pair_blocks * issued / (eval_ms * 1e-3) / VALU_PEAK,
                 "tell": {"kernel": "k_eval_reduce + k_rank + k_tell (+ the strategy's update passes): the rest "
                                    "of the generation", "kernel_ms": rest_ms, "achieved": tell_achieved / 1e12,
                          "frac": tell_achieved / VALU_PEAK, "slots_per_pair_block": tell_slots}}
-    if prob is not None and args.path == "run" and cfg.strategy == P.STRAT_OPENAI_ES:
+    if prob is not None and path == "run" and cfg.strategy == P.STRAT_OPENAI_ES:
         # whole generations: evaluate and gradient slots over the timed launch(es)
-        pair_blocks = R * (N // 2) * ((D + 3) // 4)
         slots = EVAL_SLOTS_PER_PAIR_BLOCK[prob] + TELL_SLOTS_PER_PAIR_BLOCK
         achieved = pair_blocks * slots / (ms * 1e-3)
         roof = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                 "unit": "T VALU lane-op slots/s", "frac": achieved / VALU_PEAK, "traffic": None,
                 "kernel": "es_run (k_run_fused where the geometry takes the fused loop, else the per-call kernels)",
                 "kernel_ms": ms, "slots_per_pair_block": slots, "pair_blocks_per_generation": pair_blocks}
-    if cfg.problem == P.PROB_MLP and args.path == "percall":
+    if cfg.problem == P.PROB_MLP and path == "percall":
         flops = R * N * MLP_FLOPS_PER_MEMBER
         achieved = flops / (eval_ms * 1e-3)
-        pair_blocks = R * (N // 2) * ((D + 3) // 4)
         tell_achieved = pair_blocks * TELL_SLOTS_PER_PAIR_BLOCK / (rest_ms * 1e-3)
         roof = {"bound": "mfma", "achieved": achieved / 1e12, "peak": BF16_MFMA_PEAK / 1e12, "unit": "TFLOP/s",
                 "frac": achieved / BF16_MFMA_PEAK, "traffic": None,
@@ -245,23 +264,68 @@ def main():
                                    "the rest of the generation", "kernel_ms": rest_ms,
                          "achieved": tell_achieved / 1e12, "unit": "T VALU lane-op slots/s",
                          "frac": tell_achieved / VALU_PEAK}}
+    return {"cfg": cfg, "prob": prob, "ms": ms, "eval_ms": eval_ms, "rest_ms": rest_ms, "value": value,
+            "roofline": roof, "K": K}
+
+
+# The other workloads the default run also times: name -> (path, generations
+# timed, warm-up generations).  The per-call path for the MLP (its roofline
+# is the evaluate kernel's share of the bf16 MFMA peak), es_run for the three
+# small ones (their configured generation counts, one es_run call each).
+OTHER_WORKLOADS = {"mlp_teacher": ("percall", 20, 3), "sphere_d16": ("run", 100, 100),
+                   "rosenbrock_d1000": ("run", 500, 50), "rastrigin_r1024": ("run", 200, 20)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the library runs every strategy on a single MI355X and "
+              "sharding over several GPUs is not implemented", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2212_04180_amd as P
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    res = time_workload(P, torch, args.workload, args.steps, args.warmup, args.path, dev, stream,
+                        args.copy_calibration_mib)
+    cfg, prob, ms, value = res["cfg"], res["prob"], res["ms"], res["value"]
+    R, N, D = cfg.num_runs, cfg.popsize, cfg.num_dims
+
+    others = None
+    if args.workload == "shifted_sphere_d1m" and not args.no_other_workloads:
+        others = {}
+        for name, (path, K, W) in OTHER_WORKLOADS.items():
+            o = time_workload(P, torch, name, K, W, path, dev, stream)
+            oc = o["cfg"]
+            others[name] = {"path": path, "steps": K, "ms_per_step": o["ms"], "generations_per_s": 1e3 / o["ms"],
+                            "value": o["value"], "unit": "member-dims/s",
+                            "num_runs": oc.num_runs, "popsize": oc.popsize, "num_dims": oc.num_dims,
+                            "eval_kernel_ms": o["eval_ms"], "rest_ms": o["rest_ms"], "roofline": o["roofline"]}
+
     # HBM reading of the metric: the same generation with the noise stored
     # (written once by evaluate, read once by tell) moves 4 B per member-dim.
+    # An equivalence, not a share of HBM bandwidth: the path stores no noise.
     hbm_equiv = {"bytes_per_member_dim": 4.0, "peak_member_dims_per_s": HBM_PEAK / 4.0,
-                 "frac": value / (HBM_PEAK / 4.0)}
+                 "equivalent_frac": value / (HBM_PEAK / 4.0),
+                 "reading": "throughput of a noise-storing design at the full 8 TB/s; not a share of HBM "
+                            "bandwidth (this path regenerates the noise and moves about 50 MB per generation)"}
 
     cpu = None
     if not args.no_cpu_baseline:
         sd = args.cpu_sample_dims or max(4, min(D, int(4.0e8 // (R * N))))
         cpu = cpu_baseline(cfg, sd)
-        log(f"[bench] oracle sample: {cpu['sample']} -> {cpu['value']:.3e} member-dims/s")
+        log(f"[bench] oracle sample: {cpu['sample']} -> {cpu['value']:.3e} member-dims/s "
+            f"({cpu['cores']} threads; host cores {cpu['host_cores']})")
 
     out = {
         "metric": "member-dims/sec per ES generation (ask+eval+tell)",
         "value": value,
         "unit": "member-dims/s",
         "n_gpus": 1,
-        "steps": K,
+        "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms,
         "higher_is_better": True,
@@ -274,10 +338,11 @@ def main():
                    "strategy": {0: "openai_es", 1: "pgpe", 2: "snes", 3: "sep_cma_es"}[cfg.strategy],
                    "optimizer": "clipup" if cfg.optimizer == P.OPT_CLIPUP and cfg.strategy != P.STRAT_SNES else
                    ({0: "adam", 1: "adam", 2: "snes natural gradient", 3: "cma recombination"}[cfg.strategy]),
-                   "generations_per_s": 1e3 / ms, "eval_kernel_ms": eval_ms, "rest_ms": rest_ms},
-        "roofline": roof,
+                   "generations_per_s": 1e3 / ms, "eval_kernel_ms": res["eval_ms"], "rest_ms": res["rest_ms"]},
+        "roofline": res["roofline"],
         "hbm_equivalent": hbm_equiv,
         "cpu_baseline": cpu,
+        "other_workloads": others,
     }
     print(json.dumps(out), flush=True)
 

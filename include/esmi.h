@@ -159,7 +159,28 @@ typedef struct es_config {
     float clipup_momentum;  /* ClipUp velocity decay in [0, 1)               */
     float snes_temperature; /* SNES utility temperature beta (>= 0)          */
     float elite_ratio;  /* Sep-CMA-ES: share of the population recombined, (0, 1] */
+    /* Launch plan (not part of the method; 0 = the library's choice, which
+     * is what every result in the documentation refers to).  The first two
+     * set how the fp32 partial sums are grouped, so they change the
+     * summation order and therefore the low bits of the fitness and of the
+     * gradient; the third only picks the code path of es_run.
+     *   plan_eval_blocks  Philox blocks (4 dims) per evaluate chunk, >= 0;
+     *                     each chunk's per-member partial is one fp32 sum
+     *   plan_tell_split   gradient workgroups per group of 64 Philox blocks
+     *                     (their fp64 partials are added in split order), >= 0;
+     *                     the library may lower it to keep two pair groups
+     *                     per slice, and ignores it where es_run's fused
+     *                     loop would run (those keep the fused loop's order)
+     *   plan_run_path     es_run: 1 = always the per-call kernels, 2 = the
+     *                     fused loop wherever it supports the config (in
+     *                     the fused loop's summation order, which equals the
+     *                     per-call kernels' only where the library itself
+     *                     would choose the fused loop)                     */
+    int32_t plan_eval_blocks;
+    int32_t plan_tell_split;
+    int32_t plan_run_path;
     int32_t reserved;   /* must be 0                                         */
+    int32_t reserved2;  /* must be 0                                         */
 } es_config;
 
 typedef struct es_handle es_handle;
@@ -182,7 +203,8 @@ es_status es_ask(es_handle* h, float* x_out);
  * for this generation; ES_ERR_UNSUPPORTED for ES_PROB_NONE. */
 es_status es_eval(es_handle* h, float* fitness_out);
 
-/* es_eval that also times its main kernel: start_event and stop_event
+/* Timing aid, not an operation of the paper: es_eval that also times its
+ * main kernel.  start_event and stop_event
  * (hipEvent_t handles the caller created with timing enabled; either may be
  * NULL) are recorded by that kernel's dispatch itself (hipExtLaunchKernel),
  * at its start and at its end, so the stream carries no marker packet.  The
@@ -208,9 +230,10 @@ es_status es_tell(es_handle* h, const float* fitness);
  * fitness (the member of rank 0).  Requires no open ask. */
 es_status es_run(es_handle* h, int32_t T, float* log);
 
-/* Copy out / replace the search state.  m, m1, v: device [R][D] (NULL to
- * skip); t: number of completed generations.  es_set_state requires no open
- * ask. */
+/* Copy out / replace the search state (the state fields of Listing 1; the
+ * paper defines no accessor: these are host-side plumbing).  m, m1, v:
+ * device [R][D] (NULL to skip); t: number of completed generations.
+ * es_set_state requires no open ask. */
 es_status es_get_state(es_handle* h, float* m, float* m1, float* v, int64_t* t);
 es_status es_set_state(es_handle* h, const float* m, const float* m1, const float* v, int64_t t);
 
@@ -218,9 +241,11 @@ es_status es_set_state(es_handle* h, const float* m, const float* m1, const floa
  * member: device [R][D], fitness: device [R] (NaN while none). */
 es_status es_get_best(es_handle* h, float* member, float* fitness);
 
-/* Diagnostics of the last es_tell: shaped weights y [R][N], ranks [R][N]
- * (int32), and -- when ES_FLAG_KEEP_GRAD is set -- the gradient g [R][D].
- * Device pointers; NULL to skip. */
+/* Diagnostics of the last es_tell, not operations of the paper (they expose
+ * intermediate values of the tell of Sec. 2.1 for inspection and tests):
+ * shaped weights y [R][N], ranks [R][N] (int32), and -- when
+ * ES_FLAG_KEEP_GRAD is set -- the gradient g [R][D].  Device pointers; NULL
+ * to skip. */
 es_status es_get_shaped(es_handle* h, float* y, int32_t* rank);
 es_status es_get_grad(es_handle* h, float* g);
 
@@ -243,21 +268,25 @@ es_status es_get_hparams(es_handle* h, float* sigma, float* lr);
 es_status es_get_strategy_state(es_handle* h, float* sigma_vec, float* velocity);
 es_status es_set_strategy_state(es_handle* h, const float* sigma_vec, const float* velocity);
 
-/* Weight-decay penalty of the last es_tell: pen [R][N] = (1/D) sum_d x_jd^2
- * of every member (device pointer).  ES_ERR_UNSUPPORTED when w_decay = 0. */
+/* Diagnostic, not an operation of the paper: the weight-decay penalty of the
+ * last es_tell (Sec. 3.2 shaping), pen [R][N] = (1/D) sum_d x_jd^2 of every
+ * member (device pointer).  ES_ERR_UNSUPPORTED when w_decay = 0. */
 es_status es_get_penalty(es_handle* h, float* pen);
 
-/* Problem data shared by all runs: the shift vector s [D] (shifted sphere)
- * or the flattened teacher network [D] (MLP).  Device pointer. */
+/* Accessor, not an operation of the paper: the problem data shared by all
+ * runs, the shift vector s [D] (shifted sphere) or the flattened teacher
+ * network [D] (MLP).  Device pointer. */
 es_status es_get_problem_data(es_handle* h, float* out);
 
-/* Raw stream for one (run, generation t, pair): the Philox words
- * words[4*ceil(D/4)] (uint32) and the normals eps[D].  Device pointers; NULL
+/* Test aid, not an operation of the paper: the raw stream for one (run,
+ * generation t, pair), the Philox words words[4*ceil(D/4)] (uint32) and the
+ * normals eps[D] that ask (Sec. 2.1) perturbs with.  Device pointers; NULL
  * to skip.  Uses the same device code as ask, evaluate and tell. */
 es_status es_debug_noise(es_handle* h, int32_t run, int64_t t, int32_t pair,
                          uint32_t* words, float* eps);
 
-/* Checkpoint (synchronous): with host_buf NULL, *bytes receives the size;
+/* Checkpoint (synchronous; the paper defines none -- the state is that of
+ * Listing 1): with host_buf NULL, *bytes receives the size;
  * otherwise the state (config, t, m, m1, v, best, per-run sigma and lr, the
  * sigma vector and velocity where kept) is written to host_buf.
  * es_load_state restores a checkpoint of a handle with the same config.
@@ -265,6 +294,8 @@ es_status es_debug_noise(es_handle* h, int32_t run, int64_t t, int32_t pair,
  * the same trajectory bit for bit. */
 es_status es_save_state(es_handle* h, void* host_buf, size_t* bytes);
 es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes);
+
+/* Runtime plumbing below, not operations of the paper. */
 
 /* Wait for all work enqueued by this handle (synchronous). */
 es_status es_sync(es_handle* h);

@@ -32,6 +32,42 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ------------------------------------------------------------------------ */
+/* Threads.  The loops over members (evaluation, population, penalty) and    */
+/* over blocks of dimensions (gradient and noise sums) run in parallel with  */
+/* OpenMP when the file is built with it.  Each parallel loop hands out      */
+/* independent outputs (a member's fitness, a dimension's sum) and every     */
+/* output's own sum keeps the serial order, so the results are bit-identical */
+/* for any thread count.  n <= 0 restores OpenMP's default (OMP_NUM_THREADS, */
+/* else all cores).                                                         */
+/* ------------------------------------------------------------------------ */
+void or_set_threads(int32_t n)
+{
+#ifdef _OPENMP
+    static int32_t dflt = 0; /* OpenMP's own choice, seen before the first change */
+    if (dflt == 0) dflt = (int32_t)omp_get_max_threads();
+    omp_set_num_threads(n > 0 ? n : dflt);
+#else
+    (void)n;
+#endif
+}
+
+int32_t or_get_threads(void)
+{
+#ifdef _OPENMP
+    return (int32_t)omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* Dimensions per work item of the dimension-parallel loops (a multiple of  */
+/* the four dimensions of one generator block).                              */
+#define OR_DIM_CHUNK 4096
 
 /* ------------------------------------------------------------------------ */
 /* Philox-4x32-10 (Salmon, Moraes, Dror, Shaw: "Parallel random numbers: as   */
@@ -261,6 +297,7 @@ void or_member(const or_config* c, int32_t run, uint32_t t, const float* m, int3
 
 void or_population(const or_config* c, int32_t run, uint32_t t, const float* m, float* x)
 {
+#pragma omp parallel for schedule(static)
     for (int32_t j = 0; j < c->popsize; ++j) or_member(c, run, t, m, j, x + (int64_t)j * c->num_dims);
 }
 
@@ -390,18 +427,22 @@ void or_eval_members(const or_config* c, int32_t run, uint32_t t, const float* m
                      const float* pdata, const int32_t* js, int32_t nj, float* f)
 {
     int64_t D = c->num_dims;
-    float* x = (float*)malloc(sizeof(float) * (size_t)D);
     float* YT = NULL;
     if (c->problem == OR_PROB_MLP) {
         YT = (float*)malloc(sizeof(float) * (size_t)c->mlp_batch * OR_MLP_OUT);
         or_mlp_teacher_out(c, pdata, t, YT);
     }
-    for (int32_t i = 0; i < nj; ++i) {
-        or_member(c, run, t, m, js[i], x);
-        if (c->problem == OR_PROB_MLP) f[i] = or_mlp_fitness(c, x, t, YT);
-        else f[i] = or_fitness_bbob(c->problem, x, D, pdata, c->rastrigin_a);
+#pragma omp parallel
+    {
+        float* x = (float*)malloc(sizeof(float) * (size_t)D);
+#pragma omp for schedule(static)
+        for (int32_t i = 0; i < nj; ++i) {
+            or_member(c, run, t, m, js[i], x);
+            if (c->problem == OR_PROB_MLP) f[i] = or_mlp_fitness(c, x, t, YT);
+            else f[i] = or_fitness_bbob(c->problem, x, D, pdata, c->rastrigin_a);
+        }
+        free(x);
     }
-    free(x);
     free(YT);
 }
 
@@ -499,14 +540,18 @@ void or_shape_full(const float* f, const float* pen, int32_t N, int32_t maximize
 void or_penalty(const or_config* c, int32_t run, uint32_t t, const float* m, float* pen)
 {
     int64_t D = c->num_dims;
-    float* x = (float*)malloc(sizeof(float) * (size_t)D);
-    for (int32_t j = 0; j < c->popsize; ++j) {
-        or_member(c, run, t, m, j, x);
-        double acc = 0.0;
-        for (int64_t d = 0; d < D; ++d) acc += (double)x[d] * (double)x[d];
-        pen[j] = (float)(acc / (double)D);
+#pragma omp parallel
+    {
+        float* x = (float*)malloc(sizeof(float) * (size_t)D);
+#pragma omp for schedule(static)
+        for (int32_t j = 0; j < c->popsize; ++j) {
+            or_member(c, run, t, m, j, x);
+            double acc = 0.0;
+            for (int64_t d = 0; d < D; ++d) acc += (double)x[d] * (double)x[d];
+            pen[j] = (float)(acc / (double)D);
+        }
+        free(x);
     }
-    free(x);
 }
 
 /* Exponential decay with a floor (App. B schedules), fp32: max(x*decay, final). */
@@ -526,18 +571,24 @@ void or_grad(const or_config* c, int32_t run, uint32_t t, const float* y,
              int64_t d0, int64_t nd, float* g)
 {
     int32_t N = c->popsize, half = N / 2;
-    double* acc = (double*)calloc((size_t)nd, sizeof(double));
-    float* eps = (float*)malloc(sizeof(float) * (size_t)nd);
-    for (int32_t j = 0; j < N; ++j) {
-        int32_t p = j < half ? j : j - half;
-        double sgn = j < half ? 1.0 : -1.0;
-        or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)p, t, d0, nd, eps);
-        for (int64_t i = 0; i < nd; ++i) acc[i] += (double)y[j] * sgn * (double)eps[i];
-    }
     double scale = (double)N * (double)c->sigma;
-    for (int64_t i = 0; i < nd; ++i) g[i] = (float)(acc[i] / scale);
-    free(acc);
-    free(eps);
+    int64_t nch = (nd + OR_DIM_CHUNK - 1) / OR_DIM_CHUNK;
+    /* blocks of dims in parallel; each dim sums over j = 0..N-1 in order */
+#pragma omp parallel for schedule(static)
+    for (int64_t k = 0; k < nch; ++k) {
+        int64_t a = k * OR_DIM_CHUNK, n = nd - a < OR_DIM_CHUNK ? nd - a : OR_DIM_CHUNK;
+        double* acc = (double*)calloc((size_t)n, sizeof(double));
+        float* eps = (float*)malloc(sizeof(float) * (size_t)n);
+        for (int32_t j = 0; j < N; ++j) {
+            int32_t p = j < half ? j : j - half;
+            double sgn = j < half ? 1.0 : -1.0;
+            or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)p, t, d0 + a, n, eps);
+            for (int64_t i = 0; i < n; ++i) acc[i] += (double)y[j] * sgn * (double)eps[i];
+        }
+        for (int64_t i = 0; i < n; ++i) g[a + i] = (float)(acc[i] / scale);
+        free(acc);
+        free(eps);
+    }
 }
 
 /* ------------------------------------------------------------------------ */
@@ -582,17 +633,23 @@ void or_noise_sums(const or_config* c, int32_t run, uint32_t t, const float* a, 
 {
     int32_t P = c->popsize / 2;
     int64_t D = c->num_dims;
-    float* z = (float*)malloc(sizeof(float) * (size_t)D);
-    for (int64_t d = 0; d < D; ++d) { A[d] = 0.0; B[d] = 0.0; }
-    for (int32_t p = 0; p < P; ++p) {
-        or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)p, t, 0, D, z);
-        for (int64_t d = 0; d < D; ++d) {
-            double zd = (double)z[d];
-            A[d] += (double)a[p] * zd;
-            B[d] += (double)b[p] * (zd * zd - 1.0);
+    int64_t nch = (D + OR_DIM_CHUNK - 1) / OR_DIM_CHUNK;
+    /* blocks of dims in parallel; each dim sums over the pairs in order */
+#pragma omp parallel for schedule(static)
+    for (int64_t k = 0; k < nch; ++k) {
+        int64_t d0 = k * OR_DIM_CHUNK, n = D - d0 < OR_DIM_CHUNK ? D - d0 : OR_DIM_CHUNK;
+        float* z = (float*)malloc(sizeof(float) * (size_t)n);
+        for (int64_t d = d0; d < d0 + n; ++d) { A[d] = 0.0; B[d] = 0.0; }
+        for (int32_t p = 0; p < P; ++p) {
+            or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)p, t, d0, n, z);
+            for (int64_t i = 0; i < n; ++i) {
+                double zd = (double)z[i];
+                A[d0 + i] += (double)a[p] * zd;
+                B[d0 + i] += (double)b[p] * (zd * zd - 1.0);
+            }
         }
+        free(z);
     }
-    free(z);
 }
 
 /* ClipUp (Toklu et al. 2020), the ES-adapted optimiser named in Sec. 3.1,
@@ -825,13 +882,20 @@ void or_sepcma_update(const or_config* c, int32_t run, int64_t t, const float* f
         if (rank[j] < k.mu) elite[rank[j]] = j;
     double* zw = (double*)calloc((size_t)D, sizeof(double));
     double* q = (double*)calloc((size_t)D, sizeof(double));
-    float* z = (float*)malloc(sizeof(float) * (size_t)D);
-    for (int32_t i = 0; i < k.mu; ++i) {
-        or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)elite[i], (uint32_t)t, 0, D, z);
-        for (int64_t d = 0; d < D; ++d) {
-            zw[d] += w[i] * (double)z[d];
-            q[d] += w[i] * (double)z[d] * (double)z[d];
+    int64_t nch = (D + OR_DIM_CHUNK - 1) / OR_DIM_CHUNK;
+    /* blocks of dims in parallel; each dim sums over the elites in order */
+#pragma omp parallel for schedule(static)
+    for (int64_t kc = 0; kc < nch; ++kc) {
+        int64_t d0 = kc * OR_DIM_CHUNK, n = D - d0 < OR_DIM_CHUNK ? D - d0 : OR_DIM_CHUNK;
+        float* z = (float*)malloc(sizeof(float) * (size_t)n);
+        for (int32_t i = 0; i < k.mu; ++i) {
+            or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)elite[i], (uint32_t)t, d0, n, z);
+            for (int64_t e = 0; e < n; ++e) {
+                zw[d0 + e] += w[i] * (double)z[e];
+                q[d0 + e] += w[i] * (double)z[e] * (double)z[e];
+            }
         }
+        free(z);
     }
     double a_s = sqrt(k.c_s * (2.0 - k.c_s) * k.mu_eff), n2 = 0.0;
     for (int64_t d = 0; d < D; ++d) {
@@ -853,7 +917,7 @@ void or_sepcma_update(const or_config* c, int32_t run, int64_t t, const float* f
     *sigma = (float)((double)*sigma * exp((k.c_s / k.d_s) * (nps / k.chi - 1.0)));
     if (w_out)
         for (int32_t j = 0; j < N; ++j) w_out[j] = rank[j] < k.mu ? (float)w[rank[j]] : 0.0f;
-    free(w); free(rank); free(elite); free(zw); free(q); free(z);
+    free(w); free(rank); free(elite); free(zw); free(q);
 }
 
 void or_generation_ex(const or_config* c0, int32_t run, int64_t t, const float* pdata,

@@ -36,7 +36,7 @@ def build(force: bool = False) -> str:
         tmp = _LIB + ".tmp%d" % os.getpid()
         subprocess.check_call(
             ["gcc", "-O2", "-fPIC", "-shared", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
-             "-Wall", "-o", tmp, _SRC, "-lm"])
+             "-fopenmp", "-Wall", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -145,6 +145,8 @@ def lib():
         f32, u32, i32, i64, u64 = ctypes.c_float, ctypes.c_uint32, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
         pc = P(_Cfg)
         sig = {
+            "or_set_threads": (None, [i32]),
+            "or_get_threads": (i32, []),
             "or_philox4x32_10": (None, [u32, u32, P(u32), P(u32)]),
             "or_words": (None, [u64, u32, u32, u32, i64, i64, P(u32)]),
             "or_normals": (None, [u64, u32, u32, u32, i64, i64, P(f32)]),
@@ -182,6 +184,16 @@ def lib():
             fn.restype = res
             fn.argtypes = args
     return _lib
+
+
+def set_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops (n <= 0: OpenMP's default, all
+    cores).  Results do not depend on it."""
+    lib().or_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(lib().or_get_threads())
 
 
 def _p(a, ctype=ctypes.c_float):

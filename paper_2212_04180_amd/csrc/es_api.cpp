@@ -25,6 +25,8 @@ namespace {
 enum Phase { READY = 0, ASKED = 1 };
 
 constexpr uint32_t kCheckpointMagic = 0x45534d32u;  // "ESM2"
+// no padding bytes: a checkpoint's config is compared byte for byte
+static_assert(sizeof(es_config) == 160, "es_config has padding");
 
 thread_local char g_init_err[256] = {0};
 
@@ -154,7 +156,10 @@ const char* validate(const es_config& c)
     if (c.strategy < ES_STRAT_OPENAI_ES || c.strategy > ES_STRAT_SEP_CMA) return "unknown strategy";
     if (c.strategy == ES_STRAT_SEP_CMA && !(c.elite_ratio > 0.0f && c.elite_ratio <= 1.0f))
         return "elite_ratio must be in (0, 1]";
-    if (c.reserved != 0) return "reserved must be 0";
+    if (c.reserved != 0 || c.reserved2 != 0) return "reserved fields must be 0";
+    if (c.plan_eval_blocks < 0) return "plan_eval_blocks must be >= 0";
+    if (c.plan_tell_split < 0 || c.plan_tell_split > 65535) return "plan_tell_split must be in [0, 65535]";
+    if (c.plan_run_path < 0 || c.plan_run_path > 2) return "plan_run_path must be 0, 1 or 2";
     if (c.strategy == ES_STRAT_SEP_CMA && c.problem == ES_PROB_MLP)
         return "Sep-CMA-ES takes the benchmark problems or the caller's fitness (the MLP evaluate kernel samples "
                "antithetic pairs)";
@@ -255,13 +260,6 @@ AdamConsts adam_consts(const es_config& c, int64_t t)
 bool fused_by_default(const Geometry& g, const EvalPlan& e, const es_config& c)
 {
     return fused_supported(g, e, c) && ((int64_t)g.P * g.nb <= 8192 || g.R >= 128);
-}
-
-int64_t env_i64(const char* name, int64_t dflt)
-{
-    const char* s = std::getenv(name);
-    if (!s || !*s) return dflt;
-    return std::strtoll(s, nullptr, 10);
 }
 
 void free_all(es_handle* h)
@@ -408,11 +406,11 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     g.N = cfg->popsize;
     g.P = cfg->popsize / 2;
     g.R = cfg->num_runs;
-    h->plan = eval_plan(g, env_i64("ESMI_EVAL_BLOCKS_PER_CHUNK", 0));
+    h->plan = eval_plan(g, cfg->plan_eval_blocks);
     // where es_run takes the fused loop (the rule of es_run), the per-call
     // gradient kernel sums in the fused loop's order, so both give the same bits
-    h->tell = tell_plan(g, fused_by_default(g, h->plan, *cfg), env_i64("ESMI_TELL_SPLIT", 0));
-    h->run_path = (int)env_i64("ESMI_RUN_PATH", 0);
+    h->tell = tell_plan(g, fused_by_default(g, h->plan, *cfg), cfg->plan_tell_split);
+    h->run_path = cfg->plan_run_path;
     hipError_t e = hipGetDevice(&h->device);
     const size_t rows = (size_t)g.Dp * g.R;
     if (e == hipSuccess) e = dalloc(&h->m, rows);
@@ -555,7 +553,7 @@ es_status es_run(es_handle* h, int32_t T, float* log)
     if (T == 0) return ES_OK;
     if (h->t + T > 0xFFFFFFFFll) return fail(h, ES_ERR_ARG, "es_run: generation counter would exceed 2^32");
     const bool fused_ok = fused_supported(h->g, h->plan, h->cfg);
-    // ESMI_RUN_PATH forces a path (1 per-call kernels, 2 fused loop); a forced
+    // plan_run_path forces a path (1 per-call kernels, 2 fused loop); a forced
     // fused loop on a geometry es_run would not fuse sums in its own order
     const bool fused = h->run_path == 2 ? fused_ok : h->run_path == 1 ? false : fused_by_default(h->g, h->plan, h->cfg);
     if (fused) {

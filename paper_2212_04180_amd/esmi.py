@@ -14,8 +14,7 @@ from dataclasses import dataclass, fields
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-# ESMI_LIB may point at another build of the same library (A/B timing)
-LIB_PATH = os.environ.get("ESMI_LIB") or os.path.join(_PKG, "libesmi.so")
+LIB_PATH = os.path.join(_PKG, "libesmi.so")
 
 ES_OK, ES_ERR_ARG, ES_ERR_SEQUENCE, ES_ERR_HIP, ES_ERR_OOM, ES_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 SHAPE_CENTERED_RANK, SHAPE_RAW, SHAPE_Z_SCORE = 0, 1, 2
@@ -75,7 +74,11 @@ class _Config(ctypes.Structure):
         ("clipup_momentum", ctypes.c_float),
         ("snes_temperature", ctypes.c_float),
         ("elite_ratio", ctypes.c_float),
+        ("plan_eval_blocks", ctypes.c_int32),
+        ("plan_tell_split", ctypes.c_int32),
+        ("plan_run_path", ctypes.c_int32),
         ("reserved", ctypes.c_int32),
+        ("reserved2", ctypes.c_int32),
     ]
 
 
@@ -117,7 +120,13 @@ class ESConfig:
     clipup_momentum: float = 0.9
     snes_temperature: float = 12.0
     elite_ratio: float = 0.5  # Sep-CMA-ES (App. B table)
+    # launch plan, 0 = the library's choice (esmi.h): evaluate chunk length and
+    # gradient split change the summation order; run path 1 per-call, 2 fused
+    plan_eval_blocks: int = 0
+    plan_tell_split: int = 0
+    plan_run_path: int = 0
     reserved: int = 0
+    reserved2: int = 0
 
     def cstruct(self) -> _Config:
         c = _Config()

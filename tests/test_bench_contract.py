@@ -27,5 +27,18 @@ def test_cpu_baseline_runs_the_oracle_on_a_sample(name):
     if cfg.num_runs > 8:
         cfg.num_runs = 8  # keep the CPU test short
     out = bench.cpu_baseline(cfg, 8)
-    assert out["kind"] == "oracle" and out["cores"] == 1 and out["unit"] == "member-dims/s"
-    assert out["value"] > 0 and "8 dims" in out["sample"]
+    assert out["kind"] == "oracle" and out["unit"] == "member-dims/s"
+    assert out["cores"] >= 1 and out["host_cores"] == len(os.sched_getaffinity(0))
+    assert out["value"] > 0 and out["single_thread"]["value"] > 0 and "8 dims" in out["sample"]
+    from oracle import oracle as O
+    assert O.get_threads() == out["cores"]  # the default restored after the one-thread leg
+
+
+def test_other_workloads_are_the_remaining_four():
+    sys.path.insert(0, ROOT)
+    import bench
+    from paper_2212_04180_amd import workloads
+    assert set(bench.OTHER_WORKLOADS) == {"mlp_teacher", "sphere_d16", "rosenbrock_d1000", "rastrigin_r1024"}
+    for name, (path, K, W) in bench.OTHER_WORKLOADS.items():
+        workloads.get(name)
+        assert path in ("percall", "run") and K > 0 and W >= 0

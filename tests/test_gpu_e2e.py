@@ -1,6 +1,8 @@
 """End-to-end behaviour of the GPU path (marked gpu): trajectories against the
 oracle, batching over runs, determinism, the fused loop, best-so-far,
 checkpoint/resume and the error paths of the C-ABI."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -86,7 +88,7 @@ def test_deterministic_and_fused_equals_per_call():
 
 @pytest.mark.parametrize("D,N,R,prob", [(5, 6, 3, "sphere"), (16, 34, 2, "rastrigin"), (37, 64, 5, "sphere"),
                                         (3, 2, 1, "rastrigin")])
-def test_fused_loop_equals_per_call_with_ties(D, N, R, prob, monkeypatch):
+def test_fused_loop_equals_per_call_with_ties(D, N, R, prob):
     """With the mean at 0 on a symmetric problem every antithetic pair ties in
     the first generation, so ranks are decided by index: the fused loop's
     sliced rank count and its per-dimension Adam give the per-call bits."""
@@ -95,8 +97,7 @@ def test_fused_loop_equals_per_call_with_ties(D, N, R, prob, monkeypatch):
                      problem=P.PROB_SPHERE if prob == "sphere" else P.PROB_RASTRIGIN)
     out = {}
     for path in ("1", "2"):
-        monkeypatch.setenv("ESMI_RUN_PATH", path)
-        es = P.ES(cfg)
+        es = P.ES(dataclasses.replace(cfg, plan_run_path=int(path)))
         log = _np(es.run(10))
         st = es.get_state()
         bx, bf = es.best()
@@ -216,7 +217,7 @@ def test_raw_shaping_linear_gradient_converges_to_a():
 @pytest.mark.parametrize("prob,D,N,R,T", [("sphere", 16, 32, 1, 40), ("rastrigin", 100, 64, 8, 25),
                                           ("rosenbrock", 37, 10, 3, 30), ("shifted", 1001, 8, 2, 6),
                                           ("sphere", 16, 32, 2, 600)])
-def test_fused_loop_matches_per_call_bits(prob, D, N, R, T, monkeypatch):
+def test_fused_loop_matches_per_call_bits(prob, D, N, R, T):
     """The one-launch loop (one workgroup per run) repeats the per-call
     kernels' arithmetic in the same order: identical bits.  T = 600 takes
     three launches (at most 256 generations each, their Adam bias
@@ -228,8 +229,7 @@ def test_fused_loop_matches_per_call_bits(prob, D, N, R, T, monkeypatch):
                      problem=pmap[prob], init=P.INIT_ZERO if prob == "shifted" else P.INIT_UNIFORM)
     out = {}
     for path in ("1", "2"):
-        monkeypatch.setenv("ESMI_RUN_PATH", path)
-        es = P.ES(cfg)
+        es = P.ES(dataclasses.replace(cfg, plan_run_path=int(path)))
         es.run(3)
         log = _np(es.run(T))
         st = es.get_state()

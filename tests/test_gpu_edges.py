@@ -5,6 +5,7 @@ D of 1, 3, 5 and 9 leave a partial Philox block (and for D < 4 a single one);
 N of 2 leaves one antithetic pair, N of 6 an odd pair count.  Bars as in the
 per-strategy tests: fitness 1e-5 relative, mean, per-dimension sigma,
 velocity, paths and covariance 1e-5 relative, run sigma 1e-5."""
+import dataclasses
 import pytest
 
 import stagecheck
@@ -46,7 +47,7 @@ def test_tiny_and_ragged_geometries_match_oracle(name, geom):
     stagecheck.run(P, _cfg(strategy, optimizer, *geom), 6)
 
 
-def test_largest_run_count_fused_and_per_call(monkeypatch):
+def test_largest_run_count_fused_and_per_call():
     """num_runs = 65535, the largest accepted (runs are the y dimension of the
     per-call grids): es_run through the fused loop (one workgroup per run) and
     through the per-call kernels gives the same bits, and sampled runs score
@@ -63,8 +64,7 @@ def test_largest_run_count_fused_and_per_call(monkeypatch):
                      problem=P.PROB_ROSENBROCK)
     out = {}
     for path in ("1", "2"):
-        monkeypatch.setenv("ESMI_RUN_PATH", path)
-        es = P.ES(cfg)
+        es = P.ES(dataclasses.replace(cfg, plan_run_path=int(path)))
         log = es.run(3)
         st = es.get_state()
         torch.cuda.synchronize()

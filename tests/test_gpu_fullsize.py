@@ -1,11 +1,12 @@
 """Parity at the full D = 1e6, N = 2048 shifted-sphere geometry, in the
 launch configuration the benchmark times (marked gpu).
 
-The oracle cannot run a whole generation at this size in seconds, so these
-tests check what it can compute one by one: the fitness of sampled members,
-ranks and shaped weights (exact, from the GPU's fitness vector), the gradient
-and the Adam step on windows of dimensions (a first block, one in the
-middle, the ragged tail), and for the other strategies the properties that
+The OpenAI-ES workload is compared in full for its first generations: every
+member's fitness and every dimension of g, m, m1 and v, stage by stage
+against the oracle running on all host cores (its parallel loops give the
+same bits as one thread).  All twenty generations are then followed on
+sampled members and on fixed and random windows of dimensions.  The other
+strategies are checked on sampled members, windows and the properties that
 hold at any size."""
 import dataclasses
 
@@ -49,7 +50,66 @@ def _check_fitness(es, oc, t, pdata, f, sig=None):
     assert np.all(np.abs(got - ref) <= 1e-5 * np.abs(ref)), (t, got, ref)
 
 
+@pytest.mark.timeout(900)
+def test_openai_es_adam_full_size_all_members_all_dims():
+    """Three generations of the benchmark workload, stage by stage: all 2048
+    fitness values (T2, 1e-5 relative), ranks and weights bit-exact, all 1e6
+    dims of g within the propagated bound (the normals' error bound at
+    |eps| <= 5.77 summed over the pairs' weights, plus fp32 rounding), the
+    Adam step bit-exact given the kernel's g and within the tell tier given
+    the oracle's g."""
+    import time
+    P = _P()
+    cfg = _workload("shifted_sphere_d1m", flags=P.FLAG_KEEP_GRAD)
+    D, N = cfg.num_dims, cfg.popsize
+    es = P.ES(cfg)
+    oc = to_oracle(cfg)
+    pdata = O.problem_data(oc)
+    print(f"oracle threads {O.get_threads()}", flush=True)
+    js = np.arange(N, dtype=np.int32)
+    zmax = 5.77
+    for t in range(3):
+        st = es.get_state()
+        m0, m10, v0 = _np(st["m"])[0], _np(st["m1"])[0], _np(st["v"])[0]
+        es.ask()
+        f = _np(es.eval())
+        t0 = time.perf_counter()
+        fr = O.eval_members(oc, 0, t, m0, pdata, js)
+        rel = np.abs(f[0].astype(np.float64) - fr) / np.abs(fr)
+        print(f"t {t}: oracle fitness {time.perf_counter() - t0:.1f} s, max relative error {rel.max():.2e}",
+              flush=True)
+        assert np.all(rel <= 1e-5), (t, float(rel.max()))
+        es.tell(torch.tensor(f, device="cuda"))
+        y, rk = es.shaped()
+        y, rk = _np(y)[0], _np(rk)[0]
+        np.testing.assert_array_equal(rk, O.ranks(f[0]))
+        np.testing.assert_array_equal(y, O.shape(f[0]))
+        g = _np(es.grad())[0].astype(np.float64)
+        st = es.get_state()
+        mg, m1g, vg = _np(st["m"])[0], _np(st["m1"])[0], _np(st["v"])[0]
+        t0 = time.perf_counter()
+        gref = O.grad(oc, 0, t, y).astype(np.float64)
+        w = np.abs(y[: N // 2].astype(np.float64) - y[N // 2:])
+        bound = w.sum() * (EPS_REL * zmax + EPS_ABS + 1e-6 * zmax) / (N * np.float64(np.float32(cfg.sigma)))
+        gerr = np.abs(g - gref)
+        print(f"t {t}: oracle gradient {time.perf_counter() - t0:.1f} s, max |dg| {gerr.max():.2e} "
+              f"(bound {bound:.2e}, |g| up to {np.abs(gref).max():.2e})", flush=True)
+        assert np.all(gerr <= bound + 2 * np.spacing(np.abs(gref).astype(np.float32))), t
+        ma, m1a, va = O.adam(oc, t, g.astype(np.float32), m0, m10, v0)
+        np.testing.assert_array_equal(mg, ma)
+        np.testing.assert_array_equal(m1g, m1a)
+        np.testing.assert_array_equal(vg, va)
+        mr, _, _ = O.adam(oc, t, gref.astype(np.float32), m0, m10, v0)
+        merr = np.max(np.abs(mg - mr) / np.maximum(np.abs(mr), cfg.lr))
+        print(f"t {t}: max mean error {merr:.2e} of max(|m|, lr)", flush=True)
+        assert merr <= 1e-5, t
+
+
 def test_openai_es_adam_full_size_sampled():
+    """All twenty generations of the benchmark workload, the GPU running
+    free: each generation's sampled members against the oracle from the
+    GPU's mean, and the gradient and Adam step on the fixed windows and three
+    random ones."""
     P = _P()
     cfg = _workload("shifted_sphere_d1m", flags=P.FLAG_KEEP_GRAD)
     D, N = cfg.num_dims, cfg.popsize
@@ -60,7 +120,8 @@ def test_openai_es_adam_full_size_sampled():
     err = np.abs(s_gpu.astype(np.float64) - pdata)
     assert np.all(err <= EPS_REL * np.abs(pdata) + EPS_ABS)
     assert not np.any(_np(es.get_state()["m"]))
-    for t in range(2):
+    rng = np.random.default_rng(20)
+    for t in range(20):
         st = es.get_state()
         m0, m10, v0 = _np(st["m"])[0], _np(st["m1"])[0], _np(st["v"])[0]
         es.ask()
@@ -77,7 +138,8 @@ def test_openai_es_adam_full_size_sampled():
         mg, m1g, vg = _np(st["m"])[0], _np(st["m1"])[0], _np(st["v"])[0]
         w = y[: N // 2].astype(np.float64) - y[N // 2:]
         ns = N * np.float64(np.float32(cfg.sigma))
-        for d0, nd in _windows(D):
+        extra = [(int(d), 32) for d in rng.integers(0, D - 32, size=3)]
+        for d0, nd in _windows(D) + extra:
             sl = slice(d0, d0 + nd)
             gref = O.grad(oc, 0, t, y, d0, nd)
             E = np.stack([O.noise(oc, 0, t, p, d0, nd) for p in range(N // 2)]).astype(np.float64)
@@ -186,7 +248,7 @@ def test_sepcma_full_size_sampled_and_elites():
 
 
 @pytest.mark.parametrize("name", ["sphere_d16", "rosenbrock_d1000", "rastrigin_r1024"])
-def test_run_workloads_full_size(name, monkeypatch):
+def test_run_workloads_full_size(name):
     """The es_run workloads at their full shapes: the first generation of
     every run against the oracle, then es_run as the benchmark calls it (the
     fused loop where the geometry takes it) bit-identical to per-call steps."""
@@ -208,8 +270,7 @@ def test_run_workloads_full_size(name, monkeypatch):
     assert np.max(np.abs(m - ref.m) / np.maximum(np.abs(ref.m), cfg.lr)) <= 1e-5
     out = {}
     for path in ("0", "1"):
-        monkeypatch.setenv("ESMI_RUN_PATH", path)
-        h = P.ES(cfg)
+        h = P.ES(dataclasses.replace(cfg, plan_run_path=int(path)))
         log = _np(h.run(12))
         st = h.get_state()
         bx, bf = h.best()

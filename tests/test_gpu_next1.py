@@ -7,6 +7,8 @@ keys, within 1 ulp for z-scores (the fp64 mean and deviation are reduced in a
 different order); the weight-decay mean square at the fitness tier T2; the
 mean within the tell tier T3 (1e-5 relative); fused loop and batching
 bit-identical."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -65,15 +67,14 @@ def test_schedules_and_per_run_hparams_track_oracle():
     assert np.all(sg2 >= np.float32(0.03)) and sg2[2] == np.float32(0.03)
 
 
-def test_fused_loop_with_schedules_matches_per_call_bits(monkeypatch):
+def test_fused_loop_with_schedules_matches_per_call_bits():
     P = _P()
     cfg = P.ESConfig(num_dims=100, popsize=64, num_runs=8, sigma=0.2, lr=0.02, seed=3, init_lo=-5.12,
                      init_hi=5.12, problem=P.PROB_RASTRIGIN, **SCHED)
     sig0 = np.linspace(0.1, 0.3, 8).astype(np.float32)
     out = {}
     for path in ("1", "2"):
-        monkeypatch.setenv("ESMI_RUN_PATH", path)
-        es = P.ES(cfg)
+        es = P.ES(dataclasses.replace(cfg, plan_run_path=int(path)))
         es.set_hparams(sig0, None)
         log = _np(es.run(25))
         st = es.get_state()

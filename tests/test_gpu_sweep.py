@@ -6,6 +6,8 @@ The sizes are drawn log-uniformly (D from 1 to 20000, N even from 2 to 512,
 R from 1 to 4) and capped so that the oracle finishes each case in about a
 second; they land on every remainder of D modulo the Philox block and on
 pair counts that are and are not whole pair groups."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -74,7 +76,7 @@ def _draw_fused(i):
 
 
 @pytest.mark.parametrize("i", range(16))
-def test_random_fused_loop_equals_per_call(i, monkeypatch):
+def test_random_fused_loop_equals_per_call(i):
     """es_run through the fused loop (forced) and through the per-call kernels
     give the same bits: log, mean, moments, best-so-far, sigma and lr."""
     import torch
@@ -83,8 +85,7 @@ def test_random_fused_loop_equals_per_call(i, monkeypatch):
     print("case", i, cfg, flush=True)
     out = {}
     for path in ("1", "2"):
-        monkeypatch.setenv("ESMI_RUN_PATH", path)
-        es = P.ES(cfg)
+        es = P.ES(dataclasses.replace(cfg, plan_run_path=int(path)))
         log = es.run(7)
         st = es.get_state()
         bx, bf = es.best()

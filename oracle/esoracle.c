@@ -652,6 +652,27 @@ void or_noise_sums(const or_config* c, int32_t run, uint32_t t, const float* a, 
     }
 }
 
+/* Error-bound helper for the tests (no step of the method): the fp64 sum   */
+/* S_d = sum_p |a_p| |z_pd| over the pairs, the factor by which the normals' */
+/* error bound moves a weighted noise sum such as the gradient's.            */
+void or_abs_noise_sum(const or_config* c, int32_t run, uint32_t t, const float* a, double* S)
+{
+    int32_t P = c->popsize / 2;
+    int64_t D = c->num_dims;
+    int64_t nch = (D + OR_DIM_CHUNK - 1) / OR_DIM_CHUNK;
+#pragma omp parallel for schedule(static)
+    for (int64_t k = 0; k < nch; ++k) {
+        int64_t d0 = k * OR_DIM_CHUNK, n = D - d0 < OR_DIM_CHUNK ? D - d0 : OR_DIM_CHUNK;
+        float* z = (float*)malloc(sizeof(float) * (size_t)n);
+        for (int64_t d = d0; d < d0 + n; ++d) S[d] = 0.0;
+        for (int32_t p = 0; p < P; ++p) {
+            or_normals(c->seed + (uint64_t)run, OR_DOM_NOISE, (uint32_t)p, t, d0, n, z);
+            for (int64_t i = 0; i < n; ++i) S[d0 + i] += fabs((double)a[p]) * fabs((double)z[i]);
+        }
+        free(z);
+    }
+}
+
 /* ClipUp (Toklu et al. 2020), the ES-adapted optimiser named in Sec. 3.1,
  * for minimisation.  Reading: with the fp64 norms |g| and |v'|,
  *   gh_d = fl32(g_d * fl32(1/|g|))          (0 when |g| = 0)

@@ -167,6 +167,7 @@ def lib():
             "or_decay": (f32, [f32, f32, f32]),
             "or_noise_sums": (None, [pc, i32, u32, P(f32), P(f32), P(ctypes.c_double), P(ctypes.c_double)]),
             "or_clipup": (None, [pc, f32, P(f32), i64, P(f32), P(f32)]),
+            "or_abs_noise_sum": (None, [pc, i32, u32, P(f32), P(ctypes.c_double)]),
             "or_snes_table": (None, [i32, f32, P(f32)]),
             "or_generation_ex": (None, [pc, i32, i64, P(f32), P(f32), P(f32), P(f32), P(f32), P(f32), P(f32),
                                         P(f32), P(f32), P(f32), P(f32), P(ctypes.c_double), P(f32), P(f32)]),
@@ -346,6 +347,14 @@ def noise_sums(cfg, run, t, a, b):
     B = np.zeros(cfg.num_dims, np.float64)
     lib().or_noise_sums(cfg.cstruct(), run, t, _p(a), _p(b), _p(A, ctypes.c_double), _p(B, ctypes.c_double))
     return A, B
+
+
+def abs_noise_sum(cfg, run, t, a):
+    """S_d = sum_p |a_p| |z_pd| (fp64): for error bounds of weighted noise sums."""
+    a = _f32(a)
+    S = np.zeros(cfg.num_dims, np.float64)
+    lib().or_abs_noise_sum(cfg.cstruct(), run, t, _p(a), _p(S, ctypes.c_double))
+    return S
 
 
 def clipup(cfg, lr, g, m, vel):

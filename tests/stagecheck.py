@@ -73,6 +73,41 @@ def _fitness_bound(cfg, x, scale, pdata):
     return 1e-5 * S + np.sum(g * dx, -1) + 0.5 * np.sum(h * dx * dx, -1) + 1e-30
 
 
+def grad_bound(oc, r, t, y):
+    """Per-dimension bound on |g_gpu - g_oracle| for OpenAI-ES: the normals'
+    error (T1) summed over the pairs' folded weights, plus fp32 rounding of
+    the kernel's sums (1e-6 of the same sum)."""
+    N = oc.popsize
+    w = y[: N // 2].astype(np.float64) - y[N // 2:]
+    S = O.abs_noise_sum(oc, r, t, w.astype(np.float32))
+    return ((EPS_REL + 1e-6) * S + EPS_ABS * np.sum(np.abs(w))) / (N * np.float64(np.float32(oc.sigma)))
+
+
+def adam_tolerance(oc, t, g, m1, v, delta):
+    """Per-dimension bound on the Adam step's difference when g is known to
+    within delta: lr |dq| <= lr delta sup |q'(g')| over |g' - g| <= delta, with
+    q = mhat / (sqrt(vhat) + eps), mhat = a + b g', vhat = c + d g'^2 and
+    |q'| <= |b| / S + (|a| + |b| g') d g' / S^3, S = sqrt(vhat) (an upper bound:
+    eps only enlarges the denominator).  Where g may be 0 at t = 0 (c = 0)
+    the bound is infinite: the step there follows the sign of g, a near-tie.
+    Adam's step is scale-free in g, so this term, not the fp32 rounding, sets
+    the tolerance wherever |g| is small."""
+    b1, b2 = np.float64(np.float32(oc.beta1)), np.float64(np.float32(oc.beta2))
+    tp = t + 1
+    bc1, bc2 = np.float64(np.float32(1 - b1 ** tp)), np.float64(np.float32(1 - b2 ** tp))
+    a = b1 * m1.astype(np.float64) / bc1
+    b = (1 - b1) / bc1
+    c = b2 * v.astype(np.float64) / bc2
+    d = (1 - b2) / bc2
+    g = np.abs(g.astype(np.float64))
+    gmin = np.maximum(g - delta, 0.0)
+    gmax = g + delta
+    S = np.sqrt(c + d * gmin * gmin)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        dq = np.where(S > 0, abs(b) / S + (np.abs(a) + abs(b) * gmax) * d * gmax / S ** 3, np.inf)
+    return np.float64(np.float32(oc.lr)) * delta * dq
+
+
 def _noise_rows(oc, r, t, rows, D):
     return np.stack([O.normals(oc.seed + r, O.DOM_NOISE, int(p), t, 0, D) for p in rows]).astype(np.float64)
 

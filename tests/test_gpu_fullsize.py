@@ -14,6 +14,7 @@ import numpy as np
 import pytest
 import torch
 
+import stagecheck
 from inputs import to_oracle
 from oracle import oracle as O
 
@@ -54,20 +55,20 @@ def _check_fitness(es, oc, t, pdata, f, sig=None):
 def test_openai_es_adam_full_size_all_members_all_dims():
     """Three generations of the benchmark workload, stage by stage: all 2048
     fitness values (T2, 1e-5 relative), ranks and weights bit-exact, all 1e6
-    dims of g within the propagated bound (the normals' error bound at
-    |eps| <= 5.77 summed over the pairs' weights, plus fp32 rounding), the
-    Adam step bit-exact given the kernel's g and within the tell tier given
-    the oracle's g."""
+    dims of g within their propagated bound (the normals' error bound times
+    sum_p |w_p| |eps_pd|, plus fp32 rounding), the Adam step bit-exact given
+    the kernel's g, and given the oracle's g within 1e-5 of max(|m|, lr)
+    plus g's bound carried through Adam's step (which is scale-free in g, so
+    where |g| is small its step follows g's direction alone)."""
     import time
     P = _P()
     cfg = _workload("shifted_sphere_d1m", flags=P.FLAG_KEEP_GRAD)
-    D, N = cfg.num_dims, cfg.popsize
+    N = cfg.popsize
     es = P.ES(cfg)
     oc = to_oracle(cfg)
     pdata = O.problem_data(oc)
     print(f"oracle threads {O.get_threads()}", flush=True)
     js = np.arange(N, dtype=np.int32)
-    zmax = 5.77
     for t in range(3):
         st = es.get_state()
         m0, m10, v0 = _np(st["m"])[0], _np(st["m1"])[0], _np(st["v"])[0]
@@ -89,20 +90,24 @@ def test_openai_es_adam_full_size_all_members_all_dims():
         mg, m1g, vg = _np(st["m"])[0], _np(st["m1"])[0], _np(st["v"])[0]
         t0 = time.perf_counter()
         gref = O.grad(oc, 0, t, y).astype(np.float64)
-        w = np.abs(y[: N // 2].astype(np.float64) - y[N // 2:])
-        bound = w.sum() * (EPS_REL * zmax + EPS_ABS + 1e-6 * zmax) / (N * np.float64(np.float32(cfg.sigma)))
+        delta = stagecheck.grad_bound(oc, 0, t, y)
         gerr = np.abs(g - gref)
-        print(f"t {t}: oracle gradient {time.perf_counter() - t0:.1f} s, max |dg| {gerr.max():.2e} "
-              f"(bound {bound:.2e}, |g| up to {np.abs(gref).max():.2e})", flush=True)
-        assert np.all(gerr <= bound + 2 * np.spacing(np.abs(gref).astype(np.float32))), t
+        print(f"t {t}: oracle gradient and its bound {time.perf_counter() - t0:.1f} s, max |dg| {gerr.max():.2e}, "
+              f"largest |dg| / bound {np.max(gerr / delta):.3f}, |g| up to {np.abs(gref).max():.2e}", flush=True)
+        assert np.all(gerr <= delta + 2 * np.spacing(np.abs(gref).astype(np.float32))), t
         ma, m1a, va = O.adam(oc, t, g.astype(np.float32), m0, m10, v0)
         np.testing.assert_array_equal(mg, ma)
         np.testing.assert_array_equal(m1g, m1a)
         np.testing.assert_array_equal(vg, va)
         mr, _, _ = O.adam(oc, t, gref.astype(np.float32), m0, m10, v0)
-        merr = np.max(np.abs(mg - mr) / np.maximum(np.abs(mr), cfg.lr))
-        print(f"t {t}: max mean error {merr:.2e} of max(|m|, lr)", flush=True)
-        assert merr <= 1e-5, t
+        den = np.maximum(np.abs(mr), cfg.lr)
+        prop = stagecheck.adam_tolerance(oc, t, gref, m10, v0, delta)
+        err = np.abs(mg.astype(np.float64) - mr)
+        tier = err <= 1e-5 * den
+        print(f"t {t}: mean within 1e-5 of max(|m|, lr) in {int(tier.sum())} dims; the other "
+              f"{int((~tier).sum())} within g's bound carried through Adam (largest error there "
+              f"{np.max(err[~tier] / den[~tier], initial=0):.2e} of max(|m|, lr))", flush=True)
+        assert np.all(err <= 1e-5 * den + prop), t
 
 
 def test_openai_es_adam_full_size_sampled():
@@ -146,7 +151,8 @@ def test_openai_es_adam_full_size_sampled():
             bound = (np.abs(w) @ (EPS_REL * np.abs(E) + EPS_ABS) + 1e-6 * (np.abs(w) @ np.abs(E))) / ns
             assert np.all(np.abs(g[sl] - gref) <= bound + 1e-12), (t, d0)
             mr, _, _ = O.adam(oc, t, gref, m0[sl], m10[sl], v0[sl])
-            assert np.max(np.abs(mg[sl] - mr) / np.maximum(np.abs(mr), cfg.lr)) <= 1e-5, (t, d0)
+            prop = stagecheck.adam_tolerance(oc, t, gref, m10[sl], v0[sl], bound)
+            assert np.all(np.abs(mg[sl] - mr) <= 1e-5 * np.maximum(np.abs(mr), cfg.lr) + prop), (t, d0)
             ma, m1a, va = O.adam(oc, t, g[sl], m0[sl], m10[sl], v0[sl])
             np.testing.assert_array_equal(mg[sl], ma)
             np.testing.assert_array_equal(m1g[sl], m1a)

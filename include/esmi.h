@@ -215,6 +215,32 @@ es_status es_eval(es_handle* h, float* fitness_out);
  * aid: not meant for a stream under capture. */
 es_status es_eval_timed(es_handle* h, float* fitness_out, void* start_event, void* stop_event);
 
+/* Allocation-free evaluate, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, hosts that forbid
+ * hipMalloc): es_eval's fused sample + evaluate without a handle.  It calls
+ * no hipMalloc or hipFree and allocates nothing; its per-chunk partial sums
+ * live in a static device array of 16 MiB per device (held until the
+ * process ends), whose address is looked up on the first call on a device.
+ *   cfg           a config es_init would accept; OpenAI-ES (scalar sigma)
+ *                 and the benchmark problems only (ES_ERR_UNSUPPORTED else);
+ *                 num_dims % 4 == 0 unless num_runs == 1 (ES_ERR_UNSUPPORTED)
+ *   mean          device [R][D], the runs' means
+ *   problem_data  device [D], the shift vector s for ES_PROB_SHIFTED_SPHERE
+ *                 (es_get_problem_data of a handle with this config gives
+ *                 it), NULL for the other problems
+ *   sigma         device [R], each run's sigma of generation t
+ *   t             generation whose noise is drawn, in [0, 2^32)
+ *   fitness       device [R][N] output, the same bits es_eval gives a handle
+ *                 with this config, mean, sigma and t
+ *   hip_stream    hipStream_t the kernels are enqueued on (NULL: default)
+ * ES_ERR_ARG when the evaluate's partial sums need more than 16 MiB (the
+ * default plan needs about 12.6 MB for any run count and population; a
+ * small cfg.plan_eval_blocks can need more).  Errors are reported through
+ * es_last_error(NULL).  Calls that overlap on one device (several streams or
+ * threads) share the array and race: serialise them. */
+es_status es_eval_noalloc(const es_config* cfg, const float* mean, const float* problem_data, const float* sigma,
+                          int64_t t, float* fitness, void* hip_stream);
+
 /* tell (Sec. 2.1 step 3): fitness shaping (es_shaping; with weight decay the
  * penalty pass regenerates the population once more), g = E^T y / (N sigma)
  * with eps regenerated from the counter, Adam step on the mean, best-so-far

@@ -30,9 +30,9 @@ static_assert(sizeof(es_config) == 160, "es_config has padding");
 
 thread_local char g_init_err[256] = {0};
 
-es_status init_fail(es_status s, const char* msg)
+es_status init_fail(es_status s, const char* msg, const char* who = "es_init")
 {
-    std::snprintf(g_init_err, sizeof(g_init_err), "es_init: %s", msg);
+    std::snprintf(g_init_err, sizeof(g_init_err), "%s: %s", who, msg);
     return s;
 }
 
@@ -531,6 +531,48 @@ es_status es_eval_timed(es_handle* h, float* fitness_out, void* start_event, voi
     if (h->phase != ASKED) return fail(h, ES_ERR_SEQUENCE, "es_eval_timed: no open ask");
     return enqueue_eval(h, fitness_out, reinterpret_cast<hipEvent_t>(start_event),
                         reinterpret_cast<hipEvent_t>(stop_event));
+}
+
+es_status es_eval_noalloc(const es_config* cfg, const float* mean, const float* problem_data, const float* sigma,
+                          int64_t t, float* fitness, void* hip_stream)
+{
+    constexpr const char* kNoalloc = "es_eval_noalloc";
+    if (!cfg || !mean || !sigma || !fitness) return init_fail(ES_ERR_ARG, "null argument", kNoalloc);
+    if (const char* why = validate(*cfg)) return init_fail(ES_ERR_ARG, why, kNoalloc);
+    if (cfg->strategy != ES_STRAT_OPENAI_ES)
+        return init_fail(ES_ERR_UNSUPPORTED, "OpenAI-ES sampling (the run's scalar sigma) only", kNoalloc);
+    if (cfg->problem != ES_PROB_SPHERE && cfg->problem != ES_PROB_SHIFTED_SPHERE && cfg->problem != ES_PROB_ROSENBROCK &&
+        cfg->problem != ES_PROB_RASTRIGIN)
+        return init_fail(ES_ERR_UNSUPPORTED, "the benchmark problems only (not the MLP, not none)", kNoalloc);
+    if ((cfg->problem == ES_PROB_SHIFTED_SPHERE) != (problem_data != nullptr))
+        return init_fail(ES_ERR_ARG, "problem_data is the shift vector of the shifted sphere "
+                                     "(and NULL for the other problems)", kNoalloc);
+    if (cfg->num_dims % 4 != 0 && cfg->num_runs != 1)
+        return init_fail(ES_ERR_UNSUPPORTED, "several runs need num_dims % 4 == 0", kNoalloc);
+    if (t < 0 || t > 0xFFFFFFFFll) return init_fail(ES_ERR_ARG, "t out of range", kNoalloc);
+    Geometry g;
+    g.D = cfg->num_dims;
+    g.nb = (g.D + 3) / 4;
+    g.Dp = 4 * g.nb;
+    g.N = cfg->popsize;
+    g.P = cfg->popsize / 2;
+    g.R = cfg->num_runs;
+    const EvalPlan plan = eval_plan(g, cfg->plan_eval_blocks);
+    const int64_t need = eval_partial_elems(g, plan);
+    if (need > (int64_t)NOALLOC_SCRATCH_FLOATS) {
+        std::snprintf(g_init_err, sizeof(g_init_err),
+                      "es_eval_noalloc: this evaluate needs %lld bytes of partial sums; the static scratch holds %zu",
+                      (long long)need * 4, NOALLOC_SCRATCH_FLOATS * 4);
+        return ES_ERR_ARG;
+    }
+    float* scratch = nullptr;
+    hipError_t e = noalloc_scratch(&scratch);
+    if (e != hipSuccess) return init_fail(ES_ERR_HIP, hipGetErrorString(e), kNoalloc);
+    e = launch_eval_bbob(g, *cfg, plan, (uint32_t)t, mean, problem_data, scratch, fitness, sigma, nullptr, 1.0,
+                         reinterpret_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return init_fail(ES_ERR_HIP, hipGetErrorString(e), kNoalloc);
+    g_init_err[0] = 0;
+    return ES_OK;
 }
 
 es_status es_tell(es_handle* h, const float* fitness)

@@ -158,6 +158,12 @@ hipError_t launch_timed(void (*k)(KArgs...), dim3 grid, dim3 block, uint32_t lds
     return hipGetLastError();
 }
 
+// Allocation-free evaluate: the static per-device scratch that holds its
+// partial sums (16 MiB: the D = 1e6, N = 2048 evaluate needs 12.6 MB), and
+// the current device's address of it (looked up once per device).
+constexpr size_t NOALLOC_SCRATCH_FLOATS = (size_t)4 << 20;
+hipError_t noalloc_scratch(float** out);
+
 // Largest population the rank kernel stages in LDS.
 constexpr int32_t RANK_MAX_N = 16384;
 

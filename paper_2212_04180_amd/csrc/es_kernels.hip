@@ -32,6 +32,7 @@
 #include <math.h>
 #include <stddef.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "es_device.hpp"
@@ -1767,6 +1768,34 @@ hipError_t launch_debug_noise(const Geometry& g, const es_config& c, int32_t run
     k_debug_noise<<<grid_for(g.nb, 256), 256, 0, s>>>(words, eps, c.seed + (uint64_t)run, (uint32_t)pair, t,
                                                       g.D, g.nb);
     return hipGetLastError();
+}
+
+// Scratch of the allocation-free evaluate (es_eval_noalloc): the per-chunk
+// partial sums live in this array, one copy per device, held until the
+// process ends.  Host code never passes the array's name to a kernel (on the
+// host it is a stand-in, not a device address): noalloc_scratch looks up each
+// device's address once, with that device current, and hands that out.
+static __device__ __align__(256) float scratch[NOALLOC_SCRATCH_FLOATS];
+
+hipError_t noalloc_scratch(float** out)
+{
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static float* addr[kMaxDevices] = {};
+    *out = nullptr;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = static_cast<float*>(p);
+    }
+    *out = addr[dev];
+    return hipSuccess;
 }
 
 }  // namespace esmi

@@ -25,7 +25,7 @@ STRAT_OPENAI_ES, STRAT_PGPE, STRAT_SNES, STRAT_SEP_CMA = range(4)
 OPT_ADAM, OPT_CLIPUP = range(2)
 
 # Every symbol include/esmi.h declares, in declaration order.
-EXPORTS = ("es_init", "es_ask", "es_eval", "es_eval_timed", "es_tell", "es_run", "es_get_state", "es_set_state",
+EXPORTS = ("es_init", "es_ask", "es_eval", "es_eval_timed", "es_eval_noalloc", "es_tell", "es_run", "es_get_state", "es_set_state",
            "es_get_best", "es_get_shaped", "es_get_grad", "es_set_hparams", "es_get_hparams",
            "es_get_strategy_state", "es_set_strategy_state", "es_get_penalty",
            "es_get_problem_data", "es_debug_noise",
@@ -154,6 +154,7 @@ def lib() -> ctypes.CDLL:
         "es_ask": (i32, [vp, vp]),
         "es_eval": (i32, [vp, vp]),
         "es_eval_timed": (i32, [vp, vp, vp, vp]),
+        "es_eval_noalloc": (i32, [P(_Config), vp, vp, vp, i64, vp, vp]),
         "es_tell": (i32, [vp, vp]),
         "es_run": (i32, [vp, i32, vp]),
         "es_get_state": (i32, [vp, vp, vp, vp, P(i64)]),
@@ -191,6 +192,21 @@ def _ptr(t):
     if not t.is_contiguous():
         raise ValueError("contiguous tensor expected")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def eval_noalloc(cfg: ESConfig, mean, sigma, t: int, problem_data=None, out=None, stream=None):
+    """es_eval_noalloc: the fused sample + evaluate of generation t without a
+    handle and without device allocation inside the library.  mean [R][D],
+    sigma [R], problem_data [D] or None, out [R][N]: device tensors."""
+    if out is None:
+        out = torch.empty(cfg.num_runs, cfg.popsize, dtype=torch.float32, device=mean.device)
+    st = stream if stream is not None else torch.cuda.current_stream(mean.device)
+    cs = cfg.cstruct()
+    rc = lib().es_eval_noalloc(ctypes.byref(cs), _ptr(mean), _ptr(problem_data), _ptr(sigma), int(t), _ptr(out),
+                               ctypes.c_void_p(st.cuda_stream))
+    if rc != ES_OK:
+        raise EsError(rc, lib().es_last_error(None).decode())
+    return out
 
 
 class ES:

@@ -102,6 +102,9 @@ def parse():
     ap.add_argument("--cpu-sample-dims", type=int, default=0)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter calibration)")
+    ap.add_argument("--issue-costs", action="store_true",
+                    help="measure the issue cost of the instructions behind the slot weights (libesmi_probe.so) "
+                         "and print that JSON line instead")
     return ap.parse_args()
 
 
@@ -268,6 +271,54 @@ def time_workload(P, torch, name, K, W, path, dev, stream, copy_mib=0):
             "roofline": roof, "K": K}
 
 
+# Instructions of the probe (include/esmi_probe.h) in its enum order, the
+# launch's loop count for each (a few milliseconds per launch), and the slot
+# weight the algorithmic counts above give each.
+PROBE_OPS = [("v_fma_f32", 20000, 1), ("v_bitop3_b32", 20000, 1), ("v_mad_u64_u32", 10000, 2),
+             ("v_cvt_f32_u32", 20000, 2), ("v_cvt_pk_bf16_f32", 20000, None), ("v_log_f32", 5000, 4),
+             ("v_exp_f32", 5000, None), ("v_rcp_f32", 5000, None), ("v_sqrt_f32", 5000, 4), ("v_sin_f32", 5000, 4),
+             ("v_cos_f32", 5000, 4), ("v_fma_f64", 10000, 2), ("v_add_f64", 10000, 2),
+             ("v_mfma_f32_16x16x32_bf16", 2000, None)]
+
+
+def issue_costs(torch, dev, stream):
+    """Issue rate of each probed instruction on all 256 CUs (eight waves per
+    SIMD, eight independent chains per lane), timed with HIP events; the
+    slots of an instruction are v_fma_f32's rate over its rate."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2212_04180_amd", "libesmi_probe.so"))
+    lib.es_probe_issue.restype = ctypes.c_int32
+    lib.es_probe_issue.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+    lib.es_probe_threads.restype = ctypes.c_int64
+    lib.es_probe_chains.restype = ctypes.c_int32
+    threads, chains = lib.es_probe_threads(), lib.es_probe_chains()
+    sink = torch.empty(threads, dtype=torch.int32, device=dev)
+    out = {}
+    for op, (name, iters, model) in enumerate(PROBE_OPS):
+        times = []
+        for rep in range(4):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            rc = lib.es_probe_issue(op, iters, ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+            e1.record(stream)
+            if rc != 0:
+                raise RuntimeError(f"probe {name}: hip error {rc}")
+            torch.cuda.synchronize()
+            if rep:
+                times.append(e0.elapsed_time(e1) * 1e-3)
+        t = min(times)
+        wave_instr = threads // 64 * iters * chains
+        out[name] = {"seconds": t, "wave_instructions": wave_instr, "lane_ops_per_s": wave_instr * 64 / t,
+                     "model_slots": model}
+    fma = out["v_fma_f32"]["lane_ops_per_s"]
+    for name, v in out.items():
+        v["slots"] = fma / v["lane_ops_per_s"]
+        if name.startswith("v_mfma"):
+            v["flops_per_s"] = v["wave_instructions"] * 16384 / v["seconds"]
+            v["frac_of_bf16_peak"] = v["flops_per_s"] / BF16_MFMA_PEAK
+    return {"fma_f32_lane_ops_per_s": fma, "frac_of_slot_peak": fma / VALU_PEAK, "instructions": out}
+
+
 # The other workloads the default run also times: name -> (path, generations
 # timed, warm-up generations).  The per-call path for the MLP (its roofline
 # is the evaluate kernel's share of the bf16 MFMA peak), es_run for the three
@@ -289,6 +340,13 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
+    if args.issue_costs:
+        ic = issue_costs(torch, dev, stream)
+        for name, v in ic["instructions"].items():
+            log(f"[issue] {name:26s} {v['lane_ops_per_s']:.3e} lane-ops/s  {v['slots']:.2f} slots"
+                + (f" (model {v['model_slots']})" if v["model_slots"] is not None else ""))
+        print(json.dumps({"issue_costs": ic}), flush=True)
+        return
     res = time_workload(P, torch, args.workload, args.steps, args.warmup, args.path, dev, stream,
                         args.copy_calibration_mib)
     cfg, prob, ms, value = res["cfg"], res["prob"], res["ms"], res["value"]

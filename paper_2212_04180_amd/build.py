@@ -35,8 +35,25 @@ def compile_flags():
     ]
 
 
+PROBE_SRC = "es_probe.hip"
+PROBE_LIB = os.path.join(PKG, "libesmi_probe.so")
+
+
+def build_probe(cc: str, verbose: bool = False) -> str:
+    """The issue-rate probe behind the benchmark's slot weights (a separate
+    library; the generation never loads it)."""
+    tmp = PROBE_LIB + ".tmp%d" % os.getpid()
+    cmd = [cc, *compile_flags(), "-shared", "-x", "hip", os.path.join(CSRC, PROBE_SRC), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True, stderr=None if verbose else subprocess.PIPE)
+    os.replace(tmp, PROBE_LIB)
+    return PROBE_LIB
+
+
 def build(verbose: bool = False) -> str:
     cc = hipcc()
+    build_probe(cc, verbose)
     objs = []
     for src in SOURCES:
         obj = os.path.join(CSRC, src + ".o")

@@ -51,7 +51,7 @@ constexpr int TELL_LANES = 64;    // Philox blocks per tell workgroup
 constexpr int TELL_MAX_PS = 16;   // pair slices per tell workgroup (one wave each)
 constexpr int TELL_GROUP = 16;    // fp32 pairs folded into the fp64 sum at once
 constexpr int FUSED_WG = 256;     // threads of the fused multi-generation workgroup
-constexpr int FUSED_PRIO = 1;     // wave priority of the fused loop's short phases
+constexpr int FUSED_PRIO = 3;     // wave priority of the fused loop's short phases (the highest)
 
 // MLP 64-256-256-16, flattened [out][in] per layer then the bias.  Returns
 // 1/sqrt(fan_in) for a weight and 0 for a bias.
@@ -1216,6 +1216,14 @@ struct FusedArgs {
 };
 static_assert(std::is_standard_layout<FusedArgs>::value, "offsetof(FusedArgs, bcorr) is used on the device");
 
+// Wave priority 0, 1 or 2 (s_setprio takes an immediate).
+__device__ __forceinline__ void set_long_prio(uint32_t lp)
+{
+    if (lp == 0) __builtin_amdgcn_s_setprio(0);
+    else if (lp == 1) __builtin_amdgcn_s_setprio(1);
+    else __builtin_amdgcn_s_setprio(2);
+}
+
 template <int PROB>
 __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
 {
@@ -1274,12 +1282,17 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             ac.bc1 = kb[2 * it];
             ac.bc2 = kb[2 * it + 1];
         }
-        // evaluate: items (pair, chunk).  The evaluate and gradient phases run
-        // at the base wave priority, the short phases between them (fitness,
-        // ranks, update: latency chains on a few lanes) at a raised one, so
-        // that the long phases of the other runs' workgroups on the same CU
-        // fill the issue slots around them instead of delaying them.
-        __builtin_amdgcn_s_setprio(0);
+        // evaluate: items (pair, chunk).  The short phases (fitness, ranks,
+        // update: latency chains on a few lanes) run at the highest wave
+        // priority, so that the long phases of the other runs' workgroups on
+        // the same CU fill the issue slots around them instead of delaying
+        // them.  The long phases (evaluate, gradient) take turns: their
+        // priority cycles through 0, 1, 2 over the generations, offset by the
+        // workgroup index, so that no run of a CU is always the one served
+        // last (the oldest wave otherwise wins every tie, and the youngest run
+        // of a CU set the launch's length).
+        const uint32_t lp = ((uint32_t)it + (blockIdx.x & 3u)) % 3u;
+        set_long_prio(lp);
         const int64_t items = (int64_t)a.P * a.nchunks;
         for (int64_t i = threadIdx.x; i < items; i += blockDim.x) {
             const int32_t p = (int32_t)(i % a.P);
@@ -1353,7 +1366,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             }
         }
         __syncthreads();
-        __builtin_amdgcn_s_setprio(0);
+        set_long_prio(lp);
         // tell: items (block, pair slice), slices summed in order, then Adam
         for (int64_t i = threadIdx.x; i < (int64_t)a.ps * a.nb; i += blockDim.x) {
             const int32_t s = (int32_t)(i / a.nb);

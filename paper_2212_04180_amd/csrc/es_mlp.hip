@@ -107,6 +107,16 @@ __device__ __forceinline__ bf16x8 activate(const floatx4& lo, const floatx4& hi,
     return h;
 }
 
+// Two fp32 values rounded to bf16 (round to nearest even) in one
+// v_cvt_pk_bf16_f32: lo in bits 0-15, hi in bits 16-31.  Written out because
+// the compiler otherwise paired the two members' values and repacked them.
+__device__ __forceinline__ uint32_t pk_bf16(float lo, float hi)
+{
+    uint32_t r;
+    asm("v_cvt_pk_bf16_f32 %0, %1, %2" : "=v"(r) : "v"(lo), "v"(hi));
+    return r;
+}
+
 // One Philox block (4 weights) of W2 chunk `chunk` into the chunk buffers.
 // VEC: per-dimension sigma from sr (PGPE, SNES).
 template <bool VEC>
@@ -124,15 +134,15 @@ __device__ __forceinline__ void gen_w2_block(const float* __restrict__ mr, const
         const float4 s4 = *reinterpret_cast<const float4*>(sr + 4 * b);
         sv[0] = s4.x; sv[1] = s4.y; sv[2] = s4.z; sv[3] = s4.w;
     }
-    bf16x4 vp, vm;
+    float xp[4], xm[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-        vp[k] = (__bf16)fmaf(sv[k], e[k], mv[k]);
-        vm[k] = (__bf16)fmaf(-sv[k], e[k], mv[k]);
+        xp[k] = fmaf(sv[k], e[k], mv[k]);
+        xm[k] = fmaf(-sv[k], e[k], mv[k]);
     }
     const int row = (4 * i) / MLP_H, col = (4 * i) % MLP_H;
-    *reinterpret_cast<bf16x4*>(wp + row * W2S + col) = vp;
-    *reinterpret_cast<bf16x4*>(wm + row * W2S + col) = vm;
+    *reinterpret_cast<uint2*>(wp + row * W2S + col) = make_uint2(pk_bf16(xp[0], xp[1]), pk_bf16(xp[2], xp[3]));
+    *reinterpret_cast<uint2*>(wm + row * W2S + col) = make_uint2(pk_bf16(xm[0], xm[1]), pk_bf16(xm[2], xm[3]));
 }
 
 // Layer 2 on one W2 chunk (rows [W2_ROWS*c, +W2_ROWS)) for this wave's
@@ -228,12 +238,14 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
             if constexpr (VEC) {
                 sv[0] = sw[k].x; sv[1] = sw[k].y; sv[2] = sw[k].z; sv[3] = sw[k].w;
             }
-            bf16x4 vp, vm;
+            float xp[4], xm[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                vp[i] = (__bf16)fmaf(sv[i], e[i], mv[i]);
-                vm[i] = (__bf16)fmaf(-sv[i], e[i], mv[i]);
+                xp[i] = fmaf(sv[i], e[i], mv[i]);
+                xm[i] = fmaf(-sv[i], e[i], mv[i]);
             }
+            const uint2 vp = make_uint2(pk_bf16(xp[0], xp[1]), pk_bf16(xp[2], xp[3]));
+            const uint2 vm = make_uint2(pk_bf16(xm[0], xm[1]), pk_bf16(xm[2], xm[3]));
             __bf16 *dp, *dm;
             if (k < 4) {  // W1 [256][64]
                 const int i4 = 4 * (tid + k * MLP_THREADS);
@@ -248,8 +260,8 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
                 dp = S.w2a[0] + (i4 / MLP_H) * W2S + i4 % MLP_H;
                 dm = S.w2a[1] + (i4 / MLP_H) * W2S + i4 % MLP_H;
             }
-            *reinterpret_cast<bf16x4*>(dp) = vp;
-            *reinterpret_cast<bf16x4*>(dm) = vm;
+            *reinterpret_cast<uint2*>(dp) = vp;
+            *reinterpret_cast<uint2*>(dm) = vm;
         }
         if (jb >= 0) {
             float e[4];
@@ -329,6 +341,7 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
         const __bf16* wc = (c & 1) ? S.a.w2b[mem] : S.w2a[mem];
         const bool gen = c + 1 < W2_CHUNKS;
         if (mem == 0 && gen)
+#pragma unroll
             for (int j = 0; j < W2_BLOCKS_PER_THREAD; ++j)
                 gen_w2_block<VEC>(mr, sr, k0, k1, (uint32_t)p, t, c + 1, (int)threadIdx.x + j * MLP_THREADS, sigma, nb_p,
                                   nb_m);
@@ -338,6 +351,7 @@ __global__ __launch_bounds__(MLP_THREADS) void k_eval_mlp(const float* __restric
             layer2_act(S, acc, c, mem, y, q, l16);
         }
         if (mem == 1 && gen)
+#pragma unroll
             for (int j = 0; j < W2_BLOCKS_PER_THREAD; ++j)
                 gen_w2_block<VEC>(mr, sr, k0, k1, (uint32_t)p, t, c + 1, (int)threadIdx.x + j * MLP_THREADS, sigma, nb_p,
                                   nb_m);

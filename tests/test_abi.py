@@ -56,3 +56,19 @@ def test_product_does_not_reach_the_oracle():
             if fn.endswith((".py", ".hip", ".cpp", ".hpp", ".h")):
                 text = open(os.path.join(dirpath, fn)).read()
                 assert "oracle" not in text.lower().replace("the oracle", ""), fn
+
+
+def test_probe_library_exports_its_header():
+    """The issue-rate probe (a measurement aid of the benchmark) is a library
+    of its own: the generation's library does not carry it."""
+    src = open(os.path.join(ROOT, "include", "esmi_probe.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"\b(es_probe_[a-z_]+)\s*\(", src)
+    assert set(names) == {"es_probe_issue", "es_probe_threads", "es_probe_chains"}
+    L = ctypes.CDLL(os.path.join(ROOT, "paper_2212_04180_amd", "libesmi_probe.so"))
+    for n in names:
+        assert hasattr(L, n)
+    L.es_probe_threads.restype = ctypes.c_int64
+    assert L.es_probe_threads() == 2048 * 256
+    from paper_2212_04180_amd import esmi
+    assert not hasattr(esmi.lib(), "es_probe_issue")

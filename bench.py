@@ -69,8 +69,8 @@ def profiled_traffic(workload, key="eval_hbm_bytes_request_sized", cast=int):
     per launch with each read request priced at its size (the evaluate
     kernel's scalar-cache reads are 64-B requests, the copy's 128-B);
     eval_hbm_bytes_per_launch is the copy-calibrated FETCH_SIZE + WRITE_SIZE,
-    eval_valu_issued_slots_per_pair_block the issued VALU slots read from
-    SQ_INSTS_VALU and the instruction mix."""
+    eval_valu_instructions_per_pair_block the VALU instructions the kernel
+    issues per pair-block (SQ_INSTS_VALU per wave of 64 pairs)."""
     path = os.path.join(ROOT, "profiles", f"k_eval_bbob_{workload}.txt")
     if not os.path.exists(path):
         return None
@@ -84,6 +84,29 @@ def profiled_traffic(workload, key="eval_hbm_bytes_request_sized", cast=int):
         return None
     try:
         return cast(kv[key])
+    except (KeyError, ValueError):
+        return None
+
+
+def issue_profile(key):
+    """A figure of the committed issue-rate summary (valu_issue_costs_gfx950.txt),
+    or None if it is missing or the probe source changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "valu_issue_costs_gfx950.txt")
+    src = os.path.join(ROOT, "paper_2212_04180_amd", "csrc", "es_probe.hip")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip().split()[0] if v.strip() else ""
+    with open(src, "rb") as fh:
+        if kv.get("probe_source_sha256") != hashlib.sha256(fh.read()).hexdigest():
+            return None
+    try:
+        return float(kv[key])
     except (KeyError, ValueError):
         return None
 
@@ -233,7 +256,8 @@ def time_workload(P, torch, name, K, W, path, dev, stream, copy_mib=0):
             tell_items = R * mu * ((D + 3) // 4)
         achieved = pair_blocks * eval_slots / (eval_ms * 1e-3)
         tell_achieved = tell_items * tell_slots / (rest_ms * 1e-3)
-        issued = profiled_traffic(name, "eval_valu_issued_slots_per_pair_block", float)
+        issued = profiled_traffic(name, "eval_valu_instructions_per_pair_block", float)
+        best_stream = issue_profile("fma_f32_vvv_frac_of_slot_peak")
         roof = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                 "unit": "T VALU lane-op slots/s", "frac": achieved / VALU_PEAK,
                 "traffic": profiled_traffic(name),
@@ -241,8 +265,9 @@ def time_workload(P, torch, name, K, W, path, dev, stream, copy_mib=0):
                 "kernel": "k_eval_bbob (fused sample+evaluate)",
                 "kernel_ms": eval_ms, "slots_per_pair_block": eval_slots,
                 "pair_blocks_per_launch": pair_blocks,
-                "issued_slots_per_pair_block": issued,
+                "issued_instructions_per_pair_block": issued,
                 "issued_frac": None if issued is None else pair_blocks * issued / (eval_ms * 1e-3) / VALU_PEAK,
+                "best_single_instruction_stream_frac": best_stream,
                 "tell": {"kernel": "k_eval_reduce + k_rank + k_tell (+ the strategy's update passes): the rest "
                                    "of the generation", "kernel_ms": rest_ms, "achieved": tell_achieved / 1e12,
                          "frac": tell_achieved / VALU_PEAK, "slots_per_pair_block": tell_slots}}
@@ -278,7 +303,8 @@ PROBE_OPS = [("v_fma_f32", 20000, 1), ("v_bitop3_b32", 20000, 1), ("v_mad_u64_u3
              ("v_cvt_f32_u32", 20000, 2), ("v_cvt_pk_bf16_f32", 20000, None), ("v_log_f32", 5000, 4),
              ("v_exp_f32", 5000, None), ("v_rcp_f32", 5000, None), ("v_sqrt_f32", 5000, 4), ("v_sin_f32", 5000, 4),
              ("v_cos_f32", 5000, 4), ("v_fma_f64", 10000, 2), ("v_add_f64", 10000, 2),
-             ("v_mfma_f32_16x16x32_bf16", 2000, None)]
+             ("v_mfma_f32_16x16x32_bf16", 2000, None), ("v_mul_f32", 20000, 1), ("v_xor_b32", 20000, 1),
+             ("v_fma_f32 (three VGPR sources)", 20000, 1)]
 
 
 def issue_costs(torch, dev, stream):

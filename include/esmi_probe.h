@@ -37,7 +37,10 @@ enum {
     ES_PROBE_FMA_F64 = 11,    /* v_fma_f64                          */
     ES_PROBE_ADD_F64 = 12,    /* v_add_f64                          */
     ES_PROBE_MFMA_BF16 = 13,  /* v_mfma_f32_16x16x32_bf16           */
-    ES_PROBE_NUM_OPS = 14
+    ES_PROBE_MUL_F32 = 14,    /* v_mul_f32                          */
+    ES_PROBE_XOR_B32 = 15,    /* v_xor_b32                          */
+    ES_PROBE_FMA_F32_VVV = 16, /* v_fma_f32 with three VGPR sources */
+    ES_PROBE_NUM_OPS = 17
 };
 
 int32_t es_probe_issue(int32_t op, int64_t iters, uint32_t* sink, void* hip_stream);

@@ -51,8 +51,8 @@ __global__ __launch_bounds__(PROBE_WG) void k_issue(int64_t iters, uint32_t* __r
         for (int64_t i = 0; i < iters; ++i) {
 #pragma unroll
             for (int c = 0; c < CHAINS; ++c) {
-                if constexpr (OP == ES_PROBE_FMA_F64) asm volatile("v_fma_f64 %0, %0, %1, %2" : "+v"(x[c]) : "v"(p), "v"(q));
-                else asm volatile("v_add_f64 %0, %0, %1" : "+v"(x[c]) : "v"(q));
+                if constexpr (OP == ES_PROBE_FMA_F64) asm volatile("v_fma_f64 %0, %0, %1, 0.5" : "+v"(x[c]) : "s"(p));
+                else asm volatile("v_add_f64 %0, %0, %1" : "+v"(x[c]) : "s"(q));
             }
         }
 #pragma unroll
@@ -81,10 +81,16 @@ __global__ __launch_bounds__(PROBE_WG) void k_issue(int64_t iters, uint32_t* __r
         for (int64_t i = 0; i < iters; ++i) {
 #pragma unroll
             for (int c = 0; c < CHAINS; ++c) {
-                if constexpr (OP == ES_PROBE_FMA_F32) asm volatile("v_fma_f32 %0, %0, %1, %2" : "+v"(x[c]) : "v"(p), "v"(q));
-                else if constexpr (OP == ES_PROBE_BITOP3) asm volatile("v_bitop3_b32 %0, %0, %1, %2 bitop3:0x96" : "+v"(x[c]) : "v"(p), "s"(kk));
+                // one VGPR source per instruction (the others a scalar register or
+                // an inline constant), as in most instructions of the hot kernels;
+                // ES_PROBE_FMA_F32_VVV reads three VGPRs
+                if constexpr (OP == ES_PROBE_FMA_F32) asm volatile("v_fma_f32 %0, %0, %1, 0.5" : "+v"(x[c]) : "s"(p));
+                else if constexpr (OP == ES_PROBE_FMA_F32_VVV) asm volatile("v_fma_f32 %0, %0, %1, %2" : "+v"(x[c]) : "v"(p), "v"(q));
+                else if constexpr (OP == ES_PROBE_MUL_F32) asm volatile("v_mul_f32_e32 %0, %1, %0" : "+v"(x[c]) : "s"(p));
+                else if constexpr (OP == ES_PROBE_XOR_B32) asm volatile("v_xor_b32_e32 %0, %1, %0" : "+v"(x[c]) : "s"(kk));
+                else if constexpr (OP == ES_PROBE_BITOP3) asm volatile("v_bitop3_b32 %0, %0, %1, %0 bitop3:0x96" : "+v"(x[c]) : "s"(kk));
                 else if constexpr (OP == ES_PROBE_CVT_F32_U32) asm volatile("v_cvt_f32_u32_e32 %0, %0" : "+v"(x[c]));
-                else if constexpr (OP == ES_PROBE_CVT_PK_BF16) asm volatile("v_cvt_pk_bf16_f32 %0, %0, %1" : "+v"(x[c]) : "v"(p));
+                else if constexpr (OP == ES_PROBE_CVT_PK_BF16) asm volatile("v_cvt_pk_bf16_f32 %0, %0, %1" : "+v"(x[c]) : "s"(p));
                 else if constexpr (OP == ES_PROBE_LOG) asm volatile("v_log_f32_e32 %0, %0" : "+v"(x[c]));
                 else if constexpr (OP == ES_PROBE_EXP) asm volatile("v_exp_f32_e32 %0, %0" : "+v"(x[c]));
                 else if constexpr (OP == ES_PROBE_RCP) asm volatile("v_rcp_f32_e32 %0, %0" : "+v"(x[c]));
@@ -133,6 +139,9 @@ int32_t es_probe_issue(int32_t op, int64_t iters, uint32_t* sink, void* hip_stre
     case ES_PROBE_FMA_F64: return (int32_t)launch_issue<ES_PROBE_FMA_F64>(iters, sink, s);
     case ES_PROBE_ADD_F64: return (int32_t)launch_issue<ES_PROBE_ADD_F64>(iters, sink, s);
     case ES_PROBE_MFMA_BF16: return (int32_t)launch_issue<ES_PROBE_MFMA_BF16>(iters, sink, s);
+    case ES_PROBE_MUL_F32: return (int32_t)launch_issue<ES_PROBE_MUL_F32>(iters, sink, s);
+    case ES_PROBE_XOR_B32: return (int32_t)launch_issue<ES_PROBE_XOR_B32>(iters, sink, s);
+    case ES_PROBE_FMA_F32_VVV: return (int32_t)launch_issue<ES_PROBE_FMA_F32_VVV>(iters, sink, s);
     }
     return (int32_t)hipErrorInvalidValue;
 }

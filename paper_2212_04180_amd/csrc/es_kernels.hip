@@ -1216,6 +1216,14 @@ struct FusedArgs {
 };
 static_assert(std::is_standard_layout<FusedArgs>::value, "offsetof(FusedArgs, bcorr) is used on the device");
 
+// The value of the lane whose index differs in bit 0, 1 or 2 (bit 0 and 1:
+// DPP quad permutations [1,0,3,2] and [2,3,0,1]; bit 2: ds_swizzle in
+// bitmask mode, and_mask 31, xor_mask 4).  Every lane of the wave must be
+// active.
+__device__ __forceinline__ int32_t xor_lane1(int32_t x) { return __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false); }
+__device__ __forceinline__ int32_t xor_lane2(int32_t x) { return __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false); }
+__device__ __forceinline__ int32_t xor_lane4(int32_t x) { return __builtin_amdgcn_ds_swizzle(x, (4 << 10) | 0x1F); }
+
 // Wave priority 0, 1 or 2 (s_setprio takes an immediate).
 __device__ __forceinline__ void set_long_prio(uint32_t lp)
 {
@@ -1261,12 +1269,26 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         vs[i] = a.v[goff + i];
     }
     for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) tab[j] = a.table[j];
+    // pair bounds of the gradient's slices: slice s takes pairs [P s / ps, P (s+1) / ps)
+    __shared__ int32_t sl_bound[TELL_MAX_PS + 1];
+    if (threadIdx.x <= (uint32_t)a.ps) sl_bound[threadIdx.x] = (int32_t)(((int64_t)a.P * threadIdx.x) / a.ps);
     if (threadIdx.x == 0) {
         best_k = a.best_okey[r];
         best_fv = a.best_f[r];
         best_jj = -1;
     }
     __syncthreads();
+    // Every generation a thread walks the same items: evaluate item i is
+    // (pair i % P, chunk i / P), gradient item i is (slice i / nb, block
+    // i % nb), for i = thread, thread + FUSED_WG, ...  The walks are set up
+    // here once (all sizes of a fused run fit in 32 bits: its state is in LDS)
+    // and stepped with additions inside the loop.
+    const int32_t nb32 = (int32_t)a.nb, P32 = a.P;
+    const int32_t ev_items = P32 * (int32_t)a.nchunks, tl_items = a.ps * nb32;
+    const int32_t ev_p0 = (int32_t)threadIdx.x % P32, ev_c0 = (int32_t)threadIdx.x / P32;
+    const int32_t ev_dp = FUSED_WG % P32, ev_dc = FUSED_WG / P32;
+    const int32_t tl_b0 = (int32_t)threadIdx.x % nb32, tl_s0 = (int32_t)threadIdx.x / nb32;
+    const int32_t tl_db = FUSED_WG % nb32, tl_ds = FUSED_WG / nb32;
 
     for (int32_t it = 0; it < a.T; ++it) {
         const uint32_t t = a.t0 + (uint32_t)it;
@@ -1293,16 +1315,22 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         // of a CU set the launch's length).
         const uint32_t lp = ((uint32_t)it + (blockIdx.x & 3u)) % 3u;
         set_long_prio(lp);
-        const int64_t items = (int64_t)a.P * a.nchunks;
-        for (int64_t i = threadIdx.x; i < items; i += blockDim.x) {
-            const int32_t p = (int32_t)(i % a.P);
-            const int64_t c = i / a.P;
-            const int64_t b0 = c * a.bc, b1 = b0 + a.bc < a.nb ? b0 + a.bc : a.nb;
-            double accp, accm;
-            eval_chunk<PROB, LANES_BLOCK_AND_ROW>(ms, a.pdata, k0, k1, (uint32_t)p, t, b0, b1, a.D, sigma, a.ra,
-                                                  accp, accm);
-            part[c * a.N + p] = (float)accp;
-            part[c * a.N + p + a.P] = (float)accm;
+        {
+            int32_t p = ev_p0, c = ev_c0;
+            for (int32_t i = (int32_t)threadIdx.x; i < ev_items; i += FUSED_WG) {
+                const int64_t b0 = (int64_t)c * a.bc, b1 = b0 + a.bc < a.nb ? b0 + a.bc : a.nb;
+                double accp, accm;
+                eval_chunk<PROB, LANES_BLOCK_AND_ROW>(ms, a.pdata, k0, k1, (uint32_t)p, t, b0, b1, a.D, sigma, a.ra,
+                                                      accp, accm);
+                part[c * a.N + p] = (float)accp;
+                part[c * a.N + p + P32] = (float)accm;
+                p += ev_dp;
+                c += ev_dc;
+                if (p >= P32) {
+                    p -= P32;
+                    ++c;
+                }
+            }
         }
         __syncthreads();
         __builtin_amdgcn_s_setprio(FUSED_PRIO);
@@ -1310,10 +1338,26 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         const int nq = a.nchunks < RED_SLICES ? (int)a.nchunks : RED_SLICES;  // slices beyond add 0
         for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) {
             double tot = a.add;
-            for (int q = 0; q < nq; ++q) {
-                double acc = 0.0;
-                for (int64_t c = q; c < a.nchunks; c += RED_SLICES) acc += (double)part[c * a.N + j];
-                tot += acc;
+            if (a.nchunks <= RED_SLICES) {
+                // one chunk per slice: four loads in flight ahead of the sum
+                for (int q0 = 0; q0 < nq; q0 += 4) {
+                    float pv[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) pv[u] = q0 + u < nq ? part[(q0 + u) * a.N + j] : 0.f;
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        if (q0 + u < nq) {
+                            double acc = 0.0;
+                            acc += (double)pv[u];
+                            tot += acc;
+                        }
+                }
+            } else {
+                for (int q = 0; q < nq; ++q) {
+                    double acc = 0.0;
+                    for (int64_t c = q; c < a.nchunks; c += RED_SLICES) acc += (double)part[c * a.N + j];
+                    tot += acc;
+                }
             }
             const float f = (float)tot;
             fit[j] = f;
@@ -1336,6 +1380,19 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
                     K = keys[j];
                     const int32_t s0 = q * cs, s1 = s0 + cs < a.N ? s0 + cs : a.N;
                     int32_t k = s0;
+                    for (; k + 8 <= s1; k += 8) {
+                        uint4 q4[2];
+#pragma unroll
+                        for (int u = 0; u < 2; ++u) q4[u] = *reinterpret_cast<const uint4*>(keys + k + 4 * u);
+#pragma unroll
+                        for (int u = 0; u < 2; ++u) {
+                            const int32_t kk = k + 4 * u;
+                            rk += (q4[u].x < K) | ((q4[u].x == K) & (kk < j));
+                            rk += (q4[u].y < K) | ((q4[u].y == K) & (kk + 1 < j));
+                            rk += (q4[u].z < K) | ((q4[u].z == K) & (kk + 2 < j));
+                            rk += (q4[u].w < K) | ((q4[u].w == K) & (kk + 3 < j));
+                        }
+                    }
                     for (; k + 4 <= s1; k += 4) {
                         const uint4 q4 = *reinterpret_cast<const uint4*>(keys + k);
                         rk += (q4.x < K) | ((q4.x == K) & (k < j));
@@ -1345,11 +1402,12 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
                     }
                     for (; k < s1; ++k) rk += (keys[k] < K) | ((keys[k] == K) & (k < j));
                 }
-                // every lane of the wave takes part in the exchanges
-                rk += __shfl_xor(rk, 1);
-                rk += __shfl_xor(rk, 2);
+                // every lane of the wave takes part in the exchanges (lane
+                // xor 1 and xor 2 within the quad by DPP, xor 4 by swizzle)
+                rk += xor_lane1(rk);
+                rk += xor_lane2(rk);
                 const float yj = p < a.P ? (a.raw ? (a.maximize ? -fit[j] : fit[j]) : tab[rk]) : 0.f;
-                const float yo = __shfl_xor(yj, 4);
+                const float yo = __int_as_float(xor_lane4(__float_as_int(yj)));
                 if (p < a.P && q == 0) {
                     if (mem == 0) wf[p] = yj - yo;
                     if (rk == 0) {
@@ -1368,15 +1426,20 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         __syncthreads();
         set_long_prio(lp);
         // tell: items (block, pair slice), slices summed in order, then Adam
-        for (int64_t i = threadIdx.x; i < (int64_t)a.ps * a.nb; i += blockDim.x) {
-            const int32_t s = (int32_t)(i / a.nb);
-            const int64_t b = i - (int64_t)s * a.nb;
-            const int32_t pb = (int32_t)(((int64_t)a.P * s) / a.ps);
-            const int32_t pe = (int32_t)(((int64_t)a.P * (s + 1)) / a.ps);
-            double a64[4] = {0.0, 0.0, 0.0, 0.0};
-            tell_slice<LANES_BLOCK_AND_ROW>(wf, k0, k1, (uint32_t)b, t, pb, pe, a64);
+        {
+            int32_t b = tl_b0, s = tl_s0;
+            for (int32_t i = (int32_t)threadIdx.x; i < tl_items; i += FUSED_WG) {
+                double a64[4] = {0.0, 0.0, 0.0, 0.0};
+                tell_slice<LANES_BLOCK_AND_ROW>(wf, k0, k1, (uint32_t)b, t, sl_bound[s], sl_bound[s + 1], a64);
 #pragma unroll
-            for (int k = 0; k < 4; ++k) red[((int64_t)s * a.nb + b) * 4 + k] = a64[k];
+                for (int k = 0; k < 4; ++k) red[(s * nb32 + b) * 4 + k] = a64[k];
+                b += tl_db;
+                s += tl_ds;
+                if (b >= nb32) {
+                    b -= nb32;
+                    ++s;
+                }
+            }
         }
         __syncthreads();
         __builtin_amdgcn_s_setprio(FUSED_PRIO);
@@ -1384,9 +1447,16 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         const double inv_ns = 1.0 / (2.0 * (double)a.P * (double)sigma);  // 1 / (N sigma)
         for (int64_t i = threadIdx.x; i < 4 * a.nb; i += blockDim.x) {
             // one dim per lane: the slices in order, then Adam
+            // four slices' loads in flight ahead of the ordered sum
             double s64 = red[i];
-#pragma unroll 4
-            for (int q = 1; q < a.ps; ++q) s64 += red[(int64_t)q * 4 * a.nb + i];
+            for (int q0 = 1; q0 < a.ps; q0 += 4) {
+                double rv[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) rv[u] = q0 + u < a.ps ? red[(q0 + u) * 4 * nb32 + i] : 0.0;
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (q0 + u < a.ps) s64 += rv[u];
+            }
             const float mo = ms[i];
             float mn, m1n, vn, gg;
             adam_dim(s64, inv_ns, ac, lr, i, a.D, mo, m1s[i], vs[i], mn, m1n, vn, gg);
@@ -1760,6 +1830,7 @@ hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPla
     }
     a.seed = c.seed; a.t0 = t0; a.T = T; a.D = g.D; a.nb = g.nb; a.N = g.N; a.P = g.P; a.R = g.R;
     a.bc = e.bc; a.nchunks = e.nchunks; a.ps = tell_slices(g); a.ra = c.rastrigin_a;
+    if (a.ps < 1 || a.ps > TELL_MAX_PS) return hipErrorInvalidValue;  // the kernel's slice table holds TELL_MAX_PS + 1
     a.add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;
     a.maximize = c.maximize; a.raw = c.shaping == ES_SHAPE_RAW;
     a.hp = hp;

@@ -127,7 +127,7 @@ typedef enum { ES_OPT_ADAM = 0, ES_OPT_CLIPUP = 1 } es_optimizer;
 typedef struct es_config {
     int64_t num_dims;   /* D >= 1                                           */
     uint64_t seed;      /* base seed                                         */
-    int32_t popsize;    /* N >= 2, even: N/2 antithetic pairs                */
+    int32_t popsize;    /* N >= 2, even, <= 2^24: N/2 antithetic pairs       */
     int32_t num_runs;   /* R >= 1 independent runs                           */
     float sigma;        /* > 0, perturbation scale                           */
     float lr;           /* Adam learning rate                                */
@@ -175,11 +175,18 @@ typedef struct es_config {
      *                     fused loop wherever it supports the config (in
      *                     the fused loop's summation order, which equals the
      *                     per-call kernels' only where the library itself
-     *                     would choose the fused loop)                     */
+     *                     would choose the fused loop)
+     *   plan_rank_path    how the ranks are found (same ranks, same bits
+     *                     either way): 1 = each workgroup counts against the
+     *                     run's keys in LDS (popsize <= 16384), 2 = the
+     *                     run's composite keys (key, member) are radix-sorted
+     *                     and a member's position is its rank (also needs
+     *                     num_runs * popsize < 2^31); 0 = 1 up to popsize
+     *                     16384, 2 beyond                                  */
     int32_t plan_eval_blocks;
     int32_t plan_tell_split;
     int32_t plan_run_path;
-    int32_t reserved;   /* must be 0                                         */
+    int32_t plan_rank_path;
     int32_t reserved2;  /* must be 0                                         */
 } es_config;
 

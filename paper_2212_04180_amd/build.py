@@ -14,7 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libesmi.so")
-SOURCES = ["es_kernels.hip", "es_mlp.hip", "es_api.cpp"]
+SOURCES = ["es_kernels.hip", "es_mlp.hip", "es_rank_sort.hip", "es_api.cpp"]
 ARCH = "gfx950"
 
 

@@ -88,6 +88,9 @@ struct es_handle {
     void* mlp_scratch = nullptr;  // MLP inputs and teacher outputs of the current generation
     int64_t teacher_t = -1;       // generation whose inputs and teacher outputs are in mlp_scratch
     int run_path = 0;  // 0 auto, 1 per-call kernels, 2 fused loop
+    // sort-based ranks (populations beyond RANK_MAX_N, or plan_rank_path 2)
+    bool rank_sort = false;
+    RankSortBuffers rs{};
     char err[512] = {0};
 };
 
@@ -128,7 +131,7 @@ const char* validate(const es_config& c)
     if (c.num_dims < 1) return "num_dims must be >= 1";
     if (c.num_dims > ((int64_t)1 << 34)) return "num_dims exceeds 2^34";
     if (c.popsize < 2 || (c.popsize & 1)) return "popsize must be even and >= 2";
-    if (c.popsize > RANK_MAX_N) return "popsize exceeds 16384";
+    if (c.popsize > POP_MAX_N) return "popsize exceeds 2^24";
     if (c.num_runs < 1 || c.num_runs > 65535) return "num_runs must be in [1, 65535]";
     if (!(c.sigma > 0.0f) || !std::isfinite(c.sigma)) return "sigma must be finite and > 0";
     if (!std::isfinite(c.lr) || c.lr < 0.0f) return "lr must be finite and >= 0";
@@ -156,7 +159,12 @@ const char* validate(const es_config& c)
     if (c.strategy < ES_STRAT_OPENAI_ES || c.strategy > ES_STRAT_SEP_CMA) return "unknown strategy";
     if (c.strategy == ES_STRAT_SEP_CMA && !(c.elite_ratio > 0.0f && c.elite_ratio <= 1.0f))
         return "elite_ratio must be in (0, 1]";
-    if (c.reserved != 0 || c.reserved2 != 0) return "reserved fields must be 0";
+    if (c.reserved2 != 0) return "reserved fields must be 0";
+    if (c.plan_rank_path < 0 || c.plan_rank_path > 2) return "plan_rank_path must be 0, 1 or 2";
+    if (c.plan_rank_path == 1 && c.popsize > RANK_MAX_N)
+        return "plan_rank_path 1 (ranks counted in LDS) takes popsize <= 16384";
+    if ((c.popsize > RANK_MAX_N || c.plan_rank_path == 2) && (int64_t)c.popsize * c.num_runs > INT32_MAX)
+        return "sort-based ranks need num_runs * popsize < 2^31";
     if (c.plan_eval_blocks < 0) return "plan_eval_blocks must be >= 0";
     if (c.plan_tell_split < 0 || c.plan_tell_split > 65535) return "plan_tell_split must be in [0, 65535]";
     if (c.plan_run_path < 0 || c.plan_run_path > 2) return "plan_run_path must be 0, 1 or 2";
@@ -267,7 +275,8 @@ void free_all(es_handle* h)
     void* ptrs[] = {h->m, h->m1, h->v, h->best_x, h->grad, h->best_okey, h->best_f, h->best_j, h->table,
                     h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->mlp_scratch,
                     h->tell_part, h->hp[0], h->hp[1], h->pen, h->bfold, h->sig, h->vel, h->gbuf,
-                    h->gpart, h->vpart, h->elite, h->cw, h->cmaC, h->zw, h->qd};
+                    h->gpart, h->vpart, h->elite, h->cw, h->cmaC, h->zw, h->qd,
+                    h->rs.kin, h->rs.kout, h->rs.keys, h->rs.offsets, h->rs.stats, h->rs.temp};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
 }
@@ -287,7 +296,7 @@ es_status enqueue_tell(es_handle* h, const float* fitness, float* gen_best)
     }
     ES_HIP(h, launch_rank(g, h->cfg, fitness, h->pen, h->table, h->ybar_table, h->y, h->rank, h->wfold, h->bfold,
                           h->elite, h->cma.mu, h->best_okey, h->best_f, h->best_j, gen_best, hp, h->hp[1 - h->hp_cur],
-                          h->stream),
+                          h->rank_sort ? &h->rs : nullptr, h->stream),
            "rank kernel");
     const AdamConsts a = adam_consts(h->cfg, h->t);
     TellBuffers tb;
@@ -455,6 +464,19 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     if (e == hipSuccess && clipup) e = dalloc(&h->gbuf, rows);
     if (e == hipSuccess && clipup) e = dalloc(&h->gpart, tell_groups(g) * g.R);
     if (e == hipSuccess && clipup) e = dalloc(&h->vpart, tell_groups(g) * g.R);
+    h->rank_sort = g.N > RANK_MAX_N || cfg->plan_rank_path == 2;
+    if (e == hipSuccess && h->rank_sort) {
+        const size_t n = (size_t)g.N * g.R;
+        e = dalloc(&h->rs.kin, n);
+        if (e == hipSuccess) e = dalloc(&h->rs.kout, n);
+        if (e == hipSuccess) e = dalloc(&h->rs.keys, n);
+        if (e == hipSuccess) e = dalloc(&h->rs.offsets, (size_t)g.R + 1);
+        if (e == hipSuccess) e = dalloc(&h->rs.stats, 4 * (size_t)g.R);
+        h->rs.temp_bytes = rank_sort_temp_bytes(g);
+        if (e == hipSuccess && h->rs.temp_bytes == 0) e = hipErrorInvalidValue;
+        if (e == hipSuccess) e = dalloc(reinterpret_cast<char**>(&h->rs.temp), h->rs.temp_bytes);
+        if (e == hipSuccess) e = launch_rank_offsets(g, h->rs.offsets, h->stream);
+    }
     if (e != hipSuccess) {
         free_all(h);
         delete h;

@@ -63,12 +63,28 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
                             const float* m, const float* pdata, float* partial, float* fit,
                             const float* hp, const float* svec, double div, hipStream_t s,
                             hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+// Sort-based ranks (populations beyond RANK_MAX_N, or on request): every
+// run's composite keys (order key << 32 | member) sorted ascending.
+struct RankSortBuffers {
+    uint64_t* kin;     // [R][N] composite keys
+    uint64_t* kout;    // [R][N] sorted per run
+    uint32_t* keys;    // [R][N] shaped order keys
+    int32_t* offsets;  // [R + 1] run starts r N
+    double* stats;     // [R][4] per-run statistics of the shaped keys
+    void* temp;        // sort scratch
+    size_t temp_bytes;
+};
+size_t rank_sort_temp_bytes(const Geometry& g);                                  // 0 on failure
+hipError_t launch_rank_sort(const Geometry& g, const RankSortBuffers& rs, hipStream_t s);  // kin -> kout
+hipError_t launch_rank_offsets(const Geometry& g, int32_t* offsets, hipStream_t s);
 // table: the shaping table indexed by rank (centered ranks, or SNES
-// utilities by rank), ybar_table its mean; bfold: PGPE / SNES second weight.
+// utilities by rank), ybar_table its mean; bfold: PGPE / SNES second weight;
+// rs: sort-based ranks (null: counted in LDS, N <= RANK_MAX_N).
 hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* pen,
                        const float* table, double ybar_table, float* y, int32_t* rank, float* wfold, float* bfold,
                        int32_t* elite, int32_t mu, uint32_t* best_okey, float* best_f, int32_t* best_j,
-                       float* gen_best, const float* hp_cur, float* hp_next, hipStream_t s);
+                       float* gen_best, const float* hp_cur, float* hp_next, const RankSortBuffers* rs,
+                       hipStream_t s);
 // Split of the gradient kernel's pairs: ps pair slices (one wave each) per
 // workgroup, nsplit workgroups per group of 64 Philox blocks.  With nsplit > 1
 // every workgroup stores its partial sums (part, fp64 [R][nsplit][nb][4]) and
@@ -164,7 +180,9 @@ hipError_t launch_timed(void (*k)(KArgs...), dim3 grid, dim3 block, uint32_t lds
 constexpr size_t NOALLOC_SCRATCH_FLOATS = (size_t)4 << 20;
 hipError_t noalloc_scratch(float** out);
 
-// Largest population the rank kernel stages in LDS.
+// Largest population the rank kernel stages in LDS; larger ones take the
+// sort-based ranks, up to POP_MAX_N.
 constexpr int32_t RANK_MAX_N = 16384;
+constexpr int32_t POP_MAX_N = 1 << 24;
 
 }  // namespace esmi

@@ -427,6 +427,12 @@ struct ShapeArgs {
     double ybar_table;      // mean of the shaping table (table shaping)
     int32_t* elite;         // [R][N] Sep-CMA-ES: member of rank i, i < mu
     int32_t mu;
+    // Sort-based ranks (null: the workgroup counts in LDS): the shaped order
+    // keys [R][N], the ranks [R][N] and the per-run statistics [R][4] of
+    // k_rank_stats, all made by the kernels ahead of k_rank.
+    const uint32_t* gkeys;
+    const int32_t* pre_rank;
+    const double* stats;
 };
 
 __device__ __forceinline__ float shaped_key(float f, float pen, int maximize, float w_decay)
@@ -462,52 +468,20 @@ __device__ __forceinline__ double block_sum(double v, double* red)
     return out;
 }
 
-__global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
-    const float* __restrict__ fit, const float* __restrict__ table, float* __restrict__ y,
-    int32_t* __restrict__ rank, float* __restrict__ wfold, uint32_t* __restrict__ best_okey,
-    float* __restrict__ best_f, int32_t* __restrict__ best_j, float* __restrict__ gen_best, int32_t N,
-    int32_t P, int32_t R, ShapeArgs sa)
+// Per-run statistics of the shaped keys kp[0, N) that the weights need:
+// the z-score mean and 1 / (deviation + 1e-10) (fp64, finite keys), PGPE's
+// mean of y when y is not a permutation of the table, and with weight decay
+// the raw best (smallest raw order key, lowest index first) in raw_best[2].
+// Sums over the run in one fixed order for a 256-lane workgroup, so every
+// workgroup (and k_rank_stats) gets the same bits.
+__device__ void rank_stats(const uint32_t* kp, const float* fr, const float* pr, int32_t N, const ShapeArgs& sa,
+                           double* red, uint32_t* raw_best, double& mu_out, double& inv_sd_out, double& ybar_out)
 {
-    extern __shared__ uint32_t keys[];
-    __shared__ int32_t cnt[RANK_SLICES][RANK_PAIRS][2];
-    __shared__ double red[RANK_PAIRS * RANK_SLICES];
-    __shared__ uint32_t raw_best[2];
-    const int32_t r = blockIdx.y;
-    const float* __restrict__ fr = fit + (int64_t)r * N;
-    const float* __restrict__ pr = sa.pen ? sa.pen + (int64_t)r * N : nullptr;
-    // this workgroup's own members, fetched first (used after the count)
-    const int32_t tx = threadIdx.x % RANK_PAIRS, s = threadIdx.x / RANK_PAIRS;
-    const int32_t p = blockIdx.x * RANK_PAIRS + tx;
-    const bool valid = p < P;
-    const int32_t j1 = valid ? p : 0, j2 = j1 + P;
-    const float f1 = fr[j1], f2 = fr[j2];
-    // the run's keys: eight loads per lane in flight at once
-    constexpr int KU = 8;
-    for (int32_t k0 = threadIdx.x; k0 < N; k0 += KU * (int32_t)blockDim.x) {
-        float fv[KU], pv[KU];
-#pragma unroll
-        for (int u = 0; u < KU; ++u) {
-            const int32_t k = k0 + u * (int32_t)blockDim.x;
-            fv[u] = k < N ? fr[k] : 0.0f;
-            pv[u] = pr && k < N ? pr[k] : 0.0f;
-        }
-#pragma unroll
-        for (int u = 0; u < KU; ++u) {
-            const int32_t k = k0 + u * (int32_t)blockDim.x;
-            if (k < N) keys[k] = order_key(shaped_key(fv[u], pv[u], sa.maximize, sa.w_decay), 0);
-        }
-    }
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        sa.hp_next[r] = schedule_step(sa.hp_cur[r], sa.sigma_decay, sa.sigma_final);
-        sa.hp_next[R + r] = schedule_step(sa.hp_cur[R + r], sa.lr_decay, sa.lr_final);
-    }
-    __syncthreads();
-
     double mu = 0.0, inv_sd = 0.0;
     if (sa.shaping == ES_SHAPE_Z_SCORE) {
         double sum = 0.0, n = 0.0;
         for (int32_t k = threadIdx.x; k < N; k += blockDim.x) {
-            const float v = key_value(keys[k]);
+            const float v = key_value(kp[k]);
             if (__builtin_isfinite(v)) { sum += (double)v; n += 1.0; }
         }
         sum = block_sum(sum, red);
@@ -515,7 +489,7 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
         mu = n > 0.0 ? sum / n : 0.0;
         double ss = 0.0;
         for (int32_t k = threadIdx.x; k < N; k += blockDim.x) {
-            const float v = key_value(keys[k]);
+            const float v = key_value(kp[k]);
             if (__builtin_isfinite(v)) ss += ((double)v - mu) * ((double)v - mu);
         }
         ss = block_sum(ss, red);
@@ -533,7 +507,7 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
                 yk = sa.w_decay != 0.0f ? shaped_key(fr[k], pr[k], sa.maximize, sa.w_decay)
                                         : (sa.maximize ? -fr[k] : fr[k]);
             } else {
-                const float v = key_value(keys[k]);
+                const float v = key_value(kp[k]);
                 yk = __builtin_isfinite(v) ? (float)(((double)v - mu) / inv_sd) : 0.0f;
             }
             acc += (double)yk;
@@ -557,9 +531,74 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
         __syncthreads();
     }
 
-    const uint32_t K1 = keys[j1], K2 = keys[j2];
-    const int32_t kb = (int32_t)(((int64_t)N * s) / RANK_SLICES);
-    const int32_t ke = (int32_t)(((int64_t)N * (s + 1)) / RANK_SLICES);
+    mu_out = mu;
+    inv_sd_out = inv_sd;
+    ybar_out = ybar;
+}
+
+__global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
+    const float* __restrict__ fit, const float* __restrict__ table, float* __restrict__ y,
+    int32_t* __restrict__ rank, float* __restrict__ wfold, uint32_t* __restrict__ best_okey,
+    float* __restrict__ best_f, int32_t* __restrict__ best_j, float* __restrict__ gen_best, int32_t N,
+    int32_t P, int32_t R, ShapeArgs sa)
+{
+    extern __shared__ uint32_t keys[];
+    __shared__ int32_t cnt[RANK_SLICES][RANK_PAIRS][2];
+    __shared__ double red[RANK_PAIRS * RANK_SLICES];
+    __shared__ uint32_t raw_best[2];
+    const int32_t r = blockIdx.y;
+    const float* __restrict__ fr = fit + (int64_t)r * N;
+    const float* __restrict__ pr = sa.pen ? sa.pen + (int64_t)r * N : nullptr;
+    // this workgroup's own members, fetched first (used after the count)
+    const int32_t tx = threadIdx.x % RANK_PAIRS, s = threadIdx.x / RANK_PAIRS;
+    const int32_t p = blockIdx.x * RANK_PAIRS + tx;
+    const bool valid = p < P;
+    const int32_t j1 = valid ? p : 0, j2 = j1 + P;
+    const float f1 = fr[j1], f2 = fr[j2];
+    const bool pre = sa.gkeys != nullptr;
+    // the run's keys: eight loads per lane in flight at once
+    constexpr int KU = 8;
+    for (int32_t k0 = threadIdx.x; !pre && k0 < N; k0 += KU * (int32_t)blockDim.x) {
+        float fv[KU], pv[KU];
+#pragma unroll
+        for (int u = 0; u < KU; ++u) {
+            const int32_t k = k0 + u * (int32_t)blockDim.x;
+            fv[u] = k < N ? fr[k] : 0.0f;
+            pv[u] = pr && k < N ? pr[k] : 0.0f;
+        }
+#pragma unroll
+        for (int u = 0; u < KU; ++u) {
+            const int32_t k = k0 + u * (int32_t)blockDim.x;
+            if (k < N) keys[k] = order_key(shaped_key(fv[u], pv[u], sa.maximize, sa.w_decay), 0);
+        }
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        sa.hp_next[r] = schedule_step(sa.hp_cur[r], sa.sigma_decay, sa.sigma_final);
+        sa.hp_next[R + r] = schedule_step(sa.hp_cur[R + r], sa.lr_decay, sa.lr_final);
+    }
+    __syncthreads();
+
+    double mu, inv_sd, ybar;
+    const bool penalised = sa.w_decay != 0.0f;
+    if (pre) {
+        const double* st = sa.stats + 4 * (int64_t)r;
+        mu = st[0];
+        inv_sd = st[1];
+        ybar = st[2];
+        if (threadIdx.x == 0) {
+            const uint64_t rb = __double_as_longlong(st[3]);
+            raw_best[0] = (uint32_t)(rb >> 32);
+            raw_best[1] = (uint32_t)rb;
+        }
+        __syncthreads();
+    } else {
+        rank_stats(keys, fr, pr, N, sa, red, raw_best, mu, inv_sd, ybar);
+    }
+    const uint32_t* kp = pre ? sa.gkeys + (int64_t)r * N : keys;
+    const uint32_t K1 = kp[j1], K2 = kp[j2];
+    // the count of slice s (the sort-based ranks arrive whole, in slice 0)
+    const int32_t kb = pre ? 0 : (int32_t)(((int64_t)N * s) / RANK_SLICES);
+    const int32_t ke = pre ? 0 : (int32_t)(((int64_t)N * (s + 1)) / RANK_SLICES);
     // rank_j = #{k : key_k < key_j} + #{k < j : key_k == key_j}
     int32_t c1 = 0, c2 = 0;
     int32_t k = kb;
@@ -577,6 +616,10 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
         const uint32_t kk = keys[k];
         c1 += (kk < K1) | ((kk == K1) & (k < j1));
         c2 += (kk < K2) | ((kk == K2) & (k < j2));
+    }
+    if (pre && s == 0) {
+        c1 = sa.pre_rank[(int64_t)r * N + j1];
+        c2 = sa.pre_rank[(int64_t)r * N + j2];
     }
     cnt[s][tx][0] = c1;
     cnt[s][tx][1] = c2;
@@ -633,6 +676,61 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
         } else {
             best_j[r] = -1;
         }
+    }
+}
+
+// Sort-based ranks, for populations whose keys do not fit a workgroup's LDS.
+// The composite key (order key << 32 | member) of every member sorts
+// ascending by key and then by index, so a member's position in its run's
+// sorted sequence is the count the rank kernel makes: the number of keys
+// below its own plus the equal keys of lower index.
+__global__ void k_rank_keys(const float* __restrict__ fit, const float* __restrict__ pen, int32_t N, int64_t total,
+                            int32_t maximize, float w_decay, uint32_t* __restrict__ keys, uint64_t* __restrict__ comp)
+{
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const uint32_t K = order_key(shaped_key(fit[i], pen ? pen[i] : 0.0f, maximize, w_decay), 0);
+        keys[i] = K;
+        comp[i] = ((uint64_t)K << 32) | (uint32_t)(i % N);
+    }
+}
+
+// rank[r][member] = position of the member's composite key in run r's sorted keys
+__global__ void k_rank_scatter(const uint64_t* __restrict__ sorted, int32_t N, int64_t total, int32_t* __restrict__ rank)
+{
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = i / N;
+        rank[r * N + (int64_t)(uint32_t)sorted[i]] = (int32_t)(i - r * N);
+    }
+}
+
+// Segment starts r N of the sort, r = 0 .. R.
+__global__ void k_rank_offsets(int32_t* __restrict__ off, int32_t N, int32_t R)
+{
+    for (int32_t r = blockIdx.x * blockDim.x + threadIdx.x; r <= R; r += gridDim.x * blockDim.x) off[r] = r * N;
+}
+
+// One workgroup per run: the statistics every rank workgroup of the run
+// would compute (rank_stats, the same order), stored once:
+// stats[r] = {mu, 1 / (deviation + 1e-10), ybar, raw best key << 32 | member}.
+__global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank_stats(const float* __restrict__ fit,
+                                                                       const uint32_t* __restrict__ keys, int32_t N,
+                                                                       ShapeArgs sa, double* __restrict__ stats)
+{
+    __shared__ double red[RANK_PAIRS * RANK_SLICES];
+    __shared__ uint32_t raw_best[2];
+    const int32_t r = blockIdx.x;
+    const float* fr = fit + (int64_t)r * N;
+    const float* pr = sa.pen ? sa.pen + (int64_t)r * N : nullptr;
+    if (threadIdx.x == 0) { raw_best[0] = 0xFFFFFFFFu; raw_best[1] = 0xFFFFFFFFu; }
+    __syncthreads();
+    double mu, inv_sd, ybar;
+    rank_stats(keys + (int64_t)r * N, fr, pr, N, sa, red, raw_best, mu, inv_sd, ybar);
+    if (threadIdx.x == 0) {
+        double* st = stats + 4 * (int64_t)r;
+        st[0] = mu;
+        st[1] = inv_sd;
+        st[2] = ybar;
+        st[3] = __longlong_as_double((long long)(((uint64_t)raw_best[0] << 32) | raw_best[1]));
     }
 }
 
@@ -1650,10 +1748,11 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
 hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, const float* pen,
                        const float* table, double ybar_table, float* y, int32_t* rank, float* wfold, float* bfold,
                        int32_t* elite, int32_t mu, uint32_t* best_okey, float* best_f, int32_t* best_j,
-                       float* gen_best, const float* hp_cur, float* hp_next, hipStream_t s)
+                       float* gen_best, const float* hp_cur, float* hp_next, const RankSortBuffers* rs,
+                       hipStream_t s)
 {
     const dim3 grid((unsigned)((g.P + RANK_PAIRS - 1) / RANK_PAIRS), (unsigned)g.R);
-    const size_t lds = sizeof(uint32_t) * (size_t)g.N;
+    const size_t lds = rs ? 0 : sizeof(uint32_t) * (size_t)g.N;
     ShapeArgs sa;
     sa.pen = c.w_decay != 0.0f ? pen : nullptr;
     sa.hp_cur = hp_cur;
@@ -1674,8 +1773,32 @@ hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, 
     sa.ybar_table = ybar_table;
     sa.elite = elite;
     sa.mu = mu;
+    sa.gkeys = nullptr;
+    sa.pre_rank = nullptr;
+    sa.stats = nullptr;
+    if (rs) {
+        // keys, sort, ranks and the per-run statistics ahead of the rank kernel
+        const int64_t total = (int64_t)g.R * g.N;
+        k_rank_keys<<<grid_for(total, 256), 256, 0, s>>>(fit, sa.pen, g.N, total, c.maximize, c.w_decay, rs->keys,
+                                                         rs->kin);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        e = launch_rank_sort(g, *rs, s);
+        if (e != hipSuccess) return e;
+        k_rank_scatter<<<grid_for(total, 256), 256, 0, s>>>(rs->kout, g.N, total, rank);
+        k_rank_stats<<<g.R, RANK_PAIRS * RANK_SLICES, 0, s>>>(fit, rs->keys, g.N, sa, rs->stats);
+        sa.gkeys = rs->keys;
+        sa.pre_rank = rank;
+        sa.stats = rs->stats;
+    }
     k_rank<<<grid, RANK_PAIRS * RANK_SLICES, lds, s>>>(fit, table, y, rank, wfold, best_okey, best_f, best_j,
                                                        gen_best, g.N, g.P, g.R, sa);
+    return hipGetLastError();
+}
+
+hipError_t launch_rank_offsets(const Geometry& g, int32_t* offsets, hipStream_t s)
+{
+    k_rank_offsets<<<grid_for((int64_t)g.R + 1, 256), 256, 0, s>>>(offsets, g.N, g.R);
     return hipGetLastError();
 }
 

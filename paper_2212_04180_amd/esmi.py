@@ -77,7 +77,7 @@ class _Config(ctypes.Structure):
         ("plan_eval_blocks", ctypes.c_int32),
         ("plan_tell_split", ctypes.c_int32),
         ("plan_run_path", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("plan_rank_path", ctypes.c_int32),
         ("reserved2", ctypes.c_int32),
     ]
 
@@ -121,11 +121,12 @@ class ESConfig:
     snes_temperature: float = 12.0
     elite_ratio: float = 0.5  # Sep-CMA-ES (App. B table)
     # launch plan, 0 = the library's choice (esmi.h): evaluate chunk length and
-    # gradient split change the summation order; run path 1 per-call, 2 fused
+    # gradient split change the summation order; run path 1 per-call, 2 fused;
+    # rank path 1 counted in LDS (N <= 16384), 2 radix-sorted (same ranks)
     plan_eval_blocks: int = 0
     plan_tell_split: int = 0
     plan_run_path: int = 0
-    reserved: int = 0
+    plan_rank_path: int = 0
     reserved2: int = 0
 
     def cstruct(self) -> _Config:

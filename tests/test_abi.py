@@ -72,3 +72,19 @@ def test_probe_library_exports_its_header():
     assert L.es_probe_threads() == 2048 * 256
     from paper_2212_04180_amd import esmi
     assert not hasattr(esmi.lib(), "es_probe_issue")
+
+
+def test_population_limits_are_validated_without_gpu_work():
+    """Up to 16384 members the ranks are counted in LDS; beyond, the sort-based
+    ranks take over, up to 2^24 members (rejected before any device call)."""
+    from paper_2212_04180_amd import esmi
+    L = esmi.lib()
+    h = ctypes.c_void_p()
+    for kw, msg in ((dict(popsize=(1 << 24) + 2), b"2^24"),
+                    (dict(popsize=16386, plan_rank_path=1), b"plan_rank_path 1"),
+                    (dict(popsize=64, plan_rank_path=3), b"plan_rank_path must be"),
+                    (dict(popsize=(1 << 20), num_runs=4096), b"2^31"),
+                    (dict(popsize=64, reserved2=1), b"reserved")):
+        cfg = esmi.ESConfig(num_dims=8, **kw).cstruct()
+        assert L.es_init(ctypes.byref(cfg), None, ctypes.byref(h)) == esmi.ES_ERR_ARG, kw
+        assert msg in L.es_last_error(None), (kw, L.es_last_error(None))

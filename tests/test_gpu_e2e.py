@@ -161,7 +161,7 @@ def test_error_paths():
     ok = dict(num_dims=8, popsize=4, problem=P.PROB_SPHERE)
     for bad in (dict(popsize=3), dict(popsize=0), dict(num_dims=0), dict(sigma=0.0), dict(sigma=float("nan")),
                 dict(num_runs=0), dict(beta1=1.0), dict(problem=99), dict(init_lo=1.0, init_hi=1.0),
-                dict(popsize=16386), dict(flags=8)):
+                dict(popsize=(1 << 24) + 2), dict(popsize=16386, plan_rank_path=1), dict(flags=8)):
         with pytest.raises(P.EsError) as ei:
             P.ES(P.ESConfig(**{**ok, **bad}))
         assert ei.value.status == P.esmi.ES_ERR_ARG

@@ -82,12 +82,14 @@ def test_largest_run_count_fused_and_per_call():
         assert np.all(np.abs(f[r] - fr) <= 1e-5 * np.abs(fr)), (r, f[r], fr)
 
 
+@pytest.mark.parametrize("N", [16384, 16386])
 @pytest.mark.parametrize("name", list(STRATS))
-def test_largest_population_matches_oracle(name):
-    """N = 16384, the largest accepted (the rank kernel's keys fill 64 KB of
-    LDS), D = 37 (ragged), two runs, stage by stage."""
+def test_largest_population_matches_oracle(name, N):
+    """N = 16384, the largest population whose ranks are counted in LDS (the
+    keys fill 64 KB), and N = 16386, the smallest that takes the sort-based
+    ranks; D = 37 (ragged), two runs, stage by stage."""
     P = _P()
     strategy, optimizer = STRATS[name]
-    cfg = _cfg(strategy, optimizer, 37, 16384, 2)
-    print("case", name, flush=True)
+    cfg = _cfg(strategy, optimizer, 37, N, 2)
+    print("case", name, N, flush=True)
     stagecheck.run(P, cfg, 2)

@@ -181,8 +181,9 @@ typedef struct es_config {
      *                     run's keys in LDS (popsize <= 16384), 2 = the
      *                     run's composite keys (key, member) are radix-sorted
      *                     and a member's position is its rank (also needs
-     *                     num_runs * popsize < 2^31); 0 = 1 up to popsize
-     *                     16384, 2 beyond                                  */
+     *                     num_runs * popsize < 2^31); 0 = the library's
+     *                     choice: 2 above popsize 16384, and above 10240
+     *                     when there is one run (where it is the faster)  */
     int32_t plan_eval_blocks;
     int32_t plan_tell_split;
     int32_t plan_run_path;

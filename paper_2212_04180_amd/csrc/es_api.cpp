@@ -163,7 +163,8 @@ const char* validate(const es_config& c)
     if (c.plan_rank_path < 0 || c.plan_rank_path > 2) return "plan_rank_path must be 0, 1 or 2";
     if (c.plan_rank_path == 1 && c.popsize > RANK_MAX_N)
         return "plan_rank_path 1 (ranks counted in LDS) takes popsize <= 16384";
-    if ((c.popsize > RANK_MAX_N || c.plan_rank_path == 2) && (int64_t)c.popsize * c.num_runs > INT32_MAX)
+    if ((c.popsize > RANK_MAX_N || c.plan_rank_path == 2 || (c.num_runs == 1 && c.popsize > RANK_SORT_FROM_N)) &&
+        (int64_t)c.popsize * c.num_runs > INT32_MAX)
         return "sort-based ranks need num_runs * popsize < 2^31";
     if (c.plan_eval_blocks < 0) return "plan_eval_blocks must be >= 0";
     if (c.plan_tell_split < 0 || c.plan_tell_split > 65535) return "plan_tell_split must be in [0, 65535]";
@@ -464,7 +465,8 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     if (e == hipSuccess && clipup) e = dalloc(&h->gbuf, rows);
     if (e == hipSuccess && clipup) e = dalloc(&h->gpart, tell_groups(g) * g.R);
     if (e == hipSuccess && clipup) e = dalloc(&h->vpart, tell_groups(g) * g.R);
-    h->rank_sort = g.N > RANK_MAX_N || cfg->plan_rank_path == 2;
+    h->rank_sort = g.N > RANK_MAX_N || cfg->plan_rank_path == 2 ||
+                   (cfg->plan_rank_path == 0 && g.R == 1 && g.N > RANK_SORT_FROM_N);
     if (e == hipSuccess && h->rank_sort) {
         const size_t n = (size_t)g.N * g.R;
         e = dalloc(&h->rs.kin, n);

@@ -1873,13 +1873,6 @@ TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit)
     TellPlan tp;
     tp.ps = tell_slices(g);
     if (fused_path) return tp;  // the fused loop sums all slices in one workgroup
-    // A run with few block groups: four lanes per block, so the groups of
-    // 16 blocks spread the run over four times the CUs (no split launch).
-    const int64_t groups64 = (g.nb + TELL_LANES - 1) / TELL_LANES * g.R;
-    if (groups64 < 64 && g.P >= 8 * tp.ps) {
-        tp.sub = 4;
-        return tp;
-    }
     // Few block groups (under four workgroups per CU) leave the CUs unevenly
     // loaded; then split each group's pairs over more, smaller workgroups
     // (four slices each; about 1024 workgroups, which all fit on the chip at
@@ -1887,9 +1880,14 @@ TellPlan tell_plan(const Geometry& g, bool fused_path, int64_t force_nsplit)
     const int64_t groups = (g.nb + TELL_LANES - 1) / TELL_LANES * g.R;
     int64_t nsplit = force_nsplit > 0 ? force_nsplit : groups >= 1024 ? 1 : (1024 + groups / 2) / groups;
     while (nsplit > 1 && g.P / (4 * nsplit) < 2 * TELL_GROUP) --nsplit;
-    if (nsplit <= 1 || nsplit > 65535) return tp;
-    tp.ps = 4;
-    tp.nsplit = (int32_t)nsplit;
+    if (nsplit > 1 && nsplit <= 65535) {
+        tp.ps = 4;
+        tp.nsplit = (int32_t)nsplit;
+        return tp;
+    }
+    // Too few pairs to split and few block groups: four lanes per block, so
+    // the groups of 16 blocks spread the run over four times the CUs.
+    if (groups < 64 && g.P >= 8 * tp.ps) tp.sub = 4;
     return tp;
 }
 

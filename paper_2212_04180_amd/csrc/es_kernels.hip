@@ -599,8 +599,10 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
     // the count of slice s (the sort-based ranks arrive whole, in slice 0)
     const int32_t kb = pre ? 0 : (int32_t)(((int64_t)N * s) / RANK_SLICES);
     const int32_t ke = pre ? 0 : (int32_t)(((int64_t)N * (s + 1)) / RANK_SLICES);
-    // rank_j = #{k : key_k < key_j} + #{k < j : key_k == key_j}
+    // rank_j = #{k : key_k < key_j} + #{k < j : key_k == key_j}, i.e. the
+    // number of composites (key_k, k) below (key_j, j): one 64-bit compare
     int32_t c1 = 0, c2 = 0;
+    const uint64_t cj1 = ((uint64_t)K1 << 32) | (uint32_t)j1, cj2 = ((uint64_t)K2 << 32) | (uint32_t)j2;
     int32_t k = kb;
     for (; k + 4 <= ke; k += 4) {
         uint32_t kk[4];
@@ -608,14 +610,15 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
         for (int u = 0; u < 4; ++u) kk[u] = keys[k + u];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            c1 += (kk[u] < K1) | ((kk[u] == K1) & (k + u < j1));
-            c2 += (kk[u] < K2) | ((kk[u] == K2) & (k + u < j2));
+            const uint64_t ck = ((uint64_t)kk[u] << 32) | (uint32_t)(k + u);
+            c1 += ck < cj1;
+            c2 += ck < cj2;
         }
     }
     for (; k < ke; ++k) {
-        const uint32_t kk = keys[k];
-        c1 += (kk < K1) | ((kk == K1) & (k < j1));
-        c2 += (kk < K2) | ((kk == K2) & (k < j2));
+        const uint64_t ck = ((uint64_t)keys[k] << 32) | (uint32_t)k;
+        c1 += ck < cj1;
+        c2 += ck < cj2;
     }
     if (pre && s == 0) {
         c1 = sa.pre_rank[(int64_t)r * N + j1];
@@ -1476,6 +1479,9 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
                 if (p < a.P) {
                     j = p + mem * a.P;
                     K = keys[j];
+                    // member k sorts before j when (key_k, k) < (K, j): one
+                    // 64-bit compare per key
+                    const uint64_t cj = ((uint64_t)K << 32) | (uint32_t)j;
                     const int32_t s0 = q * cs, s1 = s0 + cs < a.N ? s0 + cs : a.N;
                     int32_t k = s0;
                     for (; k + 8 <= s1; k += 8) {
@@ -1484,21 +1490,14 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
                         for (int u = 0; u < 2; ++u) q4[u] = *reinterpret_cast<const uint4*>(keys + k + 4 * u);
 #pragma unroll
                         for (int u = 0; u < 2; ++u) {
-                            const int32_t kk = k + 4 * u;
-                            rk += (q4[u].x < K) | ((q4[u].x == K) & (kk < j));
-                            rk += (q4[u].y < K) | ((q4[u].y == K) & (kk + 1 < j));
-                            rk += (q4[u].z < K) | ((q4[u].z == K) & (kk + 2 < j));
-                            rk += (q4[u].w < K) | ((q4[u].w == K) & (kk + 3 < j));
+                            const uint32_t kk = (uint32_t)(k + 4 * u);
+                            rk += ((((uint64_t)q4[u].x) << 32) | kk) < cj;
+                            rk += ((((uint64_t)q4[u].y) << 32) | (kk + 1)) < cj;
+                            rk += ((((uint64_t)q4[u].z) << 32) | (kk + 2)) < cj;
+                            rk += ((((uint64_t)q4[u].w) << 32) | (kk + 3)) < cj;
                         }
                     }
-                    for (; k + 4 <= s1; k += 4) {
-                        const uint4 q4 = *reinterpret_cast<const uint4*>(keys + k);
-                        rk += (q4.x < K) | ((q4.x == K) & (k < j));
-                        rk += (q4.y < K) | ((q4.y == K) & (k + 1 < j));
-                        rk += (q4.z < K) | ((q4.z == K) & (k + 2 < j));
-                        rk += (q4.w < K) | ((q4.w == K) & (k + 3 < j));
-                    }
-                    for (; k < s1; ++k) rk += (keys[k] < K) | ((keys[k] == K) & (k < j));
+                    for (; k < s1; ++k) rk += ((((uint64_t)keys[k]) << 32) | (uint32_t)k) < cj;
                 }
                 // every lane of the wave takes part in the exchanges (lane
                 // xor 1 and xor 2 within the quad by DPP, xor 4 by swizzle)

@@ -1364,12 +1364,12 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
     const int64_t goff = (int64_t)r * Dp;
     float sigma = a.hp[r], lr = a.hp[a.R + r];
-    for (int64_t i = threadIdx.x; i < Dp; i += blockDim.x) {
+    for (int64_t i = threadIdx.x; i < Dp; i += FUSED_WG) {
         ms[i] = a.m[goff + i];
         m1s[i] = a.m1[goff + i];
         vs[i] = a.v[goff + i];
     }
-    for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) tab[j] = a.table[j];
+    for (int32_t j = threadIdx.x; j < a.N; j += FUSED_WG) tab[j] = a.table[j];
     // pair bounds of the gradient's slices: slice s takes pairs [P s / ps, P (s+1) / ps)
     __shared__ int32_t sl_bound[TELL_MAX_PS + 1];
     if (threadIdx.x <= (uint32_t)a.ps) sl_bound[threadIdx.x] = (int32_t)(((int64_t)a.P * threadIdx.x) / a.ps);
@@ -1393,6 +1393,11 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
 
     for (int32_t it = 0; it < a.T; ++it) {
         const uint32_t t = a.t0 + (uint32_t)it;
+        // 1 / (N sigma) of this generation, used by the update at its end: the
+        // empty asm keeps the fp64 division here, where its latency hides
+        // under the evaluate phase, instead of on the update's critical path
+        double inv_ns = 1.0 / (2.0 * (double)a.P * (double)sigma);
+        asm volatile("" : "+v"(inv_ns));
         // this generation's Adam constants, from the kernel arguments: the
         // bias corrections are read through the kernarg segment pointer (the
         // launch's only explicit argument starts at its offset 0), because a
@@ -1437,7 +1442,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         __builtin_amdgcn_s_setprio(FUSED_PRIO);
         // fitness in the reduce kernel's order, and order keys
         const int nq = a.nchunks < RED_SLICES ? (int)a.nchunks : RED_SLICES;  // slices beyond add 0
-        for (int32_t j = threadIdx.x; j < a.N; j += blockDim.x) {
+        for (int32_t j = threadIdx.x; j < a.N; j += FUSED_WG) {
             double tot = a.add;
             if (a.nchunks <= RED_SLICES) {
                 // one chunk per slice: four loads in flight ahead of the sum
@@ -1541,8 +1546,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         __syncthreads();
         __builtin_amdgcn_s_setprio(FUSED_PRIO);
         const int32_t jb = best_j;
-        const double inv_ns = 1.0 / (2.0 * (double)a.P * (double)sigma);  // 1 / (N sigma)
-        for (int64_t i = threadIdx.x; i < 4 * a.nb; i += blockDim.x) {
+        for (int64_t i = threadIdx.x; i < 4 * a.nb; i += FUSED_WG) {
             // one dim per lane: the slices in order, then Adam
             // four slices' loads in flight ahead of the ordered sum
             double s64 = red[i];
@@ -1576,7 +1580,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
     if (best_jj >= 0) {
         const int32_t pbst = best_jj < a.P ? best_jj : best_jj - a.P;
         const float sg = best_jj < a.P ? best_sg : -best_sg;
-        for (int64_t b = threadIdx.x; b < a.nb; b += blockDim.x) {
+        for (int64_t b = threadIdx.x; b < a.nb; b += FUSED_WG) {
             float e[4];
             box_muller4(philox4x32_10<LANES_BLOCK_AND_ROW>(k0, k1, (uint32_t)b, (uint32_t)pbst, best_t, DOM_NOISE), e);
 #pragma unroll
@@ -1592,7 +1596,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         a.best_okey[r] = best_k;
         a.best_f[r] = best_fv;
     }
-    for (int64_t i = threadIdx.x; i < Dp; i += blockDim.x) {
+    for (int64_t i = threadIdx.x; i < Dp; i += FUSED_WG) {
         a.m[goff + i] = ms[i];
         a.m1[goff + i] = m1s[i];
         a.v[goff + i] = vs[i];

@@ -1449,7 +1449,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
                 for (int q0 = 0; q0 < nq; q0 += 4) {
                     float pv[4];
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) pv[u] = q0 + u < nq ? part[(q0 + u) * a.N + j] : 0.f;
+                    for (int u = 0; u < 4; ++u) pv[u] = part[(q0 + u < nq ? q0 + u : nq - 1) * a.N + j];
 #pragma unroll
                     for (int u = 0; u < 4; ++u)
                         if (q0 + u < nq) {
@@ -1553,7 +1553,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             for (int q0 = 1; q0 < a.ps; q0 += 4) {
                 double rv[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) rv[u] = q0 + u < a.ps ? red[(q0 + u) * 4 * nb32 + i] : 0.0;
+                for (int u = 0; u < 4; ++u) rv[u] = red[(q0 + u < a.ps ? q0 + u : a.ps - 1) * 4 * nb32 + i];
 #pragma unroll
                 for (int u = 0; u < 4; ++u)
                     if (q0 + u < a.ps) s64 += rv[u];

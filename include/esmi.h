@@ -182,8 +182,9 @@ typedef struct es_config {
      *                     run's composite keys (key, member) are radix-sorted
      *                     and a member's position is its rank (also needs
      *                     num_runs * popsize < 2^31); 0 = the library's
-     *                     choice: 2 above popsize 16384, and above 10240
-     *                     when there is one run (where it is the faster)  */
+     *                     choice: 2 above popsize 16384, and where
+     *                     num_runs * popsize^2 > 1.2e8 (where it is the
+     *                     faster), else 1                                 */
     int32_t plan_eval_blocks;
     int32_t plan_tell_split;
     int32_t plan_run_path;

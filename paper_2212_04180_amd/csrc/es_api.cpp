@@ -163,8 +163,9 @@ const char* validate(const es_config& c)
     if (c.plan_rank_path < 0 || c.plan_rank_path > 2) return "plan_rank_path must be 0, 1 or 2";
     if (c.plan_rank_path == 1 && c.popsize > RANK_MAX_N)
         return "plan_rank_path 1 (ranks counted in LDS) takes popsize <= 16384";
-    if ((c.popsize > RANK_MAX_N || c.plan_rank_path == 2 || (c.num_runs == 1 && c.popsize > RANK_SORT_FROM_N)) &&
-        (int64_t)c.popsize * c.num_runs > INT32_MAX)
+    // (the library's own choice of the sort never needs more: it picks the
+    // sort below RANK_MAX_N members only, where R N < 65536 * 16384)
+    if ((c.popsize > RANK_MAX_N || c.plan_rank_path == 2) && (int64_t)c.popsize * c.num_runs > INT32_MAX)
         return "sort-based ranks need num_runs * popsize < 2^31";
     if (c.plan_eval_blocks < 0) return "plan_eval_blocks must be >= 0";
     if (c.plan_tell_split < 0 || c.plan_tell_split > 65535) return "plan_tell_split must be in [0, 65535]";
@@ -277,7 +278,7 @@ void free_all(es_handle* h)
                     h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->mlp_scratch,
                     h->tell_part, h->hp[0], h->hp[1], h->pen, h->bfold, h->sig, h->vel, h->gbuf,
                     h->gpart, h->vpart, h->elite, h->cw, h->cmaC, h->zw, h->qd,
-                    h->rs.kin, h->rs.kout, h->rs.keys, h->rs.offsets, h->rs.stats, h->rs.temp};
+                    h->rs.kin, h->rs.kout, h->rs.keys, h->rs.stats, h->rs.temp};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
 }
@@ -466,18 +467,17 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     if (e == hipSuccess && clipup) e = dalloc(&h->gpart, tell_groups(g) * g.R);
     if (e == hipSuccess && clipup) e = dalloc(&h->vpart, tell_groups(g) * g.R);
     h->rank_sort = g.N > RANK_MAX_N || cfg->plan_rank_path == 2 ||
-                   (cfg->plan_rank_path == 0 && g.R == 1 && g.N > RANK_SORT_FROM_N);
+                   (cfg->plan_rank_path == 0 && (double)g.R * g.N * g.N > RANK_SORT_FROM_WORK);
     if (e == hipSuccess && h->rank_sort) {
         const size_t n = (size_t)g.N * g.R;
         e = dalloc(&h->rs.kin, n);
         if (e == hipSuccess) e = dalloc(&h->rs.kout, n);
         if (e == hipSuccess) e = dalloc(&h->rs.keys, n);
-        if (e == hipSuccess) e = dalloc(&h->rs.offsets, (size_t)g.R + 1);
         if (e == hipSuccess) e = dalloc(&h->rs.stats, 4 * (size_t)g.R);
+        rank_sort_bits(g, &h->rs.bn, &h->rs.br);
         h->rs.temp_bytes = rank_sort_temp_bytes(g);
         if (e == hipSuccess && h->rs.temp_bytes == 0) e = hipErrorInvalidValue;
         if (e == hipSuccess) e = dalloc(reinterpret_cast<char**>(&h->rs.temp), h->rs.temp_bytes);
-        if (e == hipSuccess) e = launch_rank_offsets(g, h->rs.offsets, h->stream);
     }
     if (e != hipSuccess) {
         free_all(h);

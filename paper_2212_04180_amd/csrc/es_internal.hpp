@@ -63,20 +63,23 @@ hipError_t launch_eval_bbob(const Geometry& g, const es_config& c, const EvalPla
                             const float* m, const float* pdata, float* partial, float* fit,
                             const float* hp, const float* svec, double div, hipStream_t s,
                             hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
-// Sort-based ranks (populations beyond RANK_MAX_N, or on request): every
-// run's composite keys (order key << 32 | member) sorted ascending.
+// Sort-based ranks (populations beyond RANK_MAX_N, or on request): the
+// composite keys run << (32 + bn) | order key << bn | member of all runs,
+// sorted ascending over their low 32 + bn + br bits in one device-wide sort
+// (bn, br: the bits of the largest member and run index; with R N < 2^31,
+// 2^(bn + br) < 4 R N, so the key fits 64 bits).
 struct RankSortBuffers {
     uint64_t* kin;     // [R][N] composite keys
-    uint64_t* kout;    // [R][N] sorted per run
+    uint64_t* kout;    // [R][N] sorted (runs in order)
     uint32_t* keys;    // [R][N] shaped order keys
-    int32_t* offsets;  // [R + 1] run starts r N
     double* stats;     // [R][4] per-run statistics of the shaped keys
     void* temp;        // sort scratch
     size_t temp_bytes;
+    int32_t bn, br;    // member and run index bits
 };
+void rank_sort_bits(const Geometry& g, int32_t* bn, int32_t* br);
 size_t rank_sort_temp_bytes(const Geometry& g);                                  // 0 on failure
 hipError_t launch_rank_sort(const Geometry& g, const RankSortBuffers& rs, hipStream_t s);  // kin -> kout
-hipError_t launch_rank_offsets(const Geometry& g, int32_t* offsets, hipStream_t s);
 // table: the shaping table indexed by rank (centered ranks, or SNES
 // utilities by rank), ybar_table its mean; bfold: PGPE / SNES second weight;
 // rs: sort-based ranks (null: counted in LDS, N <= RANK_MAX_N).
@@ -184,9 +187,11 @@ hipError_t noalloc_scratch(float** out);
 // sort-based ranks, up to POP_MAX_N.
 constexpr int32_t RANK_MAX_N = 16384;
 constexpr int32_t POP_MAX_N = 1 << 24;
-// With one run the sort-based ranks are the faster above this population
-// (measured: 10240 counted 58 us per generation against 59 sorted, 11264 66
-// against 64); with several runs the count is kept up to RANK_MAX_N.
-constexpr int32_t RANK_SORT_FROM_N = 10240;
+// The count costs R N^2 compares, the sort about R N log N plus a fixed
+// part: the sort is the faster above about this R N^2 (measured, R N^2 in
+// units of 1e8: one run 1.05 counted 58 us per generation against 59 sorted,
+// 1.27 66 against 64; 16 runs 0.67 35 against 63, 2.7 85 against 73; 64 runs
+// 0.67 33 against 72, 2.7 93 against 98).
+constexpr double RANK_SORT_FROM_WORK = 1.2e8;
 
 }  // namespace esmi

@@ -683,33 +683,33 @@ __global__ __launch_bounds__(RANK_PAIRS * RANK_SLICES) void k_rank(
 }
 
 // Sort-based ranks, for populations whose keys do not fit a workgroup's LDS.
-// The composite key (order key << 32 | member) of every member sorts
-// ascending by key and then by index, so a member's position in its run's
-// sorted sequence is the count the rank kernel makes: the number of keys
-// below its own plus the equal keys of lower index.
+// Every member's composite key (run << (32 + bn) | order key << bn | member,
+// bn = RankSortBuffers::bn) sorts ascending by run, then by key, then by
+// index, so the runs come out in order, run r in [r N, (r + 1) N), and a
+// member's position there is the count the rank kernel makes: the number of
+// keys below its own plus the equal keys of lower index.
 __global__ void k_rank_keys(const float* __restrict__ fit, const float* __restrict__ pen, int32_t N, int64_t total,
-                            int32_t maximize, float w_decay, uint32_t* __restrict__ keys, uint64_t* __restrict__ comp)
+                            int32_t maximize, float w_decay, int32_t bn, uint32_t* __restrict__ keys,
+                            uint64_t* __restrict__ comp)
 {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
         const uint32_t K = order_key(shaped_key(fit[i], pen ? pen[i] : 0.0f, maximize, w_decay), 0);
         keys[i] = K;
-        comp[i] = ((uint64_t)K << 32) | (uint32_t)(i % N);
+        const int64_t r = i / N;
+        comp[i] = ((uint64_t)r << (32 + bn)) | ((uint64_t)K << bn) | (uint64_t)(i - r * N);
     }
 }
 
-// rank[r][member] = position of the member's composite key in run r's sorted keys
-__global__ void k_rank_scatter(const uint64_t* __restrict__ sorted, int32_t N, int64_t total, int32_t* __restrict__ rank)
+// rank[r][member] = position of the member's composite key within run r's
+// slice of the sorted keys
+__global__ void k_rank_scatter(const uint64_t* __restrict__ sorted, int32_t N, int64_t total, int32_t bn,
+                               int32_t* __restrict__ rank)
 {
+    const uint64_t mask = ((uint64_t)1 << bn) - 1;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
         const int64_t r = i / N;
-        rank[r * N + (int64_t)(uint32_t)sorted[i]] = (int32_t)(i - r * N);
+        rank[r * N + (int64_t)(sorted[i] & mask)] = (int32_t)(i - r * N);
     }
-}
-
-// Segment starts r N of the sort, r = 0 .. R.
-__global__ void k_rank_offsets(int32_t* __restrict__ off, int32_t N, int32_t R)
-{
-    for (int32_t r = blockIdx.x * blockDim.x + threadIdx.x; r <= R; r += gridDim.x * blockDim.x) off[r] = r * N;
 }
 
 // One workgroup per run: the statistics every rank workgroup of the run
@@ -1782,13 +1782,13 @@ hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, 
     if (rs) {
         // keys, sort, ranks and the per-run statistics ahead of the rank kernel
         const int64_t total = (int64_t)g.R * g.N;
-        k_rank_keys<<<grid_for(total, 256), 256, 0, s>>>(fit, sa.pen, g.N, total, c.maximize, c.w_decay, rs->keys,
-                                                         rs->kin);
+        k_rank_keys<<<grid_for(total, 256), 256, 0, s>>>(fit, sa.pen, g.N, total, c.maximize, c.w_decay, rs->bn,
+                                                         rs->keys, rs->kin);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         e = launch_rank_sort(g, *rs, s);
         if (e != hipSuccess) return e;
-        k_rank_scatter<<<grid_for(total, 256), 256, 0, s>>>(rs->kout, g.N, total, rank);
+        k_rank_scatter<<<grid_for(total, 256), 256, 0, s>>>(rs->kout, g.N, total, rs->bn, rank);
         k_rank_stats<<<g.R, RANK_PAIRS * RANK_SLICES, 0, s>>>(fit, rs->keys, g.N, sa, rs->stats);
         sa.gkeys = rs->keys;
         sa.pre_rank = rank;
@@ -1796,12 +1796,6 @@ hipError_t launch_rank(const Geometry& g, const es_config& c, const float* fit, 
     }
     k_rank<<<grid, RANK_PAIRS * RANK_SLICES, lds, s>>>(fit, table, y, rank, wfold, best_okey, best_f, best_j,
                                                        gen_best, g.N, g.P, g.R, sa);
-    return hipGetLastError();
-}
-
-hipError_t launch_rank_offsets(const Geometry& g, int32_t* offsets, hipStream_t s)
-{
-    k_rank_offsets<<<grid_for((int64_t)g.R + 1, 256), 256, 0, s>>>(offsets, g.N, g.R);
     return hipGetLastError();
 }
 

@@ -9,8 +9,9 @@ here (marked gpu):
     shaping give the same bits on either path (ranks, weights, state,
     best-so-far), including z-scores, weight decay and PGPE's mean of y,
     which the sort path computes once per run instead of per workgroup;
-  - 2^17 members end to end against numpy's stable argsort of the same keys
-    (the oracle's quadratic count is too slow at that size).
+  - 2^17 members end to end, and 2^24 (the largest accepted) for one
+    generation, against numpy's stable argsort of the same keys (the
+    oracle's quadratic count is too slow at those sizes).
 """
 import numpy as np
 import pytest
@@ -136,3 +137,21 @@ def test_large_population_end_to_end():
         np.testing.assert_array_equal(y, _centered(ref, N))
     assert es.get_state()["t"] == 2
     print(f"N={N}: two generations, ranks equal to the stable argsort")
+
+
+def test_largest_population():
+    """N = 2^24, the largest accepted population (D = 4, one generation):
+    ranks and weights against a stable argsort of the GPU fitness."""
+    P = _P()
+    N = 1 << 24
+    es = P.ES(_cfg(popsize=N, num_dims=4, problem=P.PROB_SPHERE, seed=9))
+    es.ask()
+    f = _np(es.eval())
+    es.tell(torch.tensor(f, device="cuda"))
+    y, rk = es.shaped()
+    y, rk = _np(y)[0], _np(rk)[0]
+    ref = _argsort_ranks(f[0], 0)
+    np.testing.assert_array_equal(rk, ref)
+    np.testing.assert_array_equal(y, _centered(ref, N))
+    assert np.all(np.isfinite(_np(es.get_state()["m"])))
+    print(f"N={N}: ranks equal to the stable argsort")

@@ -116,7 +116,7 @@ typedef enum { ES_STRAT_OPENAI_ES = 0, ES_STRAT_PGPE = 1, ES_STRAT_SNES = 2, ES_
 typedef enum { ES_OPT_ADAM = 0, ES_OPT_CLIPUP = 1 } es_optimizer;
 
 /* Flags (es_config.flags). */
-#define ES_FLAG_KEEP_GRAD 1u /* es_tell also stores g [R][D] for es_get_grad */
+#define ES_FLAG_KEEP_GRAD 1u /* es_tell and es_run also store g [R][D] for es_get_grad */
 
 /*
  * Strategy parameters (the default_params of Listing 1; App. B, OpenAI-ES
@@ -163,7 +163,7 @@ typedef struct es_config {
      * is what every result in the documentation refers to).  The first two
      * set how the fp32 partial sums are grouped, so they change the
      * summation order and therefore the low bits of the fitness and of the
-     * gradient; the third only picks the code path of es_run.
+     * gradient; plan_run_path only picks the code path of es_run.
      *   plan_eval_blocks  Philox blocks (4 dims) per evaluate chunk, >= 0;
      *                     each chunk's per-member partial is one fp32 sum
      *   plan_tell_split   gradient workgroups per group of 64 Philox blocks
@@ -175,7 +175,22 @@ typedef struct es_config {
      *                     fused loop wherever it supports the config (in
      *                     the fused loop's summation order, which equals the
      *                     per-call kernels' only where the library itself
-     *                     would choose the fused loop)
+     *                     would choose the fused loop), 3 = the grid loop
+     *                     wherever it supports the config (always in the
+     *                     per-call kernels' order, so the same bits); 0 =
+     *                     the fused loop for small runs or many runs, the
+     *                     grid loop for a few runs of up to 131072 Philox
+     *                     pair-blocks in all (num_runs * popsize/2 *
+     *                     ceil(D/4)), else the per-call kernels.  Both loops
+     *                     run OpenAI-ES with Adam on the benchmark problems,
+     *                     centered-rank or raw shaping, no weight decay; the
+     *                     grid loop also needs popsize <= 8192
+     *   plan_grid_workgroups  workgroups per run of the grid loop, 0..16
+     *                     (0: about one per 2048 pair-blocks of a run),
+     *                     lowered to what the evaluate chunks allow (each
+     *                     workgroup owns whole chunk slices of the fitness
+     *                     reduction: at most min(chunks, 16), beyond 16
+     *                     chunks a divisor of 16); no effect on the results
      *   plan_rank_path    how the ranks are found (same ranks, same bits
      *                     either way): 1 = each workgroup counts against the
      *                     run's keys in LDS (popsize <= 16384), 2 = the
@@ -189,7 +204,7 @@ typedef struct es_config {
     int32_t plan_tell_split;
     int32_t plan_run_path;
     int32_t plan_rank_path;
-    int32_t reserved2;  /* must be 0                                         */
+    int32_t plan_grid_workgroups;
 } es_config;
 
 typedef struct es_handle es_handle;
@@ -262,7 +277,10 @@ es_status es_tell(es_handle* h, const float* fitness);
 
 /* T fused generations (the scanned loop of Listing 2) with the built-in
  * problem.  log: NULL or device [T][R] receiving each generation's best
- * fitness (the member of rank 0).  Requires no open ask. */
+ * fitness (the member of rank 0).  Requires no open ask.  The code path
+ * (per-call kernels, the fused loop of one workgroup per run, or the grid
+ * loop of a cooperative launch per up to 256 generations) follows
+ * cfg.plan_run_path. */
 es_status es_run(es_handle* h, int32_t T, float* log);
 
 /* Copy out / replace the search state (the state fields of Listing 1; the
@@ -332,11 +350,21 @@ es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes);
 
 /* Runtime plumbing below, not operations of the paper. */
 
-/* Wait for all work enqueued by this handle (synchronous). */
+/* Wait for all work enqueued by this handle (synchronous).  Not defined by
+ * the paper.  Also reports ES_ERR_HIP if a grid-loop launch of es_run ended
+ * early because a barrier wait gave up (its workgroups are resident together
+ * under a cooperative launch, so only a library fault can cause that; the
+ * state is then not valid). */
 es_status es_sync(es_handle* h);
 
 /* Current generation counter t (host value; no device work). */
 int64_t es_generation(const es_handle* h);
+
+/* The code path es_run takes for this handle (host value; no device work;
+ * not defined by the paper): 1 the per-call kernels, 2 the fused loop (one
+ * workgroup per run), 3 the grid loop (a cooperative launch of several
+ * workgroups per run); 0 for a NULL handle.  See cfg.plan_run_path. */
+int32_t es_run_path(const es_handle* h);
 
 /* Message of the last failed call on h ("" if none); with h == NULL, the
  * message of the last failed es_init on this thread.  Never NULL. */

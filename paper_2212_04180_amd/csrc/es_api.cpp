@@ -87,7 +87,11 @@ struct es_handle {
     float* pdata = nullptr;  // [Dp] shift vector or teacher
     void* mlp_scratch = nullptr;  // MLP inputs and teacher outputs of the current generation
     int64_t teacher_t = -1;       // generation whose inputs and teacher outputs are in mlp_scratch
-    int run_path = 0;  // 0 auto, 1 per-call kernels, 2 fused loop
+    int run_path = 0;  // 0 auto, 1 per-call kernels, 2 fused loop, 3 grid loop
+    int32_t grid_g = 0;             // workgroups per run of the grid loop (0: the grid loop does not apply)
+    uint32_t* grid_sync = nullptr;  // barrier counters, update flags, then the grid loop's error flag
+    double* grid_accx = nullptr;    // the grid loop's slice sums
+    uint64_t* grid_halo = nullptr;  // the grid loop's chunk-boundary words (Rosenbrock)
     // sort-based ranks (populations beyond RANK_MAX_N, or plan_rank_path 2)
     bool rank_sort = false;
     RankSortBuffers rs{};
@@ -159,7 +163,8 @@ const char* validate(const es_config& c)
     if (c.strategy < ES_STRAT_OPENAI_ES || c.strategy > ES_STRAT_SEP_CMA) return "unknown strategy";
     if (c.strategy == ES_STRAT_SEP_CMA && !(c.elite_ratio > 0.0f && c.elite_ratio <= 1.0f))
         return "elite_ratio must be in (0, 1]";
-    if (c.reserved2 != 0) return "reserved fields must be 0";
+    if (c.plan_grid_workgroups < 0 || c.plan_grid_workgroups > GRID_MAX_G)
+        return "plan_grid_workgroups must be in [0, 16]";
     if (c.plan_rank_path < 0 || c.plan_rank_path > 2) return "plan_rank_path must be 0, 1 or 2";
     if (c.plan_rank_path == 1 && c.popsize > RANK_MAX_N)
         return "plan_rank_path 1 (ranks counted in LDS) takes popsize <= 16384";
@@ -169,7 +174,7 @@ const char* validate(const es_config& c)
         return "sort-based ranks need num_runs * popsize < 2^31";
     if (c.plan_eval_blocks < 0) return "plan_eval_blocks must be >= 0";
     if (c.plan_tell_split < 0 || c.plan_tell_split > 65535) return "plan_tell_split must be in [0, 65535]";
-    if (c.plan_run_path < 0 || c.plan_run_path > 2) return "plan_run_path must be 0, 1 or 2";
+    if (c.plan_run_path < 0 || c.plan_run_path > 3) return "plan_run_path must be 0, 1, 2 or 3";
     if (c.strategy == ES_STRAT_SEP_CMA && c.problem == ES_PROB_MLP)
         return "Sep-CMA-ES takes the benchmark problems or the caller's fitness (the MLP evaluate kernel samples "
                "antithetic pairs)";
@@ -272,13 +277,37 @@ bool fused_by_default(const Geometry& g, const EvalPlan& e, const es_config& c)
     return fused_supported(g, e, c) && ((int64_t)g.P * g.nb <= 8192 || g.R >= 128);
 }
 
+// Otherwise the grid loop, where the launches of the per-call kernels (about
+// 2.5 us each, four per generation) would cost more than the work of a few
+// runs on a few dozen CUs.
+bool grid_by_default(const es_handle* h)
+{
+    const Geometry& g = h->g;
+    return h->grid_g > 0 && !fused_by_default(g, h->plan, h->cfg) &&
+           (int64_t)g.R * g.P * g.nb <= GRID_DEFAULT_WORK && (int64_t)g.R * h->grid_g <= 256;
+}
+
+// The path es_run takes: plan_run_path forces one (1 per-call kernels, 2
+// fused loop, 3 grid loop, each where it supports the config; a forced fused
+// loop on a geometry es_run would not fuse sums in its own order), 0 leaves
+// it to the rules above.
+int run_path_of(const es_handle* h)
+{
+    switch (h->run_path) {
+    case 1: return 1;
+    case 2: return fused_supported(h->g, h->plan, h->cfg) ? 2 : 1;
+    case 3: return h->grid_g > 0 ? 3 : 1;
+    default: return fused_by_default(h->g, h->plan, h->cfg) ? 2 : grid_by_default(h) ? 3 : 1;
+    }
+}
+
 void free_all(es_handle* h)
 {
     void* ptrs[] = {h->m, h->m1, h->v, h->best_x, h->grad, h->best_okey, h->best_f, h->best_j, h->table,
                     h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->mlp_scratch,
                     h->tell_part, h->hp[0], h->hp[1], h->pen, h->bfold, h->sig, h->vel, h->gbuf,
                     h->gpart, h->vpart, h->elite, h->cw, h->cmaC, h->zw, h->qd,
-                    h->rs.kin, h->rs.kout, h->rs.keys, h->rs.stats, h->rs.temp};
+                    h->rs.kin, h->rs.kout, h->rs.keys, h->rs.stats, h->rs.temp, h->grid_sync, h->grid_accx, h->grid_halo};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
 }
@@ -401,6 +430,8 @@ const char* es_last_error(const es_handle* h) { return h ? h->err : g_init_err; 
 
 int64_t es_generation(const es_handle* h) { return h ? h->t : -1; }
 
+int32_t es_run_path(const es_handle* h) { return h ? run_path_of(h) : 0; }
+
 es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
 {
     if (!cfg || !out) return init_fail(ES_ERR_ARG, "null argument");
@@ -422,6 +453,13 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     // gradient kernel sums in the fused loop's order, so both give the same bits
     h->tell = tell_plan(g, fused_by_default(g, h->plan, *cfg), cfg->plan_tell_split);
     h->run_path = cfg->plan_run_path;
+    {
+        const int32_t G = grid_workgroups(g, h->plan, cfg->plan_grid_workgroups);
+        int64_t cap = 0;
+        if (grid_supported(g, h->plan, h->tell, *cfg, G) && grid_max_resident(&cap) == hipSuccess &&
+            (int64_t)G * g.R <= cap)
+            h->grid_g = G;
+    }
     hipError_t e = hipGetDevice(&h->device);
     const size_t rows = (size_t)g.Dp * g.R;
     if (e == hipSuccess) e = dalloc(&h->m, rows);
@@ -448,6 +486,16 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
         e = dalloc(reinterpret_cast<char**>(&h->mlp_scratch), mlp_scratch_bytes());
     if (e == hipSuccess && h->tell.nsplit > 1)
         e = dalloc(&h->tell_part, tell_part_elems(g, h->tell, cfg->strategy));
+    if (e == hipSuccess && h->grid_g > 0) {
+        const size_t words = grid_sync_words(g);
+        e = dalloc(&h->grid_sync, words);
+        if (e == hipSuccess) e = hipMemsetAsync(h->grid_sync, 0, sizeof(uint32_t) * words, h->stream);
+        if (e == hipSuccess) e = dalloc(&h->grid_accx, grid_accx_elems(g));
+        // the words' tags are t + 1 >= 1 once written: 0 matches no generation
+        const size_t hw = (size_t)g.R * h->plan.nchunks;
+        if (e == hipSuccess) e = dalloc(&h->grid_halo, hw);
+        if (e == hipSuccess) e = hipMemsetAsync(h->grid_halo, 0, sizeof(uint64_t) * hw, h->stream);
+    }
     const bool pgpe_snes = cfg->strategy == ES_STRAT_PGPE || cfg->strategy == ES_STRAT_SNES;
     const bool cma = cfg->strategy == ES_STRAT_SEP_CMA;
     if (e == hipSuccess && pgpe_snes) e = dalloc(&h->bfold, (size_t)g.P * g.R);
@@ -618,11 +666,8 @@ es_status es_run(es_handle* h, int32_t T, float* log)
     if (h->cfg.problem == ES_PROB_NONE) return fail(h, ES_ERR_UNSUPPORTED, "es_run needs a built-in problem");
     if (T == 0) return ES_OK;
     if (h->t + T > 0xFFFFFFFFll) return fail(h, ES_ERR_ARG, "es_run: generation counter would exceed 2^32");
-    const bool fused_ok = fused_supported(h->g, h->plan, h->cfg);
-    // plan_run_path forces a path (1 per-call kernels, 2 fused loop); a forced
-    // fused loop on a geometry es_run would not fuse sums in its own order
-    const bool fused = h->run_path == 2 ? fused_ok : h->run_path == 1 ? false : fused_by_default(h->g, h->plan, h->cfg);
-    if (fused) {
+    const int path = run_path_of(h);
+    if (path != 1) {
         // launches of up to FUSED_MAX_T generations, each with its generations'
         // Adam bias corrections in the kernel arguments
         float bcorr[FUSED_MAX_T][2];
@@ -633,10 +678,20 @@ es_status es_run(es_handle* h, int32_t T, float* log)
                 bcorr[i][0] = a.bc1;
                 bcorr[i][1] = a.bc2;
             }
-            ES_HIP(h, launch_run_fused(h->g, h->cfg, h->plan, (uint32_t)h->t, Tc, adam_consts(h->cfg, h->t), bcorr,
-                                       h->m, h->m1, h->v, h->best_x, h->best_okey, h->best_f, h->pdata, h->table,
-                                       log ? log + (int64_t)done * h->g.R : nullptr, h->hp[h->hp_cur], h->stream),
-                   "fused generation loop");
+            float* lg = log ? log + (int64_t)done * h->g.R : nullptr;
+            if (path == 2)
+                ES_HIP(h, launch_run_fused(h->g, h->cfg, h->plan, (uint32_t)h->t, Tc, adam_consts(h->cfg, h->t), bcorr,
+                                           h->m, h->m1, h->v, h->grad, h->best_x, h->best_okey, h->best_f, h->pdata,
+                                           h->table,
+                                           lg, h->hp[h->hp_cur], h->stream),
+                       "fused generation loop");
+            else
+                ES_HIP(h, launch_run_grid(h->g, h->cfg, h->plan, h->tell, h->grid_g, (uint32_t)h->t, Tc,
+                                          adam_consts(h->cfg, h->t), bcorr, h->m, h->m1, h->v, h->grad, h->best_x,
+                                          h->best_okey, h->best_f, h->pdata, h->table, lg, h->grid_accx,
+                                          h->grid_halo, h->grid_sync,
+                                          h->hp[h->hp_cur], h->stream),
+                       "grid generation loop");
             h->t += Tc;
             done += Tc;
         }
@@ -885,6 +940,13 @@ es_status es_sync(es_handle* h)
 {
     if (!h) return ES_ERR_ARG;
     ES_HIP(h, hipStreamSynchronize(h->stream), "stream synchronize");
+    if (h->grid_sync) {
+        uint32_t flag = 0;
+        ES_HIP(h, hipMemcpy(&flag, h->grid_sync + grid_sync_words(h->g) - 1, sizeof(flag),
+                            hipMemcpyDeviceToHost),
+               "grid loop flag");
+        if (flag) return fail(h, ES_ERR_HIP, "grid generation loop: a barrier wait gave up; the state is not valid");
+    }
     return ES_OK;
 }
 

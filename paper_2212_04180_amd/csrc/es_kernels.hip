@@ -51,6 +51,8 @@ constexpr int TELL_LANES = 64;    // Philox blocks per tell workgroup
 constexpr int TELL_MAX_PS = 16;   // pair slices per tell workgroup (one wave each)
 constexpr int TELL_GROUP = 16;    // fp32 pairs folded into the fp64 sum at once
 constexpr int FUSED_WG = 256;     // threads of the fused multi-generation workgroup
+constexpr int GRID_WG = 1024;      // threads of a grid-loop workgroup (four waves per SIMD)
+constexpr uint32_t GRID_SPIN_LIMIT = 1u << 20;  // polls before a barrier wait gives up
 constexpr int FUSED_PRIO = 3;     // wave priority of the fused loop's short phases (the highest)
 
 // MLP 64-256-256-16, flattened [out][in] per layer then the bias.  Returns
@@ -232,8 +234,9 @@ template <int PROB, int V, int SM = SM_SCALAR>
 __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const float* __restrict__ pdata,
                                            uint32_t k0, uint32_t k1, uint32_t row, uint32_t t, int64_t b0,
                                            int64_t b1, int64_t D, float sg, float ra, double& accp, double& accm,
-                                           const float* __restrict__ gr = nullptr, uint32_t row2 = 0)
+                                           const float* __restrict__ gr = nullptr, uint32_t row2 = 0, int64_t mshift = 0)
 {
+    // the mean of dim d is mr[d - mshift] (a window of the row in LDS)
     constexpr bool VEC = SM != SM_SCALAR;
     const int64_t nfull = D / 4;
     const int32_t nf = (int32_t)((b1 < nfull ? b1 : nfull) - b0);  // full blocks in [b0, b1) (may be <= 0)
@@ -242,7 +245,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         float e[4], e2[4] = {0.f, 0.f, 0.f, 0.f};
         box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(b0 - 1), row, t, DOM_NOISE), e);
         if constexpr (SM == SM_INDEP) box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(b0 - 1), row2, t, DOM_NOISE), e2);
-        const float mv = mr[4 * b0 - 1];
+        const float mv = mr[4 * b0 - 1 - mshift];
         const float g = VEC ? gr[4 * b0 - 1] : sg;
         L.xlp = fmaf(g, e[3], mv);
         L.xlm = SM == SM_INDEP ? fmaf(g, e2[3], mv) : fmaf(-g, e[3], mv);
@@ -255,7 +258,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         const int64_t bg = b0 + i;
         float mv[4 * EVAL_FOLD], sv[4 * EVAL_FOLD], gv[VEC ? 4 * EVAL_FOLD : 1];
 #pragma unroll
-        for (int q = 0; q < 4 * EVAL_FOLD; ++q) mv[q] = mr[4 * bg + q];
+        for (int q = 0; q < 4 * EVAL_FOLD; ++q) mv[q] = mr[4 * bg + q - mshift];
         if constexpr (VEC) {
 #pragma unroll
             for (int q = 0; q < 4 * EVAL_FOLD; ++q) gv[q] = gr[4 * bg + q];
@@ -281,7 +284,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         const int64_t b = b0 + i;
         float mv[4], sv[4] = {0.f, 0.f, 0.f, 0.f}, gv[4] = {sg, sg, sg, sg};
 #pragma unroll
-        for (int q = 0; q < 4; ++q) mv[q] = mr[4 * b + q];
+        for (int q = 0; q < 4; ++q) mv[q] = mr[4 * b + q - mshift];
         if constexpr (VEC) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) gv[q] = gr[4 * b + q];
@@ -308,7 +311,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         if constexpr (SM == SM_INDEP) box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row2, t, DOM_NOISE), e2);
         float sp = 0.f, sm = 0.f;
         for (int k = 0; k < nv; ++k) {
-            const float mv = mr[4 * b + k];
+            const float mv = mr[4 * b + k - mshift];
             const float g = VEC ? gr[4 * b + k] : sg;
             const float xp = fmaf(g, e[k], mv), xm = SM == SM_INDEP ? fmaf(g, e2[k], mv) : fmaf(-g, e[k], mv);
             if constexpr (PROB == ES_PROB_ROSENBROCK) {
@@ -1294,6 +1297,7 @@ struct FusedArgs {
     float* m;
     float* m1;
     float* v;
+    float* grad;             // [R][Dp] or null
     float* best_x;
     uint32_t* best_okey;
     float* best_f;
@@ -1333,6 +1337,112 @@ __device__ __forceinline__ void set_long_prio(uint32_t lp)
     else __builtin_amdgcn_s_setprio(2);
 }
 
+// Best-so-far of a run inside a multi-generation loop, kept on chip: the
+// order key, fitness and member of the best so far, and the generation,
+// member and sigma of the loop's last improvement (best_x gets its noise once,
+// after the loop).
+struct LoopBest {
+    int32_t j;     // member improving on the best this generation, else -1
+    uint32_t k;
+    float fv;
+    uint32_t t;
+    int32_t jj;    // member of the last improvement (-1: none)
+    float sg;
+};
+
+// One member's fitness from its chunk partials p[c * stride], c < nchunks,
+// in the reduce kernel's order (chunk slices q < RED_SLICES, each summed in
+// chunk order, added in slice order after `add`).
+__device__ __forceinline__ double fitness_sum(const float* p, int32_t stride, int64_t nchunks, double add)
+{
+    const int nq = nchunks < RED_SLICES ? (int)nchunks : RED_SLICES;  // slices beyond add 0
+    double tot = add;
+    if (nchunks <= RED_SLICES) {
+        // one chunk per slice: four loads in flight ahead of the sum
+        for (int q0 = 0; q0 < nq; q0 += 4) {
+            float pv[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) pv[u] = p[(q0 + u < nq ? q0 + u : nq - 1) * stride];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (q0 + u < nq) {
+                    double acc = 0.0;
+                    acc += (double)pv[u];
+                    tot += acc;
+                }
+        }
+    } else {
+        for (int q = 0; q < nq; ++q) {
+            double acc = 0.0;
+            for (int64_t c = q; c < nchunks; c += RED_SLICES) acc += (double)p[c * stride];
+            tot += acc;
+        }
+    }
+    return tot;
+}
+
+// Centered ranks of one generation from the run's order keys, the folded
+// weights wf[p] = y_p - y_{p+P}, the best-so-far and (logp not null) the
+// generation's best fitness.  Eight lanes per pair: lanes 4*mem + q count
+// the keys of slice q below member p + mem*P (ties by index); the quad adds
+// its counts and the two members' weights meet across the group.  WG lanes,
+// all of them active.
+template <int WG>
+__device__ __forceinline__ void rank_pairs(const uint32_t* keys, const float* fit, const float* tab, float* wf,
+                                           int32_t N, int32_t P, int32_t raw, int32_t maximize, LoopBest& bst,
+                                           float* logp)
+{
+    const int32_t cs = ((N + 15) / 16) * 4;  // keys per slice, a multiple of 4
+    const int32_t lg = threadIdx.x & 7, mem = lg >> 2, q = lg & 3;
+    for (int32_t pb = 0; pb < P; pb += WG / 8) {
+        const int32_t p = pb + (int32_t)(threadIdx.x >> 3);
+        int32_t rk = 0, j = 0;
+        uint32_t K = 0;
+        if (p < P) {
+            j = p + mem * P;
+            K = keys[j];
+            // member k sorts before j when (key_k, k) < (K, j): one 64-bit
+            // compare per key
+            const uint64_t cj = ((uint64_t)K << 32) | (uint32_t)j;
+            const int32_t s0 = q * cs, s1 = s0 + cs < N ? s0 + cs : N;
+            int32_t k = s0;
+            for (; k + 8 <= s1; k += 8) {
+                uint4 q4[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) q4[u] = *reinterpret_cast<const uint4*>(keys + k + 4 * u);
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const uint32_t kk = (uint32_t)(k + 4 * u);
+                    rk += ((((uint64_t)q4[u].x) << 32) | kk) < cj;
+                    rk += ((((uint64_t)q4[u].y) << 32) | (kk + 1)) < cj;
+                    rk += ((((uint64_t)q4[u].z) << 32) | (kk + 2)) < cj;
+                    rk += ((((uint64_t)q4[u].w) << 32) | (kk + 3)) < cj;
+                }
+            }
+            for (; k < s1; ++k) rk += ((((uint64_t)keys[k]) << 32) | (uint32_t)k) < cj;
+        }
+        // every lane of the wave takes part in the exchanges (lane xor 1 and
+        // xor 2 within the quad by DPP, xor 4 by swizzle)
+        rk += xor_lane1(rk);
+        rk += xor_lane2(rk);
+        const float yj = p < P ? (raw ? (maximize ? -fit[j] : fit[j]) : tab[rk]) : 0.f;
+        const float yo = __int_as_float(xor_lane4(__float_as_int(yj)));
+        if (p < P && q == 0) {
+            if (mem == 0) wf[p] = yj - yo;
+            if (rk == 0) {
+                if (logp) *logp = fit[j];
+                if (K < bst.k) {
+                    bst.k = K;
+                    bst.fv = fit[j];
+                    bst.j = j;
+                } else {
+                    bst.j = -1;
+                }
+            }
+        }
+    }
+}
+
 template <int PROB>
 __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
 {
@@ -1351,14 +1461,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
     // keys start on a 16-byte boundary (they are read four at a time)
     uint32_t* keys = reinterpret_cast<uint32_t*>(ms + ((3 * Dp + a.nchunks * a.N + 2 * a.N + a.P + 3) & ~(int64_t)3));
     float* tab = reinterpret_cast<float*>(keys + ((a.N + 3) & ~3));  // [N] shaping table
-    // best-so-far of the run, kept on chip for the whole loop
-    __shared__ int32_t best_j;
-    __shared__ uint32_t best_k;
-    __shared__ float best_fv;
-    // the last improvement of the loop: generation, member, sigma
-    __shared__ uint32_t best_t;
-    __shared__ int32_t best_jj;
-    __shared__ float best_sg;
+    __shared__ LoopBest bst;
 
     const uint64_t key = a.seed + (uint64_t)r;
     const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
@@ -1374,9 +1477,9 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
     __shared__ int32_t sl_bound[TELL_MAX_PS + 1];
     if (threadIdx.x <= (uint32_t)a.ps) sl_bound[threadIdx.x] = (int32_t)(((int64_t)a.P * threadIdx.x) / a.ps);
     if (threadIdx.x == 0) {
-        best_k = a.best_okey[r];
-        best_fv = a.best_f[r];
-        best_jj = -1;
+        bst.k = a.best_okey[r];
+        bst.fv = a.best_f[r];
+        bst.jj = -1;
     }
     __syncthreads();
     // Every generation a thread walks the same items: evaluate item i is
@@ -1441,90 +1544,16 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         __syncthreads();
         __builtin_amdgcn_s_setprio(FUSED_PRIO);
         // fitness in the reduce kernel's order, and order keys
-        const int nq = a.nchunks < RED_SLICES ? (int)a.nchunks : RED_SLICES;  // slices beyond add 0
         for (int32_t j = threadIdx.x; j < a.N; j += FUSED_WG) {
-            double tot = a.add;
-            if (a.nchunks <= RED_SLICES) {
-                // one chunk per slice: four loads in flight ahead of the sum
-                for (int q0 = 0; q0 < nq; q0 += 4) {
-                    float pv[4];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) pv[u] = part[(q0 + u < nq ? q0 + u : nq - 1) * a.N + j];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u)
-                        if (q0 + u < nq) {
-                            double acc = 0.0;
-                            acc += (double)pv[u];
-                            tot += acc;
-                        }
-                }
-            } else {
-                for (int q = 0; q < nq; ++q) {
-                    double acc = 0.0;
-                    for (int64_t c = q; c < a.nchunks; c += RED_SLICES) acc += (double)part[c * a.N + j];
-                    tot += acc;
-                }
-            }
-            const float f = (float)tot;
+            const float f = (float)fitness_sum(part + j, a.N, a.nchunks, a.add);
             fit[j] = f;
             keys[j] = order_key(f, a.maximize);
         }
         __syncthreads();
         // centered ranks, the folded weights, best-so-far and the generation's
-        // log entry.  Eight lanes per pair: lanes 4*mem + q count the keys of
-        // slice q below member p + mem*P (ties by index); the quad adds its
-        // counts and the two members' weights meet across the group.
-        {
-            const int32_t cs = ((a.N + 15) / 16) * 4;  // keys per slice, a multiple of 4
-            const int32_t lg = threadIdx.x & 7, mem = lg >> 2, q = lg & 3;
-            for (int32_t pb = 0; pb < a.P; pb += FUSED_WG / 8) {
-                const int32_t p = pb + (int32_t)(threadIdx.x >> 3);
-                int32_t rk = 0, j = 0;
-                uint32_t K = 0;
-                if (p < a.P) {
-                    j = p + mem * a.P;
-                    K = keys[j];
-                    // member k sorts before j when (key_k, k) < (K, j): one
-                    // 64-bit compare per key
-                    const uint64_t cj = ((uint64_t)K << 32) | (uint32_t)j;
-                    const int32_t s0 = q * cs, s1 = s0 + cs < a.N ? s0 + cs : a.N;
-                    int32_t k = s0;
-                    for (; k + 8 <= s1; k += 8) {
-                        uint4 q4[2];
-#pragma unroll
-                        for (int u = 0; u < 2; ++u) q4[u] = *reinterpret_cast<const uint4*>(keys + k + 4 * u);
-#pragma unroll
-                        for (int u = 0; u < 2; ++u) {
-                            const uint32_t kk = (uint32_t)(k + 4 * u);
-                            rk += ((((uint64_t)q4[u].x) << 32) | kk) < cj;
-                            rk += ((((uint64_t)q4[u].y) << 32) | (kk + 1)) < cj;
-                            rk += ((((uint64_t)q4[u].z) << 32) | (kk + 2)) < cj;
-                            rk += ((((uint64_t)q4[u].w) << 32) | (kk + 3)) < cj;
-                        }
-                    }
-                    for (; k < s1; ++k) rk += ((((uint64_t)keys[k]) << 32) | (uint32_t)k) < cj;
-                }
-                // every lane of the wave takes part in the exchanges (lane
-                // xor 1 and xor 2 within the quad by DPP, xor 4 by swizzle)
-                rk += xor_lane1(rk);
-                rk += xor_lane2(rk);
-                const float yj = p < a.P ? (a.raw ? (a.maximize ? -fit[j] : fit[j]) : tab[rk]) : 0.f;
-                const float yo = __int_as_float(xor_lane4(__float_as_int(yj)));
-                if (p < a.P && q == 0) {
-                    if (mem == 0) wf[p] = yj - yo;
-                    if (rk == 0) {
-                        if (a.log) a.log[(int64_t)it * a.R + r] = fit[j];
-                        if (K < best_k) {
-                            best_k = K;
-                            best_fv = fit[j];
-                            best_j = j;
-                        } else {
-                            best_j = -1;
-                        }
-                    }
-                }
-            }
-        }
+        // log entry
+        rank_pairs<FUSED_WG>(keys, fit, tab, wf, a.N, a.P, a.raw, a.maximize, bst,
+                             a.log ? a.log + (int64_t)it * a.R + r : nullptr);
         __syncthreads();
         set_long_prio(lp);
         // tell: items (block, pair slice), slices summed in order, then Adam
@@ -1545,7 +1574,7 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
         }
         __syncthreads();
         __builtin_amdgcn_s_setprio(FUSED_PRIO);
-        const int32_t jb = best_j;
+        const int32_t jb = bst.j;
         for (int64_t i = threadIdx.x; i < 4 * a.nb; i += FUSED_WG) {
             // one dim per lane: the slices in order, then Adam
             // four slices' loads in flight ahead of the ordered sum
@@ -1564,25 +1593,26 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             // a new best: keep the mean it was sampled around; its noise is
             // added once, after the loop (same arithmetic as the per-call path)
             if (jb >= 0) a.best_x[goff + i] = mo;
+            if (a.grad) a.grad[goff + i] = gg;
             ms[i] = mn;
             m1s[i] = m1n;
             vs[i] = vn;
         }
         if (jb >= 0 && threadIdx.x == 0) {
-            best_t = t;
-            best_jj = jb;
-            best_sg = sigma;
+            bst.t = t;
+            bst.jj = jb;
+            bst.sg = sigma;
         }
         __syncthreads();
         sigma = schedule_step(sigma, a.sigma_decay, a.sigma_final);
         lr = schedule_step(lr, a.lr_decay, a.lr_final);
     }
-    if (best_jj >= 0) {
-        const int32_t pbst = best_jj < a.P ? best_jj : best_jj - a.P;
-        const float sg = best_jj < a.P ? best_sg : -best_sg;
+    if (bst.jj >= 0) {
+        const int32_t pbst = bst.jj < a.P ? bst.jj : bst.jj - a.P;
+        const float sg = bst.jj < a.P ? bst.sg : -bst.sg;
         for (int64_t b = threadIdx.x; b < a.nb; b += FUSED_WG) {
             float e[4];
-            box_muller4(philox4x32_10<LANES_BLOCK_AND_ROW>(k0, k1, (uint32_t)b, (uint32_t)pbst, best_t, DOM_NOISE), e);
+            box_muller4(philox4x32_10<LANES_BLOCK_AND_ROW>(k0, k1, (uint32_t)b, (uint32_t)pbst, bst.t, DOM_NOISE), e);
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const int64_t d = goff + 4 * b + k;
@@ -1593,14 +1623,468 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
     if (threadIdx.x == 0) {
         a.hp[r] = sigma;
         a.hp[a.R + r] = lr;
-        a.best_okey[r] = best_k;
-        a.best_f[r] = best_fv;
+        a.best_okey[r] = bst.k;
+        a.best_f[r] = bst.fv;
     }
     for (int64_t i = threadIdx.x; i < Dp; i += FUSED_WG) {
         a.m[goff + i] = ms[i];
         a.m1[goff + i] = m1s[i];
         a.v[goff + i] = vs[i];
     }
+}
+
+// ---------------------------------------------------------------------------
+// T whole generations of a run on a cooperative grid of G workgroups (grid.x;
+// runs on grid.y): the scanned loop for runs too large for one workgroup yet
+// too small to fill the chip per call, where the per-call launches would
+// cost more than the work.  The work is split by dimension: workgroup w owns
+// the evaluate chunks c = w + G i, which are whole chunk slices of the reduce
+// kernel (slice q holds the chunks q, q + RED_SLICES, ...; G divides
+// RED_SLICES, or every slice is one chunk), and for those chunks' Philox
+// blocks it evaluates every pair, forms the gradient and the update, its
+// mean, m1 and v staying in LDS.  Per generation one exchange: the members'
+// slice sums (fp64, two buffers by generation parity) behind one grid
+// barrier; every workgroup then adds them into all N fitnesses in the reduce
+// kernel's order and ranks them itself.  Rosenbrock's evaluate also reads the
+// last dim before each chunk, owned by workgroup w - 1, which publishes it
+// with the generation in one 64-bit word (a single location: no fence).
+// Chunking, reduction order and the gradient's
+// sub-slices, slices and splits are those of the handle's per-call plans, so
+// es_run gives the same bits on either path.
+struct GridArgs {
+    float* m;
+    float* m1;
+    float* v;
+    float* grad;             // [R][Dp] or null
+    float* best_x;
+    uint32_t* best_okey;
+    float* best_f;
+    const float* pdata;
+    const float* table;
+    float* log;              // [T][R] or null
+    double* accx;            // [2][R][RED_SLICES][N] slice sums of the members
+    uint64_t* halo;          // [R][nchunks] (t + 1) << 32 | the last dim of chunk c after the update of generation t
+    uint32_t* bar;           // [R] arrivals at the run's barriers, zero at launch
+    uint32_t* err;           // set nonzero when a wait gives up
+    uint64_t seed;
+    uint32_t t0;
+    int32_t T;
+    int64_t D, nb;
+    int32_t N, P, R;
+    int64_t bc, nchunks;
+    int32_t ps, nsplit, sub;  // the per-call gradient plan
+    int32_t ncw;              // most chunks of one workgroup
+    int32_t ks;               // key ranges of the rank count
+    float ra;
+    double add;
+    int32_t maximize, raw;
+    float* hp;               // [2][R] sigma, lr: read at the start, the schedule's values written at the end
+    float sigma_decay, sigma_final, lr_decay, lr_final;
+    AdamConsts ac;
+    float bcorr[FUSED_MAX_T][2];
+};
+static_assert(std::is_standard_layout<GridArgs>::value, "offsetof(GridArgs, bcorr) is used on the device");
+
+// Thread 0 polls *flag until it reaches target or the wait gives up (after
+// GRID_SPIN_LIMIT polls, or once another workgroup gave up: then *err is
+// set); false if it gave up.  Acquire at device scope after the wait.
+__device__ __forceinline__ bool spin_until(const uint32_t* flag, uint32_t target, uint32_t* err)
+{
+    for (uint32_t spins = 0; __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target; ++spins) {
+        __builtin_amdgcn_s_sleep(1);
+        if (spins >= GRID_SPIN_LIMIT || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+            __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return false;
+        }
+    }
+    __threadfence();
+    return true;
+}
+
+// Barrier of the grid.x workgroups of one run: each arrives on the run's
+// counter after a release at device scope (so its stores are visible) and
+// waits for this barrier's count.  false (every workgroup then leaves the
+// kernel) if the wait gave up; the cooperative launch keeps all workgroups
+// resident, so only a wrong kernel can make it give up.
+__device__ __forceinline__ bool grid_wait(uint32_t* cnt, uint32_t target, uint32_t* err, int32_t* ok)
+{
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __threadfence();
+        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *ok = spin_until(cnt, target, err) ? 1 : 0;
+    }
+    __syncthreads();
+    return *ok != 0;
+}
+
+// Key ranges the rank count splits into: every wave of the workgroup takes
+// one (member chunk of 64, key range) task while there are fewer member
+// chunks than waves.
+__host__ __device__ __forceinline__ int32_t grid_rank_splits(int32_t N)
+{
+    const int32_t mc = (N + 63) / 64, nw = GRID_WG / 64;
+    const int32_t ks = mc < nw ? nw / mc : 1;
+    return ks;
+}
+
+// Centered ranks of all N members (every workgroup alike), the folded
+// weights wf[p] = y_p - y_{p+P}, the best-so-far and (logp not null) the
+// generation's best fitness.  comp[k] = key_k << 32 | k, so member k sorts
+// before j exactly when comp[k] < comp[j] (ties by index).  Each wave
+// counts, for 64 members, the composites of one key range below each of
+// theirs, reading every composite at one address for the whole wave.  cnt:
+// [ks][N].
+__device__ __forceinline__ void rank_grid(const uint64_t* comp, const uint32_t* keys, const float* fit,
+                                          const float* tab, float* y, float* wf, int32_t* cnt, int32_t N, int32_t P,
+                                          int32_t ks, int32_t raw, int32_t maximize, LoopBest& bst, float* logp)
+{
+    const int32_t wave = __builtin_amdgcn_readfirstlane((int32_t)(threadIdx.x / 64)), lane = threadIdx.x % 64;
+    const int32_t tasks = (N + 63) / 64 * ks;
+    for (int32_t task = wave; task < tasks; task += GRID_WG / 64) {
+        const int32_t mc = task / ks, kr = task - mc * ks;
+        const int32_t j = mc * 64 + lane;
+        const int32_t k0 = (N * kr) / ks, k1 = (N * (kr + 1)) / ks;  // N ks < 2^31
+        // lanes past N compare against 0: nothing sorts before it
+        const uint64_t cj = j < N ? comp[j] : 0;
+        int32_t rk = 0;
+        int32_t k = k0;
+        for (; k < k1 && (k & 1); ++k) rk += comp[k] < cj;
+        // eight composites per step: four reads in flight, two counts
+        for (; k + 8 <= k1; k += 8) {
+            ulonglong2 c2[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) c2[u] = *reinterpret_cast<const ulonglong2*>(comp + k + 2 * u);
+            int32_t ra = 0, rb = 0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                ra += c2[u].x < cj;
+                rb += c2[u].y < cj;
+            }
+            rk += ra + rb;
+        }
+        for (; k < k1; ++k) rk += comp[k] < cj;
+        if (j < N) cnt[kr * N + j] = rk;
+    }
+    __syncthreads();
+    for (int32_t j = threadIdx.x; j < N; j += GRID_WG) {
+        int32_t rk = 0;
+        for (int32_t kr = 0; kr < ks; ++kr) rk += cnt[kr * N + j];
+        y[j] = raw ? (maximize ? -fit[j] : fit[j]) : tab[rk];
+        if (rk == 0) {
+            if (logp) *logp = fit[j];
+            const uint32_t K = keys[j];
+            if (K < bst.k) {
+                bst.k = K;
+                bst.fv = fit[j];
+                bst.j = j;
+            } else {
+                bst.j = -1;
+            }
+        }
+    }
+    __syncthreads();
+    for (int32_t p = threadIdx.x; p < P; p += GRID_WG) wf[p] = y[p] - y[p + P];
+}
+
+template <int PROB>
+__global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
+{
+    extern __shared__ __align__(16) double smem[];
+    const int32_t r = blockIdx.y, w = blockIdx.x, G = gridDim.x;
+    const int32_t S = a.ps * a.nsplit * a.sub;  // the gradient's sub-slices of the pairs
+    const int32_t nch = (int32_t)a.nchunks, bc = (int32_t)a.bc, nb = (int32_t)a.nb;
+    const int32_t nq = nch < RED_SLICES ? nch : RED_SLICES;
+    // own chunks c = w + G i, i < ncw; their blocks have local indices i bc + o
+    const int32_t ncw = w < nch ? (nch - w + G - 1) / G : 0;
+    const int32_t nlb = ncw * bc;        // local blocks (the last chunk's may pass nb)
+    const int32_t CW = 1 + 4 * bc;       // mean of one chunk in LDS: the dim before it, then its dims
+    // LDS: sub-slice sums (fp64) [S][ncw bc][4] | rank composites (u64) [N] |
+    // mean [ncw][CW] | m1, v [ncw bc][4] | partials [ncw][N] | fit [N] | y
+    // [N] | wf [P] | keys [N, from a 16-byte boundary] | table [N] | rank
+    // counts [ks][N] | pair bounds of the sub-slices [S + 1]
+    const int64_t st = 4 * (int64_t)a.ncw * bc;  // stride of one sub-slice in red
+    double* red = smem;
+    uint64_t* comp = reinterpret_cast<uint64_t*>(red + (int64_t)S * st);
+    float* ms = reinterpret_cast<float*>(comp + a.N);
+    float* m1s = ms + a.ncw * CW;
+    float* vs = m1s + st;
+    float* part = vs + st;
+    float* fit = part + a.ncw * a.N;
+    float* y = fit + a.N;
+    float* wf = y + a.N;
+    uint32_t* keys = reinterpret_cast<uint32_t*>(ms + ((a.ncw * CW + 2 * st + a.ncw * a.N + 2 * a.N + a.P + 3) & ~(int64_t)3));
+    float* tab = reinterpret_cast<float*>(keys + ((a.N + 3) & ~3));
+    int32_t* cnt = reinterpret_cast<int32_t*>(tab + a.N);
+    int32_t* sbd = cnt + a.ks * a.N;  // sub-slice gs takes the pairs [sbd[gs], sbd[gs + 1])
+    __shared__ LoopBest bst;
+    __shared__ int32_t ok;
+
+    const uint64_t key = a.seed + (uint64_t)r;
+    const uint32_t k0 = (uint32_t)key, k1 = (uint32_t)(key >> 32);
+    const int64_t goff = (int64_t)r * 4 * a.nb;
+    float sigma = a.hp[r], lr = a.hp[a.R + r];
+    // own dims: local dim i = 4 (i_c bc + o) + k of chunk c = w + G i_c
+    for (int32_t i = threadIdx.x; i < 4 * nlb; i += GRID_WG) {
+        const int32_t lb = i >> 2, ic = lb / bc, o = lb - ic * bc;
+        const int64_t b = (int64_t)(w + G * ic) * bc + o;
+        float mv = 0.f, m1v = 0.f, vv = 0.f;  // padding blocks past nb stay zero
+        if (b < nb) {
+            const int64_t d = goff + 4 * b + (i & 3);
+            mv = a.m[d];
+            m1v = a.m1[d];
+            vv = a.v[d];
+        }
+        ms[ic * CW + 1 + 4 * o + (i & 3)] = mv;
+        m1s[i] = m1v;
+        vs[i] = vv;
+    }
+    for (int32_t j = threadIdx.x; j < a.N; j += GRID_WG) tab[j] = a.table[j];
+    for (int32_t g = threadIdx.x; g <= S; g += GRID_WG) sbd[g] = (int32_t)(((int64_t)a.P * g) / S);
+    if (threadIdx.x == 0) {
+        bst.k = a.best_okey[r];
+        bst.fv = a.best_f[r];
+        bst.jj = -1;
+    }
+    __syncthreads();
+    uint32_t* cnt_bar = a.bar + r;
+    uint64_t* halo = a.halo + (int64_t)r * nch;
+    uint32_t arrivals = 0;
+    const int32_t ev_items = a.P * ncw, tl_items = nlb * S;
+    // Every generation a thread walks the same items, set up here and stepped
+    // by additions: evaluate item i is (pair i % P, own chunk i / P), gradient
+    // item i is (local block i % nlb, sub-slice i / nlb).
+    const int32_t ev_p0 = (int32_t)threadIdx.x % a.P, ev_c0 = (int32_t)threadIdx.x / a.P;
+    const int32_t ev_dp = GRID_WG % a.P, ev_dc = GRID_WG / a.P;
+    const int32_t tl_l0 = nlb > 0 ? (int32_t)threadIdx.x % nlb : 0, tl_g0 = nlb > 0 ? (int32_t)threadIdx.x / nlb : 0;
+    const int32_t tl_dl = nlb > 0 ? GRID_WG % nlb : 0, tl_dg = nlb > 0 ? GRID_WG / nlb : 0;
+
+    for (int32_t it = 0; it < a.T; ++it) {
+        const uint32_t t = a.t0 + (uint32_t)it;
+        double inv_ns = 1.0 / (2.0 * (double)a.P * (double)sigma);
+        asm volatile("" : "+v"(inv_ns));
+        AdamConsts ac = a.ac;
+        {
+            const float* kb = reinterpret_cast<const float*>((const char*)__builtin_amdgcn_kernarg_segment_ptr() +
+                                                             offsetof(GridArgs, bcorr));
+            ac.bc1 = kb[2 * it];
+            ac.bc2 = kb[2 * it + 1];
+        }
+        if constexpr (PROB == ES_PROB_ROSENBROCK) {
+            // the dim before each own chunk (the last of chunk c - 1, updated
+            // by workgroup w - 1): from the state at the launch's first
+            // generation, then from chunk c - 1's word once it carries this
+            // generation's tag
+            if (threadIdx.x == 0) ok = 1;
+            __syncthreads();
+            for (int32_t ic = threadIdx.x; ic < ncw; ic += GRID_WG) {
+                const int32_t c = w + G * ic;
+                float h = 0.f;
+                if (c > 0 && it == 0) {
+                    h = a.m[goff + 4 * (int64_t)c * bc - 1];
+                } else if (c > 0) {
+                    uint64_t word;
+                    for (uint32_t spins = 0;; ++spins) {
+                        word = __hip_atomic_load(halo + c - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        if ((uint32_t)(word >> 32) == t) break;
+                        __builtin_amdgcn_s_sleep(1);
+                        if (spins >= GRID_SPIN_LIMIT || __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                            __hip_atomic_fetch_or(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            ok = 0;
+                            break;
+                        }
+                    }
+                    h = __uint_as_float((uint32_t)word);
+                }
+                ms[ic * CW] = h;
+            }
+            __syncthreads();
+            if (!ok) return;
+        }
+        // evaluate: items (pair, own chunk)
+        {
+            int32_t p = ev_p0, ic = ev_c0;
+            for (int32_t i = threadIdx.x; i < ev_items; i += GRID_WG) {
+                const int64_t b0 = (int64_t)(w + G * ic) * bc, b1 = b0 + bc < nb ? b0 + bc : nb;
+                double accp, accm;
+                eval_chunk<PROB, LANES_BLOCK_AND_ROW>(ms + ic * CW + 1, a.pdata, k0, k1, (uint32_t)p, t, b0, b1, a.D,
+                                                      sigma, a.ra, accp, accm, nullptr, 0, 4 * b0);
+                part[ic * a.N + p] = (float)accp;
+                part[ic * a.N + p + a.P] = (float)accm;
+                p += ev_dp;
+                ic += ev_dc;
+                if (p >= a.P) {
+                    p -= a.P;
+                    ++ic;
+                }
+            }
+        }
+        __syncthreads();
+        // slice sums of the own slices q = w + G u (chunks q, q + RED_SLICES,
+        // ... in order), for every member
+        double* acc_out = a.accx + ((int64_t)(it & 1) * a.R + r) * RED_SLICES * a.N;
+        {
+            const int32_t per = nch <= RED_SLICES ? 1 : RED_SLICES / G;  // own chunks between two of one slice
+            const int32_t nsl = nch <= RED_SLICES ? ncw : (nq - w + G - 1) / G;
+            for (int32_t i = threadIdx.x; i < nsl * a.N; i += GRID_WG) {
+                const int32_t u = i / a.N, j = i - u * a.N;
+                double acc = 0.0;
+                for (int32_t ic = u; ic < ncw; ic += (nch <= RED_SLICES ? ncw : per)) acc += (double)part[ic * a.N + j];
+                acc_out[(int64_t)(w + G * u) * a.N + j] = acc;
+            }
+        }
+        if (!grid_wait(cnt_bar, (uint32_t)G * ++arrivals, a.err, &ok)) return;
+        // every member's fitness: the slices in order after `add`
+        for (int32_t j = threadIdx.x; j < a.N; j += GRID_WG) {
+            double sv[RED_SLICES];
+#pragma unroll
+            for (int32_t q = 0; q < RED_SLICES; ++q) sv[q] = q < nq ? acc_out[(int64_t)q * a.N + j] : 0.0;
+            double tot = a.add;
+#pragma unroll
+            for (int32_t q = 0; q < RED_SLICES; ++q)
+                if (q < nq) tot += sv[q];
+            const float f = (float)tot;
+            fit[j] = f;
+            const uint32_t K = order_key(f, a.maximize);
+            keys[j] = K;
+            comp[j] = ((uint64_t)K << 32) | (uint32_t)j;
+        }
+        __syncthreads();
+        rank_grid(comp, keys, fit, tab, y, wf, cnt, a.N, a.P, a.ks, a.raw, a.maximize, bst,
+                  (w == 0 && a.log) ? a.log + (int64_t)it * a.R + r : nullptr);
+        __syncthreads();
+        // gradient of the own blocks: items (block, sub-slice gs), gs
+        // numbering the pairs' sub-slices as the per-call kernel does:
+        // ((split z) ps + slice s) sub + lane
+        {
+            int32_t lb = tl_l0, gs = tl_g0;
+            for (int32_t i = threadIdx.x; i < tl_items; i += GRID_WG) {
+                const int32_t ic = lb / bc;
+                const int64_t b = (int64_t)(w + G * ic) * bc + (lb - ic * bc);
+                if (b < nb) {
+                    double a64[4] = {0.0, 0.0, 0.0, 0.0};
+                    tell_slice<LANES_BLOCK_AND_ROW>(wf, k0, k1, (uint32_t)b, t, sbd[gs], sbd[gs + 1], a64);
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) red[gs * st + 4 * lb + k] = a64[k];
+                }
+                lb += tl_dl;
+                gs += tl_dg;
+                if (lb >= nlb) {
+                    lb -= nlb;
+                    ++gs;
+                }
+            }
+        }
+        __syncthreads();
+        // update of the own dims: the sub-slices combined in the per-call
+        // order (the lanes of a block pairwise, into each slice's first
+        // sub-slice, one (slice, dim) per lane; then per dim the slices in
+        // order and the splits in order), then Adam
+        if (a.sub > 1) {
+            const int32_t dims = 4 * nlb;
+            for (int32_t i = threadIdx.x; i < a.nsplit * a.ps * dims; i += GRID_WG) {
+                const int32_t gi = i / dims, di = i - gi * dims;
+                double* rv = red + (int64_t)gi * a.sub * st + di;
+                double vsl = rv[0];
+                if (a.sub == 2) vsl += rv[st];
+                else vsl = (vsl + rv[st]) + (rv[2 * st] + rv[3 * st]);
+                rv[0] = vsl;
+            }
+            __syncthreads();
+        }
+        const int32_t jb = bst.j;
+        const int64_t gst = (int64_t)a.sub * st;  // from one slice's sum to the next
+        for (int32_t i = threadIdx.x; i < 4 * nlb; i += GRID_WG) {
+            const int32_t lb = i >> 2, ic = lb / bc, o = lb - ic * bc;
+            const int64_t b = (int64_t)(w + G * ic) * bc + o;
+            if (b >= nb) continue;
+            double tot = 0.0;
+            for (int32_t z = 0; z < a.nsplit; ++z) {
+                // four slices' loads in flight ahead of the ordered sum
+                const double* rz = red + (int64_t)z * a.ps * gst + i;
+                double az = rz[0];
+                for (int32_t s0 = 1; s0 < a.ps; s0 += 4) {
+                    double v4[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) v4[u] = rz[(s0 + u < a.ps ? s0 + u : a.ps - 1) * gst];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        if (s0 + u < a.ps) az += v4[u];
+                }
+                tot = z == 0 ? az : tot + az;
+            }
+            const int64_t d = 4 * b + (i & 3);
+            float* mp = ms + ic * CW + 1 + 4 * o + (i & 3);
+            const float mo = *mp;
+            float mn, m1n, vn, gg;
+            adam_dim(tot, inv_ns, ac, lr, d, a.D, mo, m1s[i], vs[i], mn, m1n, vn, gg);
+            // a new best: keep the mean it was sampled around; its noise is
+            // added once, after the loop
+            if (jb >= 0) a.best_x[goff + d] = mo;
+            *mp = mn;
+            m1s[i] = m1n;
+            vs[i] = vn;
+            a.m[goff + d] = mn;
+            if (a.grad) a.grad[goff + d] = gg;
+            if constexpr (PROB == ES_PROB_ROSENBROCK) {
+                // the last dim of a chunk that another chunk follows: published
+                // for the next generation's evaluate of that chunk
+                const int32_t c = w + G * ic;
+                if (o == bc - 1 && (i & 3) == 3 && c + 1 < nch)
+                    __hip_atomic_store(halo + c, ((uint64_t)(t + 1) << 32) | __float_as_uint(mn), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        if (jb >= 0 && threadIdx.x == 0) {
+            bst.t = t;
+            bst.jj = jb;
+            bst.sg = sigma;
+        }
+        // the next generation's evaluate reads the updated mean (and its
+        // ranks overwrite the best-so-far) only after every lane is done here
+        __syncthreads();
+        sigma = schedule_step(sigma, a.sigma_decay, a.sigma_final);
+        lr = schedule_step(lr, a.lr_decay, a.lr_final);
+    }
+    __syncthreads();
+    if (bst.jj >= 0) {
+        const int32_t pbst = bst.jj < a.P ? bst.jj : bst.jj - a.P;
+        const float sg = bst.jj < a.P ? bst.sg : -bst.sg;
+        for (int32_t lb = threadIdx.x; lb < nlb; lb += GRID_WG) {
+            const int32_t ic = lb / bc;
+            const int64_t b = (int64_t)(w + G * ic) * bc + (lb - ic * bc);
+            if (b >= nb) continue;
+            float e[4];
+            box_muller4(philox4x32_10<LANES_BLOCK_AND_ROW>(k0, k1, (uint32_t)b, (uint32_t)pbst, bst.t, DOM_NOISE), e);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int64_t d = goff + 4 * b + k;
+                a.best_x[d] = 4 * b + k < a.D ? fmaf(sg, e[k], a.best_x[d]) : 0.f;
+            }
+        }
+    }
+    if (w == 0 && threadIdx.x == 0) {
+        a.hp[r] = sigma;
+        a.hp[a.R + r] = lr;
+        a.best_okey[r] = bst.k;
+        a.best_f[r] = bst.fv;
+    }
+    for (int32_t i = threadIdx.x; i < 4 * nlb; i += GRID_WG) {
+        const int32_t lb = i >> 2, ic = lb / bc;
+        const int64_t b = (int64_t)(w + G * ic) * bc + (lb - ic * bc);
+        if (b >= nb) continue;
+        const int64_t d = goff + 4 * b + (i & 3);
+        a.m1[d] = m1s[i];
+        a.v[d] = vs[i];
+    }
+}
+
+// Barrier counters of the grid loop cleared ahead of a launch (a
+// kernel, so the clearing can sit in a captured stream).
+__global__ void k_clear_u32(uint32_t* __restrict__ p, int32_t n)
+{
+    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0u;
 }
 
 // ---------------------------------------------------------------------------
@@ -1933,13 +2417,13 @@ bool fused_supported(const Geometry& g, const EvalPlan& e, const es_config& c)
 }
 
 hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPlan& e, uint32_t t0, int32_t T,
-                            const AdamConsts& ac, const float (*bcorr)[2], float* m, float* m1, float* v,
+                            const AdamConsts& ac, const float (*bcorr)[2], float* m, float* m1, float* v, float* grad,
                             float* best_x, uint32_t* best_okey, float* best_f, const float* pdata, const float* table,
                             float* log, float* hp, hipStream_t s)
 {
     if (T < 1 || T > FUSED_MAX_T) return hipErrorInvalidValue;
     FusedArgs a;
-    a.m = m; a.m1 = m1; a.v = v; a.best_x = best_x; a.best_okey = best_okey; a.best_f = best_f;
+    a.m = m; a.m1 = m1; a.v = v; a.grad = grad; a.best_x = best_x; a.best_okey = best_okey; a.best_f = best_f;
     a.pdata = pdata; a.table = table; a.log = log;
     a.ac = ac;
     for (int32_t i = 0; i < T; ++i) {
@@ -1962,6 +2446,106 @@ hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPla
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+int32_t grid_workgroups(const Geometry& g, const EvalPlan& e, int32_t want)
+{
+    // about 2048 pair-blocks of each of evaluate and gradient per workgroup,
+    // at most one per chunk slice of the reduce kernel and, beyond
+    // RED_SLICES chunks, a divisor of RED_SLICES (workgroups own whole slices)
+    const int64_t nq = e.nchunks < RED_SLICES ? e.nchunks : RED_SLICES;
+    int64_t G = want > 0 ? want : ((int64_t)g.P * g.nb + 2047) / 2048;
+    if (G > nq) G = nq;
+    if (G < 1) G = 1;
+    if (e.nchunks > RED_SLICES)
+        while (RED_SLICES % G != 0) --G;
+    return (int32_t)G;
+}
+
+size_t grid_lds_bytes(const Geometry& g, const EvalPlan& e, const TellPlan& tp, int32_t G)
+{
+    const int64_t S = (int64_t)tp.ps * tp.nsplit * tp.sub;
+    const int64_t ncw = (e.nchunks + G - 1) / G, st = 4 * ncw * e.bc;
+    // sub-slice sums | rank composites | mean windows | m1, v | partials | fit | y | wf | keys (from a 16-byte
+    // boundary) | table | counts | pair bounds
+    size_t f32 = (size_t)(ncw * (1 + 4 * e.bc) + 2 * st + ncw * g.N + 2 * g.N + g.P);
+    f32 = (f32 + 3) & ~(size_t)3;
+    f32 += (size_t)((g.N + 3) & ~3) + (size_t)g.N + (size_t)grid_rank_splits(g.N) * g.N + (size_t)(S + 1);
+    return sizeof(double) * (size_t)(S * st + g.N) + sizeof(float) * f32;
+}
+
+bool grid_supported(const Geometry& g, const EvalPlan& e, const TellPlan& tp, const es_config& c, int32_t G)
+{
+    // what the fused loop runs (OpenAI-ES with Adam, centered ranks or raw
+    // keys, no weight decay), with every workgroup ranking the run's members
+    if (c.problem < ES_PROB_SPHERE || c.problem > ES_PROB_RASTRIGIN) return false;
+    if (c.strategy != ES_STRAT_OPENAI_ES || c.optimizer != ES_OPT_ADAM) return false;
+    if (c.shaping == ES_SHAPE_Z_SCORE || c.w_decay != 0.0f) return false;
+    if (g.N > GRID_MAX_N || (int64_t)G * g.R > 65535) return false;
+    if (tp.sub != 1 && tp.sub != 2 && tp.sub != 4) return false;
+    if ((int64_t)tp.ps * tp.nsplit * tp.sub > g.P) return false;  // every sub-slice is a pair range
+    // workgroups own whole chunk slices
+    const int64_t nq = e.nchunks < RED_SLICES ? e.nchunks : RED_SLICES;
+    if (G < 1 || G > nq || (e.nchunks > RED_SLICES && RED_SLICES % G != 0)) return false;
+    return grid_lds_bytes(g, e, tp, G) <= GRID_MAX_LDS;
+}
+
+static_assert(RED_SLICES == 16, "grid_accx_elems sizes the slice sums for 16 slices");
+
+hipError_t grid_max_resident(int64_t* out)
+{
+    int dev = 0, cus = 0, per_cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    // every grid-loop launch stays within GRID_MAX_LDS of dynamic LDS
+    if (e == hipSuccess)
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(&k_run_grid<ES_PROB_ROSENBROCK>),
+                                                         GRID_WG, GRID_MAX_LDS);
+    *out = e == hipSuccess ? (int64_t)cus * per_cu : 0;
+    return e;
+}
+
+hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan& e, const TellPlan& tp, int32_t G,
+                           uint32_t t0, int32_t T, const AdamConsts& ac, const float (*bcorr)[2], float* m, float* m1,
+                           float* v, float* grad, float* best_x, uint32_t* best_okey, float* best_f,
+                           const float* pdata, const float* table, float* log, double* accx, uint64_t* halo,
+                           uint32_t* sync, float* hp, hipStream_t s)
+{
+    if (T < 1 || T > FUSED_MAX_T || G < 1 || G > GRID_MAX_G) return hipErrorInvalidValue;
+    if (!grid_supported(g, e, tp, c, G)) return hipErrorInvalidValue;
+    GridArgs a;
+    a.m = m; a.m1 = m1; a.v = v; a.grad = grad; a.best_x = best_x; a.best_okey = best_okey; a.best_f = best_f;
+    a.pdata = pdata; a.table = table; a.log = log; a.accx = accx; a.halo = halo;
+    a.bar = sync; a.err = sync + grid_sync_words(g) - 1;
+    a.ac = ac;
+    for (int32_t i = 0; i < T; ++i) {
+        a.bcorr[i][0] = bcorr[i][0];
+        a.bcorr[i][1] = bcorr[i][1];
+    }
+    a.seed = c.seed; a.t0 = t0; a.T = T; a.D = g.D; a.nb = g.nb; a.N = g.N; a.P = g.P; a.R = g.R;
+    a.bc = e.bc; a.nchunks = e.nchunks; a.ps = tp.ps; a.nsplit = tp.nsplit; a.sub = tp.sub;
+    a.ncw = (int32_t)((e.nchunks + G - 1) / G); a.ks = grid_rank_splits(g.N);
+    a.ra = c.rastrigin_a;
+    a.add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;
+    a.maximize = c.maximize; a.raw = c.shaping == ES_SHAPE_RAW;
+    a.hp = hp;
+    a.sigma_decay = c.sigma_decay; a.sigma_final = c.sigma_final; a.lr_decay = c.lr_decay; a.lr_final = c.lr_final;
+    // barrier counters cleared; the error flag after them stays
+    const int32_t nclear = (int32_t)(grid_sync_words(g) - 1);
+    k_clear_u32<<<(nclear + 255) / 256, 256, 0, s>>>(sync, nclear);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    const uint32_t lds = (uint32_t)grid_lds_bytes(g, e, tp, G);
+    void* args[] = {&a};
+    const void* k;
+    switch (c.problem) {
+    case ES_PROB_SPHERE: k = reinterpret_cast<const void*>(&k_run_grid<ES_PROB_SPHERE>); break;
+    case ES_PROB_SHIFTED_SPHERE: k = reinterpret_cast<const void*>(&k_run_grid<ES_PROB_SHIFTED_SPHERE>); break;
+    case ES_PROB_ROSENBROCK: k = reinterpret_cast<const void*>(&k_run_grid<ES_PROB_ROSENBROCK>); break;
+    case ES_PROB_RASTRIGIN: k = reinterpret_cast<const void*>(&k_run_grid<ES_PROB_RASTRIGIN>); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipLaunchCooperativeKernel(k, dim3((unsigned)G, (unsigned)g.R), dim3(GRID_WG), args, lds, s);
 }
 
 hipError_t launch_debug_noise(const Geometry& g, const es_config& c, int32_t run, uint32_t t,

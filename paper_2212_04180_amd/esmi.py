@@ -29,7 +29,7 @@ EXPORTS = ("es_init", "es_ask", "es_eval", "es_eval_timed", "es_eval_noalloc", "
            "es_get_best", "es_get_shaped", "es_get_grad", "es_set_hparams", "es_get_hparams",
            "es_get_strategy_state", "es_set_strategy_state", "es_get_penalty",
            "es_get_problem_data", "es_debug_noise",
-           "es_save_state", "es_load_state", "es_sync", "es_generation", "es_last_error",
+           "es_save_state", "es_load_state", "es_sync", "es_generation", "es_run_path", "es_last_error",
            "es_status_string", "es_destroy")
 
 
@@ -78,7 +78,7 @@ class _Config(ctypes.Structure):
         ("plan_tell_split", ctypes.c_int32),
         ("plan_run_path", ctypes.c_int32),
         ("plan_rank_path", ctypes.c_int32),
-        ("reserved2", ctypes.c_int32),
+        ("plan_grid_workgroups", ctypes.c_int32),
     ]
 
 
@@ -127,7 +127,7 @@ class ESConfig:
     plan_tell_split: int = 0
     plan_run_path: int = 0
     plan_rank_path: int = 0
-    reserved2: int = 0
+    plan_grid_workgroups: int = 0
 
     def cstruct(self) -> _Config:
         c = _Config()
@@ -174,6 +174,7 @@ def lib() -> ctypes.CDLL:
         "es_load_state": (i32, [vp, vp, ctypes.c_size_t]),
         "es_sync": (i32, [vp]),
         "es_generation": (i64, [vp]),
+        "es_run_path": (i32, [vp]),
         "es_last_error": (ctypes.c_char_p, [vp]),
         "es_status_string": (ctypes.c_char_p, [i32]),
         "es_destroy": (None, [vp]),
@@ -249,6 +250,11 @@ class ES:
     @property
     def t(self) -> int:
         return int(lib().es_generation(self._h))
+
+    @property
+    def run_path(self) -> int:
+        """The path es_run takes: 1 per-call kernels, 2 fused loop, 3 grid loop."""
+        return int(lib().es_run_path(self._h))
 
     # -- ask / evaluate / tell ---------------------------------------------
     def ask(self, materialize: bool = False):

@@ -34,6 +34,7 @@ def test_status_strings_and_init_error_without_gpu_work():
     from paper_2212_04180_amd import esmi
     L = esmi.lib()
     assert L.es_status_string(0) == b"ok"
+    assert L.es_run_path(None) == 0 and L.es_generation(None) == -1
     assert L.es_status_string(-2).startswith(b"call out of")
     # an invalid config is rejected before any device call
     cfg = esmi.ESConfig(num_dims=8, popsize=3).cstruct()
@@ -76,7 +77,8 @@ def test_probe_library_exports_its_header():
 
 def test_population_limits_are_validated_without_gpu_work():
     """Up to 16384 members the ranks are counted in LDS; beyond, the sort-based
-    ranks take over, up to 2^24 members (rejected before any device call)."""
+    ranks take over, up to 2^24 members; launch-plan fields in range
+    (rejected before any device call)."""
     from paper_2212_04180_amd import esmi
     L = esmi.lib()
     h = ctypes.c_void_p()
@@ -84,7 +86,9 @@ def test_population_limits_are_validated_without_gpu_work():
                     (dict(popsize=16386, plan_rank_path=1), b"plan_rank_path 1"),
                     (dict(popsize=64, plan_rank_path=3), b"plan_rank_path must be"),
                     (dict(popsize=(1 << 20), num_runs=4096), b"2^31"),
-                    (dict(popsize=64, reserved2=1), b"reserved")):
+                    (dict(popsize=64, plan_run_path=4), b"plan_run_path must be"),
+                    (dict(popsize=64, plan_grid_workgroups=17), b"plan_grid_workgroups"),
+                    (dict(popsize=64, plan_grid_workgroups=-1), b"plan_grid_workgroups")):
         cfg = esmi.ESConfig(num_dims=8, **kw).cstruct()
         assert L.es_init(ctypes.byref(cfg), None, ctypes.byref(h)) == esmi.ES_ERR_ARG, kw
         assert msg in L.es_last_error(None), (kw, L.es_last_error(None))

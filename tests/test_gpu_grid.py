@@ -1,0 +1,134 @@
+"""The grid loop of es_run (a cooperative launch of several workgroups per
+run, two grid barriers per generation) against the per-call kernels (marked
+gpu).  The grid loop replays the per-call plans' chunking and summation
+order, so every case must give the same bits: per-generation log, mean, Adam
+moments, gradient, best-so-far, sigma and lr.  The per-call path itself is
+checked against the oracle stage by stage elsewhere.
+
+Covered: the Rosenbrock D=1000, N=256 workload (the library's default path
+for it, with its four-lanes-per-block gradient plan), runs longer than one
+launch (256 generations), split gradient plans, evaluate chunkings (fewer
+and more chunks than the reduce kernel's 16 slices), one workgroup, more
+workgroups than pairs, several runs, and seeded random geometries of every
+benchmark problem, both shapings, both signs and the schedules."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+
+def _P():
+    import paper_2212_04180_amd as P
+    return P
+
+
+def _run(cfg, T):
+    P = _P()
+    es = P.ES(cfg)
+    path = es.run_path
+    log = es.run(T)
+    st = es.get_state()
+    bx, bf = es.best()
+    g = es.grad()
+    torch.cuda.synchronize()
+    es.sync()
+    out = [t.cpu().numpy() for t in (log, st["m"], st["m1"], st["v"], bx, bf, g)] + list(es.get_hparams())
+    t = es.t
+    es.close()
+    return path, out, t
+
+
+def _same(cfg, T):
+    pg, og, tg = _run(dataclasses.replace(cfg, plan_run_path=3), T)
+    pc, oc, tc = _run(dataclasses.replace(cfg, plan_run_path=1), T)
+    assert pg == 3 and pc == 1, (pg, pc)
+    assert tg == tc == T
+    names = ("log", "m", "m1", "v", "best_x", "best_f", "grad", "sigma", "lr")
+    for name, a, b in zip(names, og, oc):
+        assert a.tobytes() == b.tobytes(), name
+    return og
+
+
+def _rosenbrock(**kw):
+    from paper_2212_04180_amd import workloads
+    cfg, _ = workloads.get("rosenbrock_d1000")
+    return dataclasses.replace(cfg, flags=_P().FLAG_KEEP_GRAD, **kw)
+
+
+def test_default_paths_of_the_workloads():
+    from paper_2212_04180_amd import workloads
+    P = _P()
+    want = {"sphere_d16": 2, "rosenbrock_d1000": 3, "rastrigin_r1024": 2, "shifted_sphere_d1m": 1}
+    for name, path in want.items():
+        cfg, _ = workloads.get(name)
+        es = P.ES(cfg)
+        assert es.run_path == path, (name, es.run_path)
+        es.close()
+
+
+def test_rosenbrock_workload_equals_per_call():
+    og = _same(_rosenbrock(), 40)
+    assert np.all(np.isfinite(og[1]))
+    print("Rosenbrock D=1000 N=256: 40 generations, grid loop bit-identical to the per-call kernels", flush=True)
+
+
+def test_longer_than_one_launch():
+    # 300 generations: two launches (256 + 44), the Adam bias corrections of
+    # each in its own kernel arguments; schedules on
+    _same(_rosenbrock(sigma_decay=0.99, sigma_final=0.01, lr_decay=0.995, lr_final=0.001), 300)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(popsize=512, plan_tell_split=2),          # split gradient (two workgroups' sums added in split order)
+    dict(plan_eval_blocks=7),                      # uneven evaluate chunks (the last one short), 36 chunks
+    dict(plan_eval_blocks=1),                      # 250 chunks, 16 per reduce slice
+    dict(plan_grid_workgroups=1, num_dims=60),     # one workgroup: no exchange partner
+    dict(plan_grid_workgroups=8, popsize=64),      # 8 workgroups: two chunk slices each
+    dict(num_runs=3),                              # runs on grid.y, barriers and flags per run
+    dict(maximize=1, shaping=1),                   # raw keys, maximised
+])
+def test_plan_variants(kw):
+    _same(_rosenbrock(**kw), 12)
+
+
+def test_more_workgroups_than_pairs():
+    # 13 dims in four one-block chunks: four workgroups of one chunk each (the
+    # nine asked for are lowered to the chunk count), three pairs
+    P = _P()
+    for problem in (P.PROB_RASTRIGIN, P.PROB_ROSENBROCK):
+        cfg = P.ESConfig(num_dims=13, popsize=6, num_runs=2, sigma=0.3, lr=0.05, seed=77, init_lo=-2.0,
+                         init_hi=2.0, problem=problem, plan_grid_workgroups=9, flags=P.FLAG_KEEP_GRAD)
+        _same(cfg, 20)
+
+
+def _draw(i):
+    P = _P()
+    rng = np.random.default_rng(3000 + i)
+    while True:
+        D = int(np.exp(rng.uniform(0.0, np.log(3000.0))))
+        N = 2 * int(np.exp(rng.uniform(0.0, np.log(512.0))))
+        R = int(rng.integers(1, 4))
+        G = int(rng.choice([0, 0, 1, 2, 3, 4, 8, 16]))
+        kw = dict(num_dims=D, popsize=N, num_runs=R, sigma=float(rng.uniform(0.05, 0.5)),
+                  lr=float(rng.uniform(0.005, 0.05)), seed=int(rng.integers(0, 1 << 40)), init_lo=-2.0,
+                  init_hi=2.0, problem=int(rng.integers(P.PROB_SPHERE, P.PROB_RASTRIGIN + 1)),
+                  shaping=int(rng.integers(0, 2)), maximize=int(rng.integers(0, 2)), plan_grid_workgroups=G,
+                  plan_tell_split=int(rng.choice([0, 0, 0, 2])), flags=P.FLAG_KEEP_GRAD)
+        if rng.integers(0, 2):
+            kw.update(sigma_decay=0.97, sigma_final=0.05, lr_decay=0.95, lr_final=0.002)
+        cfg = P.ESConfig(**kw)
+        es = P.ES(dataclasses.replace(cfg, plan_run_path=3))
+        ok = es.run_path == 3  # the drawn plan fits the grid loop's LDS
+        es.close()
+        if ok:
+            return cfg
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_random_grid_loop_equals_per_call(i):
+    cfg = _draw(i)
+    print("case", i, cfg, flush=True)
+    _same(cfg, 9)

@@ -69,7 +69,7 @@ def _draw_fused(i):
     kw = dict(num_dims=D, popsize=N, num_runs=R, sigma=float(rng.uniform(0.05, 0.5)),
               lr=float(rng.uniform(0.005, 0.05)), seed=int(rng.integers(0, 1 << 40)), init_lo=-2.0, init_hi=2.0,
               problem=int(rng.integers(P.PROB_SPHERE, P.PROB_RASTRIGIN + 1)), shaping=int(rng.integers(0, 2)),
-              maximize=int(rng.integers(0, 2)))
+              maximize=int(rng.integers(0, 2)), flags=P.FLAG_KEEP_GRAD)
     if rng.integers(0, 2):
         kw.update(sigma_decay=0.97, sigma_final=0.05, lr_decay=0.95, lr_final=0.002)
     return P.ESConfig(**kw)
@@ -78,7 +78,8 @@ def _draw_fused(i):
 @pytest.mark.parametrize("i", range(16))
 def test_random_fused_loop_equals_per_call(i):
     """es_run through the fused loop (forced) and through the per-call kernels
-    give the same bits: log, mean, moments, best-so-far, sigma and lr."""
+    give the same bits: log, mean, moments, best-so-far, gradient, sigma and
+    lr."""
     import torch
     P = _P()
     cfg = _draw_fused(i)
@@ -90,6 +91,6 @@ def test_random_fused_loop_equals_per_call(i):
         st = es.get_state()
         bx, bf = es.best()
         torch.cuda.synchronize()
-        out[path] = [t.cpu().numpy() for t in (log, st["m"], st["m1"], st["v"], bx, bf)] + list(es.get_hparams())
+        out[path] = [t.cpu().numpy() for t in (log, st["m"], st["m1"], st["v"], bx, bf, es.grad())] + list(es.get_hparams())
     for a, b in zip(out["1"], out["2"]):
         np.testing.assert_array_equal(a, b)

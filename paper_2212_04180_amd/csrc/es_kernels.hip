@@ -157,17 +157,27 @@ __global__ void k_ask(const float* __restrict__ m, float* __restrict__ x, uint64
 template <int PROB>
 struct BlockTerm;
 
+// acc(s, x, shift, A): the running fp32 sum s plus one dim's term, each as
+// one explicit operation (an fma where the term is a square), so that the
+// rounding never depends on how the compiler contracts the code around it
 template <>
 struct BlockTerm<ES_PROB_SPHERE> {
-    static __device__ __forceinline__ float f(float x, float, float) { return x * x; }
+    static __device__ __forceinline__ float acc(float s, float x, float, float) { return fmaf(x, x, s); }
 };
 template <>
 struct BlockTerm<ES_PROB_SHIFTED_SPHERE> {
-    static __device__ __forceinline__ float f(float x, float s, float) { const float d = x - s; return d * d; }
+    static __device__ __forceinline__ float acc(float s, float x, float sh, float)
+    {
+        const float d = __fsub_rn(x, sh);
+        return fmaf(d, d, s);
+    }
 };
 template <>
 struct BlockTerm<ES_PROB_RASTRIGIN> {
-    static __device__ __forceinline__ float f(float x, float, float a) { return fmaf(x, x, -a * cos_2pi(x)); }
+    static __device__ __forceinline__ float acc(float s, float x, float, float a)
+    {
+        return __fadd_rn(s, fmaf(x, x, __fmul_rn(-a, cos_2pi(x))));
+    }
 };
 
 __device__ __forceinline__ float rosen_term(float xi, float xn)
@@ -220,8 +230,8 @@ __device__ __forceinline__ void block_terms(const float e[4], const float e2[4],
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const float g = SM != SM_SCALAR ? gv[k] : sg;
-            sp += BlockTerm<PROB>::f(fmaf(g, e[k], mv[k]), sv[k], ra);
-            sm += BlockTerm<PROB>::f(SM == SM_INDEP ? fmaf(g, e2[k], mv[k]) : fmaf(-g, e[k], mv[k]), sv[k], ra);
+            sp = BlockTerm<PROB>::acc(sp, fmaf(g, e[k], mv[k]), sv[k], ra);
+            sm = BlockTerm<PROB>::acc(sm, SM == SM_INDEP ? fmaf(g, e2[k], mv[k]) : fmaf(-g, e[k], mv[k]), sv[k], ra);
         }
     }
 }
@@ -234,9 +244,11 @@ template <int PROB, int V, int SM = SM_SCALAR>
 __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const float* __restrict__ pdata,
                                            uint32_t k0, uint32_t k1, uint32_t row, uint32_t t, int64_t b0,
                                            int64_t b1, int64_t D, float sg, float ra, double& accp, double& accm,
-                                           const float* __restrict__ gr = nullptr, uint32_t row2 = 0, int64_t mshift = 0)
+                                           const float* __restrict__ gr = nullptr, uint32_t row2 = 0, int64_t mshift = 0,
+                                           float4* __restrict__ nout = nullptr, int32_t nstride = 0)
 {
-    // the mean of dim d is mr[d - mshift] (a window of the row in LDS)
+    // the mean of dim d is mr[d - mshift] (a window of the row in LDS); with
+    // nout, the normals of block b0 + i are also stored at nout[i nstride]
     constexpr bool VEC = SM != SM_SCALAR;
     const int64_t nfull = D / 4;
     const int32_t nf = (int32_t)((b1 < nfull ? b1 : nfull) - b0);  // full blocks in [b0, b1) (may be <= 0)
@@ -272,6 +284,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         for (int k = 0; k < EVAL_FOLD; ++k) {
             float e[4], e2[4] = {0.f, 0.f, 0.f, 0.f};
             box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(bg + k), row, t, DOM_NOISE), e);
+            if (nout) nout[(int64_t)(i + k) * nstride] = make_float4(e[0], e[1], e[2], e[3]);
             if constexpr (SM == SM_INDEP)
                 box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(bg + k), row2, t, DOM_NOISE), e2);
             block_terms<PROB, SM>(e, e2, mv + 4 * k, PROB == ES_PROB_SHIFTED_SPHERE ? sv + 4 * k : zero4,
@@ -295,6 +308,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         }
         float e[4], e2[4] = {0.f, 0.f, 0.f, 0.f};
         box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
+        if (nout) nout[(int64_t)i * nstride] = make_float4(e[0], e[1], e[2], e[3]);
         if constexpr (SM == SM_INDEP) box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row2, t, DOM_NOISE), e2);
         float sp = 0.f, sm = 0.f;
         block_terms<PROB, SM>(e, e2, mv, sv, gv, sg, ra, L, sp, sm);
@@ -308,6 +322,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         const int nv = (int)(D - 4 * b);
         float e[4], e2[4] = {0.f, 0.f, 0.f, 0.f};
         box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
+        if (nout) nout[(b - b0) * nstride] = make_float4(e[0], e[1], e[2], e[3]);
         if constexpr (SM == SM_INDEP) box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row2, t, DOM_NOISE), e2);
         float sp = 0.f, sm = 0.f;
         for (int k = 0; k < nv; ++k) {
@@ -324,8 +339,8 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
                 L.xlm = xm;
             } else {
                 const float s = PROB == ES_PROB_SHIFTED_SPHERE ? pdata[4 * b + k] : 0.f;
-                sp += BlockTerm<PROB>::f(xp, s, ra);
-                sm += BlockTerm<PROB>::f(xm, s, ra);
+                sp = BlockTerm<PROB>::acc(sp, xp, s, ra);
+                sm = BlockTerm<PROB>::acc(sm, xm, s, ra);
             }
         }
         L.accp += (double)sp;
@@ -782,6 +797,40 @@ __device__ __forceinline__ void tell_slice(const float* __restrict__ wr, uint32_
         const float w = wr[p];
 #pragma unroll
         for (int k = 0; k < 4; ++k) a32[k] = fmaf(w, e[k], a32[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) a64[k] += (double)a32[k];
+}
+
+// tell_slice with the pairs' normals of the block given (eps[p], as the
+// evaluate stored them) instead of regenerated: the same groups of
+// TELL_GROUP pairs folded into fp64, then the rest.
+__device__ __forceinline__ void tell_slice_eps(const float* __restrict__ wr, const float4* __restrict__ eps, int32_t pb,
+                                               int32_t pe, double a64[4])
+{
+    int32_t p0 = pb;
+    for (; p0 + TELL_GROUP <= pe; p0 += TELL_GROUP) {
+        float a32[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < TELL_GROUP; ++q) {
+            const float4 e = eps[p0 + q];
+            const float w = wr[p0 + q];
+            a32[0] = fmaf(w, e.x, a32[0]);
+            a32[1] = fmaf(w, e.y, a32[1]);
+            a32[2] = fmaf(w, e.z, a32[2]);
+            a32[3] = fmaf(w, e.w, a32[3]);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) a64[k] += (double)a32[k];
+    }
+    float a32[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int32_t p = p0; p < pe; ++p) {
+        const float4 e = eps[p];
+        const float w = wr[p];
+        a32[0] = fmaf(w, e.x, a32[0]);
+        a32[1] = fmaf(w, e.y, a32[1]);
+        a32[2] = fmaf(w, e.z, a32[2]);
+        a32[3] = fmaf(w, e.w, a32[3]);
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) a64[k] += (double)a32[k];
@@ -1648,6 +1697,8 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
 // kernel's order and ranks them itself.  Rosenbrock's evaluate also reads the
 // last dim before each chunk, owned by workgroup w - 1, which publishes it
 // with the generation in one 64-bit word (a single location: no fence).
+// The evaluate keeps the normals of the own blocks in LDS and the gradient
+// reads them back instead of regenerating them (they never reach memory).
 // Chunking, reduction order and the gradient's
 // sub-slices, slices and splits are those of the handle's per-call plans, so
 // es_run gives the same bits on either path.
@@ -1799,14 +1850,17 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
     const int32_t ncw = w < nch ? (nch - w + G - 1) / G : 0;
     const int32_t nlb = ncw * bc;        // local blocks (the last chunk's may pass nb)
     const int32_t CW = 1 + 4 * bc;       // mean of one chunk in LDS: the dim before it, then its dims
-    // LDS: sub-slice sums (fp64) [S][ncw bc][4] | rank composites (u64) [N] |
-    // mean [ncw][CW] | m1, v [ncw bc][4] | partials [ncw][N] | fit [N] | y
-    // [N] | wf [P] | keys [N, from a 16-byte boundary] | table [N] | rank
-    // counts [ks][N] | pair bounds of the sub-slices [S + 1]
+    // LDS: sub-slice sums (fp64) [S][ncw bc][4] | rank composites (u64) [N,
+    // N padded to even] | normals (float4) [ncw bc][P + 1] | mean [ncw][CW]
+    // | m1, v [ncw bc][4] | partials [ncw][N] | fit [N] | y [N] | wf [P] |
+    // keys [N, from a 16-byte boundary] | table [N] | rank counts [ks][N] |
+    // pair bounds of the sub-slices [S + 1]
     const int64_t st = 4 * (int64_t)a.ncw * bc;  // stride of one sub-slice in red
+    const int32_t es = a.P + 1;                  // normals of one block: one float4 per pair (odd stride: no bank conflicts)
     double* red = smem;
     uint64_t* comp = reinterpret_cast<uint64_t*>(red + (int64_t)S * st);
-    float* ms = reinterpret_cast<float*>(comp + a.N);
+    float4* eps = reinterpret_cast<float4*>(comp + ((a.N + 1) & ~1));
+    float* ms = reinterpret_cast<float*>(eps + (int64_t)a.ncw * bc * es);
     float* m1s = ms + a.ncw * CW;
     float* vs = m1s + st;
     float* part = vs + st;
@@ -1908,7 +1962,8 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
                 const int64_t b0 = (int64_t)(w + G * ic) * bc, b1 = b0 + bc < nb ? b0 + bc : nb;
                 double accp, accm;
                 eval_chunk<PROB, LANES_BLOCK_AND_ROW>(ms + ic * CW + 1, a.pdata, k0, k1, (uint32_t)p, t, b0, b1, a.D,
-                                                      sigma, a.ra, accp, accm, nullptr, 0, 4 * b0);
+                                                      sigma, a.ra, accp, accm, nullptr, 0, 4 * b0,
+                                                      eps + (int64_t)ic * bc * es + p, es);
                 part[ic * a.N + p] = (float)accp;
                 part[ic * a.N + p + a.P] = (float)accm;
                 p += ev_dp;
@@ -1963,7 +2018,7 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
                 const int64_t b = (int64_t)(w + G * ic) * bc + (lb - ic * bc);
                 if (b < nb) {
                     double a64[4] = {0.0, 0.0, 0.0, 0.0};
-                    tell_slice<LANES_BLOCK_AND_ROW>(wf, k0, k1, (uint32_t)b, t, sbd[gs], sbd[gs + 1], a64);
+                    tell_slice_eps(wf, eps + (int64_t)lb * es, sbd[gs], sbd[gs + 1], a64);
 #pragma unroll
                     for (int k = 0; k < 4; ++k) red[gs * st + 4 * lb + k] = a64[k];
                 }
@@ -2466,12 +2521,13 @@ size_t grid_lds_bytes(const Geometry& g, const EvalPlan& e, const TellPlan& tp, 
 {
     const int64_t S = (int64_t)tp.ps * tp.nsplit * tp.sub;
     const int64_t ncw = (e.nchunks + G - 1) / G, st = 4 * ncw * e.bc;
-    // sub-slice sums | rank composites | mean windows | m1, v | partials | fit | y | wf | keys (from a 16-byte
-    // boundary) | table | counts | pair bounds
+    // sub-slice sums | rank composites | normals | mean windows | m1, v | partials | fit | y | wf | keys (from a
+    // 16-byte boundary) | table | counts | pair bounds
     size_t f32 = (size_t)(ncw * (1 + 4 * e.bc) + 2 * st + ncw * g.N + 2 * g.N + g.P);
     f32 = (f32 + 3) & ~(size_t)3;
     f32 += (size_t)((g.N + 3) & ~3) + (size_t)g.N + (size_t)grid_rank_splits(g.N) * g.N + (size_t)(S + 1);
-    return sizeof(double) * (size_t)(S * st + g.N) + sizeof(float) * f32;
+    const size_t eps = 16 * (size_t)(ncw * e.bc) * ((size_t)g.P + 1);  // float4 normals
+    return sizeof(double) * (size_t)(S * st + ((g.N + 1) & ~1)) + eps + sizeof(float) * f32;
 }
 
 bool grid_supported(const Geometry& g, const EvalPlan& e, const TellPlan& tp, const es_config& c, int32_t G)
@@ -2498,6 +2554,9 @@ hipError_t grid_max_resident(int64_t* out)
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     // every grid-loop launch stays within GRID_MAX_LDS of dynamic LDS
+    if (e == hipSuccess)
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_run_grid<ES_PROB_ROSENBROCK>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)GRID_MAX_LDS);
     if (e == hipSuccess)
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(&k_run_grid<ES_PROB_ROSENBROCK>),
                                                          GRID_WG, GRID_MAX_LDS);
@@ -2545,6 +2604,9 @@ hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan
     case ES_PROB_RASTRIGIN: k = reinterpret_cast<const void*>(&k_run_grid<ES_PROB_RASTRIGIN>); break;
     default: return hipErrorInvalidValue;
     }
+    // more than 64 KB of LDS per workgroup: allowed per kernel (cheap to repeat)
+    err = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GRID_MAX_LDS);
+    if (err != hipSuccess) return err;
     return hipLaunchCooperativeKernel(k, dim3((unsigned)G, (unsigned)g.R), dim3(GRID_WG), args, lds, s);
 }
 

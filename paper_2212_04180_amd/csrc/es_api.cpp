@@ -92,6 +92,7 @@ struct es_handle {
     uint32_t* grid_sync = nullptr;  // barrier counters, update flags, then the grid loop's error flag
     double* grid_accx = nullptr;    // the grid loop's slice sums
     uint64_t* grid_halo = nullptr;  // the grid loop's chunk-boundary words (Rosenbrock)
+    uint64_t* grid_yx = nullptr;    // the grid loop's shaped-weight words, then its rank-0 words
     // sort-based ranks (populations beyond RANK_MAX_N, or plan_rank_path 2)
     bool rank_sort = false;
     RankSortBuffers rs{};
@@ -307,7 +308,8 @@ void free_all(es_handle* h)
                     h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->mlp_scratch,
                     h->tell_part, h->hp[0], h->hp[1], h->pen, h->bfold, h->sig, h->vel, h->gbuf,
                     h->gpart, h->vpart, h->elite, h->cw, h->cmaC, h->zw, h->qd,
-                    h->rs.kin, h->rs.kout, h->rs.keys, h->rs.stats, h->rs.temp, h->grid_sync, h->grid_accx, h->grid_halo};
+                    h->rs.kin, h->rs.kout, h->rs.keys, h->rs.stats, h->rs.temp, h->grid_sync, h->grid_accx, h->grid_halo,
+                    h->grid_yx};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
 }
@@ -495,6 +497,9 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
         const size_t hw = (size_t)g.R * h->plan.nchunks;
         if (e == hipSuccess) e = dalloc(&h->grid_halo, hw);
         if (e == hipSuccess) e = hipMemsetAsync(h->grid_halo, 0, sizeof(uint64_t) * hw, h->stream);
+        const size_t yw = (size_t)g.R * g.N + g.R;
+        if (e == hipSuccess) e = dalloc(&h->grid_yx, yw);
+        if (e == hipSuccess) e = hipMemsetAsync(h->grid_yx, 0, sizeof(uint64_t) * yw, h->stream);
     }
     const bool pgpe_snes = cfg->strategy == ES_STRAT_PGPE || cfg->strategy == ES_STRAT_SNES;
     const bool cma = cfg->strategy == ES_STRAT_SEP_CMA;
@@ -689,7 +694,8 @@ es_status es_run(es_handle* h, int32_t T, float* log)
                 ES_HIP(h, launch_run_grid(h->g, h->cfg, h->plan, h->tell, h->grid_g, (uint32_t)h->t, Tc,
                                           adam_consts(h->cfg, h->t), bcorr, h->m, h->m1, h->v, h->grad, h->best_x,
                                           h->best_okey, h->best_f, h->pdata, h->table, lg, h->grid_accx,
-                                          h->grid_halo, h->grid_sync,
+                                          h->grid_yx, h->grid_yx + (size_t)h->g.R * h->g.N, h->grid_halo,
+                                          h->grid_sync,
                                           h->hp[h->hp_cur], h->stream),
                        "grid generation loop");
             h->t += Tc;

@@ -155,8 +155,9 @@ hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPla
 
 // Grid loop: T generations of each run on a cooperative launch of G
 // workgroups per run, in the per-call plans' summation order.  accx: [2][R]
-// [RED_SLICES][N] fp64 slice sums; halo: [R][nchunks] words (Rosenbrock's
-// chunk boundaries, tagged by generation, never cleared).  sync:
+// [RED_SLICES][N] fp64 slice sums; yx: [R][N] shaped weights, bestx: [R] the
+// rank-0 members, halo: [R][nchunks] Rosenbrock's chunk boundaries (64-bit
+// words tagged by generation: zero at set-up, never cleared).  sync:
 // grid_sync_words uint32 -- [R] barrier counters (cleared by each launch),
 // then one error flag, set when a wait gave up (only a wrong kernel can make
 // it).
@@ -174,8 +175,8 @@ hipError_t grid_max_resident(int64_t* out);  // workgroups of the grid loop the 
 hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan& e, const TellPlan& tp, int32_t G,
                            uint32_t t0, int32_t T, const AdamConsts& ac, const float (*bcorr)[2], float* m, float* m1,
                            float* v, float* grad, float* best_x, uint32_t* best_okey, float* best_f,
-                           const float* pdata, const float* table, float* log, double* accx, uint64_t* halo,
-                           uint32_t* sync, float* hp, hipStream_t s);
+                           const float* pdata, const float* table, float* log, double* accx, uint64_t* yx,
+                           uint64_t* bestx, uint64_t* halo, uint32_t* sync, float* hp, hipStream_t s);
 
 // Neuroevolution problem (64-256-256-16 MLP vs a teacher).
 constexpr int64_t MLP_NUM_PARAMS = 86544;

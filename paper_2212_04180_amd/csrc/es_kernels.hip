@@ -249,6 +249,10 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
 {
     // the mean of dim d is mr[d - mshift] (a window of the row in LDS); with
     // nout, the normals of block b0 + i are also stored at nout[i nstride]
+    auto normals = [&](int64_t b, float e[4]) {
+        box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
+        if (nout) nout[(b - b0) * nstride] = make_float4(e[0], e[1], e[2], e[3]);
+    };
     constexpr bool VEC = SM != SM_SCALAR;
     const int64_t nfull = D / 4;
     const int32_t nf = (int32_t)((b1 < nfull ? b1 : nfull) - b0);  // full blocks in [b0, b1) (may be <= 0)
@@ -283,8 +287,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
 #pragma unroll
         for (int k = 0; k < EVAL_FOLD; ++k) {
             float e[4], e2[4] = {0.f, 0.f, 0.f, 0.f};
-            box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(bg + k), row, t, DOM_NOISE), e);
-            if (nout) nout[(int64_t)(i + k) * nstride] = make_float4(e[0], e[1], e[2], e[3]);
+            normals(bg + k, e);
             if constexpr (SM == SM_INDEP)
                 box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)(bg + k), row2, t, DOM_NOISE), e2);
             block_terms<PROB, SM>(e, e2, mv + 4 * k, PROB == ES_PROB_SHIFTED_SPHERE ? sv + 4 * k : zero4,
@@ -307,8 +310,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
             for (int q = 0; q < 4; ++q) sv[q] = pdata[4 * b + q];
         }
         float e[4], e2[4] = {0.f, 0.f, 0.f, 0.f};
-        box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
-        if (nout) nout[(int64_t)i * nstride] = make_float4(e[0], e[1], e[2], e[3]);
+        normals(b, e);
         if constexpr (SM == SM_INDEP) box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row2, t, DOM_NOISE), e2);
         float sp = 0.f, sm = 0.f;
         block_terms<PROB, SM>(e, e2, mv, sv, gv, sg, ra, L, sp, sm);
@@ -321,8 +323,7 @@ __device__ __forceinline__ void eval_chunk(const float* __restrict__ mr, const f
         const int64_t b = nfull;
         const int nv = (int)(D - 4 * b);
         float e[4], e2[4] = {0.f, 0.f, 0.f, 0.f};
-        box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row, t, DOM_NOISE), e);
-        if (nout) nout[(b - b0) * nstride] = make_float4(e[0], e[1], e[2], e[3]);
+        normals(b, e);
         if constexpr (SM == SM_INDEP) box_muller4(philox4x32_10<V>(k0, k1, (uint32_t)b, row2, t, DOM_NOISE), e2);
         float sp = 0.f, sm = 0.f;
         for (int k = 0; k < nv; ++k) {
@@ -1694,7 +1695,8 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
 // mean, m1 and v staying in LDS.  Per generation one exchange: the members'
 // slice sums (fp64, two buffers by generation parity) behind one grid
 // barrier; every workgroup then adds them into all N fitnesses in the reduce
-// kernel's order and ranks them itself.  Rosenbrock's evaluate also reads the
+// kernel's order, and ranks its share of them against all (the shaped
+// weights exchanged as tagged words, below).  Rosenbrock's evaluate also reads the
 // last dim before each chunk, owned by workgroup w - 1, which publishes it
 // with the generation in one 64-bit word (a single location: no fence).
 // The evaluate keeps the normals of the own blocks in LDS and the gradient
@@ -1714,6 +1716,8 @@ struct GridArgs {
     const float* table;
     float* log;              // [T][R] or null
     double* accx;            // [2][R][RED_SLICES][N] slice sums of the members
+    uint64_t* yx;            // [R][N] (t + 1) << 32 | shaped weight of member j in generation t
+    uint64_t* bestx;         // [R] (t + 1) << 32 | the rank-0 member of generation t
     uint64_t* halo;          // [R][nchunks] (t + 1) << 32 | the last dim of chunk c after the update of generation t
     uint32_t* bar;           // [R] arrivals at the run's barriers, zero at launch
     uint32_t* err;           // set nonzero when a wait gives up
@@ -1725,7 +1729,6 @@ struct GridArgs {
     int64_t bc, nchunks;
     int32_t ps, nsplit, sub;  // the per-call gradient plan
     int32_t ncw;              // most chunks of one workgroup
-    int32_t ks;               // key ranges of the rank count
     float ra;
     double add;
     int32_t maximize, raw;
@@ -1769,73 +1772,79 @@ __device__ __forceinline__ bool grid_wait(uint32_t* cnt, uint32_t target, uint32
     return *ok != 0;
 }
 
-// Key ranges the rank count splits into: every wave of the workgroup takes
-// one (member chunk of 64, key range) task while there are fewer member
-// chunks than waves.
-__host__ __device__ __forceinline__ int32_t grid_rank_splits(int32_t N)
+// Wait until the tagged word at src carries tag (bounded like grid_wait);
+// false if the wait gave up.
+__device__ __forceinline__ bool wait_word(const uint64_t* src, uint32_t tag, uint32_t* err, uint64_t& word)
 {
-    const int32_t mc = (N + 63) / 64, nw = GRID_WG / 64;
-    const int32_t ks = mc < nw ? nw / mc : 1;
-    return ks;
+    for (uint32_t spins = 0;; ++spins) {
+        word = __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((uint32_t)(word >> 32) == tag) return true;
+        __builtin_amdgcn_s_sleep(1);
+        if (spins >= GRID_SPIN_LIMIT || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+            __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return false;
+        }
+    }
 }
 
-// Centered ranks of all N members (every workgroup alike), the folded
-// weights wf[p] = y_p - y_{p+P}, the best-so-far and (logp not null) the
-// generation's best fitness.  comp[k] = key_k << 32 | k, so member k sorts
-// before j exactly when comp[k] < comp[j] (ties by index).  Each wave
-// counts, for 64 members, the composites of one key range below each of
-// theirs, reading every composite at one address for the whole wave.  cnt:
-// [ks][N].
-__device__ __forceinline__ void rank_grid(const uint64_t* comp, const uint32_t* keys, const float* fit,
-                                          const float* tab, float* y, float* wf, int32_t* cnt, int32_t N, int32_t P,
-                                          int32_t ks, int32_t raw, int32_t maximize, LoopBest& bst, float* logp)
+// Centered ranks, shared out: this workgroup ranks the members [N w / G,
+// N (w+1) / G) against all N composites comp[k] = key_k << 32 | k (member k
+// sorts before j exactly when comp[k] < comp[j]; one wave per member, a wave
+// sum of the lanes' counts) and publishes their shaped weights as words
+// tag << 32 | y_j, and the rank-0 member as tag << 32 | j in its own word.
+// Every workgroup then reads all N weights (and the best) back: each word is
+// one location, so no fence is needed.  Then the folded weights wf[p] = y_p
+// - y_{p+P}, the best-so-far and (logp not null) the generation's best
+// fitness.  false if a wait gave up.
+__device__ __forceinline__ bool rank_exchange(const uint64_t* comp, const uint32_t* keys, const float* fit,
+                                              const float* tab, float* y, float* wf, int32_t N, int32_t P, int32_t raw,
+                                              int32_t maximize, uint32_t tag, uint64_t* yx, uint64_t* bestx, int32_t w,
+                                              int32_t G, uint32_t* err, LoopBest& bst, float* logp, int32_t* ok)
 {
     const int32_t wave = __builtin_amdgcn_readfirstlane((int32_t)(threadIdx.x / 64)), lane = threadIdx.x % 64;
-    const int32_t tasks = (N + 63) / 64 * ks;
-    for (int32_t task = wave; task < tasks; task += GRID_WG / 64) {
-        const int32_t mc = task / ks, kr = task - mc * ks;
-        const int32_t j = mc * 64 + lane;
-        const int32_t k0 = (N * kr) / ks, k1 = (N * (kr + 1)) / ks;  // N ks < 2^31
-        // lanes past N compare against 0: nothing sorts before it
-        const uint64_t cj = j < N ? comp[j] : 0;
+    const int32_t j0 = (int32_t)(((int64_t)N * w) / G), j1 = (int32_t)(((int64_t)N * (w + 1)) / G);
+    for (int32_t j = j0 + wave; j < j1; j += GRID_WG / 64) {
+        const uint64_t cj = comp[j];
         int32_t rk = 0;
-        int32_t k = k0;
-        for (; k < k1 && (k & 1); ++k) rk += comp[k] < cj;
-        // eight composites per step: four reads in flight, two counts
-        for (; k + 8 <= k1; k += 8) {
-            ulonglong2 c2[4];
+        for (int32_t k = lane; k < N; k += 64) rk += comp[k] < cj;
 #pragma unroll
-            for (int u = 0; u < 4; ++u) c2[u] = *reinterpret_cast<const ulonglong2*>(comp + k + 2 * u);
-            int32_t ra = 0, rb = 0;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                ra += c2[u].x < cj;
-                rb += c2[u].y < cj;
-            }
-            rk += ra + rb;
+        for (int off = 32; off > 0; off >>= 1) rk += __shfl_xor(rk, off);
+        if (lane == 0) {
+            const float yj = raw ? (maximize ? -fit[j] : fit[j]) : tab[rk];
+            __hip_atomic_store(yx + j, ((uint64_t)tag << 32) | __float_as_uint(yj), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+            if (rk == 0)
+                __hip_atomic_store(bestx, ((uint64_t)tag << 32) | (uint32_t)j, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
         }
-        for (; k < k1; ++k) rk += comp[k] < cj;
-        if (j < N) cnt[kr * N + j] = rk;
     }
+    if (threadIdx.x == 0) *ok = 1;
     __syncthreads();
-    for (int32_t j = threadIdx.x; j < N; j += GRID_WG) {
-        int32_t rk = 0;
-        for (int32_t kr = 0; kr < ks; ++kr) rk += cnt[kr * N + j];
-        y[j] = raw ? (maximize ? -fit[j] : fit[j]) : tab[rk];
-        if (rk == 0) {
-            if (logp) *logp = fit[j];
-            const uint32_t K = keys[j];
+    for (int32_t j = threadIdx.x; j <= N; j += GRID_WG) {
+        uint64_t word;
+        if (!wait_word(j < N ? yx + j : bestx, tag, err, word)) {
+            *ok = 0;
+            continue;
+        }
+        if (j < N) {
+            y[j] = __uint_as_float((uint32_t)word);
+        } else {
+            const int32_t jb = (int32_t)(uint32_t)word;
+            if (logp) *logp = fit[jb];
+            const uint32_t K = keys[jb];
             if (K < bst.k) {
                 bst.k = K;
-                bst.fv = fit[j];
-                bst.j = j;
+                bst.fv = fit[jb];
+                bst.j = jb;
             } else {
                 bst.j = -1;
             }
         }
     }
     __syncthreads();
+    if (!*ok) return false;
     for (int32_t p = threadIdx.x; p < P; p += GRID_WG) wf[p] = y[p] - y[p + P];
+    return true;
 }
 
 template <int PROB>
@@ -1853,8 +1862,8 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
     // LDS: sub-slice sums (fp64) [S][ncw bc][4] | rank composites (u64) [N,
     // N padded to even] | normals (float4) [ncw bc][P + 1] | mean [ncw][CW]
     // | m1, v [ncw bc][4] | partials [ncw][N] | fit [N] | y [N] | wf [P] |
-    // keys [N, from a 16-byte boundary] | table [N] | rank counts [ks][N] |
-    // pair bounds of the sub-slices [S + 1]
+    // keys [N, from a 16-byte boundary] | table [N] | pair bounds of the
+    // sub-slices [S + 1]
     const int64_t st = 4 * (int64_t)a.ncw * bc;  // stride of one sub-slice in red
     const int32_t es = a.P + 1;                  // normals of one block: one float4 per pair (odd stride: no bank conflicts)
     double* red = smem;
@@ -1869,8 +1878,7 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
     float* wf = y + a.N;
     uint32_t* keys = reinterpret_cast<uint32_t*>(ms + ((a.ncw * CW + 2 * st + a.ncw * a.N + 2 * a.N + a.P + 3) & ~(int64_t)3));
     float* tab = reinterpret_cast<float*>(keys + ((a.N + 3) & ~3));
-    int32_t* cnt = reinterpret_cast<int32_t*>(tab + a.N);
-    int32_t* sbd = cnt + a.ks * a.N;  // sub-slice gs takes the pairs [sbd[gs], sbd[gs + 1])
+    int32_t* sbd = reinterpret_cast<int32_t*>(tab + a.N);  // sub-slice gs takes the pairs [sbd[gs], sbd[gs + 1])
     __shared__ LoopBest bst;
     __shared__ int32_t ok;
 
@@ -1938,24 +1946,16 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
                     h = a.m[goff + 4 * (int64_t)c * bc - 1];
                 } else if (c > 0) {
                     uint64_t word;
-                    for (uint32_t spins = 0;; ++spins) {
-                        word = __hip_atomic_load(halo + c - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        if ((uint32_t)(word >> 32) == t) break;
-                        __builtin_amdgcn_s_sleep(1);
-                        if (spins >= GRID_SPIN_LIMIT || __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-                            __hip_atomic_fetch_or(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                            ok = 0;
-                            break;
-                        }
-                    }
-                    h = __uint_as_float((uint32_t)word);
+                    if (wait_word(halo + c - 1, t, a.err, word)) h = __uint_as_float((uint32_t)word);
+                    else ok = 0;
                 }
                 ms[ic * CW] = h;
             }
             __syncthreads();
             if (!ok) return;
         }
-        // evaluate: items (pair, own chunk)
+        // evaluate: items (pair, own chunk); the normals of the own blocks
+        // also go to LDS for the gradient
         {
             int32_t p = ev_p0, ic = ev_c0;
             for (int32_t i = threadIdx.x; i < ev_items; i += GRID_WG) {
@@ -2005,8 +2005,10 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
             comp[j] = ((uint64_t)K << 32) | (uint32_t)j;
         }
         __syncthreads();
-        rank_grid(comp, keys, fit, tab, y, wf, cnt, a.N, a.P, a.ks, a.raw, a.maximize, bst,
-                  (w == 0 && a.log) ? a.log + (int64_t)it * a.R + r : nullptr);
+        if (!rank_exchange(comp, keys, fit, tab, y, wf, a.N, a.P, a.raw, a.maximize, t + 1, a.yx + (int64_t)r * a.N,
+                           a.bestx + r, w, G, a.err, bst, (w == 0 && a.log) ? a.log + (int64_t)it * a.R + r : nullptr,
+                           &ok))
+            return;
         __syncthreads();
         // gradient of the own blocks: items (block, sub-slice gs), gs
         // numbering the pairs' sub-slices as the per-call kernel does:
@@ -2522,10 +2524,10 @@ size_t grid_lds_bytes(const Geometry& g, const EvalPlan& e, const TellPlan& tp, 
     const int64_t S = (int64_t)tp.ps * tp.nsplit * tp.sub;
     const int64_t ncw = (e.nchunks + G - 1) / G, st = 4 * ncw * e.bc;
     // sub-slice sums | rank composites | normals | mean windows | m1, v | partials | fit | y | wf | keys (from a
-    // 16-byte boundary) | table | counts | pair bounds
+    // 16-byte boundary) | table | pair bounds
     size_t f32 = (size_t)(ncw * (1 + 4 * e.bc) + 2 * st + ncw * g.N + 2 * g.N + g.P);
     f32 = (f32 + 3) & ~(size_t)3;
-    f32 += (size_t)((g.N + 3) & ~3) + (size_t)g.N + (size_t)grid_rank_splits(g.N) * g.N + (size_t)(S + 1);
+    f32 += (size_t)((g.N + 3) & ~3) + (size_t)g.N + (size_t)(S + 1);
     const size_t eps = 16 * (size_t)(ncw * e.bc) * ((size_t)g.P + 1);  // float4 normals
     return sizeof(double) * (size_t)(S * st + ((g.N + 1) & ~1)) + eps + sizeof(float) * f32;
 }
@@ -2567,14 +2569,14 @@ hipError_t grid_max_resident(int64_t* out)
 hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan& e, const TellPlan& tp, int32_t G,
                            uint32_t t0, int32_t T, const AdamConsts& ac, const float (*bcorr)[2], float* m, float* m1,
                            float* v, float* grad, float* best_x, uint32_t* best_okey, float* best_f,
-                           const float* pdata, const float* table, float* log, double* accx, uint64_t* halo,
-                           uint32_t* sync, float* hp, hipStream_t s)
+                           const float* pdata, const float* table, float* log, double* accx, uint64_t* yx,
+                           uint64_t* bestx, uint64_t* halo, uint32_t* sync, float* hp, hipStream_t s)
 {
     if (T < 1 || T > FUSED_MAX_T || G < 1 || G > GRID_MAX_G) return hipErrorInvalidValue;
     if (!grid_supported(g, e, tp, c, G)) return hipErrorInvalidValue;
     GridArgs a;
     a.m = m; a.m1 = m1; a.v = v; a.grad = grad; a.best_x = best_x; a.best_okey = best_okey; a.best_f = best_f;
-    a.pdata = pdata; a.table = table; a.log = log; a.accx = accx; a.halo = halo;
+    a.pdata = pdata; a.table = table; a.log = log; a.accx = accx; a.yx = yx; a.bestx = bestx; a.halo = halo;
     a.bar = sync; a.err = sync + grid_sync_words(g) - 1;
     a.ac = ac;
     for (int32_t i = 0; i < T; ++i) {
@@ -2583,7 +2585,7 @@ hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan
     }
     a.seed = c.seed; a.t0 = t0; a.T = T; a.D = g.D; a.nb = g.nb; a.N = g.N; a.P = g.P; a.R = g.R;
     a.bc = e.bc; a.nchunks = e.nchunks; a.ps = tp.ps; a.nsplit = tp.nsplit; a.sub = tp.sub;
-    a.ncw = (int32_t)((e.nchunks + G - 1) / G); a.ks = grid_rank_splits(g.N);
+    a.ncw = (int32_t)((e.nchunks + G - 1) / G);
     a.ra = c.rastrigin_a;
     a.add = c.problem == ES_PROB_RASTRIGIN ? (double)c.rastrigin_a * (double)g.D : 0.0;
     a.maximize = c.maximize; a.raw = c.shaping == ES_SHAPE_RAW;

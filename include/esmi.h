@@ -352,9 +352,9 @@ es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes);
 
 /* Wait for all work enqueued by this handle (synchronous).  Not defined by
  * the paper.  Also reports ES_ERR_HIP if a grid-loop launch of es_run ended
- * early because a barrier wait gave up (its workgroups are resident together
- * under a cooperative launch, so only a library fault can cause that; the
- * state is then not valid). */
+ * early because a wait for another workgroup's values gave up (its
+ * workgroups are resident together under a cooperative launch, so only a
+ * library fault can cause that; the state is then not valid). */
 es_status es_sync(es_handle* h);
 
 /* Current generation counter t (host value; no device work). */

@@ -89,10 +89,9 @@ struct es_handle {
     int64_t teacher_t = -1;       // generation whose inputs and teacher outputs are in mlp_scratch
     int run_path = 0;  // 0 auto, 1 per-call kernels, 2 fused loop, 3 grid loop
     int32_t grid_g = 0;             // workgroups per run of the grid loop (0: the grid loop does not apply)
-    uint32_t* grid_sync = nullptr;  // barrier counters, update flags, then the grid loop's error flag
-    double* grid_accx = nullptr;    // the grid loop's slice sums
-    uint64_t* grid_halo = nullptr;  // the grid loop's chunk-boundary words (Rosenbrock)
-    uint64_t* grid_yx = nullptr;    // the grid loop's shaped-weight words, then its rank-0 words
+    uint64_t* grid_words = nullptr;  // the grid loop's tagged words
+    uint32_t* grid_err = nullptr;    // the grid loop's error flag
+    uint32_t grid_seq = 0;           // sequence number of the last grid-loop launch
     // sort-based ranks (populations beyond RANK_MAX_N, or plan_rank_path 2)
     bool rank_sort = false;
     RankSortBuffers rs{};
@@ -308,8 +307,7 @@ void free_all(es_handle* h)
                     h->y, h->rank, h->wfold, h->fit, h->partial, h->pdata, h->mlp_scratch,
                     h->tell_part, h->hp[0], h->hp[1], h->pen, h->bfold, h->sig, h->vel, h->gbuf,
                     h->gpart, h->vpart, h->elite, h->cw, h->cmaC, h->zw, h->qd,
-                    h->rs.kin, h->rs.kout, h->rs.keys, h->rs.stats, h->rs.temp, h->grid_sync, h->grid_accx, h->grid_halo,
-                    h->grid_yx};
+                    h->rs.kin, h->rs.kout, h->rs.keys, h->rs.stats, h->rs.temp, h->grid_words, h->grid_err};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
 }
@@ -489,17 +487,12 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
     if (e == hipSuccess && h->tell.nsplit > 1)
         e = dalloc(&h->tell_part, tell_part_elems(g, h->tell, cfg->strategy));
     if (e == hipSuccess && h->grid_g > 0) {
-        const size_t words = grid_sync_words(g);
-        e = dalloc(&h->grid_sync, words);
-        if (e == hipSuccess) e = hipMemsetAsync(h->grid_sync, 0, sizeof(uint32_t) * words, h->stream);
-        if (e == hipSuccess) e = dalloc(&h->grid_accx, grid_accx_elems(g));
-        // the words' tags are t + 1 >= 1 once written: 0 matches no generation
-        const size_t hw = (size_t)g.R * h->plan.nchunks;
-        if (e == hipSuccess) e = dalloc(&h->grid_halo, hw);
-        if (e == hipSuccess) e = hipMemsetAsync(h->grid_halo, 0, sizeof(uint64_t) * hw, h->stream);
-        const size_t yw = (size_t)g.R * g.N + g.R;
-        if (e == hipSuccess) e = dalloc(&h->grid_yx, yw);
-        if (e == hipSuccess) e = hipMemsetAsync(h->grid_yx, 0, sizeof(uint64_t) * yw, h->stream);
+        // zero tags: no launch waits for tag 0
+        const size_t nw = grid_word_count(g, h->plan);
+        e = dalloc(&h->grid_words, nw);
+        if (e == hipSuccess) e = hipMemsetAsync(h->grid_words, 0, sizeof(uint64_t) * nw, h->stream);
+        if (e == hipSuccess) e = dalloc(&h->grid_err, 1);
+        if (e == hipSuccess) e = hipMemsetAsync(h->grid_err, 0, sizeof(uint32_t), h->stream);
     }
     const bool pgpe_snes = cfg->strategy == ES_STRAT_PGPE || cfg->strategy == ES_STRAT_SNES;
     const bool cma = cfg->strategy == ES_STRAT_SEP_CMA;
@@ -690,14 +683,16 @@ es_status es_run(es_handle* h, int32_t T, float* log)
                                            h->table,
                                            lg, h->hp[h->hp_cur], h->stream),
                        "fused generation loop");
-            else
+            else {
+                // a sequence number the previous launch did not use, so that
+                // none of its words carries a tag this launch waits for
+                h->grid_seq = h->grid_seq % 0xFFFFFFu + 1;
                 ES_HIP(h, launch_run_grid(h->g, h->cfg, h->plan, h->tell, h->grid_g, (uint32_t)h->t, Tc,
                                           adam_consts(h->cfg, h->t), bcorr, h->m, h->m1, h->v, h->grad, h->best_x,
-                                          h->best_okey, h->best_f, h->pdata, h->table, lg, h->grid_accx,
-                                          h->grid_yx, h->grid_yx + (size_t)h->g.R * h->g.N, h->grid_halo,
-                                          h->grid_sync,
-                                          h->hp[h->hp_cur], h->stream),
+                                          h->best_okey, h->best_f, h->pdata, h->table, lg, h->grid_words, h->grid_seq,
+                                          h->grid_err, h->hp[h->hp_cur], h->stream),
                        "grid generation loop");
+            }
             h->t += Tc;
             done += Tc;
         }
@@ -946,12 +941,10 @@ es_status es_sync(es_handle* h)
 {
     if (!h) return ES_ERR_ARG;
     ES_HIP(h, hipStreamSynchronize(h->stream), "stream synchronize");
-    if (h->grid_sync) {
+    if (h->grid_err) {
         uint32_t flag = 0;
-        ES_HIP(h, hipMemcpy(&flag, h->grid_sync + grid_sync_words(h->g) - 1, sizeof(flag),
-                            hipMemcpyDeviceToHost),
-               "grid loop flag");
-        if (flag) return fail(h, ES_ERR_HIP, "grid generation loop: a barrier wait gave up; the state is not valid");
+        ES_HIP(h, hipMemcpy(&flag, h->grid_err, sizeof(flag), hipMemcpyDeviceToHost), "grid loop flag");
+        if (flag) return fail(h, ES_ERR_HIP, "grid generation loop: a wait gave up; the state is not valid");
     }
     return ES_OK;
 }

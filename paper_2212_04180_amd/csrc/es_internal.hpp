@@ -154,29 +154,31 @@ hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPla
                             float* log, float* hp, hipStream_t s);
 
 // Grid loop: T generations of each run on a cooperative launch of G
-// workgroups per run, in the per-call plans' summation order.  accx: [2][R]
-// [RED_SLICES][N] fp64 slice sums; yx: [R][N] shaped weights, bestx: [R] the
-// rank-0 members, halo: [R][nchunks] Rosenbrock's chunk boundaries (64-bit
-// words tagged by generation: zero at set-up, never cleared).  sync:
-// grid_sync_words uint32 -- [R] barrier counters (cleared by each launch),
-// then one error flag, set when a wait gave up (only a wrong kernel can make
-// it).
+// workgroups per run, in the per-call plans' summation order.  words:
+// grid_word_count tagged 64-bit words (slice sums, fitnesses, shaped weights,
+// rank-0 members, Rosenbrock's chunk boundaries), zero at set-up and never
+// cleared; seq: the launch's sequence number in [1, 2^24), different from
+// the previous launch's, so that no word left by an earlier launch carries a
+// tag this one waits for; err: set when a wait gave up (only a wrong kernel
+// can make it).
 constexpr int32_t GRID_MAX_G = 16;
 constexpr int32_t GRID_MAX_N = 8192;            // every workgroup ranks the run's members
 constexpr size_t GRID_MAX_LDS = 144 * 1024;     // of gfx950's 160 KB per workgroup
 // es_run takes the grid loop by default up to this many pair-blocks (R P nb)
 constexpr int64_t GRID_DEFAULT_WORK = 131072;
 int32_t grid_workgroups(const Geometry& g, const EvalPlan& e, int32_t want);  // want 0: the library's choice
-inline size_t grid_sync_words(const Geometry& g) { return (size_t)g.R + 1; }
-inline size_t grid_accx_elems(const Geometry& g) { return 2 * (size_t)g.R * 16 * (size_t)g.N; }
+inline size_t grid_word_count(const Geometry& g, const EvalPlan& e)
+{
+    return (size_t)g.R * ((size_t)16 * g.N * 2 + 2 * (size_t)g.N + 1 + (size_t)e.nchunks);
+}
 size_t grid_lds_bytes(const Geometry& g, const EvalPlan& e, const TellPlan& tp, int32_t G);
 bool grid_supported(const Geometry& g, const EvalPlan& e, const TellPlan& tp, const es_config& c, int32_t G);
 hipError_t grid_max_resident(int64_t* out);  // workgroups of the grid loop the device holds at once
 hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan& e, const TellPlan& tp, int32_t G,
                            uint32_t t0, int32_t T, const AdamConsts& ac, const float (*bcorr)[2], float* m, float* m1,
                            float* v, float* grad, float* best_x, uint32_t* best_okey, float* best_f,
-                           const float* pdata, const float* table, float* log, double* accx, uint64_t* yx,
-                           uint64_t* bestx, uint64_t* halo, uint32_t* sync, float* hp, hipStream_t s);
+                           const float* pdata, const float* table, float* log, uint64_t* words, uint32_t seq,
+                           uint32_t* err, float* hp, hipStream_t s);
 
 // Neuroevolution problem (64-256-256-16 MLP vs a teacher).
 constexpr int64_t MLP_NUM_PARAMS = 86544;

@@ -1692,18 +1692,24 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
 // kernel (slice q holds the chunks q, q + RED_SLICES, ...; G divides
 // RED_SLICES, or every slice is one chunk), and for those chunks' Philox
 // blocks it evaluates every pair, forms the gradient and the update, its
-// mean, m1 and v staying in LDS.  Per generation one exchange: the members'
-// slice sums (fp64, two buffers by generation parity) behind one grid
-// barrier; every workgroup then adds them into all N fitnesses in the reduce
-// kernel's order, and ranks its share of them against all (the shaped
-// weights exchanged as tagged words, below).  Rosenbrock's evaluate also reads the
-// last dim before each chunk, owned by workgroup w - 1, which publishes it
-// with the generation in one 64-bit word (a single location: no fence).
-// The evaluate keeps the normals of the own blocks in LDS and the gradient
-// reads them back instead of regenerating them (they never reach memory).
-// Chunking, reduction order and the gradient's
-// sub-slices, slices and splits are those of the handle's per-call plans, so
-// es_run gives the same bits on either path.
+// mean, m1 and v staying in LDS.  The evaluate keeps the normals of the own
+// blocks in LDS and the gradient reads them back instead of regenerating
+// them (they never reach memory).
+//
+// Workgroups exchange values only as 64-bit words that carry a tag (the
+// launch's sequence number and the generation) beside 32 bits of value: a
+// reader waits until a word carries the tag it expects, and since each word
+// is one location, no fence or barrier is needed.  Per generation: the
+// members' fp64 slice sums (two words each, high and low half), from which
+// workgroup w forms the fitness of members [N w / G, N (w+1) / G) in the
+// reduce kernel's order; all fitnesses; the shaped weights and the rank-0
+// member (each workgroup ranks its members against all N); and Rosenbrock's
+// one dim before each chunk, owned by workgroup w - 1.  A word is written
+// again only after every reader of its last value has used it, because each
+// generation's words depend on every workgroup's reads of the one before.
+// Chunking, reduction order and the gradient's sub-slices, slices and splits
+// are those of the handle's per-call plans, so es_run gives the same bits on
+// either path.
 struct GridArgs {
     float* m;
     float* m1;
@@ -1715,12 +1721,13 @@ struct GridArgs {
     const float* pdata;
     const float* table;
     float* log;              // [T][R] or null
-    double* accx;            // [2][R][RED_SLICES][N] slice sums of the members
-    uint64_t* yx;            // [R][N] (t + 1) << 32 | shaped weight of member j in generation t
-    uint64_t* bestx;         // [R] (t + 1) << 32 | the rank-0 member of generation t
-    uint64_t* halo;          // [R][nchunks] (t + 1) << 32 | the last dim of chunk c after the update of generation t
-    uint32_t* bar;           // [R] arrivals at the run's barriers, zero at launch
+    uint64_t* sx;            // [R][RED_SLICES][N][2] tag | high, tag | low half of member j's slice sum q
+    uint64_t* fx;            // [R][N] tag | fitness of member j
+    uint64_t* yx;            // [R][N] tag | shaped weight of member j
+    uint64_t* bestx;         // [R] tag | the rank-0 member
+    uint64_t* halo;          // [R][nchunks] tag | the last dim of chunk c after the update
     uint32_t* err;           // set nonzero when a wait gives up
+    uint32_t tag0;           // this launch's sequence number << 8; generation it's tag is tag0 | it
     uint64_t seed;
     uint32_t t0;
     int32_t T;
@@ -1739,41 +1746,10 @@ struct GridArgs {
 };
 static_assert(std::is_standard_layout<GridArgs>::value, "offsetof(GridArgs, bcorr) is used on the device");
 
-// Thread 0 polls *flag until it reaches target or the wait gives up (after
-// GRID_SPIN_LIMIT polls, or once another workgroup gave up: then *err is
-// set); false if it gave up.  Acquire at device scope after the wait.
-__device__ __forceinline__ bool spin_until(const uint32_t* flag, uint32_t target, uint32_t* err)
-{
-    for (uint32_t spins = 0; __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target; ++spins) {
-        __builtin_amdgcn_s_sleep(1);
-        if (spins >= GRID_SPIN_LIMIT || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-            __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            return false;
-        }
-    }
-    __threadfence();
-    return true;
-}
-
-// Barrier of the grid.x workgroups of one run: each arrives on the run's
-// counter after a release at device scope (so its stores are visible) and
-// waits for this barrier's count.  false (every workgroup then leaves the
-// kernel) if the wait gave up; the cooperative launch keeps all workgroups
-// resident, so only a wrong kernel can make it give up.
-__device__ __forceinline__ bool grid_wait(uint32_t* cnt, uint32_t target, uint32_t* err, int32_t* ok)
-{
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        __threadfence();
-        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        *ok = spin_until(cnt, target, err) ? 1 : 0;
-    }
-    __syncthreads();
-    return *ok != 0;
-}
-
-// Wait until the tagged word at src carries tag (bounded like grid_wait);
-// false if the wait gave up.
+// Wait until the tagged word at src carries tag: false (with *err set) once
+// the wait gives up, after GRID_SPIN_LIMIT polls or when another workgroup
+// gave up; the cooperative launch keeps all workgroups resident, so only a
+// wrong kernel can make it give up.
 __device__ __forceinline__ bool wait_word(const uint64_t* src, uint32_t tag, uint32_t* err, uint64_t& word)
 {
     for (uint32_t spins = 0;; ++spins) {
@@ -1860,7 +1836,8 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
     const int32_t nlb = ncw * bc;        // local blocks (the last chunk's may pass nb)
     const int32_t CW = 1 + 4 * bc;       // mean of one chunk in LDS: the dim before it, then its dims
     // LDS: sub-slice sums (fp64) [S][ncw bc][4] | rank composites (u64) [N,
-    // N padded to even] | normals (float4) [ncw bc][P + 1] | mean [ncw][CW]
+    // N padded to even] | own members' slice sums (fp64) [nmw][RED_SLICES] |
+    // normals (float4) [ncw bc][P + 1] | mean [ncw][CW]
     // | m1, v [ncw bc][4] | partials [ncw][N] | fit [N] | y [N] | wf [P] |
     // keys [N, from a 16-byte boundary] | table [N] | pair bounds of the
     // sub-slices [S + 1]
@@ -1868,7 +1845,9 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
     const int32_t es = a.P + 1;                  // normals of one block: one float4 per pair (odd stride: no bank conflicts)
     double* red = smem;
     uint64_t* comp = reinterpret_cast<uint64_t*>(red + (int64_t)S * st);
-    float4* eps = reinterpret_cast<float4*>(comp + ((a.N + 1) & ~1));
+    const int32_t j0 = (int32_t)(((int64_t)a.N * w) / G), nmw = (int32_t)(((int64_t)a.N * (w + 1)) / G) - j0;
+    double* msl = reinterpret_cast<double*>(comp + ((a.N + 1) & ~1));
+    float4* eps = reinterpret_cast<float4*>(msl + (int64_t)((a.N + G - 1) / G) * RED_SLICES);
     float* ms = reinterpret_cast<float*>(eps + (int64_t)a.ncw * bc * es);
     float* m1s = ms + a.ncw * CW;
     float* vs = m1s + st;
@@ -1909,9 +1888,9 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
         bst.jj = -1;
     }
     __syncthreads();
-    uint32_t* cnt_bar = a.bar + r;
     uint64_t* halo = a.halo + (int64_t)r * nch;
-    uint32_t arrivals = 0;
+    uint64_t* sxr = a.sx + (int64_t)r * RED_SLICES * a.N * 2;
+    uint64_t* fxr = a.fx + (int64_t)r * a.N;
     const int32_t ev_items = a.P * ncw, tl_items = nlb * S;
     // Every generation a thread walks the same items, set up here and stepped
     // by additions: evaluate item i is (pair i % P, own chunk i / P), gradient
@@ -1922,7 +1901,7 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
     const int32_t tl_dl = nlb > 0 ? GRID_WG % nlb : 0, tl_dg = nlb > 0 ? GRID_WG / nlb : 0;
 
     for (int32_t it = 0; it < a.T; ++it) {
-        const uint32_t t = a.t0 + (uint32_t)it;
+        const uint32_t t = a.t0 + (uint32_t)it, tag = a.tag0 | (uint32_t)it;
         double inv_ns = 1.0 / (2.0 * (double)a.P * (double)sigma);
         asm volatile("" : "+v"(inv_ns));
         AdamConsts ac = a.ac;
@@ -1935,8 +1914,8 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
         if constexpr (PROB == ES_PROB_ROSENBROCK) {
             // the dim before each own chunk (the last of chunk c - 1, updated
             // by workgroup w - 1): from the state at the launch's first
-            // generation, then from chunk c - 1's word once it carries this
-            // generation's tag
+            // generation, then from chunk c - 1's word once it carries the
+            // previous generation's tag
             if (threadIdx.x == 0) ok = 1;
             __syncthreads();
             for (int32_t ic = threadIdx.x; ic < ncw; ic += GRID_WG) {
@@ -1946,7 +1925,7 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
                     h = a.m[goff + 4 * (int64_t)c * bc - 1];
                 } else if (c > 0) {
                     uint64_t word;
-                    if (wait_word(halo + c - 1, t, a.err, word)) h = __uint_as_float((uint32_t)word);
+                    if (wait_word(halo + c - 1, tag - 1, a.err, word)) h = __uint_as_float((uint32_t)word);
                     else ok = 0;
                 }
                 ms[ic * CW] = h;
@@ -1976,8 +1955,7 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
         }
         __syncthreads();
         // slice sums of the own slices q = w + G u (chunks q, q + RED_SLICES,
-        // ... in order), for every member
-        double* acc_out = a.accx + ((int64_t)(it & 1) * a.R + r) * RED_SLICES * a.N;
+        // ... in order), for every member, as two words each
         {
             const int32_t per = nch <= RED_SLICES ? 1 : RED_SLICES / G;  // own chunks between two of one slice
             const int32_t nsl = nch <= RED_SLICES ? ncw : (nq - w + G - 1) / G;
@@ -1985,27 +1963,50 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
                 const int32_t u = i / a.N, j = i - u * a.N;
                 double acc = 0.0;
                 for (int32_t ic = u; ic < ncw; ic += (nch <= RED_SLICES ? ncw : per)) acc += (double)part[ic * a.N + j];
-                acc_out[(int64_t)(w + G * u) * a.N + j] = acc;
+                const uint64_t bits = (uint64_t)__double_as_longlong(acc);
+                uint64_t* wq = sxr + ((int64_t)(w + G * u) * a.N + j) * 2;
+                __hip_atomic_store(wq, ((uint64_t)tag << 32) | (bits >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(wq + 1, ((uint64_t)tag << 32) | (bits & 0xFFFFFFFFu), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
             }
         }
-        if (!grid_wait(cnt_bar, (uint32_t)G * ++arrivals, a.err, &ok)) return;
-        // every member's fitness: the slices in order after `add`
-        for (int32_t j = threadIdx.x; j < a.N; j += GRID_WG) {
-            double sv[RED_SLICES];
-#pragma unroll
-            for (int32_t q = 0; q < RED_SLICES; ++q) sv[q] = q < nq ? acc_out[(int64_t)q * a.N + j] : 0.0;
+        // the own members' slice sums, one (member, slice) per lane, then their
+        // fitness: the slices in order after `add`, published as a word
+        if (threadIdx.x == 0) ok = 1;
+        __syncthreads();
+        for (int32_t i = threadIdx.x; i < nmw * nq; i += GRID_WG) {
+            const int32_t jl = i / nq, q = i - jl * nq;
+            const uint64_t* wq = sxr + ((int64_t)q * a.N + j0 + jl) * 2;
+            uint64_t hi, lo;
+            if (wait_word(wq, tag, a.err, hi) && wait_word(wq + 1, tag, a.err, lo))
+                msl[jl * RED_SLICES + q] = __longlong_as_double((long long)(((hi & 0xFFFFFFFFu) << 32) | (lo & 0xFFFFFFFFu)));
+            else
+                ok = 0;
+        }
+        __syncthreads();
+        if (!ok) return;
+        for (int32_t jl = threadIdx.x; jl < nmw; jl += GRID_WG) {
             double tot = a.add;
-#pragma unroll
-            for (int32_t q = 0; q < RED_SLICES; ++q)
-                if (q < nq) tot += sv[q];
-            const float f = (float)tot;
+            for (int32_t q = 0; q < nq; ++q) tot += msl[jl * RED_SLICES + q];
+            __hip_atomic_store(fxr + j0 + jl, ((uint64_t)tag << 32) | __float_as_uint((float)tot), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+        // every member's fitness
+        for (int32_t j = threadIdx.x; j < a.N; j += GRID_WG) {
+            uint64_t word;
+            if (!wait_word(fxr + j, tag, a.err, word)) {
+                ok = 0;
+                continue;
+            }
+            const float f = __uint_as_float((uint32_t)word);
             fit[j] = f;
             const uint32_t K = order_key(f, a.maximize);
             keys[j] = K;
             comp[j] = ((uint64_t)K << 32) | (uint32_t)j;
         }
         __syncthreads();
-        if (!rank_exchange(comp, keys, fit, tab, y, wf, a.N, a.P, a.raw, a.maximize, t + 1, a.yx + (int64_t)r * a.N,
+        if (!ok) return;
+        if (!rank_exchange(comp, keys, fit, tab, y, wf, a.N, a.P, a.raw, a.maximize, tag, a.yx + (int64_t)r * a.N,
                            a.bestx + r, w, G, a.err, bst, (w == 0 && a.log) ? a.log + (int64_t)it * a.R + r : nullptr,
                            &ok))
             return;
@@ -2088,7 +2089,7 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
                 // for the next generation's evaluate of that chunk
                 const int32_t c = w + G * ic;
                 if (o == bc - 1 && (i & 3) == 3 && c + 1 < nch)
-                    __hip_atomic_store(halo + c, ((uint64_t)(t + 1) << 32) | __float_as_uint(mn), __ATOMIC_RELAXED,
+                    __hip_atomic_store(halo + c, ((uint64_t)tag << 32) | __float_as_uint(mn), __ATOMIC_RELAXED,
                                        __HIP_MEMORY_SCOPE_AGENT);
             }
         }
@@ -2136,13 +2137,6 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
     }
 }
 
-// Barrier counters of the grid loop cleared ahead of a launch (a
-// kernel, so the clearing can sit in a captured stream).
-__global__ void k_clear_u32(uint32_t* __restrict__ p, int32_t n)
-{
-    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) p[i] = 0u;
-}
 
 // ---------------------------------------------------------------------------
 __global__ void k_debug_noise(uint32_t* __restrict__ words, float* __restrict__ eps, uint64_t key,
@@ -2523,13 +2517,14 @@ size_t grid_lds_bytes(const Geometry& g, const EvalPlan& e, const TellPlan& tp, 
 {
     const int64_t S = (int64_t)tp.ps * tp.nsplit * tp.sub;
     const int64_t ncw = (e.nchunks + G - 1) / G, st = 4 * ncw * e.bc;
-    // sub-slice sums | rank composites | normals | mean windows | m1, v | partials | fit | y | wf | keys (from a
-    // 16-byte boundary) | table | pair bounds
+    // sub-slice sums | rank composites | own members' slice sums | normals | mean windows | m1, v | partials | fit |
+    // y | wf | keys (from a 16-byte boundary) | table | pair bounds
     size_t f32 = (size_t)(ncw * (1 + 4 * e.bc) + 2 * st + ncw * g.N + 2 * g.N + g.P);
     f32 = (f32 + 3) & ~(size_t)3;
     f32 += (size_t)((g.N + 3) & ~3) + (size_t)g.N + (size_t)(S + 1);
     const size_t eps = 16 * (size_t)(ncw * e.bc) * ((size_t)g.P + 1);  // float4 normals
-    return sizeof(double) * (size_t)(S * st + ((g.N + 1) & ~1)) + eps + sizeof(float) * f32;
+    const size_t msl = (size_t)((g.N + G - 1) / G) * RED_SLICES;
+    return sizeof(double) * (size_t)(S * st + ((g.N + 1) & ~1) + msl) + eps + sizeof(float) * f32;
 }
 
 bool grid_supported(const Geometry& g, const EvalPlan& e, const TellPlan& tp, const es_config& c, int32_t G)
@@ -2548,7 +2543,7 @@ bool grid_supported(const Geometry& g, const EvalPlan& e, const TellPlan& tp, co
     return grid_lds_bytes(g, e, tp, G) <= GRID_MAX_LDS;
 }
 
-static_assert(RED_SLICES == 16, "grid_accx_elems sizes the slice sums for 16 slices");
+static_assert(RED_SLICES == 16, "grid_word_count sizes the slice sums for 16 slices");
 
 hipError_t grid_max_resident(int64_t* out)
 {
@@ -2569,15 +2564,22 @@ hipError_t grid_max_resident(int64_t* out)
 hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan& e, const TellPlan& tp, int32_t G,
                            uint32_t t0, int32_t T, const AdamConsts& ac, const float (*bcorr)[2], float* m, float* m1,
                            float* v, float* grad, float* best_x, uint32_t* best_okey, float* best_f,
-                           const float* pdata, const float* table, float* log, double* accx, uint64_t* yx,
-                           uint64_t* bestx, uint64_t* halo, uint32_t* sync, float* hp, hipStream_t s)
+                           const float* pdata, const float* table, float* log, uint64_t* words, uint32_t seq,
+                           uint32_t* err, float* hp, hipStream_t s)
 {
     if (T < 1 || T > FUSED_MAX_T || G < 1 || G > GRID_MAX_G) return hipErrorInvalidValue;
     if (!grid_supported(g, e, tp, c, G)) return hipErrorInvalidValue;
     GridArgs a;
     a.m = m; a.m1 = m1; a.v = v; a.grad = grad; a.best_x = best_x; a.best_okey = best_okey; a.best_f = best_f;
-    a.pdata = pdata; a.table = table; a.log = log; a.accx = accx; a.yx = yx; a.bestx = bestx; a.halo = halo;
-    a.bar = sync; a.err = sync + grid_sync_words(g) - 1;
+    a.pdata = pdata; a.table = table; a.log = log;
+    a.sx = words;
+    a.fx = a.sx + (size_t)g.R * RED_SLICES * g.N * 2;
+    a.yx = a.fx + (size_t)g.R * g.N;
+    a.bestx = a.yx + (size_t)g.R * g.N;
+    a.halo = a.bestx + g.R;
+    a.err = err;
+    if (seq < 1 || seq >= (1u << 24)) return hipErrorInvalidValue;
+    a.tag0 = seq << 8;
     a.ac = ac;
     for (int32_t i = 0; i < T; ++i) {
         a.bcorr[i][0] = bcorr[i][0];
@@ -2591,11 +2593,7 @@ hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan
     a.maximize = c.maximize; a.raw = c.shaping == ES_SHAPE_RAW;
     a.hp = hp;
     a.sigma_decay = c.sigma_decay; a.sigma_final = c.sigma_final; a.lr_decay = c.lr_decay; a.lr_final = c.lr_final;
-    // barrier counters cleared; the error flag after them stays
-    const int32_t nclear = (int32_t)(grid_sync_words(g) - 1);
-    k_clear_u32<<<(nclear + 255) / 256, 256, 0, s>>>(sync, nclear);
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return err;
+    hipError_t herr;
     const uint32_t lds = (uint32_t)grid_lds_bytes(g, e, tp, G);
     void* args[] = {&a};
     const void* k;
@@ -2607,8 +2605,8 @@ hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan
     default: return hipErrorInvalidValue;
     }
     // more than 64 KB of LDS per workgroup: allowed per kernel (cheap to repeat)
-    err = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GRID_MAX_LDS);
-    if (err != hipSuccess) return err;
+    herr = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GRID_MAX_LDS);
+    if (herr != hipSuccess) return herr;
     return hipLaunchCooperativeKernel(k, dim3((unsigned)G, (unsigned)g.R), dim3(GRID_WG), args, lds, s);
 }
 

@@ -94,6 +94,28 @@ def test_plan_variants(kw):
     _same(_rosenbrock(**kw), 12)
 
 
+def test_rewound_generation_counter():
+    """es_set_state moves t back: the next launch's exchange words must not
+    take the values an earlier launch left with the same generation."""
+    P = _P()
+    cfg = _rosenbrock(num_dims=300, popsize=64)
+    out = {}
+    for path in (3, 1):
+        es = P.ES(dataclasses.replace(cfg, plan_run_path=path))
+        assert es.run_path == path
+        es.run(12)
+        st = es.get_state()
+        es.set_state(st["m"], st["m1"], st["v"], 5)  # back to t = 5 with the state of t = 12
+        log = es.run(10)
+        st = es.get_state()
+        torch.cuda.synchronize()
+        es.sync()
+        out[path] = [x.cpu().numpy() for x in (log, st["m"], st["m1"], st["v"], es.grad())]
+        es.close()
+    for name, a, b in zip(("log", "m", "m1", "v", "grad"), out[3], out[1]):
+        assert a.tobytes() == b.tobytes(), name
+
+
 def test_more_workgroups_than_pairs():
     # 13 dims in four one-block chunks: four workgroups of one chunk each (the
     # nine asked for are lowered to the chunk count), three pairs

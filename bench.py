@@ -47,6 +47,11 @@ EVAL_SLOTS_PER_PAIR_BLOCK = {"sphere": PHILOX_BM + 24, "shifted_sphere": PHILOX_
                              "rosenbrock": PHILOX_BM + 64, "rastrigin": PHILOX_BM + 88}
 # tell: Philox + Box-Muller + 4 fma (w * eps) + the fp64 fold every 16 pairs
 TELL_SLOTS_PER_PAIR_BLOCK = PHILOX_BM + 4 + 1
+# es_run's code paths (es_run_path); the grid loop's gradient reads the
+# normals the evaluate kept in LDS, so its work per pair-block omits one
+# Philox block and Box-Muller
+RUN_PATHS = {1: "per-call kernels", 2: "fused loop (k_run_fused, one workgroup per run)",
+             3: "grid loop (k_run_grid, a cooperative launch of several workgroups per run)"}
 # per-dimension sigma (PGPE, SNES): evaluate moves each dim's sigma into a
 # VGPR (4 movs per block); tell adds the second sum, 4 fma (z*z - 1) + 4 fma
 EVAL_VEC_EXTRA = 4
@@ -183,6 +188,7 @@ def time_workload(P, torch, name, K, W, path, dev, stream, copy_mib=0):
     from paper_2212_04180_amd import workloads
     cfg, _ = workloads.get(name)
     es = P.ES(cfg, device=dev, stream=stream)
+    run_path = es.run_path if path == "run" else 1
     R, N, D = cfg.num_runs, cfg.popsize, cfg.num_dims
     fit = torch.empty(R, N, device=dev)
     if copy_mib:
@@ -236,7 +242,7 @@ def time_workload(P, torch, name, K, W, path, dev, stream, copy_mib=0):
     es.close()
     value = R * N * D / (ms * 1e-3)
     phases = f" (eval kernel {eval_ms:.4f}, rest {rest_ms:.4f})" if eval_ms is not None else ""
-    log(f"[bench] {name} ({path}): {ms:.4f} ms/gen{phases}, wall {wall:.3f}s for {K} gens, "
+    log(f"[bench] {name} ({path}, {RUN_PATHS[run_path]}): {ms:.4f} ms/gen{phases}, wall {wall:.3f}s for {K} gens, "
         f"{value:.4e} member-dims/s")
 
     prob = {P.PROB_SHIFTED_SPHERE: "shifted_sphere", P.PROB_SPHERE: "sphere", P.PROB_RASTRIGIN: "rastrigin",
@@ -273,11 +279,11 @@ def time_workload(P, torch, name, K, W, path, dev, stream, copy_mib=0):
                          "frac": tell_achieved / VALU_PEAK, "slots_per_pair_block": tell_slots}}
     if prob is not None and path == "run" and cfg.strategy == P.STRAT_OPENAI_ES:
         # whole generations: evaluate and gradient slots over the timed launch(es)
-        slots = EVAL_SLOTS_PER_PAIR_BLOCK[prob] + TELL_SLOTS_PER_PAIR_BLOCK
+        slots = EVAL_SLOTS_PER_PAIR_BLOCK[prob] + TELL_SLOTS_PER_PAIR_BLOCK - (PHILOX_BM if run_path == 3 else 0)
         achieved = pair_blocks * slots / (ms * 1e-3)
         roof = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                 "unit": "T VALU lane-op slots/s", "frac": achieved / VALU_PEAK, "traffic": None,
-                "kernel": "es_run (k_run_fused where the geometry takes the fused loop, else the per-call kernels)",
+                "kernel": "es_run: " + RUN_PATHS[run_path],
                 "kernel_ms": ms, "slots_per_pair_block": slots, "pair_blocks_per_generation": pair_blocks}
     if cfg.problem == P.PROB_MLP and path == "percall":
         flops = R * N * MLP_FLOPS_PER_MEMBER
@@ -293,7 +299,7 @@ def time_workload(P, torch, name, K, W, path, dev, stream, copy_mib=0):
                          "achieved": tell_achieved / 1e12, "unit": "T VALU lane-op slots/s",
                          "frac": tell_achieved / VALU_PEAK}}
     return {"cfg": cfg, "prob": prob, "ms": ms, "eval_ms": eval_ms, "rest_ms": rest_ms, "value": value,
-            "roofline": roof, "K": K}
+            "roofline": roof, "K": K, "run_path": RUN_PATHS[run_path]}
 
 
 # Instructions of the probe (include/esmi_probe.h) in its enum order, the
@@ -384,7 +390,8 @@ def main():
         for name, (path, K, W) in OTHER_WORKLOADS.items():
             o = time_workload(P, torch, name, K, W, path, dev, stream)
             oc = o["cfg"]
-            others[name] = {"path": path, "steps": K, "ms_per_step": o["ms"], "generations_per_s": 1e3 / o["ms"],
+            others[name] = {"path": path, "code_path": o["run_path"], "steps": K, "ms_per_step": o["ms"],
+                            "generations_per_s": 1e3 / o["ms"],
                             "value": o["value"], "unit": "member-dims/s",
                             "num_runs": oc.num_runs, "popsize": oc.popsize, "num_dims": oc.num_dims,
                             "eval_kernel_ms": o["eval_ms"], "rest_ms": o["rest_ms"], "roofline": o["roofline"]}

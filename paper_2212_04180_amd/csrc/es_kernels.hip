@@ -1342,7 +1342,9 @@ __global__ __launch_bounds__(256) void k_clipup_apply(float* __restrict__ vel, f
 // small strategies: one workgroup per run, the mean and Adam moments in LDS.
 // Each phase repeats the per-call kernels' arithmetic in the same order
 // (same chunking of the evaluation, same reduction order, same pair slices
-// of the gradient), so es_run gives the same bits on either path.
+// of the gradient), so es_run gives the same bits on either path.  STASH:
+// the evaluate keeps every normal it makes in LDS and the gradient reads them
+// back instead of regenerating them (where they fit).
 struct FusedArgs {
     float* m;
     float* m1;
@@ -1493,15 +1495,18 @@ __device__ __forceinline__ void rank_pairs(const uint32_t* keys, const float* fi
     }
 }
 
-template <int PROB>
+template <int PROB, bool STASH>
 __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
 {
     extern __shared__ __align__(16) double smem[];
     const int32_t r = blockIdx.x;
     const int64_t Dp = 4 * a.nb;
-    // LDS layout: tell slices (fp64) | m | m1 | v | partial | fit | y | wf | keys (N rounded up to 4) | table
+    // LDS layout: tell slices (fp64) | normals (float4, STASH) | m | m1 | v | partial | fit | y | wf | keys (N
+    // rounded up to 4) | table
     double* red = smem;                                  // [ps][nb][4]
-    float* ms = reinterpret_cast<float*>(red + (int64_t)a.ps * a.nb * 4);
+    const int32_t es = a.P + 1;                          // normals of one block: one float4 per pair
+    float4* eps = reinterpret_cast<float4*>(red + (int64_t)a.ps * a.nb * 4);  // [nb][P + 1]
+    float* ms = reinterpret_cast<float*>(eps + (STASH ? a.nb * es : 0));
     float* m1s = ms + Dp;
     float* vs = m1s + Dp;
     float* part = vs + Dp;                               // [nchunks][N]
@@ -1580,7 +1585,8 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
                 const int64_t b0 = (int64_t)c * a.bc, b1 = b0 + a.bc < a.nb ? b0 + a.bc : a.nb;
                 double accp, accm;
                 eval_chunk<PROB, LANES_BLOCK_AND_ROW>(ms, a.pdata, k0, k1, (uint32_t)p, t, b0, b1, a.D, sigma, a.ra,
-                                                      accp, accm);
+                                                      accp, accm, nullptr, 0, 0,
+                                                      STASH ? eps + b0 * es + p : nullptr, es);
                 part[c * a.N + p] = (float)accp;
                 part[c * a.N + p + P32] = (float)accm;
                 p += ev_dp;
@@ -1611,7 +1617,10 @@ __global__ __launch_bounds__(FUSED_WG) void k_run_fused(FusedArgs a)
             int32_t b = tl_b0, s = tl_s0;
             for (int32_t i = (int32_t)threadIdx.x; i < tl_items; i += FUSED_WG) {
                 double a64[4] = {0.0, 0.0, 0.0, 0.0};
-                tell_slice<LANES_BLOCK_AND_ROW>(wf, k0, k1, (uint32_t)b, t, sl_bound[s], sl_bound[s + 1], a64);
+                if constexpr (STASH)
+                    tell_slice_eps(wf, eps + (int64_t)b * es, sl_bound[s], sl_bound[s + 1], a64);
+                else
+                    tell_slice<LANES_BLOCK_AND_ROW>(wf, k0, k1, (uint32_t)b, t, sl_bound[s], sl_bound[s + 1], a64);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) red[(s * nb32 + b) * 4 + k] = a64[k];
                 b += tl_db;
@@ -2457,6 +2466,18 @@ size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e)
     return red + sizeof(float) * f32;
 }
 
+size_t fused_stash_bytes(const Geometry& g) { return 16 * (size_t)g.nb * ((size_t)g.P + 1); }
+
+// The normals stay in LDS when the workgroup still fits FUSED_MAX_LDS and the
+// runs that share a CU (up to five of the loop's workgroups) still fit its
+// 160 KB together.
+bool fused_stash(const Geometry& g, const EvalPlan& e)
+{
+    const size_t per_run = fused_lds_bytes(g, e) + fused_stash_bytes(g);
+    const int64_t per_cu = std::min<int64_t>((g.R + 255) / 256, 5);
+    return per_run <= FUSED_MAX_LDS && per_run * (size_t)per_cu <= 160 * 1024;
+}
+
 bool fused_supported(const Geometry& g, const EvalPlan& e, const es_config& c)
 {
     if (c.problem < ES_PROB_SPHERE || c.problem > ES_PROB_RASTRIGIN) return false;
@@ -2488,14 +2509,19 @@ hipError_t launch_run_fused(const Geometry& g, const es_config& c, const EvalPla
     a.maximize = c.maximize; a.raw = c.shaping == ES_SHAPE_RAW;
     a.hp = hp;
     a.sigma_decay = c.sigma_decay; a.sigma_final = c.sigma_final; a.lr_decay = c.lr_decay; a.lr_final = c.lr_final;
-    const size_t lds = fused_lds_bytes(g, e);
+    const bool stash = fused_stash(g, e);
+    const size_t lds = fused_lds_bytes(g, e) + (stash ? fused_stash_bytes(g) : 0);
+#define ES_FUSED_LAUNCH(PROB)                                                     \
+    (stash ? (k_run_fused<PROB, true><<<g.R, FUSED_WG, lds, s>>>(a), 0)           \
+           : (k_run_fused<PROB, false><<<g.R, FUSED_WG, lds, s>>>(a), 0))
     switch (c.problem) {
-    case ES_PROB_SPHERE: k_run_fused<ES_PROB_SPHERE><<<g.R, FUSED_WG, lds, s>>>(a); break;
-    case ES_PROB_SHIFTED_SPHERE: k_run_fused<ES_PROB_SHIFTED_SPHERE><<<g.R, FUSED_WG, lds, s>>>(a); break;
-    case ES_PROB_ROSENBROCK: k_run_fused<ES_PROB_ROSENBROCK><<<g.R, FUSED_WG, lds, s>>>(a); break;
-    case ES_PROB_RASTRIGIN: k_run_fused<ES_PROB_RASTRIGIN><<<g.R, FUSED_WG, lds, s>>>(a); break;
+    case ES_PROB_SPHERE: ES_FUSED_LAUNCH(ES_PROB_SPHERE); break;
+    case ES_PROB_SHIFTED_SPHERE: ES_FUSED_LAUNCH(ES_PROB_SHIFTED_SPHERE); break;
+    case ES_PROB_ROSENBROCK: ES_FUSED_LAUNCH(ES_PROB_ROSENBROCK); break;
+    case ES_PROB_RASTRIGIN: ES_FUSED_LAUNCH(ES_PROB_RASTRIGIN); break;
     default: return hipErrorInvalidValue;
     }
+#undef ES_FUSED_LAUNCH
     return hipGetLastError();
 }
 

@@ -47,9 +47,9 @@ EVAL_SLOTS_PER_PAIR_BLOCK = {"sphere": PHILOX_BM + 24, "shifted_sphere": PHILOX_
                              "rosenbrock": PHILOX_BM + 64, "rastrigin": PHILOX_BM + 88}
 # tell: Philox + Box-Muller + 4 fma (w * eps) + the fp64 fold every 16 pairs
 TELL_SLOTS_PER_PAIR_BLOCK = PHILOX_BM + 4 + 1
-# es_run's code paths (es_run_path); the grid loop's gradient reads the
-# normals the evaluate kept in LDS, so its work per pair-block omits one
-# Philox block and Box-Muller
+# es_run's code paths (es_run_path); where a loop's gradient reads the
+# normals its evaluate kept in LDS (es_run_path's keeps_normals), its work per
+# pair-block omits one Philox block and Box-Muller
 RUN_PATHS = {1: "per-call kernels", 2: "fused loop (k_run_fused, one workgroup per run)",
              3: "grid loop (k_run_grid, a cooperative launch of several workgroups per run)"}
 # per-dimension sigma (PGPE, SNES): evaluate moves each dim's sigma into a
@@ -189,6 +189,7 @@ def time_workload(P, torch, name, K, W, path, dev, stream, copy_mib=0):
     cfg, _ = workloads.get(name)
     es = P.ES(cfg, device=dev, stream=stream)
     run_path = es.run_path if path == "run" else 1
+    keeps = path == "run" and es.run_keeps_normals
     R, N, D = cfg.num_runs, cfg.popsize, cfg.num_dims
     fit = torch.empty(R, N, device=dev)
     if copy_mib:
@@ -279,11 +280,11 @@ def time_workload(P, torch, name, K, W, path, dev, stream, copy_mib=0):
                          "frac": tell_achieved / VALU_PEAK, "slots_per_pair_block": tell_slots}}
     if prob is not None and path == "run" and cfg.strategy == P.STRAT_OPENAI_ES:
         # whole generations: evaluate and gradient slots over the timed launch(es)
-        slots = EVAL_SLOTS_PER_PAIR_BLOCK[prob] + TELL_SLOTS_PER_PAIR_BLOCK - (PHILOX_BM if run_path == 3 else 0)
+        slots = EVAL_SLOTS_PER_PAIR_BLOCK[prob] + TELL_SLOTS_PER_PAIR_BLOCK - (PHILOX_BM if keeps else 0)
         achieved = pair_blocks * slots / (ms * 1e-3)
         roof = {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK / 1e12,
                 "unit": "T VALU lane-op slots/s", "frac": achieved / VALU_PEAK, "traffic": None,
-                "kernel": "es_run: " + RUN_PATHS[run_path],
+                "kernel": "es_run: " + RUN_PATHS[run_path], "keeps_normals": bool(keeps),
                 "kernel_ms": ms, "slots_per_pair_block": slots, "pair_blocks_per_generation": pair_blocks}
     if cfg.problem == P.PROB_MLP and path == "percall":
         flops = R * N * MLP_FLOPS_PER_MEMBER

@@ -363,8 +363,12 @@ int64_t es_generation(const es_handle* h);
 /* The code path es_run takes for this handle (host value; no device work;
  * not defined by the paper): 1 the per-call kernels, 2 the fused loop (one
  * workgroup per run), 3 the grid loop (a cooperative launch of several
- * workgroups per run); 0 for a NULL handle.  See cfg.plan_run_path. */
-int32_t es_run_path(const es_handle* h);
+ * workgroups per run); 0 for a NULL handle.  See cfg.plan_run_path.
+ * keeps_normals (NULL to skip) receives 1 where that path's gradient reads
+ * the normals its evaluate kept in LDS instead of regenerating them (the
+ * grid loop always, the fused loop where they fit), else 0; the results are
+ * the same bits either way. */
+int32_t es_run_path(const es_handle* h, int32_t* keeps_normals);
 
 /* Message of the last failed call on h ("" if none); with h == NULL, the
  * message of the last failed es_init on this thread.  Never NULL. */

@@ -430,7 +430,13 @@ const char* es_last_error(const es_handle* h) { return h ? h->err : g_init_err; 
 
 int64_t es_generation(const es_handle* h) { return h ? h->t : -1; }
 
-int32_t es_run_path(const es_handle* h) { return h ? run_path_of(h) : 0; }
+int32_t es_run_path(const es_handle* h, int32_t* keeps_normals)
+{
+    const int32_t path = h ? run_path_of(h) : 0;
+    if (keeps_normals)
+        *keeps_normals = path == 3 || (path == 2 && fused_stash(h->g, h->plan)) ? 1 : 0;
+    return path;
+}
 
 es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
 {

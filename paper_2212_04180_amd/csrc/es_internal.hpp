@@ -143,6 +143,8 @@ int32_t tell_slices(const Geometry& g);
 // Fused multi-generation loop (one workgroup per run, state in LDS).
 constexpr size_t FUSED_MAX_LDS = 60 * 1024;
 size_t fused_lds_bytes(const Geometry& g, const EvalPlan& e);
+// Whether the fused loop keeps the normals in LDS for the gradient (they fit)
+bool fused_stash(const Geometry& g, const EvalPlan& e);
 bool fused_supported(const Geometry& g, const EvalPlan& e, const es_config& c);
 // Generations per fused launch: their Adam bias corrections (bcorr[i] =
 // {bc1, bc2} of generation t0 + i) travel in the kernel arguments, so a

@@ -174,7 +174,7 @@ def lib() -> ctypes.CDLL:
         "es_load_state": (i32, [vp, vp, ctypes.c_size_t]),
         "es_sync": (i32, [vp]),
         "es_generation": (i64, [vp]),
-        "es_run_path": (i32, [vp]),
+        "es_run_path": (i32, [vp, vp]),
         "es_last_error": (ctypes.c_char_p, [vp]),
         "es_status_string": (ctypes.c_char_p, [i32]),
         "es_destroy": (None, [vp]),
@@ -254,7 +254,14 @@ class ES:
     @property
     def run_path(self) -> int:
         """The path es_run takes: 1 per-call kernels, 2 fused loop, 3 grid loop."""
-        return int(lib().es_run_path(self._h))
+        return int(lib().es_run_path(self._h, None))
+
+    @property
+    def run_keeps_normals(self) -> bool:
+        """Whether es_run's gradient reads the normals its evaluate kept in LDS."""
+        k = ctypes.c_int32(0)
+        lib().es_run_path(self._h, ctypes.byref(k))
+        return bool(k.value)
 
     # -- ask / evaluate / tell ---------------------------------------------
     def ask(self, materialize: bool = False):

@@ -34,7 +34,7 @@ def test_status_strings_and_init_error_without_gpu_work():
     from paper_2212_04180_amd import esmi
     L = esmi.lib()
     assert L.es_status_string(0) == b"ok"
-    assert L.es_run_path(None) == 0 and L.es_generation(None) == -1
+    assert L.es_run_path(None, None) == 0 and L.es_generation(None) == -1
     assert L.es_status_string(-2).startswith(b"call out of")
     # an invalid config is rejected before any device call
     cfg = esmi.ESConfig(num_dims=8, popsize=3).cstruct()

@@ -59,13 +59,15 @@ def _rosenbrock(**kw):
 
 
 def test_default_paths_of_the_workloads():
+    # (path, whether the loop's gradient reads the normals its evaluate kept)
     from paper_2212_04180_amd import workloads
     P = _P()
-    want = {"sphere_d16": 2, "rosenbrock_d1000": 3, "rastrigin_r1024": 2, "shifted_sphere_d1m": 1}
-    for name, path in want.items():
+    want = {"sphere_d16": (2, True), "rosenbrock_d1000": (3, True), "rastrigin_r1024": (2, True),
+            "shifted_sphere_d1m": (1, False)}
+    for name, (path, keeps) in want.items():
         cfg, _ = workloads.get(name)
         es = P.ES(cfg)
-        assert es.run_path == path, (name, es.run_path)
+        assert (es.run_path, es.run_keeps_normals) == (path, keeps), name
         es.close()
 
 

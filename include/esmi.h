@@ -179,8 +179,9 @@ typedef struct es_config {
      *                     wherever it supports the config (always in the
      *                     per-call kernels' order, so the same bits); 0 =
      *                     the fused loop for small runs or many runs, the
-     *                     grid loop for a few runs of up to 131072 Philox
-     *                     pair-blocks in all (num_runs * popsize/2 *
+     *                     grid loop where it applies (its workgroups keep
+     *                     their share of the normals in LDS; at most 2^20
+     *                     Philox pair-blocks in all, num_runs * popsize/2 *
      *                     ceil(D/4)), else the per-call kernels.  Both loops
      *                     run OpenAI-ES with Adam on the benchmark problems,
      *                     centered-rank or raw shaping, no weight decay; the

@@ -167,7 +167,7 @@ constexpr int32_t GRID_MAX_G = 16;
 constexpr int32_t GRID_MAX_N = 8192;            // every workgroup ranks the run's members
 constexpr size_t GRID_MAX_LDS = 144 * 1024;     // of gfx950's 160 KB per workgroup
 // es_run takes the grid loop by default up to this many pair-blocks (R P nb)
-constexpr int64_t GRID_DEFAULT_WORK = 131072;
+constexpr int64_t GRID_DEFAULT_WORK = 1 << 20;
 int32_t grid_workgroups(const Geometry& g, const EvalPlan& e, int32_t want);  // want 0: the library's choice
 inline size_t grid_word_count(const Geometry& g, const EvalPlan& e)
 {

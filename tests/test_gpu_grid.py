@@ -96,6 +96,29 @@ def test_plan_variants(kw):
     _same(_rosenbrock(**kw), 12)
 
 
+def test_fused_loop_without_kept_normals():
+    """1024 runs of 600 dims and 16 members: the fused loop, whose four runs per
+    CU (about 49 KB each with the normals kept) would not fit 160 KB of LDS, so
+    its gradient regenerates them; the same bits as the per-call kernels."""
+    P = _P()
+    cfg = P.ESConfig(num_dims=600, popsize=16, num_runs=1024, sigma=0.1, lr=0.02, seed=5, init_lo=-3.0,
+                     init_hi=3.0, problem=P.PROB_RASTRIGIN, flags=P.FLAG_KEEP_GRAD)
+    es = P.ES(cfg)
+    assert (es.run_path, es.run_keeps_normals) == (2, False)
+    es.close()
+    out = {}
+    for path in (2, 1):
+        es = P.ES(dataclasses.replace(cfg, plan_run_path=path))
+        log = es.run(6)
+        st = es.get_state()
+        bx, bf = es.best()
+        torch.cuda.synchronize()
+        out[path] = [x.cpu().numpy() for x in (log, st["m"], st["m1"], st["v"], bx, bf, es.grad())]
+        es.close()
+    for name, a, b in zip(("log", "m", "m1", "v", "best_x", "best_f", "grad"), out[2], out[1]):
+        assert a.tobytes() == b.tobytes(), name
+
+
 def test_rewound_generation_counter():
     """es_set_state moves t back: the next launch's exchange words must not
     take the values an earlier launch left with the same generation."""

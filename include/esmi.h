@@ -200,12 +200,22 @@ typedef struct es_config {
      *                     num_runs * popsize < 2^31); 0 = the library's
      *                     choice: 2 above popsize 16384, and where
      *                     num_runs * popsize^2 > 1.2e8 (where it is the
-     *                     faster), else 1                                 */
+     *                     faster), else 1
+     *   plan_grid_spin_limit  polls of a word before a wait of the grid loop
+     *                     gives up (0: 2^20, which a correct launch never
+     *                     reaches; -1: every wait gives up at once, the
+     *                     failure path, for tests); no effect on the results
+     *                     of a launch whose waits all succeed.  A wait that
+     *                     gives up ends the launch early with the state not
+     *                     valid: es_sync reports it
+     *   plan_reserved     must be 0 (keeps the struct free of padding)     */
     int32_t plan_eval_blocks;
     int32_t plan_tell_split;
     int32_t plan_run_path;
     int32_t plan_rank_path;
     int32_t plan_grid_workgroups;
+    int32_t plan_grid_spin_limit;
+    int32_t plan_reserved;
 } es_config;
 
 typedef struct es_handle es_handle;
@@ -287,7 +297,8 @@ es_status es_run(es_handle* h, int32_t T, float* log);
 /* Copy out / replace the search state (the state fields of Listing 1; the
  * paper defines no accessor: these are host-side plumbing).  m, m1, v:
  * device [R][D] (NULL to skip); t: number of completed generations.
- * es_set_state requires no open ask. */
+ * es_set_state requires no open ask.  es_set_state and es_load_state also
+ * clear the failure flag of the grid loop that es_sync reports. */
 es_status es_get_state(es_handle* h, float* m, float* m1, float* v, int64_t* t);
 es_status es_set_state(es_handle* h, const float* m, const float* m1, const float* v, int64_t t);
 
@@ -354,8 +365,10 @@ es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes);
 /* Wait for all work enqueued by this handle (synchronous).  Not defined by
  * the paper.  Also reports ES_ERR_HIP if a grid-loop launch of es_run ended
  * early because a wait for another workgroup's values gave up (its
- * workgroups are resident together under a cooperative launch, so only a
- * library fault can cause that; the state is then not valid). */
+ * workgroups are resident together under a cooperative launch, so with the
+ * default cfg.plan_grid_spin_limit only a library fault can cause that; the
+ * state is then not valid, and stays reported until es_set_state or
+ * es_load_state replaces it). */
 es_status es_sync(es_handle* h);
 
 /* Current generation counter t (host value; no device work). */

@@ -26,7 +26,7 @@ enum Phase { READY = 0, ASKED = 1 };
 
 constexpr uint32_t kCheckpointMagic = 0x45534d32u;  // "ESM2"
 // no padding bytes: a checkpoint's config is compared byte for byte
-static_assert(sizeof(es_config) == 160, "es_config has padding");
+static_assert(sizeof(es_config) == 168, "es_config has padding");
 
 thread_local char g_init_err[256] = {0};
 
@@ -166,6 +166,8 @@ const char* validate(const es_config& c)
     if (c.plan_grid_workgroups < 0 || c.plan_grid_workgroups > GRID_MAX_G)
         return "plan_grid_workgroups must be in [0, 16]";
     if (c.plan_rank_path < 0 || c.plan_rank_path > 2) return "plan_rank_path must be 0, 1 or 2";
+    if (c.plan_grid_spin_limit < -1) return "plan_grid_spin_limit must be >= -1";
+    if (c.plan_reserved != 0) return "plan_reserved must be 0";
     if (c.plan_rank_path == 1 && c.popsize > RANK_MAX_N)
         return "plan_rank_path 1 (ranks counted in LDS) takes popsize <= 16384";
     // (the library's own choice of the sort never needs more: it picks the
@@ -725,6 +727,17 @@ es_status es_get_state(es_handle* h, float* m, float* m1, float* v, int64_t* t)
     return ES_OK;
 }
 
+// A new state also makes the grid loop's failure flag stale: clear it (a
+// copy rather than a memset, so that a captured stream records no memset).
+static es_status clear_grid_flag(es_handle* h)
+{
+    static const uint32_t zero = 0;
+    if (h->grid_err)
+        ES_HIP(h, hipMemcpyAsync(h->grid_err, &zero, sizeof(zero), hipMemcpyHostToDevice, h->stream),
+               "clear the grid loop flag");
+    return ES_OK;
+}
+
 es_status es_set_state(es_handle* h, const float* m, const float* m1, const float* v, int64_t t)
 {
     if (!h) return ES_ERR_ARG;
@@ -734,6 +747,7 @@ es_status es_set_state(es_handle* h, const float* m, const float* m1, const floa
     if (m && (s = copy_rows_in(h, h->m, m)) != ES_OK) return s;
     if (m1 && (s = copy_rows_in(h, h->m1, m1)) != ES_OK) return s;
     if (v && (s = copy_rows_in(h, h->v, v)) != ES_OK) return s;
+    if ((s = clear_grid_flag(h)) != ES_OK) return s;
     if (t != h->t) h->teacher_t = -1;
     h->t = t;
     return ES_OK;
@@ -937,6 +951,8 @@ es_status es_load_state(es_handle* h, const void* host_buf, size_t bytes)
         ES_HIP(h, hipMemcpyAsync(dst, p, rows, hipMemcpyHostToDevice, h->stream), "load strategy state");
         p += rows;
     }
+    es_status st = clear_grid_flag(h);
+    if (st != ES_OK) return st;
     ES_HIP(h, hipStreamSynchronize(h->stream), "load sync");
     if (hd.t != h->t) h->teacher_t = -1;
     h->t = hd.t;

@@ -52,7 +52,7 @@ constexpr int TELL_MAX_PS = 16;   // pair slices per tell workgroup (one wave ea
 constexpr int TELL_GROUP = 16;    // fp32 pairs folded into the fp64 sum at once
 constexpr int FUSED_WG = 256;     // threads of the fused multi-generation workgroup
 constexpr int GRID_WG = 1024;      // threads of a grid-loop workgroup (four waves per SIMD)
-constexpr uint32_t GRID_SPIN_LIMIT = 1u << 20;  // polls before a barrier wait gives up
+constexpr uint32_t GRID_SPIN_LIMIT = 1u << 20;  // polls before a grid-loop wait gives up (the default)
 constexpr int FUSED_PRIO = 3;     // wave priority of the fused loop's short phases (the highest)
 
 // MLP 64-256-256-16, flattened [out][in] per layer then the bias.  Returns
@@ -1736,6 +1736,7 @@ struct GridArgs {
     uint64_t* bestx;         // [R] tag | the rank-0 member
     uint64_t* halo;          // [R][nchunks] tag | the last dim of chunk c after the update
     uint32_t* err;           // set nonzero when a wait gives up
+    uint32_t spin;           // SPIN_ARG: polls before a wait gives up; 0: at once, without polling
     uint32_t tag0;           // this launch's sequence number << 8; generation it's tag is tag0 | it
     uint64_t seed;
     uint32_t t0;
@@ -1756,16 +1757,30 @@ struct GridArgs {
 static_assert(std::is_standard_layout<GridArgs>::value, "offsetof(GridArgs, bcorr) is used on the device");
 
 // Wait until the tagged word at src carries tag: false (with *err set) once
-// the wait gives up, after GRID_SPIN_LIMIT polls or when another workgroup
-// gave up; the cooperative launch keeps all workgroups resident, so only a
-// wrong kernel can make it give up.
-__device__ __forceinline__ bool wait_word(const uint64_t* src, uint32_t tag, uint32_t* err, uint64_t& word)
+// the wait gives up, after GRID_SPIN_LIMIT polls (SPIN_ARG: `spin` polls,
+// 0 giving up at once, so that a test can take the failure path) or when
+// another workgroup gave up; the cooperative launch keeps all workgroups
+// resident, so with the default limit only a wrong kernel can make it give
+// up.  A workgroup whose wait gave up leaves the kernel at its next check,
+// and so do the others once their waits see the flag.  (The limit is a
+// template choice: as a kernel argument in the default instantiation it cost
+// the loop about 8% per generation.)
+template <bool SPIN_ARG>
+__device__ __forceinline__ bool wait_word(const uint64_t* src, uint32_t tag, uint32_t* err, uint32_t spin,
+                                          uint64_t& word)
 {
+    if constexpr (SPIN_ARG) {
+        if (spin == 0) {
+            __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return false;
+        }
+    }
+    const uint32_t limit = SPIN_ARG ? spin - 1 : GRID_SPIN_LIMIT;
     for (uint32_t spins = 0;; ++spins) {
         word = __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if ((uint32_t)(word >> 32) == tag) return true;
         __builtin_amdgcn_s_sleep(1);
-        if (spins >= GRID_SPIN_LIMIT || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+        if (spins >= limit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
             __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             return false;
         }
@@ -1781,10 +1796,11 @@ __device__ __forceinline__ bool wait_word(const uint64_t* src, uint32_t tag, uin
 // one location, so no fence is needed.  Then the folded weights wf[p] = y_p
 // - y_{p+P}, the best-so-far and (logp not null) the generation's best
 // fitness.  false if a wait gave up.
+template <bool SPIN_ARG>
 __device__ __forceinline__ bool rank_exchange(const uint64_t* comp, const uint32_t* keys, const float* fit,
                                               const float* tab, float* y, float* wf, int32_t N, int32_t P, int32_t raw,
                                               int32_t maximize, uint32_t tag, uint64_t* yx, uint64_t* bestx, int32_t w,
-                                              int32_t G, uint32_t* err, LoopBest& bst, float* logp, int32_t* ok)
+                                              int32_t G, uint32_t* err, uint32_t spin, LoopBest& bst, float* logp, int32_t* ok)
 {
     const int32_t wave = __builtin_amdgcn_readfirstlane((int32_t)(threadIdx.x / 64)), lane = threadIdx.x % 64;
     const int32_t j0 = (int32_t)(((int64_t)N * w) / G), j1 = (int32_t)(((int64_t)N * (w + 1)) / G);
@@ -1807,7 +1823,7 @@ __device__ __forceinline__ bool rank_exchange(const uint64_t* comp, const uint32
     __syncthreads();
     for (int32_t j = threadIdx.x; j <= N; j += GRID_WG) {
         uint64_t word;
-        if (!wait_word(j < N ? yx + j : bestx, tag, err, word)) {
+        if (!wait_word<SPIN_ARG>(j < N ? yx + j : bestx, tag, err, spin, word)) {
             *ok = 0;
             continue;
         }
@@ -1832,7 +1848,7 @@ __device__ __forceinline__ bool rank_exchange(const uint64_t* comp, const uint32
     return true;
 }
 
-template <int PROB>
+template <int PROB, bool SPIN_ARG = false>
 __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
 {
     extern __shared__ __align__(16) double smem[];
@@ -1934,7 +1950,7 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
                     h = a.m[goff + 4 * (int64_t)c * bc - 1];
                 } else if (c > 0) {
                     uint64_t word;
-                    if (wait_word(halo + c - 1, tag - 1, a.err, word)) h = __uint_as_float((uint32_t)word);
+                    if (wait_word<SPIN_ARG>(halo + c - 1, tag - 1, a.err, a.spin, word)) h = __uint_as_float((uint32_t)word);
                     else ok = 0;
                 }
                 ms[ic * CW] = h;
@@ -1987,7 +2003,7 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
             const int32_t jl = i / nq, q = i - jl * nq;
             const uint64_t* wq = sxr + ((int64_t)q * a.N + j0 + jl) * 2;
             uint64_t hi, lo;
-            if (wait_word(wq, tag, a.err, hi) && wait_word(wq + 1, tag, a.err, lo))
+            if (wait_word<SPIN_ARG>(wq, tag, a.err, a.spin, hi) && wait_word<SPIN_ARG>(wq + 1, tag, a.err, a.spin, lo))
                 msl[jl * RED_SLICES + q] = __longlong_as_double((long long)(((hi & 0xFFFFFFFFu) << 32) | (lo & 0xFFFFFFFFu)));
             else
                 ok = 0;
@@ -2003,7 +2019,7 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
         // every member's fitness
         for (int32_t j = threadIdx.x; j < a.N; j += GRID_WG) {
             uint64_t word;
-            if (!wait_word(fxr + j, tag, a.err, word)) {
+            if (!wait_word<SPIN_ARG>(fxr + j, tag, a.err, a.spin, word)) {
                 ok = 0;
                 continue;
             }
@@ -2015,8 +2031,8 @@ __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
         }
         __syncthreads();
         if (!ok) return;
-        if (!rank_exchange(comp, keys, fit, tab, y, wf, a.N, a.P, a.raw, a.maximize, tag, a.yx + (int64_t)r * a.N,
-                           a.bestx + r, w, G, a.err, bst, (w == 0 && a.log) ? a.log + (int64_t)it * a.R + r : nullptr,
+        if (!rank_exchange<SPIN_ARG>(comp, keys, fit, tab, y, wf, a.N, a.P, a.raw, a.maximize, tag, a.yx + (int64_t)r * a.N,
+                           a.bestx + r, w, G, a.err, a.spin, bst, (w == 0 && a.log) ? a.log + (int64_t)it * a.R + r : nullptr,
                            &ok))
             return;
         __syncthreads();
@@ -2604,6 +2620,11 @@ hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan
     a.bestx = a.yx + (size_t)g.R * g.N;
     a.halo = a.bestx + g.R;
     a.err = err;
+    // polls before a wait gives up: the library's limit, a caller's, or
+    // none at all (-1: every wait gives up at once)
+    a.spin = c.plan_grid_spin_limit == 0 ? GRID_SPIN_LIMIT
+             : c.plan_grid_spin_limit < 0 ? 0u
+                                          : (uint32_t)c.plan_grid_spin_limit;
     if (seq < 1 || seq >= (1u << 24)) return hipErrorInvalidValue;
     a.tag0 = seq << 8;
     a.ac = ac;
@@ -2623,13 +2644,18 @@ hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan
     const uint32_t lds = (uint32_t)grid_lds_bytes(g, e, tp, G);
     void* args[] = {&a};
     const void* k;
+    const bool spin_arg = c.plan_grid_spin_limit != 0;
+#define ES_GRID_KERNEL(PROB)                                                                       \
+    (spin_arg ? reinterpret_cast<const void*>(&k_run_grid<PROB, true>)                             \
+              : reinterpret_cast<const void*>(&k_run_grid<PROB, false>))
     switch (c.problem) {
-    case ES_PROB_SPHERE: k = reinterpret_cast<const void*>(&k_run_grid<ES_PROB_SPHERE>); break;
-    case ES_PROB_SHIFTED_SPHERE: k = reinterpret_cast<const void*>(&k_run_grid<ES_PROB_SHIFTED_SPHERE>); break;
-    case ES_PROB_ROSENBROCK: k = reinterpret_cast<const void*>(&k_run_grid<ES_PROB_ROSENBROCK>); break;
-    case ES_PROB_RASTRIGIN: k = reinterpret_cast<const void*>(&k_run_grid<ES_PROB_RASTRIGIN>); break;
+    case ES_PROB_SPHERE: k = ES_GRID_KERNEL(ES_PROB_SPHERE); break;
+    case ES_PROB_SHIFTED_SPHERE: k = ES_GRID_KERNEL(ES_PROB_SHIFTED_SPHERE); break;
+    case ES_PROB_ROSENBROCK: k = ES_GRID_KERNEL(ES_PROB_ROSENBROCK); break;
+    case ES_PROB_RASTRIGIN: k = ES_GRID_KERNEL(ES_PROB_RASTRIGIN); break;
     default: return hipErrorInvalidValue;
     }
+#undef ES_GRID_KERNEL
     // more than 64 KB of LDS per workgroup: allowed per kernel (cheap to repeat)
     herr = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GRID_MAX_LDS);
     if (herr != hipSuccess) return herr;

@@ -79,6 +79,8 @@ class _Config(ctypes.Structure):
         ("plan_run_path", ctypes.c_int32),
         ("plan_rank_path", ctypes.c_int32),
         ("plan_grid_workgroups", ctypes.c_int32),
+        ("plan_grid_spin_limit", ctypes.c_int32),
+        ("plan_reserved", ctypes.c_int32),
     ]
 
 
@@ -121,13 +123,16 @@ class ESConfig:
     snes_temperature: float = 12.0
     elite_ratio: float = 0.5  # Sep-CMA-ES (App. B table)
     # launch plan, 0 = the library's choice (esmi.h): evaluate chunk length and
-    # gradient split change the summation order; run path 1 per-call, 2 fused;
-    # rank path 1 counted in LDS (N <= 16384), 2 radix-sorted (same ranks)
+    # gradient split change the summation order; run path 1 per-call, 2 fused,
+    # 3 grid loop; rank path 1 counted in LDS (N <= 16384), 2 radix-sorted
+    # (same ranks); grid spin limit: polls before a grid-loop wait gives up
+    # (-1: at once, the failure path)
     plan_eval_blocks: int = 0
     plan_tell_split: int = 0
     plan_run_path: int = 0
     plan_rank_path: int = 0
     plan_grid_workgroups: int = 0
+    plan_grid_spin_limit: int = 0
 
     def cstruct(self) -> _Config:
         c = _Config()

@@ -47,7 +47,7 @@ def test_config_struct_has_no_padding():
     # no padding bytes: checkpoints compare the config byte for byte
     from paper_2212_04180_amd import esmi
     fields = sum(ctypes.sizeof(t) for _, t in esmi._Config._fields_)
-    assert ctypes.sizeof(esmi._Config) == fields == 160
+    assert ctypes.sizeof(esmi._Config) == fields == 168
 
 
 def test_product_does_not_reach_the_oracle():
@@ -88,7 +88,12 @@ def test_population_limits_are_validated_without_gpu_work():
                     (dict(popsize=(1 << 20), num_runs=4096), b"2^31"),
                     (dict(popsize=64, plan_run_path=4), b"plan_run_path must be"),
                     (dict(popsize=64, plan_grid_workgroups=17), b"plan_grid_workgroups"),
-                    (dict(popsize=64, plan_grid_workgroups=-1), b"plan_grid_workgroups")):
+                    (dict(popsize=64, plan_grid_workgroups=-1), b"plan_grid_workgroups"),
+                    (dict(popsize=64, plan_grid_spin_limit=-2), b"plan_grid_spin_limit")):
         cfg = esmi.ESConfig(num_dims=8, **kw).cstruct()
         assert L.es_init(ctypes.byref(cfg), None, ctypes.byref(h)) == esmi.ES_ERR_ARG, kw
         assert msg in L.es_last_error(None), (kw, L.es_last_error(None))
+    cfg = esmi.ESConfig(num_dims=8, popsize=64).cstruct()
+    cfg.plan_reserved = 1
+    assert L.es_init(ctypes.byref(cfg), None, ctypes.byref(h)) == esmi.ES_ERR_ARG
+    assert b"plan_reserved" in L.es_last_error(None)

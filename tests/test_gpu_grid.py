@@ -10,7 +10,8 @@ for it, with its four-lanes-per-block gradient plan), runs longer than one
 launch (256 generations), split gradient plans, evaluate chunkings (fewer
 and more chunks than the reduce kernel's 16 slices), one workgroup, more
 workgroups than pairs, several runs, and seeded random geometries of every
-benchmark problem, both shapings, both signs and the schedules."""
+benchmark problem, both shapings, both signs and the schedules; and the
+failure path (waits that give up, forced from the host), reported by es_sync."""
 import dataclasses
 
 import numpy as np
@@ -139,6 +140,30 @@ def test_rewound_generation_counter():
         es.close()
     for name, a, b in zip(("log", "m", "m1", "v", "grad"), out[3], out[1]):
         assert a.tobytes() == b.tobytes(), name
+
+
+def test_wait_that_gives_up_is_reported():
+    """The failure path, forced from the host: with plan_grid_spin_limit -1
+    every wait of the grid loop gives up at once, so each launch ends early
+    (its workgroups leave the kernel at their first wait; a second launch of
+    the same es_run sees the flag and leaves too), es_sync reports it, and
+    es_set_state clears it.  A spin limit of one poll per wait gives the
+    same bits as the default wherever every wait succeeds (the limit is no
+    part of the arithmetic): not asserted, since a wait may need a second
+    poll."""
+    P = _P()
+    cfg = _rosenbrock(num_dims=300, popsize=64, plan_run_path=3, plan_grid_spin_limit=-1)
+    es = P.ES(cfg)
+    assert es.run_path == 3
+    st = es.get_state()
+    for T in (5, 300):  # one launch, then two
+        es.run(T)
+        with pytest.raises(P.EsError, match="gave up"):
+            es.sync()
+        es.set_state(st["m"], st["m1"], st["v"], 0)
+        es.sync()
+    es.close()
+    print("grid loop: forced give-up reported by es_sync and cleared by es_set_state", flush=True)
 
 
 def test_more_workgroups_than_pairs():

@@ -1,0 +1,68 @@
+"""Stream capture of the per-call entry points (marked gpu).  es_ask, es_eval
+and es_tell captured into a graph record one generation with its host-side
+arguments (the generation t, the sigma / lr buffer pair, Adam's bias
+corrections), so each replay repeats that generation on the handle's current
+state.  Checked against a second handle run eagerly on the same stream and set
+back to the same t before each of its generations, replay by replay, with
+eager work and synchronisations between the replays.  The BBOB problems with
+ranks counted in LDS: that per-call path enqueues kernels only (no memset or
+host-staged copy nodes)."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+
+def _P():
+    import paper_2212_04180_amd as P
+    return P
+
+
+def _snap(es, fit):
+    st = es.get_state()
+    bx, bf = es.best()
+    return [x.cpu().numpy() for x in (fit, st["m"], st["m1"], st["v"], es.grad(), bx, bf)]
+
+
+@pytest.mark.parametrize("problem,shaping", [("rosenbrock", 0), ("rastrigin", 0), ("shifted_sphere", 1)])
+def test_captured_generation_replays_like_eager(problem, shaping):
+    P = _P()
+    prob = {"rosenbrock": P.PROB_ROSENBROCK, "rastrigin": P.PROB_RASTRIGIN,
+            "shifted_sphere": P.PROB_SHIFTED_SPHERE}[problem]
+    cfg = P.ESConfig(num_dims=300, popsize=64, num_runs=2, sigma=0.1, lr=0.05, seed=21, init_lo=-2.0,
+                     init_hi=2.0, problem=prob, shaping=shaping, flags=P.FLAG_KEEP_GRAD)
+    s = torch.cuda.Stream()
+    A, B = P.ES(cfg, stream=s), P.ES(dataclasses.replace(cfg), stream=s)
+    fa = torch.empty(2, 64, device="cuda")
+    fb = torch.empty_like(fa)
+    with torch.cuda.stream(s):
+        for _ in range(2):
+            A.step(fa)
+            B.step(fb)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        A.ask()
+        A.eval(fa)
+        A.tell(fa)
+    assert A.t == 3  # the host counter moved on; the graph holds generation 2
+    names = ("fitness", "m", "m1", "v", "grad", "best_x", "best_f")
+    for k in range(4):
+        # replayed on the handles' stream, so that the snapshots below follow it
+        # (torch replays on the current stream; s does not wait for the default one)
+        with torch.cuda.stream(s):
+            g.replay()
+            st = B.get_state()
+            B.set_state(st["m"], st["m1"], st["v"], 2)
+            B.step(fb)
+            a, b = _snap(A, fa), _snap(B, fb)
+        torch.cuda.synchronize()
+        for name, x, y in zip(names, a, b):
+            assert x.tobytes() == y.tobytes(), (problem, k, name)
+        assert np.all(np.isfinite(a[1]))
+    A.close()
+    B.close()
+    print(f"{problem}: four replays of a captured generation equal the eager generation", flush=True)

@@ -35,9 +35,12 @@
  *   - The generation counter, sigma / lr buffer selection and sequence
  *     checks live on the host and the kernels take them as launch
  *     arguments, so a stream capture of es_ask / es_eval / es_tell records
- *     that one generation; a replay repeats it (for ES_PROB_MLP with
- *     OpenAI-ES on the inputs the replayed es_tell made for the generation
- *     after it).  For many generations per launch use es_run.
+ *     that one generation; a replay repeats it on the current state (for
+ *     ES_PROB_MLP with OpenAI-ES on the inputs the replayed es_tell made for
+ *     the generation after it), with the per-run sigma and lr of the
+ *     captured generation: schedules and Sep-CMA-ES's step size do not
+ *     advance from replay to replay.  For many generations per launch use
+ *     es_run.
  *   - Minimisation is the default (Listing 1); maximize = 1 negates keys.
  */
 #ifndef ESMI_H

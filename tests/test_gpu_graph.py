@@ -5,8 +5,8 @@ corrections), so each replay repeats that generation on the handle's current
 state.  Checked against a second handle run eagerly on the same stream and set
 back to the same t before each of its generations, replay by replay, with
 eager work and synchronisations between the replays.  The BBOB problems with
-ranks counted in LDS: that per-call path enqueues kernels only (no memset or
-host-staged copy nodes)."""
+ranks counted in LDS, OpenAI-ES, PGPE with ClipUp and SNES: that per-call path
+enqueues kernels only (no memset or host-staged copy nodes)."""
 import dataclasses
 
 import numpy as np
@@ -21,19 +21,43 @@ def _P():
     return P
 
 
-def _snap(es, fit):
+def _snap(es, fit, strategy):
+    P = _P()
     st = es.get_state()
     bx, bf = es.best()
-    return [x.cpu().numpy() for x in (fit, st["m"], st["m1"], st["v"], es.grad(), bx, bf)]
+    out = [fit, st["m"], st["m1"], st["v"], bx, bf]
+    if strategy == P.STRAT_OPENAI_ES:
+        out.append(es.grad())
+    else:
+        sg, ve = es.strategy_state(sigma=True, velocity=es.cfg.optimizer == P.OPT_CLIPUP)
+        out += [sg] + ([ve] if ve is not None else [])
+    return [x.cpu().numpy() for x in out]
 
 
-@pytest.mark.parametrize("problem,shaping", [("rosenbrock", 0), ("rastrigin", 0), ("shifted_sphere", 1)])
-def test_captured_generation_replays_like_eager(problem, shaping):
+CASES = {
+    "rosenbrock": dict(problem="rosenbrock"),
+    "rastrigin": dict(problem="rastrigin"),
+    "shifted_sphere_raw": dict(problem="shifted_sphere", shaping=1),
+    "pgpe_clipup": dict(problem="shifted_sphere", strategy="pgpe", optimizer="clipup"),
+    "snes": dict(problem="rastrigin", strategy="snes"),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_captured_generation_replays_like_eager(case):
+    """(Sep-CMA-ES is left out: its step size lives in the per-run sigma that
+    the recorded generation reads from one buffer of the pair, so replays
+    repeat the captured step size rather than follow it.)"""
     P = _P()
+    kw = CASES[case]
+    problem = kw["problem"]
     prob = {"rosenbrock": P.PROB_ROSENBROCK, "rastrigin": P.PROB_RASTRIGIN,
             "shifted_sphere": P.PROB_SHIFTED_SPHERE}[problem]
+    strategy = {"openai": P.STRAT_OPENAI_ES, "pgpe": P.STRAT_PGPE, "snes": P.STRAT_SNES}[kw.get("strategy", "openai")]
+    optimizer = P.OPT_CLIPUP if kw.get("optimizer") == "clipup" else P.OPT_ADAM
     cfg = P.ESConfig(num_dims=300, popsize=64, num_runs=2, sigma=0.1, lr=0.05, seed=21, init_lo=-2.0,
-                     init_hi=2.0, problem=prob, shaping=shaping, flags=P.FLAG_KEEP_GRAD)
+                     init_hi=2.0, problem=prob, shaping=kw.get("shaping", 0), strategy=strategy,
+                     optimizer=optimizer, flags=P.FLAG_KEEP_GRAD)
     s = torch.cuda.Stream()
     A, B = P.ES(cfg, stream=s), P.ES(dataclasses.replace(cfg), stream=s)
     fa = torch.empty(2, 64, device="cuda")
@@ -49,7 +73,7 @@ def test_captured_generation_replays_like_eager(problem, shaping):
         A.eval(fa)
         A.tell(fa)
     assert A.t == 3  # the host counter moved on; the graph holds generation 2
-    names = ("fitness", "m", "m1", "v", "grad", "best_x", "best_f")
+    names = ("fitness", "m", "m1", "v", "best_x", "best_f", "grad or sigma", "velocity")
     for k in range(4):
         # replayed on the handles' stream, so that the snapshots below follow it
         # (torch replays on the current stream; s does not wait for the default one)
@@ -58,11 +82,12 @@ def test_captured_generation_replays_like_eager(problem, shaping):
             st = B.get_state()
             B.set_state(st["m"], st["m1"], st["v"], 2)
             B.step(fb)
-            a, b = _snap(A, fa), _snap(B, fb)
+            a, b = _snap(A, fa, strategy), _snap(B, fb, strategy)
         torch.cuda.synchronize()
-        for name, x, y in zip(names, a, b):
-            assert x.tobytes() == y.tobytes(), (problem, k, name)
+        assert len(a) == len(b)
+        for i, (x, y) in enumerate(zip(a, b)):
+            assert x.tobytes() == y.tobytes(), (case, k, names[i] if i < len(names) else i)
         assert np.all(np.isfinite(a[1]))
     A.close()
     B.close()
-    print(f"{problem}: four replays of a captured generation equal the eager generation", flush=True)
+    print(f"{case}: four replays of a captured generation equal the eager generation", flush=True)

@@ -204,3 +204,81 @@ def test_random_grid_loop_equals_per_call(i):
     cfg = _draw(i)
     print("case", i, cfg, flush=True)
     _same(cfg, 9)
+
+
+def _largest(make, ok, lo, hi):
+    """A num_dims in [lo, hi] for which ok(handle) holds and ok(num_dims + 1)
+    does not (the largest one where the property is monotonic), by
+    bisection; lo must satisfy it."""
+    P = _P()
+    es = P.ES(make(lo))
+    assert ok(es), lo
+    es.close()
+    while lo < hi:
+        mid = (lo + hi + 1) // 2
+        es = P.ES(make(mid))
+        good = ok(es)
+        es.close()
+        if good:
+            lo = mid
+        else:
+            hi = mid - 1
+    return lo
+
+
+@pytest.mark.parametrize("problem,N", [("rosenbrock", 256), ("rastrigin", 1024), ("sphere", 64)])
+def test_grid_loop_at_its_lds_limit(problem, N):
+    """The largest dimension the grid loop takes for a population, counted up
+    from the first one it takes (few dims give few workgroups, each holding
+    more members' slice sums, so small D can be refused too): its LDS, sized
+    on the host, near the 144 KB it may use; the same bits as the per-call
+    kernels."""
+    P = _P()
+    prob = {"rosenbrock": P.PROB_ROSENBROCK, "rastrigin": P.PROB_RASTRIGIN, "sphere": P.PROB_SPHERE}[problem]
+
+    def make(D, path=3):
+        return P.ESConfig(num_dims=D, popsize=N, num_runs=1, sigma=0.1, lr=0.02, seed=17, init_lo=-2.0,
+                          init_hi=2.0, problem=prob, plan_run_path=path, flags=P.FLAG_KEEP_GRAD)
+
+    def grid(es):
+        return es.run_path == 3
+
+    start = None
+    for D0 in (16, 64, 256, 1000, 4000):
+        es = P.ES(make(D0))
+        ok = grid(es)
+        es.close()
+        if ok:
+            start = D0
+            break
+    assert start is not None
+    D = _largest(make, grid, start, 1 << 16)
+    print(f"{problem} N={N}: the grid loop up to D={D}", flush=True)
+    _same(make(D, 0), 4)
+
+
+def test_fused_loop_at_its_lds_limit():
+    """1024 runs of 64 members: the largest dimension the fused loop takes by
+    default (its workgroup's LDS at the limit), and the largest for which it
+    still keeps the normals; both the same bits as the per-call kernels."""
+    P = _P()
+
+    def make(D, path=0):
+        return P.ESConfig(num_dims=D, popsize=64, num_runs=1024, sigma=0.2, lr=0.02, seed=23, init_lo=-3.0,
+                          init_hi=3.0, problem=P.PROB_RASTRIGIN, plan_run_path=path, flags=P.FLAG_KEEP_GRAD)
+
+    d_fused = _largest(make, lambda es: es.run_path == 2, 8, 1 << 14)
+    d_keep = _largest(make, lambda es: es.run_path == 2 and es.run_keeps_normals, 8, d_fused)
+    print(f"fused loop up to D={d_fused}, normals kept up to D={d_keep}", flush=True)
+    for D in sorted({d_keep, d_fused}):
+        out = {}
+        for path in (2, 1):
+            es = P.ES(make(D, path))
+            log = es.run(3)
+            st = es.get_state()
+            bx, bf = es.best()
+            torch.cuda.synchronize()
+            out[path] = [x.cpu().numpy() for x in (log, st["m"], st["m1"], st["v"], bx, bf, es.grad())]
+            es.close()
+        for name, a, b in zip(("log", "m", "m1", "v", "best_x", "best_f", "grad"), out[2], out[1]):
+            assert a.tobytes() == b.tobytes(), (D, name)

@@ -282,3 +282,31 @@ def test_fused_loop_at_its_lds_limit():
             es.close()
         for name, a, b in zip(("log", "m", "m1", "v", "best_x", "best_f", "grad"), out[2], out[1]):
             assert a.tobytes() == b.tobytes(), (D, name)
+
+
+@pytest.mark.parametrize("problem", ["rosenbrock", "sphere"])
+def test_overflowing_fitness_loops_equal_per_call(problem):
+    """Means near 1e20: the fitness overflows to inf (and Rosenbrock's terms
+    to NaN), so the order keys hold ties and NaN, and both loops must still
+    give the per-call bits (log, state, best-so-far)."""
+    P = _P()
+    prob = {"rosenbrock": P.PROB_ROSENBROCK, "sphere": P.PROB_SPHERE}[problem]
+    grid = P.ESConfig(num_dims=300, popsize=64, num_runs=2, sigma=0.1, lr=0.05, seed=31, init_lo=-1e20,
+                      init_hi=1e20, problem=prob, flags=P.FLAG_KEEP_GRAD)
+    og = _same(grid, 6)
+    assert not np.all(np.isfinite(og[0]))  # the log carries the overflow
+    fused = dataclasses.replace(grid, num_dims=40, popsize=32, num_runs=200)
+    es = P.ES(fused)
+    assert es.run_path == 2
+    es.close()
+    out = {}
+    for path in (2, 1):
+        es = P.ES(dataclasses.replace(fused, plan_run_path=path))
+        log = es.run(6)
+        st = es.get_state()
+        bx, bf = es.best()
+        torch.cuda.synchronize()
+        out[path] = [x.cpu().numpy() for x in (log, st["m"], st["m1"], st["v"], bx, bf, es.grad())]
+        es.close()
+    for name, a, b in zip(("log", "m", "m1", "v", "best_x", "best_f", "grad"), out[2], out[1]):
+        assert a.tobytes() == b.tobytes(), name

@@ -41,10 +41,11 @@ MLP_FLOPS_PER_MEMBER = 2 * 256 * (64 * 256 + 256 * 256 + 256 * 16)
 #   members (both signs): 8 fma for x plus the problem's terms, and the fold
 #     of each member's fp32 block sum into fp64 (2 x (cvt 2 + add 2) = 8):
 #     sphere 8 squares -> 24; shifted sphere 8 sub + 8 squares -> 32;
-#     Rosenbrock 6 ops x 4 terms x 2 -> 64; Rastrigin 9 ops x 8 -> 88.
+#     Rosenbrock 6 ops x 4 terms x 2 -> 64; Rastrigin 8 ops x 8 -> 80 (fract of
+#     |x| (1), cos (4), -a cos (1), x^2 + that (1), the add (1)).
 PHILOX_BM = 60 + 54
 EVAL_SLOTS_PER_PAIR_BLOCK = {"sphere": PHILOX_BM + 24, "shifted_sphere": PHILOX_BM + 32,
-                             "rosenbrock": PHILOX_BM + 64, "rastrigin": PHILOX_BM + 88}
+                             "rosenbrock": PHILOX_BM + 64, "rastrigin": PHILOX_BM + 80}
 # tell: Philox + Box-Muller + 4 fma (w * eps) + the fp64 fold every 16 pairs
 TELL_SLOTS_PER_PAIR_BLOCK = PHILOX_BM + 4 + 1
 # es_run's code paths (es_run_path); where a loop's gradient reads the

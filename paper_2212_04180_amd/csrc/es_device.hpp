@@ -121,10 +121,14 @@ __device__ __forceinline__ void normals4(uint64_t key, uint32_t block, uint32_t 
 }
 
 // cos(2 pi x) for any finite x: v_cos_f32 takes revolutions and is accurate
-// for small arguments, so the integer part is removed first (exact).
+// for small arguments, so the integer part is removed first.  cos is even, so
+// the turns are taken of |x| (a free source modifier) and one v_fract_f32
+// (|x| - floor |x|, exact for a non-negative argument) does the reduction, one
+// instruction fewer than x - rint x; f(m + s) and f(m - s) stay equal bit for
+// bit, as the antithetic pairs of a symmetric problem must.
 __device__ __forceinline__ float cos_2pi(float x)
 {
-    return __builtin_amdgcn_cosf(x - __builtin_rintf(x));
+    return __builtin_amdgcn_cosf(__builtin_amdgcn_fractf(__builtin_fabsf(x)));
 }
 
 // Order-preserving map of a fitness to an unsigned key: minimisation order,

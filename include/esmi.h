@@ -211,14 +211,23 @@ typedef struct es_config {
      *                     of a launch whose waits all succeed.  A wait that
      *                     gives up ends the launch early with the state not
      *                     valid: es_sync reports it
-     *   plan_reserved     must be 0 (keeps the struct free of padding)     */
+     *   plan_grid_pack    placement of the grid loop's workgroups: 0 (the
+     *                     library's choice) packs each run's workgroups onto
+     *                     one XCD, whose L2 they then share for their
+     *                     exchanges: the launch holds (XCDs) times the
+     *                     workgroups, the hardware deals them to the XCDs in
+     *                     turn, those of x index = r (mod XCDs) work for run
+     *                     r and the others return at once; taken only where
+     *                     the device holds the larger launch resident, else
+     *                     as -1.  -1: one workgroup per participant.  No
+     *                     effect on the results, only on the time          */
     int32_t plan_eval_blocks;
     int32_t plan_tell_split;
     int32_t plan_run_path;
     int32_t plan_rank_path;
     int32_t plan_grid_workgroups;
     int32_t plan_grid_spin_limit;
-    int32_t plan_reserved;
+    int32_t plan_grid_pack;
 } es_config;
 
 typedef struct es_handle es_handle;

@@ -89,6 +89,7 @@ struct es_handle {
     int64_t teacher_t = -1;       // generation whose inputs and teacher outputs are in mlp_scratch
     int run_path = 0;  // 0 auto, 1 per-call kernels, 2 fused loop, 3 grid loop
     int32_t grid_g = 0;             // workgroups per run of the grid loop (0: the grid loop does not apply)
+    int32_t grid_xs = 1;            // x stride between a run's grid-loop workgroups (the XCD count when packed)
     uint64_t* grid_words = nullptr;  // the grid loop's tagged words
     uint32_t* grid_err = nullptr;    // the grid loop's error flag
     uint32_t grid_seq = 0;           // sequence number of the last grid-loop launch
@@ -167,7 +168,7 @@ const char* validate(const es_config& c)
         return "plan_grid_workgroups must be in [0, 16]";
     if (c.plan_rank_path < 0 || c.plan_rank_path > 2) return "plan_rank_path must be 0, 1 or 2";
     if (c.plan_grid_spin_limit < -1) return "plan_grid_spin_limit must be >= -1";
-    if (c.plan_reserved != 0) return "plan_reserved must be 0";
+    if (c.plan_grid_pack != 0 && c.plan_grid_pack != -1) return "plan_grid_pack must be 0 or -1";
     if (c.plan_rank_path == 1 && c.popsize > RANK_MAX_N)
         return "plan_rank_path 1 (ranks counted in LDS) takes popsize <= 16384";
     // (the library's own choice of the sort never needs more: it picks the
@@ -465,8 +466,16 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
         const int32_t G = grid_workgroups(g, h->plan, cfg->plan_grid_workgroups);
         int64_t cap = 0;
         if (grid_supported(g, h->plan, h->tell, *cfg, G) && grid_max_resident(&cap) == hipSuccess &&
-            (int64_t)G * g.R <= cap)
+            (int64_t)G * g.R <= cap) {
             h->grid_g = G;
+            // one XCD per run where the device holds the XCD count times the
+            // workgroups at once (workgroups are dealt to the XCDs in turn)
+            int dev = 0, xcc = 1;
+            if (cfg->plan_grid_pack == 0 && hipGetDevice(&dev) == hipSuccess &&
+                hipDeviceGetAttribute(&xcc, hipDeviceAttributeNumberOfXccs, dev) == hipSuccess && xcc > 1 &&
+                (int64_t)xcc * G * g.R <= cap)
+                h->grid_xs = xcc;
+        }
     }
     hipError_t e = hipGetDevice(&h->device);
     const size_t rows = (size_t)g.Dp * g.R;
@@ -695,7 +704,7 @@ es_status es_run(es_handle* h, int32_t T, float* log)
                 // a sequence number the previous launch did not use, so that
                 // none of its words carries a tag this launch waits for
                 h->grid_seq = h->grid_seq % 0xFFFFFFu + 1;
-                ES_HIP(h, launch_run_grid(h->g, h->cfg, h->plan, h->tell, h->grid_g, (uint32_t)h->t, Tc,
+                ES_HIP(h, launch_run_grid(h->g, h->cfg, h->plan, h->tell, h->grid_g, h->grid_xs, (uint32_t)h->t, Tc,
                                           adam_consts(h->cfg, h->t), bcorr, h->m, h->m1, h->v, h->grad, h->best_x,
                                           h->best_okey, h->best_f, h->pdata, h->table, lg, h->grid_words, h->grid_seq,
                                           h->grid_err, h->hp[h->hp_cur], h->stream),

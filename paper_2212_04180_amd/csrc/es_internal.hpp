@@ -177,6 +177,7 @@ size_t grid_lds_bytes(const Geometry& g, const EvalPlan& e, const TellPlan& tp, 
 bool grid_supported(const Geometry& g, const EvalPlan& e, const TellPlan& tp, const es_config& c, int32_t G);
 hipError_t grid_max_resident(int64_t* out);  // workgroups of the grid loop the device holds at once
 hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan& e, const TellPlan& tp, int32_t G,
+                           int32_t xs,
                            uint32_t t0, int32_t T, const AdamConsts& ac, const float (*bcorr)[2], float* m, float* m1,
                            float* v, float* grad, float* best_x, uint32_t* best_okey, float* best_f,
                            const float* pdata, const float* table, float* log, uint64_t* words, uint32_t seq,

@@ -1738,6 +1738,7 @@ struct GridArgs {
     uint32_t* err;           // set nonzero when a wait gives up
     uint32_t spin;           // SPIN_ARG: polls before a wait gives up; 0: at once, without polling
     uint32_t tag0;           // this launch's sequence number << 8; generation it's tag is tag0 | it
+    int32_t xs;              // x stride between a run's workgroups: run r's are x = r mod xs, r mod xs + xs, ...
     uint64_t seed;
     uint32_t t0;
     int32_t T;
@@ -1852,7 +1853,14 @@ template <int PROB, bool SPIN_ARG = false>
 __global__ __launch_bounds__(GRID_WG) void k_run_grid(GridArgs a)
 {
     extern __shared__ __align__(16) double smem[];
-    const int32_t r = blockIdx.y, w = blockIdx.x, G = gridDim.x;
+    // With xs > 1 the launch holds xs workgroups per working one: those with
+    // x = r mod xs, r mod xs + xs, ... work for run r, the rest leave before
+    // any access.
+    // A row of the grid is a multiple of xs wide, so the workgroups of run r
+    // all have linear index = r (mod xs): one XCD when xs is the XCD count.
+    const int32_t r = blockIdx.y, xs = a.xs;
+    if ((int32_t)blockIdx.x % xs != r % xs) return;
+    const int32_t w = (int32_t)blockIdx.x / xs, G = (int32_t)gridDim.x / xs;
     const int32_t S = a.ps * a.nsplit * a.sub;  // the gradient's sub-slices of the pairs
     const int32_t nch = (int32_t)a.nchunks, bc = (int32_t)a.bc, nb = (int32_t)a.nb;
     const int32_t nq = nch < RED_SLICES ? nch : RED_SLICES;
@@ -2604,12 +2612,13 @@ hipError_t grid_max_resident(int64_t* out)
 }
 
 hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan& e, const TellPlan& tp, int32_t G,
+                           int32_t xs,
                            uint32_t t0, int32_t T, const AdamConsts& ac, const float (*bcorr)[2], float* m, float* m1,
                            float* v, float* grad, float* best_x, uint32_t* best_okey, float* best_f,
                            const float* pdata, const float* table, float* log, uint64_t* words, uint32_t seq,
                            uint32_t* err, float* hp, hipStream_t s)
 {
-    if (T < 1 || T > FUSED_MAX_T || G < 1 || G > GRID_MAX_G) return hipErrorInvalidValue;
+    if (T < 1 || T > FUSED_MAX_T || G < 1 || G > GRID_MAX_G || xs < 1 || xs > 64) return hipErrorInvalidValue;
     if (!grid_supported(g, e, tp, c, G)) return hipErrorInvalidValue;
     GridArgs a;
     a.m = m; a.m1 = m1; a.v = v; a.grad = grad; a.best_x = best_x; a.best_okey = best_okey; a.best_f = best_f;
@@ -2627,6 +2636,7 @@ hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan
                                           : (uint32_t)c.plan_grid_spin_limit;
     if (seq < 1 || seq >= (1u << 24)) return hipErrorInvalidValue;
     a.tag0 = seq << 8;
+    a.xs = xs;
     a.ac = ac;
     for (int32_t i = 0; i < T; ++i) {
         a.bcorr[i][0] = bcorr[i][0];
@@ -2659,7 +2669,7 @@ hipError_t launch_run_grid(const Geometry& g, const es_config& c, const EvalPlan
     // more than 64 KB of LDS per workgroup: allowed per kernel (cheap to repeat)
     herr = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)GRID_MAX_LDS);
     if (herr != hipSuccess) return herr;
-    return hipLaunchCooperativeKernel(k, dim3((unsigned)G, (unsigned)g.R), dim3(GRID_WG), args, lds, s);
+    return hipLaunchCooperativeKernel(k, dim3((unsigned)(G * xs), (unsigned)g.R), dim3(GRID_WG), args, lds, s);
 }
 
 hipError_t launch_debug_noise(const Geometry& g, const es_config& c, int32_t run, uint32_t t,

@@ -80,7 +80,7 @@ class _Config(ctypes.Structure):
         ("plan_rank_path", ctypes.c_int32),
         ("plan_grid_workgroups", ctypes.c_int32),
         ("plan_grid_spin_limit", ctypes.c_int32),
-        ("plan_reserved", ctypes.c_int32),
+        ("plan_grid_pack", ctypes.c_int32),
     ]
 
 
@@ -133,6 +133,7 @@ class ESConfig:
     plan_rank_path: int = 0
     plan_grid_workgroups: int = 0
     plan_grid_spin_limit: int = 0
+    plan_grid_pack: int = 0
 
     def cstruct(self) -> _Config:
         c = _Config()

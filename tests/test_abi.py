@@ -89,11 +89,9 @@ def test_population_limits_are_validated_without_gpu_work():
                     (dict(popsize=64, plan_run_path=4), b"plan_run_path must be"),
                     (dict(popsize=64, plan_grid_workgroups=17), b"plan_grid_workgroups"),
                     (dict(popsize=64, plan_grid_workgroups=-1), b"plan_grid_workgroups"),
-                    (dict(popsize=64, plan_grid_spin_limit=-2), b"plan_grid_spin_limit")):
+                    (dict(popsize=64, plan_grid_spin_limit=-2), b"plan_grid_spin_limit"),
+                    (dict(popsize=64, plan_grid_pack=1), b"plan_grid_pack"),
+                    (dict(popsize=64, plan_grid_pack=-2), b"plan_grid_pack")):
         cfg = esmi.ESConfig(num_dims=8, **kw).cstruct()
         assert L.es_init(ctypes.byref(cfg), None, ctypes.byref(h)) == esmi.ES_ERR_ARG, kw
         assert msg in L.es_last_error(None), (kw, L.es_last_error(None))
-    cfg = esmi.ESConfig(num_dims=8, popsize=64).cstruct()
-    cfg.plan_reserved = 1
-    assert L.es_init(ctypes.byref(cfg), None, ctypes.byref(h)) == esmi.ES_ERR_ARG
-    assert b"plan_reserved" in L.es_last_error(None)

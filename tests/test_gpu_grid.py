@@ -97,6 +97,18 @@ def test_plan_variants(kw):
     _same(_rosenbrock(**kw), 12)
 
 
+@pytest.mark.parametrize("kw", [dict(), dict(num_runs=3, num_dims=300, popsize=64)])
+def test_packed_and_unpacked_launches(kw):
+    """The default launch places each run's workgroups on one XCD where the
+    device holds the larger launch (the workload; three runs on three XCDs,
+    so run r's workgroups are those with x = r mod 8); plan_grid_pack -1
+    launches one workgroup per participant.  Both give the per-call bits."""
+    a = _same(_rosenbrock(**kw), 20)
+    b = _same(_rosenbrock(plan_grid_pack=-1, **kw), 20)
+    for x, y in zip(a, b):
+        assert np.asarray(x).tobytes() == np.asarray(y).tobytes()
+
+
 def test_fused_loop_without_kept_normals():
     """1024 runs of 600 dims and 16 members: the fused loop, whose four runs per
     CU (about 49 KB each with the normals kept) would not fit 160 KB of LDS, so

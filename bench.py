@@ -235,6 +235,9 @@ def time_workload(P, torch, name, K, W, path, dev, stream, copy_mib=0):
     end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
+    # a grid-loop launch whose waits gave up ends early: raise rather than
+    # report its short time
+    es.sync()
     ms = start.elapsed_time(end) / K
     if path == "run":
         eval_ms = rest_ms = None  # es_run has no phase boundaries to time

@@ -471,10 +471,15 @@ es_status es_init(const es_config* cfg, void* hip_stream, es_handle** out)
             // one XCD per run where the device holds the XCD count times the
             // workgroups at once (workgroups are dealt to the XCDs in turn)
             int dev = 0, xcc = 1;
-            if (cfg->plan_grid_pack == 0 && hipGetDevice(&dev) == hipSuccess &&
-                hipDeviceGetAttribute(&xcc, hipDeviceAttributeNumberOfXccs, dev) == hipSuccess && xcc > 1 &&
-                (int64_t)xcc * G * g.R <= cap)
-                h->grid_xs = xcc;
+            if (cfg->plan_grid_pack == 0 && hipGetDevice(&dev) == hipSuccess) {
+                if (hipDeviceGetAttribute(&xcc, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess) {
+                    // a runtime without the attribute: no packing, and no
+                    // error left for the next launch's hipGetLastError
+                    xcc = 1;
+                    (void)hipGetLastError();
+                }
+                if (xcc > 1 && (int64_t)xcc * G * g.R <= cap) h->grid_xs = xcc;
+            }
         }
     }
     hipError_t e = hipGetDevice(&h->device);
